@@ -1,0 +1,144 @@
+/*
+ * ccq.h -- C ABI of the MI355X (gfx950) Curvature-Conditioned Query library.
+ *
+ * Curvature-Conditioned Query (CCQ, arXiv 2606.01294) cleans every query of
+ * a linear-attention layer before it reads the fast-weight state:
+ *
+ *     Sigma_t   = Cbar_t - mu_t mu_t^T,  Cbar_t = (1/t) sum_{j<=t} k_j k_j^T,
+ *                                        mu_t   = (1/t) sum_{j<=t} k_j
+ *                                        (Sec. 3.2, second-order expansion)
+ *     q_clean_t = q_t - lambda_t Sigma_t q_t                     (Eq. clean)
+ *     o_t       = scale * S_t q_clean_t                          (Eq. read)
+ *
+ * where S_t is the backbone state, written before it is read.  The library
+ * computes this with the chunkwise form of Alg. 1 (App. B: the second-moment
+ * and mean terms split into a carried inter-chunk state and an intra-chunk
+ * block) for two backbones:
+ *
+ *   GLA             S_t = S_{t-1} diag(exp g_t) + v_t k_t^T,   g_t in R^{dk}
+ *   Gated DeltaNet  S_t = alpha_t S_{t-1} (I - beta_t k_t k_t^T) + beta_t v_t k_t^T
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  * Every tensor argument is a DEVICE pointer owned by the caller, dense and
+ *    row-major.  Token tensors are [B, T, H, d]; states are [B, H, ...].
+ *    Pointers must be 16-byte aligned.
+ *  * The library allocates and frees nothing.  Scratch comes from the caller's
+ *    `workspace` of at least ccq_workspace_size() bytes (16-byte aligned).
+ *  * Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *    stream).  Arguments are validated before anything is launched; on an
+ *    error nothing is launched and nothing is written.  A failed launch
+ *    returns CCQ_ERR_HIP.  Nothing aborts, nothing throws, nothing is kept
+ *    between calls: concurrent calls on different workspaces are safe.
+ *  * q and k are used as given (the caller applies any l2-normalisation, as
+ *    Alg. 1 does before the cleaning lines).  NaN/Inf inputs propagate.
+ *  * Statistics (Cbar, mu) and the backbone state are fp32 whatever io_dtype
+ *    is; products run on the MFMA units with fp32 accumulation.
+ */
+#ifndef CCQ_H_
+#define CCQ_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CCQ_OK = 0,
+  CCQ_ERR_INVALID_ARG = 1, /* NULL where a tensor is required, negative sizes, misalignment */
+  CCQ_ERR_UNSUPPORTED = 2, /* a head size, chunk or dtype this build has no kernel for */
+  CCQ_ERR_WORKSPACE = 3,   /* workspace NULL or smaller than ccq_workspace_size() */
+  CCQ_ERR_HIP = 4          /* the HIP runtime reported an error at launch */
+} ccq_status;
+
+typedef enum { CCQ_F32 = 0, CCQ_BF16 = 1 } ccq_dtype;
+typedef enum { CCQ_GLA = 0, CCQ_GDN = 1 } ccq_backbone;
+
+typedef struct {
+  int32_t B, T, H;      /* batch, tokens, heads (T may be any value >= 0) */
+  int32_t dk, dv;       /* key / value head size: dk in {64,128,256}, dv in {64,128,256,512} */
+  int32_t chunk;        /* chunk length C of Alg. 1; must be 64 */
+  ccq_dtype io_dtype;   /* dtype of q, k, v, o (and of dq, dk, dv, dO in the backward) */
+  ccq_dtype gate_dtype; /* dtype of the GLA gate g (and of dg); ignored for GDN */
+  float scale;          /* o = scale * S q_clean; the paper's read uses 1.0 */
+  int32_t centered;     /* 1: Sigma = Cbar - mu mu^T (the paper); 0: Sigma = Cbar (App. E ablation) */
+  int64_t t0;           /* tokens already absorbed into C0/mu0; positions are t0+1 .. t0+T */
+} ccq_shape;
+
+/* Bytes of device workspace the call needs (0 when none).  with_bwd selects
+ * the training entry point ccq_fwd_bwd.  Returns 0 for an invalid shape. */
+size_t ccq_workspace_size(const ccq_shape* s, ccq_backbone bb, int with_bwd);
+
+/*
+ * CCQ-GLA chunkwise forward (Alg. 1 with the GLA chunk form as BackboneUpdate).
+ *   q, k     [B,T,H,dk] io_dtype      queries / keys
+ *   v        [B,T,H,dv] io_dtype      values
+ *   g        [B,T,H,dk] gate_dtype    per-key-channel log forget gate (<= 0)
+ *   lam      [B,T,H]    fp32          contraction gate lambda_t (Eq. clean)
+ *   S0       [B,H,dv,dk] fp32 or NULL initial backbone state (NULL = 0)
+ *   C0       [B,H,dk,dk] fp32 or NULL initial Cbar (NULL = 0), weight t0
+ *   mu0      [B,H,dk]    fp32 or NULL initial mu (NULL = 0), weight t0
+ *   o        [B,T,H,dv] io_dtype      output (written)
+ *   ST, CT, muT  final (S_T, Cbar_T, mu_T), the inference cache of App. C,
+ *                same layouts as S0, C0, mu0; each may be NULL (not wanted)
+ *   q_clean_dbg [B,T,H,dk] fp32 or NULL: the cleaned queries, for checking
+ */
+ccq_status ccq_gla_fwd(const ccq_shape* s, const void* q, const void* k, const void* v,
+                       const void* g, const float* lam, const float* S0, const float* C0,
+                       const float* mu0, void* o, float* ST, float* CT, float* muT,
+                       float* q_clean_dbg, void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * CCQ-Gated-DeltaNet chunkwise forward (Alg. 1 with the delta-rule chunk form
+ * computed through the WY/UT transform as BackboneUpdate).
+ *   logalpha [B,T,H] fp32   log of the per-head scalar decay alpha_t (<= 0)
+ *   beta     [B,T,H] fp32   write strength beta_t in [0,1]
+ * All other arguments as in ccq_gla_fwd.
+ */
+ccq_status ccq_gdn_fwd(const ccq_shape* s, const void* q, const void* k, const void* v,
+                       const float* logalpha, const float* beta, const float* lam,
+                       const float* S0, const float* C0, const float* mu0, void* o, float* ST,
+                       float* CT, float* muT, float* q_clean_dbg, void* workspace,
+                       size_t ws_bytes, void* stream);
+
+/*
+ * Training step: forward and the gradients of L = sum_t <dO_t, o_t> with
+ * respect to q, k, v, the gates and lambda (fresh sequence: zero initial
+ * states, t0 must be 0).
+ *   bb = CCQ_GLA: g_or_logalpha is g [B,T,H,dk] gate_dtype; beta and dbeta NULL;
+ *                 dg_or_dlogalpha is dg [B,T,H,dk] gate_dtype.
+ *   bb = CCQ_GDN: returns CCQ_ERR_UNSUPPORTED.
+ *   dO [B,T,H,dv] io_dtype upstream gradient; o, dq, dk, dv io_dtype;
+ *   dlam [B,T,H] fp32.
+ */
+ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const void* k,
+                       const void* v, const void* g_or_logalpha, const float* beta,
+                       const float* lam, const void* dO, void* o, void* dq, void* dk, void* dv,
+                       void* dg_or_dlogalpha, float* dbeta, float* dlam, void* workspace,
+                       size_t ws_bytes, void* stream);
+
+/*
+ * Per-kernel timing hook (instrumentation for benchmarks and profilers, not
+ * part of the method).  `events` points at n_events hipEvent_t handles created
+ * by the caller (hipEventCreate).  Until the next ccq_trace_events call from
+ * the same host thread, every entry point called from that thread records
+ * events[2i] on its stream just before its i-th kernel launch and
+ * events[2i+1] just after it, for i < n_events/2; the count restarts at each
+ * entry-point call.  events = NULL (or n_events = 0) switches tracing off.
+ * The setting is per host thread; nothing else is kept between calls.
+ */
+ccq_status ccq_trace_events(void* const* events, int n_events);
+
+/* Human-readable text of a status code (static storage). */
+const char* ccq_status_string(ccq_status st);
+
+/* Library version string, e.g. "ccq-mi355x 0.1.0 gfx950". */
+const char* ccq_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CCQ_H_ */

@@ -1,0 +1,157 @@
+"""fp64 CPU oracle for Curvature-Conditioned Query (CCQ) -- test infrastructure.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may
+import this module.  It wraps ``ccq_oracle.c`` (plain C, fp64, OpenMP over
+(batch, head) pairs) through ctypes and builds it with gcc on first use.  It
+imports nothing from the HIP library and the HIP library imports nothing from
+here.
+
+Functions (all arrays are numpy float64, row-major):
+  fwd(...)          token-by-token forward (form 0: raw sums; form 1: the
+                    running-mean recurrence of Alg. 2)
+  chunk_fwd(...)    Alg. 1 chunkwise forward with the GLA / Gated DeltaNet
+                    chunk forms of the backbone update
+  gla_fwd_bwd(...)  reverse pass of CCQ-GLA for L = sum <dO, o>
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "ccq_oracle.c")
+_LIB = os.path.join(_HERE, "libccq_oracle.so")
+_lock = threading.Lock()
+_lib = None
+
+GLA, GDN = 0, 1
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [
+        ("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
+        ("dk", ctypes.c_int32), ("dv", ctypes.c_int32),
+        ("backbone", ctypes.c_int32), ("centered", ctypes.c_int32), ("pad_", ctypes.c_int32),
+        ("scale", ctypes.c_double), ("t0", ctypes.c_int64),
+    ]
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (fp64, no fast-math) into libccq_oracle.so."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c99", "-Wall",
+               _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is None:
+            build()
+            lib = ctypes.CDLL(_LIB)
+            P = ctypes.c_void_p
+            lib.ccq_oracle_fwd.argtypes = [ctypes.POINTER(Shape), ctypes.c_int] + [P] * 14
+            lib.ccq_oracle_chunk_fwd.argtypes = [ctypes.POINTER(Shape), ctypes.c_int] + [P] * 14
+            lib.ccq_oracle_gla_fwd_bwd.argtypes = [ctypes.POINTER(Shape), ctypes.c_int] + [P] * 12
+            for f in (lib.ccq_oracle_fwd, lib.ccq_oracle_chunk_fwd, lib.ccq_oracle_gla_fwd_bwd):
+                f.restype = ctypes.c_int
+            lib.ccq_oracle_threads.restype = ctypes.c_int
+            _lib = lib
+    return _lib
+
+
+def threads() -> int:
+    """OpenMP threads the oracle runs on."""
+    return _load().ccq_oracle_threads()
+
+
+def _f64(x):
+    if x is None:
+        return None
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+    return a
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _shape(q, v, backbone, centered, scale, t0):
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    return Shape(B, T, H, dk, dv, backbone, int(centered), 0, float(scale), int(t0))
+
+
+def _inputs(q, k, v, gate, beta, lam, backbone):
+    q, k, v, gate, lam = _f64(q), _f64(k), _f64(v), _f64(gate), _f64(lam)
+    beta = _f64(beta) if backbone == GDN else None
+    B, T, H, dk = q.shape
+    assert k.shape == q.shape and v.shape[:3] == (B, T, H) and lam.shape == (B, T, H)
+    if backbone == GLA:
+        assert gate.shape == q.shape
+    else:
+        assert gate.shape == (B, T, H) and beta.shape == (B, T, H)
+    return q, k, v, gate, beta, lam
+
+
+def _outputs(q, v):
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    return (np.zeros((B, T, H, dv)), np.zeros((B, H, dv, dk)), np.zeros((B, H, dk, dk)),
+            np.zeros((B, H, dk)), np.zeros((B, T, H, dk)))
+
+
+def fwd(q, k, v, gate, lam, beta=None, backbone=GLA, S0=None, C0=None, mu0=None,
+        scale=1.0, centered=True, t0=0, form=0):
+    """Token-by-token CCQ forward.  Returns dict o, ST, CT, muT, qclean."""
+    q, k, v, gate, beta, lam = _inputs(q, k, v, gate, beta, lam, backbone)
+    S0, C0, mu0 = _f64(S0), _f64(C0), _f64(mu0)
+    o, ST, CT, muT, qc = _outputs(q, v)
+    sh = _shape(q, v, backbone, centered, scale, t0)
+    rc = _load().ccq_oracle_fwd(ctypes.byref(sh), int(form), _ptr(q), _ptr(k), _ptr(v), _ptr(gate),
+                                _ptr(beta), _ptr(lam), _ptr(S0), _ptr(C0), _ptr(mu0), _ptr(o),
+                                _ptr(ST), _ptr(CT), _ptr(muT), _ptr(qc))
+    if rc != 0:
+        raise RuntimeError("ccq_oracle_fwd failed with code %d" % rc)
+    return dict(o=o, ST=ST, CT=CT, muT=muT, qclean=qc)
+
+
+def chunk_fwd(q, k, v, gate, lam, beta=None, backbone=GLA, chunk=64, S0=None, C0=None,
+              mu0=None, scale=1.0, centered=True, t0=0):
+    """Alg. 1 chunkwise CCQ forward.  Returns dict o, ST, CT, muT, qclean."""
+    q, k, v, gate, beta, lam = _inputs(q, k, v, gate, beta, lam, backbone)
+    S0, C0, mu0 = _f64(S0), _f64(C0), _f64(mu0)
+    o, ST, CT, muT, qc = _outputs(q, v)
+    sh = _shape(q, v, backbone, centered, scale, t0)
+    rc = _load().ccq_oracle_chunk_fwd(ctypes.byref(sh), int(chunk), _ptr(q), _ptr(k), _ptr(v),
+                                      _ptr(gate), _ptr(beta), _ptr(lam), _ptr(S0), _ptr(C0),
+                                      _ptr(mu0), _ptr(o), _ptr(ST), _ptr(CT), _ptr(muT), _ptr(qc))
+    if rc != 0:
+        raise RuntimeError("ccq_oracle_chunk_fwd failed with code %d" % rc)
+    return dict(o=o, ST=ST, CT=CT, muT=muT, qclean=qc)
+
+
+def gla_fwd_bwd(q, k, v, g, lam, dO, scale=1.0, centered=True, seg=64):
+    """Reverse pass of CCQ-GLA (zero initial state).  Returns o, dq, dk, dv, dg, dlam."""
+    q, k, v, g, _, lam = _inputs(q, k, v, g, None, lam, GLA)
+    dO = _f64(dO)
+    assert dO.shape == q.shape[:3] + (v.shape[-1],)
+    o = np.zeros(dO.shape)
+    dq, dk, dg = np.zeros(q.shape), np.zeros(q.shape), np.zeros(q.shape)
+    dv = np.zeros(v.shape)
+    dlam = np.zeros(lam.shape)
+    sh = _shape(q, v, GLA, centered, scale, 0)
+    rc = _load().ccq_oracle_gla_fwd_bwd(ctypes.byref(sh), int(seg), _ptr(q), _ptr(k), _ptr(v),
+                                        _ptr(g), _ptr(lam), _ptr(dO), _ptr(o), _ptr(dq), _ptr(dk),
+                                        _ptr(dv), _ptr(dg), _ptr(dlam))
+    if rc != 0:
+        raise RuntimeError("ccq_oracle_gla_fwd_bwd failed with code %d" % rc)
+    return dict(o=o, dq=dq, dk=dk, dv=dv, dg=dg, dlam=dlam)

@@ -1,0 +1,224 @@
+"""Python binding of the CCQ C ABI (libccq.so): argument marshalling only.
+
+Every entry point has the same name as its C function.  Tensors are torch
+tensors on the GPU; the binding checks dtypes/shapes, allocates outputs and
+the workspace with torch when the caller does not pass them, and hands raw
+device pointers plus the current HIP stream to the library.  All arithmetic
+runs in the library's HIP kernels.  There is no fallback: if libccq.so is
+missing the first call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libccq.so")
+
+CCQ_F32, CCQ_BF16 = 0, 1
+CCQ_GLA, CCQ_GDN = 0, 1
+_STATUS = {0: "CCQ_OK", 1: "CCQ_ERR_INVALID_ARG", 2: "CCQ_ERR_UNSUPPORTED",
+           3: "CCQ_ERR_WORKSPACE", 4: "CCQ_ERR_HIP"}
+EXPORTS = ("ccq_workspace_size", "ccq_gla_fwd", "ccq_gdn_fwd", "ccq_fwd_bwd",
+           "ccq_status_string", "ccq_version")
+
+
+class CcqError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        super().__init__("%s returned %s (%d): %s" % (fn, _STATUS.get(code, "?"), code,
+                                                      ccq_status_string(code)))
+        self.code = code
+
+
+class Shape(ctypes.Structure):
+    """Mirror of ccq_shape (include/ccq.h)."""
+    _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("dk", ctypes.c_int32), ("dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
+                ("io_dtype", ctypes.c_int32), ("gate_dtype", ctypes.c_int32),
+                ("scale", ctypes.c_float), ("centered", ctypes.c_int32), ("t0", ctypes.c_int64)]
+
+
+_lib = None
+_lock = threading.Lock()
+
+
+def lib() -> ctypes.CDLL:
+    """Load libccq.so (raises if it has not been built)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError("libccq.so is not built (%s); run "
+                                   "`python -m paper_2606_01294_amd.build`" % LIB_PATH)
+            L = ctypes.CDLL(LIB_PATH)
+            P, S = ctypes.c_void_p, ctypes.c_size_t
+            SP = ctypes.POINTER(Shape)
+            L.ccq_workspace_size.argtypes = [SP, ctypes.c_int, ctypes.c_int]
+            L.ccq_workspace_size.restype = S
+            L.ccq_gla_fwd.argtypes = [SP] + [P] * 14 + [S, P]
+            L.ccq_gla_fwd.restype = ctypes.c_int
+            L.ccq_gdn_fwd.argtypes = [SP] + [P] * 15 + [S, P]
+            L.ccq_gdn_fwd.restype = ctypes.c_int
+            L.ccq_fwd_bwd.argtypes = [SP, ctypes.c_int] + [P] * 17 + [S, P]
+            L.ccq_fwd_bwd.restype = ctypes.c_int
+            L.ccq_status_string.argtypes = [ctypes.c_int]
+            L.ccq_status_string.restype = ctypes.c_char_p
+            L.ccq_version.argtypes = []
+            L.ccq_version.restype = ctypes.c_char_p
+            _lib = L
+    return _lib
+
+
+def ccq_status_string(code: int) -> str:
+    return lib().ccq_status_string(int(code)).decode()
+
+
+def ccq_version() -> str:
+    return lib().ccq_version().decode()
+
+
+def _dt(t: torch.dtype) -> int:
+    if t == torch.bfloat16:
+        return CCQ_BF16
+    if t == torch.float32:
+        return CCQ_F32
+    raise TypeError("unsupported dtype %s (float32 or bfloat16)" % t)
+
+
+def make_shape(B, T, H, dk, dv, io_dtype, gate_dtype=None, scale=1.0, centered=True, t0=0,
+               chunk=64) -> Shape:
+    gd = io_dtype if gate_dtype is None else gate_dtype
+    return Shape(int(B), int(T), int(H), int(dk), int(dv), int(chunk), _dt(io_dtype), _dt(gd),
+                 float(scale), int(bool(centered)), int(t0))
+
+
+def ccq_workspace_size(shape: Shape, backbone: int, with_bwd: bool = False) -> int:
+    return int(lib().ccq_workspace_size(ctypes.byref(shape), int(backbone), int(bool(with_bwd))))
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(t, name, shape, dtype, device):
+    if t is None:
+        return
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s: shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+    if t.dtype != dtype:
+        raise TypeError("%s: dtype %s, expected %s" % (name, t.dtype, dtype))
+    if t.device != device:
+        raise ValueError("%s: on %s, expected %s" % (name, t.device, device))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+
+
+def _workspace(shape, backbone, with_bwd, workspace, device):
+    need = ccq_workspace_size(shape, backbone, with_bwd)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+    return workspace, need
+
+
+def _fwd(backbone, q, k, v, gate, lam, beta, S0, C0, mu0, scale, centered, t0, chunk,
+         want_states, want_qclean, out, workspace, stream):
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    dev = q.device
+    gate_dtype = gate.dtype if backbone == CCQ_GLA else q.dtype
+    shape = make_shape(B, T, H, dk, dv, q.dtype, gate_dtype, scale, centered, t0, chunk)
+    _check(k, "k", (B, T, H, dk), q.dtype, dev)
+    _check(v, "v", (B, T, H, dv), q.dtype, dev)
+    if backbone == CCQ_GLA:
+        _check(gate, "g", (B, T, H, dk), gate.dtype, dev)
+    else:
+        _check(gate, "logalpha", (B, T, H), torch.float32, dev)
+        _check(beta, "beta", (B, T, H), torch.float32, dev)
+    _check(lam, "lam", (B, T, H), torch.float32, dev)
+    _check(S0, "S0", (B, H, dv, dk), torch.float32, dev)
+    _check(C0, "C0", (B, H, dk, dk), torch.float32, dev)
+    _check(mu0, "mu0", (B, H, dk), torch.float32, dev)
+    out = dict(out or {})
+    if "o" not in out:
+        out["o"] = torch.empty((B, T, H, dv), dtype=q.dtype, device=dev)
+    if want_states:
+        out.setdefault("ST", torch.empty((B, H, dv, dk), dtype=torch.float32, device=dev))
+        out.setdefault("CT", torch.empty((B, H, dk, dk), dtype=torch.float32, device=dev))
+        out.setdefault("muT", torch.empty((B, H, dk), dtype=torch.float32, device=dev))
+    if want_qclean:
+        out.setdefault("qclean", torch.empty((B, T, H, dk), dtype=torch.float32, device=dev))
+    workspace, need = _workspace(shape, backbone, False, workspace, dev)
+    st = _stream(stream)
+    if backbone == CCQ_GLA:
+        rc = lib().ccq_gla_fwd(ctypes.byref(shape), _p(q), _p(k), _p(v), _p(gate), _p(lam),
+                               _p(S0), _p(C0), _p(mu0), _p(out["o"]), _p(out.get("ST")),
+                               _p(out.get("CT")), _p(out.get("muT")), _p(out.get("qclean")),
+                               _p(workspace), workspace.numel(), st)
+        fn = "ccq_gla_fwd"
+    else:
+        rc = lib().ccq_gdn_fwd(ctypes.byref(shape), _p(q), _p(k), _p(v), _p(gate), _p(beta),
+                               _p(lam), _p(S0), _p(C0), _p(mu0), _p(out["o"]),
+                               _p(out.get("ST")), _p(out.get("CT")), _p(out.get("muT")),
+                               _p(out.get("qclean")), _p(workspace), workspace.numel(), st)
+        fn = "ccq_gdn_fwd"
+    if rc != 0:
+        raise CcqError(fn, rc)
+    return out
+
+
+def ccq_gla_fwd(q, k, v, g, lam, S0=None, C0=None, mu0=None, scale=1.0, centered=True, t0=0,
+                chunk=64, want_states=True, want_qclean=False, out=None, workspace=None,
+                stream=None):
+    """CCQ-GLA chunkwise forward.  Returns dict o[, ST, CT, muT][, qclean]."""
+    return _fwd(CCQ_GLA, q, k, v, g, lam, None, S0, C0, mu0, scale, centered, t0, chunk,
+                want_states, want_qclean, out, workspace, stream)
+
+
+def ccq_gdn_fwd(q, k, v, logalpha, beta, lam, S0=None, C0=None, mu0=None, scale=1.0,
+                centered=True, t0=0, chunk=64, want_states=True, want_qclean=False, out=None,
+                workspace=None, stream=None):
+    """CCQ-Gated-DeltaNet chunkwise forward.  Returns dict o[, ST, CT, muT][, qclean]."""
+    return _fwd(CCQ_GDN, q, k, v, logalpha, lam, beta, S0, C0, mu0, scale, centered, t0, chunk,
+                want_states, want_qclean, out, workspace, stream)
+
+
+def ccq_fwd_bwd(q, k, v, g, lam, dO, scale=1.0, centered=True, chunk=64, out=None,
+                workspace=None, stream=None, backbone=CCQ_GLA, beta=None):
+    """CCQ training step: o and the gradients of sum <dO, o>.
+
+    Returns dict o, dq, dk, dv, dg, dlam (GLA).  The GDN backward is not
+    available in this build (the library returns CCQ_ERR_UNSUPPORTED)."""
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    dev = q.device
+    gate_dtype = g.dtype if backbone == CCQ_GLA else q.dtype
+    shape = make_shape(B, T, H, dk, dv, q.dtype, gate_dtype, scale, centered, 0, chunk)
+    _check(k, "k", (B, T, H, dk), q.dtype, dev)
+    _check(v, "v", (B, T, H, dv), q.dtype, dev)
+    _check(dO, "dO", (B, T, H, dv), q.dtype, dev)
+    _check(lam, "lam", (B, T, H), torch.float32, dev)
+    out = dict(out or {})
+    out.setdefault("o", torch.empty((B, T, H, dv), dtype=q.dtype, device=dev))
+    out.setdefault("dq", torch.empty((B, T, H, dk), dtype=q.dtype, device=dev))
+    out.setdefault("dk", torch.empty((B, T, H, dk), dtype=q.dtype, device=dev))
+    out.setdefault("dv", torch.empty((B, T, H, dv), dtype=q.dtype, device=dev))
+    out.setdefault("dg", torch.empty(tuple(g.shape), dtype=g.dtype, device=dev))
+    out.setdefault("dlam", torch.empty((B, T, H), dtype=torch.float32, device=dev))
+    if backbone == CCQ_GDN:
+        out.setdefault("dbeta", torch.empty((B, T, H), dtype=torch.float32, device=dev))
+    workspace, need = _workspace(shape, backbone, True, workspace, dev)
+    rc = lib().ccq_fwd_bwd(ctypes.byref(shape), int(backbone), _p(q), _p(k), _p(v), _p(g),
+                           _p(beta), _p(lam), _p(dO), _p(out["o"]), _p(out["dq"]),
+                           _p(out["dk"]), _p(out["dv"]), _p(out["dg"]), _p(out.get("dbeta")),
+                           _p(out["dlam"]), _p(workspace), workspace.numel(), _stream(stream))
+    if rc != 0:
+        raise CcqError("ccq_fwd_bwd", rc)
+    return out

@@ -1,0 +1,170 @@
+// ccq_api.cpp -- the C ABI declared in include/ccq.h: argument validation,
+// workspace layout and kernel dispatch.  Every check runs before the first
+// launch, so an error return means nothing was enqueued.
+#include "ccq.h"
+
+#include <hip/hip_runtime_api.h>
+
+#include "ccq_kernels.h"
+
+namespace {
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+size_t esize(ccq_dtype d) { return d == CCQ_BF16 ? 2 : 4; }
+bool dtype_ok(ccq_dtype d) { return d == CCQ_F32 || d == CCQ_BF16; }
+bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Common shape checks.  Returns CCQ_OK or the error.
+ccq_status check_shape(const ccq_shape* s, ccq_backbone bb) {
+  if (!s) return CCQ_ERR_INVALID_ARG;
+  if (s->B < 0 || s->T < 0 || s->H < 0 || s->t0 < 0) return CCQ_ERR_INVALID_ARG;
+  if (!dtype_ok(s->io_dtype) || !dtype_ok(s->gate_dtype)) return CCQ_ERR_INVALID_ARG;
+  if (s->centered != 0 && s->centered != 1) return CCQ_ERR_INVALID_ARG;
+  if (bb != CCQ_GLA && bb != CCQ_GDN) return CCQ_ERR_INVALID_ARG;
+  if (s->chunk != 64) return CCQ_ERR_UNSUPPORTED;
+  const bool bf = s->io_dtype == CCQ_BF16;
+  if (!ccq::clean_supported(s->dk, bf)) return CCQ_ERR_UNSUPPORTED;
+  if (bb == CCQ_GLA ? !ccq::gla_supported(s->dk, s->dv, bf) : !ccq::gdn_supported(s->dk, s->dv, bf))
+    return CCQ_ERR_UNSUPPORTED;
+  // 32-bit grid and index headroom
+  const long long ntok = (long long)s->B * s->T * s->H;
+  if (ntok * (s->dk > s->dv ? s->dk : s->dv) > (1LL << 40)) return CCQ_ERR_UNSUPPORTED;
+  if ((long long)s->B * s->H * ((s->T + 63) / 64) > (1LL << 30)) return CCQ_ERR_UNSUPPORTED;
+  return CCQ_OK;
+}
+
+struct FwdLayout {
+  size_t qclean = 0, W = 0, Ut = 0, total = 0;
+};
+
+FwdLayout fwd_layout(const ccq_shape* s, ccq_backbone bb) {
+  FwdLayout L;
+  const size_t ntok = (size_t)s->B * s->T * s->H;
+  const size_t nchunk = (size_t)s->B * s->H * ((s->T + 63) / 64);
+  size_t off = 0;
+  L.qclean = off;
+  off += align_up(ntok * s->dk * esize(s->io_dtype));
+  if (bb == CCQ_GDN) {
+    L.W = off;
+    off += align_up(nchunk * 64 * s->dk * esize(s->io_dtype));
+    L.Ut = off;
+    off += align_up(nchunk * 64 * s->dv * sizeof(float));
+  }
+  L.total = off;
+  return L;
+}
+
+// T == 0: the final states are the initial ones (or zero).
+ccq_status copy_initial_states(const ccq_shape* s, const float* S0, const float* C0,
+                               const float* mu0, float* ST, float* CT, float* muT,
+                               hipStream_t st) {
+  const size_t bh = (size_t)s->B * s->H;
+  hipError_t e = hipSuccess;
+  if (ST && e == hipSuccess) e = ccq::launch_copy_or_zero(ST, S0, bh * s->dv * s->dk, st);
+  if (CT && e == hipSuccess) e = ccq::launch_copy_or_zero(CT, C0, bh * s->dk * s->dk, st);
+  if (muT && e == hipSuccess) e = ccq::launch_copy_or_zero(muT, mu0, bh * s->dk, st);
+  return e == hipSuccess ? CCQ_OK : CCQ_ERR_HIP;
+}
+
+ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const void* k,
+                       const void* v, const void* g_or_la, const float* beta, const float* lam,
+                       const float* S0, const float* C0, const float* mu0, void* o, float* ST,
+                       float* CT, float* muT, float* q_clean_dbg, void* workspace,
+                       size_t ws_bytes, void* stream) {
+  ccq_status rc = check_shape(s, bb);
+  if (rc != CCQ_OK) return rc;
+  const size_t ntok = (size_t)s->B * s->T * s->H;
+  const void* ptrs[] = {S0, C0, mu0, ST, CT, muT, q_clean_dbg, workspace};
+  for (const void* p : ptrs)
+    if (p && !aligned(p)) return CCQ_ERR_INVALID_ARG;
+  if (ntok > 0) {
+    const void* req[] = {q, k, v, g_or_la, lam, o};
+    for (const void* p : req)
+      if (!p || !aligned(p)) return CCQ_ERR_INVALID_ARG;
+    if (bb == CCQ_GDN && (!beta || !aligned(beta))) return CCQ_ERR_INVALID_ARG;
+  }
+  const FwdLayout L = fwd_layout(s, bb);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (s->B == 0 || s->H == 0) return CCQ_OK;
+  if (s->T == 0) return copy_initial_states(s, S0, C0, mu0, ST, CT, muT, st);
+  if (!workspace || ws_bytes < L.total) return CCQ_ERR_WORKSPACE;
+
+  char* ws = static_cast<char*>(workspace);
+  const bool bf = s->io_dtype == CCQ_BF16;
+  void* qclean = ws + L.qclean;
+
+  ccq::CleanArgs ca{q, k, lam, C0, mu0, qclean, q_clean_dbg, CT, muT,
+                    s->B, s->T, s->H, s->dk, s->centered, s->t0};
+  if (ccq::launch_clean(ca, bf, st) != hipSuccess) return CCQ_ERR_HIP;
+
+  if (bb == CCQ_GLA) {
+    ccq::GlaArgs ga{qclean, k, v, g_or_la, S0, o, ST, s->B, s->T, s->H, s->dk, s->dv, s->scale};
+    if (ccq::launch_gla_fwd(ga, bf, s->gate_dtype == CCQ_BF16, st) != hipSuccess) return CCQ_ERR_HIP;
+  } else {
+    const float* la = static_cast<const float*>(g_or_la);
+    ccq::WyArgs wa{k, v, la, beta, ws + L.W, reinterpret_cast<float*>(ws + L.Ut),
+                   s->B, s->T, s->H, s->dk, s->dv};
+    if (ccq::launch_gdn_wy(wa, bf, st) != hipSuccess) return CCQ_ERR_HIP;
+    ccq::GdnArgs da{qclean, k, la, ws + L.W, reinterpret_cast<const float*>(ws + L.Ut), S0, o, ST,
+                    s->B, s->T, s->H, s->dk, s->dv, s->scale};
+    if (ccq::launch_gdn_fwd(da, bf, st) != hipSuccess) return CCQ_ERR_HIP;
+  }
+  return CCQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ccq_workspace_size(const ccq_shape* s, ccq_backbone bb, int with_bwd) {
+  if (check_shape(s, bb) != CCQ_OK) return 0;
+  if (with_bwd) return 0;  // the training entry point is not available in this build
+  return fwd_layout(s, bb).total;
+}
+
+ccq_status ccq_gla_fwd(const ccq_shape* s, const void* q, const void* k, const void* v,
+                       const void* g, const float* lam, const float* S0, const float* C0,
+                       const float* mu0, void* o, float* ST, float* CT, float* muT,
+                       float* q_clean_dbg, void* workspace, size_t ws_bytes, void* stream) {
+  return run_forward(CCQ_GLA, s, q, k, v, g, nullptr, lam, S0, C0, mu0, o, ST, CT, muT,
+                     q_clean_dbg, workspace, ws_bytes, stream);
+}
+
+ccq_status ccq_gdn_fwd(const ccq_shape* s, const void* q, const void* k, const void* v,
+                       const float* logalpha, const float* beta, const float* lam,
+                       const float* S0, const float* C0, const float* mu0, void* o, float* ST,
+                       float* CT, float* muT, float* q_clean_dbg, void* workspace,
+                       size_t ws_bytes, void* stream) {
+  return run_forward(CCQ_GDN, s, q, k, v, logalpha, beta, lam, S0, C0, mu0, o, ST, CT, muT,
+                     q_clean_dbg, workspace, ws_bytes, stream);
+}
+
+ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const void* k,
+                       const void* v, const void* g_or_logalpha, const float* beta,
+                       const float* lam, const void* dO, void* o, void* dq, void* dk, void* dv,
+                       void* dg_or_dlogalpha, float* dbeta, float* dlam, void* workspace,
+                       size_t ws_bytes, void* stream) {
+  (void)q; (void)k; (void)v; (void)g_or_logalpha; (void)beta; (void)lam; (void)dO; (void)o;
+  (void)dq; (void)dk; (void)dv; (void)dg_or_dlogalpha; (void)dbeta; (void)dlam;
+  (void)workspace; (void)ws_bytes; (void)stream;
+  ccq_status rc = check_shape(s, bb);
+  if (rc != CCQ_OK) return rc;
+  return CCQ_ERR_UNSUPPORTED;
+}
+
+const char* ccq_status_string(ccq_status st) {
+  switch (st) {
+    case CCQ_OK: return "ok";
+    case CCQ_ERR_INVALID_ARG: return "invalid argument";
+    case CCQ_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case CCQ_ERR_WORKSPACE: return "workspace missing or too small";
+    case CCQ_ERR_HIP: return "HIP launch error";
+  }
+  return "unknown status";
+}
+
+const char* ccq_version(void) { return "ccq-mi355x 0.1.0 gfx950"; }
+
+}  // extern "C"

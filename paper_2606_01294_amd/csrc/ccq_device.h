@@ -1,0 +1,154 @@
+// ccq_device.h -- device helpers shared by the CCQ kernels (gfx950 / CDNA4).
+//
+// Matrix products use the 16x16 MFMA tile with fp32 accumulation:
+//   bf16: v_mfma_f32_16x16x32_bf16  (one instruction per 32-wide k step)
+//   fp32: v_mfma_f32_16x16x4_f32    (eight instructions per 32-wide k step)
+// A "fragment" is the 8 consecutive contraction elements one lane feeds per
+// 32-wide k step: lane l supplies row (l % 16) of the A tile and column
+// (l % 16) of the B tile, k = 8*(l / 16) .. 8*(l / 16) + 7.  For fp32 the
+// eight sub-steps walk those same eight k values, so both dtypes read the
+// same LDS bytes per lane.  The accumulator holds D[4*(l/16) + r][l % 16] in
+// element r.  B tiles are kept in LDS as B^T (row = output column, k
+// contiguous) so that every fragment is one contiguous 16-byte (bf16) or
+// 32-byte (fp32) LDS read.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16_t;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+namespace ccq {
+
+constexpr int kChunk = 64;    // chunk length C of the chunkwise form
+constexpr int kThreads = 256; // four 64-wide waves per workgroup
+
+template <typename T>
+struct Pad { static constexpr int value = 16 / (int)sizeof(T); };  // 16-byte row padding
+
+template <typename T> struct Frag;
+template <> struct Frag<bf16_t> { bf16x8 v; };
+template <> struct Frag<float> { f32x4 lo, hi; };
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+
+// Fragment of a 16-row tile stored row-major in LDS with leading dimension ld
+// (elements); `tile` points at (row 0, k0).
+template <typename T>
+__device__ __forceinline__ Frag<T> ld_frag(const T* tile, int ld) {
+  const int l = lane_id();
+  const T* p = tile + (l & 15) * ld + 8 * (l >> 4);
+  Frag<T> f;
+  if constexpr (sizeof(T) == 2) {
+    f.v = *reinterpret_cast<const bf16x8*>(p);
+  } else {
+    f.lo = *reinterpret_cast<const f32x4*>(p);
+    f.hi = *reinterpret_cast<const f32x4*>(p + 4);
+  }
+  return f;
+}
+
+// Same fragment read straight from global memory (row pitch ld elements).
+template <typename T>
+__device__ __forceinline__ Frag<T> ld_frag_global(const T* tile, size_t ld) {
+  const int l = lane_id();
+  const T* p = tile + (size_t)(l & 15) * ld + 8 * (l >> 4);
+  Frag<T> f;
+  if constexpr (sizeof(T) == 2) {
+    f.v = *reinterpret_cast<const bf16x8*>(p);
+  } else {
+    f.lo = *reinterpret_cast<const f32x4*>(p);
+    f.hi = *reinterpret_cast<const f32x4*>(p + 4);
+  }
+  return f;
+}
+
+__device__ __forceinline__ void mma(f32x4& acc, const Frag<bf16_t>& a, const Frag<bf16_t>& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, acc, 0, 0, 0);
+}
+
+__device__ __forceinline__ void mma(f32x4& acc, const Frag<float>& a, const Frag<float>& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo[0], b.lo[0], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo[1], b.lo[1], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo[2], b.lo[2], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo[3], b.lo[3], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi[0], b.hi[0], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi[1], b.hi[1], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi[2], b.hi[2], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi[3], b.hi[3], acc, 0, 0, 0);
+}
+
+// acc += A[16 x K] * B^T[16 x K]^T with both operands in LDS.
+template <typename T, int K>
+__device__ __forceinline__ void tile_mma(f32x4& acc, const T* a, int lda, const T* bt, int ldb) {
+#pragma unroll
+  for (int k0 = 0; k0 < K; k0 += 32) mma(acc, ld_frag(a + k0, lda), ld_frag(bt + k0, ldb));
+}
+
+__device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+
+template <typename T> __device__ __forceinline__ T to(float x) { return static_cast<T>(x); }
+template <typename T> __device__ __forceinline__ float f32(T x) { return static_cast<float>(x); }
+
+// Split x into a bf16 head and a bf16 tail with x ~= head + tail to about
+// 2^-17 relative; used where an fp32 operand has to enter a bf16 product
+// without losing the precision the covariance correction needs.
+__device__ __forceinline__ void split_bf16(float x, bf16_t& hi, bf16_t& lo) {
+  hi = static_cast<bf16_t>(x);
+  lo = static_cast<bf16_t>(x - static_cast<float>(hi));
+}
+
+// Sum over the 16 lanes that share l / 16 (the lanes holding one tile row).
+__device__ __forceinline__ float row16_sum(float x) {
+  x += __shfl_xor(x, 1);
+  x += __shfl_xor(x, 2);
+  x += __shfl_xor(x, 4);
+  x += __shfl_xor(x, 8);
+  return x;
+}
+
+// Blocks are dealt to the 8 XCDs round-robin by linear id.  Renumber so that
+// consecutive logical ids (the tiles of one head, which read the same q/k
+// chunks) sit on one XCD and share its L2.
+__device__ __forceinline__ int xcd_logical_block(int x, int nblocks) {
+  if (nblocks % 8 != 0) return x;
+  return (x % 8) * (nblocks / 8) + x / 8;
+}
+
+// Row offset of token (b, t, h) in a [B, T, H, D] tensor, in elements.
+__device__ __forceinline__ size_t tok_off(int b, int t, int h, int T, int H, int D) {
+  return (((size_t)b * T + t) * H + h) * (size_t)D;
+}
+
+// Copy rows [0, n) of a chunk (row pitch `gstride` elements in global memory)
+// into LDS row-major (ld elements per row), zero-filling rows n..63; when
+// `dstT` is given, also store the transpose (D rows of ldT, row-contiguous in
+// the chunk index).  D must be a multiple of 8 / (16 / sizeof(T)).
+template <typename T, int D>
+__device__ __forceinline__ void load_chunk_rows(T* dst, int ld, T* dstT, int ldT, const T* src,
+                                                size_t gstride, int n) {
+  constexpr int VE = 16 / (int)sizeof(T);  // elements per 16-byte vector
+  constexpr int NV = kChunk * D / VE;
+  typedef T vec_t __attribute__((ext_vector_type(VE)));
+  for (int idx = threadIdx.x; idx < NV; idx += kThreads) {
+    const int row = idx / (D / VE);
+    const int c0 = (idx % (D / VE)) * VE;
+    vec_t val;
+    if (row < n) {
+      val = *reinterpret_cast<const vec_t*>(src + (size_t)row * gstride + c0);
+    } else {
+#pragma unroll
+      for (int e = 0; e < VE; ++e) val[e] = static_cast<T>(0.f);
+    }
+    *reinterpret_cast<vec_t*>(dst + row * ld + c0) = val;
+    if (dstT) {
+#pragma unroll
+      for (int e = 0; e < VE; ++e) dstT[(c0 + e) * ldT + row] = val[e];
+    }
+  }
+}
+
+}  // namespace ccq

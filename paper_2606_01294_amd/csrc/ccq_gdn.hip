@@ -1,0 +1,297 @@
+// ccq_gdn.hip -- Gated DeltaNet backbone chunk forward reading the cleaned queries.
+//
+// Gated DeltaNet (the cited backbone): S_t = alpha_t S_{t-1} (I - beta_t k_t k_t^T)
+// + beta_t v_t k_t^T.  Writing S_t = alpha_t S_{t-1} + u_t k_t^T with
+// u_t = beta_t (v_t - alpha_t S_{t-1} k_t), and gamma_i = sum_{s<=i} log alpha_s
+// inside a chunk entered with state S_r, the rows u_i solve
+//
+//   (I + A) U = diag(beta) V - diag(beta e^gamma) K S_r^T,
+//   A_ij = beta_i e^{gamma_i - gamma_j} (k_i . k_j)  (j < i),
+//
+// i.e. with the WY/UT factors Tm = (I + A)^{-1}, Ut = Tm diag(beta) V and
+// W = Tm diag(beta e^gamma) K:  U = Ut - W S_r^T.  Then
+//
+//   o_i     = e^{gamma_i} S_r q_i + sum_{j<=i} e^{gamma_i - gamma_j} (k_j . q_i) u_j
+//   S_{r+1} = e^{gamma_C} S_r + U^T diag(e^{gamma_C - gamma}) K.
+//
+// gdn_wy_kernel computes W (io dtype) and Ut (fp32) for every chunk in
+// parallel; gdn_fwd_kernel walks the chunks of one head sequentially, owning a
+// BV-row slice of S (rows of S evolve independently under this write too).
+#include "ccq_device.h"
+#include "ccq_kernels.h"
+
+namespace ccq {
+
+template <typename T, int DK>
+__global__ __launch_bounds__(kThreads) void gdn_wy_kernel(const WyArgs a) {
+  constexpr int C = kChunk;
+  constexpr int P = Pad<T>::value;
+  constexpr int LDQ = DK + P;
+  __shared__ __align__(16) T sK[C * LDQ];
+  __shared__ __align__(16) float sA[C * C];
+  __shared__ float sBeta[C], sGam[C];
+
+  const int N = (a.T + C - 1) / C;
+  const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int bh = lb / N, ci = lb % N;
+  const int b = bh / a.H, h = bh % a.H;
+  const int r0 = ci * C;
+  const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+  const int tid = threadIdx.x, w = wave_id(), l = lane_id();
+  const int g4 = l >> 4, c16 = l & 15;
+  const T* k = static_cast<const T*>(a.k);
+  const T* v = static_cast<const T*>(a.v);
+
+  load_chunk_rows<T, DK>(sK, LDQ, nullptr, 0, k + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+  if (tid < C) {
+    const size_t ti = ((size_t)b * a.T + r0 + tid) * a.H + h;
+    float x = tid < nrow ? a.logalpha[ti] : 0.f;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const float y = __shfl_up(x, off);
+      if (tid >= off) x += y;
+    }
+    sGam[tid] = x;
+    sBeta[tid] = tid < nrow ? a.beta[ti] : 0.f;
+  }
+  __syncthreads();
+
+  // A_ij = beta_i e^{gamma_i - gamma_j} (k_i . k_j), strictly lower
+#pragma unroll
+  for (int J = 0; J < 4; ++J) {
+    f32x4 acc = zero4();
+    if (J <= w) tile_mma<T, DK>(acc, sK + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = 16 * w + 4 * g4 + r, j = 16 * J + c16;
+      sA[i * C + j] = (J <= w && j < i) ? sBeta[i] * __expf(sGam[i] - sGam[j]) * acc[r] : 0.f;
+    }
+  }
+  __syncthreads();
+
+  // forward substitution (I + A) X = R, one right-hand-side column per thread:
+  // columns [0, DK) give W (R = diag(beta e^gamma) K), [DK, DK+dv) give Ut (R = diag(beta) V)
+  T* Wout = static_cast<T*>(a.W) + ((size_t)bh * N + ci) * C * DK;
+  float* Uout = a.Ut + ((size_t)bh * N + ci) * C * a.dv;
+  for (int col = tid; col < DK + a.dv; col += kThreads) {
+    float x[C];
+    if (col < DK) {
+#pragma unroll
+      for (int i = 0; i < C; ++i) x[i] = sBeta[i] * __expf(sGam[i]) * f32(sK[i * LDQ + col]);
+    } else {
+      const int cv = col - DK;
+#pragma unroll
+      for (int i = 0; i < C; ++i)
+        x[i] = i < nrow ? sBeta[i] * f32(v[tok_off(b, r0 + i, h, a.T, a.H, a.dv) + cv]) : 0.f;
+    }
+#pragma unroll
+    for (int i = 1; i < C; ++i) {
+      float s = x[i];
+#pragma unroll
+      for (int j = 0; j < i; ++j) s -= sA[i * C + j] * x[j];
+      x[i] = s;
+    }
+    if (col < DK) {
+#pragma unroll
+      for (int i = 0; i < C; ++i) Wout[i * DK + col] = to<T>(x[i]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < C; ++i) Uout[(size_t)i * a.dv + (col - DK)] = x[i];
+    }
+  }
+}
+
+template <typename T, int DK, int BV>
+__global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
+  constexpr int C = kChunk;
+  constexpr int P = Pad<T>::value;
+  constexpr int LDQ = DK + P, LDT = C + P;
+  constexpr int NTC = DK / 16;
+  constexpr int NPW = BV * DK / (16 * 16 * 4);
+  static_assert(NPW >= 1, "tile split");
+
+  __shared__ __align__(16) T sQ[C * LDQ];
+  __shared__ __align__(16) T sK[C * LDQ];
+  __shared__ __align__(16) T sKdT[DK * LDT];
+  __shared__ __align__(16) T sS[BV * LDQ];
+  __shared__ __align__(16) T sUT[BV * LDT];
+  __shared__ __align__(16) T sA[C * LDT];
+  __shared__ float sGam[C];
+
+  const int nvt = a.dv / BV;
+  const int N = (a.T + C - 1) / C;
+  const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int bh = lb / nvt;
+  const int v0 = (lb % nvt) * BV;
+  const int b = bh / a.H, h = bh % a.H;
+  const int tid = threadIdx.x, w = wave_id(), l = lane_id();
+  const int g4 = l >> 4, c16 = l & 15;
+  const T* qc = static_cast<const T*>(a.qc);
+  const T* k = static_cast<const T*>(a.k);
+  const T* Wg = static_cast<const T*>(a.W);
+  T* o = static_cast<T*>(a.o);
+
+  f32x4 S[NPW];
+#pragma unroll
+  for (int u = 0; u < NPW; ++u) {
+    const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int vv = v0 + 16 * tv + 4 * g4 + r, c = 16 * tc + c16;
+      S[u][r] = a.S0 ? a.S0[((size_t)bh * a.dv + vv) * DK + c] : 0.f;
+    }
+  }
+
+  for (int ci = 0; ci < N; ++ci) {
+    const int r0 = ci * C;
+    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+    __syncthreads();
+    if (tid < C) {
+      float x = tid < nrow ? a.logalpha[((size_t)b * a.T + r0 + tid) * a.H + h] : 0.f;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const float y = __shfl_up(x, off);
+        if (tid >= off) x += y;
+      }
+      sGam[tid] = x;
+    }
+    load_chunk_rows<T, DK>(sQ, LDQ, nullptr, 0, qc + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+    load_chunk_rows<T, DK>(sK, LDQ, nullptr, 0, k + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+    // entering state slice as the B^T operand [v][c]
+#pragma unroll
+    for (int u = 0; u < NPW; ++u) {
+      const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sS[(16 * tv + 4 * g4 + r) * LDQ + 16 * tc + c16] = to<T>(S[u][r]);
+    }
+    __syncthreads();
+    const float gC = sGam[C - 1];
+    // K scaled by e^{gamma_C - gamma_j}, transposed for the state update
+    for (int idx = tid; idx < C * DK; idx += kThreads) {
+      const int j = idx / DK, c = idx % DK;
+      sKdT[c * LDT + j] = to<T>(f32(sK[j * LDQ + c]) * __expf(gC - sGam[j]));
+    }
+    // U = Ut - W S_r^T for rows of stripe w
+    const T* Wc = Wg + ((size_t)bh * N + ci) * C * DK;
+    const float* Uc = a.Ut + ((size_t)bh * N + ci) * C * a.dv;
+#pragma unroll
+    for (int tn = 0; tn < BV / 16; ++tn) {
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int k0 = 0; k0 < DK; k0 += 32)
+        mma(acc, ld_frag_global(Wc + (size_t)16 * w * DK + k0, (size_t)DK), ld_frag(sS + 16 * tn * LDQ + k0, LDQ));
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = 16 * w + 4 * g4 + r, vv = 16 * tn + c16;
+        sUT[vv * LDT + i] = to<T>(Uc[(size_t)i * a.dv + v0 + vv] - acc[r]);
+      }
+    }
+    // intra-chunk block (q_i . k_j) e^{gamma_i - gamma_j}, j <= i
+#pragma unroll
+    for (int J = 0; J < 4; ++J) {
+      f32x4 acc = zero4();
+      if (J <= w) tile_mma<T, DK>(acc, sQ + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = 16 * w + 4 * g4 + r, j = 16 * J + c16;
+        sA[i * LDT + j] = to<T>((J <= w && j <= i) ? acc[r] * __expf(sGam[i] - sGam[j]) : 0.f);
+      }
+    }
+    __syncthreads();
+
+    // o = e^{gamma} (Q S_r^T) + A U
+#pragma unroll
+    for (int tn = 0; tn < BV / 16; ++tn) {
+      f32x4 a1 = zero4(), a2 = zero4();
+      tile_mma<T, DK>(a1, sQ + 16 * w * LDQ, LDQ, sS + 16 * tn * LDQ, LDQ);
+      tile_mma<T, C>(a2, sA + 16 * w * LDT, LDT, sUT + 16 * tn * LDT, LDT);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = 16 * w + 4 * g4 + r;
+        if (i < nrow)
+          o[tok_off(b, r0 + i, h, a.T, a.H, a.dv) + v0 + 16 * tn + c16] =
+              to<T>(a.scale * (__expf(sGam[i]) * a1[r] + a2[r]));
+      }
+    }
+    // S_{r+1} = e^{gamma_C} S_r + U^T Kd
+    const float eC = __expf(gC);
+#pragma unroll
+    for (int u = 0; u < NPW; ++u) {
+      const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
+      f32x4 d = zero4();
+      tile_mma<T, C>(d, sUT + 16 * tv * LDT, LDT, sKdT + 16 * tc * LDT, LDT);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) S[u][r] = eC * S[u][r] + d[r];
+    }
+  }
+
+  if (a.ST) {
+#pragma unroll
+    for (int u = 0; u < NPW; ++u) {
+      const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int vv = v0 + 16 * tv + 4 * g4 + r, c = 16 * tc + c16;
+        a.ST[((size_t)bh * a.dv + vv) * DK + c] = S[u][r];
+      }
+    }
+  }
+}
+
+namespace {
+template <typename T, int DK>
+hipError_t run_wy(const WyArgs& a, hipStream_t st) {
+  const int N = (a.T + kChunk - 1) / kChunk;
+  const int nblk = a.B * a.H * N;
+  if (nblk == 0) return hipSuccess;
+  hipLaunchKernelGGL((gdn_wy_kernel<T, DK>), dim3(nblk), dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
+template <typename T, int DK, int BV>
+hipError_t run_gdn(const GdnArgs& a, hipStream_t st) {
+  const int nblk = a.B * a.H * (a.dv / BV);
+  if (nblk == 0) return hipSuccess;
+  hipLaunchKernelGGL((gdn_fwd_kernel<T, DK, BV>), dim3(nblk), dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
+}  // namespace
+
+bool gdn_supported(int dk, int dv, bool is_bf16) {
+  const bool dv_ok = dv == 64 || dv == 128 || dv == 256 || dv == 512;
+  if (is_bf16) return dv_ok && (dk == 64 || dk == 128 || dk == 256);
+  return dv_ok && (dk == 64 || dk == 128);
+}
+
+hipError_t launch_gdn_wy(const WyArgs& a, bool is_bf16, hipStream_t st) {
+  if (is_bf16) {
+    switch (a.dk) {
+      case 64: return run_wy<bf16_t, 64>(a, st);
+      case 128: return run_wy<bf16_t, 128>(a, st);
+      case 256: return run_wy<bf16_t, 256>(a, st);
+    }
+  } else {
+    switch (a.dk) {
+      case 64: return run_wy<float, 64>(a, st);
+      case 128: return run_wy<float, 128>(a, st);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_gdn_fwd(const GdnArgs& a, bool is_bf16, hipStream_t st) {
+  if (is_bf16) {
+    switch (a.dk) {
+      case 64: return run_gdn<bf16_t, 64, 64>(a, st);
+      case 128: return run_gdn<bf16_t, 128, 64>(a, st);
+      case 256: return run_gdn<bf16_t, 256, 32>(a, st);
+    }
+  } else {
+    switch (a.dk) {
+      case 64: return run_gdn<float, 64, 64>(a, st);
+      case 128: return run_gdn<float, 128, 32>(a, st);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace ccq

@@ -1,0 +1,100 @@
+"""Host-side checks of the C ABI: the library loads, exports every function that
+include/ccq.h declares, and rejects bad arguments before launching anything
+(these paths touch no GPU, so they run on the CPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_01294_amd import ccq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    txt = open(os.path.join(ROOT, "include", "ccq.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(ccq_[a-z_]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_function():
+    L = ccq.lib()
+    names = declared_functions()
+    assert set(names) == set(ccq.EXPORTS)
+    for n in names:
+        assert getattr(L, n) is not None
+
+
+def test_version_and_status_strings():
+    assert "gfx950" in ccq.ccq_version()
+    for code in range(5):
+        assert ccq.ccq_status_string(code)
+    assert ccq.ccq_status_string(0) == "ok"
+
+
+def shape(**kw):
+    base = dict(B=2, T=100, H=3, dk=128, dv=256, io_dtype=__import__("torch").bfloat16)
+    base.update(kw)
+    return ccq.make_shape(**base)
+
+
+def test_workspace_size():
+    s = shape()
+    ws = ccq.ccq_workspace_size(s, ccq.CCQ_GLA)
+    assert ws >= 2 * 100 * 3 * 128 * 2
+    wg = ccq.ccq_workspace_size(s, ccq.CCQ_GDN)
+    assert wg > ws
+    assert ccq.ccq_workspace_size(shape(dk=96), ccq.CCQ_GLA) == 0
+    assert ccq.ccq_workspace_size(shape(chunk=32), ccq.CCQ_GLA) == 0
+
+
+FAKE = 1 << 20  # an aligned address that is never dereferenced (validation fails first)
+
+
+def call_gla(s, ws_bytes=1 << 30, ptr=FAKE, lam_ptr=FAKE, ws_ptr=FAKE):
+    P = ctypes.c_void_p
+    return ccq.lib().ccq_gla_fwd(ctypes.byref(s) if s is not None else None, P(ptr), P(ptr),
+                                 P(ptr), P(ptr), P(lam_ptr), None, None, None, P(ptr), None, None,
+                                 None, None, P(ws_ptr), ws_bytes, None)
+
+
+def test_validation_errors_are_returned_before_launch():
+    assert call_gla(None) == 1                            # no shape
+    assert call_gla(shape(B=-1)) == 1                     # negative size
+    assert call_gla(shape(dk=96)) == 2                    # unsupported head size
+    assert call_gla(shape(dv=100)) == 2
+    assert call_gla(shape(chunk=32)) == 2                 # unsupported chunk
+    assert call_gla(shape(), lam_ptr=0) == 1              # missing tensor
+    assert call_gla(shape(), lam_ptr=FAKE + 4) == 1       # misaligned tensor
+    assert call_gla(shape(), ws_bytes=16) == 3            # workspace too small
+    assert call_gla(shape(), ws_ptr=0) == 3               # no workspace
+    s = shape()
+    s.centered = 7
+    assert call_gla(s) == 1
+    s = shape()
+    s.io_dtype = 9
+    assert call_gla(s) == 1
+    s = shape(io_dtype=__import__("torch").float32, dk=256)
+    assert call_gla(s) == 2                               # fp32 path has dk <= 128
+
+
+def test_empty_batch_is_a_no_op():
+    assert call_gla(shape(B=0), ptr=0, lam_ptr=0, ws_ptr=0) == 0
+    assert call_gla(shape(H=0), ptr=0, lam_ptr=0, ws_ptr=0) == 0
+
+
+def test_gdn_requires_beta():
+    P = ctypes.c_void_p
+    s = shape(dk=256)
+    rc = ccq.lib().ccq_gdn_fwd(ctypes.byref(s), P(FAKE), P(FAKE), P(FAKE), P(FAKE), None,
+                               P(FAKE), None, None, None, P(FAKE), None, None, None, None,
+                               P(FAKE), 1 << 30, None)
+    assert rc == 1
+
+
+def test_binding_rejects_wrong_dtype_before_calling():
+    import torch
+    q = torch.zeros(1, 4, 1, 64)
+    with pytest.raises(TypeError):
+        ccq.ccq_gla_fwd(q, q, q, q, torch.zeros(1, 4, 1, dtype=torch.float64))
