@@ -1,0 +1,301 @@
+#!/usr/bin/env python3
+"""Benchmark of the CCQ chunkwise forward on one MI355X.
+
+One step = one CCQ-GLA forward on the ~500M-layer shape (B=8, T=2048, H=4,
+dk=128, dv=256) plus one CCQ-Gated-DeltaNet forward on the ~1.3B-layer shape
+(B=4, T=4096, H=8, dk=dv=256), bf16 io, fp32 states, chunk 64, inputs resident
+in HBM.  `value` is the tokens of both calls divided by the mean step time.
+The line also carries the per-kernel HIP-event timings, the roofline of the
+dominant kernel, per-workload figures (including T=20480) and the fp64 CPU
+oracle timed on a bounded sample of the same inputs.
+
+    python bench.py [--gpus 1] [--steps 40] [--warmup 5]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "CCQ chunkwise fwd tokens/s per GPU (GLA & GDN, T=4K); % of MFMA peak"
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3
+CHUNK = 64
+
+
+def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
+    """Algorithmic (bytes, flops) of one launch of `kernel` on workload w: every
+    input read once, every output written once; products counted at 2 flops per
+    multiply-add, the C x C chunk blocks counted dense."""
+    BH, ntok = w.B * w.H, w.B * w.T * w.H
+    dk, dv, C = w.dk, w.dv, CHUNK
+    if kernel == "clean":
+        by = ntok * (3 * dk * io_bytes + 4) + BH * (dk * dk + dk) * 4
+        fl = ntok * (4 * dk * dk + 4 * C * dk)
+    elif kernel == "gla_fwd":
+        by = ntok * (2 * dk * io_bytes + dk * gate_bytes + 2 * dv * io_bytes) + BH * dv * dk * 4
+        fl = ntok * (2 * C * (dk + dv) + 4 * dk * dv)
+    elif kernel == "gdn_wy":
+        by = ntok * (2 * dk * io_bytes + dv * io_bytes + dv * 4 + 8)
+        fl = ntok * (2 * C * dk + C * (dk + dv))
+    elif kernel == "gdn_fwd":
+        by = ntok * (3 * dk * io_bytes + dv * 4 + dv * io_bytes + 4) + BH * dv * dk * 4
+        fl = ntok * (6 * dk * dv + 2 * C * (dk + dv))
+    else:
+        raise KeyError(kernel)
+    return by, fl
+
+
+KERNELS = {0: ["clean", "gla_fwd"], 1: ["clean", "gdn_wy", "gdn_fwd"]}
+KERNEL_SYMBOL = {"clean": "clean_kernel", "gla_fwd": "gla_fwd_kernel", "gdn_wy": "gdn_wy_kernel",
+                 "gdn_fwd": "gdn_fwd_kernel"}
+KERNEL_SOURCE = {"clean": "ccq_clean.hip", "gla_fwd": "ccq_gla.hip", "gdn_wy": "ccq_gdn.hip",
+                 "gdn_fwd": "ccq_gdn.hip"}
+
+
+def source_sha(kernel: str) -> str:
+    p = os.path.join(ROOT, "paper_2606_01294_amd", "csrc", KERNEL_SOURCE[kernel])
+    h = hashlib.sha256()
+    for f in (p, os.path.join(ROOT, "paper_2606_01294_amd", "csrc", "ccq_device.h")):
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter runs, or None when the
+    kernel's source changed since they were taken."""
+    p = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        rec = json.load(open(p)).get("%s@%s" % (kernel, workload))
+    except (ValueError, OSError):
+        return None
+    if not rec or rec.get("source_sha") != source_sha(kernel):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+class Call:
+    """One pre-allocated CCQ forward call on a workload (inputs resident on the GPU)."""
+
+    def __init__(self, w, torch, ccq, inputs):
+        self.w = w
+        d = inputs.workload_inputs(w)
+        self.cpu = d
+        self.d = inputs.to_device(d)
+        dev = self.d["q"].device
+        B, T, H, dk, dv = w.B, w.T, w.H, w.dk, w.dv
+        self.out = {"o": torch.empty((B, T, H, dv), dtype=w.dtype, device=dev),
+                    "ST": torch.empty((B, H, dv, dk), dtype=torch.float32, device=dev),
+                    "CT": torch.empty((B, H, dk, dk), dtype=torch.float32, device=dev),
+                    "muT": torch.empty((B, H, dk), dtype=torch.float32, device=dev)}
+        shape = ccq.make_shape(B, T, H, dk, dv, w.dtype, w.dtype)
+        self.ws = torch.empty(max(1, ccq.ccq_workspace_size(shape, w.backbone)), dtype=torch.uint8,
+                              device=dev)
+        self.ccq = ccq
+
+    def __call__(self):
+        d = self.d
+        if self.w.backbone == 0:
+            self.ccq.ccq_gla_fwd(d["q"], d["k"], d["v"], d["g"], d["lam"], out=self.out,
+                                 workspace=self.ws)
+        else:
+            self.ccq.ccq_gdn_fwd(d["q"], d["k"], d["v"], d["logalpha"], d["beta"], d["lam"],
+                                 out=self.out, workspace=self.ws)
+
+
+def time_calls(torch, ccq, calls, steps, warmup):
+    """Warm up, then time exactly `steps` steps (each step = every call once) between two
+    synchronisations; per-kernel durations come from HIP events the library records on
+    its stream around each of its launches."""
+    for _ in range(warmup):
+        for c in calls:
+            c()
+    torch.cuda.synchronize()
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2 * len(KERNELS[c.w.backbone]))]
+           for c in calls] for _ in range(steps)]
+    for step_ev in ev:
+        for evs in step_ev:
+            for e in evs:
+                e.record()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        for j, c in enumerate(calls):
+            ccq.ccq_trace_events(ev[i][j])
+            c()
+    ccq.ccq_trace_events(None)
+    end.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(end) / steps
+    per_kernel = []
+    for j, c in enumerate(calls):
+        names = KERNELS[c.w.backbone]
+        for kidx, name in enumerate(names):
+            ts = [ev[i][j][2 * kidx].elapsed_time(ev[i][j][2 * kidx + 1]) for i in range(steps)]
+            per_kernel.append({"workload": c.w.name, "kernel": name,
+                               "symbol": KERNEL_SYMBOL[name],
+                               "ms_mean": sum(ts) / len(ts),
+                               "ms_std": (sum((t - sum(ts) / len(ts)) ** 2 for t in ts) /
+                                          max(1, len(ts) - 1)) ** 0.5})
+    return ms_step, per_kernel
+
+
+def roofline(entry, w):
+    by, fl = kernel_cost(entry["kernel"], w)
+    sec = entry["ms_mean"] * 1e-3
+    intensity = fl / by
+    ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if intensity < ridge:
+        ach = by / sec / 1e9
+        r = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+             "frac": round(ach / PEAK_HBM_GBS, 4)}
+    else:
+        ach = fl / sec / 1e12
+        r = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
+             "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4)}
+    r["traffic"] = measured_traffic(entry["kernel"], w.name)
+    r["kernel"] = entry["symbol"]
+    r["workload"] = w.name
+    r["algorithmic_bytes"] = by
+    r["algorithmic_flops"] = fl
+    r["ms_per_launch"] = round(entry["ms_mean"], 5)
+    return r
+
+
+def cpu_baseline(calls):
+    """The fp64 oracle on the host cores, on the first n (batch, head) sequences of each
+    workload (n = min(oracle threads, B*H)), scaled to the whole step by the number of
+    sequence waves."""
+    from oracle import ccq_oracle as O
+    import numpy as np
+
+    thr = O.threads()
+    total = 0.0
+    parts = []
+    used = 1
+    for c in calls:
+        w = c.w
+        nseq = w.B * w.H
+        n = min(thr, nseq)
+        used = max(used, n)
+        pairs = [(b, h) for b in range(w.B) for h in range(w.H)][:n]
+
+        def pick(t):
+            a = t.double().numpy()
+            return np.ascontiguousarray(np.stack([a[b, :, h] for b, h in pairs])[:, :, None])
+
+        d = {k: pick(v) for k, v in c.cpu.items()}
+        t0 = time.perf_counter()
+        if w.backbone == 0:
+            O.fwd(d["q"], d["k"], d["v"], d["g"], d["lam"], backbone=O.GLA)
+        else:
+            O.fwd(d["q"], d["k"], d["v"], d["logalpha"], d["lam"], beta=d["beta"], backbone=O.GDN)
+        dt = time.perf_counter() - t0
+        total += dt * math.ceil(nseq / n)
+        parts.append("%s: %d of %d sequences in %.2f s" % (w.name, n, nseq, dt))
+    tokens = sum(c.w.tokens for c in calls)
+    return {"value": round(tokens / total, 1), "unit": "tokens/s", "cores": used,
+            "kind": "oracle",
+            "sample": "; ".join(parts) + "; whole-step time = sample time x ceil(B*H / n)"}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=40)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true", help="skip the per-workload figures")
+    args = ap.parse_args(argv)
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the CCQ hot path here is single-GPU "
+              "(heads are independent; multi-GPU sharding is a design note, not built). "
+              "Run with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2606_01294_amd import ccq, inputs
+
+    ccq.lib()  # fails loudly when libccq.so is missing
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    W = inputs.WORKLOADS
+    step_calls = [Call(W["gla_500m_t2k"], torch, ccq, inputs), Call(W["gdn_1p3b_t4k"], torch, ccq, inputs)]
+    ms_step, per_kernel = time_calls(torch, ccq, step_calls, args.steps, args.warmup)
+    tokens = sum(c.w.tokens for c in step_calls)
+    value = tokens / (ms_step * 1e-3)
+
+    wl = {c.w.name: c.w for c in step_calls}
+    dominant = max(per_kernel, key=lambda e: e["ms_mean"])
+    roof = roofline(dominant, wl[dominant["workload"]])
+    step_flops = sum(kernel_cost(e["kernel"], wl[e["workload"]])[1] for e in per_kernel)
+    step_bytes = sum(kernel_cost(e["kernel"], wl[e["workload"]])[0] for e in per_kernel)
+    kernels = []
+    for e in per_kernel:
+        by, fl = kernel_cost(e["kernel"], wl[e["workload"]])
+        kernels.append({"workload": e["workload"], "kernel": e["symbol"],
+                        "ms": round(e["ms_mean"], 5), "ms_std": round(e["ms_std"], 5),
+                        "GB_s": round(by / (e["ms_mean"] * 1e-3) / 1e9, 1),
+                        "TFLOP_s": round(fl / (e["ms_mean"] * 1e-3) / 1e12, 2)})
+
+    extra = {}
+    if not args.no_extra:
+        for name in ("gla_500m_t2k", "gdn_1p3b_t4k", "gla_500m_t20k", "gdn_1p3b_t20k"):
+            c = step_calls[0] if name == "gla_500m_t2k" else (
+                step_calls[1] if name == "gdn_1p3b_t4k" else Call(W[name], torch, ccq, inputs))
+            ms, pk = time_calls(torch, ccq, [c], max(5, args.steps // 2), 3)
+            fl = sum(kernel_cost(e["kernel"], c.w)[1] for e in pk)
+            extra[name] = {"tokens_per_s": round(c.w.tokens / (ms * 1e-3), 1), "ms": round(ms, 4),
+                           "mfma_frac": round(fl / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                           "kernels_ms": {e["symbol"]: round(e["ms_mean"], 5) for e in pk}}
+            if c not in step_calls:
+                del c
+                torch.cuda.empty_cache()
+        extra["gla_train_t4k"] = "fwd+bwd not available in this build"
+
+    cpu = None if args.no_cpu_baseline else cpu_baseline(step_calls)
+
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "ccq_fwd gla_500m_t2k+gdn_1p3b_t4k",
+                   "gla": "B=8 T=2048 H=4 dk=128 dv=256 chunk=64 bf16 io, fp32 states",
+                   "gdn": "B=4 T=4096 H=8 dk=256 dv=256 chunk=64 bf16 io, fp32 states",
+                   "tokens_per_step": tokens},
+        "mfma_frac": round(step_flops / (ms_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "hbm_frac": round(step_bytes / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "roofline": roof,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+        "extra": extra,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -58,7 +58,8 @@ typedef enum { CCQ_GLA = 0, CCQ_GDN = 1 } ccq_backbone;
 
 typedef struct {
   int32_t B, T, H;      /* batch, tokens, heads (T may be any value >= 0) */
-  int32_t dk, dv;       /* key / value head size: dk in {64,128,256}, dv in {64,128,256,512} */
+  int32_t dk, dv;       /* key / value head size: dv in {64,128,256,512}; dk in {64,128}
+                         * (GLA, or fp32 io), {64,128,256} (bf16 Gated DeltaNet) */
   int32_t chunk;        /* chunk length C of Alg. 1; must be 64 */
   ccq_dtype io_dtype;   /* dtype of q, k, v, o (and of dq, dk, dv, dO in the backward) */
   ccq_dtype gate_dtype; /* dtype of the GLA gate g (and of dg); ignored for GDN */

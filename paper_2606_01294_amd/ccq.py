@@ -23,7 +23,7 @@ CCQ_GLA, CCQ_GDN = 0, 1
 _STATUS = {0: "CCQ_OK", 1: "CCQ_ERR_INVALID_ARG", 2: "CCQ_ERR_UNSUPPORTED",
            3: "CCQ_ERR_WORKSPACE", 4: "CCQ_ERR_HIP"}
 EXPORTS = ("ccq_workspace_size", "ccq_gla_fwd", "ccq_gdn_fwd", "ccq_fwd_bwd",
-           "ccq_status_string", "ccq_version")
+           "ccq_trace_events", "ccq_status_string", "ccq_version")
 
 
 class CcqError(RuntimeError):
@@ -64,6 +64,8 @@ def lib() -> ctypes.CDLL:
             L.ccq_gdn_fwd.restype = ctypes.c_int
             L.ccq_fwd_bwd.argtypes = [SP, ctypes.c_int] + [P] * 17 + [S, P]
             L.ccq_fwd_bwd.restype = ctypes.c_int
+            L.ccq_trace_events.argtypes = [P, ctypes.c_int]
+            L.ccq_trace_events.restype = ctypes.c_int
             L.ccq_status_string.argtypes = [ctypes.c_int]
             L.ccq_status_string.restype = ctypes.c_char_p
             L.ccq_version.argtypes = []
@@ -78,6 +80,22 @@ def ccq_status_string(code: int) -> str:
 
 def ccq_version() -> str:
     return lib().ccq_version().decode()
+
+
+def ccq_trace_events(events) -> None:
+    """Per-kernel timing hook: `events` is a list of torch.cuda.Event(enable_timing=True)
+    (2 per kernel: before, after) or None to switch tracing off.  The caller keeps the
+    list alive while tracing is on."""
+    if not events:
+        rc = lib().ccq_trace_events(None, 0)
+    else:
+        for e in events:
+            e.record() if e.cuda_event == 0 else None  # make sure the event exists
+        arr = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
+        ccq_trace_events._keep = arr
+        rc = lib().ccq_trace_events(ctypes.cast(arr, ctypes.c_void_p), len(events))
+    if rc != 0:
+        raise CcqError("ccq_trace_events", rc)
 
 
 def _dt(t: torch.dtype) -> int:

@@ -9,6 +9,28 @@
 
 namespace {
 
+// Per-host-thread kernel timing hook (ccq_trace_events).
+struct Trace {
+  hipEvent_t* ev = nullptr;
+  int n = 0;
+  int next = 0;
+};
+thread_local Trace g_trace;
+
+void trace_begin_call() { g_trace.next = 0; }
+
+// Runs one launcher between the trace events of its slot, if tracing is on.
+template <typename F>
+hipError_t traced(hipStream_t st, F&& launch) {
+  const int i = g_trace.next++;
+  const bool on = g_trace.ev && 2 * i + 1 < g_trace.n;
+  if (on && hipEventRecord(g_trace.ev[2 * i], st) != hipSuccess) return hipErrorUnknown;
+  hipError_t e = launch();
+  if (e == hipSuccess && on && hipEventRecord(g_trace.ev[2 * i + 1], st) != hipSuccess)
+    return hipErrorUnknown;
+  return e;
+}
+
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -94,22 +116,25 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   char* ws = static_cast<char*>(workspace);
   const bool bf = s->io_dtype == CCQ_BF16;
   void* qclean = ws + L.qclean;
+  trace_begin_call();
 
   ccq::CleanArgs ca{q, k, lam, C0, mu0, qclean, q_clean_dbg, CT, muT,
                     s->B, s->T, s->H, s->dk, s->centered, s->t0};
-  if (ccq::launch_clean(ca, bf, st) != hipSuccess) return CCQ_ERR_HIP;
+  if (traced(st, [&] { return ccq::launch_clean(ca, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
 
   if (bb == CCQ_GLA) {
     ccq::GlaArgs ga{qclean, k, v, g_or_la, S0, o, ST, s->B, s->T, s->H, s->dk, s->dv, s->scale};
-    if (ccq::launch_gla_fwd(ga, bf, s->gate_dtype == CCQ_BF16, st) != hipSuccess) return CCQ_ERR_HIP;
+    const bool gbf = s->gate_dtype == CCQ_BF16;
+    if (traced(st, [&] { return ccq::launch_gla_fwd(ga, bf, gbf, st); }) != hipSuccess)
+      return CCQ_ERR_HIP;
   } else {
     const float* la = static_cast<const float*>(g_or_la);
     ccq::WyArgs wa{k, v, la, beta, ws + L.W, reinterpret_cast<float*>(ws + L.Ut),
                    s->B, s->T, s->H, s->dk, s->dv};
-    if (ccq::launch_gdn_wy(wa, bf, st) != hipSuccess) return CCQ_ERR_HIP;
+    if (traced(st, [&] { return ccq::launch_gdn_wy(wa, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
     ccq::GdnArgs da{qclean, k, la, ws + L.W, reinterpret_cast<const float*>(ws + L.Ut), S0, o, ST,
                     s->B, s->T, s->H, s->dk, s->dv, s->scale};
-    if (ccq::launch_gdn_fwd(da, bf, st) != hipSuccess) return CCQ_ERR_HIP;
+    if (traced(st, [&] { return ccq::launch_gdn_fwd(da, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   }
   return CCQ_OK;
 }
@@ -152,6 +177,19 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
   ccq_status rc = check_shape(s, bb);
   if (rc != CCQ_OK) return rc;
   return CCQ_ERR_UNSUPPORTED;
+}
+
+ccq_status ccq_trace_events(void* const* events, int n_events) {
+  if (events == nullptr || n_events <= 0) {
+    g_trace = Trace{};
+    return CCQ_OK;
+  }
+  for (int i = 0; i < n_events; ++i)
+    if (!events[i]) return CCQ_ERR_INVALID_ARG;
+  g_trace.ev = reinterpret_cast<hipEvent_t*>(const_cast<void**>(events));
+  g_trace.n = n_events;
+  g_trace.next = 0;
+  return CCQ_OK;
 }
 
 const char* ccq_status_string(ccq_status st) {

@@ -32,6 +32,8 @@ __global__ __launch_bounds__(kThreads, 1) void clean_kernel(const CleanArgs a) {
   constexpr int NTILE_COL = DK / 16;
   constexpr int NPW = CT * DK / (16 * 16 * 4);  // S^K tiles per wave
   static_assert(NPW >= 1, "tile split");
+  constexpr int VE = 8;
+  typedef T vec_t __attribute__((ext_vector_type(VE)));
 
   __shared__ __align__(16) T sQ[C * LDQ];
   __shared__ __align__(16) T sK[C * LDQ];
@@ -40,7 +42,7 @@ __global__ __launch_bounds__(kThreads, 1) void clean_kernel(const CleanArgs a) {
   __shared__ __align__(16) T sAl[kSplit ? C * LDA : 8];
   __shared__ __align__(16) T sSh[CT * LDQ];
   __shared__ __align__(16) T sSl[kSplit ? CT * LDQ : 8];
-  __shared__ float sM[DK];
+  __shared__ __align__(16) float sM[DK];
   __shared__ float sMq[C];
   __shared__ float sLam[C];
 
@@ -90,19 +92,37 @@ __global__ __launch_bounds__(kThreads, 1) void clean_kernel(const CleanArgs a) {
   };
   store_state_tile();
 
+  // chunk 0 in flight
+  ChunkTile<T, DK> rq, rk;
+  RowScalar rlam;
+  auto prefetch = [&](int r0) {
+    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+    rq.load(q + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+    rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+    if (tid < C) rlam.load(a.lam + ((size_t)b * a.T + r0) * a.H + h, (size_t)a.H, tid, nrow);
+  };
+  if (a.T > 0) prefetch(0);
+
   for (int r0 = 0; r0 < a.T; r0 += C) {
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
     __syncthreads();  // previous chunk's readers are done with LDS
-    load_chunk_rows<T, DK>(sQ, LDQ, nullptr, 0, q + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-    load_chunk_rows<T, DK>(sK, LDQ, sKT, LDT, k + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-    if (tid < C) sLam[tid] = tid < nrow ? a.lam[(((size_t)b * a.T + r0 + tid) * a.H + h)] : 0.f;
+    rq.store(sQ, LDQ);
+    rk.store(sK, LDQ);
+    rk.store_t(sKT, LDT);
+    if (tid < C) sLam[tid] = rlam.get();
+    if (r0 + C < a.T) prefetch(r0 + C);  // next chunk loads overlap this chunk's math
     __syncthreads();
 
-    // M_r . q_i : four threads per row
+    // M_r . q_i : four threads per row, 16-byte reads
     {
       const int row = tid >> 2, part = tid & 3;
       float s = 0.f;
-      for (int c = part * (DK / 4); c < (part + 1) * (DK / 4); ++c) s += f32(sQ[row * LDQ + c]) * sM[c];
+#pragma unroll
+      for (int c0 = part * (DK / 4); c0 < (part + 1) * (DK / 4); c0 += VE) {
+        const vec_t qv = *reinterpret_cast<const vec_t*>(sQ + row * LDQ + c0);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) s += f32(qv[e]) * sM[c0 + e];
+      }
       s += __shfl_xor(s, 1);
       s += __shfl_xor(s, 2);
       if (part == 0) sMq[row] = s;
@@ -193,7 +213,12 @@ __global__ __launch_bounds__(kThreads, 1) void clean_kernel(const CleanArgs a) {
     store_state_tile();
     for (int c = tid; c < DK; c += kThreads) {
       float s = 0.f;
-      for (int j = 0; j < C; ++j) s += f32(sK[j * LDQ + c]);
+#pragma unroll
+      for (int j0 = 0; j0 < C; j0 += VE) {
+        const vec_t kv = *reinterpret_cast<const vec_t*>(sKT + c * LDT + j0);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) s += f32(kv[e]);
+      }
       sM[c] += s;
     }
   }
@@ -239,7 +264,7 @@ hipError_t launch_clean(const CleanArgs& a, bool is_bf16, hipStream_t st) {
     switch (a.dk) {
       case 64: return run_clean<bf16_t, 64, 16>(a, st);
       case 128: return run_clean<bf16_t, 128, 32>(a, st);
-      case 256: return run_clean<bf16_t, 256, 16>(a, st);
+      case 256: return run_clean<bf16_t, 256, 32>(a, st);
     }
   } else {
     switch (a.dk) {

@@ -123,32 +123,75 @@ __device__ __forceinline__ size_t tok_off(int b, int t, int h, int T, int H, int
   return (((size_t)b * T + t) * H + h) * (size_t)D;
 }
 
-// Copy rows [0, n) of a chunk (row pitch `gstride` elements in global memory)
-// into LDS row-major (ld elements per row), zero-filling rows n..63; when
-// `dstT` is given, also store the transpose (D rows of ldT, row-contiguous in
-// the chunk index).  D must be a multiple of 8 / (16 / sizeof(T)).
+// One 64-row chunk of a [*, D] token tensor held in registers as vectors of 8
+// elements (16 bytes for bf16, 32 for fp32), so tiles of either dtype share
+// one lane -> element mapping: lane l of every wave owns row l, wave w owns
+// column groups w, w+4, ...  With the row in the lane index, a transposed LDS
+// store (D rows, chunk index contiguous) writes 64 consecutive elements per
+// instruction and is free of bank conflicts.  Rows >= n are zero.  Loads are
+// branch-free (clamped row, then select), so a whole tile is in flight at
+// once and can be issued a chunk ahead of its use.
 template <typename T, int D>
-__device__ __forceinline__ void load_chunk_rows(T* dst, int ld, T* dstT, int ldT, const T* src,
-                                                size_t gstride, int n) {
-  constexpr int VE = 16 / (int)sizeof(T);  // elements per 16-byte vector
-  constexpr int NV = kChunk * D / VE;
+struct ChunkTile {
+  static constexpr int VE = 8;
+  static constexpr int NV = kChunk * D / VE / kThreads;
+  static_assert(NV >= 1 && kChunk * D % (VE * kThreads) == 0, "tile split");
   typedef T vec_t __attribute__((ext_vector_type(VE)));
-  for (int idx = threadIdx.x; idx < NV; idx += kThreads) {
-    const int row = idx / (D / VE);
-    const int c0 = (idx % (D / VE)) * VE;
-    vec_t val;
-    if (row < n) {
-      val = *reinterpret_cast<const vec_t*>(src + (size_t)row * gstride + c0);
-    } else {
+  vec_t v[NV];
+  bool ok;  // this lane's row lies inside the sequence
+
+  __device__ __forceinline__ static int row() { return threadIdx.x & 63; }
+  __device__ __forceinline__ static int col(int u) { return ((threadIdx.x >> 6) + 4 * u) * VE; }
+
+  // Issue the loads of rows [0, n) of the chunk at src (row pitch gstride
+  // elements), n >= 1.  Rows >= n read row n-1 and are zeroed at use, so
+  // nothing here waits for the data.
+  __device__ __forceinline__ void load(const T* src, size_t gstride, int n) {
+    const int r = row();
+    ok = r < n;
+    const T* p = src + (size_t)(ok ? r : n - 1) * gstride;
 #pragma unroll
-      for (int e = 0; e < VE; ++e) val[e] = static_cast<T>(0.f);
-    }
-    *reinterpret_cast<vec_t*>(dst + row * ld + c0) = val;
-    if (dstT) {
+    for (int u = 0; u < NV; ++u) v[u] = *reinterpret_cast<const vec_t*>(p + col(u));
+  }
+  __device__ __forceinline__ vec_t get(int u) const {
+    vec_t z;
 #pragma unroll
-      for (int e = 0; e < VE; ++e) dstT[(c0 + e) * ldT + row] = val[e];
+    for (int e = 0; e < VE; ++e) z[e] = static_cast<T>(0.f);
+    return ok ? v[u] : z;
+  }
+  __device__ __forceinline__ void store(T* dst, int ld) const {
+#pragma unroll
+    for (int u = 0; u < NV; ++u) *reinterpret_cast<vec_t*>(dst + row() * ld + col(u)) = get(u);
+  }
+  template <typename U>
+  __device__ __forceinline__ void store_t(U* dstT, int ldT) const {
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      const vec_t x = get(u);
+#pragma unroll
+      for (int e = 0; e < VE; ++e) dstT[(col(u) + e) * ldT + row()] = static_cast<U>(static_cast<float>(x[e]));
     }
   }
-}
+  // fp32 copy, row-major; an odd pitch keeps it conflict-free for lane = row
+  __device__ __forceinline__ void store_f32(float* dst, int ld) const {
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      const vec_t x = get(u);
+#pragma unroll
+      for (int e = 0; e < VE; ++e) dst[row() * ld + col(u) + e] = static_cast<float>(x[e]);
+    }
+  }
+};
+
+// Scalar per-token value prefetched by lane `row` (clamped address, zeroed at use).
+struct RowScalar {
+  float x;
+  bool ok;
+  __device__ __forceinline__ void load(const float* p, size_t stride, int row, int n) {
+    ok = row < n;
+    x = p[(size_t)(ok ? row : n - 1) * stride];
+  }
+  __device__ __forceinline__ float get() const { return ok ? x : 0.f; }
+};
 
 }  // namespace ccq

@@ -42,7 +42,11 @@ __global__ __launch_bounds__(kThreads) void gdn_wy_kernel(const WyArgs a) {
   const T* k = static_cast<const T*>(a.k);
   const T* v = static_cast<const T*>(a.v);
 
-  load_chunk_rows<T, DK>(sK, LDQ, nullptr, 0, k + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+  {
+    ChunkTile<T, DK> rk;
+    rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+    rk.store(sK, LDQ);
+  }
   if (tid < C) {
     const size_t ti = ((size_t)b * a.T + r0 + tid) * a.H + h;
     float x = tid < nrow ? a.logalpha[ti] : 0.f;
@@ -108,6 +112,7 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
   constexpr int LDQ = DK + P, LDT = C + P;
   constexpr int NTC = DK / 16;
   constexpr int NPW = BV * DK / (16 * 16 * 4);
+  constexpr int NTN = BV / 16;
   static_assert(NPW >= 1, "tile split");
 
   __shared__ __align__(16) T sQ[C * LDQ];
@@ -130,6 +135,7 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
   const T* k = static_cast<const T*>(a.k);
   const T* Wg = static_cast<const T*>(a.W);
   T* o = static_cast<T*>(a.o);
+  const size_t gstride = (size_t)a.H * DK;
 
   f32x4 S[NPW];
 #pragma unroll
@@ -142,12 +148,42 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
     }
   }
 
+  // next chunk in flight: q, k tiles, log-decays (wave 0), and this wave's
+  // W fragments and Ut entries
+  ChunkTile<T, DK> rq, rk;
+  RowScalar rla;
+  Frag<T> rW[DK / 32];
+  float rU[NTN][4];
+  auto prefetch_qk = [&](int ci) {
+    const int r0 = ci * C;
+    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+    rq.load(qc + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+    rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+    if (tid < C) rla.load(a.logalpha + ((size_t)b * a.T + r0) * a.H + h, (size_t)a.H, tid, nrow);
+  };
+  auto prefetch_wu = [&](int ci) {
+    const T* Wc = Wg + ((size_t)bh * N + ci) * C * DK + (size_t)16 * w * DK;
+#pragma unroll
+    for (int kk = 0; kk < DK / 32; ++kk) rW[kk] = ld_frag_global(Wc + 32 * kk, (size_t)DK);
+    const float* Uc = a.Ut + ((size_t)bh * N + ci) * C * a.dv;
+#pragma unroll
+    for (int tn = 0; tn < NTN; ++tn)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) rU[tn][r] = Uc[(size_t)(16 * w + 4 * g4 + r) * a.dv + v0 + 16 * tn + c16];
+  };
+  if (N > 0) {
+    prefetch_qk(0);
+    prefetch_wu(0);
+  }
+
   for (int ci = 0; ci < N; ++ci) {
     const int r0 = ci * C;
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-    __syncthreads();
-    if (tid < C) {
-      float x = tid < nrow ? a.logalpha[((size_t)b * a.T + r0 + tid) * a.H + h] : 0.f;
+    __syncthreads();  // (A) previous chunk's LDS readers are done
+    rq.store(sQ, LDQ);
+    rk.store(sK, LDQ);
+    if (tid < C) {  // inclusive prefix of log alpha over the chunk (wave 0)
+      float x = rla.get();
 #pragma unroll
       for (int off = 1; off < 64; off <<= 1) {
         const float y = __shfl_up(x, off);
@@ -155,8 +191,6 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
       }
       sGam[tid] = x;
     }
-    load_chunk_rows<T, DK>(sQ, LDQ, nullptr, 0, qc + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
-    load_chunk_rows<T, DK>(sK, LDQ, nullptr, 0, k + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
     // entering state slice as the B^T operand [v][c]
 #pragma unroll
     for (int u = 0; u < NPW; ++u) {
@@ -164,28 +198,31 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) sS[(16 * tv + 4 * g4 + r) * LDQ + 16 * tc + c16] = to<T>(S[u][r]);
     }
-    __syncthreads();
+    __syncthreads();  // (B)
     const float gC = sGam[C - 1];
-    // K scaled by e^{gamma_C - gamma_j}, transposed for the state update
-    for (int idx = tid; idx < C * DK; idx += kThreads) {
-      const int j = idx / DK, c = idx % DK;
-      sKdT[c * LDT + j] = to<T>(f32(sK[j * LDQ + c]) * __expf(gC - sGam[j]));
-    }
-    // U = Ut - W S_r^T for rows of stripe w
-    const T* Wc = Wg + ((size_t)bh * N + ci) * C * DK;
-    const float* Uc = a.Ut + ((size_t)bh * N + ci) * C * a.dv;
+    // K scaled by e^{gamma_C - gamma_j}, transposed for the state update (lane = row j)
+    {
+      const int j = ChunkTile<T, DK>::row();
+      const float sc = __expf(gC - sGam[j]);
 #pragma unroll
-    for (int tn = 0; tn < BV / 16; ++tn) {
+      for (int u = 0; u < ChunkTile<T, DK>::NV; ++u)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sKdT[(ChunkTile<T, DK>::col(u) + e) * LDT + j] = to<T>(f32(rk.v[u][e]) * sc);
+    }
+    if (ci + 1 < N) prefetch_qk(ci + 1);
+    // U = Ut - W S_r^T for rows of stripe w
+#pragma unroll
+    for (int tn = 0; tn < NTN; ++tn) {
       f32x4 acc = zero4();
 #pragma unroll
-      for (int k0 = 0; k0 < DK; k0 += 32)
-        mma(acc, ld_frag_global(Wc + (size_t)16 * w * DK + k0, (size_t)DK), ld_frag(sS + 16 * tn * LDQ + k0, LDQ));
+      for (int kk = 0; kk < DK / 32; ++kk) mma(acc, rW[kk], ld_frag(sS + 16 * tn * LDQ + 32 * kk, LDQ));
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int i = 16 * w + 4 * g4 + r, vv = 16 * tn + c16;
-        sUT[vv * LDT + i] = to<T>(Uc[(size_t)i * a.dv + v0 + vv] - acc[r]);
+        sUT[vv * LDT + i] = to<T>(rU[tn][r] - acc[r]);
       }
     }
+    if (ci + 1 < N) prefetch_wu(ci + 1);
     // intra-chunk block (q_i . k_j) e^{gamma_i - gamma_j}, j <= i
 #pragma unroll
     for (int J = 0; J < 4; ++J) {
@@ -197,11 +234,11 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
         sA[i * LDT + j] = to<T>((J <= w && j <= i) ? acc[r] * __expf(sGam[i] - sGam[j]) : 0.f);
       }
     }
-    __syncthreads();
+    __syncthreads();  // (C)
 
     // o = e^{gamma} (Q S_r^T) + A U
 #pragma unroll
-    for (int tn = 0; tn < BV / 16; ++tn) {
+    for (int tn = 0; tn < NTN; ++tn) {
       f32x4 a1 = zero4(), a2 = zero4();
       tile_mma<T, DK>(a1, sQ + 16 * w * LDQ, LDQ, sS + 16 * tn * LDQ, LDQ);
       tile_mma<T, C>(a2, sA + 16 * w * LDT, LDT, sUT + 16 * tn * LDT, LDT);

@@ -25,19 +25,23 @@ template <typename T, typename TG, int DK, int BV>
 __global__ __launch_bounds__(kThreads, 1) void gla_fwd_kernel(const GlaArgs a) {
   constexpr int C = kChunk;
   constexpr int P = Pad<T>::value;
-  constexpr int LDQ = DK + P, LDT = C + P;
+  constexpr int LDQ = DK + P, LDT = C + P, LDG = DK + 1;
   constexpr int NTC = DK / 16;
   constexpr int NPW = BV * DK / (16 * 16 * 4);
   static_assert(NPW >= 1, "tile split");
-  constexpr int VE = 16 / (int)sizeof(T);
-  typedef T vec_t __attribute__((ext_vector_type(VE)));
+  static_assert(DK <= kThreads, "one thread per key channel in the scan");
 
   __shared__ __align__(16) T sQt[C * LDQ];
   __shared__ __align__(16) T sKt[C * LDQ];
   __shared__ __align__(16) T sKtT[DK * LDT];
   __shared__ __align__(16) T sVT[BV * LDT];
-  __shared__ __align__(16) T sA[C * LDT];
   __shared__ __align__(16) T sS[BV * LDQ];
+  // sG (gates, then their inclusive prefix b) is dead once Qt/Kt are built, so
+  // the intra-chunk block sA reuses its bytes
+  constexpr int kGBytes = C * LDG * 4, kABytes = C * LDT * (int)sizeof(T);
+  __shared__ __align__(16) char sGA[kGBytes > kABytes ? kGBytes : kABytes];
+  float* sG = reinterpret_cast<float*>(sGA);
+  T* sA = reinterpret_cast<T*>(sGA);
   __shared__ float sBm[DK], sDec[DK], sDecm[DK];
 
   const int nvt = a.dv / BV;
@@ -52,6 +56,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_fwd_kernel(const GlaArgs a) {
   const T* v = static_cast<const T*>(a.v);
   const TG* gate = static_cast<const TG*>(a.g);
   T* o = static_cast<T*>(a.o);
+  const size_t gstride = (size_t)a.H * DK;
 
   f32x4 S[NPW];
 #pragma unroll
@@ -64,51 +69,59 @@ __global__ __launch_bounds__(kThreads, 1) void gla_fwd_kernel(const GlaArgs a) {
     }
   }
 
+  ChunkTile<T, DK> rq, rk;
+  ChunkTile<TG, DK> rg;
+  ChunkTile<T, BV> rv;
+  auto prefetch = [&](int r0) {
+    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+    rq.load(qc + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+    rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+    rg.load(gate + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+    rv.load(v + tok_off(b, r0, h, a.T, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
+  };
+  if (a.T > 0) prefetch(0);
+
   for (int r0 = 0; r0 < a.T; r0 += C) {
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-    __syncthreads();
-    load_chunk_rows<T, DK>(sQt, LDQ, nullptr, 0, qc + tok_off(b, r0, h, a.T, a.H, DK),
-                           (size_t)a.H * DK, nrow);
-    load_chunk_rows<T, DK>(sKt, LDQ, nullptr, 0, k + tok_off(b, r0, h, a.T, a.H, DK),
-                           (size_t)a.H * DK, nrow);
-    for (int idx = tid; idx < C * BV / VE; idx += kThreads) {
-      const int row = idx / (BV / VE), c0 = (idx % (BV / VE)) * VE;
-      vec_t val;
-      if (row < nrow) {
-        val = *reinterpret_cast<const vec_t*>(v + tok_off(b, r0 + row, h, a.T, a.H, a.dv) + v0 + c0);
-      } else {
+    __syncthreads();  // (A) previous chunk's LDS readers are done
+    rg.store_f32(sG, LDG);
+    rv.store_t(sVT, LDT);
+    __syncthreads();  // (B)
+    // per key channel: inclusive log-decay prefix b_j (rows >= nrow have g = 0)
+    if (tid < DK) {
+      float x[C];
 #pragma unroll
-        for (int e = 0; e < VE; ++e) val[e] = static_cast<T>(0.f);
-      }
+      for (int j = 0; j < C; ++j) x[j] = sG[j * LDG + tid];
 #pragma unroll
-      for (int e = 0; e < VE; ++e) sVT[(c0 + e) * LDT + row] = val[e];
+      for (int j = 1; j < C; ++j) x[j] += x[j - 1];
+#pragma unroll
+      for (int j = 0; j < C; ++j) sG[j * LDG + tid] = x[j];
+      const float bm = x[C / 2 - 1], bC = x[C - 1];
+      sBm[tid] = __expf(bm);
+      sDec[tid] = __expf(bC);
+      sDecm[tid] = __expf(bC - bm);
     }
-    __syncthreads();
-
-    // per key channel: inclusive log-decay prefix, reference-point rescaling
-    for (int c = tid; c < DK; c += kThreads) {
-      float bc[C];
-      float acc = 0.f;
+    __syncthreads();  // (C)
+    // rescale to the mid-chunk reference: Qt = q e^{b - b_m}, Kt = k e^{b_m - b}
+    {
+      const int j = ChunkTile<T, DK>::row();
 #pragma unroll
-      for (int j = 0; j < C; ++j) {
-        const float gv = j < nrow ? f32(gate[tok_off(b, r0 + j, h, a.T, a.H, DK) + c]) : 0.f;
-        acc += gv;
-        bc[j] = acc;
-      }
-      const float bm = bc[C / 2 - 1], bC = bc[C - 1];
+      for (int u = 0; u < ChunkTile<T, DK>::NV; ++u) {
+        const int c0 = ChunkTile<T, DK>::col(u);
+        typename ChunkTile<T, DK>::vec_t qo, ko;
 #pragma unroll
-      for (int j = 0; j < C; ++j) {
-        sQt[j * LDQ + c] = to<T>(f32(sQt[j * LDQ + c]) * __expf(bc[j] - bm));
-        const T kt = to<T>(f32(sKt[j * LDQ + c]) * __expf(bm - bc[j]));
-        sKt[j * LDQ + c] = kt;
-        sKtT[c * LDT + j] = kt;
+        for (int e = 0; e < 8; ++e) {
+          const float d = sG[j * LDG + c0 + e] - sG[(C / 2 - 1) * LDG + c0 + e];
+          qo[e] = to<T>(f32(rq.v[u][e]) * __expf(d));
+          ko[e] = to<T>(f32(rk.v[u][e]) * __expf(-d));
+        }
+        *reinterpret_cast<typename ChunkTile<T, DK>::vec_t*>(sQt + j * LDQ + c0) = qo;
+        *reinterpret_cast<typename ChunkTile<T, DK>::vec_t*>(sKt + j * LDQ + c0) = ko;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sKtT[(c0 + e) * LDT + j] = ko[e];
       }
-      sBm[c] = __expf(bm);
-      sDec[c] = __expf(bC);
-      sDecm[c] = __expf(bC - bm);
     }
-    __syncthreads();
-
+    if (r0 + C < a.T) prefetch(r0 + C);  // registers are free: next chunk's loads overlap the math
     // entering state, rescaled to the reference point: S diag(e^{b_m})
 #pragma unroll
     for (int u = 0; u < NPW; ++u) {
@@ -119,21 +132,24 @@ __global__ __launch_bounds__(kThreads, 1) void gla_fwd_kernel(const GlaArgs a) {
         sS[vv * LDQ + c] = to<T>(S[u][r] * sBm[c]);
       }
     }
+    __syncthreads();  // (D)
     // intra-chunk causal block Qt Kt^T (diagonal included)
-    f32x4 sc[4];
+    {
+      f32x4 sc[4];
 #pragma unroll
-    for (int J = 0; J < 4; ++J) {
-      sc[J] = zero4();
-      if (J <= w) tile_mma<T, DK>(sc[J], sQt + 16 * w * LDQ, LDQ, sKt + 16 * J * LDQ, LDQ);
-    }
-#pragma unroll
-    for (int J = 0; J < 4; ++J)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * g4 + r, j = 16 * J + c16;
-        sA[i * LDT + j] = to<T>((J <= w && j <= i) ? sc[J][r] : 0.f);
+      for (int J = 0; J < 4; ++J) {
+        sc[J] = zero4();
+        if (J <= w) tile_mma<T, DK>(sc[J], sQt + 16 * w * LDQ, LDQ, sKt + 16 * J * LDQ, LDQ);
       }
-    __syncthreads();
+#pragma unroll
+      for (int J = 0; J < 4; ++J)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int i = 16 * w + 4 * g4 + r, j = 16 * J + c16;
+          sA[i * LDT + j] = to<T>((J <= w && j <= i) ? sc[J][r] : 0.f);
+        }
+    }
+    __syncthreads();  // (E)
 
     // o = Qt (S diag e^{b_m})^T + A V   for rows of stripe w, columns of the slice
 #pragma unroll
@@ -188,7 +204,6 @@ hipError_t dispatch_gla(const GlaArgs& a, hipStream_t st) {
     switch (a.dk) {
       case 64: return run_gla<T, TG, 64, 64>(a, st);
       case 128: return run_gla<T, TG, 128, 64>(a, st);
-      case 256: return run_gla<T, TG, 256, 32>(a, st);
     }
   } else {
     switch (a.dk) {
@@ -202,7 +217,7 @@ hipError_t dispatch_gla(const GlaArgs& a, hipStream_t st) {
 
 bool gla_supported(int dk, int dv, bool is_bf16) {
   const bool dv_ok = dv == 64 || dv == 128 || dv == 256 || dv == 512;
-  if (is_bf16) return dv_ok && (dk == 64 || dk == 128 || dk == 256);
+  (void)is_bf16;
   return dv_ok && (dk == 64 || dk == 128);
 }
 

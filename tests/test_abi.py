@@ -77,6 +77,7 @@ def test_validation_errors_are_returned_before_launch():
     assert call_gla(s) == 1
     s = shape(io_dtype=__import__("torch").float32, dk=256)
     assert call_gla(s) == 2                               # fp32 path has dk <= 128
+    assert call_gla(shape(dk=256)) == 2                   # GLA has dk <= 128
 
 
 def test_empty_batch_is_a_no_op():

@@ -37,7 +37,7 @@ GLA_CASES = [
     (BF16, 2, 200, 2, 128, 256, "iso", "const", "config", BF16),
     (BF16, 1, 150, 2, 128, 256, "aniso", "random", "config", F32),
     (BF16, 1, 97, 2, 64, 128, "meanshift", "const", "strong", BF16),
-    (BF16, 1, 70, 2, 256, 64, "aniso", "random", "config", BF16),
+    (BF16, 1, 70, 2, 64, 512, "aniso", "random", "config", BF16),
     (BF16, 1, 1, 2, 128, 256, "iso", "random", "config", BF16),
     (BF16, 1, 63, 1, 128, 256, "iso", "random", "config", BF16),
 ]
