@@ -62,7 +62,7 @@ def lib() -> ctypes.CDLL:
             L.ccq_gla_fwd.restype = ctypes.c_int
             L.ccq_gdn_fwd.argtypes = [SP] + [P] * 15 + [S, P]
             L.ccq_gdn_fwd.restype = ctypes.c_int
-            L.ccq_fwd_bwd.argtypes = [SP, ctypes.c_int] + [P] * 17 + [S, P]
+            L.ccq_fwd_bwd.argtypes = [SP, ctypes.c_int] + [P] * 15 + [S, P]
             L.ccq_fwd_bwd.restype = ctypes.c_int
             L.ccq_trace_events.argtypes = [P, ctypes.c_int]
             L.ccq_trace_events.restype = ctypes.c_int

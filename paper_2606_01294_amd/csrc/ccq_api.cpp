@@ -78,6 +78,32 @@ FwdLayout fwd_layout(const ccq_shape* s, ccq_backbone bb) {
   return L;
 }
 
+struct BwdLayout {
+  size_t qclean, corr, mdq, mdu, states, dstates, dqc, dqc_io, dkg, db, dbt, total;
+};
+
+BwdLayout bwd_layout(const ccq_shape* s) {
+  BwdLayout L{};
+  const size_t ntok = (size_t)s->B * s->T * s->H;
+  const size_t nchunk = (size_t)s->B * s->H * ((s->T + 63) / 64);
+  const size_t e = esize(s->io_dtype);
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t o = off; off += align_up(bytes); return o; };
+  L.qclean = take(ntok * s->dk * e);
+  L.corr = take(ntok * s->dk * 4);
+  L.mdq = take(ntok * 4);
+  L.mdu = take(ntok * 4);
+  L.states = take(nchunk * s->dv * s->dk * e);
+  L.dstates = take(nchunk * s->dv * s->dk * e);
+  L.dqc = take(ntok * s->dk * 4);
+  L.dqc_io = take(ntok * s->dk * e);
+  L.dkg = take(ntok * s->dk * 4);
+  L.db = take(ntok * s->dk * 4);
+  L.dbt = take(nchunk * s->dk * 4);
+  L.total = off;
+  return L;
+}
+
 // T == 0: the final states are the initial ones (or zero).
 ccq_status copy_initial_states(const ccq_shape* s, const float* S0, const float* C0,
                                const float* mu0, float* ST, float* CT, float* muT,
@@ -118,12 +144,12 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   void* qclean = ws + L.qclean;
   trace_begin_call();
 
-  ccq::CleanArgs ca{q, k, lam, C0, mu0, qclean, q_clean_dbg, CT, muT,
+  ccq::CleanArgs ca{q, k, lam, C0, mu0, qclean, q_clean_dbg, CT, muT, nullptr, nullptr, nullptr,
                     s->B, s->T, s->H, s->dk, s->centered, s->t0};
   if (traced(st, [&] { return ccq::launch_clean(ca, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
 
   if (bb == CCQ_GLA) {
-    ccq::GlaArgs ga{qclean, k, v, g_or_la, S0, o, ST, s->B, s->T, s->H, s->dk, s->dv, s->scale};
+    ccq::GlaArgs ga{qclean, k, v, g_or_la, S0, o, ST, nullptr, s->B, s->T, s->H, s->dk, s->dv, s->scale};
     const bool gbf = s->gate_dtype == CCQ_BF16;
     if (traced(st, [&] { return ccq::launch_gla_fwd(ga, bf, gbf, st); }) != hipSuccess)
       return CCQ_ERR_HIP;
@@ -145,7 +171,10 @@ extern "C" {
 
 size_t ccq_workspace_size(const ccq_shape* s, ccq_backbone bb, int with_bwd) {
   if (check_shape(s, bb) != CCQ_OK) return 0;
-  if (with_bwd) return 0;  // the training entry point is not available in this build
+  if (with_bwd) {
+    if (bb != CCQ_GLA || !ccq::bwd_supported(s->dk, s->dv, s->io_dtype == CCQ_BF16)) return 0;
+    return bwd_layout(s).total;
+  }
   return fwd_layout(s, bb).total;
 }
 
@@ -171,12 +200,60 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
                        const float* lam, const void* dO, void* o, void* dq, void* dk, void* dv,
                        void* dg_or_dlogalpha, float* dbeta, float* dlam, void* workspace,
                        size_t ws_bytes, void* stream) {
-  (void)q; (void)k; (void)v; (void)g_or_logalpha; (void)beta; (void)lam; (void)dO; (void)o;
-  (void)dq; (void)dk; (void)dv; (void)dg_or_dlogalpha; (void)dbeta; (void)dlam;
-  (void)workspace; (void)ws_bytes; (void)stream;
+  (void)beta;
+  (void)dbeta;
   ccq_status rc = check_shape(s, bb);
   if (rc != CCQ_OK) return rc;
-  return CCQ_ERR_UNSUPPORTED;
+  if (bb != CCQ_GLA) return CCQ_ERR_UNSUPPORTED;  // the Gated DeltaNet backward is not built
+  if (s->t0 != 0) return CCQ_ERR_INVALID_ARG;     // a training step starts from zero states
+  const bool bf = s->io_dtype == CCQ_BF16;
+  const bool gbf = s->gate_dtype == CCQ_BF16;
+  if (!ccq::bwd_supported(s->dk, s->dv, bf)) return CCQ_ERR_UNSUPPORTED;
+  const size_t ntok = (size_t)s->B * s->T * s->H;
+  if (workspace && !aligned(workspace)) return CCQ_ERR_INVALID_ARG;
+  if (ntok > 0) {
+    const void* req[] = {q, k, v, g_or_logalpha, lam, dO, o, dq, dk, dv, dg_or_dlogalpha, dlam};
+    for (const void* p : req)
+      if (!p || !aligned(p)) return CCQ_ERR_INVALID_ARG;
+  }
+  if (ntok == 0) return CCQ_OK;
+  const BwdLayout L = bwd_layout(s);
+  if (!workspace || ws_bytes < L.total) return CCQ_ERR_WORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  float* corr = reinterpret_cast<float*>(ws + L.corr);
+  float* mdq = reinterpret_cast<float*>(ws + L.mdq);
+  float* mdu = reinterpret_cast<float*>(ws + L.mdu);
+  float* dqc = reinterpret_cast<float*>(ws + L.dqc);
+  float* dkg = reinterpret_cast<float*>(ws + L.dkg);
+  float* db = reinterpret_cast<float*>(ws + L.db);
+  float* dbt = reinterpret_cast<float*>(ws + L.dbt);
+  trace_begin_call();
+
+  // forward: cleaned queries (with Sigma q and m.q kept), then GLA keeping S_r
+  ccq::CleanArgs c1{q, k, lam, nullptr, nullptr, ws + L.qclean, nullptr, nullptr, nullptr,
+                    nullptr, corr, mdq, s->B, s->T, s->H, s->dk, s->centered, 0};
+  if (traced(st, [&] { return ccq::launch_clean(c1, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::GlaArgs ga{ws + L.qclean, k, v, g_or_logalpha, nullptr, o, nullptr, ws + L.states,
+                  s->B, s->T, s->H, s->dk, s->dv, s->scale};
+  if (traced(st, [&] { return ccq::launch_gla_fwd(ga, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  // backward: dS scan, chunk gradients, decay gradient, dq, dk
+  ccq::DstateArgs da{ws + L.qclean, g_or_logalpha, dO, ws + L.dstates, s->B, s->T, s->H, s->dk,
+                     s->dv, s->scale};
+  if (traced(st, [&] { return ccq::launch_gla_dstate(da, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::GlaBwdArgs ba{ws + L.qclean, k, v, g_or_logalpha, dO, ws + L.states, ws + L.dstates, corr,
+                     dqc, ws + L.dqc_io, dkg, dv, db, dbt, dlam, s->B, s->T, s->H, s->dk, s->dv,
+                     s->scale};
+  if (traced(st, [&] { return ccq::launch_gla_bwd_chunk(ba, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::DgArgs ga2{db, dbt, dg_or_dlogalpha, s->B, s->T, s->H, s->dk};
+  if (traced(st, [&] { return ccq::launch_gla_dg(ga2, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::CleanArgs c2{ws + L.dqc_io, k, lam, nullptr, nullptr, dq, nullptr, nullptr, nullptr,
+                    dqc, nullptr, mdu, s->B, s->T, s->H, s->dk, s->centered, 0};
+  if (traced(st, [&] { return ccq::launch_clean(c2, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::CcqDkArgs ka{q, k, ws + L.dqc_io, lam, mdq, mdu, dkg, dk, s->B, s->T, s->H, s->dk,
+                    s->centered};
+  if (traced(st, [&] { return ccq::launch_ccq_dk(ka, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  return CCQ_OK;
 }
 
 ccq_status ccq_trace_events(void* const* events, int n_events) {

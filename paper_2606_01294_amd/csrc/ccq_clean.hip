@@ -148,6 +148,7 @@ __global__ __launch_bounds__(kThreads, 1) void clean_kernel(const CleanArgs a) {
       rs = row16_sum(rs);
       cq[r] = sMq[i] + rs;
       inv_t[r] = 1.f / (t0f + (float)(r0 + i + 1));
+      if (a.mdot && n0 == 0 && c16 == 0 && i < nrow) a.mdot[((size_t)b * a.T + r0 + i) * a.H + h] = cq[r];
     }
 #pragma unroll
     for (int J = 0; J < 4; ++J) {
@@ -194,11 +195,13 @@ __global__ __launch_bounds__(kThreads, 1) void clean_kernel(const CleanArgs a) {
         const int col = n0 + 16 * tn + c16;
         float c = a1[r] + a2[r] * inv_t[r];
         if (a.centered) c -= cq[r] * inv_t[r] * inv_t[r] * sM[col];
-        const float qcv = f32(sQ[i * LDQ + col]) - sLam[i] * c;
         if (i < nrow) {
           const size_t off = tok_off(b, r0 + i, h, a.T, a.H, DK) + col;
+          const float base = a.base ? a.base[off] : f32(sQ[i * LDQ + col]);
+          const float qcv = base - sLam[i] * c;
           qc_out[off] = to<T>(qcv);
           if (a.qclean_dbg) a.qclean_dbg[off] = qcv;
+          if (a.corr) a.corr[off] = c;
         }
       }
     }

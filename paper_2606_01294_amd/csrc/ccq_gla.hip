@@ -122,7 +122,11 @@ __global__ __launch_bounds__(kThreads, 1) void gla_fwd_kernel(const GlaArgs a) {
       }
     }
     if (r0 + C < a.T) prefetch(r0 + C);  // registers are free: next chunk's loads overlap the math
-    // entering state, rescaled to the reference point: S diag(e^{b_m})
+    // entering state, rescaled to the reference point: S diag(e^{b_m});
+    // the training pass also keeps S_r itself for the backward
+    T* st_out = a.states ? static_cast<T*>(a.states) +
+                               (((size_t)bh * ((a.T + C - 1) / C) + r0 / C) * a.dv + v0) * DK
+                         : nullptr;
 #pragma unroll
     for (int u = 0; u < NPW; ++u) {
       const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
@@ -130,6 +134,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_fwd_kernel(const GlaArgs a) {
       for (int r = 0; r < 4; ++r) {
         const int vv = 16 * tv + 4 * g4 + r, c = 16 * tc + c16;
         sS[vv * LDQ + c] = to<T>(S[u][r] * sBm[c]);
+        if (st_out) st_out[(size_t)vv * DK + c] = to<T>(S[u][r]);
       }
     }
     __syncthreads();  // (D)

@@ -7,17 +7,22 @@
 
 namespace ccq {
 
-// Query contraction (Eq. clean evaluated chunkwise, App. B / Alg. 1).
+// Query contraction (Eq. clean evaluated chunkwise, App. B / Alg. 1):
+// out = base - lam * Sigma_t x  (base = x when null).  The backward pass runs
+// the same kernel on x = dL/dq_clean, since (I - lam Sigma)^T = I - lam Sigma.
 struct CleanArgs {
-  const void* q;      // [B,T,H,dk] io
+  const void* q;      // x: [B,T,H,dk] io
   const void* k;      // [B,T,H,dk] io
   const float* lam;   // [B,T,H]
   const float* C0;    // [B,H,dk,dk] or null
   const float* mu0;   // [B,H,dk] or null
-  void* qclean;       // [B,T,H,dk] io (workspace)
-  float* qclean_dbg;  // [B,T,H,dk] fp32 or null
+  void* qclean;       // out: [B,T,H,dk] io
+  float* qclean_dbg;  // out in fp32, or null
   float* CT;          // [B,H,dk,dk] or null
   float* muT;         // [B,H,dk] or null
+  const float* base;  // [B,T,H,dk] fp32 or null
+  float* corr;        // Sigma_t x_t, [B,T,H,dk] fp32, or null
+  float* mdot;        // m_t . x_t (raw key sum), [B,T,H] fp32, or null
   int B, T, H, dk;
   int centered;
   int64_t t0;
@@ -32,6 +37,7 @@ struct GlaArgs {
   const float* S0;    // [B,H,dv,dk] or null
   void* o;            // [B,T,H,dv] io
   float* ST;          // [B,H,dv,dk] or null
+  void* states;       // chunk-entry states S_r, [B*H, N, dv, dk] io, or null
   int B, T, H, dk, dv;
   float scale;
 };
@@ -61,6 +67,57 @@ struct GdnArgs {
   float scale;
 };
 
+// ---- training step (CCQ-GLA backward) ----
+// Reverse scan of the state adjoint dS (decayed like S); stores the adjoint
+// of the state leaving each chunk.
+struct DstateArgs {
+  const void* qc;     // [B,T,H,dk] io (cleaned queries)
+  const void* g;      // [B,T,H,dk] gate dtype
+  const void* dO;     // [B,T,H,dv] io
+  void* dstates;      // [B*H, N, dv, dk] io
+  int B, T, H, dk, dv;
+  float scale;
+};
+
+// Chunk-parallel GLA gradients given S_r and dS_{r+1}.
+struct GlaBwdArgs {
+  const void* qc; const void* k; const void* v; const void* g; const void* dO;
+  const void* states;   // [B*H, N, dv, dk] io
+  const void* dstates;  // [B*H, N, dv, dk] io
+  const float* corr;    // Sigma_t q_t, [B,T,H,dk] fp32
+  float* dqc;           // dL/dq_clean [B,T,H,dk] fp32
+  void* dqc_io;         // same, io dtype
+  float* dk_gla;        // GLA part of dL/dk [B,T,H,dk] fp32
+  void* dv_out;         // [B,T,H,dv] io
+  float* db;            // dL/d(cumulative log decay) [B,T,H,dk] fp32
+  float* db_tot;        // per-chunk column sums of db [B*H, N, dk]
+  float* dlam;          // [B,T,H]
+  int B, T, H, dk, dv;
+  float scale;
+};
+
+// dg_s = sum_{t >= s} db_t (reverse cumulative sum over the sequence).
+struct DgArgs {
+  const float* db;
+  const float* db_tot;
+  void* dg;             // [B,T,H,dk] gate dtype
+  int B, T, H, dk;
+};
+
+// Key gradient of the contraction (reverse scan of an undecayed dk x dk state).
+struct CcqDkArgs {
+  const void* q;        // [B,T,H,dk] io
+  const void* k;        // [B,T,H,dk] io
+  const void* u;        // dL/dq_clean, io
+  const float* lam;     // [B,T,H]
+  const float* mdot_q;  // m_t . q_t
+  const float* mdot_u;  // m_t . u_t
+  const float* dk_gla;  // [B,T,H,dk] fp32, added to the result
+  void* dk_out;         // [B,T,H,dk] io
+  int B, T, H, dk;
+  int centered;
+};
+
 // Each launcher returns hipSuccess or the launch error.  is_bf16 selects the
 // io dtype (bf16 or fp32); shapes are validated by the caller.
 hipError_t launch_clean(const CleanArgs& a, bool is_bf16, hipStream_t st);
@@ -68,6 +125,12 @@ hipError_t launch_gla_fwd(const GlaArgs& a, bool is_bf16, bool gate_bf16, hipStr
 hipError_t launch_gdn_wy(const WyArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_gdn_fwd(const GdnArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_copy_or_zero(float* dst, const float* src, size_t n, hipStream_t st);
+
+hipError_t launch_gla_dstate(const DstateArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
+hipError_t launch_gla_bwd_chunk(const GlaBwdArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
+hipError_t launch_gla_dg(const DgArgs& a, bool gate_bf16, hipStream_t st);
+hipError_t launch_ccq_dk(const CcqDkArgs& a, bool is_bf16, hipStream_t st);
+bool bwd_supported(int dk, int dv, bool is_bf16);
 
 // Supported-shape predicates (used by validation before any launch).
 bool clean_supported(int dk, bool is_bf16);

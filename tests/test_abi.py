@@ -99,3 +99,22 @@ def test_binding_rejects_wrong_dtype_before_calling():
     q = torch.zeros(1, 4, 1, 64)
     with pytest.raises(TypeError):
         ccq.ccq_gla_fwd(q, q, q, q, torch.zeros(1, 4, 1, dtype=torch.float64))
+
+
+def call_bwd(s, bb=0, ws_bytes=1 << 34, ptr=FAKE):
+    P = ctypes.c_void_p
+    return ccq.lib().ccq_fwd_bwd(ctypes.byref(s), bb, P(ptr), P(ptr), P(ptr), P(ptr), None,
+                                 P(ptr), P(ptr), P(ptr), P(ptr), P(ptr), P(ptr), P(ptr), None,
+                                 P(ptr), P(ptr), ws_bytes, None)
+
+
+def test_training_entry_point_validation():
+    assert ccq.ccq_workspace_size(shape(), ccq.CCQ_GLA, True) > ccq.ccq_workspace_size(
+        shape(), ccq.CCQ_GLA, False)
+    assert ccq.ccq_workspace_size(shape(dk=256), ccq.CCQ_GDN, True) == 0
+    assert call_bwd(shape(dk=256), bb=1) == 2               # no Gated DeltaNet backward
+    s = shape()
+    s.t0 = 5
+    assert call_bwd(s) == 1                                 # training starts from zero state
+    assert call_bwd(shape(), ws_bytes=100) == 3             # workspace too small
+    assert call_bwd(shape(io_dtype=__import__("torch").float32, dk=128)) == 2
