@@ -50,16 +50,46 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     elif kernel == "gdn_fwd":
         by = ntok * (3 * dk * io_bytes + dv * 4 + dv * io_bytes + 4) + BH * dv * dk * 4
         fl = ntok * (6 * dk * dv + 2 * C * (dk + dv))
+    elif kernel == "gla_fwd_train":   # forward that also writes the chunk-entry states
+        by = ntok * (2 * dk * io_bytes + dk * gate_bytes + 2 * dv * io_bytes + dv * dk * io_bytes // C)
+        fl = ntok * (2 * C * (dk + dv) + 4 * dk * dv)
+    elif kernel == "clean_train":     # contraction exporting Sigma q (fp32) and m.q
+        by = ntok * (3 * dk * io_bytes + 4 + 4 * dk + 4)
+        fl = ntok * (4 * dk * dk + 4 * C * dk)
+    elif kernel == "clean_dq":        # dq = (I - lam Sigma) dq_clean, fp32 base
+        by = ntok * (2 * dk * io_bytes + 4 * dk + dk * io_bytes + 8)
+        fl = ntok * (4 * dk * dk + 4 * C * dk)
+    elif kernel == "gla_dstate":
+        by = ntok * (dk * io_bytes + dk * gate_bytes + dv * io_bytes + dv * dk * io_bytes // C)
+        fl = ntok * (2 * dk * dv)
+    elif kernel == "gla_bwd_chunk":
+        by = ntok * (2 * dk * io_bytes + dk * gate_bytes + 3 * dv * io_bytes + 2 * dv * dk * io_bytes // C
+                     + 4 * dk + 12 * dk + dk * io_bytes + 4)
+        fl = ntok * (6 * dk * dv + 4 * C * dv + 6 * C * dk)
+    elif kernel == "gla_dg":
+        by = ntok * (4 * dk + dk * gate_bytes)
+        fl = ntok * dk
+    elif kernel == "ccq_dk":
+        by = ntok * (3 * dk * io_bytes + 12 + 4 * dk + dk * io_bytes)
+        fl = ntok * (6 * dk * dk + 8 * C * dk)
     else:
         raise KeyError(kernel)
     return by, fl
 
 
-KERNELS = {0: ["clean", "gla_fwd"], 1: ["clean", "gdn_wy", "gdn_fwd"]}
+KERNELS = {0: ["clean", "gla_fwd"], 1: ["clean", "gdn_wy", "gdn_fwd"],
+           "train": ["clean_train", "gla_fwd_train", "gla_dstate", "gla_bwd_chunk", "gla_dg",
+                     "clean_dq", "ccq_dk"]}
 KERNEL_SYMBOL = {"clean": "clean_kernel", "gla_fwd": "gla_fwd_kernel", "gdn_wy": "gdn_wy_kernel",
-                 "gdn_fwd": "gdn_fwd_kernel"}
+                 "gdn_fwd": "gdn_fwd_kernel", "clean_train": "clean_kernel",
+                 "gla_fwd_train": "gla_fwd_kernel", "clean_dq": "clean_kernel",
+                 "gla_dstate": "gla_dstate_kernel", "gla_bwd_chunk": "gla_bwd_chunk_kernel",
+                 "gla_dg": "gla_dg_kernel", "ccq_dk": "ccq_dk_kernel"}
 KERNEL_SOURCE = {"clean": "ccq_clean.hip", "gla_fwd": "ccq_gla.hip", "gdn_wy": "ccq_gdn.hip",
-                 "gdn_fwd": "ccq_gdn.hip"}
+                 "gdn_fwd": "ccq_gdn.hip", "clean_train": "ccq_clean.hip",
+                 "gla_fwd_train": "ccq_gla.hip", "clean_dq": "ccq_clean.hip",
+                 "gla_dstate": "ccq_bwd.hip", "gla_bwd_chunk": "ccq_bwd.hip",
+                 "gla_dg": "ccq_bwd.hip", "ccq_dk": "ccq_bwd.hip"}
 
 
 def source_sha(kernel: str) -> str:
@@ -100,13 +130,22 @@ class Call:
                     "CT": torch.empty((B, H, dk, dk), dtype=torch.float32, device=dev),
                     "muT": torch.empty((B, H, dk), dtype=torch.float32, device=dev)}
         shape = ccq.make_shape(B, T, H, dk, dv, w.dtype, w.dtype)
-        self.ws = torch.empty(max(1, ccq.ccq_workspace_size(shape, w.backbone)), dtype=torch.uint8,
-                              device=dev)
+        self.ws = torch.empty(max(1, ccq.ccq_workspace_size(shape, w.backbone, w.train)),
+                              dtype=torch.uint8, device=dev)
+        if w.train:
+            self.out = {"o": self.out["o"]}
+            for name, ref in (("dq", "q"), ("dk", "k"), ("dv", "v"), ("dg", "g")):
+                self.out[name] = torch.empty_like(self.d[ref])
+            self.out["dlam"] = torch.empty_like(self.d["lam"])
         self.ccq = ccq
+        self.kernels = KERNELS["train" if w.train else w.backbone]
 
     def __call__(self):
         d = self.d
-        if self.w.backbone == 0:
+        if self.w.train:
+            self.ccq.ccq_fwd_bwd(d["q"], d["k"], d["v"], d["g"], d["lam"], d["dO"], out=self.out,
+                                 workspace=self.ws)
+        elif self.w.backbone == 0:
             self.ccq.ccq_gla_fwd(d["q"], d["k"], d["v"], d["g"], d["lam"], out=self.out,
                                  workspace=self.ws)
         else:
@@ -122,7 +161,7 @@ def time_calls(torch, ccq, calls, steps, warmup):
         for c in calls:
             c()
     torch.cuda.synchronize()
-    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2 * len(KERNELS[c.w.backbone]))]
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2 * len(c.kernels))]
            for c in calls] for _ in range(steps)]
     for step_ev in ev:
         for evs in step_ev:
@@ -141,8 +180,7 @@ def time_calls(torch, ccq, calls, steps, warmup):
     ms_step = start.elapsed_time(end) / steps
     per_kernel = []
     for j, c in enumerate(calls):
-        names = KERNELS[c.w.backbone]
-        for kidx, name in enumerate(names):
+        for kidx, name in enumerate(c.kernels):
             ts = [ev[i][j][2 * kidx].elapsed_time(ev[i][j][2 * kidx + 1]) for i in range(steps)]
             per_kernel.append({"workload": c.w.name, "kernel": name,
                                "symbol": KERNEL_SYMBOL[name],
@@ -254,18 +292,20 @@ def main(argv=None):
 
     extra = {}
     if not args.no_extra:
-        for name in ("gla_500m_t2k", "gdn_1p3b_t4k", "gla_500m_t20k", "gdn_1p3b_t20k"):
+        for name in ("gla_500m_t2k", "gdn_1p3b_t4k", "gla_500m_t20k", "gdn_1p3b_t20k",
+                     "gla_train_t4k"):
             c = step_calls[0] if name == "gla_500m_t2k" else (
                 step_calls[1] if name == "gdn_1p3b_t4k" else Call(W[name], torch, ccq, inputs))
             ms, pk = time_calls(torch, ccq, [c], max(5, args.steps // 2), 3)
             fl = sum(kernel_cost(e["kernel"], c.w)[1] for e in pk)
+            dom = max(pk, key=lambda e: e["ms_mean"])
             extra[name] = {"tokens_per_s": round(c.w.tokens / (ms * 1e-3), 1), "ms": round(ms, 4),
                            "mfma_frac": round(fl / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-                           "kernels_ms": {e["symbol"]: round(e["ms_mean"], 5) for e in pk}}
+                           "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
+                           "roofline": roofline(dom, c.w)}
             if c not in step_calls:
                 del c
                 torch.cuda.empty_cache()
-        extra["gla_train_t4k"] = "fwd+bwd not available in this build"
 
     cpu = None if args.no_cpu_baseline else cpu_baseline(step_calls)
 

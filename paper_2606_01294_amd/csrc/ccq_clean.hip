@@ -28,28 +28,27 @@ __global__ __launch_bounds__(kThreads, 1) void clean_kernel(const CleanArgs a) {
   constexpr int C = kChunk;
   constexpr int P = Pad<T>::value;
   constexpr bool kSplit = sizeof(T) == 2;  // bf16: carry a tail for fp32 operands
-  constexpr int LDQ = DK + P, LDT = C + P, LDA = C + P;
-  constexpr int NTILE_COL = DK / 16;
-  constexpr int NPW = CT * DK / (16 * 16 * 4);  // S^K tiles per wave
-  static_assert(NPW >= 1, "tile split");
+  constexpr int LDQ = DK + P, LDA = C + P;
+  constexpr int NTN = CT / 16;                     // column tiles of the slice
+  constexpr int NPW = CT * DK / (16 * 16 * 4);     // state tiles per wave
+  constexpr int RPW = (DK / 16) / 4;               // state row tiles per wave
+  static_assert(NPW >= 1 && RPW >= 1 && NPW == RPW * NTN, "tile split");
   constexpr int VE = 8;
   typedef T vec_t __attribute__((ext_vector_type(VE)));
 
   __shared__ __align__(16) T sQ[C * LDQ];
   __shared__ __align__(16) T sK[C * LDQ];
-  __shared__ __align__(16) T sKT[DK * LDT];
-  __shared__ __align__(16) T sAh[C * LDA];
+  __shared__ __align__(16) T sAh[C * LDA];  // A'[i][j]
   __shared__ __align__(16) T sAl[kSplit ? C * LDA : 8];
-  __shared__ __align__(16) T sSh[CT * LDQ];
+  __shared__ __align__(16) T sSh[CT * LDQ];  // S^K rows n0.. as B^T operand [n][c]
   __shared__ __align__(16) T sSl[kSplit ? CT * LDQ : 8];
   __shared__ __align__(16) float sM[DK];
-  __shared__ float sMq[C];
-  __shared__ float sLam[C];
+  __shared__ float sMq[C], sCq[C], sLam[C];
 
   const int ntiles = DK / CT;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
   const int bh = lb / ntiles;
-  const int n0 = (lb % ntiles) * CT;  // first S^K row / q_clean column of this block
+  const int n0 = (lb % ntiles) * CT;  // first S^K column / q_clean column of this block
   const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
@@ -59,40 +58,51 @@ __global__ __launch_bounds__(kThreads, 1) void clean_kernel(const CleanArgs a) {
   const size_t gstride = (size_t)a.H * DK;
   const float t0f = (float)a.t0;
 
-  // carried state: S^K rows [n0, n0+CT) as fp32 accumulators, M in LDS
-  f32x4 sk[NPW];
+  // carried state, transposed: tile u holds S^K[c][n], c = 16 tr + 4 g4 + r (all
+  // DK rows over the waves), n = n0 + 16 tn + c16; Mt[v] holds the key sum of
+  // row tile (w RPW + v) in column 0.
+  f32x4 sk[NPW], Mt[RPW];
 #pragma unroll
   for (int u = 0; u < NPW; ++u) {
-    const int tau = w * NPW + u, tr = tau / NTILE_COL, tc = tau % NTILE_COL;
+    const int tr = w * RPW + u / NTN, tn = u % NTN;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int n = n0 + 16 * tr + 4 * g4 + r, c = 16 * tc + c16;
-      sk[u][r] = a.C0 ? t0f * a.C0[((size_t)bh * DK + n) * DK + c] : 0.f;
+      const int c = 16 * tr + 4 * g4 + r, n = n0 + 16 * tn + c16;
+      sk[u][r] = a.C0 ? t0f * a.C0[((size_t)bh * DK + c) * DK + n] : 0.f;
     }
   }
-  for (int c = tid; c < DK; c += kThreads) sM[c] = a.mu0 ? t0f * a.mu0[(size_t)bh * DK + c] : 0.f;
+#pragma unroll
+  for (int v = 0; v < RPW; ++v)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int c = 16 * (w * RPW + v) + 4 * g4 + r;
+      Mt[v][r] = (a.mu0 && c16 == 0) ? t0f * a.mu0[(size_t)bh * DK + c] : 0.f;
+    }
 
-  auto store_state_tile = [&]() {
+  auto publish_state = [&]() {  // S^K -> sSh/sSl [n][c], key sum -> sM
 #pragma unroll
     for (int u = 0; u < NPW; ++u) {
-      const int tau = w * NPW + u, tr = tau / NTILE_COL, tc = tau % NTILE_COL;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int n = 16 * tr + 4 * g4 + r, c = 16 * tc + c16;
-        if constexpr (kSplit) {
-          bf16_t hi, lo;
-          split_bf16(sk[u][r], hi, lo);
-          sSh[n * LDQ + c] = hi;
-          sSl[n * LDQ + c] = lo;
-        } else {
-          sSh[n * LDQ + c] = sk[u][r];
-        }
+      const int tr = w * RPW + u / NTN, tn = u % NTN;
+      const int off = (16 * tn + c16) * LDQ + 16 * tr + 4 * g4;
+      if constexpr (kSplit) {
+        bf16_t h0, h1, h2, h3, l0, l1, l2, l3;
+        split_bf16(sk[u][0], h0, l0);
+        split_bf16(sk[u][1], h1, l1);
+        split_bf16(sk[u][2], h2, l2);
+        split_bf16(sk[u][3], h3, l3);
+        *reinterpret_cast<bf16x4*>(sSh + off) = bf16x4{h0, h1, h2, h3};
+        *reinterpret_cast<bf16x4*>(sSl + off) = bf16x4{l0, l1, l2, l3};
+      } else {
+        store4(sSh + off, sk[u][0], sk[u][1], sk[u][2], sk[u][3]);
       }
     }
+    if (c16 == 0)
+#pragma unroll
+      for (int v = 0; v < RPW; ++v)
+        *reinterpret_cast<f32x4*>(sM + 16 * (w * RPW + v) + 4 * g4) = Mt[v];
   };
-  store_state_tile();
+  publish_state();
 
-  // chunk 0 in flight
   ChunkTile<T, DK> rq, rk;
   RowScalar rlam;
   auto prefetch = [&](int r0) {
@@ -105,15 +115,14 @@ __global__ __launch_bounds__(kThreads, 1) void clean_kernel(const CleanArgs a) {
 
   for (int r0 = 0; r0 < a.T; r0 += C) {
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-    __syncthreads();  // previous chunk's readers are done with LDS
+    __syncthreads();  // (A) previous chunk's readers are done with LDS
     rq.store(sQ, LDQ);
     rk.store(sK, LDQ);
-    rk.store_t(sKT, LDT);
     if (tid < C) sLam[tid] = rlam.get();
-    if (r0 + C < a.T) prefetch(r0 + C);  // next chunk loads overlap this chunk's math
-    __syncthreads();
+    if (r0 + C < a.T) prefetch(r0 + C);  // next chunk's loads overlap this chunk's math
+    __syncthreads();  // (B)
 
-    // M_r . q_i : four threads per row, 16-byte reads
+    // M_r . q_i: four threads per row
     {
       const int row = tid >> 2, part = tid & 3;
       float s = 0.f;
@@ -127,61 +136,65 @@ __global__ __launch_bounds__(kThreads, 1) void clean_kernel(const CleanArgs a) {
       s += __shfl_xor(s, 2);
       if (part == 0) sMq[row] = s;
     }
-    // masked score block q_i . k_j for row stripe w (tiles J <= w)
+    // transposed score tiles: sc[J][r] = k_j . q_i, j = 16 J + 4 g4 + r, i = 16 w + c16
     f32x4 sc[4];
 #pragma unroll
     for (int J = 0; J < 4; ++J) {
       sc[J] = zero4();
-      if (J <= w) tile_mma<T, DK>(sc[J], sQ + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+      if (J <= w) tile_mma<T, DK>(sc[J], sK + 16 * J * LDQ, LDQ, sQ + 16 * w * LDQ, LDQ);
     }
-    __syncthreads();  // sMq visible
-    float cq[4], inv_t[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int i = 16 * w + 4 * g4 + r;
+    __syncthreads();  // (C) sMq visible
+    {
+      const int i = 16 * w + c16;
       float rs = 0.f;
 #pragma unroll
+      for (int J = 0; J < 4; ++J)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (J <= w && 16 * J + 4 * g4 + r <= i) rs += sc[J][r];
+      rs += __shfl_xor(rs, 16);
+      rs += __shfl_xor(rs, 32);
+      const float cq = sMq[i] + rs;   // m_t . q_i (raw key sum up to t_i)
+      const float it = 1.f / (t0f + (float)(r0 + i + 1));
+      if (g4 == 0) sCq[i] = cq;
+      if (a.mdot && n0 == 0 && g4 == 0 && i < nrow) a.mdot[((size_t)b * a.T + r0 + i) * a.H + h] = cq;
+      const float mean = a.centered ? cq * it * it : 0.f;
+      // A'[i][j] = (q_i . k_j)/t_i - cq_i/t_i^2 for j <= i, written as row i
+#pragma unroll
       for (int J = 0; J < 4; ++J) {
-        const int j = 16 * J + c16;
-        if (J <= w && j <= i) rs += sc[J][r];
-      }
-      rs = row16_sum(rs);
-      cq[r] = sMq[i] + rs;
-      inv_t[r] = 1.f / (t0f + (float)(r0 + i + 1));
-      if (a.mdot && n0 == 0 && c16 == 0 && i < nrow) a.mdot[((size_t)b * a.T + r0 + i) * a.H + h] = cq[r];
-    }
+        float x[4];
 #pragma unroll
-    for (int J = 0; J < 4; ++J) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * g4 + r, j = 16 * J + c16;
-        float val = 0.f;
-        if (J <= w && j <= i) {
-          val = sc[J][r] * inv_t[r];
-          if (a.centered) val -= cq[r] * inv_t[r] * inv_t[r];
+        for (int r = 0; r < 4; ++r) {
+          const int j = 16 * J + 4 * g4 + r;
+          x[r] = (J <= w && j <= i) ? sc[J][r] * it - mean : 0.f;
         }
+        const int off = i * LDA + 16 * J + 4 * g4;
         if constexpr (kSplit) {
-          bf16_t hi, lo;
-          split_bf16(val, hi, lo);
-          sAh[i * LDA + j] = hi;
-          sAl[i * LDA + j] = lo;
+          bf16_t h0, h1, h2, h3, l0, l1, l2, l3;
+          split_bf16(x[0], h0, l0);
+          split_bf16(x[1], h1, l1);
+          split_bf16(x[2], h2, l2);
+          split_bf16(x[3], h3, l3);
+          *reinterpret_cast<bf16x4*>(sAh + off) = bf16x4{h0, h1, h2, h3};
+          *reinterpret_cast<bf16x4*>(sAl + off) = bf16x4{l0, l1, l2, l3};
         } else {
-          sAh[i * LDA + j] = val;
+          store4(sAh + off, x[0], x[1], x[2], x[3]);
         }
       }
     }
-    __syncthreads();
+    __syncthreads();  // (D)
 
     // c and q_clean for rows of stripe w, columns [n0, n0 + CT)
 #pragma unroll
-    for (int tn = 0; tn < CT / 16; ++tn) {
+    for (int tn = 0; tn < NTN; ++tn) {
       f32x4 a1 = zero4(), a2 = zero4();
-      const T* kt = sKT + (n0 + 16 * tn) * LDT;
 #pragma unroll
       for (int k0 = 0; k0 < C; k0 += 32) {
-        const Frag<T> fb = ld_frag(kt + k0, LDT);
-        mma(a1, ld_frag(sAh + 16 * w * LDA + k0, LDA), fb);
-        if constexpr (kSplit) mma(a1, ld_frag(sAl + 16 * w * LDA + k0, LDA), fb);
+        if (k0 <= 16 * w) {  // A' is zero for j > i
+          const Frag<T> fb = ld_frag_tr(sK + k0 * LDQ + n0 + 16 * tn, LDQ);
+          mma(a1, ld_frag(sAh + 16 * w * LDA + k0, LDA), fb);
+          if constexpr (kSplit) mma(a1, ld_frag(sAl + 16 * w * LDA + k0, LDA), fb);
+        }
       }
 #pragma unroll
       for (int k0 = 0; k0 < DK; k0 += 32) {
@@ -189,12 +202,13 @@ __global__ __launch_bounds__(kThreads, 1) void clean_kernel(const CleanArgs a) {
         mma(a2, fa, ld_frag(sSh + 16 * tn * LDQ + k0, LDQ));
         if constexpr (kSplit) mma(a2, fa, ld_frag(sSl + 16 * tn * LDQ + k0, LDQ));
       }
+      const int col = n0 + 16 * tn + c16;
+      const float mcol = a.centered ? sM[col] : 0.f;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int i = 16 * w + 4 * g4 + r;
-        const int col = n0 + 16 * tn + c16;
-        float c = a1[r] + a2[r] * inv_t[r];
-        if (a.centered) c -= cq[r] * inv_t[r] * inv_t[r] * sM[col];
+        const float it = 1.f / (t0f + (float)(r0 + i + 1));
+        const float c = a1[r] + a2[r] * it - sCq[i] * it * it * mcol;
         if (i < nrow) {
           const size_t off = tok_off(b, r0 + i, h, a.T, a.H, DK) + col;
           const float base = a.base ? a.base[off] : f32(sQ[i * LDQ + col]);
@@ -205,25 +219,26 @@ __global__ __launch_bounds__(kThreads, 1) void clean_kernel(const CleanArgs a) {
         }
       }
     }
-    __syncthreads();  // all reads of the S^K tile and of M are done
+    __syncthreads();  // (E) the state tile and M have been read
 
-    // S^K_{r+1} = S^K_r + K^T K for rows [n0, n0+CT); M_{r+1} = M_r + sum_j k_j
+    // S^K_{r+1} = S^K_r + K^T K (columns n0..), M_{r+1} = M_r + sum_j k_j
+    {
+      const Frag<T> ones = ones_col_frag<T>();
 #pragma unroll
-    for (int u = 0; u < NPW; ++u) {
-      const int tau = w * NPW + u, tr = tau / NTILE_COL, tc = tau % NTILE_COL;
-      tile_mma<T, C>(sk[u], sKT + (n0 + 16 * tr) * LDT, LDT, sKT + 16 * tc * LDT, LDT);
-    }
-    store_state_tile();
-    for (int c = tid; c < DK; c += kThreads) {
-      float s = 0.f;
+      for (int k0 = 0; k0 < C; k0 += 32) {
+        Frag<T> fb[NTN];
 #pragma unroll
-      for (int j0 = 0; j0 < C; j0 += VE) {
-        const vec_t kv = *reinterpret_cast<const vec_t*>(sKT + c * LDT + j0);
+        for (int tn = 0; tn < NTN; ++tn) fb[tn] = ld_frag_tr(sK + k0 * LDQ + n0 + 16 * tn, LDQ);
 #pragma unroll
-        for (int e = 0; e < VE; ++e) s += f32(kv[e]);
+        for (int v = 0; v < RPW; ++v) {
+          const Frag<T> fa = ld_frag_tr(sK + k0 * LDQ + 16 * (w * RPW + v), LDQ);
+#pragma unroll
+          for (int tn = 0; tn < NTN; ++tn) mma(sk[v * NTN + tn], fa, fb[tn]);
+          mma(Mt[v], fa, ones);
+        }
       }
-      sM[c] += s;
     }
+    publish_state();
   }
   __syncthreads();
 
@@ -234,11 +249,11 @@ __global__ __launch_bounds__(kThreads, 1) void clean_kernel(const CleanArgs a) {
     if (a.CT) {
 #pragma unroll
       for (int u = 0; u < NPW; ++u) {
-        const int tau = w * NPW + u, tr = tau / NTILE_COL, tc = tau % NTILE_COL;
+        const int tr = w * RPW + u / NTN, tn = u % NTN;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int n = n0 + 16 * tr + 4 * g4 + r, c = 16 * tc + c16;
-          a.CT[((size_t)bh * DK + n) * DK + c] = sk[u][r] * inv;
+          const int c = 16 * tr + 4 * g4 + r, n = n0 + 16 * tn + c16;
+          a.CT[((size_t)bh * DK + c) * DK + n] = sk[u][r] * inv;
         }
       }
     }
@@ -272,7 +287,7 @@ hipError_t launch_clean(const CleanArgs& a, bool is_bf16, hipStream_t st) {
   } else {
     switch (a.dk) {
       case 64: return run_clean<float, 64, 16>(a, st);
-      case 128: return run_clean<float, 128, 16>(a, st);
+      case 128: return run_clean<float, 128, 32>(a, st);
     }
   }
   return hipErrorInvalidValue;

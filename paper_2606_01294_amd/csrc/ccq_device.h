@@ -66,6 +66,67 @@ __device__ __forceinline__ Frag<T> ld_frag_global(const T* tile, size_t ld) {
   return f;
 }
 
+// Fragment of a transposed operand: element (m, k) of the MFMA operand is
+// X[k][m] of a row-major LDS tile X (k runs along X's rows).  `base` points at
+// X[k0][m0], ld is X's row pitch in elements (a multiple of 4).  For bf16 this
+// uses the gfx950 transposing LDS read: within each 16-lane group, lane j
+// addresses row k0 + 8g + j/4, column m0 + 4 (j % 4), and lane i receives
+// X[k0 + 8g .. + 3][m0 + i]; a second read covers the next four rows.
+template <typename T>
+__device__ __forceinline__ Frag<T> ld_frag_tr(const T* base, int ld);
+
+template <>
+__device__ __forceinline__ Frag<bf16_t> ld_frag_tr<bf16_t>(const bf16_t* base, int ld) {
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  const int l = lane_id(), g = l >> 4, j = l & 15;
+  const bf16_t* p = base + (8 * g + (j >> 2)) * ld + 4 * (j & 3);
+  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p));
+  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 4 * ld));
+  Frag<bf16_t> f;
+  f.v = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return f;
+}
+
+template <>
+__device__ __forceinline__ Frag<float> ld_frag_tr<float>(const float* base, int ld) {
+  const int l = lane_id(), g = l >> 4, m = l & 15;
+  Frag<float> f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    f.lo[e] = base[(8 * g + e) * ld + m];
+    f.hi[e] = base[(8 * g + 4 + e) * ld + m];
+  }
+  return f;
+}
+
+// B fragment of the 16-column tile whose column 0 is all ones (the rest zero):
+// acc += A * ones gives the row sums of A in column 0.
+template <typename T>
+__device__ __forceinline__ Frag<T> ones_col_frag() {
+  const T one = static_cast<T>((lane_id() & 15) == 0 ? 1.f : 0.f);
+  Frag<T> f;
+  if constexpr (sizeof(T) == 2) {
+    f.v = bf16x8{one, one, one, one, one, one, one, one};
+  } else {
+    f.lo = f32x4{one, one, one, one};
+    f.hi = f.lo;
+  }
+  return f;
+}
+
+// Store the four accumulator values of this lane (rows 4g..4g+3 of the tile,
+// one column) as four consecutive elements of row `col` of a row-major LDS
+// array: the transposed tile, written with one 8- or 16-byte store.
+template <typename T>
+__device__ __forceinline__ void store4(T* p, float x0, float x1, float x2, float x3) {
+  if constexpr (sizeof(T) == 2) {
+    *reinterpret_cast<bf16x4*>(p) = bf16x4{static_cast<bf16_t>(x0), static_cast<bf16_t>(x1),
+                                           static_cast<bf16_t>(x2), static_cast<bf16_t>(x3)};
+  } else {
+    *reinterpret_cast<f32x4*>(p) = f32x4{x0, x1, x2, x3};
+  }
+}
+
 __device__ __forceinline__ void mma(f32x4& acc, const Frag<bf16_t>& a, const Frag<bf16_t>& b) {
   acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, acc, 0, 0, 0);
 }

@@ -109,18 +109,18 @@ template <typename T, int DK, int BV>
 __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
   constexpr int C = kChunk;
   constexpr int P = Pad<T>::value;
-  constexpr int LDQ = DK + P, LDT = C + P;
-  constexpr int NTC = DK / 16;
-  constexpr int NPW = BV * DK / (16 * 16 * 4);
-  constexpr int NTN = BV / 16;
-  static_assert(NPW >= 1, "tile split");
+  constexpr int LDQ = DK + P, LDV = BV + P, LDA = C + P;
+  constexpr int NTV = BV / 16;
+  constexpr int RPW = (DK / 16) / 4;  // key row tiles of S^T per wave
+  constexpr int NPW = RPW * NTV;
+  static_assert(RPW >= 1, "tile split");
 
   __shared__ __align__(16) T sQ[C * LDQ];
   __shared__ __align__(16) T sK[C * LDQ];
-  __shared__ __align__(16) T sKdT[DK * LDT];
-  __shared__ __align__(16) T sS[BV * LDQ];
-  __shared__ __align__(16) T sUT[BV * LDT];
-  __shared__ __align__(16) T sA[C * LDT];
+  __shared__ __align__(16) T sS[BV * LDQ];   // S_r slice as [v][c]
+  __shared__ __align__(16) T sU[C * LDV];    // U[j][v]
+  __shared__ __align__(16) T sUd[C * LDV];   // U[j][v] e^{gamma_C - gamma_j}
+  __shared__ __align__(16) T sA[C * LDA];    // (q_i . k_j) e^{gamma_i - gamma_j}, j <= i
   __shared__ float sGam[C];
 
   const int nvt = a.dv / BV;
@@ -137,23 +137,25 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
   T* o = static_cast<T*>(a.o);
   const size_t gstride = (size_t)a.H * DK;
 
+  // state, transposed: tile u holds S[v][c] at c = 16 (w RPW + u / NTV) + 4 g4 + r,
+  // v = v0 + 16 (u % NTV) + c16
   f32x4 S[NPW];
 #pragma unroll
   for (int u = 0; u < NPW; ++u) {
-    const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
+    const int tr = w * RPW + u / NTV, tv = u % NTV;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int vv = v0 + 16 * tv + 4 * g4 + r, c = 16 * tc + c16;
+      const int c = 16 * tr + 4 * g4 + r, vv = v0 + 16 * tv + c16;
       S[u][r] = a.S0 ? a.S0[((size_t)bh * a.dv + vv) * DK + c] : 0.f;
     }
   }
 
   // next chunk in flight: q, k tiles, log-decays (wave 0), and this wave's
-  // W fragments and Ut entries
+  // W fragments (rows 16w..16w+15) and Ut entries (transposed tiles of U)
   ChunkTile<T, DK> rq, rk;
   RowScalar rla;
   Frag<T> rW[DK / 32];
-  float rU[NTN][4];
+  f32x4 rU[NTV];
   auto prefetch_qk = [&](int ci) {
     const int r0 = ci * C;
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
@@ -165,11 +167,9 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
     const T* Wc = Wg + ((size_t)bh * N + ci) * C * DK + (size_t)16 * w * DK;
 #pragma unroll
     for (int kk = 0; kk < DK / 32; ++kk) rW[kk] = ld_frag_global(Wc + 32 * kk, (size_t)DK);
-    const float* Uc = a.Ut + ((size_t)bh * N + ci) * C * a.dv;
+    const float* Uc = a.Ut + (((size_t)bh * N + ci) * C + 16 * w + c16) * a.dv + v0 + 4 * g4;
 #pragma unroll
-    for (int tn = 0; tn < NTN; ++tn)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) rU[tn][r] = Uc[(size_t)(16 * w + 4 * g4 + r) * a.dv + v0 + 16 * tn + c16];
+    for (int tv = 0; tv < NTV; ++tv) rU[tv] = *reinterpret_cast<const f32x4*>(Uc + 16 * tv);
   };
   if (N > 0) {
     prefetch_qk(0);
@@ -191,84 +191,90 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
       }
       sGam[tid] = x;
     }
-    // entering state slice as the B^T operand [v][c]
 #pragma unroll
     for (int u = 0; u < NPW; ++u) {
-      const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) sS[(16 * tv + 4 * g4 + r) * LDQ + 16 * tc + c16] = to<T>(S[u][r]);
+      const int tr = w * RPW + u / NTV, tv = u % NTV;
+      store4(sS + (16 * tv + c16) * LDQ + 16 * tr + 4 * g4, S[u][0], S[u][1], S[u][2], S[u][3]);
     }
     __syncthreads();  // (B)
-    const float gC = sGam[C - 1];
-    // K scaled by e^{gamma_C - gamma_j}, transposed for the state update (lane = row j)
-    {
-      const int j = ChunkTile<T, DK>::row();
-      const float sc = __expf(gC - sGam[j]);
-#pragma unroll
-      for (int u = 0; u < ChunkTile<T, DK>::NV; ++u)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) sKdT[(ChunkTile<T, DK>::col(u) + e) * LDT + j] = to<T>(f32(rk.v[u][e]) * sc);
-    }
     if (ci + 1 < N) prefetch_qk(ci + 1);
-    // U = Ut - W S_r^T for rows of stripe w
+    const float gC = sGam[C - 1];
+    {
+      // U^T tiles for rows i of stripe w: U[i][v] = Ut[i][v] - (W S_r^T)[i][v]
+      const int i = 16 * w + c16;
+      const float ud = __expf(gC - sGam[i]);
 #pragma unroll
-    for (int tn = 0; tn < NTN; ++tn) {
-      f32x4 acc = zero4();
+      for (int tv = 0; tv < NTV; ++tv) {
+        f32x4 acc = zero4();
 #pragma unroll
-      for (int kk = 0; kk < DK / 32; ++kk) mma(acc, rW[kk], ld_frag(sS + 16 * tn * LDQ + 32 * kk, LDQ));
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * g4 + r, vv = 16 * tn + c16;
-        sUT[vv * LDT + i] = to<T>(rU[tn][r] - acc[r]);
+        for (int kk = 0; kk < DK / 32; ++kk) mma(acc, ld_frag(sS + 16 * tv * LDQ + 32 * kk, LDQ), rW[kk]);
+        const float u0 = rU[tv][0] - acc[0], u1 = rU[tv][1] - acc[1];
+        const float u2 = rU[tv][2] - acc[2], u3 = rU[tv][3] - acc[3];
+        const int off = i * LDV + 16 * tv + 4 * g4;
+        store4(sU + off, u0, u1, u2, u3);
+        store4(sUd + off, u0 * ud, u1 * ud, u2 * ud, u3 * ud);
       }
-    }
-    if (ci + 1 < N) prefetch_wu(ci + 1);
-    // intra-chunk block (q_i . k_j) e^{gamma_i - gamma_j}, j <= i
+      if (ci + 1 < N) prefetch_wu(ci + 1);
+      // intra block, transposed tiles: (k_j . q_i) e^{gamma_i - gamma_j}, stored as A[i][j]
+      const float gi = sGam[i];
 #pragma unroll
-    for (int J = 0; J < 4; ++J) {
-      f32x4 acc = zero4();
-      if (J <= w) tile_mma<T, DK>(acc, sQ + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+      for (int J = 0; J < 4; ++J) {
+        f32x4 sc = zero4();
+        if (J <= w) tile_mma<T, DK>(sc, sK + 16 * J * LDQ, LDQ, sQ + 16 * w * LDQ, LDQ);
+        float x[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * g4 + r, j = 16 * J + c16;
-        sA[i * LDT + j] = to<T>((J <= w && j <= i) ? acc[r] * __expf(sGam[i] - sGam[j]) : 0.f);
+        for (int r = 0; r < 4; ++r) {
+          const int j = 16 * J + 4 * g4 + r;
+          x[r] = (J <= w && j <= i) ? sc[r] * __expf(gi - sGam[j]) : 0.f;
+        }
+        store4(sA + i * LDA + 16 * J + 4 * g4, x[0], x[1], x[2], x[3]);
       }
     }
     __syncthreads();  // (C)
 
     // o = e^{gamma} (Q S_r^T) + A U
 #pragma unroll
-    for (int tn = 0; tn < NTN; ++tn) {
+    for (int tv = 0; tv < NTV; ++tv) {
       f32x4 a1 = zero4(), a2 = zero4();
-      tile_mma<T, DK>(a1, sQ + 16 * w * LDQ, LDQ, sS + 16 * tn * LDQ, LDQ);
-      tile_mma<T, C>(a2, sA + 16 * w * LDT, LDT, sUT + 16 * tn * LDT, LDT);
+      tile_mma<T, DK>(a1, sQ + 16 * w * LDQ, LDQ, sS + 16 * tv * LDQ, LDQ);
+#pragma unroll
+      for (int k0 = 0; k0 < C; k0 += 32)
+        if (k0 <= 16 * w) mma(a2, ld_frag(sA + 16 * w * LDA + k0, LDA), ld_frag_tr(sU + k0 * LDV + 16 * tv, LDV));
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int i = 16 * w + 4 * g4 + r;
         if (i < nrow)
-          o[tok_off(b, r0 + i, h, a.T, a.H, a.dv) + v0 + 16 * tn + c16] =
+          o[tok_off(b, r0 + i, h, a.T, a.H, a.dv) + v0 + 16 * tv + c16] =
               to<T>(a.scale * (__expf(sGam[i]) * a1[r] + a2[r]));
       }
     }
-    // S_{r+1} = e^{gamma_C} S_r + U^T Kd
+    // S^T <- e^{gamma_C} S^T + K^T Ud
     const float eC = __expf(gC);
 #pragma unroll
-    for (int u = 0; u < NPW; ++u) {
-      const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
-      f32x4 d = zero4();
-      tile_mma<T, C>(d, sUT + 16 * tv * LDT, LDT, sKdT + 16 * tc * LDT, LDT);
+    for (int u = 0; u < NPW; ++u)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) S[u][r] = eC * S[u][r] + d[r];
+      for (int r = 0; r < 4; ++r) S[u][r] *= eC;
+#pragma unroll
+    for (int k0 = 0; k0 < C; k0 += 32) {
+      Frag<T> fb[NTV];
+#pragma unroll
+      for (int tv = 0; tv < NTV; ++tv) fb[tv] = ld_frag_tr(sUd + k0 * LDV + 16 * tv, LDV);
+#pragma unroll
+      for (int rr = 0; rr < RPW; ++rr) {
+        const Frag<T> fa = ld_frag_tr(sK + k0 * LDQ + 16 * (w * RPW + rr), LDQ);
+#pragma unroll
+        for (int tv = 0; tv < NTV; ++tv) mma(S[rr * NTV + tv], fa, fb[tv]);
+      }
     }
   }
 
   if (a.ST) {
 #pragma unroll
     for (int u = 0; u < NPW; ++u) {
-      const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
+      const int tr = w * RPW + u / NTV, tv = u % NTV;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int vv = v0 + 16 * tv + 4 * g4 + r, c = 16 * tc + c16;
+        const int c = 16 * tr + 4 * g4 + r, vv = v0 + 16 * tv + c16;
         a.ST[((size_t)bh * a.dv + vv) * DK + c] = S[u][r];
       }
     }

@@ -25,24 +25,23 @@ template <typename T, typename TG, int DK, int BV>
 __global__ __launch_bounds__(kThreads, 1) void gla_fwd_kernel(const GlaArgs a) {
   constexpr int C = kChunk;
   constexpr int P = Pad<T>::value;
-  constexpr int LDQ = DK + P, LDT = C + P, LDG = DK + 1;
-  constexpr int NTC = DK / 16;
-  constexpr int NPW = BV * DK / (16 * 16 * 4);
-  static_assert(NPW >= 1, "tile split");
-  static_assert(DK <= kThreads, "one thread per key channel in the scan");
+  constexpr int LDQ = DK + P, LDV = BV + P, LDA = C + P, LDG = DK + 1;
+  constexpr int NTV = BV / 16;                 // value tiles of the slice
+  constexpr int RPW = (DK / 16) / 4;           // key row tiles of S^T per wave
+  constexpr int NPW = RPW * NTV;
+  static_assert(RPW >= 1 && DK <= kThreads, "tile split");
 
-  __shared__ __align__(16) T sQt[C * LDQ];
-  __shared__ __align__(16) T sKt[C * LDQ];
-  __shared__ __align__(16) T sKtT[DK * LDT];
-  __shared__ __align__(16) T sVT[BV * LDT];
-  __shared__ __align__(16) T sS[BV * LDQ];
-  // sG (gates, then their inclusive prefix b) is dead once Qt/Kt are built, so
-  // the intra-chunk block sA reuses its bytes
-  constexpr int kGBytes = C * LDG * 4, kABytes = C * LDT * (int)sizeof(T);
+  __shared__ __align__(16) T sQt[C * LDQ];   // q e^{b - b_m}
+  __shared__ __align__(16) T sKt[C * LDQ];   // k e^{b_m - b}
+  __shared__ __align__(16) T sV[C * LDV];    // value slice, row-major
+  __shared__ __align__(16) T sS[BV * LDQ];   // S diag(e^{b_m}) as B^T operand [v][c]
+  // sG (gates, then their prefix b) is dead once Qt/Kt are built; the intra
+  // block A[i][j] reuses its bytes
+  constexpr int kGBytes = C * LDG * 4, kABytes = C * LDA * (int)sizeof(T);
   __shared__ __align__(16) char sGA[kGBytes > kABytes ? kGBytes : kABytes];
   float* sG = reinterpret_cast<float*>(sGA);
   T* sA = reinterpret_cast<T*>(sGA);
-  __shared__ float sBm[DK], sDec[DK], sDecm[DK];
+  __shared__ __align__(16) float sBm[DK], sDecm[DK];
 
   const int nvt = a.dv / BV;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
@@ -57,14 +56,17 @@ __global__ __launch_bounds__(kThreads, 1) void gla_fwd_kernel(const GlaArgs a) {
   const TG* gate = static_cast<const TG*>(a.g);
   T* o = static_cast<T*>(a.o);
   const size_t gstride = (size_t)a.H * DK;
+  const int N = (a.T + C - 1) / C;
 
+  // state, transposed: tile u holds S[v][c] at c = 16 (w RPW + u / NTV) + 4 g4 + r,
+  // v = v0 + 16 (u % NTV) + c16
   f32x4 S[NPW];
 #pragma unroll
   for (int u = 0; u < NPW; ++u) {
-    const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
+    const int tr = w * RPW + u / NTV, tv = u % NTV;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int vv = v0 + 16 * tv + 4 * g4 + r, c = 16 * tc + c16;
+      const int c = 16 * tr + 4 * g4 + r, vv = v0 + 16 * tv + c16;
       S[u][r] = a.S0 ? a.S0[((size_t)bh * a.dv + vv) * DK + c] : 0.f;
     }
   }
@@ -81,11 +83,12 @@ __global__ __launch_bounds__(kThreads, 1) void gla_fwd_kernel(const GlaArgs a) {
   };
   if (a.T > 0) prefetch(0);
 
-  for (int r0 = 0; r0 < a.T; r0 += C) {
+  for (int ci = 0; ci < N; ++ci) {
+    const int r0 = ci * C;
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
     __syncthreads();  // (A) previous chunk's LDS readers are done
     rg.store_f32(sG, LDG);
-    rv.store_t(sVT, LDT);
+    rv.store(sV, LDV);
     __syncthreads();  // (B)
     // per key channel: inclusive log-decay prefix b_j (rows >= nrow have g = 0)
     if (tid < DK) {
@@ -98,7 +101,6 @@ __global__ __launch_bounds__(kThreads, 1) void gla_fwd_kernel(const GlaArgs a) {
       for (int j = 0; j < C; ++j) sG[j * LDG + tid] = x[j];
       const float bm = x[C / 2 - 1], bC = x[C - 1];
       sBm[tid] = __expf(bm);
-      sDec[tid] = __expf(bC);
       sDecm[tid] = __expf(bC - bm);
     }
     __syncthreads();  // (C)
@@ -108,86 +110,95 @@ __global__ __launch_bounds__(kThreads, 1) void gla_fwd_kernel(const GlaArgs a) {
 #pragma unroll
       for (int u = 0; u < ChunkTile<T, DK>::NV; ++u) {
         const int c0 = ChunkTile<T, DK>::col(u);
+        const auto xq = rq.get(u), xk = rk.get(u);
         typename ChunkTile<T, DK>::vec_t qo, ko;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const float d = sG[j * LDG + c0 + e] - sG[(C / 2 - 1) * LDG + c0 + e];
-          qo[e] = to<T>(f32(rq.v[u][e]) * __expf(d));
-          ko[e] = to<T>(f32(rk.v[u][e]) * __expf(-d));
+          qo[e] = to<T>(f32(xq[e]) * __expf(d));
+          ko[e] = to<T>(f32(xk[e]) * __expf(-d));
         }
         *reinterpret_cast<typename ChunkTile<T, DK>::vec_t*>(sQt + j * LDQ + c0) = qo;
         *reinterpret_cast<typename ChunkTile<T, DK>::vec_t*>(sKt + j * LDQ + c0) = ko;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) sKtT[(c0 + e) * LDT + j] = ko[e];
       }
     }
-    if (r0 + C < a.T) prefetch(r0 + C);  // registers are free: next chunk's loads overlap the math
-    // entering state, rescaled to the reference point: S diag(e^{b_m});
-    // the training pass also keeps S_r itself for the backward
-    T* st_out = a.states ? static_cast<T*>(a.states) +
-                               (((size_t)bh * ((a.T + C - 1) / C) + r0 / C) * a.dv + v0) * DK
-                         : nullptr;
+    if (ci + 1 < N) prefetch(r0 + C);  // registers are free: next chunk's loads overlap the math
+    // entering state rescaled to the reference point, S diag(e^{b_m}), as [v][c]
+    // (training: S_r itself is kept for the backward)
+    T* st_out = a.states ? static_cast<T*>(a.states) + (((size_t)bh * N + ci) * a.dv + v0) * DK : nullptr;
 #pragma unroll
     for (int u = 0; u < NPW; ++u) {
-      const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int vv = 16 * tv + 4 * g4 + r, c = 16 * tc + c16;
-        sS[vv * LDQ + c] = to<T>(S[u][r] * sBm[c]);
-        if (st_out) st_out[(size_t)vv * DK + c] = to<T>(S[u][r]);
-      }
+      const int tr = w * RPW + u / NTV, tv = u % NTV;
+      const int c = 16 * tr + 4 * g4, vv = 16 * tv + c16;
+      const f32x4 bm = *reinterpret_cast<const f32x4*>(sBm + c);
+      store4(sS + vv * LDQ + c, S[u][0] * bm[0], S[u][1] * bm[1], S[u][2] * bm[2], S[u][3] * bm[3]);
+      if (st_out) store4(st_out + (size_t)vv * DK + c, S[u][0], S[u][1], S[u][2], S[u][3]);
     }
-    __syncthreads();  // (D)
-    // intra-chunk causal block Qt Kt^T (diagonal included)
+    __syncthreads();  // (D) sG dead, sQt/sKt/sS ready
+    // intra block, transposed tiles: k_j e^{b_m-b_j} . q_i e^{b_i-b_m}, stored as A[i][j] (j <= i)
     {
-      f32x4 sc[4];
+      const int i = 16 * w + c16;
 #pragma unroll
       for (int J = 0; J < 4; ++J) {
-        sc[J] = zero4();
-        if (J <= w) tile_mma<T, DK>(sc[J], sQt + 16 * w * LDQ, LDQ, sKt + 16 * J * LDQ, LDQ);
+        f32x4 sc = zero4();
+        if (J <= w) tile_mma<T, DK>(sc, sKt + 16 * J * LDQ, LDQ, sQt + 16 * w * LDQ, LDQ);
+        float x[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) x[r] = (J <= w && 16 * J + 4 * g4 + r <= i) ? sc[r] : 0.f;
+        store4(sA + i * LDA + 16 * J + 4 * g4, x[0], x[1], x[2], x[3]);
       }
-#pragma unroll
-      for (int J = 0; J < 4; ++J)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int i = 16 * w + 4 * g4 + r, j = 16 * J + c16;
-          sA[i * LDT + j] = to<T>((J <= w && j <= i) ? sc[J][r] : 0.f);
-        }
     }
     __syncthreads();  // (E)
 
     // o = Qt (S diag e^{b_m})^T + A V   for rows of stripe w, columns of the slice
 #pragma unroll
-    for (int tn = 0; tn < BV / 16; ++tn) {
+    for (int tv = 0; tv < NTV; ++tv) {
       f32x4 acc = zero4();
-      tile_mma<T, DK>(acc, sQt + 16 * w * LDQ, LDQ, sS + 16 * tn * LDQ, LDQ);
-      tile_mma<T, C>(acc, sA + 16 * w * LDT, LDT, sVT + 16 * tn * LDT, LDT);
+      tile_mma<T, DK>(acc, sQt + 16 * w * LDQ, LDQ, sS + 16 * tv * LDQ, LDQ);
+#pragma unroll
+      for (int k0 = 0; k0 < C; k0 += 32)
+        if (k0 <= 16 * w) mma(acc, ld_frag(sA + 16 * w * LDA + k0, LDA), ld_frag_tr(sV + k0 * LDV + 16 * tv, LDV));
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int i = 16 * w + 4 * g4 + r;
-        if (i < nrow) o[tok_off(b, r0 + i, h, a.T, a.H, a.dv) + v0 + 16 * tn + c16] = to<T>(a.scale * acc[r]);
+        if (i < nrow) o[tok_off(b, r0 + i, h, a.T, a.H, a.dv) + v0 + 16 * tv + c16] = to<T>(a.scale * acc[r]);
       }
     }
-    // S <- S diag(e^{b_C}) + (V^T Kt) diag(e^{b_C - b_m})
+    // S^T <- diag(e^{b_C}) S^T + diag(e^{b_C - b_m}) Kt^T V
 #pragma unroll
-    for (int u = 0; u < NPW; ++u) {
-      const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
-      f32x4 d = zero4();
-      tile_mma<T, C>(d, sVT + 16 * tv * LDT, LDT, sKtT + 16 * tc * LDT, LDT);
-      const int c = 16 * tc + c16;
-      const float dec = sDec[c], decm = sDecm[c];
+    for (int k0 = 0; k0 < C; k0 += 32) {
+      Frag<T> fb[NTV];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) S[u][r] = S[u][r] * dec + d[r] * decm;
+      for (int tv = 0; tv < NTV; ++tv) fb[tv] = ld_frag_tr(sV + k0 * LDV + 16 * tv, LDV);
+#pragma unroll
+      for (int rr = 0; rr < RPW; ++rr) {
+        const Frag<T> fa = ld_frag_tr(sKt + k0 * LDQ + 16 * (w * RPW + rr), LDQ);
+#pragma unroll
+        for (int tv = 0; tv < NTV; ++tv) {
+          f32x4& st = S[rr * NTV + tv];
+          if (k0 == 0) {  // (S e^{b_m} + Kt^T V) e^{b_C - b_m} = S e^{b_C} + (Kt^T V) e^{b_C - b_m}
+            const f32x4 bm = *reinterpret_cast<const f32x4*>(sBm + 16 * (w * RPW + rr) + 4 * g4);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) st[r] *= bm[r];
+          }
+          mma(st, fa, fb[tv]);
+          if (k0 + 32 >= C) {
+            const f32x4 decm = *reinterpret_cast<const f32x4*>(sDecm + 16 * (w * RPW + rr) + 4 * g4);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) st[r] *= decm[r];
+          }
+        }
+      }
     }
   }
 
   if (a.ST) {
 #pragma unroll
     for (int u = 0; u < NPW; ++u) {
-      const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
+      const int tr = w * RPW + u / NTV, tv = u % NTV;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int vv = v0 + 16 * tv + 4 * g4 + r, c = 16 * tc + c16;
+        const int c = 16 * tr + 4 * g4 + r, vv = v0 + 16 * tv + c16;
         a.ST[((size_t)bh * a.dv + vv) * DK + c] = S[u][r];
       }
     }
