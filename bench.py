@@ -256,6 +256,9 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip the per-workload figures")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy 5 times (HBM counter "
+                         "calibration for rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
     args = ap.parse_args(argv)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -267,6 +270,15 @@ def main(argv=None):
     import torch
     from paper_2606_01294_amd import ccq, inputs
 
+    if args.copy_calibration:
+        x = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        y = torch.empty_like(x)
+        for _ in range(5):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": x.numel() * 4, "copy_bytes_written": y.numel() * 4,
+                          "launches": 5}))
+        return 0
     ccq.lib()  # fails loudly when libccq.so is missing
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
