@@ -41,18 +41,23 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     if kernel == "clean":
         by = ntok * (3 * dk * io_bytes + 4) + BH * (dk * dk + dk) * 4
         fl = ntok * (4 * dk * dk + 4 * C * dk)
-    elif kernel == "gla_fwd":
-        by = ntok * (2 * dk * io_bytes + dk * gate_bytes + 2 * dv * io_bytes) + BH * dv * dk * 4
-        fl = ntok * (2 * C * (dk + dv) + 4 * dk * dv)
+    elif kernel == "gla_state":     # k, g, v in; chunk-entry states and final state out
+        by = ntok * (dk * io_bytes + dk * gate_bytes + dv * io_bytes + dv * dk * io_bytes // C) \
+            + BH * dv * dk * 4
+        fl = ntok * (2 * dk * dv)
+    elif kernel == "gla_out":       # q_clean, k, g, v, chunk states in; o out
+        by = ntok * (2 * dk * io_bytes + dk * gate_bytes + 2 * dv * io_bytes + dv * dk * io_bytes // C)
+        fl = ntok * (2 * C * dk + 2 * dk * dv + 2 * C * dv)
     elif kernel == "gdn_wy":
         by = ntok * (2 * dk * io_bytes + dv * io_bytes + dv * 4 + 8)
         fl = ntok * (2 * C * dk + C * (dk + dv))
-    elif kernel == "gdn_fwd":
-        by = ntok * (3 * dk * io_bytes + dv * 4 + dv * io_bytes + 4) + BH * dv * dk * 4
-        fl = ntok * (6 * dk * dv + 2 * C * (dk + dv))
-    elif kernel == "gla_fwd_train":   # forward that also writes the chunk-entry states
-        by = ntok * (2 * dk * io_bytes + dk * gate_bytes + 2 * dv * io_bytes + dv * dk * io_bytes // C)
-        fl = ntok * (2 * C * (dk + dv) + 4 * dk * dv)
+    elif kernel == "gdn_state":     # k, W, Ut, log alpha in; chunk states, U, final state out
+        by = ntok * (2 * dk * io_bytes + dv * 4 + 4 + dv * dk * io_bytes // C + dv * io_bytes) \
+            + BH * dv * dk * 4
+        fl = ntok * (4 * dk * dv)
+    elif kernel == "gdn_out":       # q_clean, k, chunk states, U, log alpha in; o out
+        by = ntok * (2 * dk * io_bytes + dv * dk * io_bytes // C + 2 * dv * io_bytes + 4)
+        fl = ntok * (2 * C * dk + 2 * dk * dv + 2 * C * dv)
     elif kernel == "clean_train":     # contraction exporting Sigma q (fp32) and m.q
         by = ntok * (3 * dk * io_bytes + 4 + 4 * dk + 4)
         fl = ntok * (4 * dk * dk + 4 * C * dk)
@@ -77,17 +82,18 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     return by, fl
 
 
-KERNELS = {0: ["clean", "gla_fwd"], 1: ["clean", "gdn_wy", "gdn_fwd"],
-           "train": ["clean_train", "gla_fwd_train", "gla_dstate", "gla_bwd_chunk", "gla_dg",
+KERNELS = {0: ["clean", "gla_state", "gla_out"], 1: ["clean", "gdn_wy", "gdn_state", "gdn_out"],
+           "train": ["clean_train", "gla_state", "gla_out", "gla_dstate", "gla_bwd_chunk", "gla_dg",
                      "clean_dq", "ccq_dk"]}
-KERNEL_SYMBOL = {"clean": "clean_kernel", "gla_fwd": "gla_fwd_kernel", "gdn_wy": "gdn_wy_kernel",
-                 "gdn_fwd": "gdn_fwd_kernel", "clean_train": "clean_kernel",
-                 "gla_fwd_train": "gla_fwd_kernel", "clean_dq": "clean_kernel",
-                 "gla_dstate": "gla_dstate_kernel", "gla_bwd_chunk": "gla_bwd_chunk_kernel",
-                 "gla_dg": "gla_dg_kernel", "ccq_dk": "ccq_dk_kernel"}
-KERNEL_SOURCE = {"clean": "ccq_clean.hip", "gla_fwd": "ccq_gla.hip", "gdn_wy": "ccq_gdn.hip",
-                 "gdn_fwd": "ccq_gdn.hip", "clean_train": "ccq_clean.hip",
-                 "gla_fwd_train": "ccq_gla.hip", "clean_dq": "ccq_clean.hip",
+KERNEL_SYMBOL = {"clean": "clean_kernel", "gla_state": "gla_state_kernel", "gla_out": "gla_out_kernel",
+                 "gdn_wy": "gdn_wy_kernel", "gdn_state": "gdn_state_kernel",
+                 "gdn_out": "gdn_out_kernel", "clean_train": "clean_kernel",
+                 "clean_dq": "clean_kernel", "gla_dstate": "gla_dstate_kernel",
+                 "gla_bwd_chunk": "gla_bwd_chunk_kernel", "gla_dg": "gla_dg_kernel",
+                 "ccq_dk": "ccq_dk_kernel"}
+KERNEL_SOURCE = {"clean": "ccq_clean.hip", "gla_state": "ccq_gla.hip", "gla_out": "ccq_gla.hip",
+                 "gdn_wy": "ccq_gdn.hip", "gdn_state": "ccq_gdn.hip", "gdn_out": "ccq_gdn.hip",
+                 "clean_train": "ccq_clean.hip", "clean_dq": "ccq_clean.hip",
                  "gla_dstate": "ccq_bwd.hip", "gla_bwd_chunk": "ccq_bwd.hip",
                  "gla_dg": "ccq_bwd.hip", "ccq_dk": "ccq_bwd.hip"}
 

@@ -58,21 +58,24 @@ ccq_status check_shape(const ccq_shape* s, ccq_backbone bb) {
 }
 
 struct FwdLayout {
-  size_t qclean = 0, W = 0, Ut = 0, total = 0;
+  size_t qclean = 0, states = 0, W = 0, Ut = 0, U = 0, total = 0;
 };
 
+// q_clean, the chunk-entry states S_r and, for Gated DeltaNet, the WY/UT
+// factors W, Ut and the corrected values U of every chunk.
 FwdLayout fwd_layout(const ccq_shape* s, ccq_backbone bb) {
   FwdLayout L;
   const size_t ntok = (size_t)s->B * s->T * s->H;
   const size_t nchunk = (size_t)s->B * s->H * ((s->T + 63) / 64);
+  const size_t e = esize(s->io_dtype);
   size_t off = 0;
-  L.qclean = off;
-  off += align_up(ntok * s->dk * esize(s->io_dtype));
+  auto take = [&](size_t bytes) { const size_t o = off; off += align_up(bytes); return o; };
+  L.qclean = take(ntok * s->dk * e);
+  L.states = take(nchunk * s->dv * s->dk * e);
   if (bb == CCQ_GDN) {
-    L.W = off;
-    off += align_up(nchunk * 64 * s->dk * esize(s->io_dtype));
-    L.Ut = off;
-    off += align_up(nchunk * 64 * s->dv * sizeof(float));
+    L.W = take(nchunk * 64 * s->dk * e);
+    L.Ut = take(nchunk * 64 * s->dv * sizeof(float));
+    L.U = take(nchunk * 64 * s->dv * e);
   }
   L.total = off;
   return L;
@@ -149,18 +152,22 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   if (traced(st, [&] { return ccq::launch_clean(ca, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
 
   if (bb == CCQ_GLA) {
-    ccq::GlaArgs ga{qclean, k, v, g_or_la, S0, o, ST, nullptr, s->B, s->T, s->H, s->dk, s->dv, s->scale};
     const bool gbf = s->gate_dtype == CCQ_BF16;
-    if (traced(st, [&] { return ccq::launch_gla_fwd(ga, bf, gbf, st); }) != hipSuccess)
-      return CCQ_ERR_HIP;
+    ccq::GlaStateArgs sa{k, v, g_or_la, S0, ST, ws + L.states, s->B, s->T, s->H, s->dk, s->dv};
+    if (traced(st, [&] { return ccq::launch_gla_state(sa, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+    ccq::GlaOutArgs oa{qclean, k, v, g_or_la, ws + L.states, o, s->B, s->T, s->H, s->dk, s->dv, s->scale};
+    if (traced(st, [&] { return ccq::launch_gla_out(oa, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   } else {
     const float* la = static_cast<const float*>(g_or_la);
     ccq::WyArgs wa{k, v, la, beta, ws + L.W, reinterpret_cast<float*>(ws + L.Ut),
                    s->B, s->T, s->H, s->dk, s->dv};
     if (traced(st, [&] { return ccq::launch_gdn_wy(wa, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
-    ccq::GdnArgs da{qclean, k, la, ws + L.W, reinterpret_cast<const float*>(ws + L.Ut), S0, o, ST,
-                    s->B, s->T, s->H, s->dk, s->dv, s->scale};
-    if (traced(st, [&] { return ccq::launch_gdn_fwd(da, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+    ccq::GdnArgs da{k, la, ws + L.W, reinterpret_cast<const float*>(ws + L.Ut), S0, ST,
+                    ws + L.states, ws + L.U, s->B, s->T, s->H, s->dk, s->dv};
+    if (traced(st, [&] { return ccq::launch_gdn_state(da, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+    ccq::GdnOutArgs oa{qclean, k, la, ws + L.states, ws + L.U, o, s->B, s->T, s->H, s->dk, s->dv,
+                       s->scale};
+    if (traced(st, [&] { return ccq::launch_gdn_out(oa, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   }
   return CCQ_OK;
 }
@@ -234,9 +241,12 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
   ccq::CleanArgs c1{q, k, lam, nullptr, nullptr, ws + L.qclean, nullptr, nullptr, nullptr,
                     nullptr, corr, mdq, s->B, s->T, s->H, s->dk, s->centered, 0};
   if (traced(st, [&] { return ccq::launch_clean(c1, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
-  ccq::GlaArgs ga{ws + L.qclean, k, v, g_or_logalpha, nullptr, o, nullptr, ws + L.states,
-                  s->B, s->T, s->H, s->dk, s->dv, s->scale};
-  if (traced(st, [&] { return ccq::launch_gla_fwd(ga, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::GlaStateArgs sa{k, v, g_or_logalpha, nullptr, nullptr, ws + L.states, s->B, s->T, s->H,
+                       s->dk, s->dv};
+  if (traced(st, [&] { return ccq::launch_gla_state(sa, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::GlaOutArgs oa{ws + L.qclean, k, v, g_or_logalpha, ws + L.states, o, s->B, s->T, s->H, s->dk,
+                     s->dv, s->scale};
+  if (traced(st, [&] { return ccq::launch_gla_out(oa, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   // backward: dS scan, chunk gradients, decay gradient, dq, dk
   ccq::DstateArgs da{ws + L.qclean, g_or_logalpha, dO, ws + L.dstates, s->B, s->T, s->H, s->dk,
                      s->dv, s->scale};

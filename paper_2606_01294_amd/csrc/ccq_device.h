@@ -24,6 +24,12 @@ namespace ccq {
 
 constexpr int kChunk = 64;    // chunk length C of the chunkwise form
 constexpr int kThreads = 256; // four 64-wide waves per workgroup
+constexpr int kOutThreads = 512;  // eight waves: chunk-parallel output kernels
+
+// The 16 16x16 tiles of a 64x64 chunk block, lower ones (I >= J) first:
+// tile t < 10 is (I, J) with J <= I, tiles 10..15 are the upper ones.
+__device__ __forceinline__ int intra_tile_row(int t) { return (int)((0x940ffa94ull >> (2 * t)) & 3); }
+__device__ __forceinline__ int intra_tile_col(int t) { return (int)((0xfb9e4910ull >> (2 * t)) & 3); }
 
 template <typename T>
 struct Pad { static constexpr int value = 16 / (int)sizeof(T); };  // 16-byte row padding
@@ -192,17 +198,18 @@ __device__ __forceinline__ size_t tok_off(int b, int t, int h, int T, int H, int
 // instruction and is free of bank conflicts.  Rows >= n are zero.  Loads are
 // branch-free (clamped row, then select), so a whole tile is in flight at
 // once and can be issued a chunk ahead of its use.
-template <typename T, int D>
+template <typename T, int D, int NT = kThreads>
 struct ChunkTile {
   static constexpr int VE = 8;
-  static constexpr int NV = kChunk * D / VE / kThreads;
-  static_assert(NV >= 1 && kChunk * D % (VE * kThreads) == 0, "tile split");
+  static constexpr int NW = NT / 64;  // waves sharing the tile
+  static constexpr int NV = kChunk * D / VE / NT;
+  static_assert(NV >= 1 && kChunk * D % (VE * NT) == 0, "tile split");
   typedef T vec_t __attribute__((ext_vector_type(VE)));
   vec_t v[NV];
   bool ok;  // this lane's row lies inside the sequence
 
   __device__ __forceinline__ static int row() { return threadIdx.x & 63; }
-  __device__ __forceinline__ static int col(int u) { return ((threadIdx.x >> 6) + 4 * u) * VE; }
+  __device__ __forceinline__ static int col(int u) { return ((threadIdx.x >> 6) + NW * u) * VE; }
 
   // Issue the loads of rows [0, n) of the chunk at src (row pitch gstride
   // elements), n >= 1.  Rows >= n read row n-1 and are zeroed at use, so

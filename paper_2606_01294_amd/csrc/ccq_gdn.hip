@@ -15,8 +15,10 @@
 //   S_{r+1} = e^{gamma_C} S_r + U^T diag(e^{gamma_C - gamma}) K.
 //
 // gdn_wy_kernel computes W (io dtype) and Ut (fp32) for every chunk in
-// parallel; gdn_fwd_kernel walks the chunks of one head sequentially, owning a
-// BV-row slice of S (rows of S evolve independently under this write too).
+// parallel; gdn_state_kernel walks the chunks of one head sequentially, owning
+// a BV-row slice of S (rows of S evolve independently under this write too),
+// and stores S_r and U for every chunk; gdn_out_kernel then forms the outputs
+// of all chunks in parallel.
 #include "ccq_device.h"
 #include "ccq_kernels.h"
 
@@ -105,22 +107,21 @@ __global__ __launch_bounds__(kThreads) void gdn_wy_kernel(const WyArgs a) {
   }
 }
 
+// State recurrence over the chunks of one head for a BV-row slice of S:
+//   S_r -> states;  U = Ut - W S_r^T -> U;  S_{r+1} = e^{gamma_C} S_r + U^T diag(e^{gamma_C - gamma}) K.
 template <typename T, int DK, int BV>
-__global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
+__global__ __launch_bounds__(kThreads, 1) void gdn_state_kernel(const GdnArgs a) {
   constexpr int C = kChunk;
   constexpr int P = Pad<T>::value;
-  constexpr int LDQ = DK + P, LDV = BV + P, LDA = C + P;
+  constexpr int LDQ = DK + P, LDV = BV + P;
   constexpr int NTV = BV / 16;
   constexpr int RPW = (DK / 16) / 4;  // key row tiles of S^T per wave
   constexpr int NPW = RPW * NTV;
   static_assert(RPW >= 1, "tile split");
 
-  __shared__ __align__(16) T sQ[C * LDQ];
   __shared__ __align__(16) T sK[C * LDQ];
   __shared__ __align__(16) T sS[BV * LDQ];   // S_r slice as [v][c]
-  __shared__ __align__(16) T sU[C * LDV];    // U[j][v]
   __shared__ __align__(16) T sUd[C * LDV];   // U[j][v] e^{gamma_C - gamma_j}
-  __shared__ __align__(16) T sA[C * LDA];    // (q_i . k_j) e^{gamma_i - gamma_j}, j <= i
   __shared__ float sGam[C];
 
   const int nvt = a.dv / BV;
@@ -131,10 +132,8 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
   const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
-  const T* qc = static_cast<const T*>(a.qc);
   const T* k = static_cast<const T*>(a.k);
   const T* Wg = static_cast<const T*>(a.W);
-  T* o = static_cast<T*>(a.o);
   const size_t gstride = (size_t)a.H * DK;
 
   // state, transposed: tile u holds S[v][c] at c = 16 (w RPW + u / NTV) + 4 g4 + r,
@@ -150,16 +149,13 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
     }
   }
 
-  // next chunk in flight: q, k tiles, log-decays (wave 0), and this wave's
-  // W fragments (rows 16w..16w+15) and Ut entries (transposed tiles of U)
-  ChunkTile<T, DK> rq, rk;
+  ChunkTile<T, DK> rk;
   RowScalar rla;
   Frag<T> rW[DK / 32];
   f32x4 rU[NTV];
-  auto prefetch_qk = [&](int ci) {
+  auto prefetch_k = [&](int ci) {
     const int r0 = ci * C;
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-    rq.load(qc + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
     rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
     if (tid < C) rla.load(a.logalpha + ((size_t)b * a.T + r0) * a.H + h, (size_t)a.H, tid, nrow);
   };
@@ -172,15 +168,12 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
     for (int tv = 0; tv < NTV; ++tv) rU[tv] = *reinterpret_cast<const f32x4*>(Uc + 16 * tv);
   };
   if (N > 0) {
-    prefetch_qk(0);
+    prefetch_k(0);
     prefetch_wu(0);
   }
 
   for (int ci = 0; ci < N; ++ci) {
-    const int r0 = ci * C;
-    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
     __syncthreads();  // (A) previous chunk's LDS readers are done
-    rq.store(sQ, LDQ);
     rk.store(sK, LDQ);
     if (tid < C) {  // inclusive prefix of log alpha over the chunk (wave 0)
       float x = rla.get();
@@ -191,18 +184,24 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
       }
       sGam[tid] = x;
     }
+    {
+      T* st_out = static_cast<T*>(a.states) + (((size_t)bh * N + ci) * a.dv + v0) * DK;
 #pragma unroll
-    for (int u = 0; u < NPW; ++u) {
-      const int tr = w * RPW + u / NTV, tv = u % NTV;
-      store4(sS + (16 * tv + c16) * LDQ + 16 * tr + 4 * g4, S[u][0], S[u][1], S[u][2], S[u][3]);
+      for (int u = 0; u < NPW; ++u) {
+        const int tr = w * RPW + u / NTV, tv = u % NTV;
+        const int off = (16 * tv + c16) * LDQ + 16 * tr + 4 * g4;
+        store4(sS + off, S[u][0], S[u][1], S[u][2], S[u][3]);
+        store4(st_out + (size_t)(16 * tv + c16) * DK + 16 * tr + 4 * g4, S[u][0], S[u][1], S[u][2], S[u][3]);
+      }
     }
     __syncthreads();  // (B)
-    if (ci + 1 < N) prefetch_qk(ci + 1);
+    if (ci + 1 < N) prefetch_k(ci + 1);
     const float gC = sGam[C - 1];
     {
       // U^T tiles for rows i of stripe w: U[i][v] = Ut[i][v] - (W S_r^T)[i][v]
       const int i = 16 * w + c16;
       const float ud = __expf(gC - sGam[i]);
+      T* u_out = static_cast<T*>(a.U) + (((size_t)bh * N + ci) * C + i) * a.dv + v0 + 4 * g4;
 #pragma unroll
       for (int tv = 0; tv < NTV; ++tv) {
         f32x4 acc = zero4();
@@ -210,44 +209,12 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
         for (int kk = 0; kk < DK / 32; ++kk) mma(acc, ld_frag(sS + 16 * tv * LDQ + 32 * kk, LDQ), rW[kk]);
         const float u0 = rU[tv][0] - acc[0], u1 = rU[tv][1] - acc[1];
         const float u2 = rU[tv][2] - acc[2], u3 = rU[tv][3] - acc[3];
-        const int off = i * LDV + 16 * tv + 4 * g4;
-        store4(sU + off, u0, u1, u2, u3);
-        store4(sUd + off, u0 * ud, u1 * ud, u2 * ud, u3 * ud);
+        store4(u_out + 16 * tv, u0, u1, u2, u3);
+        store4(sUd + i * LDV + 16 * tv + 4 * g4, u0 * ud, u1 * ud, u2 * ud, u3 * ud);
       }
       if (ci + 1 < N) prefetch_wu(ci + 1);
-      // intra block, transposed tiles: (k_j . q_i) e^{gamma_i - gamma_j}, stored as A[i][j]
-      const float gi = sGam[i];
-#pragma unroll
-      for (int J = 0; J < 4; ++J) {
-        f32x4 sc = zero4();
-        if (J <= w) tile_mma<T, DK>(sc, sK + 16 * J * LDQ, LDQ, sQ + 16 * w * LDQ, LDQ);
-        float x[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int j = 16 * J + 4 * g4 + r;
-          x[r] = (J <= w && j <= i) ? sc[r] * __expf(gi - sGam[j]) : 0.f;
-        }
-        store4(sA + i * LDA + 16 * J + 4 * g4, x[0], x[1], x[2], x[3]);
-      }
     }
     __syncthreads();  // (C)
-
-    // o = e^{gamma} (Q S_r^T) + A U
-#pragma unroll
-    for (int tv = 0; tv < NTV; ++tv) {
-      f32x4 a1 = zero4(), a2 = zero4();
-      tile_mma<T, DK>(a1, sQ + 16 * w * LDQ, LDQ, sS + 16 * tv * LDQ, LDQ);
-#pragma unroll
-      for (int k0 = 0; k0 < C; k0 += 32)
-        if (k0 <= 16 * w) mma(a2, ld_frag(sA + 16 * w * LDA + k0, LDA), ld_frag_tr(sU + k0 * LDV + 16 * tv, LDV));
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * g4 + r;
-        if (i < nrow)
-          o[tok_off(b, r0 + i, h, a.T, a.H, a.dv) + v0 + 16 * tv + c16] =
-              to<T>(a.scale * (__expf(sGam[i]) * a1[r] + a2[r]));
-      }
-    }
     // S^T <- e^{gamma_C} S^T + K^T Ud
     const float eC = __expf(gC);
 #pragma unroll
@@ -281,6 +248,102 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_fwd_kernel(const GdnArgs a) {
   }
 }
 
+// Output of one chunk for a 64-wide value slice (eight waves):
+//   o_i = scale * (e^{gamma_i} (S_r q_i) + sum_{j<=i} e^{gamma_i - gamma_j} (k_j . q_i) u_j)
+
+template <typename T, int DK>
+__global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArgs a) {
+  constexpr int C = kChunk, BVO = 64;
+  constexpr int P = Pad<T>::value;
+  constexpr int LDQ = DK + P, LDV = BVO + P, LDA = C + P;
+
+  __shared__ __align__(16) T sQ[C * LDQ];
+  __shared__ __align__(16) T sK[C * LDQ];
+  __shared__ __align__(16) T sS[BVO * LDQ];  // S_r rows v0.. as [v][c]
+  __shared__ __align__(16) T sU[C * LDV];
+  __shared__ __align__(16) T sA[C * LDA];
+  __shared__ float sGam[C];
+
+  const int nvt = a.dv / BVO;
+  const int N = (a.T + C - 1) / C;
+  const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int vt = lb % nvt, ci = (lb / nvt) % N, bh = lb / (nvt * N);
+  const int v0 = vt * BVO;
+  const int b = bh / a.H, h = bh % a.H;
+  const int r0 = ci * C;
+  const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+  const int tid = threadIdx.x, w = tid >> 6, l = lane_id();
+  const int g4 = l >> 4, c16 = l & 15;
+  const size_t gstride = (size_t)a.H * DK;
+  {
+    ChunkTile<T, DK, kOutThreads> rq, rk, rs;
+    ChunkTile<T, BVO, kOutThreads> ru;
+    rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+    rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+    rs.load(static_cast<const T*>(a.states) + (((size_t)bh * N + ci) * a.dv + v0) * DK, (size_t)DK, C);
+    ru.load(static_cast<const T*>(a.U) + ((size_t)bh * N + ci) * C * a.dv + v0, (size_t)a.dv, C);
+    rq.store(sQ, LDQ);
+    rk.store(sK, LDQ);
+    rs.store(sS, LDQ);
+    ru.store(sU, LDV);
+    if (tid < C) {
+      RowScalar rla;
+      rla.load(a.logalpha + ((size_t)b * a.T + r0) * a.H + h, (size_t)a.H, tid, nrow);
+      float x = rla.get();
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const float y = __shfl_up(x, off);
+        if (tid >= off) x += y;
+      }
+      sGam[tid] = x;
+    }
+  }
+  __syncthreads();
+  // intra block: ten lower tiles (I >= J) round-robin over the waves, six zero tiles
+  {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int t = w + 8 * s;
+      const int I = intra_tile_row(t), J = intra_tile_col(t);
+      const int i = 16 * I + c16;
+      float x[4] = {0.f, 0.f, 0.f, 0.f};
+      if (t < 10) {
+        f32x4 sc = zero4();
+        tile_mma<T, DK>(sc, sK + 16 * J * LDQ, LDQ, sQ + 16 * I * LDQ, LDQ);
+        const float gi = sGam[i];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int j = 16 * J + 4 * g4 + r;
+          x[r] = j <= i ? sc[r] * __expf(gi - sGam[j]) : 0.f;
+        }
+      }
+      store4(sA + i * LDA + 16 * J + 4 * g4, x[0], x[1], x[2], x[3]);
+    }
+  }
+  __syncthreads();
+  // o tiles: stripe w % 4, value tiles 2 (w / 4) and 2 (w / 4) + 1
+  {
+    const int st = w & 3;
+    T* o = static_cast<T*>(a.o);
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int tv = 2 * (w >> 2) + s;
+      f32x4 a1 = zero4(), a2 = zero4();
+      tile_mma<T, DK>(a1, sQ + 16 * st * LDQ, LDQ, sS + 16 * tv * LDQ, LDQ);
+#pragma unroll
+      for (int k0 = 0; k0 < C; k0 += 32)
+        if (k0 <= 16 * st) mma(a2, ld_frag(sA + 16 * st * LDA + k0, LDA), ld_frag_tr(sU + k0 * LDV + 16 * tv, LDV));
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = 16 * st + 4 * g4 + r;
+        if (i < nrow)
+          o[tok_off(b, r0 + i, h, a.T, a.H, a.dv) + v0 + 16 * tv + c16] =
+              to<T>(a.scale * (__expf(sGam[i]) * a1[r] + a2[r]));
+      }
+    }
+  }
+}
+
 namespace {
 template <typename T, int DK>
 hipError_t run_wy(const WyArgs& a, hipStream_t st) {
@@ -291,10 +354,17 @@ hipError_t run_wy(const WyArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 template <typename T, int DK, int BV>
-hipError_t run_gdn(const GdnArgs& a, hipStream_t st) {
+hipError_t run_gdn_state(const GdnArgs& a, hipStream_t st) {
   const int nblk = a.B * a.H * (a.dv / BV);
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((gdn_fwd_kernel<T, DK, BV>), dim3(nblk), dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((gdn_state_kernel<T, DK, BV>), dim3(nblk), dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
+template <typename T, int DK>
+hipError_t run_gdn_out(const GdnOutArgs& a, hipStream_t st) {
+  const int nblk = a.B * a.H * ((a.T + kChunk - 1) / kChunk) * (a.dv / 64);
+  if (nblk == 0) return hipSuccess;
+  hipLaunchKernelGGL((gdn_out_kernel<T, DK>), dim3(nblk), dim3(kOutThreads), 0, st, a);
   return hipGetLastError();
 }
 }  // namespace
@@ -321,17 +391,33 @@ hipError_t launch_gdn_wy(const WyArgs& a, bool is_bf16, hipStream_t st) {
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_gdn_fwd(const GdnArgs& a, bool is_bf16, hipStream_t st) {
+hipError_t launch_gdn_state(const GdnArgs& a, bool is_bf16, hipStream_t st) {
   if (is_bf16) {
     switch (a.dk) {
-      case 64: return run_gdn<bf16_t, 64, 64>(a, st);
-      case 128: return run_gdn<bf16_t, 128, 64>(a, st);
-      case 256: return run_gdn<bf16_t, 256, 32>(a, st);
+      case 64: return run_gdn_state<bf16_t, 64, 64>(a, st);
+      case 128: return run_gdn_state<bf16_t, 128, 64>(a, st);
+      case 256: return run_gdn_state<bf16_t, 256, 32>(a, st);
     }
   } else {
     switch (a.dk) {
-      case 64: return run_gdn<float, 64, 64>(a, st);
-      case 128: return run_gdn<float, 128, 32>(a, st);
+      case 64: return run_gdn_state<float, 64, 64>(a, st);
+      case 128: return run_gdn_state<float, 128, 32>(a, st);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_gdn_out(const GdnOutArgs& a, bool is_bf16, hipStream_t st) {
+  if (is_bf16) {
+    switch (a.dk) {
+      case 64: return run_gdn_out<bf16_t, 64>(a, st);
+      case 128: return run_gdn_out<bf16_t, 128>(a, st);
+      case 256: return run_gdn_out<bf16_t, 256>(a, st);
+    }
+  } else {
+    switch (a.dk) {
+      case 64: return run_gdn_out<float, 64>(a, st);
+      case 128: return run_gdn_out<float, 128>(a, st);
     }
   }
   return hipErrorInvalidValue;

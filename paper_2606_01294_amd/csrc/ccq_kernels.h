@@ -28,16 +28,26 @@ struct CleanArgs {
   int64_t t0;
 };
 
-// GLA chunk forward reading the cleaned queries.
-struct GlaArgs {
-  const void* qc;     // [B,T,H,dk] io (cleaned queries)
+// GLA state recurrence (sequential over chunks) for one 64x64 tile of S:
+// writes the chunk-entry states S_r of every chunk.
+struct GlaStateArgs {
   const void* k;      // [B,T,H,dk] io
   const void* v;      // [B,T,H,dv] io
   const void* g;      // [B,T,H,dk] gate dtype
   const float* S0;    // [B,H,dv,dk] or null
-  void* o;            // [B,T,H,dv] io
   float* ST;          // [B,H,dv,dk] or null
-  void* states;       // chunk-entry states S_r, [B*H, N, dv, dk] io, or null
+  void* states;       // [B*H, N, dv, dk] io
+  int B, T, H, dk, dv;
+};
+
+// GLA output, one workgroup per (chunk, 64-wide value slice).
+struct GlaOutArgs {
+  const void* qc;     // [B,T,H,dk] io (cleaned queries)
+  const void* k;      // [B,T,H,dk] io
+  const void* v;      // [B,T,H,dv] io
+  const void* g;      // [B,T,H,dk] gate dtype
+  const void* states; // [B*H, N, dv, dk] io
+  void* o;            // [B,T,H,dv] io
   int B, T, H, dk, dv;
   float scale;
 };
@@ -53,16 +63,28 @@ struct WyArgs {
   int B, T, H, dk, dv;
 };
 
-// Gated DeltaNet chunk forward (sequential over chunks).
+// Gated DeltaNet state recurrence (sequential over chunks): writes the
+// chunk-entry states S_r and the corrected values U of every chunk.
 struct GdnArgs {
-  const void* qc;        // [B,T,H,dk] io (cleaned queries)
   const void* k;         // [B,T,H,dk] io
   const float* logalpha; // [B,T,H]
   const void* W;         // workspace, as WyArgs
   const float* Ut;       // workspace, as WyArgs
   const float* S0;       // [B,H,dv,dk] or null
-  void* o;               // [B,T,H,dv] io
   float* ST;             // [B,H,dv,dk] or null
+  void* states;          // [B*H, N, dv, dk] io (workspace)
+  void* U;               // [B*H, N, C, dv] io (workspace)
+  int B, T, H, dk, dv;
+};
+
+// Gated DeltaNet output, one workgroup per (chunk, 64-wide value slice).
+struct GdnOutArgs {
+  const void* qc;        // [B,T,H,dk] io (cleaned queries)
+  const void* k;         // [B,T,H,dk] io
+  const float* logalpha; // [B,T,H]
+  const void* states;    // [B*H, N, dv, dk] io
+  const void* U;         // [B*H, N, C, dv] io
+  void* o;               // [B,T,H,dv] io
   int B, T, H, dk, dv;
   float scale;
 };
@@ -121,9 +143,11 @@ struct CcqDkArgs {
 // Each launcher returns hipSuccess or the launch error.  is_bf16 selects the
 // io dtype (bf16 or fp32); shapes are validated by the caller.
 hipError_t launch_clean(const CleanArgs& a, bool is_bf16, hipStream_t st);
-hipError_t launch_gla_fwd(const GlaArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
+hipError_t launch_gla_state(const GlaStateArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
+hipError_t launch_gla_out(const GlaOutArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
 hipError_t launch_gdn_wy(const WyArgs& a, bool is_bf16, hipStream_t st);
-hipError_t launch_gdn_fwd(const GdnArgs& a, bool is_bf16, hipStream_t st);
+hipError_t launch_gdn_state(const GdnArgs& a, bool is_bf16, hipStream_t st);
+hipError_t launch_gdn_out(const GdnOutArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_copy_or_zero(float* dst, const float* src, size_t n, hipStream_t st);
 
 hipError_t launch_gla_dstate(const DstateArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
