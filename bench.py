@@ -30,6 +30,7 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3
 CHUNK = 64
+CLEAN_SEG = 8     # chunks per segment of the query contraction (kCleanSeg)
 
 
 def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
@@ -38,9 +39,26 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     multiply-add, the C x C chunk blocks counted dense."""
     BH, ntok = w.B * w.H, w.B * w.T * w.H
     dk, dv, C = w.dk, w.dv, CHUNK
-    if kernel == "clean":
-        by = ntok * (3 * dk * io_bytes + 4) + BH * (dk * dk + dk) * 4
-        fl = ntok * (4 * dk * dk + 4 * C * dk)
+    NC = -(-w.T // C)
+    NS = -(-NC // CLEAN_SEG)
+    stats = BH * NS * dk * dk               # elements of the segment statistics
+    if kernel == "clean_gram":      # k in; segment Gram (fp32) and chunk key sums out
+        by = ntok * dk * io_bytes + stats * 4 + BH * NC * dk * 4
+        fl = ntok * 2 * dk * dk
+    elif kernel == "clean_msum":    # chunk key sums in; centres and prefixes out
+        by = BH * NC * dk * 8 + BH * NS * dk * 8
+        fl = BH * NC * dk * 2
+    elif kernel == "clean_prefix":  # Gram in (fp32); entry second moments out (io)
+        by = stats * (4 + io_bytes) + BH * NS * dk * 8
+        fl = stats * 6
+    elif kernel in ("clean_out", "clean_out_train", "clean_dq"):
+        # x, k, lam, entry moments, chunk key sums in; x_clean out (+ Sigma x, m.x)
+        by = ntok * (3 * dk * io_bytes + 4) + stats * io_bytes + BH * NC * dk * 4
+        if kernel == "clean_out_train":
+            by += ntok * (4 * dk + 4)
+        elif kernel == "clean_dq":
+            by += ntok * (4 * dk + 4)
+        fl = ntok * (2 * dk * dk + 4 * C * dk)
     elif kernel == "gla_state":     # k, g, v in; chunk-entry states and final state out
         by = ntok * (dk * io_bytes + dk * gate_bytes + dv * io_bytes + dv * dk * io_bytes // C) \
             + BH * dv * dk * 4
@@ -58,12 +76,6 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     elif kernel == "gdn_out":       # q_clean, k, chunk states, U, log alpha in; o out
         by = ntok * (2 * dk * io_bytes + dv * dk * io_bytes // C + 2 * dv * io_bytes + 4)
         fl = ntok * (2 * C * dk + 2 * dk * dv + 2 * C * dv)
-    elif kernel == "clean_train":     # contraction exporting Sigma q (fp32) and m.q
-        by = ntok * (3 * dk * io_bytes + 4 + 4 * dk + 4)
-        fl = ntok * (4 * dk * dk + 4 * C * dk)
-    elif kernel == "clean_dq":        # dq = (I - lam Sigma) dq_clean, fp32 base
-        by = ntok * (2 * dk * io_bytes + 4 * dk + dk * io_bytes + 8)
-        fl = ntok * (4 * dk * dk + 4 * C * dk)
     elif kernel == "gla_dstate":
         by = ntok * (dk * io_bytes + dk * gate_bytes + dv * io_bytes + dv * dk * io_bytes // C)
         fl = ntok * (2 * dk * dv)
@@ -82,20 +94,32 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     return by, fl
 
 
-KERNELS = {0: ["clean", "gla_state", "gla_out"], 1: ["clean", "gdn_wy", "gdn_state", "gdn_out"],
-           "train": ["clean_train", "gla_state", "gla_out", "gla_dstate", "gla_bwd_chunk", "gla_dg",
-                     "clean_dq", "ccq_dk"]}
-KERNEL_SYMBOL = {"clean": "clean_kernel", "gla_state": "gla_state_kernel", "gla_out": "gla_out_kernel",
+CLEAN = ["clean_gram", "clean_msum", "clean_prefix"]
+KERNELS = {0: CLEAN + ["clean_out", "gla_state", "gla_out"],
+           1: CLEAN + ["clean_out", "gdn_wy", "gdn_state", "gdn_out"],
+           "train": CLEAN + ["clean_out_train", "gla_state", "gla_out", "gla_dstate",
+                             "gla_bwd_chunk", "gla_dg", "clean_dq", "ccq_dk"]}
+KERNEL_SYMBOL = {"clean_gram": "clean_gram_kernel", "clean_msum": "clean_msum_kernel",
+                 "clean_prefix": "clean_prefix_kernel", "clean_out": "clean_out_kernel",
+                 "clean_out_train": "clean_out_kernel", "clean_dq": "clean_out_kernel",
+                 "gla_state": "gla_state_kernel", "gla_out": "gla_out_kernel",
                  "gdn_wy": "gdn_wy_kernel", "gdn_state": "gdn_state_kernel",
-                 "gdn_out": "gdn_out_kernel", "clean_train": "clean_kernel",
-                 "clean_dq": "clean_kernel", "gla_dstate": "gla_dstate_kernel",
+                 "gdn_out": "gdn_out_kernel", "gla_dstate": "gla_dstate_kernel",
                  "gla_bwd_chunk": "gla_bwd_chunk_kernel", "gla_dg": "gla_dg_kernel",
                  "ccq_dk": "ccq_dk_kernel"}
-KERNEL_SOURCE = {"clean": "ccq_clean.hip", "gla_state": "ccq_gla.hip", "gla_out": "ccq_gla.hip",
-                 "gdn_wy": "ccq_gdn.hip", "gdn_state": "ccq_gdn.hip", "gdn_out": "ccq_gdn.hip",
-                 "clean_train": "ccq_clean.hip", "clean_dq": "ccq_clean.hip",
-                 "gla_dstate": "ccq_bwd.hip", "gla_bwd_chunk": "ccq_bwd.hip",
-                 "gla_dg": "ccq_bwd.hip", "ccq_dk": "ccq_bwd.hip"}
+
+
+def _source(kernel: str) -> str:
+    if kernel.startswith("clean"):
+        return "ccq_clean.hip"
+    if kernel in ("gla_state", "gla_out"):
+        return "ccq_gla.hip"
+    if kernel.startswith("gdn"):
+        return "ccq_gdn.hip"
+    return "ccq_bwd.hip"
+
+
+KERNEL_SOURCE = {k: _source(k) for k in KERNEL_SYMBOL}
 
 
 def source_sha(kernel: str) -> str:

@@ -57,8 +57,54 @@ ccq_status check_shape(const ccq_shape* s, ccq_backbone bb) {
   return CCQ_OK;
 }
 
+// Workspace of the query contraction: segment and chunk key statistics.
+struct CleanWs {
+  size_t gram = 0, sprime = 0, csum = 0, mr = 0, cs = 0, ms = 0;
+};
+
+template <typename Take>
+CleanWs take_clean_ws(const ccq_shape* s, Take&& take) {
+  const size_t bh = (size_t)s->B * s->H, dk = s->dk;
+  const size_t nc = (s->T + 63) / 64, ns = (nc + ccq::kCleanSeg - 1) / ccq::kCleanSeg;
+  CleanWs c;
+  c.gram = take(bh * ns * dk * dk * 4);
+  c.sprime = take(bh * ns * dk * dk * esize(s->io_dtype));
+  c.csum = take(bh * nc * dk * 4);
+  c.mr = take(bh * nc * dk * 4);
+  c.cs = take(bh * ns * dk * 4);
+  c.ms = take(bh * ns * dk * 4);
+  return c;
+}
+
+ccq::CleanArgs clean_args(const ccq_shape* s, char* ws, const CleanWs& c) {
+  ccq::CleanArgs a{};
+  a.gram = reinterpret_cast<float*>(ws + c.gram);
+  a.sprime = ws + c.sprime;
+  a.csum = reinterpret_cast<float*>(ws + c.csum);
+  a.mr = reinterpret_cast<float*>(ws + c.mr);
+  a.cs = reinterpret_cast<float*>(ws + c.cs);
+  a.ms = reinterpret_cast<float*>(ws + c.ms);
+  a.B = s->B;
+  a.T = s->T;
+  a.H = s->H;
+  a.dk = s->dk;
+  a.centered = s->centered;
+  a.seg = ccq::kCleanSeg;
+  a.t0 = s->t0;
+  return a;
+}
+
+// Key statistics of the contraction (depend on k only).
+hipError_t run_clean_stats(const ccq::CleanArgs& a, bool bf, hipStream_t st) {
+  hipError_t e = traced(st, [&] { return ccq::launch_clean_gram(a, bf, st); });
+  if (e == hipSuccess) e = traced(st, [&] { return ccq::launch_clean_msum(a, st); });
+  if (e == hipSuccess) e = traced(st, [&] { return ccq::launch_clean_prefix(a, bf, st); });
+  return e;
+}
+
 struct FwdLayout {
   size_t qclean = 0, states = 0, W = 0, Ut = 0, U = 0, total = 0;
+  CleanWs clean;
 };
 
 // q_clean, the chunk-entry states S_r and, for Gated DeltaNet, the WY/UT
@@ -72,6 +118,7 @@ FwdLayout fwd_layout(const ccq_shape* s, ccq_backbone bb) {
   auto take = [&](size_t bytes) { const size_t o = off; off += align_up(bytes); return o; };
   L.qclean = take(ntok * s->dk * e);
   L.states = take(nchunk * s->dv * s->dk * e);
+  L.clean = take_clean_ws(s, take);
   if (bb == CCQ_GDN) {
     L.W = take(nchunk * 64 * s->dk * e);
     L.Ut = take(nchunk * 64 * s->dv * sizeof(float));
@@ -83,6 +130,7 @@ FwdLayout fwd_layout(const ccq_shape* s, ccq_backbone bb) {
 
 struct BwdLayout {
   size_t qclean, corr, mdq, mdu, states, dstates, dqc, dqc_io, dkg, db, dbt, total;
+  CleanWs clean;
 };
 
 BwdLayout bwd_layout(const ccq_shape* s) {
@@ -103,6 +151,7 @@ BwdLayout bwd_layout(const ccq_shape* s) {
   L.dkg = take(ntok * s->dk * 4);
   L.db = take(ntok * s->dk * 4);
   L.dbt = take(nchunk * s->dk * 4);
+  L.clean = take_clean_ws(s, take);
   L.total = off;
   return L;
 }
@@ -147,9 +196,18 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   void* qclean = ws + L.qclean;
   trace_begin_call();
 
-  ccq::CleanArgs ca{q, k, lam, C0, mu0, qclean, q_clean_dbg, CT, muT, nullptr, nullptr, nullptr,
-                    s->B, s->T, s->H, s->dk, s->centered, s->t0};
-  if (traced(st, [&] { return ccq::launch_clean(ca, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::CleanArgs ca = clean_args(s, ws, L.clean);
+  ca.q = q;
+  ca.k = k;
+  ca.lam = lam;
+  ca.C0 = C0;
+  ca.mu0 = mu0;
+  ca.qclean = qclean;
+  ca.qclean_dbg = q_clean_dbg;
+  ca.CT = CT;
+  ca.muT = muT;
+  if (run_clean_stats(ca, bf, st) != hipSuccess) return CCQ_ERR_HIP;
+  if (traced(st, [&] { return ccq::launch_clean_out(ca, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
 
   if (bb == CCQ_GLA) {
     const bool gbf = s->gate_dtype == CCQ_BF16;
@@ -238,9 +296,15 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
   trace_begin_call();
 
   // forward: cleaned queries (with Sigma q and m.q kept), then GLA keeping S_r
-  ccq::CleanArgs c1{q, k, lam, nullptr, nullptr, ws + L.qclean, nullptr, nullptr, nullptr,
-                    nullptr, corr, mdq, s->B, s->T, s->H, s->dk, s->centered, 0};
-  if (traced(st, [&] { return ccq::launch_clean(c1, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::CleanArgs c1 = clean_args(s, ws, L.clean);
+  c1.q = q;
+  c1.k = k;
+  c1.lam = lam;
+  c1.qclean = ws + L.qclean;
+  c1.corr = corr;
+  c1.mdot = mdq;
+  if (run_clean_stats(c1, bf, st) != hipSuccess) return CCQ_ERR_HIP;
+  if (traced(st, [&] { return ccq::launch_clean_out(c1, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   ccq::GlaStateArgs sa{k, v, g_or_logalpha, nullptr, nullptr, ws + L.states, s->B, s->T, s->H,
                        s->dk, s->dv};
   if (traced(st, [&] { return ccq::launch_gla_state(sa, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
@@ -257,9 +321,14 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
   if (traced(st, [&] { return ccq::launch_gla_bwd_chunk(ba, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   ccq::DgArgs ga2{db, dbt, dg_or_dlogalpha, s->B, s->T, s->H, s->dk};
   if (traced(st, [&] { return ccq::launch_gla_dg(ga2, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
-  ccq::CleanArgs c2{ws + L.dqc_io, k, lam, nullptr, nullptr, dq, nullptr, nullptr, nullptr,
-                    dqc, nullptr, mdu, s->B, s->T, s->H, s->dk, s->centered, 0};
-  if (traced(st, [&] { return ccq::launch_clean(c2, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::CleanArgs c2 = clean_args(s, ws, L.clean);  // same keys: statistics reused
+  c2.q = ws + L.dqc_io;
+  c2.k = k;
+  c2.lam = lam;
+  c2.qclean = dq;
+  c2.base = dqc;
+  c2.mdot = mdu;
+  if (traced(st, [&] { return ccq::launch_clean_out(c2, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   ccq::CcqDkArgs ka{q, k, ws + L.dqc_io, lam, mdq, mdu, dkg, dk, s->B, s->T, s->H, s->dk,
                     s->centered};
   if (traced(st, [&] { return ccq::launch_ccq_dk(ka, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;

@@ -1,275 +1,399 @@
-// ccq_clean.hip -- CCQ query contraction, chunkwise (Alg. 1 cleaning lines,
-// App. B).  For every token t of chunk r (positions t = t0 + rC + i, 1-based):
+// ccq_clean.hip -- CCQ query contraction (Eq. clean), chunkwise (App. B,
+// Alg. 1).  For token t (1-based position t = t0 + index + 1):
 //
-//   c_t       = Sigma_t q_t = (1/t) K_t q_t - (1/t^2) m_t (m_t . q_t)
-//   K_t       = S^K_r + sum_{rC<j<=t} k_j k_j^T   (carried state + intra block)
-//   m_t       = M_r   + sum_{rC<j<=t} k_j         (carried sum + cumsum)
-//   q_clean_t = q_t - lambda_t c_t                 (Eq. clean)
+//   Sigma_t   = Cbar_t - mu_t mu_t^T,  Cbar_t = (1/t) sum_{j<=t} k_j k_j^T,
+//   mu_t      = m_t / t,               m_t    = sum_{j<=t} k_j
+//   q_clean_t = q_t - lambda_t Sigma_t q_t
 //
-// One workgroup owns one head and a 'CT'-row slice of the symmetric S^K state
-// (fp32 MFMA accumulators, carried across the sequential chunk loop) and
-// produces the matching CT columns of q_clean.  Both intra-chunk terms are
-// folded into one masked C x C block applied to the chunk's keys:
+// Sigma_t is unchanged when every key is shifted by one vector c, which this
+// file uses to keep bf16 products well conditioned when the keys share a
+// large common mean:
 //
-//   c_i = sum_{j<=i} A'_ij k_j + (1/t_i) S^K_r q_i - (cq_i / t_i^2) M_r,
-//   A'_ij = (q_i . k_j)/t_i - cq_i/t_i^2,   cq_i = m_{t_i} . q_i = M_r.q_i + sum_{j<=i} q_i.k_j
+//   t Sigma_t q = sum_{j<=t} (k_j - c)(k_j - c)^T q - (m'_t . q) m'_t / t,
+//   m'_t = m_t - t c.
 //
-// so that q_i.k_j (exact bf16 products, fp32 sums) feeds both the second-moment
-// and the mean term.  fp32 operands of the bf16 products (A' and S^K) enter
-// as a bf16 head plus a bf16 tail, which keeps the Cbar - mu mu^T cancellation
-// (keys with a strong common mean) at ~1e-5 of |Cbar q|.
+// The sequence is cut into segments of `seg` chunks and c = c_s is the mean
+// key of segment s.  For token i of chunk r in segment s:
+//
+//   t_i Sigma q_i = S'_s q_i + sum_{j in s, j<=i} (q_i . k'_j) k'_j - (cq'_i / t_i) m'_i
+//   S'_s  = sum_{j before s} (k_j - c_s)(k_j - c_s)^T      (entry second moment)
+//   k'_j  = k_j - c_s,  cq'_i = m'_i . q_i
+//
+// Four kernels:
+//   clean_gram    raw sums of k k^T per segment and of k per chunk
+//   clean_msum    key-sum prefixes and the segment centres c_s
+//   clean_prefix  S'_s by a prefix over segments (fp32), stored in io dtype
+//   clean_out     one workgroup per chunk: S'_s q plus the causal product
+//                 over the segment's centred keys, all in MFMA tiles
+// Without centring (Sigma = Cbar) the same kernels run with c_s = 0 and no
+// mean terms.
 #include "ccq_device.h"
 #include "ccq_kernels.h"
 
 namespace ccq {
+namespace {
 
-template <typename T, int DK, int CT>
-__global__ __launch_bounds__(kThreads, 1) void clean_kernel(const CleanArgs a) {
-  constexpr int C = kChunk;
-  constexpr int P = Pad<T>::value;
-  constexpr bool kSplit = sizeof(T) == 2;  // bf16: carry a tail for fp32 operands
-  constexpr int LDQ = DK + P, LDA = C + P;
-  constexpr int NTN = CT / 16;                     // column tiles of the slice
-  constexpr int NPW = CT * DK / (16 * 16 * 4);     // state tiles per wave
-  constexpr int RPW = (DK / 16) / 4;               // state row tiles per wave
-  static_assert(NPW >= 1 && RPW >= 1 && NPW == RPW * NTN, "tile split");
-  constexpr int VE = 8;
-  typedef T vec_t __attribute__((ext_vector_type(VE)));
+__host__ __device__ inline int n_chunks(int T) { return (T + kChunk - 1) / kChunk; }
+__host__ __device__ inline int n_segs(int T, int seg) { return (n_chunks(T) + seg - 1) / seg; }
 
-  __shared__ __align__(16) T sQ[C * LDQ];
-  __shared__ __align__(16) T sK[C * LDQ];
-  __shared__ __align__(16) T sAh[C * LDA];  // A'[i][j]
-  __shared__ __align__(16) T sAl[kSplit ? C * LDA : 8];
-  __shared__ __align__(16) T sSh[CT * LDQ];  // S^K rows n0.. as B^T operand [n][c]
-  __shared__ __align__(16) T sSl[kSplit ? CT * LDQ : 8];
-  __shared__ __align__(16) float sM[DK];
-  __shared__ float sMq[C], sCq[C], sLam[C];
+template <typename T>
+__device__ __forceinline__ float frag_elem(const Frag<T>& f, int e) {
+  if constexpr (sizeof(T) == 2) {
+    return static_cast<float>(f.v[e]);
+  } else {
+    return e < 4 ? f.lo[e] : f.hi[e - 4];
+  }
+}
 
-  const int ntiles = DK / CT;
+template <typename T>
+__device__ __forceinline__ f32x4 load4f(const T* p) {
+  if constexpr (sizeof(T) == 2) {
+    const bf16x4 v = *reinterpret_cast<const bf16x4*>(p);
+    return f32x4{f32(v[0]), f32(v[1]), f32(v[2]), f32(v[3])};
+  } else {
+    return *reinterpret_cast<const f32x4*>(p);
+  }
+}
+
+}  // namespace
+
+// Raw segment Gram matrix G_s = sum_{j in s} k_j k_j^T, one 64-column slice
+// per workgroup (wave w owns rows [w DK/4, (w+1) DK/4)); the workgroups of
+// slice 0 also write the key sum of every chunk.
+template <typename T, int DK>
+__global__ __launch_bounds__(kThreads) void clean_gram_kernel(const CleanArgs a) {
+  constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P;
+  constexpr int RT = DK / 64;  // 16-row tiles per wave
+  __shared__ __align__(16) T sK[C * LDK];
+
+  const int NC = n_chunks(a.T), NS = n_segs(a.T, a.seg), NB = DK / 64;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int bh = lb / ntiles;
-  const int n0 = (lb % ntiles) * CT;  // first S^K column / q_clean column of this block
+  const int tb = lb % NB, s = (lb / NB) % NS, bh = lb / (NB * NS);
   const int b = bh / a.H, h = bh % a.H;
-  const int tid = threadIdx.x, w = wave_id(), l = lane_id();
-  const int g4 = l >> 4, c16 = l & 15;
-  const T* q = static_cast<const T*>(a.q);
+  const int w = wave_id(), l = lane_id(), g4 = l >> 4, c16 = l & 15;
+  const int a0 = w * (DK / 4), b0 = 64 * tb;
+  const bool sums = tb == 0;
   const T* k = static_cast<const T*>(a.k);
-  T* qc_out = static_cast<T*>(a.qclean);
   const size_t gstride = (size_t)a.H * DK;
-  const float t0f = (float)a.t0;
+  const int cbeg = s * a.seg, cend = min(NC, cbeg + a.seg);
 
-  // carried state, transposed: tile u holds S^K[c][n], c = 16 tr + 4 g4 + r (all
-  // DK rows over the waves), n = n0 + 16 tn + c16; Mt[v] holds the key sum of
-  // row tile (w RPW + v) in column 0.
-  f32x4 sk[NPW], Mt[RPW];
+  f32x4 acc[RT][4];
 #pragma unroll
-  for (int u = 0; u < NPW; ++u) {
-    const int tr = w * RPW + u / NTN, tn = u % NTN;
+  for (int v = 0; v < RT; ++v)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int c = 16 * tr + 4 * g4 + r, n = n0 + 16 * tn + c16;
-      sk[u][r] = a.C0 ? t0f * a.C0[((size_t)bh * DK + c) * DK + n] : 0.f;
+    for (int t = 0; t < 4; ++t) acc[v][t] = zero4();
+
+  ChunkTile<T, DK> rk;
+  auto load = [&](int c) {
+    rk.load(k + tok_off(b, c * C, h, a.T, a.H, DK), gstride, min(C, a.T - c * C));
+  };
+  load(cbeg);
+  const Frag<T> ones = ones_col_frag<T>();
+
+  for (int c = cbeg; c < cend; ++c) {
+    __syncthreads();  // previous chunk's readers are done
+    rk.store(sK, LDK);
+    if (c + 1 < cend) load(c + 1);
+    __syncthreads();
+    f32x4 msum[RT];
+#pragma unroll
+    for (int v = 0; v < RT; ++v) msum[v] = zero4();
+#pragma unroll
+    for (int k0 = 0; k0 < C; k0 += 32) {
+      Frag<T> fb[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) fb[t] = ld_frag_tr(sK + k0 * LDK + b0 + 16 * t, LDK);
+#pragma unroll
+      for (int v = 0; v < RT; ++v) {
+        const Frag<T> fa = ld_frag_tr(sK + k0 * LDK + a0 + 16 * v, LDK);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) mma(acc[v][t], fa, fb[t]);
+        if (sums) mma(msum[v], fa, ones);
+      }
+    }
+    if (sums && c16 == 0) {
+#pragma unroll
+      for (int v = 0; v < RT; ++v)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          a.csum[((size_t)bh * NC + c) * DK + a0 + 16 * v + 4 * g4 + r] = msum[v][r];
     }
   }
+  float* G = a.gram + ((size_t)bh * NS + s) * DK * DK;
 #pragma unroll
-  for (int v = 0; v < RPW; ++v)
+  for (int v = 0; v < RT; ++v)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int c = 16 * (w * RPW + v) + 4 * g4 + r;
-      Mt[v][r] = (a.mu0 && c16 == 0) ? t0f * a.mu0[(size_t)bh * DK + c] : 0.f;
-    }
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        G[(size_t)(a0 + 16 * v + 4 * g4 + r) * DK + b0 + 16 * t + c16] = acc[v][t][r];
+}
 
-  auto publish_state = [&]() {  // S^K -> sSh/sSl [n][c], key sum -> sM
+// Key-sum prefixes, one thread per feature: the centre c_s of each segment,
+// the key sum before each segment and before each chunk about that centre,
+// and the final mean.
+__global__ void clean_msum_kernel(const CleanArgs a) {
+  const int bh = blockIdx.x, d = threadIdx.x, DK = a.dk;  // blockDim.x == dk
+  const int NC = n_chunks(a.T), NS = n_segs(a.T, a.seg);
+  const float* cs = a.csum + (size_t)bh * NC * DK + d;
+  float run = a.mu0 ? (float)a.t0 * a.mu0[(size_t)bh * DK + d] : 0.f;  // raw key sum
+  for (int s = 0; s < NS; ++s) {
+    const int cbeg = s * a.seg, cend = min(NC, cbeg + a.seg);
+    float tot = 0.f;
+    for (int c = cbeg; c < cend; ++c) tot += cs[(size_t)c * DK];
+    const int len = min(a.T, cend * kChunk) - cbeg * kChunk;
+    const float cen = a.centered ? tot / (float)len : 0.f;
+    const float ns = (float)(a.t0 + (int64_t)cbeg * kChunk);  // tokens before the segment
+    float mp = run - ns * cen;
+    a.cs[((size_t)bh * NS + s) * DK + d] = cen;
+    a.ms[((size_t)bh * NS + s) * DK + d] = mp;
+    for (int c = cbeg; c < cend; ++c) {
+      a.mr[((size_t)bh * NC + c) * DK + d] = mp;
+      const int rows = min(kChunk, a.T - c * kChunk);
+      mp += cs[(size_t)c * DK] - (float)rows * cen;
+    }
+    run += tot;
+  }
+  if (a.muT) a.muT[(size_t)bh * DK + d] = run / (float)(a.t0 + a.T);
+}
+
+// S'_s = S_s - M'_s c_s^T - c_s M'_s^T - n_s c_s c_s^T with S_s the raw second
+// moment before segment s (prefix of the Gram matrices, fp32) and M'_s the key
+// sum about c_s; four elements per thread.  Also the final Cbar_T.
+template <typename T, int DK>
+__global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
+  constexpr int PER = DK * DK / 4 / 256;  // workgroups per head
+  const int bh = blockIdx.x / PER;
+  const int e = ((blockIdx.x % PER) * 256 + threadIdx.x) * 4;
+  const int ra = e / DK, cb = e % DK;
+  const int NS = n_segs(a.T, a.seg);
+  const float t0f = (float)a.t0;
+  f32x4 acc = zero4();
+  if (a.C0) acc = *reinterpret_cast<const f32x4*>(a.C0 + ((size_t)bh * DK + ra) * DK + cb) * t0f;
+  T* Sp = static_cast<T*>(a.sprime);
+  for (int s = 0; s < NS; ++s) {
+    const size_t so = (size_t)bh * NS + s;
+    const float ca = a.cs[so * DK + ra], ma = a.ms[so * DK + ra];
+    const f32x4 cb4 = *reinterpret_cast<const f32x4*>(a.cs + so * DK + cb);
+    const f32x4 mb4 = *reinterpret_cast<const f32x4*>(a.ms + so * DK + cb);
+    const f32x4 g = *reinterpret_cast<const f32x4*>(a.gram + (so * DK + ra) * DK + cb);
+    const float ns = t0f + (float)((int64_t)s * a.seg * kChunk);
+    f32x4 o;
 #pragma unroll
-    for (int u = 0; u < NPW; ++u) {
-      const int tr = w * RPW + u / NTN, tn = u % NTN;
-      const int off = (16 * tn + c16) * LDQ + 16 * tr + 4 * g4;
-      if constexpr (kSplit) {
-        bf16_t h0, h1, h2, h3, l0, l1, l2, l3;
-        split_bf16(sk[u][0], h0, l0);
-        split_bf16(sk[u][1], h1, l1);
-        split_bf16(sk[u][2], h2, l2);
-        split_bf16(sk[u][3], h3, l3);
-        *reinterpret_cast<bf16x4*>(sSh + off) = bf16x4{h0, h1, h2, h3};
-        *reinterpret_cast<bf16x4*>(sSl + off) = bf16x4{l0, l1, l2, l3};
+    for (int q = 0; q < 4; ++q) o[q] = acc[q] - ma * cb4[q] - ca * mb4[q] - ns * ca * cb4[q];
+    store4(Sp + (so * DK + ra) * DK + cb, o[0], o[1], o[2], o[3]);
+    acc += g;
+  }
+  if (a.CT)
+    *reinterpret_cast<f32x4*>(a.CT + ((size_t)bh * DK + ra) * DK + cb) =
+        acc * (1.f / (t0f + (float)a.T));
+}
+
+// One workgroup per chunk; wave w owns rows i = 16 w .. 16 w + 15.  All
+// products are kept transposed (output feature n in the accumulator row, token
+// i in its column) so that score tiles feed the next product from registers:
+//   acc^T  = S'_s x^T                                   (S' rows from L2)
+//   sc^T   = K'_blk x^T,  acc^T += K'_blk^T sc^T        (each block of the segment)
+// On the diagonal block the scores are masked to j <= i and shifted by
+// -cq'_i / t_i, which folds the within-chunk part of m'_i into the product.
+template <typename T, int DK>
+__global__ __launch_bounds__(kThreads, 2) void clean_out_kernel(const CleanArgs a) {
+  constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P;
+  constexpr int NK = DK / 32, NN = DK / 16;
+  typedef typename ChunkTile<T, DK>::vec_t vec_t;
+  __shared__ __align__(16) T sK[2][C * LDK];
+  __shared__ __align__(16) float sC[DK], sMr[DK], sMs[DK];
+
+  const int NC = n_chunks(a.T), NS = n_segs(a.T, a.seg);
+  const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int bh = lb / NC, ch = lb % NC;
+  const int b = bh / a.H, h = bh % a.H;
+  const int s = ch / a.seg, cbeg = s * a.seg;
+  const int r0 = ch * C, nrow = min(C, a.T - r0);
+  const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g4 = l >> 4, c16 = l & 15;
+  const T* x = static_cast<const T*>(a.q);
+  const T* k = static_cast<const T*>(a.k);
+  const size_t gstride = (size_t)a.H * DK;
+  const float t0f = (float)a.t0;
+  const size_t so = (size_t)bh * NS + s;
+
+  // this wave's rows of x as B fragments (column = token); rows past the end
+  // repeat the last row and are never written back
+  const int i = 16 * w + c16;
+  const bool iok = i < nrow;
+  Frag<T> qf[NK];
+  {
+    const T* xr = x + tok_off(b, r0 + (iok ? i : nrow - 1), h, a.T, a.H, DK) + 8 * g4;
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+      if constexpr (sizeof(T) == 2) {
+        qf[kk].v = *reinterpret_cast<const bf16x8*>(xr + 32 * kk);
       } else {
-        store4(sSh + off, sk[u][0], sk[u][1], sk[u][2], sk[u][3]);
+        qf[kk].lo = *reinterpret_cast<const f32x4*>(xr + 32 * kk);
+        qf[kk].hi = *reinterpret_cast<const f32x4*>(xr + 32 * kk + 4);
       }
     }
-    if (c16 == 0)
-#pragma unroll
-      for (int v = 0; v < RPW; ++v)
-        *reinterpret_cast<f32x4*>(sM + 16 * (w * RPW + v) + 4 * g4) = Mt[v];
+  }
+  ChunkTile<T, DK> rk;
+  auto load_block = [&](int c) {
+    rk.load(k + tok_off(b, c * C, h, a.T, a.H, DK), gstride, min(C, a.T - c * C));
   };
-  publish_state();
+  load_block(cbeg);
+  for (int d = tid; d < DK; d += kThreads) {
+    sC[d] = a.cs[so * DK + d];
+    sMs[d] = a.ms[so * DK + d];
+    sMr[d] = a.mr[((size_t)bh * NC + ch) * DK + d];
+  }
 
-  ChunkTile<T, DK> rq, rk;
-  RowScalar rlam;
-  auto prefetch = [&](int r0) {
-    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-    rq.load(q + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-    rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-    if (tid < C) rlam.load(a.lam + ((size_t)b * a.T + r0) * a.H + h, (size_t)a.H, tid, nrow);
-  };
-  if (a.T > 0) prefetch(0);
-
-  for (int r0 = 0; r0 < a.T; r0 += C) {
-    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-    __syncthreads();  // (A) previous chunk's readers are done with LDS
-    rq.store(sQ, LDQ);
-    rk.store(sK, LDQ);
-    if (tid < C) sLam[tid] = rlam.get();
-    if (r0 + C < a.T) prefetch(r0 + C);  // next chunk's loads overlap this chunk's math
-    __syncthreads();  // (B)
-
-    // M_r . q_i: four threads per row
-    {
-      const int row = tid >> 2, part = tid & 3;
-      float s = 0.f;
+  // entry term S'_s x_i
+  f32x4 acc[NN];
+  const T* sp = static_cast<const T*>(a.sprime) + so * DK * DK;
 #pragma unroll
-      for (int c0 = part * (DK / 4); c0 < (part + 1) * (DK / 4); c0 += VE) {
-        const vec_t qv = *reinterpret_cast<const vec_t*>(sQ + row * LDQ + c0);
+  for (int tn = 0; tn < NN; ++tn) {
+    acc[tn] = zero4();
 #pragma unroll
-        for (int e = 0; e < VE; ++e) s += f32(qv[e]) * sM[c0 + e];
-      }
-      s += __shfl_xor(s, 1);
-      s += __shfl_xor(s, 2);
-      if (part == 0) sMq[row] = s;
+    for (int kk = 0; kk < NK; ++kk)
+      mma(acc[tn], ld_frag_global(sp + (size_t)(16 * tn) * DK + 32 * kk, (size_t)DK), qf[kk]);
+  }
+  __syncthreads();  // sC, sMs, sMr
+
+  // M'_s . x_i and c_s . x_i (each lane holds 8 features per k step)
+  float mq = 0.f, cx = 0.f;
+#pragma unroll
+  for (int kk = 0; kk < NK; ++kk)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int d = 32 * kk + 8 * g4 + e;
+      const float xv = frag_elem(qf[kk], e);
+      mq += xv * sMs[d];
+      cx += xv * sC[d];
     }
-    // transposed score tiles: sc[J][r] = k_j . q_i, j = 16 J + 4 g4 + r, i = 16 w + c16
+  mq += __shfl_xor(mq, 16);
+  mq += __shfl_xor(mq, 32);
+  cx += __shfl_xor(cx, 16);
+  cx += __shfl_xor(cx, 32);
+
+  const float ti = t0f + (float)(r0 + i + 1);
+  float rs = 0.f, cqp = 0.f;
+  for (int jb = cbeg; jb <= ch; ++jb) {
+    T* buf = sK[(jb - cbeg) & 1];
+    // centred keys of block jb; the other buffer may still be read by a
+    // wave working on block jb - 1, this one was released by the last barrier
+#pragma unroll
+    for (int u = 0; u < ChunkTile<T, DK>::NV; ++u) {
+      const vec_t kv = rk.get(u);
+      const int col = ChunkTile<T, DK>::col(u);
+      vec_t y;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) y[e] = to<T>(f32(kv[e]) - sC[col + e]);
+      *reinterpret_cast<vec_t*>(buf + ChunkTile<T, DK>::row() * LDK + col) = y;
+    }
+    if (jb < ch) load_block(jb + 1);
+    __syncthreads();
+
+    const bool diag = jb == ch;
     f32x4 sc[4];
 #pragma unroll
     for (int J = 0; J < 4; ++J) {
       sc[J] = zero4();
-      if (J <= w) tile_mma<T, DK>(sc[J], sK + 16 * J * LDQ, LDQ, sQ + 16 * w * LDQ, LDQ);
+      if (!diag || J <= w)
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) mma(sc[J], ld_frag(buf + 16 * J * LDK + 32 * kk, LDK), qf[kk]);
     }
-    __syncthreads();  // (C) sMq visible
-    {
-      const int i = 16 * w + c16;
-      float rs = 0.f;
+    if (diag) {
 #pragma unroll
       for (int J = 0; J < 4; ++J)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          if (J <= w && 16 * J + 4 * g4 + r <= i) rs += sc[J][r];
+          if (16 * J + 4 * g4 + r > i) sc[J][r] = 0.f;
+    }
+#pragma unroll
+    for (int J = 0; J < 4; ++J) rs += sc[J][0] + sc[J][1] + sc[J][2] + sc[J][3];
+    if (diag) {
       rs += __shfl_xor(rs, 16);
       rs += __shfl_xor(rs, 32);
-      const float cq = sMq[i] + rs;   // m_t . q_i (raw key sum up to t_i)
-      const float it = 1.f / (t0f + (float)(r0 + i + 1));
-      if (g4 == 0) sCq[i] = cq;
-      if (a.mdot && n0 == 0 && g4 == 0 && i < nrow) a.mdot[((size_t)b * a.T + r0 + i) * a.H + h] = cq;
-      const float mean = a.centered ? cq * it * it : 0.f;
-      // A'[i][j] = (q_i . k_j)/t_i - cq_i/t_i^2 for j <= i, written as row i
+      cqp = mq + rs;  // m'_i . x_i
+      if (a.centered) {
+        const float sub = cqp / ti;
 #pragma unroll
-      for (int J = 0; J < 4; ++J) {
-        float x[4];
+        for (int J = 0; J < 4; ++J)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int j = 16 * J + 4 * g4 + r;
-          x[r] = (J <= w && j <= i) ? sc[J][r] * it - mean : 0.f;
-        }
-        const int off = i * LDA + 16 * J + 4 * g4;
-        if constexpr (kSplit) {
-          bf16_t h0, h1, h2, h3, l0, l1, l2, l3;
-          split_bf16(x[0], h0, l0);
-          split_bf16(x[1], h1, l1);
-          split_bf16(x[2], h2, l2);
-          split_bf16(x[3], h3, l3);
-          *reinterpret_cast<bf16x4*>(sAh + off) = bf16x4{h0, h1, h2, h3};
-          *reinterpret_cast<bf16x4*>(sAl + off) = bf16x4{l0, l1, l2, l3};
-        } else {
-          store4(sAh + off, x[0], x[1], x[2], x[3]);
-        }
+          for (int r = 0; r < 4; ++r)
+            if (16 * J + 4 * g4 + r <= i) sc[J][r] -= sub;
       }
     }
-    __syncthreads();  // (D)
-
-    // c and q_clean for rows of stripe w, columns [n0, n0 + CT)
+    const Frag<T> f0 = acc_pair_frag<T>(sc[0], sc[1]);
+    const Frag<T> f1 = acc_pair_frag<T>(sc[2], sc[3]);
+    const bool upper = !diag || w >= 2;  // keys 32..63 can precede row i
 #pragma unroll
-    for (int tn = 0; tn < NTN; ++tn) {
-      f32x4 a1 = zero4(), a2 = zero4();
-#pragma unroll
-      for (int k0 = 0; k0 < C; k0 += 32) {
-        if (k0 <= 16 * w) {  // A' is zero for j > i
-          const Frag<T> fb = ld_frag_tr(sK + k0 * LDQ + n0 + 16 * tn, LDQ);
-          mma(a1, ld_frag(sAh + 16 * w * LDA + k0, LDA), fb);
-          if constexpr (kSplit) mma(a1, ld_frag(sAl + 16 * w * LDA + k0, LDA), fb);
-        }
-      }
-#pragma unroll
-      for (int k0 = 0; k0 < DK; k0 += 32) {
-        const Frag<T> fa = ld_frag(sQ + 16 * w * LDQ + k0, LDQ);
-        mma(a2, fa, ld_frag(sSh + 16 * tn * LDQ + k0, LDQ));
-        if constexpr (kSplit) mma(a2, fa, ld_frag(sSl + 16 * tn * LDQ + k0, LDQ));
-      }
-      const int col = n0 + 16 * tn + c16;
-      const float mcol = a.centered ? sM[col] : 0.f;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * g4 + r;
-        const float it = 1.f / (t0f + (float)(r0 + i + 1));
-        const float c = a1[r] + a2[r] * it - sCq[i] * it * it * mcol;
-        if (i < nrow) {
-          const size_t off = tok_off(b, r0 + i, h, a.T, a.H, DK) + col;
-          const float base = a.base ? a.base[off] : f32(sQ[i * LDQ + col]);
-          const float qcv = base - sLam[i] * c;
-          qc_out[off] = to<T>(qcv);
-          if (a.qclean_dbg) a.qclean_dbg[off] = qcv;
-          if (a.corr) a.corr[off] = c;
-        }
-      }
+    for (int tn = 0; tn < NN; ++tn) {
+      mma(acc[tn], ld_frag_tr_acc(buf + 16 * tn, LDK), f0);
+      if (upper) mma(acc[tn], ld_frag_tr_acc(buf + 32 * LDK + 16 * tn, LDK), f1);
     }
-    __syncthreads();  // (E) the state tile and M have been read
-
-    // S^K_{r+1} = S^K_r + K^T K (columns n0..), M_{r+1} = M_r + sum_j k_j
-    {
-      const Frag<T> ones = ones_col_frag<T>();
-#pragma unroll
-      for (int k0 = 0; k0 < C; k0 += 32) {
-        Frag<T> fb[NTN];
-#pragma unroll
-        for (int tn = 0; tn < NTN; ++tn) fb[tn] = ld_frag_tr(sK + k0 * LDQ + n0 + 16 * tn, LDQ);
-#pragma unroll
-        for (int v = 0; v < RPW; ++v) {
-          const Frag<T> fa = ld_frag_tr(sK + k0 * LDQ + 16 * (w * RPW + v), LDQ);
-#pragma unroll
-          for (int tn = 0; tn < NTN; ++tn) mma(sk[v * NTN + tn], fa, fb[tn]);
-          mma(Mt[v], fa, ones);
-        }
-      }
-    }
-    publish_state();
   }
-  __syncthreads();
 
-  // final normalised statistics Cbar_T = S^K_T / t, mu_T = M_T / t
-  const float tfin = t0f + (float)a.T;
-  if (tfin > 0.f) {
-    const float inv = 1.f / tfin;
-    if (a.CT) {
+  if (!iok) return;
+  const float inv = 1.f / ti;
+  const float lam = a.lam[((size_t)b * a.T + r0 + i) * a.H + h];
+  const float msub = a.centered ? cqp * inv : 0.f;
+  const size_t rowoff = tok_off(b, r0 + i, h, a.T, a.H, DK);
+  T* qc = static_cast<T*>(a.qclean);
 #pragma unroll
-      for (int u = 0; u < NPW; ++u) {
-        const int tr = w * RPW + u / NTN, tn = u % NTN;
+  for (int tn = 0; tn < NN; ++tn) {
+    const int n = 16 * tn + 4 * g4;
+    const f32x4 mr = *reinterpret_cast<const f32x4*>(sMr + n);
+    f32x4 c, o;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int c = 16 * tr + 4 * g4 + r, n = n0 + 16 * tn + c16;
-          a.CT[((size_t)bh * DK + c) * DK + n] = sk[u][r] * inv;
-        }
-      }
-    }
-    if (a.muT && n0 == 0)
-      for (int c = tid; c < DK; c += kThreads) a.muT[(size_t)bh * DK + c] = sM[c] * inv;
+    for (int r = 0; r < 4; ++r) c[r] = (acc[tn][r] - msub * mr[r]) * inv;
+    const f32x4 xb = a.base ? *reinterpret_cast<const f32x4*>(a.base + rowoff + n) : load4f(x + rowoff + n);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) o[r] = xb[r] - lam * c[r];
+    store4(qc + rowoff + n, o[0], o[1], o[2], o[3]);
+    if (a.qclean_dbg) *reinterpret_cast<f32x4*>(a.qclean_dbg + rowoff + n) = o;
+    if (a.corr) *reinterpret_cast<f32x4*>(a.corr + rowoff + n) = c;
   }
+  if (a.mdot && g4 == 0) a.mdot[((size_t)b * a.T + r0 + i) * a.H + h] = cqp + ti * cx;  // raw m . x
 }
 
 namespace {
-template <typename T, int DK, int CT>
-hipError_t run_clean(const CleanArgs& a, hipStream_t st) {
-  const int nblk = a.B * a.H * (DK / CT);
+template <typename T, int DK>
+hipError_t run_gram(const CleanArgs& a, hipStream_t st) {
+  const long long nblk = (long long)a.B * a.H * n_segs(a.T, a.seg) * (DK / 64);
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((clean_kernel<T, DK, CT>), dim3(nblk), dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((clean_gram_kernel<T, DK>), dim3((unsigned)nblk), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
+template <typename T, int DK>
+hipError_t run_prefix(const CleanArgs& a, hipStream_t st) {
+  const long long nblk = (long long)a.B * a.H * (DK * DK / 1024);
+  if (nblk == 0) return hipSuccess;
+  hipLaunchKernelGGL((clean_prefix_kernel<T, DK>), dim3((unsigned)nblk), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+template <typename T, int DK>
+hipError_t run_out(const CleanArgs& a, hipStream_t st) {
+  const long long nblk = (long long)a.B * a.H * n_chunks(a.T);
+  if (nblk == 0) return hipSuccess;
+  hipLaunchKernelGGL((clean_out_kernel<T, DK>), dim3((unsigned)nblk), dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+#define CCQ_CLEAN_DISPATCH(fn, a, bf, st)                      \
+  do {                                                         \
+    if (bf) {                                                  \
+      switch ((a).dk) {                                        \
+        case 64: return fn<bf16_t, 64>((a), (st));             \
+        case 128: return fn<bf16_t, 128>((a), (st));           \
+        case 256: return fn<bf16_t, 256>((a), (st));           \
+      }                                                        \
+    } else {                                                   \
+      switch ((a).dk) {                                        \
+        case 64: return fn<float, 64>((a), (st));              \
+        case 128: return fn<float, 128>((a), (st));            \
+      }                                                        \
+    }                                                          \
+    return hipErrorInvalidValue;                               \
+  } while (0)
 }  // namespace
 
 bool clean_supported(int dk, bool is_bf16) {
@@ -277,20 +401,23 @@ bool clean_supported(int dk, bool is_bf16) {
   return dk == 64 || dk == 128;
 }
 
-hipError_t launch_clean(const CleanArgs& a, bool is_bf16, hipStream_t st) {
-  if (is_bf16) {
-    switch (a.dk) {
-      case 64: return run_clean<bf16_t, 64, 16>(a, st);
-      case 128: return run_clean<bf16_t, 128, 32>(a, st);
-      case 256: return run_clean<bf16_t, 256, 32>(a, st);
-    }
-  } else {
-    switch (a.dk) {
-      case 64: return run_clean<float, 64, 16>(a, st);
-      case 128: return run_clean<float, 128, 32>(a, st);
-    }
-  }
-  return hipErrorInvalidValue;
+hipError_t launch_clean_gram(const CleanArgs& a, bool is_bf16, hipStream_t st) {
+  CCQ_CLEAN_DISPATCH(run_gram, a, is_bf16, st);
+}
+
+hipError_t launch_clean_msum(const CleanArgs& a, hipStream_t st) {
+  const int nblk = a.B * a.H;
+  if (nblk == 0 || a.T == 0) return hipSuccess;
+  hipLaunchKernelGGL(clean_msum_kernel, dim3(nblk), dim3(a.dk), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_clean_prefix(const CleanArgs& a, bool is_bf16, hipStream_t st) {
+  CCQ_CLEAN_DISPATCH(run_prefix, a, is_bf16, st);
+}
+
+hipError_t launch_clean_out(const CleanArgs& a, bool is_bf16, hipStream_t st) {
+  CCQ_CLEAN_DISPATCH(run_out, a, is_bf16, st);
 }
 
 }  // namespace ccq

@@ -105,6 +105,55 @@ __device__ __forceinline__ Frag<float> ld_frag_tr<float>(const float* base, int 
   return f;
 }
 
+// Transposed-operand fragment whose k slots follow two stacked accumulator
+// tiles (rows 0..15 and 16..31 of a 32-row block): slot 8g + e is row 4g + e
+// for e < 4 and row 16 + 4g + (e - 4) otherwise.  Paired with
+// acc_pair_frag, a product can consume a score tile straight from the
+// accumulators of an earlier one, with no trip through LDS.  `base` points at
+// X[k0][m0] of a row-major LDS tile with row pitch ld.
+template <typename T>
+__device__ __forceinline__ Frag<T> ld_frag_tr_acc(const T* base, int ld);
+
+template <>
+__device__ __forceinline__ Frag<bf16_t> ld_frag_tr_acc<bf16_t>(const bf16_t* base, int ld) {
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  const int l = lane_id(), g = l >> 4, j = l & 15;
+  const bf16_t* p = base + (4 * g + (j >> 2)) * ld + 4 * (j & 3);
+  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p));
+  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 16 * ld));
+  Frag<bf16_t> f;
+  f.v = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return f;
+}
+
+template <>
+__device__ __forceinline__ Frag<float> ld_frag_tr_acc<float>(const float* base, int ld) {
+  const int l = lane_id(), g = l >> 4, m = l & 15;
+  Frag<float> f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    f.lo[e] = base[(4 * g + e) * ld + m];
+    f.hi[e] = base[(16 + 4 * g + e) * ld + m];
+  }
+  return f;
+}
+
+// B fragment (k = accumulator row, n = accumulator column) built from two
+// accumulator tiles: x holds rows 0..15, y rows 16..31 of the k range.
+template <typename T>
+__device__ __forceinline__ Frag<T> acc_pair_frag(const f32x4& x, const f32x4& y) {
+  Frag<T> f;
+  if constexpr (sizeof(T) == 2) {
+    f.v = bf16x8{static_cast<bf16_t>(x[0]), static_cast<bf16_t>(x[1]), static_cast<bf16_t>(x[2]),
+                 static_cast<bf16_t>(x[3]), static_cast<bf16_t>(y[0]), static_cast<bf16_t>(y[1]),
+                 static_cast<bf16_t>(y[2]), static_cast<bf16_t>(y[3])};
+  } else {
+    f.lo = x;
+    f.hi = y;
+  }
+  return f;
+}
+
 // B fragment of the 16-column tile whose column 0 is all ones (the rest zero):
 // acc += A * ones gives the row sums of A in column 0.
 template <typename T>

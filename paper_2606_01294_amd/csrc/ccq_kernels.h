@@ -9,7 +9,13 @@ namespace ccq {
 
 // Query contraction (Eq. clean evaluated chunkwise, App. B / Alg. 1):
 // out = base - lam * Sigma_t x  (base = x when null).  The backward pass runs
-// the same kernel on x = dL/dq_clean, since (I - lam Sigma)^T = I - lam Sigma.
+// the output kernel again on x = dL/dq_clean, since (I - lam Sigma)^T =
+// I - lam Sigma, reusing the key statistics of the forward.
+//
+// The sequence is cut into segments of `seg` chunks.  Key statistics are
+// formed per segment (clean_gram, clean_msum, clean_prefix); each chunk's
+// output then needs only its segment's entry statistics and the keys of the
+// segment up to the chunk (clean_out), so every chunk runs in parallel.
 struct CleanArgs {
   const void* q;      // x: [B,T,H,dk] io
   const void* k;      // [B,T,H,dk] io
@@ -23,8 +29,16 @@ struct CleanArgs {
   const float* base;  // [B,T,H,dk] fp32 or null
   float* corr;        // Sigma_t x_t, [B,T,H,dk] fp32, or null
   float* mdot;        // m_t . x_t (raw key sum), [B,T,H] fp32, or null
+  // workspace: NC = chunks, NS = segments per sequence
+  float* gram;        // [B*H, NS, dk, dk] raw segment sums of k k^T
+  void* sprime;       // [B*H, NS, dk, dk] io: entry second moment about c_s
+  float* csum;        // [B*H, NC, dk] key sum of every chunk
+  float* mr;          // [B*H, NC, dk] key sum before the chunk, about c_s
+  float* cs;          // [B*H, NS, dk] centre c_s of each segment
+  float* ms;          // [B*H, NS, dk] raw key sum before each segment
   int B, T, H, dk;
   int centered;
+  int seg;            // chunks per segment
   int64_t t0;
 };
 
@@ -142,7 +156,11 @@ struct CcqDkArgs {
 
 // Each launcher returns hipSuccess or the launch error.  is_bf16 selects the
 // io dtype (bf16 or fp32); shapes are validated by the caller.
-hipError_t launch_clean(const CleanArgs& a, bool is_bf16, hipStream_t st);
+hipError_t launch_clean_gram(const CleanArgs& a, bool is_bf16, hipStream_t st);
+hipError_t launch_clean_msum(const CleanArgs& a, hipStream_t st);
+hipError_t launch_clean_prefix(const CleanArgs& a, bool is_bf16, hipStream_t st);
+hipError_t launch_clean_out(const CleanArgs& a, bool is_bf16, hipStream_t st);
+constexpr int kCleanSeg = 8;   // chunks per segment of the query contraction
 hipError_t launch_gla_state(const GlaStateArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
 hipError_t launch_gla_out(const GlaOutArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
 hipError_t launch_gdn_wy(const WyArgs& a, bool is_bf16, hipStream_t st);
