@@ -42,11 +42,11 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     NC = -(-w.T // C)
     NS = -(-NC // CLEAN_SEG)
     stats = BH * NS * dk * dk               # elements of the segment statistics
-    if kernel == "clean_gram":      # k in; segment Gram (fp32) and chunk key sums out
-        by = ntok * dk * io_bytes + stats * 4 + BH * NC * dk * 4
+    if kernel == "clean_gram":      # k in; segment Gram (fp32), chunk and segment key sums out
+        by = ntok * dk * io_bytes + stats * 4 + BH * (NC + NS) * dk * 4
         fl = ntok * 2 * dk * dk
-    elif kernel == "clean_msum":    # chunk key sums in; centres and prefixes out
-        by = BH * NC * dk * 8 + BH * NS * dk * 8
+    elif kernel == "clean_msum":    # chunk and segment key sums in; centres and prefixes out
+        by = BH * NC * dk * 8 + BH * NS * dk * 12
         fl = BH * NC * dk * 2
     elif kernel == "clean_prefix":  # Gram in (fp32); entry second moments out (io)
         by = stats * (4 + io_bytes) + BH * NS * dk * 8
@@ -66,14 +66,14 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     elif kernel == "gla_out":       # q_clean, k, g, v, chunk states in; o out
         by = ntok * (2 * dk * io_bytes + dk * gate_bytes + 2 * dv * io_bytes + dv * dk * io_bytes // C)
         fl = ntok * (2 * C * dk + 2 * dk * dv + 2 * C * dv)
-    elif kernel == "gdn_wy":
-        by = ntok * (2 * dk * io_bytes + dv * io_bytes + dv * 4 + 8)
-        fl = ntok * (2 * C * dk + C * (dk + dv))
-    elif kernel == "gdn_state":     # k, W, Ut, log alpha in; chunk states, U, final state out
-        by = ntok * (2 * dk * io_bytes + dv * 4 + 4 + dv * dk * io_bytes // C + dv * io_bytes) \
-            + BH * dv * dk * 4
-        fl = ntok * (4 * dk * dv)
-    elif kernel == "gdn_out":       # q_clean, k, chunk states, U, log alpha in; o out
+    elif kernel == "gdn_tri":       # k, log alpha, beta in; chunk transforms Tm and decays out
+        by = ntok * (dk * io_bytes + 8 + C * io_bytes + 4)
+        fl = ntok * (2 * C * dk)
+    elif kernel == "gdn_state":     # k, v, Tm, decays, beta in; chunk states, U, final state out
+        by = ntok * (dk * io_bytes + dv * io_bytes + C * io_bytes + 8 + dv * dk * io_bytes // C
+                     + dv * io_bytes) + BH * dv * dk * 4
+        fl = ntok * (4 * dk * dv + 2 * C * dv)
+    elif kernel == "gdn_out":       # q_clean, k, chunk states, U, decays in; o out
         by = ntok * (2 * dk * io_bytes + dv * dk * io_bytes // C + 2 * dv * io_bytes + 4)
         fl = ntok * (2 * C * dk + 2 * dk * dv + 2 * C * dv)
     elif kernel == "gla_dstate":
@@ -96,14 +96,14 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
 
 CLEAN = ["clean_gram", "clean_msum", "clean_prefix"]
 KERNELS = {0: CLEAN + ["clean_out", "gla_state", "gla_out"],
-           1: CLEAN + ["clean_out", "gdn_wy", "gdn_state", "gdn_out"],
+           1: CLEAN + ["clean_out", "gdn_tri", "gdn_state", "gdn_out"],
            "train": CLEAN + ["clean_out_train", "gla_state", "gla_out", "gla_dstate",
                              "gla_bwd_chunk", "gla_dg", "clean_dq", "ccq_dk"]}
 KERNEL_SYMBOL = {"clean_gram": "clean_gram_kernel", "clean_msum": "clean_msum_kernel",
                  "clean_prefix": "clean_prefix_kernel", "clean_out": "clean_out_kernel",
                  "clean_out_train": "clean_out_kernel", "clean_dq": "clean_out_kernel",
                  "gla_state": "gla_state_kernel", "gla_out": "gla_out_kernel",
-                 "gdn_wy": "gdn_wy_kernel", "gdn_state": "gdn_state_kernel",
+                 "gdn_tri": "gdn_tri_kernel", "gdn_state": "gdn_state_kernel",
                  "gdn_out": "gdn_out_kernel", "gla_dstate": "gla_dstate_kernel",
                  "gla_bwd_chunk": "gla_bwd_chunk_kernel", "gla_dg": "gla_dg_kernel",
                  "ccq_dk": "ccq_dk_kernel"}

@@ -59,7 +59,7 @@ ccq_status check_shape(const ccq_shape* s, ccq_backbone bb) {
 
 // Workspace of the query contraction: segment and chunk key statistics.
 struct CleanWs {
-  size_t gram = 0, sprime = 0, csum = 0, mr = 0, cs = 0, ms = 0;
+  size_t gram = 0, sprime = 0, csum = 0, ssum = 0, mr = 0, cs = 0, ms = 0;
 };
 
 template <typename Take>
@@ -70,6 +70,7 @@ CleanWs take_clean_ws(const ccq_shape* s, Take&& take) {
   c.gram = take(bh * ns * dk * dk * 4);
   c.sprime = take(bh * ns * dk * dk * esize(s->io_dtype));
   c.csum = take(bh * nc * dk * 4);
+  c.ssum = take(bh * ns * dk * 4);
   c.mr = take(bh * nc * dk * 4);
   c.cs = take(bh * ns * dk * 4);
   c.ms = take(bh * ns * dk * 4);
@@ -81,6 +82,7 @@ ccq::CleanArgs clean_args(const ccq_shape* s, char* ws, const CleanWs& c) {
   a.gram = reinterpret_cast<float*>(ws + c.gram);
   a.sprime = ws + c.sprime;
   a.csum = reinterpret_cast<float*>(ws + c.csum);
+  a.ssum = reinterpret_cast<float*>(ws + c.ssum);
   a.mr = reinterpret_cast<float*>(ws + c.mr);
   a.cs = reinterpret_cast<float*>(ws + c.cs);
   a.ms = reinterpret_cast<float*>(ws + c.ms);
@@ -103,12 +105,12 @@ hipError_t run_clean_stats(const ccq::CleanArgs& a, bool bf, hipStream_t st) {
 }
 
 struct FwdLayout {
-  size_t qclean = 0, states = 0, W = 0, Ut = 0, U = 0, total = 0;
+  size_t qclean = 0, states = 0, Tm = 0, gam = 0, U = 0, total = 0;
   CleanWs clean;
 };
 
-// q_clean, the chunk-entry states S_r and, for Gated DeltaNet, the WY/UT
-// factors W, Ut and the corrected values U of every chunk.
+// q_clean, the chunk-entry states S_r and, for Gated DeltaNet, the chunk
+// transforms Tm, the cumulative log decays and the corrected values U.
 FwdLayout fwd_layout(const ccq_shape* s, ccq_backbone bb) {
   FwdLayout L;
   const size_t ntok = (size_t)s->B * s->T * s->H;
@@ -120,8 +122,8 @@ FwdLayout fwd_layout(const ccq_shape* s, ccq_backbone bb) {
   L.states = take(nchunk * s->dv * s->dk * e);
   L.clean = take_clean_ws(s, take);
   if (bb == CCQ_GDN) {
-    L.W = take(nchunk * 64 * s->dk * e);
-    L.Ut = take(nchunk * 64 * s->dv * sizeof(float));
+    L.Tm = take(nchunk * 64 * 64 * e);
+    L.gam = take(nchunk * 64 * sizeof(float));
     L.U = take(nchunk * 64 * s->dv * e);
   }
   L.total = off;
@@ -217,13 +219,13 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
     if (traced(st, [&] { return ccq::launch_gla_out(oa, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   } else {
     const float* la = static_cast<const float*>(g_or_la);
-    ccq::WyArgs wa{k, v, la, beta, ws + L.W, reinterpret_cast<float*>(ws + L.Ut),
-                   s->B, s->T, s->H, s->dk, s->dv};
-    if (traced(st, [&] { return ccq::launch_gdn_wy(wa, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
-    ccq::GdnArgs da{k, la, ws + L.W, reinterpret_cast<const float*>(ws + L.Ut), S0, ST,
-                    ws + L.states, ws + L.U, s->B, s->T, s->H, s->dk, s->dv};
+    float* gam = reinterpret_cast<float*>(ws + L.gam);
+    ccq::TriArgs ta{k, la, beta, ws + L.Tm, gam, s->B, s->T, s->H, s->dk, s->dv};
+    if (traced(st, [&] { return ccq::launch_gdn_tri(ta, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+    ccq::GdnArgs da{k, v, beta, ws + L.Tm, gam, S0, ST, ws + L.states, ws + L.U, s->B, s->T, s->H,
+                    s->dk, s->dv};
     if (traced(st, [&] { return ccq::launch_gdn_state(da, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
-    ccq::GdnOutArgs oa{qclean, k, la, ws + L.states, ws + L.U, o, s->B, s->T, s->H, s->dk, s->dv,
+    ccq::GdnOutArgs oa{qclean, k, gam, ws + L.states, ws + L.U, o, s->B, s->T, s->H, s->dk, s->dv,
                        s->scale};
     if (traced(st, [&] { return ccq::launch_gdn_out(oa, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   }

@@ -59,7 +59,7 @@ __device__ __forceinline__ f32x4 load4f(const T* p) {
 
 // Raw segment Gram matrix G_s = sum_{j in s} k_j k_j^T, one 64-column slice
 // per workgroup (wave w owns rows [w DK/4, (w+1) DK/4)); the workgroups of
-// slice 0 also write the key sum of every chunk.
+// slice 0 also write the key sums of every chunk and of the segment.
 template <typename T, int DK>
 __global__ __launch_bounds__(kThreads) void clean_gram_kernel(const CleanArgs a) {
   constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P;
@@ -89,6 +89,9 @@ __global__ __launch_bounds__(kThreads) void clean_gram_kernel(const CleanArgs a)
   };
   load(cbeg);
   const Frag<T> ones = ones_col_frag<T>();
+  f32x4 stot[RT];
+#pragma unroll
+  for (int v = 0; v < RT; ++v) stot[v] = zero4();
 
   for (int c = cbeg; c < cend; ++c) {
     __syncthreads();  // previous chunk's readers are done
@@ -113,11 +116,20 @@ __global__ __launch_bounds__(kThreads) void clean_gram_kernel(const CleanArgs a)
     }
     if (sums && c16 == 0) {
 #pragma unroll
-      for (int v = 0; v < RT; ++v)
+      for (int v = 0; v < RT; ++v) {
+        stot[v] += msum[v];
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           a.csum[((size_t)bh * NC + c) * DK + a0 + 16 * v + 4 * g4 + r] = msum[v][r];
+      }
     }
+  }
+  if (sums && c16 == 0) {
+#pragma unroll
+    for (int v = 0; v < RT; ++v)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        a.ssum[((size_t)bh * NS + s) * DK + a0 + 16 * v + 4 * g4 + r] = stot[v][r];
   }
   float* G = a.gram + ((size_t)bh * NS + s) * DK * DK;
 #pragma unroll
@@ -129,32 +141,31 @@ __global__ __launch_bounds__(kThreads) void clean_gram_kernel(const CleanArgs a)
         G[(size_t)(a0 + 16 * v + 4 * g4 + r) * DK + b0 + 16 * t + c16] = acc[v][t][r];
 }
 
-// Key-sum prefixes, one thread per feature: the centre c_s of each segment,
-// the key sum before each segment and before each chunk about that centre,
-// and the final mean.
+// Key-sum prefixes, one workgroup per (head, segment) and one thread per
+// feature: the centre c_s, the key sums before the segment and before each of
+// its chunks about that centre, and (last segment) the final mean.
 __global__ void clean_msum_kernel(const CleanArgs a) {
-  const int bh = blockIdx.x, d = threadIdx.x, DK = a.dk;  // blockDim.x == dk
+  const int DK = a.dk, d = threadIdx.x;  // blockDim.x == dk
   const int NC = n_chunks(a.T), NS = n_segs(a.T, a.seg);
+  const int bh = blockIdx.x / NS, s = blockIdx.x % NS;
+  const float* ss = a.ssum + (size_t)bh * NS * DK + d;
+  float run = a.mu0 ? (float)a.t0 * a.mu0[(size_t)bh * DK + d] : 0.f;  // raw key sum before s
+  for (int p = 0; p < s; ++p) run += ss[(size_t)p * DK];
+  const float tot = ss[(size_t)s * DK];
+  const int cbeg = s * a.seg, cend = min(NC, cbeg + a.seg);
+  const int len = min(a.T, cend * kChunk) - cbeg * kChunk;
+  const float cen = a.centered ? tot / (float)len : 0.f;
+  const float ns = (float)(a.t0 + (int64_t)cbeg * kChunk);  // tokens before the segment
+  float mp = run - ns * cen;
+  a.cs[((size_t)bh * NS + s) * DK + d] = cen;
+  a.ms[((size_t)bh * NS + s) * DK + d] = mp;
   const float* cs = a.csum + (size_t)bh * NC * DK + d;
-  float run = a.mu0 ? (float)a.t0 * a.mu0[(size_t)bh * DK + d] : 0.f;  // raw key sum
-  for (int s = 0; s < NS; ++s) {
-    const int cbeg = s * a.seg, cend = min(NC, cbeg + a.seg);
-    float tot = 0.f;
-    for (int c = cbeg; c < cend; ++c) tot += cs[(size_t)c * DK];
-    const int len = min(a.T, cend * kChunk) - cbeg * kChunk;
-    const float cen = a.centered ? tot / (float)len : 0.f;
-    const float ns = (float)(a.t0 + (int64_t)cbeg * kChunk);  // tokens before the segment
-    float mp = run - ns * cen;
-    a.cs[((size_t)bh * NS + s) * DK + d] = cen;
-    a.ms[((size_t)bh * NS + s) * DK + d] = mp;
-    for (int c = cbeg; c < cend; ++c) {
-      a.mr[((size_t)bh * NC + c) * DK + d] = mp;
-      const int rows = min(kChunk, a.T - c * kChunk);
-      mp += cs[(size_t)c * DK] - (float)rows * cen;
-    }
-    run += tot;
+  for (int c = cbeg; c < cend; ++c) {
+    a.mr[((size_t)bh * NC + c) * DK + d] = mp;
+    const int rows = min(kChunk, a.T - c * kChunk);
+    mp += cs[(size_t)c * DK] - (float)rows * cen;
   }
-  if (a.muT) a.muT[(size_t)bh * DK + d] = run / (float)(a.t0 + a.T);
+  if (a.muT && s == NS - 1) a.muT[(size_t)bh * DK + d] = (run + tot) / (float)(a.t0 + a.T);
 }
 
 // S'_s = S_s - M'_s c_s^T - c_s M'_s^T - n_s c_s c_s^T with S_s the raw second
@@ -406,9 +417,9 @@ hipError_t launch_clean_gram(const CleanArgs& a, bool is_bf16, hipStream_t st) {
 }
 
 hipError_t launch_clean_msum(const CleanArgs& a, hipStream_t st) {
-  const int nblk = a.B * a.H;
-  if (nblk == 0 || a.T == 0) return hipSuccess;
-  hipLaunchKernelGGL(clean_msum_kernel, dim3(nblk), dim3(a.dk), 0, st, a);
+  const long long nblk = (long long)a.B * a.H * n_segs(a.T, a.seg);
+  if (nblk == 0) return hipSuccess;
+  hipLaunchKernelGGL(clean_msum_kernel, dim3((unsigned)nblk), dim3(a.dk), 0, st, a);
   return hipGetLastError();
 }
 

@@ -138,6 +138,26 @@ __device__ __forceinline__ Frag<float> ld_frag_tr_acc<float>(const float* base, 
   return f;
 }
 
+// Row-operand fragment in the same k-slot order as ld_frag_tr_acc: lane l
+// reads row (l % 16) of a row-major tile at k = 4g .. 4g+3 and 16 + 4g ..
+// 16 + 4g + 3 (g = l / 16).  `tile` points at (row 0, k0); works for LDS or
+// global pointers.
+template <typename T>
+__device__ __forceinline__ Frag<T> ld_frag_acc(const T* tile, size_t ld) {
+  const int l = lane_id(), g = l >> 4;
+  const T* p = tile + (size_t)(l & 15) * ld + 4 * g;
+  Frag<T> f;
+  if constexpr (sizeof(T) == 2) {
+    const bf16x4 lo = *reinterpret_cast<const bf16x4*>(p);
+    const bf16x4 hi = *reinterpret_cast<const bf16x4*>(p + 16);
+    f.v = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  } else {
+    f.lo = *reinterpret_cast<const f32x4*>(p);
+    f.hi = *reinterpret_cast<const f32x4*>(p + 16);
+  }
+  return f;
+}
+
 // B fragment (k = accumulator row, n = accumulator column) built from two
 // accumulator tiles: x holds rows 0..15, y rows 16..31 of the k range.
 template <typename T>
@@ -152,6 +172,40 @@ __device__ __forceinline__ Frag<T> acc_pair_frag(const f32x4& x, const f32x4& y)
     f.hi = y;
   }
   return f;
+}
+
+// Storage position, within its 32-element block, that puts logical element c
+// where an accumulator pair keeps it: lane group g holds logical 4g..4g+3 and
+// 16+4g..16+4g+3, stored at 8g..8g+7.  A row written in this order is read
+// back by ld_frag / ld_frag_global (8 contiguous elements) in the k-slot order
+// of ld_frag_tr_acc / acc_pair_frag.
+__host__ __device__ __forceinline__ int acc_pos(int c) {
+  return (c & ~31) | (((c & 15) >> 2) << 3) | ((c & 16) >> 2) | (c & 3);
+}
+// Inverse of acc_pos: the logical element stored at position p.
+__host__ __device__ __forceinline__ int acc_logical(int p) {
+  return (p & ~31) | (((p >> 2) & 1) << 4) | (((p >> 3) & 3) << 2) | (p & 3);
+}
+
+// Store two accumulator tiles' lane values (x: logical 4g..4g+3, y: 16+4g..)
+// as the 8 contiguous elements at p (acc_pos order): one 16- or 32-byte store.
+template <typename T>
+__device__ __forceinline__ void store_acc_pair(T* p, const f32x4& x, const f32x4& y) {
+  if constexpr (sizeof(T) == 2) {
+    *reinterpret_cast<bf16x8*>(p) = acc_pair_frag<T>(x, y).v;
+  } else {
+    *reinterpret_cast<f32x4*>(p) = x;
+    *reinterpret_cast<f32x4*>(p + 4) = y;
+  }
+}
+
+// acc += A[16 x 16] B[16 x 16] in fp32 (four 16x16x4 steps), both operands
+// row-major in LDS: A at a (pitch lda), B at b (pitch ldb, rows = k).
+__device__ __forceinline__ void mma16_f32(f32x4& acc, const float* a, int lda, const float* b, int ldb) {
+  const int l = lane_id(), g = l >> 4, m = l & 15;
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk)
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[m * lda + 4 * kk + g], b[(4 * kk + g) * ldb + m], acc, 0, 0, 0);
 }
 
 // B fragment of the 16-column tile whose column 0 is all ones (the rest zero):

@@ -5,33 +5,41 @@
 // u_t = beta_t (v_t - alpha_t S_{t-1} k_t), and gamma_i = sum_{s<=i} log alpha_s
 // inside a chunk entered with state S_r, the rows u_i solve
 //
-//   (I + A) U = diag(beta) V - diag(beta e^gamma) K S_r^T,
+//   (I + A) U = diag(beta) (V - diag(e^gamma) K S_r^T),
 //   A_ij = beta_i e^{gamma_i - gamma_j} (k_i . k_j)  (j < i),
 //
-// i.e. with the WY/UT factors Tm = (I + A)^{-1}, Ut = Tm diag(beta) V and
-// W = Tm diag(beta e^gamma) K:  U = Ut - W S_r^T.  Then
+// so with Tm = (I + A)^{-1}:  U = Tm R,  R = diag(beta) (V - diag(e^gamma) K S_r^T).
+// Then
 //
 //   o_i     = e^{gamma_i} S_r q_i + sum_{j<=i} e^{gamma_i - gamma_j} (k_j . q_i) u_j
 //   S_{r+1} = e^{gamma_C} S_r + U^T diag(e^{gamma_C - gamma}) K.
 //
-// gdn_wy_kernel computes W (io dtype) and Ut (fp32) for every chunk in
-// parallel; gdn_state_kernel walks the chunks of one head sequentially, owning
-// a BV-row slice of S (rows of S evolve independently under this write too),
-// and stores S_r and U for every chunk; gdn_out_kernel then forms the outputs
-// of all chunks in parallel.
+// gdn_tri_kernel forms Tm for every chunk in parallel (MFMA block inversion in
+// fp32); gdn_state_kernel walks the chunks of one head in order, keeping a
+// slice of S in MFMA accumulators, and stores S_r and U for every chunk;
+// gdn_out_kernel then forms the outputs of all chunks in parallel.  S_r and
+// U^T are stored with each 32-element block in accumulator-pair order
+// (acc_pos), so the state kernel writes them with 16-byte stores and the
+// output kernel reads them as MFMA operands as they are.
 #include "ccq_device.h"
 #include "ccq_kernels.h"
 
 namespace ccq {
 
+// Tm = (I + A)^{-1} of one chunk, plus the chunk's cumulative log decays.
+// Blocks of 16: the diagonal blocks are inverted by forward substitution,
+// then wave w forms column block w, X_iw = -D_i sum_{m=w}^{i-1} A_im X_mw.
 template <typename T, int DK>
-__global__ __launch_bounds__(kThreads) void gdn_wy_kernel(const WyArgs a) {
+__global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
   constexpr int C = kChunk;
   constexpr int P = Pad<T>::value;
   constexpr int LDQ = DK + P;
+  constexpr int LDA = C + 4;  // fp32 pitch of A and X
   __shared__ __align__(16) T sK[C * LDQ];
-  __shared__ __align__(16) float sA[C * C];
-  __shared__ float sBeta[C], sGam[C];
+  __shared__ __align__(16) float sA[C * LDA];
+  __shared__ __align__(16) float sX[C * LDA];
+  __shared__ __align__(16) float sY[4][16 * 17];
+  __shared__ __align__(16) float sGam[C], sBeta[C];
 
   const int N = (a.T + C - 1) / C;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
@@ -41,16 +49,14 @@ __global__ __launch_bounds__(kThreads) void gdn_wy_kernel(const WyArgs a) {
   const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
   const int tid = threadIdx.x, w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
-  const T* k = static_cast<const T*>(a.k);
-  const T* v = static_cast<const T*>(a.v);
 
   {
     ChunkTile<T, DK> rk;
-    rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+    rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
     rk.store(sK, LDQ);
   }
   if (tid < C) {
-    const size_t ti = ((size_t)b * a.T + r0 + tid) * a.H + h;
+    const size_t ti = ((size_t)b * a.T + r0 + (tid < nrow ? tid : nrow - 1)) * a.H + h;
     float x = tid < nrow ? a.logalpha[ti] : 0.f;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
@@ -59,10 +65,11 @@ __global__ __launch_bounds__(kThreads) void gdn_wy_kernel(const WyArgs a) {
     }
     sGam[tid] = x;
     sBeta[tid] = tid < nrow ? a.beta[ti] : 0.f;
+    a.gam[((size_t)bh * N + ci) * C + tid] = x;
   }
   __syncthreads();
 
-  // A_ij = beta_i e^{gamma_i - gamma_j} (k_i . k_j), strictly lower
+  // A (strictly lower), row tile w
 #pragma unroll
   for (int J = 0; J < 4; ++J) {
     f32x4 acc = zero4();
@@ -70,275 +77,329 @@ __global__ __launch_bounds__(kThreads) void gdn_wy_kernel(const WyArgs a) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int i = 16 * w + 4 * g4 + r, j = 16 * J + c16;
-      sA[i * C + j] = (J <= w && j < i) ? sBeta[i] * __expf(sGam[i] - sGam[j]) * acc[r] : 0.f;
+      sA[i * LDA + j] = j < i ? sBeta[i] * __expf(sGam[i] - sGam[j]) * acc[r] : 0.f;
     }
   }
   __syncthreads();
 
-  // forward substitution (I + A) X = R, one right-hand-side column per thread:
-  // columns [0, DK) give W (R = diag(beta e^gamma) K), [DK, DK+dv) give Ut (R = diag(beta) V)
-  T* Wout = static_cast<T*>(a.W) + ((size_t)bh * N + ci) * C * DK;
-  float* Uout = a.Ut + ((size_t)bh * N + ci) * C * a.dv;
-  for (int col = tid; col < DK + a.dv; col += kThreads) {
-    float x[C];
-    if (col < DK) {
+  // diagonal blocks: lane l < 16 of wave w solves column l of block w
+  if (l < 16) {
+    float x[16];
+    const float* Ab = sA + 16 * w * LDA + 16 * w;
 #pragma unroll
-      for (int i = 0; i < C; ++i) x[i] = sBeta[i] * __expf(sGam[i]) * f32(sK[i * LDQ + col]);
-    } else {
-      const int cv = col - DK;
+    for (int i = 0; i < 16; ++i) {
+      float s = i == l ? 1.f : 0.f;
 #pragma unroll
-      for (int i = 0; i < C; ++i)
-        x[i] = i < nrow ? sBeta[i] * f32(v[tok_off(b, r0 + i, h, a.T, a.H, a.dv) + cv]) : 0.f;
-    }
-#pragma unroll
-    for (int i = 1; i < C; ++i) {
-      float s = x[i];
-#pragma unroll
-      for (int j = 0; j < i; ++j) s -= sA[i * C + j] * x[j];
+      for (int m = 0; m < i; ++m) s -= Ab[i * LDA + m] * x[m];
       x[i] = s;
     }
-    if (col < DK) {
 #pragma unroll
-      for (int i = 0; i < C; ++i) Wout[i * DK + col] = to<T>(x[i]);
-    } else {
+    for (int i = 0; i < 16; ++i) sX[(16 * w + i) * LDA + 16 * w + l] = x[i];
+  }
+  for (int idx = tid; idx < C * C; idx += kThreads) {
+    const int i = idx / C, j = idx % C;
+    if ((j >> 4) > (i >> 4)) sX[i * LDA + j] = 0.f;
+  }
+  __syncthreads();
+
+  // off-diagonal blocks of column block w (LDS traffic local to the wave)
+  for (int i = w + 1; i < 4; ++i) {
+    f32x4 y = zero4();
+    for (int m = w; m < i; ++m) mma16_f32(y, sA + 16 * i * LDA + 16 * m, LDA, sX + 16 * m * LDA + 16 * w, LDA);
 #pragma unroll
-      for (int i = 0; i < C; ++i) Uout[(size_t)i * a.dv + (col - DK)] = x[i];
-    }
+    for (int r = 0; r < 4; ++r) sY[w][(4 * g4 + r) * 17 + c16] = y[r];
+    f32x4 x = zero4();
+    mma16_f32(x, sX + 16 * i * LDA + 16 * i, LDA, sY[w], 17);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sX[(16 * i + 4 * g4 + r) * LDA + 16 * w + c16] = -x[r];
+  }
+  __syncthreads();
+
+  // Tm rows i, each 32-column block in acc_pos order
+  T* Tout = static_cast<T*>(a.Tm) + ((size_t)bh * N + ci) * C * C;
+  for (int idx = tid; idx < C * C; idx += kThreads) {
+    const int i = idx / C, p = idx % C;
+    Tout[idx] = to<T>(sX[i * LDA + acc_logical(p)]);
   }
 }
 
-// State recurrence over the chunks of one head for a BV-row slice of S:
-//   S_r -> states;  U = Ut - W S_r^T -> U;  S_{r+1} = e^{gamma_C} S_r + U^T diag(e^{gamma_C - gamma}) K.
-template <typename T, int DK, int BV>
-__global__ __launch_bounds__(kThreads, 1) void gdn_state_kernel(const GdnArgs a) {
-  constexpr int C = kChunk;
+// State recurrence over the chunks of one head.  Wave w of the workgroup owns
+// the 16 values v = v0 + 16 w .. of S for every key feature, held transposed
+// in MFMA accumulators (row c, column v).  Per chunk:
+//   S_r -> states;   P = K S_r^T;   R = diag(beta) (V - diag(e^gamma) P);
+//   U = Tm R -> U^T; S^T <- e^{gamma_C} S^T + K^T diag(e^{gamma_C - gamma}) U.
+// Every product takes its S, R or U operand straight from the accumulators of
+// the step before (acc_pair_frag).  K, Tm and the V slice are staged through
+// double-buffered LDS: one barrier per chunk.
+template <typename T, int DK, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) {
+  constexpr int C = kChunk, NT = 64 * NW, BVS = 16 * NW;
   constexpr int P = Pad<T>::value;
-  constexpr int LDQ = DK + P, LDV = BV + P;
-  constexpr int NTV = BV / 16;
-  constexpr int RPW = (DK / 16) / 4;  // key row tiles of S^T per wave
-  constexpr int NPW = RPW * NTV;
-  static_assert(RPW >= 1, "tile split");
+  constexpr int LDQ = DK + P, LDT = C + P, LDV = BVS + P;
+  constexpr int NCT = DK / 16;  // key-feature tiles of S^T
+  constexpr int NK = DK / 32;
 
-  __shared__ __align__(16) T sK[C * LDQ];
-  __shared__ __align__(16) T sS[BV * LDQ];   // S_r slice as [v][c]
-  __shared__ __align__(16) T sUd[C * LDV];   // U[j][v] e^{gamma_C - gamma_j}
-  __shared__ float sGam[C];
+  __shared__ __align__(16) T sK[2][C * LDQ];
+  __shared__ __align__(16) T sT[2][C * LDT];
+  __shared__ __align__(16) T sV[2][C * LDV];
+  __shared__ __align__(16) float sGam[2][C], sBeta[2][C];
 
-  const int nvt = a.dv / BV;
+  const int nvt = a.dv / BVS;
   const int N = (a.T + C - 1) / C;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
   const int bh = lb / nvt;
-  const int v0 = (lb % nvt) * BV;
-  const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
+  const int v0 = (lb % nvt) * BVS;
+  const int v = v0 + 16 * w + c16;  // this lane's value column
+  const int b = bh / a.H, h = bh % a.H;
   const T* k = static_cast<const T*>(a.k);
-  const T* Wg = static_cast<const T*>(a.W);
-  const size_t gstride = (size_t)a.H * DK;
+  const T* vin = static_cast<const T*>(a.v);
+  const T* Tg = static_cast<const T*>(a.Tm);
 
-  // state, transposed: tile u holds S[v][c] at c = 16 (w RPW + u / NTV) + 4 g4 + r,
-  // v = v0 + 16 (u % NTV) + c16
-  f32x4 S[NPW];
+  // S^T[c][v], c = 16 tc + 4 g4 + r
+  f32x4 S[NCT];
 #pragma unroll
-  for (int u = 0; u < NPW; ++u) {
-    const int tr = w * RPW + u / NTV, tv = u % NTV;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int c = 16 * tr + 4 * g4 + r, vv = v0 + 16 * tv + c16;
-      S[u][r] = a.S0 ? a.S0[((size_t)bh * a.dv + vv) * DK + c] : 0.f;
-    }
+  for (int tc = 0; tc < NCT; ++tc) {
+    if (a.S0)
+      S[tc] = *reinterpret_cast<const f32x4*>(a.S0 + ((size_t)bh * a.dv + v) * DK + 16 * tc + 4 * g4);
+    else
+      S[tc] = zero4();
   }
 
-  ChunkTile<T, DK> rk;
-  RowScalar rla;
-  Frag<T> rW[DK / 32];
-  f32x4 rU[NTV];
-  auto prefetch_k = [&](int ci) {
+  ChunkTile<T, DK, NT> rk;
+  ChunkTile<T, C, NT> rt;
+  ChunkTile<T, BVS, NT> rv;
+  RowScalar rg, rb;
+  auto prefetch = [&](int ci) {
     const int r0 = ci * C;
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-    rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-    if (tid < C) rla.load(a.logalpha + ((size_t)b * a.T + r0) * a.H + h, (size_t)a.H, tid, nrow);
+    rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+    rt.load(Tg + ((size_t)bh * N + ci) * C * C, (size_t)C, C);
+    rv.load(vin + tok_off(b, r0, h, a.T, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
+    if (tid < C) {
+      rg.load(a.gam + ((size_t)bh * N + ci) * C, 1, tid, C);
+      rb.load(a.beta + ((size_t)b * a.T + r0) * a.H + h, (size_t)a.H, tid, nrow);
+    }
   };
-  auto prefetch_wu = [&](int ci) {
-    const T* Wc = Wg + ((size_t)bh * N + ci) * C * DK + (size_t)16 * w * DK;
-#pragma unroll
-    for (int kk = 0; kk < DK / 32; ++kk) rW[kk] = ld_frag_global(Wc + 32 * kk, (size_t)DK);
-    const float* Uc = a.Ut + (((size_t)bh * N + ci) * C + 16 * w + c16) * a.dv + v0 + 4 * g4;
-#pragma unroll
-    for (int tv = 0; tv < NTV; ++tv) rU[tv] = *reinterpret_cast<const f32x4*>(Uc + 16 * tv);
-  };
-  if (N > 0) {
-    prefetch_k(0);
-    prefetch_wu(0);
-  }
+  if (N > 0) prefetch(0);
 
   for (int ci = 0; ci < N; ++ci) {
-    __syncthreads();  // (A) previous chunk's LDS readers are done
-    rk.store(sK, LDQ);
-    if (tid < C) {  // inclusive prefix of log alpha over the chunk (wave 0)
-      float x = rla.get();
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const float y = __shfl_up(x, off);
-        if (tid >= off) x += y;
-      }
-      sGam[tid] = x;
+    const int buf = ci & 1;
+    // the other buffer was released by every wave at the previous barrier
+    rk.store(sK[buf], LDQ);
+    rt.store(sT[buf], LDT);
+    rv.store(sV[buf], LDV);
+    if (tid < C) {
+      sGam[buf][tid] = rg.get();
+      sBeta[buf][tid] = rb.get();
     }
-    {
-      T* st_out = static_cast<T*>(a.states) + (((size_t)bh * N + ci) * a.dv + v0) * DK;
+    if (ci + 1 < N) prefetch(ci + 1);
+    __syncthreads();
+    const T* Kb = sK[buf];
+
+    // S_r -> states (acc_pos order)
+    T* st_out = static_cast<T*>(a.states) + (((size_t)bh * N + ci) * a.dv + v) * DK + 8 * g4;
 #pragma unroll
-      for (int u = 0; u < NPW; ++u) {
-        const int tr = w * RPW + u / NTV, tv = u % NTV;
-        const int off = (16 * tv + c16) * LDQ + 16 * tr + 4 * g4;
-        store4(sS + off, S[u][0], S[u][1], S[u][2], S[u][3]);
-        store4(st_out + (size_t)(16 * tv + c16) * DK + 16 * tr + 4 * g4, S[u][0], S[u][1], S[u][2], S[u][3]);
+    for (int m = 0; m < NK; ++m) store_acc_pair(st_out + 32 * m, S[2 * m], S[2 * m + 1]);
+
+    // P = K S_r^T, row tile J; LDS reads run one tile ahead of their products
+    Frag<T> sf[NK];
+#pragma unroll
+    for (int m = 0; m < NK; ++m) sf[m] = acc_pair_frag<T>(S[2 * m], S[2 * m + 1]);
+    f32x4 R[4];
+    Frag<T> kf[2][NK];
+#pragma unroll
+    for (int m = 0; m < NK; ++m) kf[0][m] = ld_frag_acc(Kb + 32 * m, (size_t)LDQ);
+#pragma unroll
+    for (int J = 0; J < 4; ++J) {
+      if (J + 1 < 4)
+#pragma unroll
+        for (int m = 0; m < NK; ++m) kf[(J + 1) & 1][m] = ld_frag_acc(Kb + 16 * (J + 1) * LDQ + 32 * m, (size_t)LDQ);
+      __builtin_amdgcn_sched_barrier(0);
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int m = 0; m < NK; ++m) mma(acc, kf[J & 1][m], sf[m]);
+      R[J] = acc;
+    }
+    // R = beta (V - e^gamma P); V rows 32 m + 4 g4 + r and 32 m + 16 + 4 g4 + r
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      const Frag<T> vf = ld_frag_tr_acc(sV[buf] + 32 * m * LDV + 16 * w, LDV);
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int J = 2 * m + hh;
+        const f32x4 gj = *reinterpret_cast<const f32x4*>(&sGam[buf][16 * J + 4 * g4]);
+        const f32x4 bj = *reinterpret_cast<const f32x4*>(&sBeta[buf][16 * J + 4 * g4]);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float vv;
+          if constexpr (sizeof(T) == 2) {
+            vv = f32(vf.v[4 * hh + r]);
+          } else {
+            vv = hh ? vf.hi[r] : vf.lo[r];
+          }
+          R[J][r] = bj[r] * (vv - __expf(gj[r]) * R[J][r]);
+        }
       }
     }
-    __syncthreads();  // (B)
-    if (ci + 1 < N) prefetch_k(ci + 1);
-    const float gC = sGam[C - 1];
-    {
-      // U^T tiles for rows i of stripe w: U[i][v] = Ut[i][v] - (W S_r^T)[i][v]
-      const int i = 16 * w + c16;
-      const float ud = __expf(gC - sGam[i]);
-      T* u_out = static_cast<T*>(a.U) + (((size_t)bh * N + ci) * C + i) * a.dv + v0 + 4 * g4;
+    // U = Tm R (Tm rows are stored in acc_pos order)
+    const Frag<T> rf0 = acc_pair_frag<T>(R[0], R[1]);
+    const Frag<T> rf1 = acc_pair_frag<T>(R[2], R[3]);
+    f32x4 U[4];
 #pragma unroll
-      for (int tv = 0; tv < NTV; ++tv) {
-        f32x4 acc = zero4();
-#pragma unroll
-        for (int kk = 0; kk < DK / 32; ++kk) mma(acc, ld_frag(sS + 16 * tv * LDQ + 32 * kk, LDQ), rW[kk]);
-        const float u0 = rU[tv][0] - acc[0], u1 = rU[tv][1] - acc[1];
-        const float u2 = rU[tv][2] - acc[2], u3 = rU[tv][3] - acc[3];
-        store4(u_out + 16 * tv, u0, u1, u2, u3);
-        store4(sUd + i * LDV + 16 * tv + 4 * g4, u0 * ud, u1 * ud, u2 * ud, u3 * ud);
-      }
-      if (ci + 1 < N) prefetch_wu(ci + 1);
+    for (int I = 0; I < 4; ++I) {
+      U[I] = zero4();
+      mma(U[I], ld_frag(sT[buf] + 16 * I * LDT, LDT), rf0);
+      mma(U[I], ld_frag(sT[buf] + 16 * I * LDT + 32, LDT), rf1);
     }
-    __syncthreads();  // (C)
-    // S^T <- e^{gamma_C} S^T + K^T Ud
+    // U^T -> [v][j] (acc_pos order), then U e^{gamma_C - gamma_i}
+    T* u_out = static_cast<T*>(a.U) + (((size_t)bh * N + ci) * a.dv + v) * C + 8 * g4;
+    store_acc_pair(u_out, U[0], U[1]);
+    store_acc_pair(u_out + 32, U[2], U[3]);
+    const float gC = sGam[buf][C - 1];
+#pragma unroll
+    for (int I = 0; I < 4; ++I) {
+      const f32x4 gi = *reinterpret_cast<const f32x4*>(&sGam[buf][16 * I + 4 * g4]);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) U[I][r] *= __expf(gC - gi[r]);
+    }
+    const Frag<T> ud0 = acc_pair_frag<T>(U[0], U[1]);
+    const Frag<T> ud1 = acc_pair_frag<T>(U[2], U[3]);
     const float eC = __expf(gC);
+    constexpr int TB = 4;  // key-feature tiles per batch of transposing reads
+    Frag<T> tf[2][TB][2];
 #pragma unroll
-    for (int u = 0; u < NPW; ++u)
+    for (int t = 0; t < TB; ++t) {
+      tf[0][t][0] = ld_frag_tr_acc(Kb + 16 * t, LDQ);
+      tf[0][t][1] = ld_frag_tr_acc(Kb + 32 * LDQ + 16 * t, LDQ);
+    }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) S[u][r] *= eC;
+    for (int tb = 0; tb < NCT / TB; ++tb) {
+      if (tb + 1 < NCT / TB)
 #pragma unroll
-    for (int k0 = 0; k0 < C; k0 += 32) {
-      Frag<T> fb[NTV];
+        for (int t = 0; t < TB; ++t) {
+          const int tc = TB * (tb + 1) + t;
+          tf[(tb + 1) & 1][t][0] = ld_frag_tr_acc(Kb + 16 * tc, LDQ);
+          tf[(tb + 1) & 1][t][1] = ld_frag_tr_acc(Kb + 32 * LDQ + 16 * tc, LDQ);
+        }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int tv = 0; tv < NTV; ++tv) fb[tv] = ld_frag_tr(sUd + k0 * LDV + 16 * tv, LDV);
-#pragma unroll
-      for (int rr = 0; rr < RPW; ++rr) {
-        const Frag<T> fa = ld_frag_tr(sK + k0 * LDQ + 16 * (w * RPW + rr), LDQ);
-#pragma unroll
-        for (int tv = 0; tv < NTV; ++tv) mma(S[rr * NTV + tv], fa, fb[tv]);
+      for (int t = 0; t < TB; ++t) {
+        const int tc = TB * tb + t;
+        S[tc] *= eC;
+        mma(S[tc], tf[tb & 1][t][0], ud0);
+        mma(S[tc], tf[tb & 1][t][1], ud1);
       }
     }
   }
 
   if (a.ST) {
 #pragma unroll
-    for (int u = 0; u < NPW; ++u) {
-      const int tr = w * RPW + u / NTV, tv = u % NTV;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int c = 16 * tr + 4 * g4 + r, vv = v0 + 16 * tv + c16;
-        a.ST[((size_t)bh * a.dv + vv) * DK + c] = S[u][r];
-      }
-    }
+    for (int tc = 0; tc < NCT; ++tc)
+      *reinterpret_cast<f32x4*>(a.ST + ((size_t)bh * a.dv + v) * DK + 16 * tc + 4 * g4) = S[tc];
   }
 }
 
-// Output of one chunk for a 64-wide value slice (eight waves):
-//   o_i = scale * (e^{gamma_i} (S_r q_i) + sum_{j<=i} e^{gamma_i - gamma_j} (k_j . q_i) u_j)
-
-template <typename T, int DK>
+// Outputs of one chunk (eight waves).  The decayed, masked scores
+//   P_ij = e^{gamma_i - gamma_j} (q_i . k_j)  (j <= i)
+// are formed once (ten nonzero 16 x 16 tiles over the waves) and kept in LDS;
+// wave w then owns VPW value tiles for IPW token tiles and forms, transposed,
+//   O^T = e^{gamma_i} (S_r Q^T) + U^T P^T,
+// with rows of S_r and U^T read straight from global memory as MFMA operands.
+template <typename T, int DK, int VPW, int IPW>
 __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArgs a) {
-  constexpr int C = kChunk, BVO = 64;
+  constexpr int C = kChunk;
   constexpr int P = Pad<T>::value;
-  constexpr int LDQ = DK + P, LDV = BVO + P, LDA = C + P;
+  constexpr int LDQ = DK + P, LDP = C + P;
+  constexpr int NK = DK / 32;
+  constexpr int NIG = 4 / IPW;  // token-tile groups
+  constexpr int NVG = 8 / NIG;  // value-tile groups
+  static_assert(NVG * NIG == 8, "wave split");
 
   __shared__ __align__(16) T sQ[C * LDQ];
   __shared__ __align__(16) T sK[C * LDQ];
-  __shared__ __align__(16) T sS[BVO * LDQ];  // S_r rows v0.. as [v][c]
-  __shared__ __align__(16) T sU[C * LDV];
-  __shared__ __align__(16) T sA[C * LDA];
-  __shared__ float sGam[C];
+  __shared__ __align__(16) T sP[C * LDP];  // P[i][acc_pos(j)]
+  __shared__ __align__(16) float sGam[C];
 
-  const int nvt = a.dv / BVO;
   const int N = (a.T + C - 1) / C;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int vt = lb % nvt, ci = (lb / nvt) % N, bh = lb / (nvt * N);
-  const int v0 = vt * BVO;
+  const int bh = lb / N, ci = lb % N;
   const int b = bh / a.H, h = bh % a.H;
   const int r0 = ci * C;
   const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
   const int tid = threadIdx.x, w = tid >> 6, l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
+  const int vg = w % NVG, ig = w / NVG;
   const size_t gstride = (size_t)a.H * DK;
+
+  // this wave's S_r and U^T fragments (rows v, acc_pos order), issued first
+  const T* Sg = static_cast<const T*>(a.states) + ((size_t)bh * N + ci) * a.dv * DK;
+  const T* Ug = static_cast<const T*>(a.U) + ((size_t)bh * N + ci) * a.dv * C;
+  Frag<T> sfr[VPW][NK], ufr[VPW][2];
+#pragma unroll
+  for (int vt = 0; vt < VPW; ++vt) {
+    const int vr = 16 * (vg * VPW + vt);
+#pragma unroll
+    for (int m = 0; m < NK; ++m) sfr[vt][m] = ld_frag_global(Sg + (size_t)vr * DK + 32 * m, (size_t)DK);
+#pragma unroll
+    for (int m = 0; m < 2; ++m) ufr[vt][m] = ld_frag_global(Ug + (size_t)vr * C + 32 * m, (size_t)C);
+  }
   {
-    ChunkTile<T, DK, kOutThreads> rq, rk, rs;
-    ChunkTile<T, BVO, kOutThreads> ru;
+    ChunkTile<T, DK, kOutThreads> rq, rk;
     rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
     rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-    rs.load(static_cast<const T*>(a.states) + (((size_t)bh * N + ci) * a.dv + v0) * DK, (size_t)DK, C);
-    ru.load(static_cast<const T*>(a.U) + ((size_t)bh * N + ci) * C * a.dv + v0, (size_t)a.dv, C);
+    if (tid < C) sGam[tid] = a.gam[((size_t)bh * N + ci) * C + tid];
     rq.store(sQ, LDQ);
     rk.store(sK, LDQ);
-    rs.store(sS, LDQ);
-    ru.store(sU, LDV);
-    if (tid < C) {
-      RowScalar rla;
-      rla.load(a.logalpha + ((size_t)b * a.T + r0) * a.H + h, (size_t)a.H, tid, nrow);
-      float x = rla.get();
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const float y = __shfl_up(x, off);
-        if (tid >= off) x += y;
-      }
-      sGam[tid] = x;
-    }
   }
   __syncthreads();
-  // intra block: ten lower tiles (I >= J) round-robin over the waves, six zero tiles
-  {
+
+  // P tiles: ten lower tiles (I >= J) over the waves, the six upper ones zero;
+  // computed transposed (row j, column i) and stored as rows i
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const int t = w + 8 * s;
-      const int I = intra_tile_row(t), J = intra_tile_col(t);
-      const int i = 16 * I + c16;
-      float x[4] = {0.f, 0.f, 0.f, 0.f};
-      if (t < 10) {
-        f32x4 sc = zero4();
-        tile_mma<T, DK>(sc, sK + 16 * J * LDQ, LDQ, sQ + 16 * I * LDQ, LDQ);
-        const float gi = sGam[i];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int j = 16 * J + 4 * g4 + r;
-          x[r] = j <= i ? sc[r] * __expf(gi - sGam[j]) : 0.f;
-        }
-      }
-      store4(sA + i * LDA + 16 * J + 4 * g4, x[0], x[1], x[2], x[3]);
-    }
-  }
-  __syncthreads();
-  // o tiles: stripe w % 4, value tiles 2 (w / 4) and 2 (w / 4) + 1
-  {
-    const int st = w & 3;
-    T* o = static_cast<T*>(a.o);
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const int tv = 2 * (w >> 2) + s;
-      f32x4 a1 = zero4(), a2 = zero4();
-      tile_mma<T, DK>(a1, sQ + 16 * st * LDQ, LDQ, sS + 16 * tv * LDQ, LDQ);
-#pragma unroll
-      for (int k0 = 0; k0 < C; k0 += 32)
-        if (k0 <= 16 * st) mma(a2, ld_frag(sA + 16 * st * LDA + k0, LDA), ld_frag_tr(sU + k0 * LDV + 16 * tv, LDV));
+  for (int s = 0; s < 2; ++s) {
+    const int t = w + 8 * s;
+    const int I = intra_tile_row(t), J = intra_tile_col(t);
+    const int i = 16 * I + c16;
+    float x[4] = {0.f, 0.f, 0.f, 0.f};
+    if (t < 10) {
+      f32x4 sc = zero4();
+      tile_mma<T, DK>(sc, sK + 16 * J * LDQ, LDQ, sQ + 16 * I * LDQ, LDQ);
+      const float gi = sGam[i];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int i = 16 * st + 4 * g4 + r;
-        if (i < nrow)
-          o[tok_off(b, r0 + i, h, a.T, a.H, a.dv) + v0 + 16 * tv + c16] =
-              to<T>(a.scale * (__expf(sGam[i]) * a1[r] + a2[r]));
+        const int j = 16 * J + 4 * g4 + r;
+        x[r] = j <= i ? sc[r] * __expf(gi - sGam[j]) : 0.f;
+      }
+    }
+    store4(sP + i * LDP + acc_pos(16 * J + 4 * g4), x[0], x[1], x[2], x[3]);
+  }
+  __syncthreads();
+
+  T* o = static_cast<T*>(a.o);
+#pragma unroll
+  for (int it = 0; it < IPW; ++it) {
+    const int I = ig * IPW + it;
+    const int i = 16 * I + c16;
+    Frag<T> qf[NK];
+#pragma unroll
+    for (int m = 0; m < NK; ++m) qf[m] = ld_frag_acc(sQ + 16 * I * LDQ + 32 * m, (size_t)LDQ);
+    const Frag<T> pf0 = ld_frag(sP + 16 * I * LDP, LDP);
+    const Frag<T> pf1 = ld_frag(sP + 16 * I * LDP + 32, LDP);
+    const float ei = __expf(sGam[i]);
+#pragma unroll
+    for (int vt = 0; vt < VPW; ++vt) {
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int m = 0; m < NK; ++m) mma(acc, sfr[vt][m], qf[m]);
+      acc *= ei;
+      mma(acc, ufr[vt][0], pf0);
+      if (I >= 2) mma(acc, ufr[vt][1], pf1);  // keys 32..63 precede row i only for I >= 2
+      if (i < nrow) {
+        const int vcol = 16 * (vg * VPW + vt) + 4 * g4;
+        store4(o + tok_off(b, r0 + i, h, a.T, a.H, a.dv) + vcol, a.scale * acc[0], a.scale * acc[1],
+               a.scale * acc[2], a.scale * acc[3]);
       }
     }
   }
@@ -346,26 +407,36 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
 
 namespace {
 template <typename T, int DK>
-hipError_t run_wy(const WyArgs& a, hipStream_t st) {
+hipError_t run_tri(const TriArgs& a, hipStream_t st) {
   const int N = (a.T + kChunk - 1) / kChunk;
   const int nblk = a.B * a.H * N;
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((gdn_wy_kernel<T, DK>), dim3(nblk), dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((gdn_tri_kernel<T, DK>), dim3(nblk), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
-template <typename T, int DK, int BV>
+template <typename T, int DK, int NW>
 hipError_t run_gdn_state(const GdnArgs& a, hipStream_t st) {
-  const int nblk = a.B * a.H * (a.dv / BV);
+  const int nblk = a.B * a.H * (a.dv / (16 * NW));
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((gdn_state_kernel<T, DK, BV>), dim3(nblk), dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((gdn_state_kernel<T, DK, NW>), dim3(nblk), dim3(64 * NW), 0, st, a);
+  return hipGetLastError();
+}
+template <typename T, int DK, int VPW, int IPW>
+hipError_t run_gdn_out_v(const GdnOutArgs& a, hipStream_t st) {
+  const int nblk = a.B * a.H * ((a.T + kChunk - 1) / kChunk);
+  if (nblk == 0) return hipSuccess;
+  hipLaunchKernelGGL((gdn_out_kernel<T, DK, VPW, IPW>), dim3(nblk), dim3(kOutThreads), 0, st, a);
   return hipGetLastError();
 }
 template <typename T, int DK>
 hipError_t run_gdn_out(const GdnOutArgs& a, hipStream_t st) {
-  const int nblk = a.B * a.H * ((a.T + kChunk - 1) / kChunk) * (a.dv / 64);
-  if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((gdn_out_kernel<T, DK>), dim3(nblk), dim3(kOutThreads), 0, st, a);
-  return hipGetLastError();
+  switch (a.dv) {
+    case 64: return run_gdn_out_v<T, DK, 1, 2>(a, st);
+    case 128: return run_gdn_out_v<T, DK, 1, 4>(a, st);
+    case 256: return run_gdn_out_v<T, DK, 2, 4>(a, st);
+    case 512: return run_gdn_out_v<T, DK, 4, 4>(a, st);
+  }
+  return hipErrorInvalidValue;
 }
 }  // namespace
 
@@ -375,33 +446,36 @@ bool gdn_supported(int dk, int dv, bool is_bf16) {
   return dv_ok && (dk == 64 || dk == 128);
 }
 
-hipError_t launch_gdn_wy(const WyArgs& a, bool is_bf16, hipStream_t st) {
+hipError_t launch_gdn_tri(const TriArgs& a, bool is_bf16, hipStream_t st) {
   if (is_bf16) {
     switch (a.dk) {
-      case 64: return run_wy<bf16_t, 64>(a, st);
-      case 128: return run_wy<bf16_t, 128>(a, st);
-      case 256: return run_wy<bf16_t, 256>(a, st);
+      case 64: return run_tri<bf16_t, 64>(a, st);
+      case 128: return run_tri<bf16_t, 128>(a, st);
+      case 256: return run_tri<bf16_t, 256>(a, st);
     }
   } else {
     switch (a.dk) {
-      case 64: return run_wy<float, 64>(a, st);
-      case 128: return run_wy<float, 128>(a, st);
+      case 64: return run_tri<float, 64>(a, st);
+      case 128: return run_tri<float, 128>(a, st);
     }
   }
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_gdn_state(const GdnArgs& a, bool is_bf16, hipStream_t st) {
+  // four waves (64 values) per workgroup when that still gives every CU a
+  // workgroup, else two (dv >= 64, so both divide dv)
+  const bool wide = (long long)a.B * a.H * (a.dv / 64) >= 256;
   if (is_bf16) {
     switch (a.dk) {
-      case 64: return run_gdn_state<bf16_t, 64, 64>(a, st);
-      case 128: return run_gdn_state<bf16_t, 128, 64>(a, st);
-      case 256: return run_gdn_state<bf16_t, 256, 32>(a, st);
+      case 64: return wide ? run_gdn_state<bf16_t, 64, 4>(a, st) : run_gdn_state<bf16_t, 64, 2>(a, st);
+      case 128: return wide ? run_gdn_state<bf16_t, 128, 4>(a, st) : run_gdn_state<bf16_t, 128, 2>(a, st);
+      case 256: return wide ? run_gdn_state<bf16_t, 256, 4>(a, st) : run_gdn_state<bf16_t, 256, 2>(a, st);
     }
   } else {
     switch (a.dk) {
-      case 64: return run_gdn_state<float, 64, 64>(a, st);
-      case 128: return run_gdn_state<float, 128, 32>(a, st);
+      case 64: return wide ? run_gdn_state<float, 64, 4>(a, st) : run_gdn_state<float, 64, 2>(a, st);
+      case 128: return wide ? run_gdn_state<float, 128, 4>(a, st) : run_gdn_state<float, 128, 2>(a, st);
     }
   }
   return hipErrorInvalidValue;

@@ -33,6 +33,7 @@ struct CleanArgs {
   float* gram;        // [B*H, NS, dk, dk] raw segment sums of k k^T
   void* sprime;       // [B*H, NS, dk, dk] io: entry second moment about c_s
   float* csum;        // [B*H, NC, dk] key sum of every chunk
+  float* ssum;        // [B*H, NS, dk] key sum of every segment
   float* mr;          // [B*H, NC, dk] key sum before the chunk, about c_s
   float* cs;          // [B*H, NS, dk] centre c_s of each segment
   float* ms;          // [B*H, NS, dk] raw key sum before each segment
@@ -66,14 +67,14 @@ struct GlaOutArgs {
   float scale;
 };
 
-// Gated DeltaNet WY/UT chunk transform (chunk-parallel).
-struct WyArgs {
+// Gated DeltaNet chunk transform (chunk-parallel): Tm = (I + A)^{-1} and the
+// within-chunk cumulative log decays gamma.
+struct TriArgs {
   const void* k;         // [B,T,H,dk] io
-  const void* v;         // [B,T,H,dv] io
   const float* logalpha; // [B,T,H]
   const float* beta;     // [B,T,H]
-  void* W;               // [B*H, N, C, dk] io (workspace)
-  float* Ut;             // [B*H, N, C, dv] fp32 (workspace)
+  void* Tm;              // [B*H, N, C, C] io (workspace), columns in acc_pos order
+  float* gam;            // [B*H, N, C] fp32 (workspace)
   int B, T, H, dk, dv;
 };
 
@@ -81,23 +82,24 @@ struct WyArgs {
 // chunk-entry states S_r and the corrected values U of every chunk.
 struct GdnArgs {
   const void* k;         // [B,T,H,dk] io
-  const float* logalpha; // [B,T,H]
-  const void* W;         // workspace, as WyArgs
-  const float* Ut;       // workspace, as WyArgs
+  const void* v;         // [B,T,H,dv] io
+  const float* beta;     // [B,T,H]
+  const void* Tm;        // workspace, as TriArgs
+  const float* gam;      // workspace, as TriArgs
   const float* S0;       // [B,H,dv,dk] or null
   float* ST;             // [B,H,dv,dk] or null
-  void* states;          // [B*H, N, dv, dk] io (workspace)
-  void* U;               // [B*H, N, C, dv] io (workspace)
+  void* states;          // [B*H, N, dv, dk] io (workspace), dk in acc_pos order
+  void* U;               // [B*H, N, dv, C] io (workspace): U^T, C in acc_pos order
   int B, T, H, dk, dv;
 };
 
-// Gated DeltaNet output, one workgroup per (chunk, 64-wide value slice).
+// Gated DeltaNet output, one workgroup per chunk.
 struct GdnOutArgs {
   const void* qc;        // [B,T,H,dk] io (cleaned queries)
   const void* k;         // [B,T,H,dk] io
-  const float* logalpha; // [B,T,H]
-  const void* states;    // [B*H, N, dv, dk] io
-  const void* U;         // [B*H, N, C, dv] io
+  const float* gam;      // workspace, as TriArgs
+  const void* states;    // as GdnArgs
+  const void* U;         // as GdnArgs
   void* o;               // [B,T,H,dv] io
   int B, T, H, dk, dv;
   float scale;
@@ -163,7 +165,7 @@ hipError_t launch_clean_out(const CleanArgs& a, bool is_bf16, hipStream_t st);
 constexpr int kCleanSeg = 8;   // chunks per segment of the query contraction
 hipError_t launch_gla_state(const GlaStateArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
 hipError_t launch_gla_out(const GlaOutArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
-hipError_t launch_gdn_wy(const WyArgs& a, bool is_bf16, hipStream_t st);
+hipError_t launch_gdn_tri(const TriArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_gdn_state(const GdnArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_gdn_out(const GdnOutArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_copy_or_zero(float* dst, const float* src, size_t n, hipStream_t st);
