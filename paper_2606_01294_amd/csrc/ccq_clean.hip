@@ -83,7 +83,7 @@ __global__ __launch_bounds__(kThreads) void clean_gram_kernel(const CleanArgs a)
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[v][t] = zero4();
 
-  ChunkTile<T, DK> rk;
+  RowTile<T, DK> rk;
   auto load = [&](int c) {
     rk.load(k + tok_off(b, c * C, h, a.T, a.H, DK), gstride, min(C, a.T - c * C));
   };
@@ -211,7 +211,7 @@ template <typename T, int DK>
 __global__ __launch_bounds__(kThreads, 2) void clean_out_kernel(const CleanArgs a) {
   constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P;
   constexpr int NK = DK / 32, NN = DK / 16;
-  typedef typename ChunkTile<T, DK>::vec_t vec_t;
+  typedef typename RowTile<T, DK>::vec_t vec_t;
   __shared__ __align__(16) T sK[2][C * LDK];
   __shared__ __align__(16) float sC[DK], sMr[DK], sMs[DK];
 
@@ -245,7 +245,7 @@ __global__ __launch_bounds__(kThreads, 2) void clean_out_kernel(const CleanArgs 
       }
     }
   }
-  ChunkTile<T, DK> rk;
+  RowTile<T, DK> rk;
   auto load_block = [&](int c) {
     rk.load(k + tok_off(b, c * C, h, a.T, a.H, DK), gstride, min(C, a.T - c * C));
   };
@@ -291,13 +291,13 @@ __global__ __launch_bounds__(kThreads, 2) void clean_out_kernel(const CleanArgs 
     // centred keys of block jb; the other buffer may still be read by a
     // wave working on block jb - 1, this one was released by the last barrier
 #pragma unroll
-    for (int u = 0; u < ChunkTile<T, DK>::NV; ++u) {
+    for (int u = 0; u < RowTile<T, DK>::NV; ++u) {
       const vec_t kv = rk.get(u);
-      const int col = ChunkTile<T, DK>::col(u);
+      const int col = RowTile<T, DK>::col(u);
       vec_t y;
 #pragma unroll
       for (int e = 0; e < 8; ++e) y[e] = to<T>(f32(kv[e]) - sC[col + e]);
-      *reinterpret_cast<vec_t*>(buf + ChunkTile<T, DK>::row() * LDK + col) = y;
+      *reinterpret_cast<vec_t*>(buf + RowTile<T, DK>::row(u) * LDK + col) = y;
     }
     if (jb < ch) load_block(jb + 1);
     __syncthreads();

@@ -354,6 +354,46 @@ struct ChunkTile {
   }
 };
 
+// One 64-row chunk of a [*, D] token tensor staged for a row-major LDS copy,
+// with coalesced global loads: vector e = tid + NT u (8 elements) is row
+// e / (D / 8), column 8 (e % (D / 8)), so consecutive lanes read consecutive
+// 16- or 32-byte pieces of a row and one wave instruction covers whole rows.
+// Rows >= n read row n - 1 and are zeroed at use, so issuing the loads never
+// waits for data.
+template <typename T, int D, int NT = kThreads>
+struct RowTile {
+  static constexpr int VE = 8;
+  static constexpr int VPR = D / VE;             // vectors per row
+  static constexpr int NV = kChunk * VPR / NT;   // vectors per thread
+  static_assert(D % VE == 0 && NV >= 1 && kChunk * VPR % NT == 0, "tile split");
+  typedef T vec_t __attribute__((ext_vector_type(VE)));
+  vec_t v[NV];
+  uint32_t ok;  // bit u: vector u's row lies inside the sequence
+
+  __device__ __forceinline__ static int row(int u) { return ((int)threadIdx.x + NT * u) / VPR; }
+  __device__ __forceinline__ static int col(int u) { return (((int)threadIdx.x + NT * u) % VPR) * VE; }
+
+  __device__ __forceinline__ void load(const T* src, size_t gstride, int n) {
+    ok = 0;
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      const int r = row(u);
+      ok |= (r < n ? 1u : 0u) << u;
+      v[u] = *reinterpret_cast<const vec_t*>(src + (size_t)(r < n ? r : n - 1) * gstride + col(u));
+    }
+  }
+  __device__ __forceinline__ vec_t get(int u) const {
+    vec_t z;
+#pragma unroll
+    for (int e = 0; e < VE; ++e) z[e] = static_cast<T>(0.f);
+    return ((ok >> u) & 1u) ? v[u] : z;
+  }
+  __device__ __forceinline__ void store(T* dst, int ld) const {
+#pragma unroll
+    for (int u = 0; u < NV; ++u) *reinterpret_cast<vec_t*>(dst + row(u) * ld + col(u)) = get(u);
+  }
+};
+
 // Scalar per-token value prefetched by lane `row` (clamped address, zeroed at use).
 struct RowScalar {
   float x;

@@ -18,9 +18,10 @@
 // fp32); gdn_state_kernel walks the chunks of one head in order, keeping a
 // slice of S in MFMA accumulators, and stores S_r and U for every chunk;
 // gdn_out_kernel then forms the outputs of all chunks in parallel.  S_r and
-// U^T are stored with each 32-element block in accumulator-pair order
-// (acc_pos), so the state kernel writes them with 16-byte stores and the
-// output kernel reads them as MFMA operands as they are.
+// U^T are stored fragment-native: per 16-row value tile and 32-wide k step a
+// contiguous 16 x 32 block, each row in accumulator-pair order (acc_pos), so
+// the state kernel writes and the output kernel reads 1 KB per instruction,
+// already in MFMA operand order.
 #include "ccq_device.h"
 #include "ccq_kernels.h"
 
@@ -51,7 +52,7 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
   const int g4 = l >> 4, c16 = l & 15;
 
   {
-    ChunkTile<T, DK> rk;
+    RowTile<T, DK> rk;
     rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
     rk.store(sK, LDQ);
   }
@@ -167,9 +168,9 @@ __global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) 
       S[tc] = zero4();
   }
 
-  ChunkTile<T, DK, NT> rk;
-  ChunkTile<T, C, NT> rt;
-  ChunkTile<T, BVS, NT> rv;
+  RowTile<T, DK, NT> rk;
+  RowTile<T, C, NT> rt;
+  RowTile<T, BVS, NT> rv;
   RowScalar rg, rb;
   auto prefetch = [&](int ci) {
     const int r0 = ci * C;
@@ -198,10 +199,12 @@ __global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) 
     __syncthreads();
     const T* Kb = sK[buf];
 
-    // S_r -> states (acc_pos order)
-    T* st_out = static_cast<T*>(a.states) + (((size_t)bh * N + ci) * a.dv + v) * DK + 8 * g4;
+    // S_r -> states, fragment-native: 1 KB per (value tile, k step)
+    const int vt = (v0 >> 4) + w;
+    T* st_out = static_cast<T*>(a.states) + ((size_t)bh * N + ci) * a.dv * DK +
+                ((size_t)vt * NK * 16 + c16) * 32 + 8 * g4;
 #pragma unroll
-    for (int m = 0; m < NK; ++m) store_acc_pair(st_out + 32 * m, S[2 * m], S[2 * m + 1]);
+    for (int m = 0; m < NK; ++m) store_acc_pair(st_out + 16 * 32 * m, S[2 * m], S[2 * m + 1]);
 
     // P = K S_r^T, row tile J; LDS reads run one tile ahead of their products
     Frag<T> sf[NK];
@@ -254,9 +257,9 @@ __global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) 
       mma(U[I], ld_frag(sT[buf] + 16 * I * LDT + 32, LDT), rf1);
     }
     // U^T -> [v][j] (acc_pos order), then U e^{gamma_C - gamma_i}
-    T* u_out = static_cast<T*>(a.U) + (((size_t)bh * N + ci) * a.dv + v) * C + 8 * g4;
+    T* u_out = static_cast<T*>(a.U) + ((size_t)bh * N + ci) * a.dv * C + ((size_t)vt * 2 * 16 + c16) * 32 + 8 * g4;
     store_acc_pair(u_out, U[0], U[1]);
-    store_acc_pair(u_out + 32, U[2], U[3]);
+    store_acc_pair(u_out + 16 * 32, U[2], U[3]);
     const float gC = sGam[buf][C - 1];
 #pragma unroll
     for (int I = 0; I < 4; ++I) {
@@ -333,20 +336,20 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
   const int vg = w % NVG, ig = w / NVG;
   const size_t gstride = (size_t)a.H * DK;
 
-  // this wave's S_r and U^T fragments (rows v, acc_pos order), issued first
+  // this wave's S_r and U^T fragments (fragment-native, 1 KB each), issued first
   const T* Sg = static_cast<const T*>(a.states) + ((size_t)bh * N + ci) * a.dv * DK;
   const T* Ug = static_cast<const T*>(a.U) + ((size_t)bh * N + ci) * a.dv * C;
   Frag<T> sfr[VPW][NK], ufr[VPW][2];
 #pragma unroll
   for (int vt = 0; vt < VPW; ++vt) {
-    const int vr = 16 * (vg * VPW + vt);
+    const int vtile = vg * VPW + vt;
 #pragma unroll
-    for (int m = 0; m < NK; ++m) sfr[vt][m] = ld_frag_global(Sg + (size_t)vr * DK + 32 * m, (size_t)DK);
+    for (int m = 0; m < NK; ++m) sfr[vt][m] = ld_frag_global(Sg + ((size_t)vtile * NK + m) * 16 * 32, 32);
 #pragma unroll
-    for (int m = 0; m < 2; ++m) ufr[vt][m] = ld_frag_global(Ug + (size_t)vr * C + 32 * m, (size_t)C);
+    for (int m = 0; m < 2; ++m) ufr[vt][m] = ld_frag_global(Ug + ((size_t)vtile * 2 + m) * 16 * 32, 32);
   }
   {
-    ChunkTile<T, DK, kOutThreads> rq, rk;
+    RowTile<T, DK, kOutThreads> rq, rk;
     rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
     rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
     if (tid < C) sGam[tid] = a.gam[((size_t)bh * N + ci) * C + tid];

@@ -88,8 +88,9 @@ struct GdnArgs {
   const float* gam;      // workspace, as TriArgs
   const float* S0;       // [B,H,dv,dk] or null
   float* ST;             // [B,H,dv,dk] or null
-  void* states;          // [B*H, N, dv, dk] io (workspace), dk in acc_pos order
-  void* U;               // [B*H, N, dv, C] io (workspace): U^T, C in acc_pos order
+  void* states;          // [B*H, N, dv/16, dk/32, 16, 32] io (workspace): S_r, rows
+                         // in acc_pos order (fragment-native)
+  void* U;               // [B*H, N, dv/16, 2, 16, 32] io (workspace): U^T, likewise
   int B, T, H, dk, dv;
 };
 
