@@ -170,7 +170,8 @@ __global__ void clean_msum_kernel(const CleanArgs a) {
 
 // S'_s = S_s - M'_s c_s^T - c_s M'_s^T - n_s c_s c_s^T with S_s the raw second
 // moment before segment s (prefix of the Gram matrices, fp32) and M'_s the key
-// sum about c_s; four elements per thread.  Also the final Cbar_T.
+// sum about c_s; four elements per thread.  S'_s is stored in 64-column
+// slices, each a contiguous [dk][64] block.  Also the final Cbar_T.
 template <typename T, int DK>
 __global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
   constexpr int PER = DK * DK / 4 / 256;  // workgroups per head
@@ -192,7 +193,7 @@ __global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
     f32x4 o;
 #pragma unroll
     for (int q = 0; q < 4; ++q) o[q] = acc[q] - ma * cb4[q] - ca * mb4[q] - ns * ca * cb4[q];
-    store4(Sp + (so * DK + ra) * DK + cb, o[0], o[1], o[2], o[3]);
+    store4(Sp + so * DK * DK + ((size_t)(cb >> 6) * DK + ra) * 64 + (cb & 63), o[0], o[1], o[2], o[3]);
     acc += g;
   }
   if (a.CT)
@@ -203,16 +204,20 @@ __global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
 // One workgroup per chunk; wave w owns rows i = 16 w .. 16 w + 15.  All
 // products are kept transposed (output feature n in the accumulator row, token
 // i in its column) so that score tiles feed the next product from registers:
-//   acc^T  = S'_s x^T                                   (S' rows from L2)
+//   acc^T  = S'_s x^T               (S' staged through LDS one 64-column slice
+//                                     at a time, double-buffered)
 //   sc^T   = K'_blk x^T,  acc^T += K'_blk^T sc^T        (each block of the segment)
+// The slice buffers are reused for the key blocks.
 // On the diagonal block the scores are masked to j <= i and shifted by
 // -cq'_i / t_i, which folds the within-chunk part of m'_i into the product.
 template <typename T, int DK>
 __global__ __launch_bounds__(kThreads, 2) void clean_out_kernel(const CleanArgs a) {
-  constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P;
-  constexpr int NK = DK / 32, NN = DK / 16;
+  constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P, LDP = 64 + P;
+  constexpr int NK = DK / 32, NN = DK / 16, NP = DK / 64;
+  constexpr int BUF = (DK * LDP > C * LDK) ? DK * LDP : C * LDK;  // elements per buffer
+  constexpr int NVS = DK * 64 / 8 / kThreads;                     // slice vectors per thread
   typedef typename RowTile<T, DK>::vec_t vec_t;
-  __shared__ __align__(16) T sK[2][C * LDK];
+  __shared__ __align__(16) T sbuf[2 * BUF];
   __shared__ __align__(16) float sC[DK], sMr[DK], sMs[DK];
 
   const int NC = n_chunks(a.T), NS = n_segs(a.T, a.seg);
@@ -256,17 +261,36 @@ __global__ __launch_bounds__(kThreads, 2) void clean_out_kernel(const CleanArgs 
     sMr[d] = a.mr[((size_t)bh * NC + ch) * DK + d];
   }
 
-  // entry term S'_s x_i
+  // entry term S'_s x_i, one 64-column slice of S' per step
   f32x4 acc[NN];
-  const T* sp = static_cast<const T*>(a.sprime) + so * DK * DK;
 #pragma unroll
-  for (int tn = 0; tn < NN; ++tn) {
-    acc[tn] = zero4();
+  for (int tn = 0; tn < NN; ++tn) acc[tn] = zero4();
+  {
+    const T* sp = static_cast<const T*>(a.sprime) + so * DK * DK;
+    vec_t ps[NVS];
+    auto load_slice = [&](int p) {
 #pragma unroll
-    for (int kk = 0; kk < NK; ++kk)
-      mma(acc[tn], ld_frag_global(sp + (size_t)(16 * tn) * DK + 32 * kk, (size_t)DK), qf[kk]);
+      for (int u = 0; u < NVS; ++u)
+        ps[u] = *reinterpret_cast<const vec_t*>(sp + (size_t)p * DK * 64 + (size_t)(tid + kThreads * u) * 8);
+    };
+    load_slice(0);
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      T* pb = sbuf + (p & 1) * BUF;
+#pragma unroll
+      for (int u = 0; u < NVS; ++u) {
+        const int e = tid + kThreads * u;
+        *reinterpret_cast<vec_t*>(pb + (e >> 3) * LDP + 8 * (e & 7)) = ps[u];
+      }
+      if (p + 1 < NP) load_slice(p + 1);
+      __syncthreads();  // (also publishes sC, sMs, sMr)
+#pragma unroll
+      for (int tn = 0; tn < NN; ++tn) {
+        mma(acc[tn], ld_frag(pb + 16 * tn * LDP, LDP), qf[2 * p]);
+        mma(acc[tn], ld_frag(pb + 16 * tn * LDP + 32, LDP), qf[2 * p + 1]);
+      }
+    }
   }
-  __syncthreads();  // sC, sMs, sMr
 
   // M'_s . x_i and c_s . x_i (each lane holds 8 features per k step)
   float mq = 0.f, cx = 0.f;
@@ -287,9 +311,9 @@ __global__ __launch_bounds__(kThreads, 2) void clean_out_kernel(const CleanArgs 
   const float ti = t0f + (float)(r0 + i + 1);
   float rs = 0.f, cqp = 0.f;
   for (int jb = cbeg; jb <= ch; ++jb) {
-    T* buf = sK[(jb - cbeg) & 1];
-    // centred keys of block jb; the other buffer may still be read by a
-    // wave working on block jb - 1, this one was released by the last barrier
+    T* buf = sbuf + ((NP + jb - cbeg) & 1) * BUF;
+    // centred keys of block jb; the other buffer may still be read by a wave
+    // working on the step before, this one was released by the last barrier
 #pragma unroll
     for (int u = 0; u < RowTile<T, DK>::NV; ++u) {
       const vec_t kv = rk.get(u);

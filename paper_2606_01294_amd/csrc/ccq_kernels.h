@@ -31,7 +31,8 @@ struct CleanArgs {
   float* mdot;        // m_t . x_t (raw key sum), [B,T,H] fp32, or null
   // workspace: NC = chunks, NS = segments per sequence
   float* gram;        // [B*H, NS, dk, dk] raw segment sums of k k^T
-  void* sprime;       // [B*H, NS, dk, dk] io: entry second moment about c_s
+  void* sprime;       // [B*H, NS, dk/64, dk, 64] io: entry second moment about c_s,
+                      // in 64-column slices
   float* csum;        // [B*H, NC, dk] key sum of every chunk
   float* ssum;        // [B*H, NS, dk] key sum of every segment
   float* mr;          // [B*H, NC, dk] key sum before the chunk, about c_s
