@@ -199,6 +199,17 @@ __device__ __forceinline__ void store_acc_pair(T* p, const f32x4& x, const f32x4
   }
 }
 
+// Store a fragment's 8 elements contiguously (one 16- or 32-byte store).
+template <typename T>
+__device__ __forceinline__ void store_frag(T* p, const Frag<T>& f) {
+  if constexpr (sizeof(T) == 2) {
+    *reinterpret_cast<bf16x8*>(p) = f.v;
+  } else {
+    *reinterpret_cast<f32x4*>(p) = f.lo;
+    *reinterpret_cast<f32x4*>(p + 4) = f.hi;
+  }
+}
+
 // acc += A[16 x 16] B[16 x 16] in fp32 (four 16x16x4 steps), both operands
 // row-major in LDS: A at a (pitch lda), B at b (pitch ldb, rows = k).
 __device__ __forceinline__ void mma16_f32(f32x4& acc, const float* a, int lda, const float* b, int ldb) {

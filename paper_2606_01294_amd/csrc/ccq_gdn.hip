@@ -183,6 +183,23 @@ __global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) 
       rb.load(a.beta + ((size_t)b * a.T + r0) * a.H + h, (size_t)a.H, tid, nrow);
     }
   };
+  // S_r and U^T of chunk ci are written back at the start of iteration ci + 1,
+  // after that iteration's LDS copies: all vector memory operations share one
+  // in-order counter, so a store issued just before the next chunk's loads
+  // are waited for would have its write latency added to every chunk.
+  // Both are stored fragment-native: 1 KB per (value tile, k step).
+  const int vt = (v0 >> 4) + w;
+  T* st_base = static_cast<T*>(a.states) + ((size_t)vt * NK * 16 + c16) * 32 + 8 * g4;
+  T* u_base = static_cast<T*>(a.U) + ((size_t)vt * 2 * 16 + c16) * 32 + 8 * g4;
+  Frag<T> sf[NK], uf[2];
+  auto write_back = [&](int cw) {
+    T* st_out = st_base + ((size_t)bh * N + cw) * a.dv * DK;
+#pragma unroll
+    for (int m = 0; m < NK; ++m) store_frag(st_out + 16 * 32 * m, sf[m]);
+    T* u_out = u_base + ((size_t)bh * N + cw) * a.dv * C;
+    store_frag(u_out, uf[0]);
+    store_frag(u_out + 16 * 32, uf[1]);
+  };
   if (N > 0) prefetch(0);
 
   for (int ci = 0; ci < N; ++ci) {
@@ -195,19 +212,12 @@ __global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) 
       sGam[buf][tid] = rg.get();
       sBeta[buf][tid] = rb.get();
     }
+    if (ci > 0) write_back(ci - 1);
     if (ci + 1 < N) prefetch(ci + 1);
     __syncthreads();
     const T* Kb = sK[buf];
 
-    // S_r -> states, fragment-native: 1 KB per (value tile, k step)
-    const int vt = (v0 >> 4) + w;
-    T* st_out = static_cast<T*>(a.states) + ((size_t)bh * N + ci) * a.dv * DK +
-                ((size_t)vt * NK * 16 + c16) * 32 + 8 * g4;
-#pragma unroll
-    for (int m = 0; m < NK; ++m) store_acc_pair(st_out + 16 * 32 * m, S[2 * m], S[2 * m + 1]);
-
     // P = K S_r^T, row tile J; LDS reads run one tile ahead of their products
-    Frag<T> sf[NK];
 #pragma unroll
     for (int m = 0; m < NK; ++m) sf[m] = acc_pair_frag<T>(S[2 * m], S[2 * m + 1]);
     f32x4 R[4];
@@ -256,10 +266,9 @@ __global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) 
       mma(U[I], ld_frag(sT[buf] + 16 * I * LDT, LDT), rf0);
       mma(U[I], ld_frag(sT[buf] + 16 * I * LDT + 32, LDT), rf1);
     }
-    // U^T -> [v][j] (acc_pos order), then U e^{gamma_C - gamma_i}
-    T* u_out = static_cast<T*>(a.U) + ((size_t)bh * N + ci) * a.dv * C + ((size_t)vt * 2 * 16 + c16) * 32 + 8 * g4;
-    store_acc_pair(u_out, U[0], U[1]);
-    store_acc_pair(u_out + 16 * 32, U[2], U[3]);
+    // U^T (kept for the write-back), then U e^{gamma_C - gamma_i}
+    uf[0] = acc_pair_frag<T>(U[0], U[1]);
+    uf[1] = acc_pair_frag<T>(U[2], U[3]);
     const float gC = sGam[buf][C - 1];
 #pragma unroll
     for (int I = 0; I < 4; ++I) {
@@ -297,6 +306,7 @@ __global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) 
     }
   }
 
+  if (N > 0) write_back(N - 1);
   if (a.ST) {
 #pragma unroll
     for (int tc = 0; tc < NCT; ++tc)
