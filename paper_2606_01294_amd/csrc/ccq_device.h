@@ -374,13 +374,15 @@ struct ChunkTile {
 template <typename T, int D, int NT = kThreads>
 struct RowTile {
   static constexpr int VE = 8;
-  static constexpr int VPR = D / VE;             // vectors per row
-  static constexpr int NV = kChunk * VPR / NT;   // vectors per thread
-  static_assert(D % VE == 0 && NV >= 1 && kChunk * VPR % NT == 0, "tile split");
+  static constexpr int VPR = D / VE;                  // vectors per row
+  static constexpr int TOT = kChunk * VPR;            // vectors in the tile
+  static constexpr int NV = (TOT + NT - 1) / NT;      // vectors per thread
+  static_assert(D % VE == 0, "row split");
   typedef T vec_t __attribute__((ext_vector_type(VE)));
   vec_t v[NV];
-  uint32_t ok;  // bit u: vector u's row lies inside the sequence
+  uint32_t ok;  // bit u: vector u exists and its row lies inside the sequence
 
+  __device__ __forceinline__ static bool mine(int u) { return TOT % NT == 0 || (int)threadIdx.x + NT * u < TOT; }
   __device__ __forceinline__ static int row(int u) { return ((int)threadIdx.x + NT * u) / VPR; }
   __device__ __forceinline__ static int col(int u) { return (((int)threadIdx.x + NT * u) % VPR) * VE; }
 
@@ -388,6 +390,7 @@ struct RowTile {
     ok = 0;
 #pragma unroll
     for (int u = 0; u < NV; ++u) {
+      if (!mine(u)) continue;
       const int r = row(u);
       ok |= (r < n ? 1u : 0u) << u;
       v[u] = *reinterpret_cast<const vec_t*>(src + (size_t)(r < n ? r : n - 1) * gstride + col(u));
@@ -401,7 +404,8 @@ struct RowTile {
   }
   __device__ __forceinline__ void store(T* dst, int ld) const {
 #pragma unroll
-    for (int u = 0; u < NV; ++u) *reinterpret_cast<vec_t*>(dst + row(u) * ld + col(u)) = get(u);
+    for (int u = 0; u < NV; ++u)
+      if (mine(u)) *reinterpret_cast<vec_t*>(dst + row(u) * ld + col(u)) = get(u);
   }
 };
 

@@ -124,26 +124,33 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
   }
 }
 
-// State recurrence over the chunks of one head.  Wave w of the workgroup owns
-// the 16 values v = v0 + 16 w .. of S for every key feature, held transposed
-// in MFMA accumulators (row c, column v).  Per chunk:
-//   S_r -> states;   P = K S_r^T;   R = diag(beta) (V - diag(e^gamma) P);
-//   U = Tm R -> U^T; S^T <- e^{gamma_C} S^T + K^T diag(e^{gamma_C - gamma}) U.
+// State recurrence over the chunks of one head.  A workgroup owns NPR value
+// slices of 16 (v = v0 + 16 p + ..); each slice is shared by NH waves, wave
+// (p, hq) keeping key features c in [hq DK/NH, (hq+1) DK/NH) of S^T[c][v] in
+// MFMA accumulators.  Per chunk:
+//   S_r -> states;  P = K S_r^T (partial over the wave's features, summed over
+//   the NH waves through LDS);  R = diag(beta) (V - diag(e^gamma) P);
+//   U = Tm R -> U^T;  S^T <- e^{gamma_C} S^T + K^T diag(e^{gamma_C - gamma}) U.
 // Every product takes its S, R or U operand straight from the accumulators of
 // the step before (acc_pair_frag).  K, Tm and the V slice are staged through
-// double-buffered LDS: one barrier per chunk.
-template <typename T, int DK, int NW>
-__global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) {
-  constexpr int C = kChunk, NT = 64 * NW, BVS = 16 * NW;
+// double-buffered LDS.  Splitting the features over NH waves shortens the
+// chain of dependent products per chunk and puts NH times more waves on the
+// chip, which matters because the chunks of a head are strictly sequential.
+template <typename T, int DK, int NPR, int NH>
+__global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnArgs a) {
+  constexpr int C = kChunk, NW = NPR * NH, NT = 64 * NW, BVS = 16 * NPR;
   constexpr int P = Pad<T>::value;
   constexpr int LDQ = DK + P, LDT = C + P, LDV = BVS + P;
-  constexpr int NCT = DK / 16;  // key-feature tiles of S^T
-  constexpr int NK = DK / 32;
+  constexpr int DKH = DK / NH;     // key features per wave
+  constexpr int NCT = DKH / 16;    // key-feature tiles per wave
+  constexpr int NKH = DKH / 32;    // 32-wide k steps per wave
+  static_assert(NKH >= 1, "key split");
 
   __shared__ __align__(16) T sK[2][C * LDQ];
   __shared__ __align__(16) T sT[2][C * LDT];
   __shared__ __align__(16) T sV[2][C * LDV];
   __shared__ __align__(16) float sGam[2][C], sBeta[2][C];
+  __shared__ __align__(16) f32x4 sX[NH > 1 ? NW * 4 * 64 : 1];  // partial P of every wave
 
   const int nvt = a.dv / BVS;
   const int N = (a.T + C - 1) / C;
@@ -151,19 +158,22 @@ __global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) 
   const int bh = lb / nvt;
   const int tid = threadIdx.x, w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
+  const int pr = w / NH, hq = w % NH;
   const int v0 = (lb % nvt) * BVS;
-  const int v = v0 + 16 * w + c16;  // this lane's value column
+  const int vs = 16 * pr + c16;     // value column within the workgroup's slice
+  const int v = v0 + vs;
+  const int c0 = hq * DKH;          // first key feature of this wave
   const int b = bh / a.H, h = bh % a.H;
   const T* k = static_cast<const T*>(a.k);
   const T* vin = static_cast<const T*>(a.v);
   const T* Tg = static_cast<const T*>(a.Tm);
 
-  // S^T[c][v], c = 16 tc + 4 g4 + r
+  // S^T[c][v], c = c0 + 16 tc + 4 g4 + r
   f32x4 S[NCT];
 #pragma unroll
   for (int tc = 0; tc < NCT; ++tc) {
     if (a.S0)
-      S[tc] = *reinterpret_cast<const f32x4*>(a.S0 + ((size_t)bh * a.dv + v) * DK + 16 * tc + 4 * g4);
+      S[tc] = *reinterpret_cast<const f32x4*>(a.S0 + ((size_t)bh * a.dv + v) * DK + c0 + 16 * tc + 4 * g4);
     else
       S[tc] = zero4();
   }
@@ -183,22 +193,25 @@ __global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) 
       rb.load(a.beta + ((size_t)b * a.T + r0) * a.H + h, (size_t)a.H, tid, nrow);
     }
   };
+
   // S_r and U^T of chunk ci are written back at the start of iteration ci + 1,
   // after that iteration's LDS copies: all vector memory operations share one
   // in-order counter, so a store issued just before the next chunk's loads
   // are waited for would have its write latency added to every chunk.
   // Both are stored fragment-native: 1 KB per (value tile, k step).
-  const int vt = (v0 >> 4) + w;
-  T* st_base = static_cast<T*>(a.states) + ((size_t)vt * NK * 16 + c16) * 32 + 8 * g4;
+  const int vt = (v0 >> 4) + pr;
+  T* st_base = static_cast<T*>(a.states) + (((size_t)vt * (DK / 32) + hq * NKH) * 16 + c16) * 32 + 8 * g4;
   T* u_base = static_cast<T*>(a.U) + ((size_t)vt * 2 * 16 + c16) * 32 + 8 * g4;
-  Frag<T> sf[NK], uf[2];
+  Frag<T> sf[NKH], uf[2];
   auto write_back = [&](int cw) {
     T* st_out = st_base + ((size_t)bh * N + cw) * a.dv * DK;
 #pragma unroll
-    for (int m = 0; m < NK; ++m) store_frag(st_out + 16 * 32 * m, sf[m]);
-    T* u_out = u_base + ((size_t)bh * N + cw) * a.dv * C;
-    store_frag(u_out, uf[0]);
-    store_frag(u_out + 16 * 32, uf[1]);
+    for (int m = 0; m < NKH; ++m) store_frag(st_out + 16 * 32 * m, sf[m]);
+    if (hq == 0) {
+      T* u_out = u_base + ((size_t)bh * N + cw) * a.dv * C;
+      store_frag(u_out, uf[0]);
+      store_frag(u_out + 16 * 32, uf[1]);
+    }
   };
   if (N > 0) prefetch(0);
 
@@ -217,28 +230,42 @@ __global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) 
     __syncthreads();
     const T* Kb = sK[buf];
 
-    // P = K S_r^T, row tile J; LDS reads run one tile ahead of their products
+    // P = K S_r^T over this wave's features; LDS reads run one row tile ahead
 #pragma unroll
-    for (int m = 0; m < NK; ++m) sf[m] = acc_pair_frag<T>(S[2 * m], S[2 * m + 1]);
+    for (int m = 0; m < NKH; ++m) sf[m] = acc_pair_frag<T>(S[2 * m], S[2 * m + 1]);
     f32x4 R[4];
-    Frag<T> kf[2][NK];
+    Frag<T> kf[2][NKH];
 #pragma unroll
-    for (int m = 0; m < NK; ++m) kf[0][m] = ld_frag_acc(Kb + 32 * m, (size_t)LDQ);
+    for (int m = 0; m < NKH; ++m) kf[0][m] = ld_frag_acc(Kb + c0 + 32 * m, (size_t)LDQ);
 #pragma unroll
     for (int J = 0; J < 4; ++J) {
       if (J + 1 < 4)
 #pragma unroll
-        for (int m = 0; m < NK; ++m) kf[(J + 1) & 1][m] = ld_frag_acc(Kb + 16 * (J + 1) * LDQ + 32 * m, (size_t)LDQ);
+        for (int m = 0; m < NKH; ++m) kf[(J + 1) & 1][m] = ld_frag_acc(Kb + 16 * (J + 1) * LDQ + c0 + 32 * m, (size_t)LDQ);
       __builtin_amdgcn_sched_barrier(0);
       f32x4 acc = zero4();
 #pragma unroll
-      for (int m = 0; m < NK; ++m) mma(acc, kf[J & 1][m], sf[m]);
+      for (int m = 0; m < NKH; ++m) mma(acc, kf[J & 1][m], sf[m]);
       R[J] = acc;
+    }
+    if constexpr (NH > 1) {
+      // sum the NH partial products of this value slice, in a fixed order so
+      // every wave of the slice holds bit-identical P
+#pragma unroll
+      for (int J = 0; J < 4; ++J) sX[(w * 4 + J) * 64 + l] = R[J];
+      __syncthreads();
+#pragma unroll
+      for (int J = 0; J < 4; ++J) {
+        f32x4 sum = sX[((pr * NH) * 4 + J) * 64 + l];
+#pragma unroll
+        for (int hh = 1; hh < NH; ++hh) sum += sX[((pr * NH + hh) * 4 + J) * 64 + l];
+        R[J] = sum;
+      }
     }
     // R = beta (V - e^gamma P); V rows 32 m + 4 g4 + r and 32 m + 16 + 4 g4 + r
 #pragma unroll
     for (int m = 0; m < 2; ++m) {
-      const Frag<T> vf = ld_frag_tr_acc(sV[buf] + 32 * m * LDV + 16 * w, LDV);
+      const Frag<T> vf = ld_frag_tr_acc(sV[buf] + 32 * m * LDV + 16 * pr, LDV);
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
         const int J = 2 * m + hh;
@@ -279,12 +306,12 @@ __global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) 
     const Frag<T> ud0 = acc_pair_frag<T>(U[0], U[1]);
     const Frag<T> ud1 = acc_pair_frag<T>(U[2], U[3]);
     const float eC = __expf(gC);
-    constexpr int TB = 4;  // key-feature tiles per batch of transposing reads
+    constexpr int TB = NCT < 4 ? NCT : 4;  // key-feature tiles per batch of transposing reads
     Frag<T> tf[2][TB][2];
 #pragma unroll
     for (int t = 0; t < TB; ++t) {
-      tf[0][t][0] = ld_frag_tr_acc(Kb + 16 * t, LDQ);
-      tf[0][t][1] = ld_frag_tr_acc(Kb + 32 * LDQ + 16 * t, LDQ);
+      tf[0][t][0] = ld_frag_tr_acc(Kb + c0 + 16 * t, LDQ);
+      tf[0][t][1] = ld_frag_tr_acc(Kb + 32 * LDQ + c0 + 16 * t, LDQ);
     }
 #pragma unroll
     for (int tb = 0; tb < NCT / TB; ++tb) {
@@ -292,8 +319,8 @@ __global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) 
 #pragma unroll
         for (int t = 0; t < TB; ++t) {
           const int tc = TB * (tb + 1) + t;
-          tf[(tb + 1) & 1][t][0] = ld_frag_tr_acc(Kb + 16 * tc, LDQ);
-          tf[(tb + 1) & 1][t][1] = ld_frag_tr_acc(Kb + 32 * LDQ + 16 * tc, LDQ);
+          tf[(tb + 1) & 1][t][0] = ld_frag_tr_acc(Kb + c0 + 16 * tc, LDQ);
+          tf[(tb + 1) & 1][t][1] = ld_frag_tr_acc(Kb + 32 * LDQ + c0 + 16 * tc, LDQ);
         }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -310,7 +337,7 @@ __global__ __launch_bounds__(64 * NW, 1) void gdn_state_kernel(const GdnArgs a) 
   if (a.ST) {
 #pragma unroll
     for (int tc = 0; tc < NCT; ++tc)
-      *reinterpret_cast<f32x4*>(a.ST + ((size_t)bh * a.dv + v) * DK + 16 * tc + 4 * g4) = S[tc];
+      *reinterpret_cast<f32x4*>(a.ST + ((size_t)bh * a.dv + v) * DK + c0 + 16 * tc + 4 * g4) = S[tc];
   }
 }
 
@@ -427,12 +454,27 @@ hipError_t run_tri(const TriArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((gdn_tri_kernel<T, DK>), dim3(nblk), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
-template <typename T, int DK, int NW>
-hipError_t run_gdn_state(const GdnArgs& a, hipStream_t st) {
-  const int nblk = a.B * a.H * (a.dv / (16 * NW));
+template <typename T, int DK, int NPR, int NH>
+hipError_t run_gdn_state_v(const GdnArgs& a, hipStream_t st) {
+  const int nblk = a.B * a.H * (a.dv / (16 * NPR));
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((gdn_state_kernel<T, DK, NW>), dim3(nblk), dim3(64 * NW), 0, st, a);
+  hipLaunchKernelGGL((gdn_state_kernel<T, DK, NPR, NH>), dim3(nblk), dim3(64 * NPR * NH), 0, st, a);
   return hipGetLastError();
+}
+// Split the key features over as many waves (1, 2, 4 or 8, at least 32
+// features each) as it takes to give every SIMD of the chip a wave, with four
+// waves per workgroup where the split allows.
+template <typename T, int DK>
+hipError_t run_gdn_state(const GdnArgs& a, hipStream_t st) {
+  const long long slices = (long long)a.B * a.H * (a.dv / 16);
+  constexpr int kSimds = 1024;
+  if (slices >= kSimds || DK < 64) return run_gdn_state_v<T, DK, 4, 1>(a, st);
+  if (slices * 2 >= kSimds || DK < 128) return run_gdn_state_v<T, DK, 2, 2>(a, st);
+  if constexpr (DK >= 128) {
+    if (slices * 4 >= kSimds || DK < 256) return run_gdn_state_v<T, DK, 1, 4>(a, st);
+  }
+  if constexpr (DK >= 256) return run_gdn_state_v<T, DK, 1, 8>(a, st);
+  return hipErrorInvalidValue;
 }
 template <typename T, int DK, int VPW, int IPW>
 hipError_t run_gdn_out_v(const GdnOutArgs& a, hipStream_t st) {
@@ -476,19 +518,16 @@ hipError_t launch_gdn_tri(const TriArgs& a, bool is_bf16, hipStream_t st) {
 }
 
 hipError_t launch_gdn_state(const GdnArgs& a, bool is_bf16, hipStream_t st) {
-  // four waves (64 values) per workgroup when that still gives every CU a
-  // workgroup, else two (dv >= 64, so both divide dv)
-  const bool wide = (long long)a.B * a.H * (a.dv / 64) >= 256;
   if (is_bf16) {
     switch (a.dk) {
-      case 64: return wide ? run_gdn_state<bf16_t, 64, 4>(a, st) : run_gdn_state<bf16_t, 64, 2>(a, st);
-      case 128: return wide ? run_gdn_state<bf16_t, 128, 4>(a, st) : run_gdn_state<bf16_t, 128, 2>(a, st);
-      case 256: return wide ? run_gdn_state<bf16_t, 256, 4>(a, st) : run_gdn_state<bf16_t, 256, 2>(a, st);
+      case 64: return run_gdn_state<bf16_t, 64>(a, st);
+      case 128: return run_gdn_state<bf16_t, 128>(a, st);
+      case 256: return run_gdn_state<bf16_t, 256>(a, st);
     }
   } else {
     switch (a.dk) {
-      case 64: return wide ? run_gdn_state<float, 64, 4>(a, st) : run_gdn_state<float, 64, 2>(a, st);
-      case 128: return wide ? run_gdn_state<float, 128, 4>(a, st) : run_gdn_state<float, 128, 2>(a, st);
+      case 64: return run_gdn_state<float, 64>(a, st);
+      case 128: return run_gdn_state<float, 128>(a, st);
     }
   }
   return hipErrorInvalidValue;
