@@ -72,6 +72,31 @@ def test_gdn_parity_small(case):
     compare(GDN, d, dtype)
 
 
+# The Gated DeltaNet state pass splits each 16-wide value slice over 1, 2, 4 or
+# 8 waves depending on how many slices (B * H * dv / 16) the call has; these
+# batch shapes reach every split the small cases above do not.
+GDN_SPLIT_CASES = [
+    # dtype, B, H, dk, dv  -> slices
+    (BF16, 4, 16, 256, 256),   # 1024: one wave per slice
+    (BF16, 2, 16, 256, 256),   # 512: two
+    (BF16, 1, 16, 256, 256),   # 256: four
+    (BF16, 4, 16, 128, 256),   # 1024: one
+    (BF16, 2, 16, 128, 256),   # 512: two
+    (BF16, 8, 16, 64, 128),    # 1024: one
+    (F32, 8, 16, 128, 128),    # 1024: one
+    (F32, 4, 16, 64, 128),     # 512: two
+]
+
+
+@pytest.mark.parametrize("case", GDN_SPLIT_CASES, ids=lambda c: "%s-B%dH%d-dk%d-dv%d" % (
+    str(c[0]).split(".")[-1], c[1], c[2], c[3], c[4]))
+def test_gdn_parity_state_splits(case):
+    dtype, B, H, dk, dv = case
+    say("gdn split", case)
+    d = make_inputs(GDN, B, 70, H, dk, dv, dtype, seed=300 + B * H + dk, keys="aniso", lam="random")
+    compare(GDN, d, dtype)
+
+
 @pytest.mark.parametrize("backbone", [GLA, GDN])
 @pytest.mark.parametrize("dtype", [F32, BF16])
 def test_uncentred_scaled_with_initial_states(backbone, dtype):
