@@ -201,32 +201,40 @@ __global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
         acc * (1.f / (t0f + (float)a.T));
 }
 
-// One workgroup per chunk; wave w owns rows i = 16 w .. 16 w + 15.  All
-// products are kept transposed (output feature n in the accumulator row, token
-// i in its column) so that score tiles feed the next product from registers:
+// One workgroup per CPW consecutive chunks of a segment; wave w owns rows
+// i = 16 (w % 4) .. + 15 of chunk w / 4.  All products are kept transposed
+// (output feature n in the accumulator row, token i in its column) so that
+// score tiles feed the next product from registers:
 //   acc^T  = S'_s x^T               (S' staged through LDS one 64-column slice
 //                                     at a time, double-buffered)
 //   sc^T   = K'_blk x^T,  acc^T += K'_blk^T sc^T        (each block of the segment)
-// The slice buffers are reused for the key blocks.
+// The slice buffers are reused for the key blocks, and both are shared by the
+// CPW chunks, which halves (CPW = 2) the global round trips per chunk.
 // On the diagonal block the scores are masked to j <= i and shifted by
 // -cq'_i / t_i, which folds the within-chunk part of m'_i into the product.
-template <typename T, int DK>
-__global__ __launch_bounds__(kThreads, 2) void clean_out_kernel(const CleanArgs a) {
+template <typename T, int DK, int CPW>
+__global__ __launch_bounds__(kThreads * CPW, 1) void clean_out_kernel(const CleanArgs a) {
   constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P, LDP = 64 + P;
+  constexpr int NT = kThreads * CPW;
   constexpr int NK = DK / 32, NN = DK / 16, NP = DK / 64;
   constexpr int BUF = (DK * LDP > C * LDK) ? DK * LDP : C * LDK;  // elements per buffer
-  constexpr int NVS = DK * 64 / 8 / kThreads;                     // slice vectors per thread
-  typedef typename RowTile<T, DK>::vec_t vec_t;
+  constexpr int NVS = DK * 64 / 8 / NT;                            // slice vectors per thread
+  static_assert(NVS >= 1 && DK * 64 % (8 * NT) == 0, "slice split");
+  typedef typename RowTile<T, DK, NT>::vec_t vec_t;
   __shared__ __align__(16) T sbuf[2 * BUF];
-  __shared__ __align__(16) float sC[DK], sMr[DK], sMs[DK];
+  __shared__ __align__(16) float sC[DK], sMs[DK], sMr[CPW][DK];
 
   const int NC = n_chunks(a.T), NS = n_segs(a.T, a.seg);
+  const int NG = (NC + CPW - 1) / CPW;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int bh = lb / NC, ch = lb % NC;
+  const int bh = lb / NG, ch0 = (lb % NG) * CPW;
+  const int chl = min(NC - 1, ch0 + CPW - 1);  // last chunk of the group
   const int b = bh / a.H, h = bh % a.H;
-  const int s = ch / a.seg, cbeg = s * a.seg;
-  const int r0 = ch * C, nrow = min(C, a.T - r0);
+  const int s = ch0 / a.seg, cbeg = s * a.seg;
   const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g4 = l >> 4, c16 = l & 15;
+  const int wr = w & 3, ch = ch0 + (w >> 2);
+  const bool has = ch < NC;  // this wave's chunk exists
+  const int r0 = ch * C, nrow = has ? min(C, a.T - r0) : 0;
   const T* x = static_cast<const T*>(a.q);
   const T* k = static_cast<const T*>(a.k);
   const size_t gstride = (size_t)a.H * DK;
@@ -235,11 +243,12 @@ __global__ __launch_bounds__(kThreads, 2) void clean_out_kernel(const CleanArgs 
 
   // this wave's rows of x as B fragments (column = token); rows past the end
   // repeat the last row and are never written back
-  const int i = 16 * w + c16;
+  const int i = 16 * wr + c16;
   const bool iok = i < nrow;
   Frag<T> qf[NK];
   {
-    const T* xr = x + tok_off(b, r0 + (iok ? i : nrow - 1), h, a.T, a.H, DK) + 8 * g4;
+    const int row = has ? r0 + (iok ? i : nrow - 1) : 0;
+    const T* xr = x + tok_off(b, row, h, a.T, a.H, DK) + 8 * g4;
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk) {
       if constexpr (sizeof(T) == 2) {
@@ -250,15 +259,16 @@ __global__ __launch_bounds__(kThreads, 2) void clean_out_kernel(const CleanArgs 
       }
     }
   }
-  RowTile<T, DK> rk;
+  RowTile<T, DK, NT> rk;
   auto load_block = [&](int c) {
     rk.load(k + tok_off(b, c * C, h, a.T, a.H, DK), gstride, min(C, a.T - c * C));
   };
   load_block(cbeg);
-  for (int d = tid; d < DK; d += kThreads) {
+  for (int d = tid; d < DK; d += NT) {
     sC[d] = a.cs[so * DK + d];
     sMs[d] = a.ms[so * DK + d];
-    sMr[d] = a.mr[((size_t)bh * NC + ch) * DK + d];
+#pragma unroll
+    for (int c = 0; c < CPW; ++c) sMr[c][d] = ch0 + c < NC ? a.mr[((size_t)bh * NC + ch0 + c) * DK + d] : 0.f;
   }
 
   // entry term S'_s x_i, one 64-column slice of S' per step
@@ -266,28 +276,40 @@ __global__ __launch_bounds__(kThreads, 2) void clean_out_kernel(const CleanArgs 
 #pragma unroll
   for (int tn = 0; tn < NN; ++tn) acc[tn] = zero4();
   {
+    // all slices are requested up front when they fit in registers (the whole
+    // of S' is DK * DK / 8 / NT vectors per thread), else one slice ahead
+    constexpr bool kAll = NVS * NP <= 16;
+    constexpr int NB = kAll ? NP : 2;
     const T* sp = static_cast<const T*>(a.sprime) + so * DK * DK;
-    vec_t ps[NVS];
+    vec_t ps[NB][NVS];
     auto load_slice = [&](int p) {
 #pragma unroll
       for (int u = 0; u < NVS; ++u)
-        ps[u] = *reinterpret_cast<const vec_t*>(sp + (size_t)p * DK * 64 + (size_t)(tid + kThreads * u) * 8);
+        ps[kAll ? p : (p & 1)][u] =
+            *reinterpret_cast<const vec_t*>(sp + (size_t)p * DK * 64 + (size_t)(tid + NT * u) * 8);
     };
-    load_slice(0);
+    if constexpr (kAll) {
+#pragma unroll
+      for (int p = 0; p < NP; ++p) load_slice(p);
+    } else {
+      load_slice(0);
+    }
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
       T* pb = sbuf + (p & 1) * BUF;
 #pragma unroll
       for (int u = 0; u < NVS; ++u) {
-        const int e = tid + kThreads * u;
-        *reinterpret_cast<vec_t*>(pb + (e >> 3) * LDP + 8 * (e & 7)) = ps[u];
+        const int e = tid + NT * u;
+        *reinterpret_cast<vec_t*>(pb + (e >> 3) * LDP + 8 * (e & 7)) = ps[kAll ? p : (p & 1)][u];
       }
-      if (p + 1 < NP) load_slice(p + 1);
+      if (!kAll && p + 1 < NP) load_slice(p + 1);
       __syncthreads();  // (also publishes sC, sMs, sMr)
+      if (has) {
 #pragma unroll
-      for (int tn = 0; tn < NN; ++tn) {
-        mma(acc[tn], ld_frag(pb + 16 * tn * LDP, LDP), qf[2 * p]);
-        mma(acc[tn], ld_frag(pb + 16 * tn * LDP + 32, LDP), qf[2 * p + 1]);
+        for (int tn = 0; tn < NN; ++tn) {
+          mma(acc[tn], ld_frag(pb + 16 * tn * LDP, LDP), qf[2 * p]);
+          mma(acc[tn], ld_frag(pb + 16 * tn * LDP + 32, LDP), qf[2 * p + 1]);
+        }
       }
     }
   }
@@ -310,28 +332,29 @@ __global__ __launch_bounds__(kThreads, 2) void clean_out_kernel(const CleanArgs 
 
   const float ti = t0f + (float)(r0 + i + 1);
   float rs = 0.f, cqp = 0.f;
-  for (int jb = cbeg; jb <= ch; ++jb) {
+  for (int jb = cbeg; jb <= chl; ++jb) {
     T* buf = sbuf + ((NP + jb - cbeg) & 1) * BUF;
     // centred keys of block jb; the other buffer may still be read by a wave
     // working on the step before, this one was released by the last barrier
 #pragma unroll
-    for (int u = 0; u < RowTile<T, DK>::NV; ++u) {
+    for (int u = 0; u < RowTile<T, DK, NT>::NV; ++u) {
       const vec_t kv = rk.get(u);
-      const int col = RowTile<T, DK>::col(u);
+      const int col = RowTile<T, DK, NT>::col(u);
       vec_t y;
 #pragma unroll
       for (int e = 0; e < 8; ++e) y[e] = to<T>(f32(kv[e]) - sC[col + e]);
-      *reinterpret_cast<vec_t*>(buf + RowTile<T, DK>::row(u) * LDK + col) = y;
+      *reinterpret_cast<vec_t*>(buf + RowTile<T, DK, NT>::row(u) * LDK + col) = y;
     }
-    if (jb < ch) load_block(jb + 1);
+    if (jb < chl) load_block(jb + 1);
     __syncthreads();
+    if (!has || jb > ch) continue;  // wave-uniform: this chunk's window has ended
 
     const bool diag = jb == ch;
     f32x4 sc[4];
 #pragma unroll
     for (int J = 0; J < 4; ++J) {
       sc[J] = zero4();
-      if (!diag || J <= w)
+      if (!diag || J <= wr)
 #pragma unroll
         for (int kk = 0; kk < NK; ++kk) mma(sc[J], ld_frag(buf + 16 * J * LDK + 32 * kk, LDK), qf[kk]);
     }
@@ -359,7 +382,7 @@ __global__ __launch_bounds__(kThreads, 2) void clean_out_kernel(const CleanArgs 
     }
     const Frag<T> f0 = acc_pair_frag<T>(sc[0], sc[1]);
     const Frag<T> f1 = acc_pair_frag<T>(sc[2], sc[3]);
-    const bool upper = !diag || w >= 2;  // keys 32..63 can precede row i
+    const bool upper = !diag || wr >= 2;  // keys 32..63 can precede row i
 #pragma unroll
     for (int tn = 0; tn < NN; ++tn) {
       mma(acc[tn], ld_frag_tr_acc(buf + 16 * tn, LDK), f0);
@@ -368,24 +391,44 @@ __global__ __launch_bounds__(kThreads, 2) void clean_out_kernel(const CleanArgs 
   }
 
   if (!iok) return;
+  // epilogue: every load is issued before the first store, and the optional
+  // outputs are written in loops of their own, so the loads and stores of the
+  // NN tiles overlap instead of forming NN round trips to memory
   const float inv = 1.f / ti;
   const float lam = a.lam[((size_t)b * a.T + r0 + i) * a.H + h];
   const float msub = a.centered ? cqp * inv : 0.f;
-  const size_t rowoff = tok_off(b, r0 + i, h, a.T, a.H, DK);
+  const size_t rowoff = tok_off(b, r0 + i, h, a.T, a.H, DK) + 4 * g4;
+  const float* mrow = sMr[w >> 2] + 4 * g4;
+  f32x4 xb[NN];
+  if (a.base) {
+#pragma unroll
+    for (int tn = 0; tn < NN; ++tn) xb[tn] = *reinterpret_cast<const f32x4*>(a.base + rowoff + 16 * tn);
+  } else {
+#pragma unroll
+    for (int tn = 0; tn < NN; ++tn) xb[tn] = load4f(x + rowoff + 16 * tn);
+  }
+#pragma unroll
+  for (int tn = 0; tn < NN; ++tn) {  // acc <- Sigma_t x_t (the correction before lambda)
+    const f32x4 mr = *reinterpret_cast<const f32x4*>(mrow + 16 * tn);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[tn][r] = (acc[tn][r] - msub * mr[r]) * inv;
+  }
   T* qc = static_cast<T*>(a.qclean);
 #pragma unroll
   for (int tn = 0; tn < NN; ++tn) {
-    const int n = 16 * tn + 4 * g4;
-    const f32x4 mr = *reinterpret_cast<const f32x4*>(sMr + n);
-    f32x4 c, o;
+    f32x4 o;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) c[r] = (acc[tn][r] - msub * mr[r]) * inv;
-    const f32x4 xb = a.base ? *reinterpret_cast<const f32x4*>(a.base + rowoff + n) : load4f(x + rowoff + n);
+    for (int r = 0; r < 4; ++r) o[r] = xb[tn][r] - lam * acc[tn][r];
+    store4(qc + rowoff + 16 * tn, o[0], o[1], o[2], o[3]);
+    xb[tn] = o;
+  }
+  if (a.qclean_dbg) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) o[r] = xb[r] - lam * c[r];
-    store4(qc + rowoff + n, o[0], o[1], o[2], o[3]);
-    if (a.qclean_dbg) *reinterpret_cast<f32x4*>(a.qclean_dbg + rowoff + n) = o;
-    if (a.corr) *reinterpret_cast<f32x4*>(a.corr + rowoff + n) = c;
+    for (int tn = 0; tn < NN; ++tn) *reinterpret_cast<f32x4*>(a.qclean_dbg + rowoff + 16 * tn) = xb[tn];
+  }
+  if (a.corr) {
+#pragma unroll
+    for (int tn = 0; tn < NN; ++tn) *reinterpret_cast<f32x4*>(a.corr + rowoff + 16 * tn) = acc[tn];
   }
   if (a.mdot && g4 == 0) a.mdot[((size_t)b * a.T + r0 + i) * a.H + h] = cqp + ti * cx;  // raw m . x
 }
@@ -407,9 +450,15 @@ hipError_t run_prefix(const CleanArgs& a, hipStream_t st) {
 }
 template <typename T, int DK>
 hipError_t run_out(const CleanArgs& a, hipStream_t st) {
-  const long long nblk = (long long)a.B * a.H * n_chunks(a.T);
-  if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((clean_out_kernel<T, DK>), dim3((unsigned)nblk), dim3(kThreads), 0, st, a);
+  const int nc = n_chunks(a.T);
+  if ((long long)a.B * a.H * nc == 0) return hipSuccess;
+  if (nc >= 2 && a.seg % 2 == 0) {  // two chunks per workgroup (never across a segment)
+    const long long nblk = (long long)a.B * a.H * ((nc + 1) / 2);
+    hipLaunchKernelGGL((clean_out_kernel<T, DK, 2>), dim3((unsigned)nblk), dim3(2 * kThreads), 0, st, a);
+  } else {
+    const long long nblk = (long long)a.B * a.H * nc;
+    hipLaunchKernelGGL((clean_out_kernel<T, DK, 1>), dim3((unsigned)nblk), dim3(kThreads), 0, st, a);
+  }
   return hipGetLastError();
 }
 
