@@ -45,11 +45,8 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     if kernel == "clean_gram":      # k in; segment Gram (fp32), chunk and segment key sums out
         by = ntok * dk * io_bytes + stats * 4 + BH * (NC + NS) * dk * 4
         fl = ntok * 2 * dk * dk
-    elif kernel == "clean_msum":    # chunk and segment key sums in; centres and prefixes out
-        by = BH * NC * dk * 8 + BH * NS * dk * 12
-        fl = BH * NC * dk * 2
-    elif kernel == "clean_prefix":  # Gram in (fp32); entry second moments out (io)
-        by = stats * (4 + io_bytes) + BH * NS * dk * 8
+    elif kernel == "clean_prefix":  # Gram (fp32) and segment key sums in; entry moments out (io)
+        by = stats * (4 + io_bytes) + BH * NS * dk * 4 + BH * dk * 4
         fl = stats * 6
     elif kernel in ("clean_out", "clean_out_train", "clean_dq"):
         # x, k, lam, entry moments, chunk key sums in; x_clean out (+ Sigma x, m.x)
@@ -94,12 +91,12 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     return by, fl
 
 
-CLEAN = ["clean_gram", "clean_msum", "clean_prefix"]
+CLEAN = ["clean_gram", "clean_prefix"]
 KERNELS = {0: CLEAN + ["clean_out", "gla_state", "gla_out"],
            1: CLEAN + ["clean_out", "gdn_tri", "gdn_state", "gdn_out"],
            "train": CLEAN + ["clean_out_train", "gla_state", "gla_out", "gla_dstate",
                              "gla_bwd_chunk", "gla_dg", "clean_dq", "ccq_dk"]}
-KERNEL_SYMBOL = {"clean_gram": "clean_gram_kernel", "clean_msum": "clean_msum_kernel",
+KERNEL_SYMBOL = {"clean_gram": "clean_gram_kernel",
                  "clean_prefix": "clean_prefix_kernel", "clean_out": "clean_out_kernel",
                  "clean_out_train": "clean_out_kernel", "clean_dq": "clean_out_kernel",
                  "gla_state": "gla_state_kernel", "gla_out": "gla_out_kernel",

@@ -59,7 +59,7 @@ ccq_status check_shape(const ccq_shape* s, ccq_backbone bb) {
 
 // Workspace of the query contraction: segment and chunk key statistics.
 struct CleanWs {
-  size_t gram = 0, sprime = 0, csum = 0, ssum = 0, mr = 0, cs = 0, ms = 0;
+  size_t gram = 0, sprime = 0, csum = 0, ssum = 0;
 };
 
 template <typename Take>
@@ -71,9 +71,6 @@ CleanWs take_clean_ws(const ccq_shape* s, Take&& take) {
   c.sprime = take(bh * ns * dk * dk * esize(s->io_dtype));
   c.csum = take(bh * nc * dk * 4);
   c.ssum = take(bh * ns * dk * 4);
-  c.mr = take(bh * nc * dk * 4);
-  c.cs = take(bh * ns * dk * 4);
-  c.ms = take(bh * ns * dk * 4);
   return c;
 }
 
@@ -83,9 +80,6 @@ ccq::CleanArgs clean_args(const ccq_shape* s, char* ws, const CleanWs& c) {
   a.sprime = ws + c.sprime;
   a.csum = reinterpret_cast<float*>(ws + c.csum);
   a.ssum = reinterpret_cast<float*>(ws + c.ssum);
-  a.mr = reinterpret_cast<float*>(ws + c.mr);
-  a.cs = reinterpret_cast<float*>(ws + c.cs);
-  a.ms = reinterpret_cast<float*>(ws + c.ms);
   a.B = s->B;
   a.T = s->T;
   a.H = s->H;
@@ -99,7 +93,6 @@ ccq::CleanArgs clean_args(const ccq_shape* s, char* ws, const CleanWs& c) {
 // Key statistics of the contraction (depend on k only).
 hipError_t run_clean_stats(const ccq::CleanArgs& a, bool bf, hipStream_t st) {
   hipError_t e = traced(st, [&] { return ccq::launch_clean_gram(a, bf, st); });
-  if (e == hipSuccess) e = traced(st, [&] { return ccq::launch_clean_msum(a, st); });
   if (e == hipSuccess) e = traced(st, [&] { return ccq::launch_clean_prefix(a, bf, st); });
   return e;
 }

@@ -19,11 +19,10 @@
 //   S'_s  = sum_{j before s} (k_j - c_s)(k_j - c_s)^T      (entry second moment)
 //   k'_j  = k_j - c_s,  cq'_i = m'_i . q_i
 //
-// Four kernels:
-//   clean_gram    raw sums of k k^T per segment and of k per chunk
-//   clean_msum    key-sum prefixes and the segment centres c_s
+// Three kernels:
+//   clean_gram    raw sums of k k^T per segment, and of k per chunk and segment
 //   clean_prefix  S'_s by a prefix over segments (fp32), stored in io dtype
-//   clean_out     one workgroup per chunk: S'_s q plus the causal product
+//   clean_out     one workgroup per chunk pair: S'_s q plus the causal product
 //                 over the segment's centred keys, all in MFMA tiles
 // Without centring (Sigma = Cbar) the same kernels run with c_s = 0 and no
 // mean terms.
@@ -141,64 +140,49 @@ __global__ __launch_bounds__(kThreads) void clean_gram_kernel(const CleanArgs a)
         G[(size_t)(a0 + 16 * v + 4 * g4 + r) * DK + b0 + 16 * t + c16] = acc[v][t][r];
 }
 
-// Key-sum prefixes, one workgroup per (head, segment) and one thread per
-// feature: the centre c_s, the key sums before the segment and before each of
-// its chunks about that centre, and (last segment) the final mean.
-__global__ void clean_msum_kernel(const CleanArgs a) {
-  const int DK = a.dk, d = threadIdx.x;  // blockDim.x == dk
-  const int NC = n_chunks(a.T), NS = n_segs(a.T, a.seg);
-  const int bh = blockIdx.x / NS, s = blockIdx.x % NS;
-  const float* ss = a.ssum + (size_t)bh * NS * DK + d;
-  float run = a.mu0 ? (float)a.t0 * a.mu0[(size_t)bh * DK + d] : 0.f;  // raw key sum before s
-  for (int p = 0; p < s; ++p) run += ss[(size_t)p * DK];
-  const float tot = ss[(size_t)s * DK];
-  const int cbeg = s * a.seg, cend = min(NC, cbeg + a.seg);
-  const int len = min(a.T, cend * kChunk) - cbeg * kChunk;
-  const float cen = a.centered ? tot / (float)len : 0.f;
-  const float ns = (float)(a.t0 + (int64_t)cbeg * kChunk);  // tokens before the segment
-  float mp = run - ns * cen;
-  a.cs[((size_t)bh * NS + s) * DK + d] = cen;
-  a.ms[((size_t)bh * NS + s) * DK + d] = mp;
-  const float* cs = a.csum + (size_t)bh * NC * DK + d;
-  for (int c = cbeg; c < cend; ++c) {
-    a.mr[((size_t)bh * NC + c) * DK + d] = mp;
-    const int rows = min(kChunk, a.T - c * kChunk);
-    mp += cs[(size_t)c * DK] - (float)rows * cen;
-  }
-  if (a.muT && s == NS - 1) a.muT[(size_t)bh * DK + d] = (run + tot) / (float)(a.t0 + a.T);
-}
-
 // S'_s = S_s - M'_s c_s^T - c_s M'_s^T - n_s c_s c_s^T with S_s the raw second
-// moment before segment s (prefix of the Gram matrices, fp32) and M'_s the key
-// sum about c_s; four elements per thread.  S'_s is stored in 64-column
-// slices, each a contiguous [dk][64] block.  Also the final Cbar_T.
+// moment before segment s (prefix of the Gram matrices, fp32), c_s the mean
+// key of segment s, n_s the tokens before it and M'_s = M_s - n_s c_s the key
+// sum before it about c_s (running sums of the segment key sums, kept for this
+// thread's row and four columns); four elements per thread.  S'_s is stored in
+// 64-column slices, each a contiguous [dk][64] block.  Also the final Cbar_T
+// and mu_T.
 template <typename T, int DK>
 __global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
   constexpr int PER = DK * DK / 4 / 256;  // workgroups per head
   const int bh = blockIdx.x / PER;
   const int e = ((blockIdx.x % PER) * 256 + threadIdx.x) * 4;
   const int ra = e / DK, cb = e % DK;
-  const int NS = n_segs(a.T, a.seg);
+  const int NC = n_chunks(a.T), NS = n_segs(a.T, a.seg);
   const float t0f = (float)a.t0;
   f32x4 acc = zero4();
   if (a.C0) acc = *reinterpret_cast<const f32x4*>(a.C0 + ((size_t)bh * DK + ra) * DK + cb) * t0f;
+  float run_a = a.mu0 ? t0f * a.mu0[(size_t)bh * DK + ra] : 0.f;  // raw key sums before s
+  f32x4 run_b = a.mu0 ? *reinterpret_cast<const f32x4*>(a.mu0 + (size_t)bh * DK + cb) * t0f : zero4();
   T* Sp = static_cast<T*>(a.sprime);
   for (int s = 0; s < NS; ++s) {
     const size_t so = (size_t)bh * NS + s;
-    const float ca = a.cs[so * DK + ra], ma = a.ms[so * DK + ra];
-    const f32x4 cb4 = *reinterpret_cast<const f32x4*>(a.cs + so * DK + cb);
-    const f32x4 mb4 = *reinterpret_cast<const f32x4*>(a.ms + so * DK + cb);
+    const int cbeg = s * a.seg, cend = min(NC, cbeg + a.seg);
+    const float len = (float)(min(a.T, cend * kChunk) - cbeg * kChunk);
+    const float ns = t0f + (float)((int64_t)cbeg * kChunk);
+    const float tot_a = a.ssum[so * DK + ra];
+    const f32x4 tot_b = *reinterpret_cast<const f32x4*>(a.ssum + so * DK + cb);
     const f32x4 g = *reinterpret_cast<const f32x4*>(a.gram + (so * DK + ra) * DK + cb);
-    const float ns = t0f + (float)((int64_t)s * a.seg * kChunk);
+    const float ca = a.centered ? tot_a / len : 0.f;
+    const f32x4 cb4 = a.centered ? tot_b / len : zero4();
+    const float ma = run_a - ns * ca;
+    const f32x4 mb4 = run_b - ns * cb4;
     f32x4 o;
 #pragma unroll
     for (int q = 0; q < 4; ++q) o[q] = acc[q] - ma * cb4[q] - ca * mb4[q] - ns * ca * cb4[q];
     store4(Sp + so * DK * DK + ((size_t)(cb >> 6) * DK + ra) * 64 + (cb & 63), o[0], o[1], o[2], o[3]);
     acc += g;
+    run_a += tot_a;
+    run_b += tot_b;
   }
-  if (a.CT)
-    *reinterpret_cast<f32x4*>(a.CT + ((size_t)bh * DK + ra) * DK + cb) =
-        acc * (1.f / (t0f + (float)a.T));
+  const float inv = 1.f / (t0f + (float)a.T);
+  if (a.CT) *reinterpret_cast<f32x4*>(a.CT + ((size_t)bh * DK + ra) * DK + cb) = acc * inv;
+  if (a.muT && ra == 0) *reinterpret_cast<f32x4*>(a.muT + (size_t)bh * DK + cb) = run_b * inv;
 }
 
 // One workgroup per CPW consecutive chunks of a segment; wave w owns rows
@@ -264,11 +248,25 @@ __global__ __launch_bounds__(kThreads * CPW, 1) void clean_out_kernel(const Clea
     rk.load(k + tok_off(b, c * C, h, a.T, a.H, DK), gstride, min(C, a.T - c * C));
   };
   load_block(cbeg);
+  // key statistics of the segment, one thread per feature: the centre c_s, the
+  // key sum before the segment about c_s (M'_s) and before each of this
+  // group's chunks (M'_r), from the segment and chunk key sums
   for (int d = tid; d < DK; d += NT) {
-    sC[d] = a.cs[so * DK + d];
-    sMs[d] = a.ms[so * DK + d];
-#pragma unroll
-    for (int c = 0; c < CPW; ++c) sMr[c][d] = ch0 + c < NC ? a.mr[((size_t)bh * NC + ch0 + c) * DK + d] : 0.f;
+    const float* ss = a.ssum + (size_t)bh * NS * DK + d;
+    float run = a.mu0 ? t0f * a.mu0[(size_t)bh * DK + d] : 0.f;
+#pragma unroll 8
+    for (int p = 0; p < s; ++p) run += ss[(size_t)p * DK];
+    const int cend = min(NC, cbeg + a.seg);
+    const float len = (float)(min(a.T, cend * C) - cbeg * C);
+    const float cen = a.centered ? ss[(size_t)s * DK] / len : 0.f;
+    float mp = run - (t0f + (float)(cbeg * C)) * cen;
+    sC[d] = cen;
+    sMs[d] = mp;
+    const float* cs = a.csum + (size_t)bh * NC * DK + d;
+    for (int c = cbeg; c <= chl; ++c) {
+      if (c >= ch0) sMr[c - ch0][d] = mp;
+      mp += cs[(size_t)c * DK] - (float)min(C, a.T - c * C) * cen;
+    }
   }
 
   // entry term S'_s x_i, one 64-column slice of S' per step
@@ -487,13 +485,6 @@ bool clean_supported(int dk, bool is_bf16) {
 
 hipError_t launch_clean_gram(const CleanArgs& a, bool is_bf16, hipStream_t st) {
   CCQ_CLEAN_DISPATCH(run_gram, a, is_bf16, st);
-}
-
-hipError_t launch_clean_msum(const CleanArgs& a, hipStream_t st) {
-  const long long nblk = (long long)a.B * a.H * n_segs(a.T, a.seg);
-  if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL(clean_msum_kernel, dim3((unsigned)nblk), dim3(a.dk), 0, st, a);
-  return hipGetLastError();
 }
 
 hipError_t launch_clean_prefix(const CleanArgs& a, bool is_bf16, hipStream_t st) {

@@ -13,7 +13,7 @@ namespace ccq {
 // I - lam Sigma, reusing the key statistics of the forward.
 //
 // The sequence is cut into segments of `seg` chunks.  Key statistics are
-// formed per segment (clean_gram, clean_msum, clean_prefix); each chunk's
+// formed per segment (clean_gram, clean_prefix); each chunk's
 // output then needs only its segment's entry statistics and the keys of the
 // segment up to the chunk (clean_out), so every chunk runs in parallel.
 struct CleanArgs {
@@ -35,9 +35,6 @@ struct CleanArgs {
                       // in 64-column slices
   float* csum;        // [B*H, NC, dk] key sum of every chunk
   float* ssum;        // [B*H, NS, dk] key sum of every segment
-  float* mr;          // [B*H, NC, dk] key sum before the chunk, about c_s
-  float* cs;          // [B*H, NS, dk] centre c_s of each segment
-  float* ms;          // [B*H, NS, dk] raw key sum before each segment
   int B, T, H, dk;
   int centered;
   int seg;            // chunks per segment
@@ -161,7 +158,6 @@ struct CcqDkArgs {
 // Each launcher returns hipSuccess or the launch error.  is_bf16 selects the
 // io dtype (bf16 or fp32); shapes are validated by the caller.
 hipError_t launch_clean_gram(const CleanArgs& a, bool is_bf16, hipStream_t st);
-hipError_t launch_clean_msum(const CleanArgs& a, hipStream_t st);
 hipError_t launch_clean_prefix(const CleanArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_clean_out(const CleanArgs& a, bool is_bf16, hipStream_t st);
 constexpr int kCleanSeg = 8;   // chunks per segment of the query contraction
