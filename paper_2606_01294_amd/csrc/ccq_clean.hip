@@ -56,45 +56,48 @@ __device__ __forceinline__ f32x4 load4f(const T* p) {
 
 }  // namespace
 
-// Raw segment Gram matrix G_s = sum_{j in s} k_j k_j^T, one 64-column slice
-// per workgroup (wave w owns rows [w DK/4, (w+1) DK/4)); the workgroups of
-// slice 0 also write the key sums of every chunk and of the segment.
+// Raw segment Gram matrix G_s = sum_{j in s} k_j k_j^T, one workgroup per
+// (head, segment); wave w owns rows [w RW, (w+1) RW) and all columns, so each
+// chunk of keys is read from memory once.  The chunk and segment key sums come
+// from the same products (a ones column).  G is symmetric: each tile is
+// written transposed, as rows of four consecutive features (16-byte stores).
 template <typename T, int DK>
-__global__ __launch_bounds__(kThreads) void clean_gram_kernel(const CleanArgs a) {
+__global__ __launch_bounds__(64 * (DK >= 128 ? 8 : 4), 1) void clean_gram_kernel(const CleanArgs a) {
   constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P;
-  constexpr int RT = DK / 64;  // 16-row tiles per wave
-  __shared__ __align__(16) T sK[C * LDK];
+  constexpr int NWG = DK >= 128 ? 8 : 4, NTG = 64 * NWG;
+  constexpr int RW = DK / NWG;  // rows per wave
+  constexpr int RT = RW / 16;   // row tiles per wave
+  constexpr int CT = DK / 16;   // column tiles
+  __shared__ __align__(16) T sK[2][C * LDK];
 
-  const int NC = n_chunks(a.T), NS = n_segs(a.T, a.seg), NB = DK / 64;
+  const int NC = n_chunks(a.T), NS = n_segs(a.T, a.seg);
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int tb = lb % NB, s = (lb / NB) % NS, bh = lb / (NB * NS);
+  const int bh = lb / NS, s = lb % NS;
   const int b = bh / a.H, h = bh % a.H;
   const int w = wave_id(), l = lane_id(), g4 = l >> 4, c16 = l & 15;
-  const int a0 = w * (DK / 4), b0 = 64 * tb;
-  const bool sums = tb == 0;
+  const int a0 = w * RW;
   const T* k = static_cast<const T*>(a.k);
   const size_t gstride = (size_t)a.H * DK;
   const int cbeg = s * a.seg, cend = min(NC, cbeg + a.seg);
 
-  f32x4 acc[RT][4];
+  f32x4 acc[RT][CT], stot[RT];
 #pragma unroll
-  for (int v = 0; v < RT; ++v)
+  for (int v = 0; v < RT; ++v) {
+    stot[v] = zero4();
 #pragma unroll
-    for (int t = 0; t < 4; ++t) acc[v][t] = zero4();
+    for (int t = 0; t < CT; ++t) acc[v][t] = zero4();
+  }
 
-  RowTile<T, DK> rk;
+  RowTile<T, DK, NTG> rk;
   auto load = [&](int c) {
     rk.load(k + tok_off(b, c * C, h, a.T, a.H, DK), gstride, min(C, a.T - c * C));
   };
   load(cbeg);
   const Frag<T> ones = ones_col_frag<T>();
-  f32x4 stot[RT];
-#pragma unroll
-  for (int v = 0; v < RT; ++v) stot[v] = zero4();
 
   for (int c = cbeg; c < cend; ++c) {
-    __syncthreads();  // previous chunk's readers are done
-    rk.store(sK, LDK);
+    T* buf = sK[(c - cbeg) & 1];  // the other buffer may still be read by a slower wave
+    rk.store(buf, LDK);
     if (c + 1 < cend) load(c + 1);
     __syncthreads();
     f32x4 msum[RT];
@@ -102,42 +105,39 @@ __global__ __launch_bounds__(kThreads) void clean_gram_kernel(const CleanArgs a)
     for (int v = 0; v < RT; ++v) msum[v] = zero4();
 #pragma unroll
     for (int k0 = 0; k0 < C; k0 += 32) {
-      Frag<T> fb[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) fb[t] = ld_frag_tr(sK + k0 * LDK + b0 + 16 * t, LDK);
+      Frag<T> fa[RT];
 #pragma unroll
       for (int v = 0; v < RT; ++v) {
-        const Frag<T> fa = ld_frag_tr(sK + k0 * LDK + a0 + 16 * v, LDK);
+        fa[v] = ld_frag_tr(buf + k0 * LDK + a0 + 16 * v, LDK);
+        mma(msum[v], fa[v], ones);
+      }
 #pragma unroll
-        for (int t = 0; t < 4; ++t) mma(acc[v][t], fa, fb[t]);
-        if (sums) mma(msum[v], fa, ones);
+      for (int t = 0; t < CT; ++t) {
+        const Frag<T> fb = ld_frag_tr(buf + k0 * LDK + 16 * t, LDK);
+#pragma unroll
+        for (int v = 0; v < RT; ++v) mma(acc[v][t], fa[v], fb);
       }
     }
-    if (sums && c16 == 0) {
+    if (c16 == 0) {
 #pragma unroll
       for (int v = 0; v < RT; ++v) {
         stot[v] += msum[v];
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          a.csum[((size_t)bh * NC + c) * DK + a0 + 16 * v + 4 * g4 + r] = msum[v][r];
+        *reinterpret_cast<f32x4*>(a.csum + ((size_t)bh * NC + c) * DK + a0 + 16 * v + 4 * g4) = msum[v];
       }
     }
   }
-  if (sums && c16 == 0) {
+  if (c16 == 0) {
 #pragma unroll
     for (int v = 0; v < RT; ++v)
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        a.ssum[((size_t)bh * NS + s) * DK + a0 + 16 * v + 4 * g4 + r] = stot[v][r];
+      *reinterpret_cast<f32x4*>(a.ssum + ((size_t)bh * NS + s) * DK + a0 + 16 * v + 4 * g4) = stot[v];
   }
+  // acc[v][t][r] = G[a0 + 16 v + 4 g4 + r][16 t + c16], stored at the mirror position
   float* G = a.gram + ((size_t)bh * NS + s) * DK * DK;
 #pragma unroll
   for (int v = 0; v < RT; ++v)
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        G[(size_t)(a0 + 16 * v + 4 * g4 + r) * DK + b0 + 16 * t + c16] = acc[v][t][r];
+    for (int t = 0; t < CT; ++t)
+      *reinterpret_cast<f32x4*>(G + (size_t)(16 * t + c16) * DK + a0 + 16 * v + 4 * g4) = acc[v][t];
 }
 
 // S'_s = S_s - M'_s c_s^T - c_s M'_s^T - n_s c_s c_s^T with S_s the raw second
@@ -434,9 +434,10 @@ __global__ __launch_bounds__(kThreads * CPW, 1) void clean_out_kernel(const Clea
 namespace {
 template <typename T, int DK>
 hipError_t run_gram(const CleanArgs& a, hipStream_t st) {
-  const long long nblk = (long long)a.B * a.H * n_segs(a.T, a.seg) * (DK / 64);
+  const long long nblk = (long long)a.B * a.H * n_segs(a.T, a.seg);
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((clean_gram_kernel<T, DK>), dim3((unsigned)nblk), dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((clean_gram_kernel<T, DK>), dim3((unsigned)nblk), dim3(64 * (DK >= 128 ? 8 : 4)), 0,
+                     st, a);
   return hipGetLastError();
 }
 template <typename T, int DK>
