@@ -129,81 +129,95 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
   }
 }
 
-// Outputs of one chunk for a 64-wide value slice (eight waves):
+// Outputs of one chunk (eight waves), all value columns:
 //   o = scale * (Qt (S_r diag e^{b_m})^T + (Qt Kt^T masked) V)
-template <typename T, typename TG, int DK>
+// The gate prefix is scanned in parallel (TPC threads per key channel), the
+// masked score block is formed once (ten nonzero 16 x 16 tiles over the
+// waves) and kept in LDS in accumulator-pair order, and each wave then owns
+// value tiles for IPW token tiles, transposed: O^T = S_r' Qt^T + V^T P^T, with
+// rows of S_r read straight from global memory and scaled by e^{b_m} per key
+// channel.  V is staged VP columns at a time.
+template <typename T, typename TG, int DK, int VP, int VPW, int IPW>
 __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArgs a) {
-  constexpr int C = kChunk, BVO = 64;
+  constexpr int C = kChunk, NT = kOutThreads;
   constexpr int P = Pad<T>::value;
-  constexpr int LDQ = DK + P, LDV = BVO + P, LDA = C + P, LDG = DK + 1;
-  static_assert(DK <= kOutThreads, "one thread per key channel in the scan");
+  constexpr int LDQ = DK + P, LDV = VP + P, LDP = C + P, LDB = DK + 4;
+  constexpr int NK = DK / 32;
+  constexpr int NIG = 4 / IPW, NVG = 8 / NIG;
+  static_assert(NVG * NIG == 8 && NVG * VPW * 16 == VP, "wave split");
+  constexpr int TPC = NT / DK, TOK = C / TPC;  // scan: threads per channel, tokens per thread
+  static_assert(TPC * DK == NT && TOK * TPC == C, "scan split");
 
   __shared__ __align__(16) T sQt[C * LDQ];
   __shared__ __align__(16) T sKt[C * LDQ];
-  __shared__ __align__(16) T sS[BVO * LDQ];
   __shared__ __align__(16) T sV[C * LDV];
-  constexpr int kGBytes = C * LDG * 4, kABytes = C * LDA * (int)sizeof(T);
-  __shared__ __align__(16) char sGA[kGBytes > kABytes ? kGBytes : kABytes];
-  float* sG = reinterpret_cast<float*>(sGA);  // gates, then their prefix b
-  T* sA = reinterpret_cast<T*>(sGA);          // intra block, once sG is dead
+  constexpr int kBBytes = C * LDB * 4, kPBytes = C * LDP * (int)sizeof(T);
+  __shared__ __align__(16) char sBP[kBBytes > kPBytes ? kBBytes : kPBytes];
+  float* sB = reinterpret_cast<float*>(sBP);  // gates, then their prefix b
+  T* sP = reinterpret_cast<T*>(sBP);          // masked scores, once sB is dead
   __shared__ __align__(16) float sBm[DK];
+  __shared__ float sTot[TPC][DK];
 
-  const int nvt = a.dv / BVO;
   const int N = (a.T + C - 1) / C;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int vt = lb % nvt, ci = (lb / nvt) % N, bh = lb / (nvt * N);
-  const int v0 = vt * BVO;
+  const int bh = lb / N, ci = lb % N;
   const int b = bh / a.H, h = bh % a.H;
   const int r0 = ci * C;
   const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
   const int tid = threadIdx.x, w = tid >> 6, l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
+  const int vg = w % NVG, ig = w / NVG;
   const size_t gstride = (size_t)a.H * DK;
 
-  ChunkTile<T, DK, kOutThreads> rq, rk, rs;
-  ChunkTile<TG, DK, kOutThreads> rg;
-  {
-    ChunkTile<T, BVO, kOutThreads> rv;
-    rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-    rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-    rg.load(static_cast<const TG*>(a.g) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-    rs.load(static_cast<const T*>(a.states) + (((size_t)bh * N + ci) * a.dv + v0) * DK, (size_t)DK, C);
-    rv.load(static_cast<const T*>(a.v) + tok_off(b, r0, h, a.T, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
-    rg.store_f32(sG, LDG);
-    rv.store(sV, LDV);
+  RowTile<T, DK, NT> rq, rk;
+  RowTile<TG, DK, NT> rg;
+  rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+  rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+  rg.load(static_cast<const TG*>(a.g) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+#pragma unroll
+  for (int u = 0; u < RowTile<TG, DK, NT>::NV; ++u) {  // gates as fp32 rows
+    const auto x = rg.get(u);
+    float* dst = sB + RowTile<TG, DK, NT>::row(u) * LDB + RowTile<TG, DK, NT>::col(u);
+    *reinterpret_cast<f32x4*>(dst) = f32x4{f32(x[0]), f32(x[1]), f32(x[2]), f32(x[3])};
+    *reinterpret_cast<f32x4*>(dst + 4) = f32x4{f32(x[4]), f32(x[5]), f32(x[6]), f32(x[7])};
   }
   __syncthreads();
-  if (tid < DK) {
-    float x[C];
+  {  // inclusive prefix over the chunk, TPC threads per channel
+    const int c = tid % DK, part = tid / DK, j0 = part * TOK;
+    float x[TOK];
 #pragma unroll
-    for (int j = 0; j < C; ++j) x[j] = sG[j * LDG + tid];
+    for (int j = 0; j < TOK; ++j) x[j] = sB[(j0 + j) * LDB + c];
 #pragma unroll
-    for (int j = 1; j < C; ++j) x[j] += x[j - 1];
+    for (int j = 1; j < TOK; ++j) x[j] += x[j - 1];
+    sTot[part][c] = x[TOK - 1];
+    __syncthreads();
+    float off = 0.f;
 #pragma unroll
-    for (int j = 0; j < C; ++j) sG[j * LDG + tid] = x[j];
-    sBm[tid] = __expf(x[C / 2 - 1]);
+    for (int p2 = 0; p2 < TPC - 1; ++p2)
+      if (p2 < part) off += sTot[p2][c];
+#pragma unroll
+    for (int j = 0; j < TOK; ++j) sB[(j0 + j) * LDB + c] = x[j] + off;
+    if (j0 <= C / 2 - 1 && C / 2 - 1 < j0 + TOK) sBm[c] = __expf(x[C / 2 - 1 - j0] + off);
   }
   __syncthreads();
-  {
-    const int j = ChunkTile<T, DK, kOutThreads>::row();
+  // Qt = q e^{b - b_m}, Kt = k e^{b_m - b}
 #pragma unroll
-    for (int u = 0; u < ChunkTile<T, DK, kOutThreads>::NV; ++u) {
-      const int cc = ChunkTile<T, DK, kOutThreads>::col(u);
-      const auto xq = rq.get(u), xk = rk.get(u), xs = rs.get(u);
-      typename ChunkTile<T, DK, kOutThreads>::vec_t qo, ko, so;
+  for (int u = 0; u < RowTile<T, DK, NT>::NV; ++u) {
+    const int j = RowTile<T, DK, NT>::row(u), cc = RowTile<T, DK, NT>::col(u);
+    const auto xq = rq.get(u), xk = rk.get(u);
+    typename RowTile<T, DK, NT>::vec_t qo, ko;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float d = sG[j * LDG + cc + e] - sG[(C / 2 - 1) * LDG + cc + e];
-        qo[e] = to<T>(f32(xq[e]) * __expf(d));
-        ko[e] = to<T>(f32(xk[e]) * __expf(-d));
-        so[e] = to<T>(f32(xs[e]) * sBm[cc + e]);  // row j of the tile is value v0 + j
-      }
-      *reinterpret_cast<typename ChunkTile<T, DK, kOutThreads>::vec_t*>(sQt + j * LDQ + cc) = qo;
-      *reinterpret_cast<typename ChunkTile<T, DK, kOutThreads>::vec_t*>(sKt + j * LDQ + cc) = ko;
-      *reinterpret_cast<typename ChunkTile<T, DK, kOutThreads>::vec_t*>(sS + j * LDQ + cc) = so;
+    for (int e = 0; e < 8; ++e) {
+      const float d = sB[j * LDB + cc + e] - sB[(C / 2 - 1) * LDB + cc + e];
+      qo[e] = to<T>(f32(xq[e]) * __expf(d));
+      ko[e] = to<T>(f32(xk[e]) * __expf(-d));
     }
+    *reinterpret_cast<typename RowTile<T, DK, NT>::vec_t*>(sQt + j * LDQ + cc) = qo;
+    *reinterpret_cast<typename RowTile<T, DK, NT>::vec_t*>(sKt + j * LDQ + cc) = ko;
   }
-  __syncthreads();  // sG is dead from here on
+  __syncthreads();  // sB is dead from here on
+
+  // masked score tiles, transposed (row j, column i), stored as rows i
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     const int t = w + 8 * s;
@@ -216,24 +230,59 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
 #pragma unroll
       for (int r = 0; r < 4; ++r) x[r] = (16 * J + 4 * g4 + r <= i) ? sc[r] : 0.f;
     }
-    store4(sA + i * LDA + 16 * J + 4 * g4, x[0], x[1], x[2], x[3]);
+    store4(sP + i * LDP + acc_pos(16 * J + 4 * g4), x[0], x[1], x[2], x[3]);
   }
-  __syncthreads();
-  {
-    const int st = w & 3;
-    T* o = static_cast<T*>(a.o);
+
+  const T* Sg = static_cast<const T*>(a.states) + ((size_t)bh * N + ci) * a.dv * DK;
+  T* o = static_cast<T*>(a.o);
+  for (int vp = 0; vp < a.dv; vp += VP) {
+    if (vp > 0) __syncthreads();  // every wave is done with the previous V slice
+    {
+      RowTile<T, VP, NT> rv;
+      rv.load(static_cast<const T*>(a.v) + tok_off(b, r0, h, a.T, a.H, a.dv) + vp, (size_t)a.H * a.dv, nrow);
+      rv.store(sV, LDV);
+    }
+    // this wave's rows of S_r (k = key channel), scaled by e^{b_m}
+    Frag<T> sfr[VPW][NK];
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const int tv = 2 * (w >> 2) + s;
-      f32x4 acc = zero4();
-      tile_mma<T, DK>(acc, sQt + 16 * st * LDQ, LDQ, sS + 16 * tv * LDQ, LDQ);
+    for (int vt = 0; vt < VPW; ++vt) {
+      const int vr = vp + 16 * (vg * VPW + vt);
 #pragma unroll
-      for (int k0 = 0; k0 < C; k0 += 32)
-        if (k0 <= 16 * st) mma(acc, ld_frag(sA + 16 * st * LDA + k0, LDA), ld_frag_tr(sV + k0 * LDV + 16 * tv, LDV));
+      for (int m = 0; m < NK; ++m) {
+        Frag<T> f = ld_frag_global(Sg + (size_t)vr * DK + 32 * m, (size_t)DK);
+        const f32x4 e0 = *reinterpret_cast<const f32x4*>(sBm + 32 * m + 8 * g4);
+        const f32x4 e1 = *reinterpret_cast<const f32x4*>(sBm + 32 * m + 8 * g4 + 4);
+        if constexpr (sizeof(T) == 2) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i = 16 * st + 4 * g4 + r;
-        if (i < nrow) o[tok_off(b, r0 + i, h, a.T, a.H, a.dv) + v0 + 16 * tv + c16] = to<T>(a.scale * acc[r]);
+          for (int e = 0; e < 8; ++e) f.v[e] = to<T>(f32(f.v[e]) * (e < 4 ? e0[e] : e1[e - 4]));
+        } else {
+          f.lo *= e0;
+          f.hi *= e1;
+        }
+        sfr[vt][m] = f;
+      }
+    }
+    __syncthreads();  // sV and sP are ready
+#pragma unroll
+    for (int it = 0; it < IPW; ++it) {
+      const int I = ig * IPW + it;
+      const int i = 16 * I + c16;
+      Frag<T> qf[NK];
+#pragma unroll
+      for (int m = 0; m < NK; ++m) qf[m] = ld_frag(sQt + 16 * I * LDQ + 32 * m, LDQ);
+      const Frag<T> pf0 = ld_frag(sP + 16 * I * LDP, LDP);
+      const Frag<T> pf1 = ld_frag(sP + 16 * I * LDP + 32, LDP);
+#pragma unroll
+      for (int vt = 0; vt < VPW; ++vt) {
+        const int vl = 16 * (vg * VPW + vt);  // value column within the slice
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int m = 0; m < NK; ++m) mma(acc, sfr[vt][m], qf[m]);
+        mma(acc, ld_frag_tr_acc(sV + vl, LDV), pf0);
+        if (I >= 2) mma(acc, ld_frag_tr_acc(sV + 32 * LDV + vl, LDV), pf1);  // keys 32..63 precede row i
+        if (i < nrow)
+          store4(o + tok_off(b, r0 + i, h, a.T, a.H, a.dv) + vp + vl + 4 * g4, a.scale * acc[0],
+                 a.scale * acc[1], a.scale * acc[2], a.scale * acc[3]);
       }
     }
   }
@@ -247,17 +296,30 @@ hipError_t run_gla_state(const GlaStateArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((gla_state_kernel<T, TG>), dim3(nblk), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
+template <typename T, typename TG, int DK, int VP, int VPW, int IPW>
+hipError_t run_gla_out_v(const GlaOutArgs& a, hipStream_t st) {
+  const int nblk = a.B * a.H * ((a.T + kChunk - 1) / kChunk);
+  if (nblk == 0) return hipSuccess;
+  hipLaunchKernelGGL((gla_out_kernel<T, TG, DK, VP, VPW, IPW>), dim3(nblk), dim3(kOutThreads), 0, st, a);
+  return hipGetLastError();
+}
+// V is staged at most 256 columns (fp32: 128) at a time.
+template <typename T, typename TG, int DK>
+hipError_t run_gla_out_dk(const GlaOutArgs& a, hipStream_t st) {
+  constexpr bool kWide = sizeof(T) == 2;
+  switch (a.dv) {
+    case 64: return run_gla_out_v<T, TG, DK, 64, 1, 2>(a, st);
+    case 128: return run_gla_out_v<T, TG, DK, 128, 1, 4>(a, st);
+    default:
+      if constexpr (kWide) return run_gla_out_v<T, TG, DK, 256, 2, 4>(a, st);
+      else return run_gla_out_v<T, TG, DK, 128, 1, 4>(a, st);
+  }
+}
 template <typename T, typename TG>
 hipError_t run_gla_out(const GlaOutArgs& a, hipStream_t st) {
-  const int nblk = a.B * a.H * ((a.T + kChunk - 1) / kChunk) * (a.dv / 64);
-  if (nblk == 0) return hipSuccess;
-  if (a.dk == 64)
-    hipLaunchKernelGGL((gla_out_kernel<T, TG, 64>), dim3(nblk), dim3(kOutThreads), 0, st, a);
-  else if (a.dk == 128)
-    hipLaunchKernelGGL((gla_out_kernel<T, TG, 128>), dim3(nblk), dim3(kOutThreads), 0, st, a);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+  if (a.dk == 64) return run_gla_out_dk<T, TG, 64>(a, st);
+  if (a.dk == 128) return run_gla_out_dk<T, TG, 128>(a, st);
+  return hipErrorInvalidValue;
 }
 }  // namespace
 
