@@ -36,15 +36,6 @@ __host__ __device__ inline int n_chunks(int T) { return (T + kChunk - 1) / kChun
 __host__ __device__ inline int n_segs(int T, int seg) { return (n_chunks(T) + seg - 1) / seg; }
 
 template <typename T>
-__device__ __forceinline__ float frag_elem(const Frag<T>& f, int e) {
-  if constexpr (sizeof(T) == 2) {
-    return static_cast<float>(f.v[e]);
-  } else {
-    return e < 4 ? f.lo[e] : f.hi[e - 4];
-  }
-}
-
-template <typename T>
 __device__ __forceinline__ f32x4 load4f(const T* p) {
   if constexpr (sizeof(T) == 2) {
     const bf16x4 v = *reinterpret_cast<const bf16x4*>(p);

@@ -199,6 +199,25 @@ __device__ __forceinline__ void store_acc_pair(T* p, const f32x4& x, const f32x4
   }
 }
 
+template <typename T>
+__device__ __forceinline__ float frag_elem(const Frag<T>& f, int e) {
+  if constexpr (sizeof(T) == 2) {
+    return static_cast<float>(f.v[e]);
+  } else {
+    return e < 4 ? f.lo[e] : f.hi[e - 4];
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void set_frag_elem(Frag<T>& f, int e, float x) {
+  if constexpr (sizeof(T) == 2) {
+    f.v[e] = static_cast<bf16_t>(x);
+  } else {
+    if (e < 4) f.lo[e] = x;
+    else f.hi[e - 4] = x;
+  }
+}
+
 // Store a fragment's 8 elements contiguously (one 16- or 32-byte store).
 template <typename T>
 __device__ __forceinline__ void store_frag(T* p, const Frag<T>& f) {

@@ -7,8 +7,8 @@
 //   o_i     = S_r (q_i * e^{b_i}) + sum_{j<=i} [sum_c q_i[c] k_j[c] e^{b_i[c]-b_j[c]}] v_j
 //   S_{r+1} = S_r diag(e^{b_C}) + sum_j v_j (k_j * e^{b_C - b_j})^T
 //
-// gla_state_kernel carries one 64x64 tile of S through the chunks of a head
-// (rows and columns of S evolve independently under the GLA write) and
+// gla_state_kernel carries a 64-channel tile of S through the chunks of a
+// head (rows and columns of S evolve independently under the GLA write) and
 // stores S_r for every chunk; gla_out_kernel forms every chunk's outputs in
 // parallel.  The output uses a mid-chunk reference m = C/2: Qt = q * e^{b - b_m},
 // Kt = k * e^{b_m - b}, so Qt Kt^T carries e^{b_i - b_j} with factors of at most
@@ -19,43 +19,51 @@
 
 namespace ccq {
 
-template <typename T, typename TG>
+// State recurrence over the chunks of one head for 64 key channels and VB
+// values.  Wave w owns channels c0 + 16 w .. + 15 (rows of S^T in its MFMA
+// accumulators) for all VB values.  Per chunk the keys, gates and values are
+// staged once (double-buffered LDS, one barrier); each wave then reads its
+// channels' gates and keys transposed (lane = channel, 8 tokens per lane and
+// k step), scans the gates in registers (8-token runs, then shuffles across
+// the four lane groups) and forms the decayed keys k e^{b_C - b} directly as
+// the MFMA operand of  S^T <- diag(e^{b_C}) S^T + Kd^T V.  S_r is written
+// back one iteration late (all vector memory operations share one in-order
+// counter, so a store just before the next loads are waited for would add
+// its latency to every chunk).
+template <typename T, typename TG, int NVT>
 __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateArgs a) {
-  constexpr int C = kChunk, BK = 64, BV = 64;
-  constexpr int P = Pad<T>::value;
-  constexpr int LDK = BK + P, LDV = BV + P, LDG = BK + 1;
-  constexpr int NTV = BV / 16;  // wave w owns key rows 16w..16w+15 of the tile, all value tiles
+  constexpr int C = kChunk, BK = 64, VB = 16 * NVT;
+  constexpr int P = Pad<T>::value, PG = Pad<TG>::value;
+  constexpr int LDK = BK + P, LDG = BK + PG, LDV = VB + P;
 
-  __shared__ __align__(16) T sKd[C * LDK];  // k e^{b_C - b}
-  __shared__ __align__(16) T sV[C * LDV];
-  __shared__ float sG[C * LDG];
-  __shared__ float sDec[BK];
+  __shared__ __align__(16) T sK[2][C * LDK];
+  __shared__ __align__(16) TG sG[2][C * LDG];
+  __shared__ __align__(16) T sV[2][C * LDV];
 
-  const int nkt = a.dk / BK, nvt = a.dv / BV;
+  const int nkt = a.dk / BK, nvt = a.dv / VB;
   const int N = (a.T + C - 1) / C;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
   const int bh = lb / (nkt * nvt), kt = (lb / nvt) % nkt, vt = lb % nvt;
-  const int c0 = kt * BK, v0 = vt * BV;
+  const int c0 = kt * BK, v0 = vt * VB;
   const int b = bh / a.H, h = bh % a.H;
-  const int tid = threadIdx.x, w = wave_id(), l = lane_id();
+  const int w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
   const T* k = static_cast<const T*>(a.k);
   const T* v = static_cast<const T*>(a.v);
   const TG* gate = static_cast<const TG*>(a.g);
 
-  // S^T tile: S[tv][r] = S[v][c], c = c0 + 16 w + 4 g4 + r, v = v0 + 16 tv + c16
-  f32x4 S[NTV];
+  // S^T tiles: S[tv][r] = S[v][c], c = c0 + 16 w + 4 g4 + r, v = v0 + 16 tv + c16
+  f32x4 S[NVT];
 #pragma unroll
-  for (int tv = 0; tv < NTV; ++tv)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int c = c0 + 16 * w + 4 * g4 + r, vv = v0 + 16 * tv + c16;
-      S[tv][r] = a.S0 ? a.S0[((size_t)bh * a.dv + vv) * a.dk + c] : 0.f;
-    }
+  for (int tv = 0; tv < NVT; ++tv) {
+    const int vv = v0 + 16 * tv + c16;
+    S[tv] = a.S0 ? *reinterpret_cast<const f32x4*>(a.S0 + ((size_t)bh * a.dv + vv) * a.dk + c0 + 16 * w + 4 * g4)
+                 : zero4();
+  }
 
-  ChunkTile<T, BK> rk;
-  ChunkTile<TG, BK> rg;
-  ChunkTile<T, BV> rv;
+  RowTile<T, BK> rk;
+  RowTile<TG, BK> rg;
+  RowTile<T, VB> rv;
   auto prefetch = [&](int ci) {
     const int r0 = ci * C;
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
@@ -63,69 +71,76 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
     rg.load(gate + tok_off(b, r0, h, a.T, a.H, a.dk) + c0, (size_t)a.H * a.dk, nrow);
     rv.load(v + tok_off(b, r0, h, a.T, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
   };
+  f32x4 Sr[NVT];  // S_r kept for the deferred write-back
+  auto write_back = [&](int cw) {
+    T* st = static_cast<T*>(a.states) + (((size_t)bh * N + cw) * a.dv + v0) * a.dk + c0 + 16 * w + 4 * g4;
+#pragma unroll
+    for (int tv = 0; tv < NVT; ++tv)
+      store4(st + (size_t)(16 * tv + c16) * a.dk, Sr[tv][0], Sr[tv][1], Sr[tv][2], Sr[tv][3]);
+  };
   if (N > 0) prefetch(0);
 
   for (int ci = 0; ci < N; ++ci) {
-    __syncthreads();  // (A)
-    rg.store_f32(sG, LDG);
-    rv.store(sV, LDV);
-    {  // S_r, the state entering this chunk
-      T* st = static_cast<T*>(a.states) + (((size_t)bh * N + ci) * a.dv + v0) * a.dk + c0 + 16 * w + 4 * g4;
-#pragma unroll
-      for (int tv = 0; tv < NTV; ++tv)
-        store4(st + (size_t)(16 * tv + c16) * a.dk, S[tv][0], S[tv][1], S[tv][2], S[tv][3]);
-    }
-    __syncthreads();  // (B)
-    if (tid < BK) {  // inclusive log-decay prefix of key channel c0 + tid
-      float x[C];
-#pragma unroll
-      for (int j = 0; j < C; ++j) x[j] = sG[j * LDG + tid];
-#pragma unroll
-      for (int j = 1; j < C; ++j) x[j] += x[j - 1];
-#pragma unroll
-      for (int j = 0; j < C; ++j) sG[j * LDG + tid] = x[j];
-      sDec[tid] = __expf(x[C - 1]);
-    }
-    __syncthreads();  // (C)
-    {
-      const int j = ChunkTile<T, BK>::row();
-#pragma unroll
-      for (int u = 0; u < ChunkTile<T, BK>::NV; ++u) {
-        const int cc = ChunkTile<T, BK>::col(u);
-        const auto xk = rk.get(u);
-        typename ChunkTile<T, BK>::vec_t ko;
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          ko[e] = to<T>(f32(xk[e]) * __expf(sG[(C - 1) * LDG + cc + e] - sG[j * LDG + cc + e]));
-        *reinterpret_cast<typename ChunkTile<T, BK>::vec_t*>(sKd + j * LDK + cc) = ko;
-      }
-    }
+    const int buf = ci & 1;  // the other buffer was released at the previous barrier
+    rk.store(sK[buf], LDK);
+    rg.store(sG[buf], LDG);
+    rv.store(sV[buf], LDV);
+    if (ci > 0) write_back(ci - 1);
     if (ci + 1 < N) prefetch(ci + 1);
-    __syncthreads();  // (D)
-    // S^T <- diag(e^{b_C}) S^T + Kd^T V
-    {
-      const f32x4 dec = *reinterpret_cast<const f32x4*>(sDec + 16 * w + 4 * g4);
 #pragma unroll
-      for (int tv = 0; tv < NTV; ++tv)
+    for (int tv = 0; tv < NVT; ++tv) Sr[tv] = S[tv];
+    __syncthreads();
+
+    // gates and keys of this wave's channels: lane = channel c0 + 16 w + c16,
+    // tokens 32 m + 8 g4 + e
+    const Frag<TG> gf0 = ld_frag_tr(sG[buf] + 16 * w, LDG);
+    const Frag<TG> gf1 = ld_frag_tr(sG[buf] + 32 * LDG + 16 * w, LDG);
+    const Frag<T> kf0 = ld_frag_tr(sK[buf] + 16 * w, LDK);
+    const Frag<T> kf1 = ld_frag_tr(sK[buf] + 32 * LDK + 16 * w, LDK);
+    float pb[2][8], tot[2], ex[2], half[2];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) S[tv][r] *= dec[r];
+    for (int e = 0; e < 8; ++e) {
+      pb[0][e] = frag_elem(gf0, e) + (e ? pb[0][e - 1] : 0.f);
+      pb[1][e] = frag_elem(gf1, e) + (e ? pb[1][e - 1] : 0.f);
+    }
 #pragma unroll
-      for (int k0 = 0; k0 < C; k0 += 32) {
-        const Frag<T> fa = ld_frag_tr(sKd + k0 * LDK + 16 * w, LDK);
+    for (int m = 0; m < 2; ++m) {  // scan of the 8-token totals over the four lane groups
+      tot[m] = pb[m][7];
+      float sc = tot[m];
+      const float u1 = __shfl_up(sc, 16);
+      if (g4 >= 1) sc += u1;
+      const float u2 = __shfl_up(sc, 32);
+      if (g4 >= 2) sc += u2;
+      ex[m] = sc - tot[m];
+      half[m] = __shfl(sc, 48 + c16);
+    }
+    const float bC = half[0] + half[1];
+    Frag<T> kd0, kd1;
 #pragma unroll
-        for (int tv = 0; tv < NTV; ++tv) mma(S[tv], fa, ld_frag_tr(sV + k0 * LDV + 16 * tv, LDV));
-      }
+    for (int e = 0; e < 8; ++e) {
+      const float b0 = ex[0] + pb[0][e], b1 = half[0] + ex[1] + pb[1][e];
+      set_frag_elem(kd0, e, frag_elem(kf0, e) * __expf(bC - b0));
+      set_frag_elem(kd1, e, frag_elem(kf1, e) * __expf(bC - b1));
+    }
+    // S^T <- diag(e^{b_C}) S^T + Kd^T V; row c = 4 g4 + r of the tile needs e^{b_C[c]}
+    f32x4 dec;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) dec[r] = __expf(__shfl(bC, 4 * g4 + r));
+#pragma unroll
+    for (int tv = 0; tv < NVT; ++tv) {
+      S[tv] *= dec;
+      mma(S[tv], kd0, ld_frag_tr(sV[buf] + 16 * tv, LDV));
+      mma(S[tv], kd1, ld_frag_tr(sV[buf] + 32 * LDV + 16 * tv, LDV));
     }
   }
 
+  if (N > 0) write_back(N - 1);
   if (a.ST) {
 #pragma unroll
-    for (int tv = 0; tv < NTV; ++tv)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int c = c0 + 16 * w + 4 * g4 + r, vv = v0 + 16 * tv + c16;
-        a.ST[((size_t)bh * a.dv + vv) * a.dk + c] = S[tv][r];
-      }
+    for (int tv = 0; tv < NVT; ++tv) {
+      const int vv = v0 + 16 * tv + c16;
+      *reinterpret_cast<f32x4*>(a.ST + ((size_t)bh * a.dv + vv) * a.dk + c0 + 16 * w + 4 * g4) = S[tv];
+    }
   }
 }
 
@@ -289,12 +304,20 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
 }
 
 namespace {
+template <typename T, typename TG, int NVT>
+hipError_t run_gla_state_v(const GlaStateArgs& a, hipStream_t st) {
+  const int nblk = a.B * a.H * (a.dk / 64) * (a.dv / (16 * NVT));
+  if (nblk == 0) return hipSuccess;
+  hipLaunchKernelGGL((gla_state_kernel<T, TG, NVT>), dim3(nblk), dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
+// 64-wide value slices when they still give every SIMD a wave, else 32 or 16.
 template <typename T, typename TG>
 hipError_t run_gla_state(const GlaStateArgs& a, hipStream_t st) {
-  const int nblk = a.B * a.H * (a.dk / 64) * (a.dv / 64);
-  if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((gla_state_kernel<T, TG>), dim3(nblk), dim3(kThreads), 0, st, a);
-  return hipGetLastError();
+  const long long waves64 = (long long)a.B * a.H * (a.dk / 64) * (a.dv / 64) * 4;
+  if (waves64 >= 1024) return run_gla_state_v<T, TG, 4>(a, st);
+  if (waves64 * 2 >= 1024) return run_gla_state_v<T, TG, 2>(a, st);
+  return run_gla_state_v<T, TG, 1>(a, st);
 }
 template <typename T, typename TG, int DK, int VP, int VPW, int IPW>
 hipError_t run_gla_out_v(const GlaOutArgs& a, hipStream_t st) {
