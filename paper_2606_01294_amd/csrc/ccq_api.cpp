@@ -116,7 +116,7 @@ FwdLayout fwd_layout(const ccq_shape* s, ccq_backbone bb) {
   L.clean = take_clean_ws(s, take);
   if (bb == CCQ_GDN) {
     L.Tm = take(nchunk * 64 * 64 * e);
-    L.gam = take(nchunk * 64 * sizeof(float));
+    L.gam = take(nchunk * 5 * 64 * sizeof(float));
     L.U = take(nchunk * 64 * s->dv * e);
   }
   L.total = off;

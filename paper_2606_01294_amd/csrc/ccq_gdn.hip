@@ -27,7 +27,9 @@
 
 namespace ccq {
 
-// Tm = (I + A)^{-1} of one chunk, plus the chunk's cumulative log decays.
+// Tm = (I + A)^{-1} of one chunk, plus the chunk's decay coefficients
+// (gamma_j, beta_j e^{gamma_j}, beta_j, e^{gamma_C - gamma_j}, e^{gamma_C}), so the
+// sequential state pass needs no exponentials.
 // Blocks of 16: the diagonal blocks are inverted by forward substitution,
 // then wave w forms column block w, X_iw = -D_i sum_{m=w}^{i-1} A_im X_mw.
 template <typename T, int DK>
@@ -64,9 +66,16 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
       const float y = __shfl_up(x, off);
       if (tid >= off) x += y;
     }
+    const float bt = tid < nrow ? a.beta[ti] : 0.f;
+    const float gC = __shfl(x, C - 1);
     sGam[tid] = x;
-    sBeta[tid] = tid < nrow ? a.beta[ti] : 0.f;
-    a.gam[((size_t)bh * N + ci) * C + tid] = x;
+    sBeta[tid] = bt;
+    float* cf = a.gam + ((size_t)bh * N + ci) * 5 * C + tid;
+    cf[0] = x;                      // gamma_j
+    cf[C] = bt * __expf(x);         // beta_j e^{gamma_j}
+    cf[2 * C] = bt;                 // beta_j
+    cf[3 * C] = __expf(gC - x);     // e^{gamma_C - gamma_j}
+    cf[4 * C] = __expf(gC);         // e^{gamma_C}
   }
   __syncthreads();
 
@@ -149,7 +158,7 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
   __shared__ __align__(16) T sK[2][C * LDQ];
   __shared__ __align__(16) T sT[2][C * LDT];
   __shared__ __align__(16) T sV[2][C * LDV];
-  __shared__ __align__(16) float sGam[2][C], sBeta[2][C];
+  __shared__ __align__(16) float sCf[2][4][C];  // beta e^gamma, beta, e^{gamma_C - gamma}, e^{gamma_C}
   __shared__ __align__(16) f32x4 sX[NH > 1 ? NW * 4 * 64 : 1];  // partial P of every wave
 
   const int nvt = a.dv / BVS;
@@ -178,19 +187,25 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
       S[tc] = zero4();
   }
 
-  RowTile<T, DK, NT> rk;
-  RowTile<T, C, NT> rt;
-  RowTile<T, BVS, NT> rv;
-  RowScalar rg, rb;
-  auto prefetch = [&](int ci) {
+  // two register sets of prefetched chunk data: chunk ci is loaded two
+  // iterations ahead into set ci & 1 (the loop is unrolled by two so the sets
+  // stay in registers)
+  struct Stage {
+    RowTile<T, DK, NT> rk;
+    RowTile<T, C, NT> rt;
+    RowTile<T, BVS, NT> rv;
+    RowScalar cf[4];
+  };
+  Stage st[2];
+  auto prefetch = [&](Stage& sg, int ci) {
     const int r0 = ci * C;
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-    rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
-    rt.load(Tg + ((size_t)bh * N + ci) * C * C, (size_t)C, C);
-    rv.load(vin + tok_off(b, r0, h, a.T, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
+    sg.rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+    sg.rt.load(Tg + ((size_t)bh * N + ci) * C * C, (size_t)C, C);
+    sg.rv.load(vin + tok_off(b, r0, h, a.T, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
     if (tid < C) {
-      rg.load(a.gam + ((size_t)bh * N + ci) * C, 1, tid, C);
-      rb.load(a.beta + ((size_t)b * a.T + r0) * a.H + h, (size_t)a.H, tid, nrow);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) sg.cf[q].load(a.gam + (((size_t)bh * N + ci) * 5 + 1 + q) * C, 1, tid, C);
     }
   };
 
@@ -213,20 +228,19 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
       store_frag(u_out + 16 * 32, uf[1]);
     }
   };
-  if (N > 0) prefetch(0);
 
-  for (int ci = 0; ci < N; ++ci) {
+  auto step = [&](Stage& sg, int ci) {
     const int buf = ci & 1;
-    // the other buffer was released by every wave at the previous barrier
-    rk.store(sK[buf], LDQ);
-    rt.store(sT[buf], LDT);
-    rv.store(sV[buf], LDV);
+    // the LDS buffer was released by every wave at the previous barrier
+    sg.rk.store(sK[buf], LDQ);
+    sg.rt.store(sT[buf], LDT);
+    sg.rv.store(sV[buf], LDV);
     if (tid < C) {
-      sGam[buf][tid] = rg.get();
-      sBeta[buf][tid] = rb.get();
+#pragma unroll
+      for (int q = 0; q < 4; ++q) sCf[buf][q][tid] = sg.cf[q].get();
     }
     if (ci > 0) write_back(ci - 1);
-    if (ci + 1 < N) prefetch(ci + 1);
+    if (ci + 2 < N) prefetch(sg, ci + 2);
     __syncthreads();
     const T* Kb = sK[buf];
 
@@ -262,25 +276,17 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
         R[J] = sum;
       }
     }
-    // R = beta (V - e^gamma P); V rows 32 m + 4 g4 + r and 32 m + 16 + 4 g4 + r
+    // R = beta V - beta e^gamma P; V rows 32 m + 4 g4 + r and 32 m + 16 + 4 g4 + r
 #pragma unroll
     for (int m = 0; m < 2; ++m) {
       const Frag<T> vf = ld_frag_tr_acc(sV[buf] + 32 * m * LDV + 16 * pr, LDV);
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
         const int J = 2 * m + hh;
-        const f32x4 gj = *reinterpret_cast<const f32x4*>(&sGam[buf][16 * J + 4 * g4]);
-        const f32x4 bj = *reinterpret_cast<const f32x4*>(&sBeta[buf][16 * J + 4 * g4]);
+        const f32x4 bg = *reinterpret_cast<const f32x4*>(&sCf[buf][0][16 * J + 4 * g4]);
+        const f32x4 bj = *reinterpret_cast<const f32x4*>(&sCf[buf][1][16 * J + 4 * g4]);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float vv;
-          if constexpr (sizeof(T) == 2) {
-            vv = f32(vf.v[4 * hh + r]);
-          } else {
-            vv = hh ? vf.hi[r] : vf.lo[r];
-          }
-          R[J][r] = bj[r] * (vv - __expf(gj[r]) * R[J][r]);
-        }
+        for (int r = 0; r < 4; ++r) R[J][r] = bj[r] * frag_elem(vf, 4 * hh + r) - bg[r] * R[J][r];
       }
     }
     // U = Tm R (Tm rows are stored in acc_pos order)
@@ -296,16 +302,11 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
     // U^T (kept for the write-back), then U e^{gamma_C - gamma_i}
     uf[0] = acc_pair_frag<T>(U[0], U[1]);
     uf[1] = acc_pair_frag<T>(U[2], U[3]);
-    const float gC = sGam[buf][C - 1];
 #pragma unroll
-    for (int I = 0; I < 4; ++I) {
-      const f32x4 gi = *reinterpret_cast<const f32x4*>(&sGam[buf][16 * I + 4 * g4]);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) U[I][r] *= __expf(gC - gi[r]);
-    }
+    for (int I = 0; I < 4; ++I) U[I] *= *reinterpret_cast<const f32x4*>(&sCf[buf][2][16 * I + 4 * g4]);
     const Frag<T> ud0 = acc_pair_frag<T>(U[0], U[1]);
     const Frag<T> ud1 = acc_pair_frag<T>(U[2], U[3]);
-    const float eC = __expf(gC);
+    const float eC = sCf[buf][3][0];
     constexpr int TB = NCT < 4 ? NCT : 4;  // key-feature tiles per batch of transposing reads
     Frag<T> tf[2][TB][2];
 #pragma unroll
@@ -331,6 +332,13 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
         mma(S[tc], tf[tb & 1][t][1], ud1);
       }
     }
+  };
+
+  if (N > 0) prefetch(st[0], 0);
+  if (N > 1) prefetch(st[1], 1);
+  for (int ci = 0; ci < N; ci += 2) {
+    step(st[0], ci);
+    if (ci + 1 < N) step(st[1], ci + 1);
   }
 
   if (N > 0) write_back(N - 1);
@@ -389,7 +397,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
     RowTile<T, DK, kOutThreads> rq, rk;
     rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
     rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-    if (tid < C) sGam[tid] = a.gam[((size_t)bh * N + ci) * C + tid];
+    if (tid < C) sGam[tid] = a.gam[((size_t)bh * N + ci) * 5 * C + tid];
     rq.store(sQ, LDQ);
     rk.store(sK, LDQ);
   }

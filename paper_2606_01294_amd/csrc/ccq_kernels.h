@@ -66,13 +66,15 @@ struct GlaOutArgs {
 };
 
 // Gated DeltaNet chunk transform (chunk-parallel): Tm = (I + A)^{-1} and the
-// within-chunk cumulative log decays gamma.
+// chunk's decay coefficients.
 struct TriArgs {
   const void* k;         // [B,T,H,dk] io
   const float* logalpha; // [B,T,H]
   const float* beta;     // [B,T,H]
   void* Tm;              // [B*H, N, C, C] io (workspace), columns in acc_pos order
-  float* gam;            // [B*H, N, C] fp32 (workspace)
+  float* gam;            // [B*H, N, 5, C] fp32 (workspace): gamma_j (cumulative log
+                         // decay in the chunk), beta_j e^{gamma_j}, beta_j,
+                         // e^{gamma_C - gamma_j}, e^{gamma_C}
   int B, T, H, dk, dv;
 };
 
