@@ -92,8 +92,8 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
 
 
 CLEAN = ["clean_gram", "clean_prefix"]
-KERNELS = {0: CLEAN + ["clean_out", "gla_state", "gla_out"],
-           1: CLEAN + ["clean_out", "gdn_tri", "gdn_state", "gdn_out"],
+KERNELS = {0: ["gla_state"] + CLEAN + ["clean_out", "gla_out"],
+           1: ["gdn_tri", "gdn_state"] + CLEAN + ["clean_out", "gdn_out"],
            "train": CLEAN + ["clean_out_train", "gla_state", "gla_out", "gla_dstate",
                              "gla_bwd_chunk", "gla_dg", "clean_dq", "ccq_dk"]}
 KERNEL_SYMBOL = {"clean_gram": "clean_gram_kernel",
