@@ -30,7 +30,15 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3
 CHUNK = 64
-CLEAN_SEG = 8     # chunks per segment of the query contraction (kCleanSeg)
+
+
+def clean_seg(bh: int, nc: int) -> int:
+    """Chunks per segment of the query contraction (the library's policy: the
+    longest of 8, 4, 2 that still gives every compute unit a workgroup)."""
+    seg = 8
+    while seg > 2 and bh * (-(-nc // seg)) < 256:
+        seg //= 2
+    return seg
 
 
 def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
@@ -40,7 +48,7 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     BH, ntok = w.B * w.H, w.B * w.T * w.H
     dk, dv, C = w.dk, w.dv, CHUNK
     NC = -(-w.T // C)
-    NS = -(-NC // CLEAN_SEG)
+    NS = -(-NC // clean_seg(BH, NC))
     stats = BH * NS * dk * dk               # elements of the segment statistics
     if kernel == "clean_gram":      # k in; segment Gram (fp32), chunk and segment key sums out
         by = ntok * dk * io_bytes + stats * 4 + BH * (NC + NS) * dk * 4

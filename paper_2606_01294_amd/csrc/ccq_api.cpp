@@ -110,7 +110,8 @@ struct CleanWs {
 template <typename Take>
 CleanWs take_clean_ws(const ccq_shape* s, Take&& take) {
   const size_t bh = (size_t)s->B * s->H, dk = s->dk;
-  const size_t nc = (s->T + 63) / 64, ns = (nc + ccq::kCleanSeg - 1) / ccq::kCleanSeg;
+  const size_t nc = (s->T + 63) / 64, seg = ccq::clean_seg((long long)bh, (long long)nc);
+  const size_t ns = (nc + seg - 1) / seg;
   CleanWs c;
   c.gram = take(bh * ns * dk * dk * 4);
   c.sprime = take(bh * ns * dk * dk * esize(s->io_dtype));
@@ -130,7 +131,7 @@ ccq::CleanArgs clean_args(const ccq_shape* s, char* ws, const CleanWs& c) {
   a.H = s->H;
   a.dk = s->dk;
   a.centered = s->centered;
-  a.seg = ccq::kCleanSeg;
+  a.seg = ccq::clean_seg((long long)s->B * s->H, (s->T + 63) / 64);
   a.t0 = s->t0;
   return a;
 }

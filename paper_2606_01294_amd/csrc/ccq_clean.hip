@@ -22,8 +22,9 @@
 // Three kernels:
 //   clean_gram    raw sums of k k^T per segment, and of k per chunk and segment
 //   clean_prefix  S'_s by a prefix over segments (fp32), stored in io dtype
-//   clean_out     one workgroup per chunk pair: S'_s q plus the causal product
-//                 over the segment's centred keys, all in MFMA tiles
+//   clean_out     one workgroup per segment: walks its chunks in order with
+//                 S'_r (S'_s plus the centred keys of the segment's earlier
+//                 chunks) held in MFMA accumulators
 // Without centring (Sigma = Cbar) the same kernels run with c_s = 0 and no
 // mean terms.
 #include "ccq_device.h"
@@ -50,8 +51,7 @@ __device__ __forceinline__ f32x4 load4f(const T* p) {
 // Raw segment Gram matrix G_s = sum_{j in s} k_j k_j^T, one workgroup per
 // (head, segment); wave w owns rows [w RW, (w+1) RW) and all columns, so each
 // chunk of keys is read from memory once.  The chunk and segment key sums come
-// from the same products (a ones column).  G is symmetric: each tile is
-// written transposed, as rows of four consecutive features (16-byte stores).
+// from the same products (a ones column).
 template <typename T, int DK>
 __global__ __launch_bounds__(64 * (DK >= 128 ? 8 : 4), 1) void clean_gram_kernel(const CleanArgs a) {
   constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P;
@@ -122,43 +122,46 @@ __global__ __launch_bounds__(64 * (DK >= 128 ? 8 : 4), 1) void clean_gram_kernel
     for (int v = 0; v < RT; ++v)
       *reinterpret_cast<f32x4*>(a.ssum + ((size_t)bh * NS + s) * DK + a0 + 16 * v + 4 * g4) = stot[v];
   }
-  // acc[v][t][r] = G[a0 + 16 v + 4 g4 + r][16 t + c16], stored at the mirror position
+  // acc[v][t] is accumulator tile (rows m = a0 + 16 v .., columns n = 16 t ..),
+  // stored fragment-native: 1 KB per tile, lane-contiguous
   float* G = a.gram + ((size_t)bh * NS + s) * DK * DK;
 #pragma unroll
   for (int v = 0; v < RT; ++v)
 #pragma unroll
     for (int t = 0; t < CT; ++t)
-      *reinterpret_cast<f32x4*>(G + (size_t)(16 * t + c16) * DK + a0 + 16 * v + 4 * g4) = acc[v][t];
+      *reinterpret_cast<f32x4*>(G + ((size_t)(t * CT + a0 / 16 + v) * 64 + l) * 4) = acc[v][t];
 }
 
 // S'_s = S_s - M'_s c_s^T - c_s M'_s^T - n_s c_s c_s^T with S_s the raw second
 // moment before segment s (prefix of the Gram matrices, fp32), c_s the mean
 // key of segment s, n_s the tokens before it and M'_s = M_s - n_s c_s the key
-// sum before it about c_s (running sums of the segment key sums, kept for this
-// thread's row and four columns); four elements per thread.  S'_s is stored in
-// 64-column slices, each a contiguous [dk][64] block.  Also the final Cbar_T
-// and mu_T.
+// sum before it about c_s (running sums of the segment key sums).  Each thread
+// owns four consecutive fragment-native elements, (m .. m + 3, n): one scalar
+// index n and a vector of four m.  Also the final Cbar_T and mu_T.
 template <typename T, int DK>
 __global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
   constexpr int PER = DK * DK / 4 / 256;  // workgroups per head
+  constexpr int NMT = DK / 16;
   const int bh = blockIdx.x / PER;
-  const int e = ((blockIdx.x % PER) * 256 + threadIdx.x) * 4;
-  const int ra = e / DK, cb = e % DK;
-  const int NC = n_chunks(a.T), NS = n_segs(a.T, a.seg);
+  const int g = (blockIdx.x % PER) * 256 + threadIdx.x;  // element offset / 4
+  const int l = g & 63, tile = g >> 6;
+  const int n = 16 * (tile / NMT) + (l & 15);
+  const int m = 16 * (tile % NMT) + 4 * (l >> 4);
+  const int NS = n_segs(a.T, a.seg), NC = n_chunks(a.T);
   const float t0f = (float)a.t0;
   f32x4 acc = zero4();
-  if (a.C0) acc = *reinterpret_cast<const f32x4*>(a.C0 + ((size_t)bh * DK + ra) * DK + cb) * t0f;
-  float run_a = a.mu0 ? t0f * a.mu0[(size_t)bh * DK + ra] : 0.f;  // raw key sums before s
-  f32x4 run_b = a.mu0 ? *reinterpret_cast<const f32x4*>(a.mu0 + (size_t)bh * DK + cb) * t0f : zero4();
+  if (a.C0) acc = *reinterpret_cast<const f32x4*>(a.C0 + ((size_t)bh * DK + n) * DK + m) * t0f;
+  float run_a = a.mu0 ? t0f * a.mu0[(size_t)bh * DK + n] : 0.f;  // raw key sums before s
+  f32x4 run_b = a.mu0 ? *reinterpret_cast<const f32x4*>(a.mu0 + (size_t)bh * DK + m) * t0f : zero4();
   T* Sp = static_cast<T*>(a.sprime);
   for (int s = 0; s < NS; ++s) {
     const size_t so = (size_t)bh * NS + s;
     const int cbeg = s * a.seg, cend = min(NC, cbeg + a.seg);
     const float len = (float)(min(a.T, cend * kChunk) - cbeg * kChunk);
     const float ns = t0f + (float)((int64_t)cbeg * kChunk);
-    const float tot_a = a.ssum[so * DK + ra];
-    const f32x4 tot_b = *reinterpret_cast<const f32x4*>(a.ssum + so * DK + cb);
-    const f32x4 g = *reinterpret_cast<const f32x4*>(a.gram + (so * DK + ra) * DK + cb);
+    const float tot_a = a.ssum[so * DK + n];
+    const f32x4 tot_b = *reinterpret_cast<const f32x4*>(a.ssum + so * DK + m);
+    const f32x4 gm = *reinterpret_cast<const f32x4*>(a.gram + so * DK * DK + 4 * (size_t)g);
     const float ca = a.centered ? tot_a / len : 0.f;
     const f32x4 cb4 = a.centered ? tot_b / len : zero4();
     const float ma = run_a - ns * ca;
@@ -166,260 +169,324 @@ __global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
     f32x4 o;
 #pragma unroll
     for (int q = 0; q < 4; ++q) o[q] = acc[q] - ma * cb4[q] - ca * mb4[q] - ns * ca * cb4[q];
-    store4(Sp + so * DK * DK + ((size_t)(cb >> 6) * DK + ra) * 64 + (cb & 63), o[0], o[1], o[2], o[3]);
-    acc += g;
+    store4(Sp + so * DK * DK + 4 * (size_t)g, o[0], o[1], o[2], o[3]);
+    acc += gm;
     run_a += tot_a;
     run_b += tot_b;
   }
   const float inv = 1.f / (t0f + (float)a.T);
-  if (a.CT) *reinterpret_cast<f32x4*>(a.CT + ((size_t)bh * DK + ra) * DK + cb) = acc * inv;
-  if (a.muT && ra == 0) *reinterpret_cast<f32x4*>(a.muT + (size_t)bh * DK + cb) = run_b * inv;
+  if (a.CT) *reinterpret_cast<f32x4*>(a.CT + ((size_t)bh * DK + n) * DK + m) = acc * inv;
+  if (a.muT && n == 0) *reinterpret_cast<f32x4*>(a.muT + (size_t)bh * DK + m) = run_b * inv;
 }
 
-// One workgroup per CPW consecutive chunks of a segment; wave w owns rows
-// i = 16 (w % 4) .. + 15 of chunk w / 4.  All products are kept transposed
-// (output feature n in the accumulator row, token i in its column) so that
-// score tiles feed the next product from registers:
-//   acc^T  = S'_s x^T               (S' staged through LDS one 64-column slice
-//                                     at a time, double-buffered)
-//   sc^T   = K'_blk x^T,  acc^T += K'_blk^T sc^T        (each block of the segment)
-// The slice buffers are reused for the key blocks, and both are shared by the
-// CPW chunks, which halves (CPW = 2) the global round trips per chunk.
-// On the diagonal block the scores are masked to j <= i and shifted by
-// -cq'_i / t_i, which folds the within-chunk part of m'_i into the product.
-template <typename T, int DK, int CPW>
-__global__ __launch_bounds__(kThreads * CPW, 1) void clean_out_kernel(const CleanArgs a) {
-  constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P, LDP = 64 + P;
-  constexpr int NT = kThreads * CPW;
-  constexpr int NK = DK / 32, NN = DK / 16, NP = DK / 64;
-  constexpr int BUF = (DK * LDP > C * LDK) ? DK * LDP : C * LDK;  // elements per buffer
-  constexpr int NVS = DK * 64 / 8 / NT;                            // slice vectors per thread
-  static_assert(NVS >= 1 && DK * 64 % (8 * NT) == 0, "slice split");
-  typedef typename RowTile<T, DK, NT>::vec_t vec_t;
-  __shared__ __align__(16) T sbuf[2 * BUF];
-  __shared__ __align__(16) float sC[DK], sMs[DK], sMr[CPW][DK];
+// Causal score tile t of a 64-token chunk (t < 10): key tile J <= token tile I.
+__device__ __forceinline__ int causal_tile_i(int t) { return t >= 6 ? 3 : t >= 3 ? 2 : t >= 1 ? 1 : 0; }
+
+// One workgroup per (head, segment) walks the segment's chunks in order with
+// S'_r, the second moment about c_s of every key before chunk r, held in MFMA
+// accumulators: wave w owns columns n in [w NCW, (w + 1) NCW) of S' and all
+// of its rows.  Per chunk r (x: the chunk's rows of q, K': its keys minus c_s):
+//   out^T  = S'_r x^T                  (S' enters as bf16 operands from registers)
+//   sc     = K' x^T, masked to j <= i and shifted by -cq'_i / t_i
+//   out^T += K'^T sc
+//   S'_{r+1} = S'_r + K'^T K'
+// The shift folds the within-chunk part of the mean term into the product;
+// cq'_i = m'_i . x_i comes from the score row sums and M'_r . x_i.  x and K'
+// are staged in LDS once per chunk; q_clean is formed in place over x and is
+// copied out with row-contiguous stores while the next chunk is staged.
+template <typename T, int DK, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a) {
+  constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P, LDP = C + P, LDQ = C + 4;
+  constexpr int NT = 64 * NW, VPR = DK / 8;
+  constexpr int NCW = DK / NW, NNT = NCW / 16, NMT = DK / 16, NK = DK / 32;
+  constexpr int TPI = NT / C, JPT = C / TPI, FPT = DK / TPI;  // per-token split of the row sums
+  constexpr int NV = C * VPR / NT;                            // staged vectors per thread
+  static_assert(NCW % 16 == 0 && NNT >= 1, "column split");
+  static_assert(NT >= DK && JPT % 8 == 0 && FPT % 8 == 0 && C * VPR % NT == 0, "thread split");
+  typedef RowTile<T, DK, NT> Tile;
+  typedef typename Tile::vec_t vec_t;
+  // bf16 chunks are prefetched straight into LDS (x then k, unpadded); fp32
+  // ones, whose staging area would not fit beside the rest, into registers.
+  // One LDS block, hot arrays first so that their offsets fit in the
+  // instructions' immediate field.
+  constexpr bool kDma = sizeof(T) == 2;
+  constexpr int oX = 0, oK = oX + C * LDK * (int)sizeof(T), oS = oK + C * LDK * (int)sizeof(T);
+  constexpr int oP = oS + C * LDQ * 4, oC = oP + C * LDP * (int)sizeof(T), oM = oC + DK * 4;
+  constexpr int oCq = oM + DK * 4, oLam = oCq + C * 4, oSt = oLam + C * 4;
+  constexpr int oEnd = oSt + (kDma ? 2 * C * DK * (int)sizeof(T) : 16);
+  __shared__ __align__(16) char smem[oEnd];
+  T* const sX = reinterpret_cast<T*>(smem + oX);         // x rows, then q_clean rows
+  T* const sK = reinterpret_cast<T*>(smem + oK);         // centred keys
+  float* const sS = reinterpret_cast<float*>(smem + oS); // raw scores, [i][j]
+  T* const sP = reinterpret_cast<T*>(smem + oP);         // masked, shifted scores, [i][j]
+  float* const sC = reinterpret_cast<float*>(smem + oC);
+  float* const sM = reinterpret_cast<float*>(smem + oM);
+  float* const sCq = reinterpret_cast<float*>(smem + oCq);
+  float* const sLam = reinterpret_cast<float*>(smem + oLam);
+  T* const sSt = reinterpret_cast<T*>(smem + oSt);
 
   const int NC = n_chunks(a.T), NS = n_segs(a.T, a.seg);
-  const int NG = (NC + CPW - 1) / CPW;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int bh = lb / NG, ch0 = (lb % NG) * CPW;
-  const int chl = min(NC - 1, ch0 + CPW - 1);  // last chunk of the group
+  const int bh = lb / NS, s = lb % NS;
   const int b = bh / a.H, h = bh % a.H;
-  const int s = ch0 / a.seg, cbeg = s * a.seg;
-  const int tid = threadIdx.x, w = wave_id(), l = lane_id(), g4 = l >> 4, c16 = l & 15;
-  const int wr = w & 3, ch = ch0 + (w >> 2);
-  const bool has = ch < NC;  // this wave's chunk exists
-  const int r0 = ch * C, nrow = has ? min(C, a.T - r0) : 0;
+  const int cbeg = s * a.seg, cend = min(NC, cbeg + a.seg);
+  const int tid = threadIdx.x;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n0 = w * NCW;
   const T* x = static_cast<const T*>(a.q);
   const T* k = static_cast<const T*>(a.k);
+  T* qc = static_cast<T*>(a.qclean);
   const size_t gstride = (size_t)a.H * DK;
   const float t0f = (float)a.t0;
   const size_t so = (size_t)bh * NS + s;
 
-  // this wave's rows of x as B fragments (column = token); rows past the end
-  // repeat the last row and are never written back
-  const int i = 16 * wr + c16;
-  const bool iok = i < nrow;
-  Frag<T> qf[NK];
-  {
-    const int row = has ? r0 + (iok ? i : nrow - 1) : 0;
-    const T* xr = x + tok_off(b, row, h, a.T, a.H, DK) + 8 * g4;
-#pragma unroll
-    for (int kk = 0; kk < NK; ++kk) {
-      if constexpr (sizeof(T) == 2) {
-        qf[kk].v = *reinterpret_cast<const bf16x8*>(xr + 32 * kk);
-      } else {
-        qf[kk].lo = *reinterpret_cast<const f32x4*>(xr + 32 * kk);
-        qf[kk].hi = *reinterpret_cast<const f32x4*>(xr + 32 * kk + 4);
-      }
+  Tile rx, rk;
+  RowScalar rl;
+  auto prefetch = [&](int c) {
+    const int r0 = c * C, n = min(C, a.T - r0);
+    if constexpr (kDma) {
+      LdsStream<DK, NW>::load(x + tok_off(b, r0, h, a.T, a.H, DK), gstride, n, sSt);
+      LdsStream<DK, NW>::load(k + tok_off(b, r0, h, a.T, a.H, DK), gstride, n, sSt + C * DK);
+    } else {
+      rx.load(x + tok_off(b, r0, h, a.T, a.H, DK), gstride, n);
+      rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), gstride, n);
     }
-  }
-  RowTile<T, DK, NT> rk;
-  auto load_block = [&](int c) {
-    rk.load(k + tok_off(b, c * C, h, a.T, a.H, DK), gstride, min(C, a.T - c * C));
+    if (tid < C) rl.load(a.lam + ((size_t)b * a.T + r0) * a.H + h, (size_t)a.H, tid, n);
   };
-  load_block(cbeg);
-  // key statistics of the segment, one thread per feature: the centre c_s, the
-  // key sum before the segment about c_s (M'_s) and before each of this
-  // group's chunks (M'_r), from the segment and chunk key sums
-  for (int d = tid; d < DK; d += NT) {
-    const float* ss = a.ssum + (size_t)bh * NS * DK + d;
-    float run = a.mu0 ? t0f * a.mu0[(size_t)bh * DK + d] : 0.f;
+  prefetch(cbeg);
+
+  // segment centre c_s and key sum before the segment about it, M'_s; one
+  // thread per feature
+  float cen = 0.f;
+  if (tid < DK) {
+    const float* ss = a.ssum + (size_t)bh * NS * DK + tid;
+    float run = a.mu0 ? t0f * a.mu0[(size_t)bh * DK + tid] : 0.f;
 #pragma unroll 8
     for (int p = 0; p < s; ++p) run += ss[(size_t)p * DK];
-    const int cend = min(NC, cbeg + a.seg);
     const float len = (float)(min(a.T, cend * C) - cbeg * C);
-    const float cen = a.centered ? ss[(size_t)s * DK] / len : 0.f;
-    float mp = run - (t0f + (float)(cbeg * C)) * cen;
-    sC[d] = cen;
-    sMs[d] = mp;
-    const float* cs = a.csum + (size_t)bh * NC * DK + d;
-    for (int c = cbeg; c <= chl; ++c) {
-      if (c >= ch0) sMr[c - ch0][d] = mp;
-      mp += cs[(size_t)c * DK] - (float)min(C, a.T - c * C) * cen;
-    }
+    cen = a.centered ? ss[(size_t)s * DK] / len : 0.f;
+    sC[tid] = cen;
+    sM[tid] = run - (t0f + (float)((int64_t)cbeg * C)) * cen;
   }
-
-  // entry term S'_s x_i, one 64-column slice of S' per step
-  f32x4 acc[NN];
-#pragma unroll
-  for (int tn = 0; tn < NN; ++tn) acc[tn] = zero4();
+  // entry moment S'_s: S[nt][mt] is tile (n0 / 16 + nt, mt) of the
+  // fragment-native layout (rows m = 16 mt + 4 (l / 16) + r, column n0 + 16 nt + l % 16)
+  f32x4 S[NNT][NMT];
   {
-    // all slices are requested up front when they fit in registers (the whole
-    // of S' is DK * DK / 8 / NT vectors per thread), else one slice ahead
-    constexpr bool kAll = NVS * NP <= 16;
-    constexpr int NB = kAll ? NP : 2;
-    const T* sp = static_cast<const T*>(a.sprime) + so * DK * DK;
-    vec_t ps[NB][NVS];
-    auto load_slice = [&](int p) {
+    const T* sp = static_cast<const T*>(a.sprime) + so * DK * DK + ((size_t)(n0 / 16) * NMT * 64 + (tid & 63)) * 4;
 #pragma unroll
-      for (int u = 0; u < NVS; ++u)
-        ps[kAll ? p : (p & 1)][u] =
-            *reinterpret_cast<const vec_t*>(sp + (size_t)p * DK * 64 + (size_t)(tid + NT * u) * 8);
-    };
-    if constexpr (kAll) {
+    for (int nt = 0; nt < NNT; ++nt)
 #pragma unroll
-      for (int p = 0; p < NP; ++p) load_slice(p);
-    } else {
-      load_slice(0);
-    }
+      for (int mt = 0; mt < NMT; ++mt) S[nt][mt] = load4f(sp + ((size_t)nt * NMT + mt) * 256);
+  }
+  if constexpr (kDma) wait_vm_all();
+  __syncthreads();  // sC, first chunk
+
+  float csum = 0.f;  // key sum of the current chunk, feature tid
+  for (int c = cbeg; c < cend; ++c) {
+    const int r0 = c * C, nrow = min(C, a.T - r0);
+    // stage chunk c; each thread first copies out the q_clean of chunk c - 1
+    // (always a full chunk) held at the same places
+    {
+      const int t_ = opaque(tid);
 #pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      T* pb = sbuf + (p & 1) * BUF;
+      for (int u = 0; u < NV; ++u) {
+        const int e = t_ + NT * u, row = e / VPR, col = (e % VPR) * 8;
+        T* px = sX + row * LDK + col;
+        if (c > cbeg)
+          *reinterpret_cast<vec_t*>(qc + tok_off(b, r0 - C + row, h, a.T, a.H, DK) + col) =
+              *reinterpret_cast<const vec_t*>(px);
+        vec_t xv, kv, y;
+        if constexpr (kDma) {
+          xv = *reinterpret_cast<const vec_t*>(sSt + 8 * e);
+          kv = *reinterpret_cast<const vec_t*>(sSt + C * DK + 8 * e);
+        } else {
+          xv = rx.get(u);
+          kv = rk.get(u);
+        }
 #pragma unroll
-      for (int u = 0; u < NVS; ++u) {
-        const int e = tid + NT * u;
-        *reinterpret_cast<vec_t*>(pb + (e >> 3) * LDP + 8 * (e & 7)) = ps[kAll ? p : (p & 1)][u];
+        for (int q = 0; q < 8; ++q) {
+          xv[q] = row < nrow ? xv[q] : to<T>(0.f);
+          y[q] = to<T>(row < nrow ? f32(kv[q]) - sC[col + q] : 0.f);
+        }
+        *reinterpret_cast<vec_t*>(px) = xv;
+        *reinterpret_cast<vec_t*>(sK + row * LDK + col) = y;
       }
-      if (!kAll && p + 1 < NP) load_slice(p + 1);
-      __syncthreads();  // (also publishes sC, sMs, sMr)
-      if (has) {
+    }
+    if (tid < C) sLam[tid] = rl.get();
+    if (tid < DK) {
+      if (c > cbeg) sM[tid] += csum - (float)C * cen;  // M'_c
+      csum = a.csum[((size_t)bh * NC + c) * DK + tid];
+    }
+    __syncthreads();  // (1) x, K', M'_c staged; the staging area is free
+    if (c + 1 < cend) prefetch(c + 1);
+
+    // raw scores of the causal tiles this wave owns, to sS[i][j]; then
+    // out^T = S'_r x^T: acc[nt][I] holds features n0 + 16 nt + 4 (l / 16) + r
+    // of token 16 I + l % 16
+    f32x4 acc[NNT][4];
+    {
+      const int l_ = opaque(tid & 63), g_ = l_ >> 4, c_ = l_ & 15;
+      const T* pxa = sX + c_ * LDK + 4 * g_;
+      const T* pka = sK + c_ * LDK + 4 * g_;
+      for (int t = w; t < 10; t += NW) {
+        const int I = causal_tile_i(t), J = t - I * (I + 1) / 2;
+        f32x4 sc = zero4();
 #pragma unroll
-        for (int tn = 0; tn < NN; ++tn) {
-          mma(acc[tn], ld_frag(pb + 16 * tn * LDP, LDP), qf[2 * p]);
-          mma(acc[tn], ld_frag(pb + 16 * tn * LDP + 32, LDP), qf[2 * p + 1]);
+        for (int p = 0; p < NK; ++p)
+          mma(sc, frag_acc_at(pka + 16 * J * LDK + 32 * p), frag_acc_at(pxa + 16 * I * LDK + 32 * p));
+        *reinterpret_cast<f32x4*>(sS + (16 * I + c_) * LDQ + 16 * J + 4 * g_) = sc;
+      }
+#pragma unroll
+      for (int nt = 0; nt < NNT; ++nt)
+#pragma unroll
+        for (int I = 0; I < 4; ++I) acc[nt][I] = zero4();
+#pragma unroll
+      for (int p = 0; p < NK; ++p) {
+        Frag<T> xf[4], af[NNT];
+#pragma unroll
+        for (int I = 0; I < 4; ++I) xf[I] = frag_acc_at(pxa + 16 * I * LDK + 32 * p);
+#pragma unroll
+        for (int nt = 0; nt < NNT; ++nt) af[nt] = acc_pair_frag<T>(S[nt][2 * p], S[nt][2 * p + 1]);
+#pragma unroll
+        for (int I = 0; I < 4; ++I)
+#pragma unroll
+          for (int nt = 0; nt < NNT; ++nt) mma(acc[nt][I], af[nt], xf[I]);
+      }
+    }
+    __syncthreads();  // (2) scores complete
+
+    // cq'_i = M'_r . x_i + sum_{j <= i} sc_ij, and the shifted scores; TPI
+    // consecutive threads per token
+    {
+      const int t_ = opaque(tid);
+      const int i = t_ / TPI, pp = t_ % TPI;
+      const float ti = t0f + (float)(r0 + i + 1);
+      float sv[JPT];
+      float rs = 0.f, mq = 0.f, cx = 0.f;
+      const float* srow = sS + i * LDQ + JPT * pp;
+#pragma unroll
+      for (int e = 0; e < JPT; e += 4) {
+        const f32x4 v4 = *reinterpret_cast<const f32x4*>(srow + e);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          sv[e + q] = JPT * pp + e + q <= i ? v4[q] : 0.f;
+          rs += sv[e + q];
         }
       }
-    }
-  }
-
-  // M'_s . x_i and c_s . x_i (each lane holds 8 features per k step)
-  float mq = 0.f, cx = 0.f;
+      const T* xrow = sX + i * LDK + FPT * pp;
+      const float* mrow = sM + FPT * pp;
+      const float* crow = sC + FPT * pp;
 #pragma unroll
-  for (int kk = 0; kk < NK; ++kk)
+      for (int e = 0; e < FPT; e += 8) {
+        const vec_t xv = *reinterpret_cast<const vec_t*>(xrow + e);
+        const f32x4 m0 = *reinterpret_cast<const f32x4*>(mrow + e), m1 = *reinterpret_cast<const f32x4*>(mrow + e + 4);
+        const f32x4 c0 = *reinterpret_cast<const f32x4*>(crow + e), c1 = *reinterpret_cast<const f32x4*>(crow + e + 4);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int d = 32 * kk + 8 * g4 + e;
-      const float xv = frag_elem(qf[kk], e);
-      mq += xv * sMs[d];
-      cx += xv * sC[d];
-    }
-  mq += __shfl_xor(mq, 16);
-  mq += __shfl_xor(mq, 32);
-  cx += __shfl_xor(cx, 16);
-  cx += __shfl_xor(cx, 32);
-
-  const float ti = t0f + (float)(r0 + i + 1);
-  float rs = 0.f, cqp = 0.f;
-  for (int jb = cbeg; jb <= chl; ++jb) {
-    T* buf = sbuf + ((NP + jb - cbeg) & 1) * BUF;
-    // centred keys of block jb; the other buffer may still be read by a wave
-    // working on the step before, this one was released by the last barrier
+        for (int q = 0; q < 4; ++q) {
+          mq += f32(xv[q]) * m0[q] + f32(xv[q + 4]) * m1[q];
+          cx += f32(xv[q]) * c0[q] + f32(xv[q + 4]) * c1[q];
+        }
+      }
+      rs = group_sum<TPI>(rs);
+      mq = group_sum<TPI>(mq);
+      cx = group_sum<TPI>(cx);
+      const float cqp = mq + rs;
+      const float sub = a.centered ? cqp / ti : 0.f;
+      T* prow = sP + i * LDP + JPT * pp;
 #pragma unroll
-    for (int u = 0; u < RowTile<T, DK, NT>::NV; ++u) {
-      const vec_t kv = rk.get(u);
-      const int col = RowTile<T, DK, NT>::col(u);
-      vec_t y;
+      for (int e = 0; e < JPT; e += 8) {
+        vec_t y;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) y[e] = to<T>(f32(kv[e]) - sC[col + e]);
-      *reinterpret_cast<vec_t*>(buf + RowTile<T, DK, NT>::row(u) * LDK + col) = y;
-    }
-    if (jb < chl) load_block(jb + 1);
-    __syncthreads();
-    if (!has || jb > ch) continue;  // wave-uniform: this chunk's window has ended
-
-    const bool diag = jb == ch;
-    f32x4 sc[4];
-#pragma unroll
-    for (int J = 0; J < 4; ++J) {
-      sc[J] = zero4();
-      if (!diag || J <= wr)
-#pragma unroll
-        for (int kk = 0; kk < NK; ++kk) mma(sc[J], ld_frag(buf + 16 * J * LDK + 32 * kk, LDK), qf[kk]);
-    }
-    if (diag) {
-#pragma unroll
-      for (int J = 0; J < 4; ++J)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (16 * J + 4 * g4 + r > i) sc[J][r] = 0.f;
-    }
-#pragma unroll
-    for (int J = 0; J < 4; ++J) rs += sc[J][0] + sc[J][1] + sc[J][2] + sc[J][3];
-    if (diag) {
-      rs += __shfl_xor(rs, 16);
-      rs += __shfl_xor(rs, 32);
-      cqp = mq + rs;  // m'_i . x_i
-      if (a.centered) {
-        const float sub = cqp / ti;
-#pragma unroll
-        for (int J = 0; J < 4; ++J)
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (16 * J + 4 * g4 + r <= i) sc[J][r] -= sub;
+        for (int q = 0; q < 8; ++q) y[q] = to<T>(JPT * pp + e + q <= i ? sv[e + q] - sub : 0.f);
+        *reinterpret_cast<vec_t*>(prow + e) = y;
+      }
+      if (pp == 0) {
+        sCq[i] = cqp;
+        if (a.mdot && i < nrow) a.mdot[((size_t)b * a.T + r0 + i) * a.H + h] = cqp + ti * cx;  // raw m . x
       }
     }
-    const Frag<T> f0 = acc_pair_frag<T>(sc[0], sc[1]);
-    const Frag<T> f1 = acc_pair_frag<T>(sc[2], sc[3]);
-    const bool upper = !diag || wr >= 2;  // keys 32..63 can precede row i
+    __syncthreads();  // (3) shifted scores complete
+
+    {
+      const int l_ = opaque(tid & 63), g_ = l_ >> 4, c_ = l_ & 15;
+      const T* ptr = sK + frag_tr_lane_off<T>(l_, LDK);
+      // K'^T fragments of this wave's columns (intra-chunk product and update)
+      Frag<T> kb[NNT][2];
 #pragma unroll
-    for (int tn = 0; tn < NN; ++tn) {
-      mma(acc[tn], ld_frag_tr_acc(buf + 16 * tn, LDK), f0);
-      if (upper) mma(acc[tn], ld_frag_tr_acc(buf + 32 * LDK + 16 * tn, LDK), f1);
+      for (int nt = 0; nt < NNT; ++nt)
+#pragma unroll
+        for (int q = 0; q < 2; ++q) kb[nt][q] = frag_tr_at(ptr + 32 * q * LDK + n0 + 16 * nt, LDK);
+      // out^T += K'^T sc (keys 32..63 only reach tokens 32..63)
+      const T* pp_ = sP + c_ * LDP + 8 * g_;
+#pragma unroll
+      for (int I = 0; I < 4; ++I)
+#pragma unroll
+        for (int q = 0; q < (I >= 2 ? 2 : 1); ++q) {
+          const Frag<T> pf = frag_at(pp_ + 16 * I * LDP + 32 * q);
+#pragma unroll
+          for (int nt = 0; nt < NNT; ++nt) mma(acc[nt][I], kb[nt][q], pf);
+        }
+
+      // q_clean = base - lam / t (out - cq' / t M'_r), written over x
+#pragma unroll
+      for (int I = 0; I < 4; ++I) {
+        const int i = 16 * I + c_;
+        f32x4 xb[NNT];
+#pragma unroll
+        for (int nt = 0; nt < NNT; ++nt) {
+          const int n = n0 + 16 * nt + 4 * g_;
+          xb[nt] = a.base ? *reinterpret_cast<const f32x4*>(a.base + tok_off(b, r0 + min(i, nrow - 1), h, a.T, a.H, DK) + n)
+                          : load4f(sX + i * LDK + n);
+        }
+        const float inv = 1.f / (t0f + (float)(r0 + i + 1));
+        const float msub = a.centered ? sCq[i] * inv : 0.f;
+        const float lam = sLam[i];
+#pragma unroll
+        for (int nt = 0; nt < NNT; ++nt) {
+          const int n = n0 + 16 * nt + 4 * g_;
+          const f32x4 mr = *reinterpret_cast<const f32x4*>(sM + n);
+          f32x4 cr, o;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            cr[r] = (acc[nt][I][r] - msub * mr[r]) * inv;  // Sigma_t x_t
+            o[r] = xb[nt][r] - lam * cr[r];
+          }
+          store4(sX + i * LDK + n, o[0], o[1], o[2], o[3]);
+          if (i < nrow) {
+            const size_t off = tok_off(b, r0 + i, h, a.T, a.H, DK) + n;
+            if (a.qclean_dbg) *reinterpret_cast<f32x4*>(a.qclean_dbg + off) = o;
+            if (a.corr) *reinterpret_cast<f32x4*>(a.corr + off) = cr;
+          }
+        }
+      }
+
+      // S'_{r+1} = S'_r + K'^T K' (not needed after the segment's last chunk)
+      if (c + 1 < cend) {
+#pragma unroll
+        for (int mt = 0; mt < NMT; ++mt)
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            const Frag<T> ka = frag_tr_at(ptr + 32 * q * LDK + 16 * mt, LDK);
+#pragma unroll
+            for (int nt = 0; nt < NNT; ++nt) mma(S[nt][mt], ka, kb[nt][q]);
+          }
+      }
     }
+    if constexpr (kDma) wait_vm_all();
+    __syncthreads();  // (4) q_clean of chunk c complete, next chunk arrived; x, K', scores released
   }
 
-  if (!iok) return;
-  // epilogue: every load is issued before the first store, and the optional
-  // outputs are written in loops of their own, so the loads and stores of the
-  // NN tiles overlap instead of forming NN round trips to memory
-  const float inv = 1.f / ti;
-  const float lam = a.lam[((size_t)b * a.T + r0 + i) * a.H + h];
-  const float msub = a.centered ? cqp * inv : 0.f;
-  const size_t rowoff = tok_off(b, r0 + i, h, a.T, a.H, DK) + 4 * g4;
-  const float* mrow = sMr[w >> 2] + 4 * g4;
-  f32x4 xb[NN];
-  if (a.base) {
+  // copy out the last chunk
+  {
+    const int r0 = (cend - 1) * C, nrow = min(C, a.T - r0);
 #pragma unroll
-    for (int tn = 0; tn < NN; ++tn) xb[tn] = *reinterpret_cast<const f32x4*>(a.base + rowoff + 16 * tn);
-  } else {
-#pragma unroll
-    for (int tn = 0; tn < NN; ++tn) xb[tn] = load4f(x + rowoff + 16 * tn);
+    for (int u = 0; u < NV; ++u) {
+      const int e = tid + NT * u, row = e / VPR, col = (e % VPR) * 8;
+      if (row < nrow)
+        *reinterpret_cast<vec_t*>(qc + tok_off(b, r0 + row, h, a.T, a.H, DK) + col) =
+            *reinterpret_cast<const vec_t*>(sX + row * LDK + col);
+    }
   }
-#pragma unroll
-  for (int tn = 0; tn < NN; ++tn) {  // acc <- Sigma_t x_t (the correction before lambda)
-    const f32x4 mr = *reinterpret_cast<const f32x4*>(mrow + 16 * tn);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) acc[tn][r] = (acc[tn][r] - msub * mr[r]) * inv;
-  }
-  T* qc = static_cast<T*>(a.qclean);
-#pragma unroll
-  for (int tn = 0; tn < NN; ++tn) {
-    f32x4 o;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) o[r] = xb[tn][r] - lam * acc[tn][r];
-    store4(qc + rowoff + 16 * tn, o[0], o[1], o[2], o[3]);
-    xb[tn] = o;
-  }
-  if (a.qclean_dbg) {
-#pragma unroll
-    for (int tn = 0; tn < NN; ++tn) *reinterpret_cast<f32x4*>(a.qclean_dbg + rowoff + 16 * tn) = xb[tn];
-  }
-  if (a.corr) {
-#pragma unroll
-    for (int tn = 0; tn < NN; ++tn) *reinterpret_cast<f32x4*>(a.corr + rowoff + 16 * tn) = acc[tn];
-  }
-  if (a.mdot && g4 == 0) a.mdot[((size_t)b * a.T + r0 + i) * a.H + h] = cqp + ti * cx;  // raw m . x
 }
 
 namespace {
@@ -440,15 +507,10 @@ hipError_t run_prefix(const CleanArgs& a, hipStream_t st) {
 }
 template <typename T, int DK>
 hipError_t run_out(const CleanArgs& a, hipStream_t st) {
-  const int nc = n_chunks(a.T);
-  if ((long long)a.B * a.H * nc == 0) return hipSuccess;
-  if (nc >= 2 && a.seg % 2 == 0) {  // two chunks per workgroup (never across a segment)
-    const long long nblk = (long long)a.B * a.H * ((nc + 1) / 2);
-    hipLaunchKernelGGL((clean_out_kernel<T, DK, 2>), dim3((unsigned)nblk), dim3(2 * kThreads), 0, st, a);
-  } else {
-    const long long nblk = (long long)a.B * a.H * nc;
-    hipLaunchKernelGGL((clean_out_kernel<T, DK, 1>), dim3((unsigned)nblk), dim3(kThreads), 0, st, a);
-  }
+  const long long nblk = (long long)a.B * a.H * n_segs(a.T, a.seg);
+  if (nblk == 0) return hipSuccess;
+  constexpr int NW = DK >= 128 ? 8 : 4;
+  hipLaunchKernelGGL((clean_out_kernel<T, DK, NW>), dim3((unsigned)nblk), dim3(64 * NW), 0, st, a);
   return hipGetLastError();
 }
 

@@ -428,6 +428,106 @@ struct RowTile {
   }
 };
 
+// One 64-row chunk of a [*, D] token tensor streamed from global memory
+// straight into LDS (gfx950 global_load_lds_dwordx4: each lane's 16 bytes land
+// at the wave's LDS base + 16 * lane), so a prefetch holds no registers.  The
+// destination is row-major with pitch D (no padding); one wave instruction
+// covers RPI whole rows, and the NW waves of the workgroup split the
+// instructions.  Rows >= n repeat row n - 1; the caller masks them.  The data
+// is visible to the workgroup after s_waitcnt vmcnt(0) and a barrier.
+template <int D, int NW>
+struct LdsStream {
+  static constexpr int VPR = D * 2 / 16;   // 16-byte pieces per bf16 row
+  static constexpr int RPI = 64 / VPR;     // rows per wave instruction
+  static constexpr int NI = kChunk / RPI / NW;  // instructions per wave
+  static_assert(VPR <= 64 && 64 % VPR == 0 && kChunk % (RPI * NW) == 0, "stream split");
+  __device__ __forceinline__ static void load(const bf16_t* src, size_t gstride, int n, bf16_t* dst) {
+    typedef __attribute__((address_space(3))) void lds_void;
+    const int l = lane_id(), w = wave_id();
+#pragma unroll
+    for (int it = 0; it < NI; ++it) {
+      const int ins = w * NI + it;
+      const int row = ins * RPI + l / VPR;
+      const bf16_t* p = src + (size_t)(row < n ? row : n - 1) * gstride + (l % VPR) * 8;
+      __builtin_amdgcn_global_load_lds((const void*)p, (lds_void*)(dst + ins * RPI * D), 16, 0, 0);
+    }
+  }
+};
+
+__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// x, opaque to the optimiser: addresses derived from it are formed where they
+// are used instead of being hoisted out of a loop and held in registers.
+__device__ __forceinline__ int opaque(int x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+// Fragment loads from a pointer that already includes the lane's offset.
+// frag_at: 8 contiguous elements (ld_frag with p = tile + (l % 16) ld + 8 (l / 16)).
+// frag_acc_at: elements 0..3 and 16..19 (ld_frag_acc with p = tile + (l % 16) ld + 4 (l / 16)).
+// frag_tr_at: ld_frag_tr with p = base + (8 (l / 16) + (l % 16) / 4) ld + 4 (l % 4)
+// for bf16, p = base + 8 (l / 16) ld + l % 16 for fp32.
+template <typename T>
+__device__ __forceinline__ Frag<T> frag_at(const T* p) {
+  Frag<T> f;
+  if constexpr (sizeof(T) == 2) {
+    f.v = *reinterpret_cast<const bf16x8*>(p);
+  } else {
+    f.lo = *reinterpret_cast<const f32x4*>(p);
+    f.hi = *reinterpret_cast<const f32x4*>(p + 4);
+  }
+  return f;
+}
+template <typename T>
+__device__ __forceinline__ Frag<T> frag_acc_at(const T* p) {
+  Frag<T> f;
+  if constexpr (sizeof(T) == 2) {
+    const bf16x4 lo = *reinterpret_cast<const bf16x4*>(p);
+    const bf16x4 hi = *reinterpret_cast<const bf16x4*>(p + 16);
+    f.v = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  } else {
+    f.lo = *reinterpret_cast<const f32x4*>(p);
+    f.hi = *reinterpret_cast<const f32x4*>(p + 16);
+  }
+  return f;
+}
+template <typename T>
+__device__ __forceinline__ Frag<T> frag_tr_at(const T* p, int ld) {
+  Frag<T> f;
+  if constexpr (sizeof(T) == 2) {
+    typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p));
+    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 4 * ld));
+    f.v = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      f.lo[e] = p[e * ld];
+      f.hi[e] = p[(4 + e) * ld];
+    }
+  }
+  return f;
+}
+template <typename T>
+__device__ __forceinline__ int frag_tr_lane_off(int l, int ld) {
+  const int g = l >> 4, j = l & 15;
+  if constexpr (sizeof(T) == 2) return (8 * g + (j >> 2)) * ld + 4 * (j & 3);
+  else return 8 * g * ld + j;
+}
+
+// Sum over aligned groups of n consecutive lanes (n = 2, 4, 8, 16), by
+// swizzles (no address registers).
+template <int N>
+__device__ __forceinline__ float group_sum(float x) {
+  static_assert(N == 2 || N == 4 || N == 8 || N == 16, "group");
+  x += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x041F));
+  if constexpr (N >= 4) x += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x081F));
+  if constexpr (N >= 8) x += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x101F));
+  if constexpr (N >= 16) x += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x201F));
+  return x;
+}
+
 // Scalar per-token value prefetched by lane `row` (clamped address, zeroed at use).
 struct RowScalar {
   float x;

@@ -187,16 +187,14 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
       S[tc] = zero4();
   }
 
-  // two register sets of prefetched chunk data: chunk ci is loaded two
-  // iterations ahead into set ci & 1 (the loop is unrolled by two so the sets
-  // stay in registers)
+  // chunk data prefetched into registers one iteration ahead
   struct Stage {
     RowTile<T, DK, NT> rk;
     RowTile<T, C, NT> rt;
     RowTile<T, BVS, NT> rv;
     RowScalar cf[4];
   };
-  Stage st[2];
+  Stage st;
   auto prefetch = [&](Stage& sg, int ci) {
     const int r0 = ci * C;
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
@@ -240,7 +238,7 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
       for (int q = 0; q < 4; ++q) sCf[buf][q][tid] = sg.cf[q].get();
     }
     if (ci > 0) write_back(ci - 1);
-    if (ci + 2 < N) prefetch(sg, ci + 2);
+    if (ci + 1 < N) prefetch(sg, ci + 1);
     __syncthreads();
     const T* Kb = sK[buf];
 
@@ -334,12 +332,8 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
     }
   };
 
-  if (N > 0) prefetch(st[0], 0);
-  if (N > 1) prefetch(st[1], 1);
-  for (int ci = 0; ci < N; ci += 2) {
-    step(st[0], ci);
-    if (ci + 1 < N) step(st[1], ci + 1);
-  }
+  if (N > 0) prefetch(st, 0);
+  for (int ci = 0; ci < N; ++ci) step(st, ci);
 
   if (N > 0) write_back(N - 1);
   if (a.ST) {

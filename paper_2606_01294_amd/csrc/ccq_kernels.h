@@ -13,9 +13,14 @@ namespace ccq {
 // I - lam Sigma, reusing the key statistics of the forward.
 //
 // The sequence is cut into segments of `seg` chunks.  Key statistics are
-// formed per segment (clean_gram, clean_prefix); each chunk's
-// output then needs only its segment's entry statistics and the keys of the
-// segment up to the chunk (clean_out), so every chunk runs in parallel.
+// formed per segment (clean_gram, clean_prefix); each segment's outputs then
+// need only its entry statistics and its own keys (clean_out walks the
+// segment's chunks in order), so the segments run in parallel.
+//
+// dk x dk statistics are stored fragment-native, in the order a 16x16 MFMA
+// accumulator keeps them: element (m, n), the coefficient of x_m in (C x)_n,
+// sits in tile (n / 16) (dk / 16) + m / 16 (1 KB fp32 per tile), lane
+// n % 16 + 16 ((m % 16) / 4), slot m % 4.
 struct CleanArgs {
   const void* q;      // x: [B,T,H,dk] io
   const void* k;      // [B,T,H,dk] io
@@ -30,9 +35,9 @@ struct CleanArgs {
   float* corr;        // Sigma_t x_t, [B,T,H,dk] fp32, or null
   float* mdot;        // m_t . x_t (raw key sum), [B,T,H] fp32, or null
   // workspace: NC = chunks, NS = segments per sequence
-  float* gram;        // [B*H, NS, dk, dk] raw segment sums of k k^T
-  void* sprime;       // [B*H, NS, dk/64, dk, 64] io: entry second moment about c_s,
-                      // in 64-column slices
+  float* gram;        // [B*H, NS, dk*dk] raw segment sums of k k^T, fragment-native
+  void* sprime;       // [B*H, NS, dk*dk] io: entry second moment about c_s,
+                      // fragment-native
   float* csum;        // [B*H, NC, dk] key sum of every chunk
   float* ssum;        // [B*H, NS, dk] key sum of every segment
   int B, T, H, dk;
@@ -162,7 +167,13 @@ struct CcqDkArgs {
 hipError_t launch_clean_gram(const CleanArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_clean_prefix(const CleanArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_clean_out(const CleanArgs& a, bool is_bf16, hipStream_t st);
-constexpr int kCleanSeg = 8;   // chunks per segment of the query contraction
+// Chunks per segment of the query contraction for bh heads of nc chunks: the
+// longest of 8, 4, 2 that still gives every compute unit a workgroup.
+inline int clean_seg(long long bh, long long nc) {
+  int seg = 8;
+  while (seg > 2 && bh * ((nc + seg - 1) / seg) < 256) seg /= 2;
+  return seg;
+}
 hipError_t launch_gla_state(const GlaStateArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
 hipError_t launch_gla_out(const GlaOutArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
 hipError_t launch_gdn_tri(const TriArgs& a, bool is_bf16, hipStream_t st);
