@@ -179,6 +179,21 @@ __global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
   if (a.muT && n == 0) *reinterpret_cast<f32x4*>(a.muT + (size_t)bh * DK + m) = run_b * inv;
 }
 
+// Transposed fragment at a lane-offset pointer (frag_tr_at); for bf16 the two
+// reads are issued as inline assembly so that the compiler does not drain the
+// streamed prefetch before them (the caller waits with lds_wait).
+template <typename T>
+__device__ __forceinline__ Frag<T> frag_tr_any(const T* p, int ld) {
+  if constexpr (sizeof(T) == 2) {
+    const bf16x4 lo = ds_read_tr16_asm(p), hi = ds_read_tr16_asm(p + 4 * ld);
+    Frag<T> f;
+    f.v = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return f;
+  } else {
+    return frag_tr_at(p, ld);
+  }
+}
+
 // Causal score tile t of a 64-token chunk (t < 10): key tile J <= token tile I.
 __device__ __forceinline__ int causal_tile_i(int t) { return t >= 6 ? 3 : t >= 3 ? 2 : t >= 1 ? 1 : 0; }
 
@@ -194,7 +209,7 @@ __device__ __forceinline__ int causal_tile_i(int t) { return t >= 6 ? 3 : t >= 3
 // cq'_i = m'_i . x_i comes from the score row sums and M'_r . x_i.  x and K'
 // are staged in LDS once per chunk; q_clean is formed in place over x and is
 // copied out with row-contiguous stores while the next chunk is staged.
-template <typename T, int DK, int NW>
+template <typename T, int DK, int NW, bool TRAIN>
 __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a) {
   constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P, LDP = C + P, LDQ = C + 4;
   constexpr int NT = 64 * NW, VPR = DK / 8;
@@ -284,10 +299,29 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
   float csum = 0.f;  // key sum of the current chunk, feature tid
   for (int c = cbeg; c < cend; ++c) {
     const int r0 = c * C, nrow = min(C, a.T - r0);
+    // per-token and per-feature values first: waiting for their loads costs
+    // nothing here, while after the stores below it would also wait for those
+    if (tid < C) sLam[tid] = rl.get();
+    if (tid < DK) {
+      if (c > cbeg) sM[tid] += csum - (float)C * cen;  // M'_c
+      csum = a.csum[((size_t)bh * NC + c) * DK + tid];
+    }
     // stage chunk c; each thread first copies out the q_clean of chunk c - 1
-    // (always a full chunk) held at the same places
+    // (always a full chunk) held at the same places.  The streamed chunk is
+    // read before any store is issued, so that no wait on it can cover a store.
     {
       const int t_ = opaque(tid);
+      vec_t xv[NV], kv[NV];
+#pragma unroll
+      for (int u = 0; u < NV; ++u) {
+        if constexpr (kDma) {
+          xv[u] = *reinterpret_cast<const vec_t*>(sSt + 8 * (t_ + NT * u));
+          kv[u] = *reinterpret_cast<const vec_t*>(sSt + C * DK + 8 * (t_ + NT * u));
+        } else {
+          xv[u] = rx.get(u);
+          kv[u] = rk.get(u);
+        }
+      }
 #pragma unroll
       for (int u = 0; u < NV; ++u) {
         const int e = t_ + NT * u, row = e / VPR, col = (e % VPR) * 8;
@@ -295,29 +329,17 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
         if (c > cbeg)
           *reinterpret_cast<vec_t*>(qc + tok_off(b, r0 - C + row, h, a.T, a.H, DK) + col) =
               *reinterpret_cast<const vec_t*>(px);
-        vec_t xv, kv, y;
-        if constexpr (kDma) {
-          xv = *reinterpret_cast<const vec_t*>(sSt + 8 * e);
-          kv = *reinterpret_cast<const vec_t*>(sSt + C * DK + 8 * e);
-        } else {
-          xv = rx.get(u);
-          kv = rk.get(u);
-        }
+        vec_t y;
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-          xv[q] = row < nrow ? xv[q] : to<T>(0.f);
-          y[q] = to<T>(row < nrow ? f32(kv[q]) - sC[col + q] : 0.f);
+          xv[u][q] = row < nrow ? xv[u][q] : to<T>(0.f);
+          y[q] = to<T>(row < nrow ? f32(kv[u][q]) - sC[col + q] : 0.f);
         }
-        *reinterpret_cast<vec_t*>(px) = xv;
+        *reinterpret_cast<vec_t*>(px) = xv[u];
         *reinterpret_cast<vec_t*>(sK + row * LDK + col) = y;
       }
     }
-    if (tid < C) sLam[tid] = rl.get();
-    if (tid < DK) {
-      if (c > cbeg) sM[tid] += csum - (float)C * cen;  // M'_c
-      csum = a.csum[((size_t)bh * NC + c) * DK + tid];
-    }
-    __syncthreads();  // (1) x, K', M'_c staged; the staging area is free
+    lds_barrier();  // (1) x, K', M'_c staged; the staging area is free
     if (c + 1 < cend) prefetch(c + 1);
 
     // raw scores of the causal tiles this wave owns, to sS[i][j]; then
@@ -353,7 +375,7 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
           for (int nt = 0; nt < NNT; ++nt) mma(acc[nt][I], af[nt], xf[I]);
       }
     }
-    __syncthreads();  // (2) scores complete
+    lds_barrier();  // (2) scores complete
 
     // cq'_i = M'_r . x_i + sum_{j <= i} sc_ij, and the shifted scores; TPI
     // consecutive threads per token
@@ -402,10 +424,10 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
       }
       if (pp == 0) {
         sCq[i] = cqp;
-        if (a.mdot && i < nrow) a.mdot[((size_t)b * a.T + r0 + i) * a.H + h] = cqp + ti * cx;  // raw m . x
+        if (TRAIN && a.mdot && i < nrow) a.mdot[((size_t)b * a.T + r0 + i) * a.H + h] = cqp + ti * cx;  // raw m . x
       }
     }
-    __syncthreads();  // (3) shifted scores complete
+    lds_barrier();  // (3) shifted scores complete
 
     {
       const int l_ = opaque(tid & 63), g_ = l_ >> 4, c_ = l_ & 15;
@@ -415,7 +437,10 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
 #pragma unroll
       for (int nt = 0; nt < NNT; ++nt)
 #pragma unroll
-        for (int q = 0; q < 2; ++q) kb[nt][q] = frag_tr_at(ptr + 32 * q * LDK + n0 + 16 * nt, LDK);
+        for (int q = 0; q < 2; ++q) kb[nt][q] = frag_tr_any(ptr + 32 * q * LDK + n0 + 16 * nt, LDK);
+      if constexpr (kDma)
+#pragma unroll
+        for (int nt = 0; nt < NNT; ++nt) lds_wait(kb[nt]);
       // out^T += K'^T sc (keys 32..63 only reach tokens 32..63)
       const T* pp_ = sP + c_ * LDP + 8 * g_;
 #pragma unroll
@@ -435,8 +460,11 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
 #pragma unroll
         for (int nt = 0; nt < NNT; ++nt) {
           const int n = n0 + 16 * nt + 4 * g_;
-          xb[nt] = a.base ? *reinterpret_cast<const f32x4*>(a.base + tok_off(b, r0 + min(i, nrow - 1), h, a.T, a.H, DK) + n)
-                          : load4f(sX + i * LDK + n);
+          if constexpr (TRAIN)
+            xb[nt] = a.base ? *reinterpret_cast<const f32x4*>(a.base + tok_off(b, r0 + min(i, nrow - 1), h, a.T, a.H, DK) + n)
+                            : load4f(sX + i * LDK + n);
+          else
+            xb[nt] = load4f(sX + i * LDK + n);
         }
         const float inv = 1.f / (t0f + (float)(r0 + i + 1));
         const float msub = a.centered ? sCq[i] * inv : 0.f;
@@ -452,7 +480,7 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
             o[r] = xb[nt][r] - lam * cr[r];
           }
           store4(sX + i * LDK + n, o[0], o[1], o[2], o[3]);
-          if (i < nrow) {
+          if (TRAIN && i < nrow) {
             const size_t off = tok_off(b, r0 + i, h, a.T, a.H, DK) + n;
             if (a.qclean_dbg) *reinterpret_cast<f32x4*>(a.qclean_dbg + off) = o;
             if (a.corr) *reinterpret_cast<f32x4*>(a.corr + off) = cr;
@@ -460,20 +488,36 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
         }
       }
 
-      // S'_{r+1} = S'_r + K'^T K' (not needed after the segment's last chunk)
+      // S'_{r+1} = S'_r + K'^T K' (not needed after the segment's last chunk);
+      // transposed key reads two m tiles ahead of their products
       if (c + 1 < cend) {
+        constexpr int G = 2, NG = NMT / G;
+        Frag<T> ka[2][2 * G];
+        auto load_group = [&](Frag<T>(&f)[2 * G], int g) {
 #pragma unroll
-        for (int mt = 0; mt < NMT; ++mt)
+          for (int e = 0; e < G; ++e)
 #pragma unroll
-          for (int q = 0; q < 2; ++q) {
-            const Frag<T> ka = frag_tr_at(ptr + 32 * q * LDK + 16 * mt, LDK);
+            for (int q = 0; q < 2; ++q) f[2 * e + q] = frag_tr_any(ptr + 32 * q * LDK + 16 * (G * g + e), LDK);
+        };
+        load_group(ka[0], 0);
 #pragma unroll
-            for (int nt = 0; nt < NNT; ++nt) mma(S[nt][mt], ka, kb[nt][q]);
+        for (int g = 0; g < NG; ++g) {
+          if (g + 1 < NG) load_group(ka[(g + 1) & 1], g + 1);
+          if constexpr (kDma) {
+            if (g + 1 < NG) lds_wait_but<4 * G>(ka[g & 1]);
+            else lds_wait(ka[g & 1]);
           }
+#pragma unroll
+          for (int e = 0; e < G; ++e)
+#pragma unroll
+            for (int q = 0; q < 2; ++q)
+#pragma unroll
+              for (int nt = 0; nt < NNT; ++nt) mma(S[nt][G * g + e], ka[g & 1][2 * e + q], kb[nt][q]);
+        }
       }
     }
     if constexpr (kDma) wait_vm_all();
-    __syncthreads();  // (4) q_clean of chunk c complete, next chunk arrived; x, K', scores released
+    lds_barrier();  // (4) q_clean of chunk c complete, next chunk arrived; x, K', scores released
   }
 
   // copy out the last chunk
@@ -510,7 +554,10 @@ hipError_t run_out(const CleanArgs& a, hipStream_t st) {
   const long long nblk = (long long)a.B * a.H * n_segs(a.T, a.seg);
   if (nblk == 0) return hipSuccess;
   constexpr int NW = DK >= 128 ? 8 : 4;
-  hipLaunchKernelGGL((clean_out_kernel<T, DK, NW>), dim3((unsigned)nblk), dim3(64 * NW), 0, st, a);
+  if (a.base || a.corr || a.mdot || a.qclean_dbg)
+    hipLaunchKernelGGL((clean_out_kernel<T, DK, NW, true>), dim3((unsigned)nblk), dim3(64 * NW), 0, st, a);
+  else
+    hipLaunchKernelGGL((clean_out_kernel<T, DK, NW, false>), dim3((unsigned)nblk), dim3(64 * NW), 0, st, a);
   return hipGetLastError();
 }
 

@@ -456,6 +456,41 @@ struct LdsStream {
 
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Workgroup barrier that orders LDS only: waits for this wave's LDS
+// operations, not for its global loads and stores (a __syncthreads() fence
+// would also drain the vector-memory counter, i.e. every prefetch in flight).
+// Also a compiler barrier for memory accesses.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Transposing LDS read (as ld_frag_tr) issued as inline assembly.  The
+// compiler treats the builtin form as possibly reading data that a
+// global_load_lds still in flight is writing and drains every outstanding
+// vector-memory operation before it, which would serialise a streamed
+// prefetch; this form is invisible to its counters, so the caller makes the
+// result valid with lds_wait() before use (the LDS returns data in order, so
+// the compiler's own waits for later reads stay correct).
+__device__ __forceinline__ bf16x4 ds_read_tr16_asm(const void* p) {
+  bf16x4 r;
+  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(a));
+  return r;
+}
+// s_waitcnt lgkmcnt(0), with the fragments passed through it so that no use
+// of them can be scheduled above the wait.
+template <int N>
+__device__ __forceinline__ void lds_wait(Frag<bf16_t> (&f)[N]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(f[i].v));
+}
+// The same, leaving the K most recently issued LDS operations in flight.
+template <int K, int N>
+__device__ __forceinline__ void lds_wait_but(Frag<bf16_t> (&f)[N]) {
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(K) : "memory");
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(f[i].v));
+}
+
 // x, opaque to the optimiser: addresses derived from it are formed where they
 // are used instead of being hoisted out of a loop and held in registers.
 __device__ __forceinline__ int opaque(int x) {

@@ -343,6 +343,297 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
   }
 }
 
+// The same recurrence for bf16 with the chunk operands streamed straight into
+// LDS (global_load_lds_dwordx4), two chunks ahead, through a ring of three
+// stages: K (64 x DK), Tm (64 x 64), the V slice (64 x BVS) and the four
+// coefficient rows.  No registers hold prefetched data and no instructions
+// copy it; the vector-memory counter is waited on explicitly, with the chunk
+// stores of the two previous chunks allowed to remain in flight.  Rows are
+// unpadded, so K and Tm are stored with their 16-byte pieces permuted per row
+// (an XOR of the piece index) to keep the fragment reads free of bank
+// conflicts: piece p of K row r sits at p ^ kswz(r), of Tm row r at p ^ tswz(r).
+__device__ __forceinline__ int kswz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+__device__ __forceinline__ int tswz(int r) { return (r >> 1) & 7; }
+
+template <int X>
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(X) : "memory");
+}
+
+template <int DK, int NPR, int NH>
+__global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const GdnArgs a) {
+  typedef bf16_t T;
+  typedef __attribute__((address_space(3))) void lds_void;
+  constexpr int C = kChunk, NW = NPR * NH, BVS = 16 * NPR;
+  constexpr int DKH = DK / NH, NCT = DKH / 16, NKH = DKH / 32;
+  constexpr int RB = DK * 2;                                  // K row bytes
+  constexpr int KB = C * RB, TB = C * C * 2, VB = C * BVS * 2, FB = 4 * C * 4;
+  constexpr int NIK = KB / 1024, NIT = TB / 1024, NIV = VB / 1024;
+  constexpr int NIW = (NIK + NIT + NIV) / NW + 1;             // 1 KB pieces per wave and chunk
+  constexpr int SB = KB + TB + VB + FB, NSTAGE = 3;
+  constexpr int XB = NH > 1 ? NW * 4 * 64 * 16 : 16;
+  constexpr int NSW = NKH + (NH == 1 ? 2 : 1);                // stores per wave per chunk
+  static_assert(DK == 128 || DK == 256, "key width");
+  static_assert(NH == 1 || NH == 2, "key split");
+  static_assert(NKH >= 1 && VB % 1024 == 0, "tiles");
+  __shared__ __align__(1024) char smem[NSTAGE * SB + XB + 1024];
+  f32x4* const sX = reinterpret_cast<f32x4*>(smem + NSTAGE * SB);
+  char* const sDummy = smem + NSTAGE * SB + XB;
+
+  const int nvt = a.dv / BVS;
+  const int N = (a.T + C - 1) / C;
+  const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int bh = lb / nvt;
+  const int l = lane_id(), g4 = l >> 4, c16 = l & 15;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int pr = w / NH, hq = w % NH;
+  const int v0 = (lb % nvt) * BVS;
+  const int v = v0 + 16 * pr + c16;
+  const int c0 = hq * DKH;
+  const int b = bh / a.H, h = bh % a.H;
+  const T* k = static_cast<const T*>(a.k);
+  const T* vin = static_cast<const T*>(a.v);
+  const T* Tg = static_cast<const T*>(a.Tm);
+
+  // chunk ci into stage ci % 3.  Piece i of each operand goes to wave i % NW,
+  // so every wave issues the same number of pieces of each kind.  Addresses
+  // are a per-chunk base (uniform) plus a 32-bit per-lane offset; rows past
+  // the end of the sequence read row nrow - 1 (finite data; the chunk
+  // transform zeroes their contribution).
+  static_assert(NIK % NW == 0 && NIT % NW == 0 && NIV % NW == 0, "piece split");
+  auto issue = [&](int ci) {
+    char* sb = smem + (ci % NSTAGE) * SB;
+    const int r0 = ci * C, nrow = min(C, a.T - r0);
+    const int hs = a.H * DK, hv = a.H * a.dv;
+    const T* kb = k + tok_off(b, r0, h, a.T, a.H, DK);
+    const T* tb = Tg + ((size_t)bh * N + ci) * C * C;
+    const T* vb = vin + tok_off(b, r0, h, a.T, a.H, a.dv) + v0;
+#pragma unroll
+    for (int it = 0; it < NIK / NW; ++it) {
+      constexpr int CPR = DK / 8;
+      const int ins = it * NW + w, row = ins * (64 / CPR) + l / CPR;
+      const int off = min(row, nrow - 1) * hs + 8 * ((l % CPR) ^ kswz(row));
+      __builtin_amdgcn_global_load_lds((const void*)(kb + off), (lds_void*)(sb + ins * 1024), 16, 0, 0);
+    }
+#pragma unroll
+    for (int it = 0; it < NIT / NW; ++it) {
+      const int ins = it * NW + w, row = ins * 8 + l / 8;
+      const int off = row * C + 8 * ((l % 8) ^ tswz(row));
+      __builtin_amdgcn_global_load_lds((const void*)(tb + off), (lds_void*)(sb + KB + ins * 1024), 16, 0, 0);
+    }
+#pragma unroll
+    for (int it = 0; it < NIV / NW; ++it) {
+      constexpr int CPR = BVS / 8;
+      const int ins = it * NW + w, row = ins * (64 / CPR) + l / CPR;
+      const int off = min(row, nrow - 1) * hv + 8 * (l % CPR);
+      __builtin_amdgcn_global_load_lds((const void*)(vb + off), (lds_void*)(sb + KB + TB + ins * 1024), 16, 0, 0);
+    }
+    // the coefficient rows (one piece; the other waves load it into a spare area)
+    __builtin_amdgcn_global_load_lds((const void*)(a.gam + (((size_t)bh * N + ci) * 5 + 1) * C + 4 * l),
+                                     (lds_void*)(w == 0 ? sb + KB + TB + VB : sDummy), 16, 0, 0);
+  };
+  // wait until chunk ci has landed: the pieces and stores issued after its own
+  // may stay in flight (stores of chunk ci - 2, pieces of ci + 1, stores of ci - 1)
+  auto wait_chunk = [&](int ci) {
+    const bool more = ci + 1 < N;
+    if (ci >= 2) {
+      if (more) wait_vm<2 * NSW + NIW>();
+      else wait_vm<2 * NSW>();
+    } else if (ci == 1) {
+      if (more) wait_vm<NSW + NIW>();
+      else wait_vm<NSW>();
+    } else {
+      if (more) wait_vm<NIW>();
+      else wait_vm<0>();
+    }
+  };
+
+  if (N > 0) issue(0);
+  if (N > 1) issue(1);
+
+  // S^T[c][v], c = c0 + 16 tc + 4 g4 + r
+  f32x4 S[NCT];
+#pragma unroll
+  for (int tc = 0; tc < NCT; ++tc) {
+    if (a.S0)
+      S[tc] = *reinterpret_cast<const f32x4*>(a.S0 + ((size_t)bh * a.dv + v) * DK + c0 + 16 * tc + 4 * g4);
+    else
+      S[tc] = zero4();
+  }
+
+  const int vt = (v0 >> 4) + pr;
+  T* st_base = static_cast<T*>(a.states) + (((size_t)vt * (DK / 32) + hq * NKH) * 16 + c16) * 32 + 8 * g4;
+  T* u_base = static_cast<T*>(a.U) + ((size_t)vt * 2 * 16 + c16) * 32 + 8 * g4;
+
+  for (int ci = 0; ci < N; ++ci) {
+    const char* sb = smem + (ci % NSTAGE) * SB;
+    const char* Kb = sb;
+    const T* Tb = reinterpret_cast<const T*>(sb + KB);
+    const T* Vb = reinterpret_cast<const T*>(sb + KB + TB);
+    const float* Fb = reinterpret_cast<const float*>(sb + KB + TB + VB);
+    wait_chunk(ci);
+    lds_barrier();  // chunk ci visible; stage (ci + 2) % 3 and the exchange area released
+    if (ci + 2 < N) issue(ci + 2);
+
+    // P = K S_r^T over this wave's features: K rows 16 J + c16, features in
+    // accumulator-pair order (pieces (c0 + 32 m) / 8 + g4 / 2 and + 2)
+    Frag<T> sf[NKH];
+#pragma unroll
+    for (int m = 0; m < NKH; ++m) sf[m] = acc_pair_frag<T>(S[2 * m], S[2 * m + 1]);
+    const int ks = kswz(c16), kb8 = (g4 & 1) * 8;
+    auto kfrag = [&](int J, int m) {
+      const char* row = Kb + (16 * J + c16) * RB + kb8;
+      const int p0 = (c0 + 32 * m) / 8 + (g4 >> 1);
+      const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row + 16 * (p0 ^ ks));
+      const bf16x4 hi = *reinterpret_cast<const bf16x4*>(row + 16 * ((p0 + 2) ^ ks));
+      Frag<T> f;
+      f.v = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      return f;
+    };
+    // the V slice, transposed (issued now, waited for where used)
+    Frag<T> vf[2];
+    {
+      const int j = c16;
+      const char* pv = reinterpret_cast<const char*>(Vb) + (4 * g4 + (j >> 2)) * (2 * BVS) + 32 * pr + 8 * (j & 3);
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        const bf16x4 lo = ds_read_tr16_asm(pv + 32 * m * 2 * BVS);
+        const bf16x4 hi = ds_read_tr16_asm(pv + (32 * m + 16) * 2 * BVS);
+        vf[m].v = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      }
+    }
+    f32x4 R[4];
+    {
+      Frag<T> kf[2][NKH];
+#pragma unroll
+      for (int m = 0; m < NKH; ++m) kf[0][m] = kfrag(0, m);
+#pragma unroll
+      for (int J = 0; J < 4; ++J) {
+        if (J + 1 < 4)
+#pragma unroll
+          for (int m = 0; m < NKH; ++m) kf[(J + 1) & 1][m] = kfrag(J + 1, m);
+        __builtin_amdgcn_sched_barrier(0);
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int m = 0; m < NKH; ++m) mma(acc, kf[J & 1][m], sf[m]);
+        R[J] = acc;
+      }
+    }
+    // coefficients and Tm rows, read now so that their latency overlaps the
+    // exchange
+    Frag<T> tfr[4][2];
+    f32x4 bg[4], bj[4], dd[4];
+#pragma unroll
+    for (int J = 0; J < 4; ++J) {
+      bg[J] = *reinterpret_cast<const f32x4*>(Fb + 16 * J + 4 * g4);
+      bj[J] = *reinterpret_cast<const f32x4*>(Fb + C + 16 * J + 4 * g4);
+      dd[J] = *reinterpret_cast<const f32x4*>(Fb + 2 * C + 16 * J + 4 * g4);
+    }
+    const float eC = Fb[3 * C];
+    {
+      const int ts = tswz(c16);
+#pragma unroll
+      for (int I = 0; I < 4; ++I)
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+          tfr[I][q].v = *reinterpret_cast<const bf16x8*>(reinterpret_cast<const char*>(Tb) + (16 * I + c16) * 128 +
+                                                         16 * ((4 * q + g4) ^ ts));
+    }
+    if constexpr (NH > 1) {
+      // sum the NH partial products of this value slice, in a fixed order so
+      // every wave of the slice holds bit-identical P
+#pragma unroll
+      for (int J = 0; J < 4; ++J) sX[(w * 4 + J) * 64 + l] = R[J];
+      lds_barrier();
+      f32x4 part[NH][4];
+#pragma unroll
+      for (int hh = 0; hh < NH; ++hh)
+#pragma unroll
+        for (int J = 0; J < 4; ++J) part[hh][J] = sX[((pr * NH + hh) * 4 + J) * 64 + l];
+#pragma unroll
+      for (int J = 0; J < 4; ++J) {
+        f32x4 sum = part[0][J];
+#pragma unroll
+        for (int hh = 1; hh < NH; ++hh) sum += part[hh][J];
+        R[J] = sum;
+      }
+    }
+    // K^T of this wave's features for the update (rows 4 g4 + j / 4 (+ 16) of
+    // each 32-token half, pieces (c0 + 16 t) / 8 + (j % 4) / 2), issued now so
+    // that they arrive while R and U are formed
+    Frag<T> tf[NCT][2];
+    {
+      const int j = c16, rr = 4 * g4 + (j >> 2), rs = kswz(rr), hb = (j & 1) * 8;
+#pragma unroll
+      for (int t = 0; t < NCT; ++t)
+#pragma unroll
+        for (int kq = 0; kq < 2; ++kq) {
+          const int p = (c0 + 16 * t) / 8 + ((j & 3) >> 1);
+          const char* pl = Kb + (32 * kq + rr) * RB + 16 * (p ^ rs) + hb;
+          const bf16x4 lo = ds_read_tr16_asm(pl);
+          const bf16x4 hi = ds_read_tr16_asm(pl + 16 * RB);
+          tf[t][kq].v = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        }
+    }
+    lds_wait_but<(4 * NCT < 15 ? 4 * NCT : 15)>(vf);  // at most 15 LDS reads stay in flight
+    // R = beta V - beta e^gamma P
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int J = 2 * m + hh;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) R[J][r] = bj[J][r] * frag_elem(vf[m], 4 * hh + r) - bg[J][r] * R[J][r];
+      }
+    // U = Tm R (Tm rows are stored in acc_pos order)
+    const Frag<T> rf0 = acc_pair_frag<T>(R[0], R[1]);
+    const Frag<T> rf1 = acc_pair_frag<T>(R[2], R[3]);
+    f32x4 U[4];
+#pragma unroll
+    for (int I = 0; I < 4; ++I) {
+      U[I] = zero4();
+      mma(U[I], tfr[I][0], rf0);
+      mma(U[I], tfr[I][1], rf1);
+    }
+    Frag<T> uf[2];
+    uf[0] = acc_pair_frag<T>(U[0], U[1]);
+    uf[1] = acc_pair_frag<T>(U[2], U[3]);
+#pragma unroll
+    for (int I = 0; I < 4; ++I) U[I] *= dd[I];
+    const Frag<T> ud0 = acc_pair_frag<T>(U[0], U[1]);
+    const Frag<T> ud1 = acc_pair_frag<T>(U[2], U[3]);
+    // S^T <- e^{gamma_C} S^T + K^T diag(e^{gamma_C - gamma}) U
+#pragma unroll
+    for (int t = 1; t < NCT; ++t) lds_wait(tf[t]);
+#pragma unroll
+    for (int tc = 0; tc < NCT; ++tc) {
+      S[tc] *= eC;
+      mma(S[tc], tf[tc][0], ud0);
+      mma(S[tc], tf[tc][1], ud1);
+    }
+    // S_r and U^T of this chunk, fragment-native (1 KB per value tile and k step)
+    {
+      T* st_out = st_base + ((size_t)bh * N + ci) * a.dv * DK;
+#pragma unroll
+      for (int m = 0; m < NKH; ++m) store_frag(st_out + 16 * 32 * m, sf[m]);
+      T* u_out = u_base + ((size_t)bh * N + ci) * a.dv * C;
+      if constexpr (NH == 1) {
+        store_frag(u_out, uf[0]);
+        store_frag(u_out + 16 * 32, uf[1]);
+      } else {
+        store_frag(u_out + 16 * 32 * hq, hq == 0 ? uf[0] : uf[1]);
+      }
+    }
+  }
+
+  if (a.ST) {
+    wait_vm<0>();
+#pragma unroll
+    for (int tc = 0; tc < NCT; ++tc)
+      *reinterpret_cast<f32x4*>(a.ST + ((size_t)bh * a.dv + v) * DK + c0 + 16 * tc + 4 * g4) = S[tc];
+  }
+}
+
 // Outputs of one chunk (eight waves).  The decayed, masked scores
 //   P_ij = e^{gamma_i - gamma_j} (q_i . k_j)  (j <= i)
 // are formed once (ten nonzero 16 x 16 tiles over the waves) and kept in LDS;
@@ -466,10 +757,20 @@ hipError_t run_gdn_state_v(const GdnArgs& a, hipStream_t st) {
 // Split the key features over as many waves (1, 2, 4 or 8, at least 32
 // features each) as it takes to give every SIMD of the chip a wave, with four
 // waves per workgroup where the split allows.
+template <int DK, int NPR, int NH>
+hipError_t run_gdn_state_dma(const GdnArgs& a, hipStream_t st) {
+  const int nblk = a.B * a.H * (a.dv / (16 * NPR));
+  if (nblk == 0) return hipSuccess;
+  hipLaunchKernelGGL((gdn_state_dma_kernel<DK, NPR, NH>), dim3(nblk), dim3(64 * NPR * NH), 0, st, a);
+  return hipGetLastError();
+}
 template <typename T, int DK>
 hipError_t run_gdn_state(const GdnArgs& a, hipStream_t st) {
   const long long slices = (long long)a.B * a.H * (a.dv / 16);
   constexpr int kSimds = 1024;
+  if constexpr (sizeof(T) == 2 && (DK == 128 || DK == 256)) {
+    if (slices * 2 >= kSimds && a.dv % 32 == 0) return run_gdn_state_dma<DK, 2, 2>(a, st);
+  }
   if (slices >= kSimds || DK < 64) return run_gdn_state_v<T, DK, 4, 1>(a, st);
   if (slices * 2 >= kSimds || DK < 128) return run_gdn_state_v<T, DK, 2, 2>(a, st);
   if constexpr (DK >= 128) {
