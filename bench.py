@@ -108,7 +108,7 @@ KERNEL_SYMBOL = {"clean_gram": "clean_gram_kernel",
                  "clean_prefix": "clean_prefix_kernel", "clean_out": "clean_out_kernel",
                  "clean_out_train": "clean_out_kernel", "clean_dq": "clean_out_kernel",
                  "gla_state": "gla_state_kernel", "gla_out": "gla_out_kernel",
-                 "gdn_tri": "gdn_tri_kernel", "gdn_state": "gdn_state_kernel",
+                 "gdn_tri": "gdn_tri_kernel", "gdn_state": "gdn_state_dma_kernel",
                  "gdn_out": "gdn_out_kernel", "gla_dstate": "gla_dstate_kernel",
                  "gla_bwd_chunk": "gla_bwd_chunk_kernel", "gla_dg": "gla_dg_kernel",
                  "ccq_dk": "ccq_dk_kernel"}
