@@ -666,7 +666,20 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
   const int vg = w % NVG, ig = w / NVG;
   const size_t gstride = (size_t)a.H * DK;
 
-  // this wave's S_r and U^T fragments (fragment-native, 1 KB each), issued first
+  {
+    RowTile<T, DK, kOutThreads> rq, rk;
+    rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+    rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+    if (tid < C) sGam[tid] = a.gam[((size_t)bh * N + ci) * 5 * C + tid];
+    rq.store(sQ, LDQ);
+    rk.store(sK, LDQ);
+  }
+  __syncthreads();
+
+  // this wave's S_r and U^T fragments (fragment-native, 1 KB each), issued
+  // after the staging of q and k so that the two sets of registers are not
+  // live at once (two workgroups fit on a compute unit); they arrive while the
+  // score tiles are formed
   const T* Sg = static_cast<const T*>(a.states) + ((size_t)bh * N + ci) * a.dv * DK;
   const T* Ug = static_cast<const T*>(a.U) + ((size_t)bh * N + ci) * a.dv * C;
   Frag<T> sfr[VPW][NK], ufr[VPW][2];
@@ -678,15 +691,6 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
 #pragma unroll
     for (int m = 0; m < 2; ++m) ufr[vt][m] = ld_frag_global(Ug + ((size_t)vtile * 2 + m) * 16 * 32, 32);
   }
-  {
-    RowTile<T, DK, kOutThreads> rq, rk;
-    rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-    rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-    if (tid < C) sGam[tid] = a.gam[((size_t)bh * N + ci) * 5 * C + tid];
-    rq.store(sQ, LDQ);
-    rk.store(sK, LDQ);
-  }
-  __syncthreads();
 
   // P tiles: ten lower tiles (I >= J) over the waves, the six upper ones zero;
   // computed transposed (row j, column i) and stored as rows i
@@ -715,24 +719,28 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
   for (int it = 0; it < IPW; ++it) {
     const int I = ig * IPW + it;
     const int i = 16 * I + c16;
-    Frag<T> qf[NK];
+    // S_r Q^T one k step at a time (one q fragment live), both value tiles
+    f32x4 acc[VPW];
 #pragma unroll
-    for (int m = 0; m < NK; ++m) qf[m] = ld_frag_acc(sQ + 16 * I * LDQ + 32 * m, (size_t)LDQ);
+    for (int vt = 0; vt < VPW; ++vt) acc[vt] = zero4();
+#pragma unroll
+    for (int m = 0; m < NK; ++m) {
+      const Frag<T> qf = ld_frag_acc(sQ + 16 * I * LDQ + 32 * m, (size_t)LDQ);
+#pragma unroll
+      for (int vt = 0; vt < VPW; ++vt) mma(acc[vt], sfr[vt][m], qf);
+    }
     const Frag<T> pf0 = ld_frag(sP + 16 * I * LDP, LDP);
     const Frag<T> pf1 = ld_frag(sP + 16 * I * LDP + 32, LDP);
     const float ei = __expf(sGam[i]);
 #pragma unroll
     for (int vt = 0; vt < VPW; ++vt) {
-      f32x4 acc = zero4();
-#pragma unroll
-      for (int m = 0; m < NK; ++m) mma(acc, sfr[vt][m], qf[m]);
-      acc *= ei;
-      mma(acc, ufr[vt][0], pf0);
-      if (I >= 2) mma(acc, ufr[vt][1], pf1);  // keys 32..63 precede row i only for I >= 2
+      acc[vt] *= ei;
+      mma(acc[vt], ufr[vt][0], pf0);
+      if (I >= 2) mma(acc[vt], ufr[vt][1], pf1);  // keys 32..63 precede row i only for I >= 2
       if (i < nrow) {
         const int vcol = 16 * (vg * VPW + vt) + 4 * g4;
-        store4(o + tok_off(b, r0 + i, h, a.T, a.H, a.dv) + vcol, a.scale * acc[0], a.scale * acc[1],
-               a.scale * acc[2], a.scale * acc[3]);
+        store4(o + tok_off(b, r0 + i, h, a.T, a.H, a.dv) + vcol, a.scale * acc[vt][0], a.scale * acc[vt][1],
+               a.scale * acc[vt][2], a.scale * acc[vt][3]);
       }
     }
   }

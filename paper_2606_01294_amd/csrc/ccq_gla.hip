@@ -165,11 +165,13 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
 
   __shared__ __align__(16) T sQt[C * LDQ];
   __shared__ __align__(16) T sKt[C * LDQ];
-  __shared__ __align__(16) T sV[C * LDV];
-  constexpr int kBBytes = C * LDB * 4, kPBytes = C * LDP * (int)sizeof(T);
-  __shared__ __align__(16) char sBP[kBBytes > kPBytes ? kBBytes : kPBytes];
-  float* sB = reinterpret_cast<float*>(sBP);  // gates, then their prefix b
-  T* sP = reinterpret_cast<T*>(sBP);          // masked scores, once sB is dead
+  // the gates (fp32) share their space with the masked scores and the V slice,
+  // both written only once the gates are dead: two workgroups fit on a CU
+  constexpr int kBBytes = C * LDB * 4, kPBytes = C * LDP * (int)sizeof(T), kVBytes = C * LDV * (int)sizeof(T);
+  __shared__ __align__(16) char sBPV[kBBytes > kPBytes + kVBytes ? kBBytes : kPBytes + kVBytes];
+  float* sB = reinterpret_cast<float*>(sBPV);     // gates, then their prefix b
+  T* sP = reinterpret_cast<T*>(sBPV);             // masked scores, once sB is dead
+  T* sV = reinterpret_cast<T*>(sBPV + kPBytes);   // V slice, once sB is dead
   __shared__ __align__(16) float sBm[DK];
   __shared__ float sTot[TPC][DK];
 
@@ -282,22 +284,26 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
     for (int it = 0; it < IPW; ++it) {
       const int I = ig * IPW + it;
       const int i = 16 * I + c16;
-      Frag<T> qf[NK];
+      // S_r' Qt^T one k step at a time (one q fragment live), all value tiles
+      f32x4 acc[VPW];
 #pragma unroll
-      for (int m = 0; m < NK; ++m) qf[m] = ld_frag(sQt + 16 * I * LDQ + 32 * m, LDQ);
+      for (int vt = 0; vt < VPW; ++vt) acc[vt] = zero4();
+#pragma unroll
+      for (int m = 0; m < NK; ++m) {
+        const Frag<T> qf = ld_frag(sQt + 16 * I * LDQ + 32 * m, LDQ);
+#pragma unroll
+        for (int vt = 0; vt < VPW; ++vt) mma(acc[vt], sfr[vt][m], qf);
+      }
       const Frag<T> pf0 = ld_frag(sP + 16 * I * LDP, LDP);
       const Frag<T> pf1 = ld_frag(sP + 16 * I * LDP + 32, LDP);
 #pragma unroll
       for (int vt = 0; vt < VPW; ++vt) {
         const int vl = 16 * (vg * VPW + vt);  // value column within the slice
-        f32x4 acc = zero4();
-#pragma unroll
-        for (int m = 0; m < NK; ++m) mma(acc, sfr[vt][m], qf[m]);
-        mma(acc, ld_frag_tr_acc(sV + vl, LDV), pf0);
-        if (I >= 2) mma(acc, ld_frag_tr_acc(sV + 32 * LDV + vl, LDV), pf1);  // keys 32..63 precede row i
+        mma(acc[vt], ld_frag_tr_acc(sV + vl, LDV), pf0);
+        if (I >= 2) mma(acc[vt], ld_frag_tr_acc(sV + 32 * LDV + vl, LDV), pf1);  // keys 32..63 precede row i
         if (i < nrow)
-          store4(o + tok_off(b, r0 + i, h, a.T, a.H, a.dv) + vp + vl + 4 * g4, a.scale * acc[0],
-                 a.scale * acc[1], a.scale * acc[2], a.scale * acc[3]);
+          store4(o + tok_off(b, r0 + i, h, a.T, a.H, a.dv) + vp + vl + 4 * g4, a.scale * acc[vt][0],
+                 a.scale * acc[vt][1], a.scale * acc[vt][2], a.scale * acc[vt][3]);
       }
     }
   }
