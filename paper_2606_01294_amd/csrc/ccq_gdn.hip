@@ -38,9 +38,13 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
   constexpr int P = Pad<T>::value;
   constexpr int LDQ = DK + P;
   constexpr int LDA = C + 4;  // fp32 pitch of A and X
-  __shared__ __align__(16) T sK[C * LDQ];
-  __shared__ __align__(16) float sA[C * LDA];
-  __shared__ __align__(16) float sX[C * LDA];
+  // K is dead once A is formed: A and X (fp32) then take its space, which lets
+  // four workgroups share a compute unit
+  constexpr int kKBytes = C * LDQ * (int)sizeof(T), kAXBytes = 2 * C * LDA * 4;
+  __shared__ __align__(16) char sKAX[kKBytes > kAXBytes ? kKBytes : kAXBytes];
+  T* const sK = reinterpret_cast<T*>(sKAX);
+  float* const sA = reinterpret_cast<float*>(sKAX);
+  float* const sX = sA + C * LDA;
   __shared__ __align__(16) float sY[4][16 * 17];
   __shared__ __align__(16) float sGam[C], sBeta[C];
 
@@ -53,20 +57,24 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
   const int tid = threadIdx.x, w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
 
-  {
-    RowTile<T, DK> rk;
-    rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
-    rk.store(sK, LDQ);
-  }
+  // all global loads first (K, the log decays and beta), one round trip
+  RowTile<T, DK> rk;
+  rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+  float la = 0.f, bt = 0.f;
   if (tid < C) {
     const size_t ti = ((size_t)b * a.T + r0 + (tid < nrow ? tid : nrow - 1)) * a.H + h;
-    float x = tid < nrow ? a.logalpha[ti] : 0.f;
+    la = a.logalpha[ti];
+    bt = a.beta[ti];
+  }
+  rk.store(sK, LDQ);
+  if (tid < C) {
+    float x = tid < nrow ? la : 0.f;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
       const float y = __shfl_up(x, off);
       if (tid >= off) x += y;
     }
-    const float bt = tid < nrow ? a.beta[ti] : 0.f;
+    bt = tid < nrow ? bt : 0.f;
     const float gC = __shfl(x, C - 1);
     sGam[tid] = x;
     sBeta[tid] = bt;
@@ -79,15 +87,20 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
   }
   __syncthreads();
 
-  // A (strictly lower), row tile w
+  // A (strictly lower), row tile w; written once every wave is done with K
+  f32x4 acc[4];
 #pragma unroll
   for (int J = 0; J < 4; ++J) {
-    f32x4 acc = zero4();
-    if (J <= w) tile_mma<T, DK>(acc, sK + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+    acc[J] = zero4();
+    if (J <= w) tile_mma<T, DK>(acc[J], sK + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int J = 0; J < 4; ++J) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int i = 16 * w + 4 * g4 + r, j = 16 * J + c16;
-      sA[i * LDA + j] = j < i ? sBeta[i] * __expf(sGam[i] - sGam[j]) * acc[r] : 0.f;
+      sA[i * LDA + j] = j < i ? sBeta[i] * __expf(sGam[i] - sGam[j]) * acc[J][r] : 0.f;
     }
   }
   __syncthreads();
