@@ -32,6 +32,13 @@ PEAK_FP32_TFLOPS = 157.3
 CHUNK = 64
 
 
+def gla_seg(bh: int, nc: int, dk: int, dv: int) -> int:
+    """Chunks per segment of the GLA state pass (the library's policy; 0 = one
+    segment): segments only when the unsegmented pass leaves SIMDs idle."""
+    waves = bh * (dk // 64) * (dv // 64) * 4
+    return 8 if (waves < 1024 and nc > 8) else 0
+
+
 def clean_seg(bh: int, nc: int) -> int:
     """Chunks per segment of the query contraction (the library's policy: the
     longest of 8, 4, 2 that still gives every compute unit a workgroup)."""
@@ -49,6 +56,10 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     dk, dv, C = w.dk, w.dv, CHUNK
     NC = -(-w.T // C)
     NS = -(-NC // clean_seg(BH, NC))
+    gs = gla_seg(BH, NC, dk, dv)
+    GS = -(-NC // gs) if gs else 1   # segments of the GLA state pass
+    if kernel in ("gla_state", "gla_out") and getattr(w, "train", False):
+        GS = 1
     stats = BH * NS * dk * dk               # elements of the segment statistics
     if kernel == "clean_gram":      # k in; segment Gram (fp32), chunk and segment key sums out
         by = ntok * dk * io_bytes + stats * 4 + BH * (NC + NS) * dk * 4
@@ -64,12 +75,16 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
         elif kernel == "clean_dq":
             by += ntok * (4 * dk + 4)
         fl = ntok * (2 * dk * dk + 4 * C * dk)
-    elif kernel == "gla_state":     # k, g, v in; chunk-entry states and final state out
+    elif kernel == "gla_state":     # k, g, v in; chunk-entry (segment-local) states, segment totals out
         by = ntok * (dk * io_bytes + dk * gate_bytes + dv * io_bytes + dv * dk * io_bytes // C) \
-            + BH * dv * dk * 4
+            + BH * GS * dv * dk * 4 + (BH * (GS + NC) * dk * 4 if GS > 1 else 0)
         fl = ntok * (2 * dk * dv)
-    elif kernel == "gla_out":       # q_clean, k, g, v, chunk states in; o out
-        by = ntok * (2 * dk * io_bytes + dk * gate_bytes + 2 * dv * io_bytes + dv * dk * io_bytes // C)
+    elif kernel == "gla_scan":      # segment totals in; segment entry states and final state out
+        by = BH * GS * (dv * dk * 4 + dk * 4) + BH * (GS - 1) * dv * dk * io_bytes + BH * dv * dk * 4
+        fl = BH * GS * dv * dk * 2
+    elif kernel == "gla_out":       # q_clean, k, g, v, chunk states, segment entry states in; o out
+        by = ntok * (2 * dk * io_bytes + dk * gate_bytes + 2 * dv * io_bytes + dv * dk * io_bytes // C) \
+            + (BH * (GS - 1) * dv * dk * io_bytes + BH * NC * dk * 4 if GS > 1 else 0)
         fl = ntok * (2 * C * dk + 2 * dk * dv + 2 * C * dv)
     elif kernel == "gdn_tri":       # k, log alpha, beta in; chunk transforms Tm and decays out
         by = ntok * (dk * io_bytes + 8 + C * io_bytes + 4)
@@ -101,13 +116,14 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
 
 CLEAN = ["clean_gram", "clean_prefix"]
 KERNELS = {0: ["gla_state"] + CLEAN + ["clean_out", "gla_out"],
+           "gla_seg": ["gla_state", "gla_scan"] + CLEAN + ["clean_out", "gla_out"],
            1: ["gdn_tri", "gdn_state"] + CLEAN + ["clean_out", "gdn_out"],
            "train": CLEAN + ["clean_out_train", "gla_state", "gla_out", "gla_dstate",
                              "gla_bwd_chunk", "gla_dg", "clean_dq", "ccq_dk"]}
 KERNEL_SYMBOL = {"clean_gram": "clean_gram_kernel",
                  "clean_prefix": "clean_prefix_kernel", "clean_out": "clean_out_kernel",
                  "clean_out_train": "clean_out_kernel", "clean_dq": "clean_out_kernel",
-                 "gla_state": "gla_state_kernel", "gla_out": "gla_out_kernel",
+                 "gla_state": "gla_state_kernel", "gla_scan": "gla_scan_kernel", "gla_out": "gla_out_kernel",
                  "gdn_tri": "gdn_tri_kernel", "gdn_state": "gdn_state_dma_kernel",
                  "gdn_out": "gdn_out_kernel", "gla_dstate": "gla_dstate_kernel",
                  "gla_bwd_chunk": "gla_bwd_chunk_kernel", "gla_dg": "gla_dg_kernel",
@@ -117,7 +133,7 @@ KERNEL_SYMBOL = {"clean_gram": "clean_gram_kernel",
 def _source(kernel: str) -> str:
     if kernel.startswith("clean"):
         return "ccq_clean.hip"
-    if kernel in ("gla_state", "gla_out"):
+    if kernel in ("gla_state", "gla_scan", "gla_out"):
         return "ccq_gla.hip"
     if kernel.startswith("gdn"):
         return "ccq_gdn.hip"
@@ -173,7 +189,12 @@ class Call:
                 self.out[name] = torch.empty_like(self.d[ref])
             self.out["dlam"] = torch.empty_like(self.d["lam"])
         self.ccq = ccq
-        self.kernels = KERNELS["train" if w.train else w.backbone]
+        if w.train:
+            self.kernels = KERNELS["train"]
+        elif w.backbone == 0 and gla_seg(B * H, -(-T // CHUNK), dk, dv):
+            self.kernels = KERNELS["gla_seg"]   # the state pass in segments adds a scan
+        else:
+            self.kernels = KERNELS[w.backbone]
 
     def __call__(self):
         d = self.d

@@ -145,6 +145,8 @@ hipError_t run_clean_stats(const ccq::CleanArgs& a, bool bf, hipStream_t st) {
 
 struct FwdLayout {
   size_t qclean = 0, states = 0, Tm = 0, gam = 0, U = 0, total = 0;
+  size_t segsum = 0, segdec = 0, cdec = 0, entries = 0;  // GLA state pass in segments
+  int gla_seg = 0;
   CleanWs clean;
 };
 
@@ -160,6 +162,17 @@ FwdLayout fwd_layout(const ccq_shape* s, ccq_backbone bb) {
   L.qclean = take(ntok * s->dk * e);
   L.states = take(nchunk * s->dv * s->dk * e);
   L.clean = take_clean_ws(s, take);
+  if (bb == CCQ_GLA) {
+    const long long nc = (s->T + 63) / 64;
+    L.gla_seg = ccq::gla_seg((long long)s->B * s->H, nc, s->dk, s->dv);
+    if (L.gla_seg > 0) {
+      const size_t bh = (size_t)s->B * s->H, ns = (nc + L.gla_seg - 1) / L.gla_seg;
+      L.segsum = take(bh * ns * s->dv * s->dk * sizeof(float));
+      L.segdec = take(bh * ns * s->dk * sizeof(float));
+      L.cdec = take(nchunk * s->dk * sizeof(float));
+      L.entries = take(bh * ns * s->dv * s->dk * e);
+    }
+  }
   if (bb == CCQ_GDN) {
     L.Tm = take(nchunk * 64 * 64 * e);
     L.gam = take(nchunk * 5 * 64 * sizeof(float));
@@ -245,8 +258,23 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   float* gam = reinterpret_cast<float*>(ws + L.gam);
   const bool gbf = s->gate_dtype == CCQ_BF16;
   if (bb == CCQ_GLA) {
+    // segments of the state pass run in parallel; a scan over the segment
+    // totals gives every segment's entry state and S_T
     ccq::GlaStateArgs sa{k, v, g_or_la, S0, ST, ws + L.states, s->B, s->T, s->H, s->dk, s->dv};
+    if (L.gla_seg > 0) {
+      sa.seg = L.gla_seg;
+      sa.ST = nullptr;
+      sa.segsum = reinterpret_cast<float*>(ws + L.segsum);
+      sa.segdec = reinterpret_cast<float*>(ws + L.segdec);
+      sa.cdec = reinterpret_cast<float*>(ws + L.cdec);
+    }
     if (traced(ss, [&] { return ccq::launch_gla_state(sa, bf, gbf, ss); }) != hipSuccess) return CCQ_ERR_HIP;
+    if (L.gla_seg > 0) {
+      const int nc = (s->T + 63) / 64;
+      ccq::GlaScanArgs ga{sa.segsum, sa.segdec, ws + L.entries, ST, s->B, s->H, s->dk, s->dv,
+                          (nc + L.gla_seg - 1) / L.gla_seg};
+      if (traced(ss, [&] { return ccq::launch_gla_scan(ga, bf, ss); }) != hipSuccess) return CCQ_ERR_HIP;
+    }
   } else {
     ccq::TriArgs ta{k, la, beta, ws + L.Tm, gam, s->B, s->T, s->H, s->dk, s->dv};
     if (traced(ss, [&] { return ccq::launch_gdn_tri(ta, bf, ss); }) != hipSuccess) return CCQ_ERR_HIP;
@@ -273,6 +301,11 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   if (join_from(*sd, st) != hipSuccess) return CCQ_ERR_HIP;
   if (bb == CCQ_GLA) {
     ccq::GlaOutArgs oa{qclean, k, v, g_or_la, ws + L.states, o, s->B, s->T, s->H, s->dk, s->dv, s->scale};
+    if (L.gla_seg > 0) {
+      oa.seg = L.gla_seg;
+      oa.entries = ws + L.entries;
+      oa.cdec = reinterpret_cast<const float*>(ws + L.cdec);
+    }
     if (traced(st, [&] { return ccq::launch_gla_out(oa, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   } else {
     ccq::GdnOutArgs oa{qclean, k, gam, ws + L.states, ws + L.U, o, s->B, s->T, s->H, s->dk, s->dv,

@@ -42,9 +42,11 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
 
   const int nkt = a.dk / BK, nvt = a.dv / VB;
   const int N = (a.T + C - 1) / C;
+  const int SL = a.seg > 0 ? a.seg : N, NS = (N + SL - 1) / SL;  // segment length and count
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int bh = lb / (nkt * nvt), kt = (lb / nvt) % nkt, vt = lb % nvt;
+  const int vt = lb % nvt, kt = (lb / nvt) % nkt, sg = (lb / (nvt * nkt)) % NS, bh = lb / (nvt * nkt * NS);
   const int c0 = kt * BK, v0 = vt * VB;
+  const int cb = sg * SL, ce = min(N, cb + SL);  // this segment's chunks
   const int b = bh / a.H, h = bh % a.H;
   const int w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
@@ -57,8 +59,9 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
 #pragma unroll
   for (int tv = 0; tv < NVT; ++tv) {
     const int vv = v0 + 16 * tv + c16;
-    S[tv] = a.S0 ? *reinterpret_cast<const f32x4*>(a.S0 + ((size_t)bh * a.dv + vv) * a.dk + c0 + 16 * w + 4 * g4)
-                 : zero4();
+    S[tv] = (a.S0 && sg == 0)
+                ? *reinterpret_cast<const f32x4*>(a.S0 + ((size_t)bh * a.dv + vv) * a.dk + c0 + 16 * w + 4 * g4)
+                : zero4();
   }
 
   RowTile<T, BK> rk;
@@ -78,15 +81,16 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
     for (int tv = 0; tv < NVT; ++tv)
       store4(st + (size_t)(16 * tv + c16) * a.dk, Sr[tv][0], Sr[tv][1], Sr[tv][2], Sr[tv][3]);
   };
-  if (N > 0) prefetch(0);
+  if (cb < ce) prefetch(cb);
+  float le = 0.f;  // log decay of this lane's channel since the segment began
 
-  for (int ci = 0; ci < N; ++ci) {
-    const int buf = ci & 1;  // the other buffer was released at the previous barrier
+  for (int ci = cb; ci < ce; ++ci) {
+    const int buf = (ci - cb) & 1;  // the other buffer was released at the previous barrier
     rk.store(sK[buf], LDK);
     rg.store(sG[buf], LDG);
     rv.store(sV[buf], LDV);
-    if (ci > 0) write_back(ci - 1);
-    if (ci + 1 < N) prefetch(ci + 1);
+    if (ci > cb) write_back(ci - 1);
+    if (ci + 1 < ce) prefetch(ci + 1);
 #pragma unroll
     for (int tv = 0; tv < NVT; ++tv) Sr[tv] = S[tv];
     __syncthreads();
@@ -115,6 +119,8 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
       half[m] = __shfl(sc, 48 + c16);
     }
     const float bC = half[0] + half[1];
+    if (a.cdec && vt == 0 && g4 == 0) a.cdec[((size_t)bh * N + ci) * a.dk + c0 + 16 * w + c16] = __expf(le);
+    le += bC;
     Frag<T> kd0, kd1;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -134,14 +140,39 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
     }
   }
 
-  if (N > 0) write_back(N - 1);
-  if (a.ST) {
+  if (cb < ce) write_back(ce - 1);
+  // the segment's total: the local state at its end and its decay (or, with
+  // one segment, the final state)
+  float* out = a.segsum ? a.segsum + ((size_t)bh * NS + sg) * a.dv * a.dk
+                        : (a.ST ? a.ST + (size_t)bh * a.dv * a.dk : nullptr);  // one segment: sg = 0
+  if (out) {
 #pragma unroll
     for (int tv = 0; tv < NVT; ++tv) {
       const int vv = v0 + 16 * tv + c16;
-      *reinterpret_cast<f32x4*>(a.ST + ((size_t)bh * a.dv + vv) * a.dk + c0 + 16 * w + 4 * g4) = S[tv];
+      *reinterpret_cast<f32x4*>(out + (size_t)vv * a.dk + c0 + 16 * w + 4 * g4) = S[tv];
     }
   }
+  if (a.segdec && vt == 0 && g4 == 0) a.segdec[((size_t)bh * NS + sg) * a.dk + c0 + 16 * w + c16] = __expf(le);
+}
+
+// Entry state of every segment of the GLA state pass, four elements per
+// thread: E_0 = 0, E_{j+1} = E_j diag(segdec_j) + segsum_j, S_T = E_NS.
+template <typename T>
+__global__ __launch_bounds__(256) void gla_scan_kernel(const GlaScanArgs a) {
+  const size_t DD = (size_t)a.dv * a.dk;
+  const size_t e4 = ((size_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (e4 >= (size_t)a.B * a.H * DD) return;
+  const size_t bh = e4 / DD, el = e4 % DD;
+  const int c = (int)(el % a.dk);
+  f32x4 x = zero4();
+  for (int j = 0; j < a.NS; ++j) {
+    const size_t so = bh * a.NS + j;
+    if (j > 0) store4(static_cast<T*>(a.entries) + so * DD + el, x[0], x[1], x[2], x[3]);
+    const f32x4 d = *reinterpret_cast<const f32x4*>(a.segdec + so * a.dk + c);
+    const f32x4 s = *reinterpret_cast<const f32x4*>(a.segsum + so * DD + el);
+    x = x * d + s;
+  }
+  if (a.ST) *reinterpret_cast<f32x4*>(a.ST + bh * DD + el) = x;
 }
 
 // Outputs of one chunk (eight waves), all value columns:
@@ -172,7 +203,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
   float* sB = reinterpret_cast<float*>(sBPV);     // gates, then their prefix b
   T* sP = reinterpret_cast<T*>(sBPV);             // masked scores, once sB is dead
   T* sV = reinterpret_cast<T*>(sBPV + kPBytes);   // V slice, once sB is dead
-  __shared__ __align__(16) float sBm[DK];
+  __shared__ __align__(16) float sBm[DK], sBe[DK];  // e^{b_m}; the same times the decay since the segment began
   __shared__ float sTot[TPC][DK];
 
   const int N = (a.T + C - 1) / C;
@@ -185,6 +216,10 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
   const int g4 = l >> 4, c16 = l & 15;
   const int vg = w % NVG, ig = w / NVG;
   const size_t gstride = (size_t)a.H * DK;
+  // past the first segment of the state pass, S_r = local state + the
+  // segment's entry state decayed to this chunk (per key channel)
+  const int sg = a.seg > 0 ? ci / a.seg : 0;
+  const bool ent = sg > 0 && a.entries;
 
   RowTile<T, DK, NT> rq, rk;
   RowTile<TG, DK, NT> rg;
@@ -214,7 +249,11 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
       if (p2 < part) off += sTot[p2][c];
 #pragma unroll
     for (int j = 0; j < TOK; ++j) sB[(j0 + j) * LDB + c] = x[j] + off;
-    if (j0 <= C / 2 - 1 && C / 2 - 1 < j0 + TOK) sBm[c] = __expf(x[C / 2 - 1 - j0] + off);
+    if (j0 <= C / 2 - 1 && C / 2 - 1 < j0 + TOK) {
+      const float bm = __expf(x[C / 2 - 1 - j0] + off);
+      sBm[c] = bm;
+      if (ent) sBe[c] = bm * a.cdec[((size_t)bh * N + ci) * DK + c];
+    }
   }
   __syncthreads();
   // Qt = q e^{b - b_m}, Kt = k e^{b_m - b}
@@ -251,6 +290,8 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
   }
 
   const T* Sg = static_cast<const T*>(a.states) + ((size_t)bh * N + ci) * a.dv * DK;
+  const int NS = a.seg > 0 ? (N + a.seg - 1) / a.seg : 1;
+  const T* Eg = ent ? static_cast<const T*>(a.entries) + ((size_t)bh * NS + sg) * a.dv * DK : nullptr;
   T* o = static_cast<T*>(a.o);
   for (int vp = 0; vp < a.dv; vp += VP) {
     if (vp > 0) __syncthreads();  // every wave is done with the previous V slice
@@ -269,7 +310,14 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
         Frag<T> f = ld_frag_global(Sg + (size_t)vr * DK + 32 * m, (size_t)DK);
         const f32x4 e0 = *reinterpret_cast<const f32x4*>(sBm + 32 * m + 8 * g4);
         const f32x4 e1 = *reinterpret_cast<const f32x4*>(sBm + 32 * m + 8 * g4 + 4);
-        if constexpr (sizeof(T) == 2) {
+        if (ent) {
+          const Frag<T> fe = ld_frag_global(Eg + (size_t)vr * DK + 32 * m, (size_t)DK);
+          const f32x4 d0 = *reinterpret_cast<const f32x4*>(sBe + 32 * m + 8 * g4);
+          const f32x4 d1 = *reinterpret_cast<const f32x4*>(sBe + 32 * m + 8 * g4 + 4);
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            set_frag_elem(f, e, frag_elem(f, e) * (e < 4 ? e0[e] : e1[e - 4]) + frag_elem(fe, e) * (e < 4 ? d0[e] : d1[e - 4]));
+        } else if constexpr (sizeof(T) == 2) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) f.v[e] = to<T>(f32(f.v[e]) * (e < 4 ? e0[e] : e1[e - 4]));
         } else {
@@ -310,9 +358,13 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
 }
 
 namespace {
+int gla_nseg(const GlaStateArgs& a) {
+  const int N = (a.T + kChunk - 1) / kChunk;
+  return a.seg > 0 ? (N + a.seg - 1) / a.seg : 1;
+}
 template <typename T, typename TG, int NVT>
 hipError_t run_gla_state_v(const GlaStateArgs& a, hipStream_t st) {
-  const int nblk = a.B * a.H * (a.dk / 64) * (a.dv / (16 * NVT));
+  const int nblk = a.B * a.H * (a.dk / 64) * (a.dv / (16 * NVT)) * gla_nseg(a);
   if (nblk == 0) return hipSuccess;
   hipLaunchKernelGGL((gla_state_kernel<T, TG, NVT>), dim3(nblk), dim3(kThreads), 0, st, a);
   return hipGetLastError();
@@ -320,7 +372,7 @@ hipError_t run_gla_state_v(const GlaStateArgs& a, hipStream_t st) {
 // 64-wide value slices when they still give every SIMD a wave, else 32 or 16.
 template <typename T, typename TG>
 hipError_t run_gla_state(const GlaStateArgs& a, hipStream_t st) {
-  const long long waves64 = (long long)a.B * a.H * (a.dk / 64) * (a.dv / 64) * 4;
+  const long long waves64 = (long long)a.B * a.H * (a.dk / 64) * (a.dv / 64) * 4 * gla_nseg(a);
   if (waves64 >= 1024) return run_gla_state_v<T, TG, 4>(a, st);
   if (waves64 * 2 >= 1024) return run_gla_state_v<T, TG, 2>(a, st);
   return run_gla_state_v<T, TG, 1>(a, st);
@@ -361,6 +413,15 @@ bool gla_supported(int dk, int dv, bool is_bf16) {
 hipError_t launch_gla_state(const GlaStateArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st) {
   if (is_bf16) return gate_bf16 ? run_gla_state<bf16_t, bf16_t>(a, st) : run_gla_state<bf16_t, float>(a, st);
   return gate_bf16 ? run_gla_state<float, bf16_t>(a, st) : run_gla_state<float, float>(a, st);
+}
+
+hipError_t launch_gla_scan(const GlaScanArgs& a, bool is_bf16, hipStream_t st) {
+  const long long n4 = (long long)a.B * a.H * a.dv * a.dk / 4;
+  if (n4 == 0) return hipSuccess;
+  const unsigned nblk = (unsigned)((n4 + 255) / 256);
+  if (is_bf16) hipLaunchKernelGGL((gla_scan_kernel<bf16_t>), dim3(nblk), dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((gla_scan_kernel<float>), dim3(nblk), dim3(256), 0, st, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_gla_out(const GlaOutArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st) {

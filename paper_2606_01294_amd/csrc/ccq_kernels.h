@@ -46,16 +46,37 @@ struct CleanArgs {
   int64_t t0;
 };
 
-// GLA state recurrence (sequential over chunks) for one 64x64 tile of S:
-// writes the chunk-entry states S_r of every chunk.
+// GLA state recurrence (sequential over chunks) for one 64-channel tile of S.
+// The chunks are cut into segments of `seg` (0: one segment); every segment
+// starts from zero (the first from S0), so the segments run in parallel, and
+// its chunk-entry states are the contributions of its own earlier chunks.
+// With one segment they are the chunk-entry states S_r themselves.  Because
+// the GLA transition is diagonal, the true S_r is the local state plus the
+// segment's entry state scaled per key channel by the decay since the
+// segment began (cdec); gla_scan forms the entry states from the segment
+// totals (segsum, segdec).
 struct GlaStateArgs {
   const void* k;      // [B,T,H,dk] io
   const void* v;      // [B,T,H,dv] io
   const void* g;      // [B,T,H,dk] gate dtype
   const float* S0;    // [B,H,dv,dk] or null
-  float* ST;          // [B,H,dv,dk] or null
-  void* states;       // [B*H, N, dv, dk] io
+  float* ST;          // [B,H,dv,dk] or null (one segment only)
+  void* states;       // [B*H, N, dv, dk] io: chunk-entry local states
   int B, T, H, dk, dv;
+  int seg;            // chunks per segment, 0 = all
+  float* segsum;      // [B*H, NS, dv, dk] fp32: local state at each segment's end (NS > 1)
+  float* segdec;      // [B*H, NS, dk] fp32: e^{sum of the segment's log decays}
+  float* cdec;        // [B*H, N, dk] fp32: e^{log decays of the segment before each chunk}
+};
+
+// Entry state of every segment, E_0 = 0 (S0 is inside segment 0's states),
+// E_{j+1} = E_j diag(segdec_j) + segsum_j; the last one gives S_T.
+struct GlaScanArgs {
+  const float* segsum;
+  const float* segdec;
+  void* entries;      // [B*H, NS, dv, dk] io (segment 0 unused)
+  float* ST;          // [B,H,dv,dk] or null
+  int B, H, dk, dv, NS;
 };
 
 // GLA output, one workgroup per (chunk, 64-wide value slice).
@@ -68,6 +89,9 @@ struct GlaOutArgs {
   void* o;            // [B,T,H,dv] io
   int B, T, H, dk, dv;
   float scale;
+  int seg;              // chunks per segment of the state pass (0 = one segment)
+  const void* entries;  // [B*H, NS, dv, dk] io, or null with one segment
+  const float* cdec;    // [B*H, N, dk] fp32, or null with one segment
 };
 
 // Gated DeltaNet chunk transform (chunk-parallel): Tm = (I + A)^{-1} and the
@@ -176,6 +200,14 @@ inline int clean_seg(long long bh, long long nc) {
 }
 hipError_t launch_gla_state(const GlaStateArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
 hipError_t launch_gla_out(const GlaOutArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
+hipError_t launch_gla_scan(const GlaScanArgs& a, bool is_bf16, hipStream_t st);
+// Chunks per segment of the GLA state pass (0: one segment) for bh heads of
+// nc chunks: segments only when the unsegmented pass (four waves per 64 x 64
+// tile of S) would not give every SIMD of the chip a wave.
+inline int gla_seg(long long bh, long long nc, int dk, int dv) {
+  const long long waves = bh * (dk / 64) * (dv / 64) * 4;
+  return (waves < 1024 && nc > 8) ? 8 : 0;
+}
 hipError_t launch_gdn_tri(const TriArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_gdn_state(const GdnArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_gdn_out(const GdnOutArgs& a, bool is_bf16, hipStream_t st);

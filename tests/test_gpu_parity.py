@@ -53,6 +53,28 @@ def test_gla_parity_small(case):
     compare(GLA, d, dtype)
 
 
+# More than 8 chunks with few heads: the GLA state pass runs in segments of 8
+# chunks (the last one short and ending in a ragged chunk), joined by the
+# segment scan; with an initial state, which enters segment 0 only.
+GLA_SEG_CASES = [
+    # dtype, B, T, H, dk, dv, gate dtype
+    (F32, 1, 600, 2, 64, 64, F32),
+    (BF16, 2, 1100, 1, 128, 256, BF16),
+    (BF16, 1, 530, 2, 64, 512, F32),
+]
+
+
+@pytest.mark.parametrize("case", GLA_SEG_CASES, ids=lambda c: "%s-T%d-dk%d-dv%d" % (
+    str(c[0]).split(".")[-1], c[2], c[4], c[5]))
+def test_gla_parity_segments(case):
+    dtype, B, T, H, dk, dv, gdt = case
+    say("gla segments", case)
+    d = make_inputs(GLA, B, T, H, dk, dv, dtype, gate_dtype=gdt, seed=400 + T, keys="aniso",
+                    lam="random")
+    S0 = np.random.default_rng(T).standard_normal((B, H, dv, dk)) * 0.2
+    compare(GLA, d, dtype, S0=S0.astype(np.float32).astype(np.float64))
+
+
 GDN_CASES = [
     (F32, 1, 200, 2, 64, 64, "iso", "const"),
     (F32, 1, 130, 2, 128, 256, "aniso", "random"),
