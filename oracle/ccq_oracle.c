@@ -24,8 +24,8 @@
  *           applied after the product");
  *   form 1: Alg. 2 (recurrent inference), running-mean updates of Cbar, mu;
  *   chunk : Alg. 1 (chunkwise forward), with the backbone's chunk forms.
- * and one reverse pass (GLA + CCQ), recomputing each 64-token segment from
- * checkpointed states.
+ * and two reverse passes (GLA + CCQ, Gated DeltaNet + CCQ), recomputing each
+ * segment from checkpointed states.
  *
  * Readings where the paper is silent or garbled (each also recorded in the
  * design notes):
@@ -593,6 +593,195 @@ int ccq_oracle_gla_fwd_bwd(const ccq_oracle_shape* s, int seg, const double* q, 
     }
     free(ckS); free(ckK); free(ckm); free(segS); free(segK); free(segm); free(segc); free(segqc);
     free(S); free(K); free(m); free(dS); free(dK); free(dm); free(dqc); free(dc);
+  }
+  return err;
+}
+
+/*
+ * Reverse pass of CCQ-Gated DeltaNet for L = sum_t <dO_t, o_t> (fresh start:
+ * zero initial states, t0 = 0).  The contraction part is the one of the GLA
+ * reverse pass above; the backbone write is
+ *   y_t = S_{t-1} k_t,   S_t = a_t S_{t-1} - a_t b_t y_t k_t^T + b_t v_t k_t^T
+ * (a_t = e^{logalpha_t}, b_t = beta_t; the cited Gated DeltaNet recurrence).
+ * With dS the adjoint of S_t (after this token's read) and z = dS k_t:
+ *   dv_t        = b_t z
+ *   dbeta_t     = z . (v_t - a_t y_t)
+ *   dlogalpha_t = a_t (<dS, S_{t-1}> - b_t z . y_t)
+ *   dk_t       += b_t dS^T (v_t - a_t y_t) - a_t b_t S_{t-1}^T z
+ *   dS         <- a_t (dS - b_t z k_t^T)          (adjoint of S_{t-1})
+ * States are checkpointed every `seg` tokens and each segment is recomputed
+ * forward before its reverse.
+ */
+int ccq_oracle_gdn_fwd_bwd(const ccq_oracle_shape* s, int seg, const double* q, const double* k,
+                           const double* v, const double* logalpha, const double* beta,
+                           const double* lam, const double* dO, double* o, double* dq,
+                           double* dk_out, double* dv_out, double* dlogalpha, double* dbeta,
+                           double* dlam) {
+  if (!s || seg <= 0 || s->backbone != 1 || s->t0 != 0 || s->B < 0 || s->T < 0 || s->H < 0 ||
+      s->dk <= 0 || s->dv <= 0)
+    return 1;
+  const int B = s->B, T = s->T, H = s->H, dk = s->dk, dv = s->dv;
+  const int nseg = (T + seg - 1) / seg;
+  int err = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int bh = 0; bh < B * H; ++bh) {
+    const int b = bh / H, h = bh % H;
+    const size_t SZ = (size_t)dv * dk, KZ = (size_t)dk * dk;
+    double* ckS = malloc(sizeof(double) * SZ * (nseg > 0 ? nseg : 1));
+    double* ckK = malloc(sizeof(double) * KZ * (nseg > 0 ? nseg : 1));
+    double* ckm = malloc(sizeof(double) * dk * (nseg > 0 ? nseg : 1));
+    double* segS = malloc(sizeof(double) * SZ * (seg + 1));
+    double* segK = malloc(sizeof(double) * KZ * seg);
+    double* segm = malloc(sizeof(double) * dk * seg);
+    double* segc = malloc(sizeof(double) * dk * seg);
+    double* segqc = malloc(sizeof(double) * dk * seg);
+    double* S = malloc(sizeof(double) * SZ);
+    double* K = malloc(sizeof(double) * KZ);
+    double* m = malloc(sizeof(double) * dk);
+    double* dS = malloc(sizeof(double) * SZ);
+    double* dK = malloc(sizeof(double) * KZ);
+    double* dm = malloc(sizeof(double) * dk);
+    double* dqc = malloc(sizeof(double) * dk);
+    double* dc = malloc(sizeof(double) * dk);
+    double* y = malloc(sizeof(double) * dv);
+    double* z = malloc(sizeof(double) * dv);
+    if (!ckS || !ckK || !ckm || !segS || !segK || !segm || !segc || !segqc || !S || !K || !m ||
+        !dS || !dK || !dm || !dqc || !dc || !y || !z) {
+#pragma omp atomic write
+      err = 2;
+    } else {
+      memset(S, 0, sizeof(double) * SZ);
+      memset(K, 0, sizeof(double) * KZ);
+      memset(m, 0, sizeof(double) * dk);
+      /* forward sweep: checkpoints and o */
+      for (int t = 0; t < T; ++t) {
+        if (t % seg == 0) {
+          memcpy(ckS + (size_t)(t / seg) * SZ, S, sizeof(double) * SZ);
+          memcpy(ckK + (size_t)(t / seg) * KZ, K, sizeof(double) * KZ);
+          memcpy(ckm + (size_t)(t / seg) * dk, m, sizeof(double) * dk);
+        }
+        const size_t ti = tok(s, b, t, h);
+        const double *kt = k + ti * dk, *qt = q + ti * dk, *vt = v + ti * dv;
+        const double tau = t + 1.0;
+        for (int a = 0; a < dk; ++a)
+          for (int bb = 0; bb < dk; ++bb) K[a * dk + bb] += kt[a] * kt[bb];
+        for (int a = 0; a < dk; ++a) m[a] += kt[a];
+        double mq = 0.0;
+        for (int a = 0; a < dk; ++a) mq += m[a] * qt[a];
+        for (int a = 0; a < dk; ++a) {
+          double acc = 0.0;
+          for (int bb = 0; bb < dk; ++bb) acc += K[a * dk + bb] * qt[bb];
+          dqc[a] = qt[a] - lam[ti] * (acc / tau - (s->centered ? m[a] * mq / (tau * tau) : 0.0));
+        }
+        backbone_write(s, S, kt, vt, NULL, logalpha[ti], beta[ti], y);
+        for (int r = 0; r < dv; ++r) {
+          double acc = 0.0;
+          for (int a = 0; a < dk; ++a) acc += S[r * dk + a] * dqc[a];
+          o[ti * dv + r] = s->scale * acc;
+        }
+      }
+      memset(dS, 0, sizeof(double) * SZ);
+      memset(dK, 0, sizeof(double) * KZ);
+      memset(dm, 0, sizeof(double) * dk);
+      for (int sg = nseg - 1; sg >= 0; --sg) {
+        const int start = sg * seg;
+        const int end = (start + seg) < T ? (start + seg) : T;
+        memcpy(segS, ckS + (size_t)sg * SZ, sizeof(double) * SZ);
+        memcpy(K, ckK + (size_t)sg * KZ, sizeof(double) * KZ);
+        memcpy(m, ckm + (size_t)sg * dk, sizeof(double) * dk);
+        for (int t = start; t < end; ++t) {
+          const int lt = t - start;
+          const size_t ti = tok(s, b, t, h);
+          const double *kt = k + ti * dk, *qt = q + ti * dk, *vt = v + ti * dv;
+          const double tau = t + 1.0;
+          for (int a = 0; a < dk; ++a)
+            for (int bb = 0; bb < dk; ++bb) K[a * dk + bb] += kt[a] * kt[bb];
+          for (int a = 0; a < dk; ++a) m[a] += kt[a];
+          memcpy(segK + (size_t)lt * KZ, K, sizeof(double) * KZ);
+          memcpy(segm + (size_t)lt * dk, m, sizeof(double) * dk);
+          double mq = 0.0;
+          for (int a = 0; a < dk; ++a) mq += m[a] * qt[a];
+          for (int a = 0; a < dk; ++a) {
+            double acc = 0.0;
+            for (int bb = 0; bb < dk; ++bb) acc += K[a * dk + bb] * qt[bb];
+            const double c = acc / tau - (s->centered ? m[a] * mq / (tau * tau) : 0.0);
+            segc[(size_t)lt * dk + a] = c;
+            segqc[(size_t)lt * dk + a] = qt[a] - lam[ti] * c;
+          }
+          double* Sn = segS + (size_t)(lt + 1) * SZ;
+          memcpy(Sn, segS + (size_t)lt * SZ, sizeof(double) * SZ);
+          backbone_write(s, Sn, kt, vt, NULL, logalpha[ti], beta[ti], y);
+        }
+        for (int t = end - 1; t >= start; --t) {
+          const int lt = t - start;
+          const size_t ti = tok(s, b, t, h);
+          const double *kt = k + ti * dk, *qt = q + ti * dk, *vt = v + ti * dv;
+          const double* dOt = dO + ti * dv;
+          const double tau = t + 1.0;
+          const double al = exp(logalpha[ti]), bt = beta[ti];
+          const double* St = segS + (size_t)(lt + 1) * SZ;
+          const double* Sprev = segS + (size_t)lt * SZ;
+          const double* Kt = segK + (size_t)lt * KZ;
+          const double* mt = segm + (size_t)lt * dk;
+          const double* ct = segc + (size_t)lt * dk;
+          const double* qct = segqc + (size_t)lt * dk;
+          /* read o_t = scale S_t qc_t */
+          for (int r = 0; r < dv; ++r)
+            for (int a = 0; a < dk; ++a) dS[r * dk + a] += s->scale * dOt[r] * qct[a];
+          for (int a = 0; a < dk; ++a) {
+            double acc = 0.0;
+            for (int r = 0; r < dv; ++r) acc += St[r * dk + a] * dOt[r];
+            dqc[a] = s->scale * acc;
+          }
+          /* contraction qc_t = q_t - lam_t c_t */
+          double dl = 0.0;
+          for (int a = 0; a < dk; ++a) dl -= dqc[a] * ct[a];
+          dlam[ti] = dl;
+          for (int a = 0; a < dk; ++a) dc[a] = -lam[ti] * dqc[a];
+          double mdc = 0.0, mq = 0.0;
+          for (int a = 0; a < dk; ++a) { mdc += mt[a] * dc[a]; mq += mt[a] * qt[a]; }
+          for (int a = 0; a < dk; ++a) {
+            double acc = 0.0;
+            for (int bb = 0; bb < dk; ++bb) acc += Kt[a * dk + bb] * dc[bb];
+            dq[ti * dk + a] = dqc[a] + acc / tau - (s->centered ? mt[a] * mdc / (tau * tau) : 0.0);
+          }
+          for (int a = 0; a < dk; ++a)
+            for (int bb = 0; bb < dk; ++bb) dK[a * dk + bb] += dc[a] * qt[bb] / tau;
+          if (s->centered)
+            for (int a = 0; a < dk; ++a) dm[a] -= (dc[a] * mq + qt[a] * mdc) / (tau * tau);
+          /* backbone write */
+          for (int r = 0; r < dv; ++r) {
+            double ay = 0.0, az = 0.0;
+            for (int a = 0; a < dk; ++a) {
+              ay += Sprev[r * dk + a] * kt[a];
+              az += dS[r * dk + a] * kt[a];
+            }
+            y[r] = ay;
+            z[r] = az;
+          }
+          double db = 0.0, zy = 0.0, dSS = 0.0;
+          for (int r = 0; r < dv; ++r) {
+            dv_out[ti * dv + r] = bt * z[r];
+            db += z[r] * (vt[r] - al * y[r]);
+            zy += z[r] * y[r];
+          }
+          for (size_t i = 0; i < SZ; ++i) dSS += dS[i] * Sprev[i];
+          dbeta[ti] = db;
+          dlogalpha[ti] = al * (dSS - bt * zy);
+          for (int a = 0; a < dk; ++a) {
+            double acc = 0.0;
+            for (int r = 0; r < dv; ++r)
+              acc += bt * dS[r * dk + a] * (vt[r] - al * y[r]) - al * bt * Sprev[r * dk + a] * z[r];
+            for (int bb = 0; bb < dk; ++bb) acc += (dK[a * dk + bb] + dK[bb * dk + a]) * kt[bb];
+            dk_out[ti * dk + a] = acc + dm[a];
+          }
+          for (int r = 0; r < dv; ++r)
+            for (int a = 0; a < dk; ++a) dS[r * dk + a] = al * (dS[r * dk + a] - bt * z[r] * kt[a]);
+        }
+      }
+    }
+    free(ckS); free(ckK); free(ckm); free(segS); free(segK); free(segm); free(segc); free(segqc);
+    free(S); free(K); free(m); free(dS); free(dK); free(dm); free(dqc); free(dc); free(y); free(z);
   }
   return err;
 }

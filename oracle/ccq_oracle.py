@@ -12,6 +12,7 @@ Functions (all arrays are numpy float64, row-major):
   chunk_fwd(...)    Alg. 1 chunkwise forward with the GLA / Gated DeltaNet
                     chunk forms of the backbone update
   gla_fwd_bwd(...)  reverse pass of CCQ-GLA for L = sum <dO, o>
+  gdn_fwd_bwd(...)  reverse pass of CCQ-Gated DeltaNet for L = sum <dO, o>
 """
 from __future__ import annotations
 
@@ -61,7 +62,9 @@ def _load():
             lib.ccq_oracle_fwd.argtypes = [ctypes.POINTER(Shape), ctypes.c_int] + [P] * 14
             lib.ccq_oracle_chunk_fwd.argtypes = [ctypes.POINTER(Shape), ctypes.c_int] + [P] * 14
             lib.ccq_oracle_gla_fwd_bwd.argtypes = [ctypes.POINTER(Shape), ctypes.c_int] + [P] * 12
-            for f in (lib.ccq_oracle_fwd, lib.ccq_oracle_chunk_fwd, lib.ccq_oracle_gla_fwd_bwd):
+            lib.ccq_oracle_gdn_fwd_bwd.argtypes = [ctypes.POINTER(Shape), ctypes.c_int] + [P] * 14
+            for f in (lib.ccq_oracle_fwd, lib.ccq_oracle_chunk_fwd, lib.ccq_oracle_gla_fwd_bwd,
+                      lib.ccq_oracle_gdn_fwd_bwd):
                 f.restype = ctypes.c_int
             lib.ccq_oracle_threads.restype = ctypes.c_int
             _lib = lib
@@ -155,3 +158,23 @@ def gla_fwd_bwd(q, k, v, g, lam, dO, scale=1.0, centered=True, seg=64):
     if rc != 0:
         raise RuntimeError("ccq_oracle_gla_fwd_bwd failed with code %d" % rc)
     return dict(o=o, dq=dq, dk=dk, dv=dv, dg=dg, dlam=dlam)
+
+
+def gdn_fwd_bwd(q, k, v, logalpha, beta, lam, dO, scale=1.0, centered=True, seg=64):
+    """Reverse pass of CCQ-Gated DeltaNet (zero initial state).  Returns o, dq, dk, dv,
+    dlogalpha, dbeta, dlam."""
+    q, k, v, logalpha, beta, lam = _inputs(q, k, v, logalpha, beta, lam, GDN)
+    dO = _f64(dO)
+    assert dO.shape == q.shape[:3] + (v.shape[-1],)
+    o = np.zeros(dO.shape)
+    dq, dk = np.zeros(q.shape), np.zeros(q.shape)
+    dv = np.zeros(v.shape)
+    dla, dbeta, dlam = np.zeros(lam.shape), np.zeros(lam.shape), np.zeros(lam.shape)
+    sh = _shape(q, v, GDN, centered, scale, 0)
+    rc = _load().ccq_oracle_gdn_fwd_bwd(ctypes.byref(sh), int(seg), _ptr(q), _ptr(k), _ptr(v),
+                                        _ptr(logalpha), _ptr(beta), _ptr(lam), _ptr(dO), _ptr(o),
+                                        _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dla), _ptr(dbeta),
+                                        _ptr(dlam))
+    if rc != 0:
+        raise RuntimeError("ccq_oracle_gdn_fwd_bwd failed with code %d" % rc)
+    return dict(o=o, dq=dq, dk=dk, dv=dv, dlogalpha=dla, dbeta=dbeta, dlam=dlam)

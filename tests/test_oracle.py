@@ -352,3 +352,60 @@ def test_reverse_pass_segment_length_does_not_matter():
     b = O.gla_fwd_bwd(d["q"], d["k"], d["v"], d["gate"], d["lam"], dO, seg=7)
     for key in a:
         np.testing.assert_allclose(a[key], b[key], rtol=1e-12, atol=1e-12, err_msg=key)
+
+
+@pytest.mark.parametrize("centered,scale", [(True, 1.0), (False, 0.5)])
+def test_gdn_reverse_pass_matches_finite_differences(centered, scale):
+    """Gated DeltaNet + CCQ: gradients of L = sum <dO, o> from the oracle's reverse pass
+    against central finite differences of the oracle forward, along random directions, at
+    the size of the small fp32 workload (B=1, T=256, H=2, dk=dv=64)."""
+    rng = np.random.default_rng(17)
+    B, T, H, dk, dv = 1, 256, 2, 64, 64
+    d = rnd_inputs(rng, B, T, H, dk, dv, backbone=O.GDN)
+    dO = rng.standard_normal((B, T, H, dv))
+    gr = O.gdn_fwd_bwd(d["q"], d["k"], d["v"], d["gate"], d["beta"], d["lam"], dO, scale=scale,
+                       centered=centered, seg=64)
+    base = run(d, backbone=O.GDN, scale=scale, centered=centered)
+    np.testing.assert_allclose(gr["o"], base["o"], rtol=1e-12, atol=1e-12)
+
+    def loss(dd):
+        return float(np.sum(dO * run(dd, backbone=O.GDN, scale=scale, centered=centered)["o"]))
+
+    h = 1e-5
+    for name, gname in (("q", "dq"), ("k", "dk"), ("v", "dv"), ("gate", "dlogalpha"),
+                        ("beta", "dbeta"), ("lam", "dlam")):
+        e = rng.standard_normal(d[name].shape)
+        dp = dict(d)
+        dm = dict(d)
+        dp[name] = d[name] + h * e
+        dm[name] = d[name] - h * e
+        fd = (loss(dp) - loss(dm)) / (2 * h)
+        an = float(np.sum(gr[gname] * e))
+        assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (name, fd, an)
+
+
+def test_gdn_reverse_pass_segment_length_does_not_matter():
+    rng = np.random.default_rng(18)
+    d = rnd_inputs(rng, 1, 70, 2, 8, 5, backbone=O.GDN)
+    dO = rng.standard_normal((1, 70, 2, 5))
+    a = O.gdn_fwd_bwd(d["q"], d["k"], d["v"], d["gate"], d["beta"], d["lam"], dO, seg=64)
+    b = O.gdn_fwd_bwd(d["q"], d["k"], d["v"], d["gate"], d["beta"], d["lam"], dO, seg=7)
+    for key in a:
+        np.testing.assert_allclose(a[key], b[key], rtol=1e-12, atol=1e-12, err_msg=key)
+
+
+def test_gdn_reverse_pass_without_contraction_or_decay():
+    """With lam = 0, alpha = 1 and beta = 1 on one token the layer is o = (q . k) v, whose
+    gradients are dq = (dO . v) k, dk = (dO . v) q, dv = (q . k) dO; dbeta = (dO . v)(q . k)
+    (the write v k^T enters with weight beta), and dlogalpha = 0 (nothing to decay)."""
+    rng = np.random.default_rng(19)
+    q, k, v, dO = (rng.standard_normal((1, 1, 1, n)) for n in (4, 4, 3, 3))
+    z = np.zeros((1, 1, 1))
+    r = O.gdn_fwd_bwd(q, k, v, z, z + 1.0, z, dO)
+    qk, dv_ = float(np.sum(q * k)), float(np.sum(dO * v))
+    np.testing.assert_allclose(r["o"], qk * v, rtol=1e-14)
+    np.testing.assert_allclose(r["dq"], dv_ * k, rtol=1e-14)
+    np.testing.assert_allclose(r["dk"], dv_ * q, rtol=1e-14)
+    np.testing.assert_allclose(r["dv"], qk * dO, rtol=1e-14)
+    np.testing.assert_allclose(r["dbeta"], dv_ * qk, rtol=1e-14)
+    np.testing.assert_allclose(r["dlogalpha"], 0.0, atol=1e-15)
