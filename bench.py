@@ -6,8 +6,9 @@ dk=128, dv=256) plus one CCQ-Gated-DeltaNet forward on the ~1.3B-layer shape
 (B=4, T=4096, H=8, dk=dv=256), bf16 io, fp32 states, chunk 64, inputs resident
 in HBM.  `value` is the tokens of both calls divided by the mean step time.
 The line also carries the per-kernel HIP-event timings, the roofline of the
-dominant kernel, per-workload figures (including T=20480) and the fp64 CPU
-oracle timed on a bounded sample of the same inputs.
+dominant kernel, per-workload figures (including T=20480 and the GLA and Gated
+DeltaNet training steps) and the fp64 CPU oracle timed on a bounded sample of
+the same inputs.
 
     python bench.py [--gpus 1] [--steps 40] [--warmup 5]
 """
@@ -91,7 +92,7 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
         fl = ntok * (2 * C * dk)
     elif kernel == "gdn_state":     # k, v, Tm, decays, beta in; chunk states, U, final state out
         by = ntok * (dk * io_bytes + dv * io_bytes + C * io_bytes + 8 + dv * dk * io_bytes // C
-                     + dv * io_bytes) + BH * dv * dk * 4
+                     + dv * io_bytes) + (0 if getattr(w, "train", False) else BH * dv * dk * 4)
         fl = ntok * (4 * dk * dv + 2 * C * dv)
     elif kernel == "gdn_out":       # q_clean, k, chunk states, U, decays in; o out
         by = ntok * (2 * dk * io_bytes + dv * dk * io_bytes // C + 2 * dv * io_bytes + 4)
@@ -106,6 +107,18 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     elif kernel == "gla_dg":
         by = ntok * (4 * dk + dk * gate_bytes)
         fl = ntok * dk
+    elif kernel == "gdn_bwd_prep":  # q_clean, k, gamma, Tm in; decayed scores P^T and Tm^T out
+        by = ntok * (2 * dk * io_bytes + 4 + 3 * C * io_bytes)
+        fl = ntok * (2 * C * dk)
+    elif kernel == "gdn_dstate":    # q_clean, k, dO, P^T, Tm^T, decays in; dS_{r+1}, dR out
+        by = ntok * (2 * dk * io_bytes + 2 * dv * io_bytes + 2 * C * io_bytes + 16
+                     + dv * dk * io_bytes // C)
+        fl = ntok * (6 * dk * dv + 4 * C * dv)
+    elif kernel == "gdn_bwd_chunk":  # q_clean, k, v, dO, dR, U, S_r, dS_{r+1}, Sigma q, decays in;
+        # dq_clean (fp32 and io), backbone dk (fp32), dv, dlogalpha, dbeta, dlam out
+        by = ntok * (3 * dk * io_bytes + 5 * dv * io_bytes + 2 * dv * dk * io_bytes // C
+                     + 12 * dk + 28)
+        fl = ntok * (6 * dk * dv + 4 * C * dv + 12 * C * dk)
     elif kernel == "ccq_dk":
         by = ntok * (3 * dk * io_bytes + 12 + 4 * dk + dk * io_bytes)
         fl = ntok * (6 * dk * dk + 8 * C * dk)
@@ -119,7 +132,10 @@ KERNELS = {0: ["gla_state"] + CLEAN + ["clean_out", "gla_out"],
            "gla_seg": ["gla_state", "gla_scan"] + CLEAN + ["clean_out", "gla_out"],
            1: ["gdn_tri", "gdn_state"] + CLEAN + ["clean_out", "gdn_out"],
            "train": CLEAN + ["clean_out_train", "gla_state", "gla_out", "gla_dstate",
-                             "gla_bwd_chunk", "gla_dg", "clean_dq", "ccq_dk"]}
+                             "gla_bwd_chunk", "gla_dg", "clean_dq", "ccq_dk"],
+           "gdn_train": CLEAN + ["clean_out_train", "gdn_tri", "gdn_state", "gdn_out",
+                                 "gdn_bwd_prep", "gdn_dstate", "gdn_bwd_chunk", "clean_dq",
+                                 "ccq_dk"]}
 KERNEL_SYMBOL = {"clean_gram": "clean_gram_kernel",
                  "clean_prefix": "clean_prefix_kernel", "clean_out": "clean_out_kernel",
                  "clean_out_train": "clean_out_kernel", "clean_dq": "clean_out_kernel",
@@ -127,7 +143,8 @@ KERNEL_SYMBOL = {"clean_gram": "clean_gram_kernel",
                  "gdn_tri": "gdn_tri_kernel", "gdn_state": "gdn_state_dma_kernel",
                  "gdn_out": "gdn_out_kernel", "gla_dstate": "gla_dstate_kernel",
                  "gla_bwd_chunk": "gla_bwd_chunk_kernel", "gla_dg": "gla_dg_kernel",
-                 "ccq_dk": "ccq_dk_kernel"}
+                 "gdn_bwd_prep": "gdn_bwd_prep_kernel", "gdn_dstate": "gdn_dstate_kernel",
+                 "gdn_bwd_chunk": "gdn_bwd_chunk_kernel", "ccq_dk": "ccq_dk_kernel"}
 
 
 def _source(kernel: str) -> str:
@@ -135,6 +152,8 @@ def _source(kernel: str) -> str:
         return "ccq_clean.hip"
     if kernel in ("gla_state", "gla_scan", "gla_out"):
         return "ccq_gla.hip"
+    if kernel in ("gdn_bwd_prep", "gdn_dstate", "gdn_bwd_chunk"):
+        return "ccq_gdn_bwd.hip"
     if kernel.startswith("gdn"):
         return "ccq_gdn.hip"
     return "ccq_bwd.hip"
@@ -185,12 +204,15 @@ class Call:
                               dtype=torch.uint8, device=dev)
         if w.train:
             self.out = {"o": self.out["o"]}
-            for name, ref in (("dq", "q"), ("dk", "k"), ("dv", "v"), ("dg", "g")):
+            gate = "g" if w.backbone == 0 else "logalpha"
+            for name, ref in (("dq", "q"), ("dk", "k"), ("dv", "v"), ("dg", gate)):
                 self.out[name] = torch.empty_like(self.d[ref])
             self.out["dlam"] = torch.empty_like(self.d["lam"])
+            if w.backbone == 1:
+                self.out["dbeta"] = torch.empty_like(self.d["beta"])
         self.ccq = ccq
         if w.train:
-            self.kernels = KERNELS["train"]
+            self.kernels = KERNELS["train" if w.backbone == 0 else "gdn_train"]
         elif w.backbone == 0 and gla_seg(B * H, -(-T // CHUNK), dk, dv):
             self.kernels = KERNELS["gla_seg"]   # the state pass in segments adds a scan
         else:
@@ -198,9 +220,12 @@ class Call:
 
     def __call__(self):
         d = self.d
-        if self.w.train:
+        if self.w.train and self.w.backbone == 0:
             self.ccq.ccq_fwd_bwd(d["q"], d["k"], d["v"], d["g"], d["lam"], d["dO"], out=self.out,
                                  workspace=self.ws)
+        elif self.w.train:
+            self.ccq.ccq_fwd_bwd(d["q"], d["k"], d["v"], d["logalpha"], d["lam"], d["dO"],
+                                 out=self.out, workspace=self.ws, backbone=1, beta=d["beta"])
         elif self.w.backbone == 0:
             self.ccq.ccq_gla_fwd(d["q"], d["k"], d["v"], d["g"], d["lam"], out=self.out,
                                  workspace=self.ws)
@@ -361,7 +386,7 @@ def main(argv=None):
     extra = {}
     if not args.no_extra:
         for name in ("gla_500m_t2k", "gdn_1p3b_t4k", "gla_500m_t20k", "gdn_1p3b_t20k",
-                     "gla_train_t4k"):
+                     "gla_train_t4k", "gdn_train_t4k"):
             c = step_calls[0] if name == "gla_500m_t2k" else (
                 step_calls[1] if name == "gdn_1p3b_t4k" else Call(W[name], torch, ccq, inputs))
             ms, pk = time_calls(torch, ccq, [c], max(5, args.steps // 2), 3)

@@ -110,9 +110,15 @@ ccq_status ccq_gdn_fwd(const ccq_shape* s, const void* q, const void* k, const v
  * states, t0 must be 0).
  *   bb = CCQ_GLA: g_or_logalpha is g [B,T,H,dk] gate_dtype; beta and dbeta NULL;
  *                 dg_or_dlogalpha is dg [B,T,H,dk] gate_dtype.
- *   bb = CCQ_GDN: returns CCQ_ERR_UNSUPPORTED.
+ *   bb = CCQ_GDN: g_or_logalpha is log alpha [B,T,H] fp32 and beta [B,T,H]
+ *                 fp32 is required; dg_or_dlogalpha is d(log alpha) [B,T,H]
+ *                 fp32 and dbeta [B,T,H] fp32 is required.  The backbone
+ *                 gradients follow the reverse of the chunk form through the
+ *                 WY/UT transform (Alg. 1's BackboneUpdate for the delta rule).
  *   dO [B,T,H,dv] io_dtype upstream gradient; o, dq, dk, dv io_dtype;
  *   dlam [B,T,H] fp32.
+ * Supported: chunk = 64, dv in {64,128,256,512}, and dk in {64,128} for bf16
+ * io or dk = 64 for fp32 io; other shapes return CCQ_ERR_UNSUPPORTED.
  */
 ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const void* k,
                        const void* v, const void* g_or_logalpha, const float* beta,

@@ -212,13 +212,22 @@ def ccq_fwd_bwd(q, k, v, g, lam, dO, scale=1.0, centered=True, chunk=64, out=Non
                 workspace=None, stream=None, backbone=CCQ_GLA, beta=None):
     """CCQ training step: o and the gradients of sum <dO, o>.
 
-    Returns dict o, dq, dk, dv, dg, dlam (GLA).  The GDN backward is not
-    available in this build (the library returns CCQ_ERR_UNSUPPORTED)."""
+    GLA: g is the log-forget gate [B,T,H,dk]; returns dict o, dq, dk, dv, dg, dlam.
+    Gated DeltaNet (backbone=CCQ_GDN): g is log alpha [B,T,H] fp32 and beta
+    [B,T,H] fp32 is required; returns o, dq, dk, dv, dg (= d log alpha), dbeta,
+    dlam."""
     B, T, H, dk = q.shape
     dv = v.shape[-1]
     dev = q.device
     gate_dtype = g.dtype if backbone == CCQ_GLA else q.dtype
     shape = make_shape(B, T, H, dk, dv, q.dtype, gate_dtype, scale, centered, 0, chunk)
+    if backbone == CCQ_GLA:
+        _check(g, "g", (B, T, H, dk), g.dtype, dev)
+    else:
+        if beta is None:
+            raise ValueError("beta is required for the Gated DeltaNet training step")
+        _check(g, "logalpha", (B, T, H), torch.float32, dev)
+        _check(beta, "beta", (B, T, H), torch.float32, dev)
     _check(k, "k", (B, T, H, dk), q.dtype, dev)
     _check(v, "v", (B, T, H, dv), q.dtype, dev)
     _check(dO, "dO", (B, T, H, dv), q.dtype, dev)

@@ -210,6 +210,40 @@ BwdLayout bwd_layout(const ccq_shape* s) {
   return L;
 }
 
+// Training step of CCQ-Gated DeltaNet: the forward's q_clean, key statistics,
+// chunk transforms, S_r and U, then the backward's PT, Tm^T, dS_{r+1} and dR.
+struct GdnBwdLayout {
+  size_t qclean, corr, mdq, mdu, states, Tm, gam, U, PT, TmT, dstates, dR, dqc, dqc_io, dkb, total;
+  CleanWs clean;
+};
+
+GdnBwdLayout gdn_bwd_layout(const ccq_shape* s) {
+  GdnBwdLayout L{};
+  const size_t ntok = (size_t)s->B * s->T * s->H;
+  const size_t nchunk = (size_t)s->B * s->H * ((s->T + 63) / 64);
+  const size_t e = esize(s->io_dtype);
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t o = off; off += align_up(bytes); return o; };
+  L.qclean = take(ntok * s->dk * e);
+  L.corr = take(ntok * s->dk * 4);
+  L.mdq = take(ntok * 4);
+  L.mdu = take(ntok * 4);
+  L.states = take(nchunk * s->dv * s->dk * e);
+  L.Tm = take(nchunk * 64 * 64 * e);
+  L.gam = take(nchunk * 5 * 64 * sizeof(float));
+  L.U = take(nchunk * 64 * s->dv * e);
+  L.PT = take(nchunk * 64 * 64 * e);
+  L.TmT = take(nchunk * 64 * 64 * e);
+  L.dstates = take(nchunk * s->dv * s->dk * e);
+  L.dR = take(ntok * s->dv * e);
+  L.dqc = take(ntok * s->dk * 4);
+  L.dqc_io = take(ntok * s->dk * e);
+  L.dkb = take(ntok * s->dk * 4);
+  L.clean = take_clean_ws(s, take);
+  L.total = off;
+  return L;
+}
+
 // T == 0: the final states are the initial ones (or zero).
 ccq_status copy_initial_states(const ccq_shape* s, const float* S0, const float* C0,
                                const float* mu0, float* ST, float* CT, float* muT,
@@ -315,6 +349,68 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   return CCQ_OK;
 }
 
+// CCQ-Gated DeltaNet training step (arguments validated by the caller).
+ccq_status gdn_fwd_bwd(const ccq_shape* s, const void* q, const void* k, const void* v,
+                       const float* la, const float* beta, const float* lam, const void* dO,
+                       void* o, void* dq, void* dk, void* dv, float* dla, float* dbeta,
+                       float* dlam, void* workspace, size_t ws_bytes, void* stream) {
+  const GdnBwdLayout L = gdn_bwd_layout(s);
+  if (!workspace || ws_bytes < L.total) return CCQ_ERR_WORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  const bool bf = s->io_dtype == CCQ_BF16;
+  float* corr = reinterpret_cast<float*>(ws + L.corr);
+  float* mdq = reinterpret_cast<float*>(ws + L.mdq);
+  float* mdu = reinterpret_cast<float*>(ws + L.mdu);
+  float* gam = reinterpret_cast<float*>(ws + L.gam);
+  float* dqc = reinterpret_cast<float*>(ws + L.dqc);
+  float* dkb = reinterpret_cast<float*>(ws + L.dkb);
+  trace_begin_call();
+
+  // forward: cleaned queries (with Sigma q and m.q kept), chunk transforms,
+  // S_r and U, outputs
+  ccq::CleanArgs c1 = clean_args(s, ws, L.clean);
+  c1.q = q;
+  c1.k = k;
+  c1.lam = lam;
+  c1.qclean = ws + L.qclean;
+  c1.corr = corr;
+  c1.mdot = mdq;
+  if (run_clean_stats(c1, bf, st) != hipSuccess) return CCQ_ERR_HIP;
+  if (traced(st, [&] { return ccq::launch_clean_out(c1, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::TriArgs ta{k, la, beta, ws + L.Tm, gam, s->B, s->T, s->H, s->dk, s->dv};
+  if (traced(st, [&] { return ccq::launch_gdn_tri(ta, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::GdnArgs sa{k, v, beta, ws + L.Tm, gam, nullptr, nullptr, ws + L.states, ws + L.U, s->B,
+                  s->T, s->H, s->dk, s->dv};
+  if (traced(st, [&] { return ccq::launch_gdn_state(sa, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::GdnOutArgs oa{ws + L.qclean, k, gam, ws + L.states, ws + L.U, o, s->B, s->T, s->H, s->dk,
+                     s->dv, s->scale};
+  if (traced(st, [&] { return ccq::launch_gdn_out(oa, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  // backward: PT and Tm^T, the reverse state scan, chunk gradients, dq, dk
+  ccq::GdnPrepArgs pa{ws + L.qclean, k, gam, ws + L.Tm, ws + L.PT, ws + L.TmT, s->B, s->T, s->H,
+                      s->dk, s->dv};
+  if (traced(st, [&] { return ccq::launch_gdn_bwd_prep(pa, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::GdnDstateArgs da{ws + L.qclean, k, dO, gam, ws + L.PT, ws + L.TmT, ws + L.dstates, ws + L.dR,
+                        s->B, s->T, s->H, s->dk, s->dv, s->scale};
+  if (traced(st, [&] { return ccq::launch_gdn_dstate(da, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::GdnBwdArgs ba{ws + L.qclean, k, v, dO, gam, ws + L.states, ws + L.U, ws + L.dstates,
+                     ws + L.dR, corr, dqc, ws + L.dqc_io, dkb, dv, dla, dbeta, dlam, s->B, s->T,
+                     s->H, s->dk, s->dv, s->scale};
+  if (traced(st, [&] { return ccq::launch_gdn_bwd_chunk(ba, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::CleanArgs c2 = clean_args(s, ws, L.clean);  // same keys: statistics reused
+  c2.q = ws + L.dqc_io;
+  c2.k = k;
+  c2.lam = lam;
+  c2.qclean = dq;
+  c2.base = dqc;
+  c2.mdot = mdu;
+  if (traced(st, [&] { return ccq::launch_clean_out(c2, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  ccq::CcqDkArgs ka{q, k, ws + L.dqc_io, lam, mdq, mdu, dkb, dk, s->B, s->T, s->H, s->dk,
+                    s->centered};
+  if (traced(st, [&] { return ccq::launch_ccq_dk(ka, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  return CCQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -322,8 +418,8 @@ extern "C" {
 size_t ccq_workspace_size(const ccq_shape* s, ccq_backbone bb, int with_bwd) {
   if (check_shape(s, bb) != CCQ_OK) return 0;
   if (with_bwd) {
-    if (bb != CCQ_GLA || !ccq::bwd_supported(s->dk, s->dv, s->io_dtype == CCQ_BF16)) return 0;
-    return bwd_layout(s).total;
+    if (!ccq::bwd_supported(s->dk, s->dv, s->io_dtype == CCQ_BF16)) return 0;
+    return bb == CCQ_GLA ? bwd_layout(s).total : gdn_bwd_layout(s).total;
   }
   return fwd_layout(s, bb).total;
 }
@@ -350,11 +446,8 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
                        const float* lam, const void* dO, void* o, void* dq, void* dk, void* dv,
                        void* dg_or_dlogalpha, float* dbeta, float* dlam, void* workspace,
                        size_t ws_bytes, void* stream) {
-  (void)beta;
-  (void)dbeta;
   ccq_status rc = check_shape(s, bb);
   if (rc != CCQ_OK) return rc;
-  if (bb != CCQ_GLA) return CCQ_ERR_UNSUPPORTED;  // the Gated DeltaNet backward is not built
   if (s->t0 != 0) return CCQ_ERR_INVALID_ARG;     // a training step starts from zero states
   const bool bf = s->io_dtype == CCQ_BF16;
   const bool gbf = s->gate_dtype == CCQ_BF16;
@@ -365,8 +458,14 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
     const void* req[] = {q, k, v, g_or_logalpha, lam, dO, o, dq, dk, dv, dg_or_dlogalpha, dlam};
     for (const void* p : req)
       if (!p || !aligned(p)) return CCQ_ERR_INVALID_ARG;
+    if (bb == CCQ_GDN && (!beta || !aligned(beta) || !dbeta || !aligned(dbeta)))
+      return CCQ_ERR_INVALID_ARG;
   }
   if (ntok == 0) return CCQ_OK;
+  if (bb == CCQ_GDN)
+    return gdn_fwd_bwd(s, q, k, v, static_cast<const float*>(g_or_logalpha), beta, lam, dO, o, dq,
+                       dk, dv, static_cast<float*>(dg_or_dlogalpha), dbeta, dlam, workspace,
+                       ws_bytes, stream);
   const BwdLayout L = bwd_layout(s);
   if (!workspace || ws_bytes < L.total) return CCQ_ERR_WORKSPACE;
   hipStream_t st = static_cast<hipStream_t>(stream);

@@ -1,0 +1,595 @@
+// ccq_gdn_bwd.hip -- CCQ-Gated DeltaNet training step: gradients of the
+// backbone, L = sum_t <dO_t, o_t>.
+//
+// Forward of chunk r (see ccq_gdn.hip), entered with state S_r, Q = q_clean,
+// gamma the cumulative log decay inside the chunk, G = e^gamma, Tm = (I+A)^{-1}:
+//   W = V - diag(G) K S_r^T,  U = Tm diag(beta) W,
+//   P_ij = e^{gamma_i - gamma_j} (q_i . k_j)  (j <= i),
+//   O = s [diag(G) Q S_r^T + P U],
+//   S_{r+1} = e^{gamma_C} S_r + U^T diag(e^{gamma_C - gamma}) K.
+// Reverse, with dO' = s dO and D = dL/dS_{r+1} (zero after the last chunk):
+//   dU = P^T dO' + diag(e^{gamma_C - gamma}) K D^T,   dR = Tm^T dU,
+//   dS_r = e^{gamma_C} D + dO'^T diag(G) Q - dR^T diag(beta G) K      (sequential)
+// and, chunk-parallel, with G1 = dO' S_r, G2 = dR S_r, G3 = U D,
+// dPm = M o (dO' U^T) (M_ij = e^{gamma_i - gamma_j}, j <= i),
+// dA = -(dR U^T) strictly below the diagonal, E = diag(beta) (M o dA):
+//   dQ      = diag(G) G1 + dPm K
+//   dK      = dPm^T Q + diag(e^{gamma_C - gamma}) G3 - diag(beta G) G2 + E K + E^T K
+//   dV      = diag(beta) dR
+//   dbeta_i = dR_i . V_i - G_i (G2_i . k_i) + sum_{j<i} (M o dA)_ij (k_i . k_j)
+//   dgamma_i = G_i (G1_i . q_i) + rowsum_i(F) - colsum_i(F) - beta_i G_i (G2_i . k_i)
+//              + rowsum_i(Fa) - colsum_i(Fa) - e^{gamma_C - gamma_i} (G3_i . k_i),
+//     F = dPm o (Q K^T), Fa = E o (K K^T); the last row of the chunk also takes
+//     sum_i e^{gamma_C - gamma_i} (G3_i . k_i) + e^{gamma_C} <D, S_r>,
+//   dlogalpha_s = sum_{i >= s} dgamma_i  (inside the chunk).
+// dQ is dL/dq_clean; the contraction's part of the gradients follows as for
+// GLA (ccq_bwd.hip).
+#include "ccq_device.h"
+#include "ccq_kernels.h"
+
+namespace ccq {
+
+// ----------------------------------------------------------------------------
+// Per chunk: PT[j][i] = e^{gamma_i - gamma_j} (qc_i . k_j) for j <= i, else 0
+// (row-major, plain order), and Tm^T with rows in acc_pos order
+// (TmT[i][acc_pos(j)] = Tm[j][i]; Tm itself is stored as Tm[j][acc_pos(i)]).
+template <typename T, int DK>
+__global__ __launch_bounds__(kThreads) void gdn_bwd_prep_kernel(const GdnPrepArgs a) {
+  constexpr int C = kChunk;
+  constexpr int P = Pad<T>::value;
+  constexpr int LDQ = DK + P, LDP = C + P;
+  __shared__ __align__(16) T sQ[C * LDQ];
+  __shared__ __align__(16) T sK[C * LDQ];
+  __shared__ __align__(16) T sTm[C * LDP];
+  __shared__ float sGam[C];
+
+  const int N = (a.T + C - 1) / C;
+  const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int bh = lb / N, ci = lb % N;
+  const int b = bh / a.H, h = bh % a.H;
+  const int r0 = ci * C;
+  const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+  const int tid = threadIdx.x, w = wave_id(), l = lane_id();
+  const int g4 = l >> 4, c16 = l & 15;
+  const size_t cidx = (size_t)bh * N + ci;
+  {
+    RowTile<T, DK> rq, rk;
+    RowTile<T, C> rt;
+    rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+    rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+    rt.load(static_cast<const T*>(a.Tm) + cidx * C * C, (size_t)C, C);
+    if (tid < C) sGam[tid] = a.gam[cidx * 5 * C + tid];
+    rq.store(sQ, LDQ);
+    rk.store(sK, LDQ);
+    rt.store(sTm, LDP);
+  }
+  __syncthreads();
+
+  // wave w: rows i of stripe w against every key tile J; P^T stored as rows j
+  T* PT = static_cast<T*>(a.PT) + cidx * C * C;
+#pragma unroll
+  for (int J = 0; J < 4; ++J) {
+    f32x4 acc = zero4();
+    if (J <= w) tile_mma<T, DK>(acc, sQ + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+    const int j = 16 * J + c16;
+    float x[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = 16 * w + 4 * g4 + r;
+      x[r] = (J <= w && j <= i) ? acc[r] * __expf(sGam[i] - sGam[j]) : 0.f;
+    }
+    store4(PT + (size_t)j * C + 16 * w + 4 * g4, x[0], x[1], x[2], x[3]);
+  }
+  T* TmT = static_cast<T*>(a.TmT) + cidx * C * C;
+  for (int idx = tid; idx < C * C; idx += kThreads) {
+    const int i = idx / C, p = idx % C;
+    TmT[idx] = sTm[acc_logical(p) * LDP + acc_pos(i)];
+  }
+}
+
+// ----------------------------------------------------------------------------
+// Reverse scan of D = dL/dS_{r+1} over the chunks of one head.  A workgroup
+// owns NPR value tiles of 16; wave p keeps D^T[c][v] for all key features c
+// of its tile in MFMA accumulators.  Per chunk (last to first):
+//   store D;  X = diag(e^{gamma_C - gamma}) K D^T;  dU = X + PT dO';
+//   dR = Tm^T dU -> stored;  D <- e^{gamma_C} D + (G Q)^T dO' - K^T diag(beta G) dR.
+// The chunk's K, G Q, PT, Tm^T and dO' slice are prefetched into registers
+// one chunk ahead and staged through LDS.
+template <typename T, int DK, int NPR>
+__global__ __launch_bounds__(64 * NPR, 1) void gdn_dstate_kernel(const GdnDstateArgs a) {
+  constexpr int C = kChunk, NT = 64 * NPR, BVS = 16 * NPR;
+  constexpr int P = Pad<T>::value;
+  constexpr int LDQ = DK + P, LDP = C + P;
+  constexpr int NCT = DK / 16, NK = DK / 32;
+
+  __shared__ __align__(16) T sK[C * LDQ];
+  __shared__ __align__(16) T sQ[C * LDQ];      // e^{gamma_i} qc_i
+  __shared__ __align__(16) T sPT[C * LDP];
+  __shared__ __align__(16) T sTT[C * LDP];     // Tm^T, rows in acc_pos order
+  __shared__ __align__(16) T sdOT[BVS * LDP];  // (s dO)^T of the workgroup's values
+  __shared__ __align__(16) float sCf[3][C];    // e^{gamma_C - gamma}, beta e^gamma, e^{gamma_C}
+
+  const int nvt = a.dv / BVS;
+  const int N = (a.T + C - 1) / C;
+  const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int bh = lb / nvt;
+  const int v0 = (lb % nvt) * BVS;
+  const int b = bh / a.H, h = bh % a.H;
+  const int tid = threadIdx.x, pr = wave_id(), l = lane_id();
+  const int g4 = l >> 4, c16 = l & 15;
+  const int v = v0 + 16 * pr + c16;
+  const T* qc = static_cast<const T*>(a.qc);
+  const T* k = static_cast<const T*>(a.k);
+  const T* dO = static_cast<const T*>(a.dO);
+  T* dst = static_cast<T*>(a.dstates);
+  T* dRg = static_cast<T*>(a.dR);
+
+  f32x4 D[NCT];
+#pragma unroll
+  for (int tc = 0; tc < NCT; ++tc) D[tc] = zero4();
+
+  struct Stage {
+    RowTile<T, DK, NT> rk;
+    ChunkTile<T, DK, NT> rq;   // lane = token row, so one decay per lane
+    RowTile<T, C, NT> rp, rt;
+    ChunkTile<T, BVS, NT> rdo;
+    float gq;                  // gamma of this lane's token row
+    RowScalar cf[3];
+  };
+  Stage st;
+  auto prefetch = [&](int ci) {
+    const int r0 = ci * C;
+    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+    const size_t cidx = (size_t)bh * N + ci;
+    st.rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+    st.rq.load(qc + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+    st.rp.load(static_cast<const T*>(a.PT) + cidx * C * C, (size_t)C, C);
+    st.rt.load(static_cast<const T*>(a.TmT) + cidx * C * C, (size_t)C, C);
+    st.rdo.load(dO + tok_off(b, r0, h, a.T, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
+    st.gq = a.gam[cidx * 5 * C + (tid & 63)];
+    if (tid < C) {
+      st.cf[0].load(a.gam + (cidx * 5 + 3) * C, 1, tid, C);
+      st.cf[1].load(a.gam + (cidx * 5 + 1) * C, 1, tid, C);
+      st.cf[2].load(a.gam + (cidx * 5 + 4) * C, 1, tid, C);
+    }
+  };
+  if (N > 0) prefetch(N - 1);
+
+  for (int ci = N - 1; ci >= 0; --ci) {
+    const int r0 = ci * C;
+    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+    const size_t cidx = (size_t)bh * N + ci;
+    __syncthreads();  // every wave is done with the previous chunk's LDS
+    st.rk.store(sK, LDQ);
+    st.rp.store(sPT, LDP);
+    st.rt.store(sTT, LDP);
+    {
+      typedef typename ChunkTile<T, DK, NT>::vec_t vq;
+      const int row = ChunkTile<T, DK, NT>::row();
+      const float eg = __expf(st.gq);
+#pragma unroll
+      for (int u = 0; u < ChunkTile<T, DK, NT>::NV; ++u) {
+        const vq x = st.rq.get(u);
+        vq y;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] = to<T>(eg * f32(x[e]));
+        *reinterpret_cast<vq*>(sQ + row * LDQ + ChunkTile<T, DK, NT>::col(u)) = y;
+      }
+#pragma unroll
+      for (int u = 0; u < ChunkTile<T, BVS, NT>::NV; ++u) {
+        const auto x = st.rdo.get(u);
+        const int c0 = ChunkTile<T, BVS, NT>::col(u);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sdOT[(c0 + e) * LDP + row] = to<T>(a.scale * f32(x[e]));
+      }
+    }
+    if (tid < C) {
+#pragma unroll
+      for (int q = 0; q < 3; ++q) sCf[q][tid] = st.cf[q].get();
+    }
+    {  // D is the adjoint of the state leaving chunk ci
+      T* out = dst + (cidx * a.dv + v) * DK + 4 * g4;
+#pragma unroll
+      for (int tc = 0; tc < NCT; ++tc) store4(out + 16 * tc, D[tc][0], D[tc][1], D[tc][2], D[tc][3]);
+    }
+    if (ci > 0) prefetch(ci - 1);
+    __syncthreads();
+
+    // X = K D^T (D^T from the accumulators), rows scaled by e^{gamma_C - gamma_i}
+    Frag<T> df[NK];
+#pragma unroll
+    for (int m = 0; m < NK; ++m) df[m] = acc_pair_frag<T>(D[2 * m], D[2 * m + 1]);
+    f32x4 dU[4];
+#pragma unroll
+    for (int I = 0; I < 4; ++I) {
+      dU[I] = zero4();
+#pragma unroll
+      for (int m = 0; m < NK; ++m) mma(dU[I], ld_frag_acc(sK + 16 * I * LDQ + 32 * m, (size_t)LDQ), df[m]);
+      dU[I] *= *reinterpret_cast<const f32x4*>(&sCf[0][16 * I + 4 * g4]);
+    }
+    // dU += PT dO'
+    const Frag<T> of0 = ld_frag(sdOT + 16 * pr * LDP, LDP);
+    const Frag<T> of1 = ld_frag(sdOT + 16 * pr * LDP + 32, LDP);
+#pragma unroll
+    for (int I = 0; I < 4; ++I) {
+      mma(dU[I], ld_frag(sPT + 16 * I * LDP, LDP), of0);
+      mma(dU[I], ld_frag(sPT + 16 * I * LDP + 32, LDP), of1);
+    }
+    // dR = Tm^T dU
+    const Frag<T> uf0 = acc_pair_frag<T>(dU[0], dU[1]);
+    const Frag<T> uf1 = acc_pair_frag<T>(dU[2], dU[3]);
+    f32x4 dR[4];
+#pragma unroll
+    for (int I = 0; I < 4; ++I) {
+      dR[I] = zero4();
+      mma(dR[I], ld_frag(sTT + 16 * I * LDP, LDP), uf0);
+      mma(dR[I], ld_frag(sTT + 16 * I * LDP + 32, LDP), uf1);
+    }
+#pragma unroll
+    for (int I = 0; I < 4; ++I)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = 16 * I + 4 * g4 + r;
+        if (i < nrow) dRg[tok_off(b, r0 + i, h, a.T, a.H, a.dv) + v] = to<T>(dR[I][r]);
+      }
+    // D <- e^{gamma_C} D + (G Q)^T dO' - K^T diag(beta G) dR
+#pragma unroll
+    for (int I = 0; I < 4; ++I) dR[I] *= -*reinterpret_cast<const f32x4*>(&sCf[1][16 * I + 4 * g4]);
+    const Frag<T> rf0 = acc_pair_frag<T>(dR[0], dR[1]);
+    const Frag<T> rf1 = acc_pair_frag<T>(dR[2], dR[3]);
+    const float eC = sCf[2][0];
+#pragma unroll
+    for (int tc = 0; tc < NCT; ++tc) {
+      D[tc] *= eC;
+      mma(D[tc], ld_frag_tr(sQ + 16 * tc, LDQ), of0);
+      mma(D[tc], ld_frag_tr(sQ + 32 * LDQ + 16 * tc, LDQ), of1);
+      mma(D[tc], ld_frag_tr_acc(sK + 16 * tc, LDQ), rf0);
+      mma(D[tc], ld_frag_tr_acc(sK + 32 * LDQ + 16 * tc, LDQ), rf1);
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------
+// One workgroup per chunk (four waves, wave w owning token rows 16w..16w+15):
+// the C x C products Q K^T and K K^T, then a loop over BV-wide value slices
+// accumulating G1 = dO' S_r, G2 = dR S_r, G3 = U D, dO' U^T and dR U^T, then
+// the C x C-weighted sums and the per-element and per-row epilogue.
+template <typename T, int DK, int BV>
+__global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwdArgs a) {
+  constexpr int C = kChunk;
+  constexpr int P = Pad<T>::value;
+  constexpr int LDQ = DK + P, LDT = C + P, LDV = BV + P;
+  constexpr int NTC = DK / 16;
+  constexpr int ES = (int)sizeof(T);
+  static_assert(BV % 32 == 0 && DK % 32 == 0, "tiles");
+
+  __shared__ __align__(16) T sQT[DK * LDT];  // qc^T (key channel rows)
+  __shared__ __align__(16) T sKT[DK * LDT];
+  __shared__ float sGam[C], sBeta[C], sDec[C];
+  __shared__ float sColF[4][C], sColA[4][C], sRV[4][C];
+  __shared__ float sDg[C];
+  __shared__ float sRed[2][4];
+  constexpr int kR1 = 2 * C * LDQ * ES;
+  constexpr int kR2 = 4 * C * LDV * ES + 2 * DK * LDV * ES;
+  constexpr int kR3 = 4 * C * LDT * ES;
+  constexpr int kR = kR1 > kR2 ? (kR1 > kR3 ? kR1 : kR3) : (kR2 > kR3 ? kR2 : kR3);
+  __shared__ __align__(16) char sR[kR];
+
+  const int N = (a.T + C - 1) / C;
+  const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int bh = lb / N, ci = lb % N;
+  const int b = bh / a.H, h = bh % a.H;
+  const int r0 = ci * C;
+  const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+  const int tid = threadIdx.x, w = wave_id(), l = lane_id();
+  const int g4 = l >> 4, c16 = l & 15;
+  const size_t cidx = (size_t)bh * N + ci;
+  const size_t gsk = (size_t)a.H * DK, gsv = (size_t)a.H * a.dv;
+  const float eC = a.gam[(cidx * 5 + 4) * C];
+
+  // ---- phase 1: Q K^T and K K^T (rows of stripe w, tiles J <= w)
+  f32x4 QK[4], KK[4];
+  {
+    T* sQ = reinterpret_cast<T*>(sR);
+    T* sK = sQ + C * LDQ;
+    ChunkTile<T, DK> rq, rk;
+    rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gsk, nrow);
+    rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gsk, nrow);
+    if (tid < C) {
+      sGam[tid] = a.gam[cidx * 5 * C + tid];
+      sBeta[tid] = a.gam[(cidx * 5 + 2) * C + tid];
+      sDec[tid] = a.gam[(cidx * 5 + 3) * C + tid];
+    }
+    rq.store(sQ, LDQ);
+    rk.store(sK, LDQ);
+    rq.store_t(sQT, LDT);
+    rk.store_t(sKT, LDT);
+    __syncthreads();
+#pragma unroll
+    for (int J = 0; J < 4; ++J) {
+      QK[J] = zero4();
+      KK[J] = zero4();
+      if (J <= w) {
+        tile_mma<T, DK>(QK[J], sQ + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+        tile_mma<T, DK>(KK[J], sK + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+      }
+    }
+    __syncthreads();  // sQ, sK dead
+  }
+
+  // ---- phase 2: value slices
+  f32x4 G1[NTC], G2[NTC], G3[NTC], dP[4], dA[4];
+#pragma unroll
+  for (int ct = 0; ct < NTC; ++ct) { G1[ct] = zero4(); G2[ct] = zero4(); G3[ct] = zero4(); }
+#pragma unroll
+  for (int J = 0; J < 4; ++J) { dP[J] = zero4(); dA[J] = zero4(); }
+  float rv = 0.f, dss = 0.f;
+  {
+    T* sdO = reinterpret_cast<T*>(sR);
+    T* sdR = sdO + C * LDV;
+    T* sU = sdR + C * LDV;
+    T* sV = sU + C * LDV;
+    T* sST = sV + C * LDV;  // S_r^T [c][v]
+    T* sDT = sST + DK * LDV;  // D^T [c][v]
+    const T* Sg = static_cast<const T*>(a.states) + cidx * a.dv * DK;
+    const T* Ug = static_cast<const T*>(a.U) + cidx * a.dv * C;
+    const T* Dg = static_cast<const T*>(a.dstates) + cidx * a.dv * DK;
+    T* dvout = static_cast<T*>(a.dv_out);
+    typedef T v8 __attribute__((ext_vector_type(8)));
+    for (int vv0 = 0; vv0 < a.dv; vv0 += BV) {
+      {
+        ChunkTile<T, BV> rdo, rdr, rvv;
+        rdo.load(static_cast<const T*>(a.dO) + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
+        rdr.load(static_cast<const T*>(a.dR) + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
+        rvv.load(static_cast<const T*>(a.v) + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
+        const int row = ChunkTile<T, BV>::row();
+        const float bt = sBeta[row];
+#pragma unroll
+        for (int u = 0; u < ChunkTile<T, BV>::NV; ++u) {
+          const int c0 = ChunkTile<T, BV>::col(u);
+          const v8 xo = rdo.get(u), xr = rdr.get(u), xv = rvv.get(u);
+          v8 yo, yd;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            yo[e] = to<T>(a.scale * f32(xo[e]));
+            yd[e] = to<T>(bt * f32(xr[e]));
+            rv += f32(xr[e]) * f32(xv[e]);
+          }
+          *reinterpret_cast<v8*>(sdO + row * LDV + c0) = yo;
+          *reinterpret_cast<v8*>(sdR + row * LDV + c0) = xr;
+          *reinterpret_cast<v8*>(sV + row * LDV + c0) = xv;
+          if (row < nrow) *reinterpret_cast<v8*>(dvout + tok_off(b, r0 + row, h, a.T, a.H, a.dv) + vv0 + c0) = yd;
+        }
+      }
+      // S_r and U^T slices (fragment-native: per value tile and 32-wide k
+      // block, 16 rows of 32 in acc_pos order) and D (plain rows)
+      for (int q = tid; q < BV * DK / 8; q += kThreads) {
+        const int vt = q / (2 * DK), rem = q % (2 * DK);
+        const int m = rem / 64, vr = (rem % 64) / 4, pp = rem % 4;
+        const v8 x = *reinterpret_cast<const v8*>(Sg + (size_t)(vv0 / 16 + vt) * 16 * DK + (size_t)(m * 16 + vr) * 32 + 8 * pp);
+        const int vl = 16 * vt + vr;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sST[(32 * m + acc_logical(8 * pp + e)) * LDV + vl] = x[e];
+        const int vd = q / (DK / 8), cd = (q % (DK / 8)) * 8;
+        const v8 y = *reinterpret_cast<const v8*>(Dg + (size_t)(vv0 + vd) * DK + cd);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sDT[(cd + e) * LDV + vd] = y[e];
+      }
+      for (int q = tid; q < BV * C / 8; q += kThreads) {
+        const int vt = q / 128, rem = q % 128;
+        const int m = rem / 64, vr = (rem % 64) / 4, pp = rem % 4;
+        const v8 x = *reinterpret_cast<const v8*>(Ug + (size_t)(vv0 / 16 + vt) * 16 * C + (size_t)(m * 16 + vr) * 32 + 8 * pp);
+        const int vl = 16 * vt + vr;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sU[(32 * m + acc_logical(8 * pp + e)) * LDV + vl] = x[e];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int J = 0; J < 4; ++J) {
+        if (J <= w) {
+          tile_mma<T, BV>(dP[J], sdO + 16 * w * LDV, LDV, sU + 16 * J * LDV, LDV);
+          tile_mma<T, BV>(dA[J], sdR + 16 * w * LDV, LDV, sU + 16 * J * LDV, LDV);
+        }
+      }
+#pragma unroll
+      for (int ct = 0; ct < NTC; ++ct) {
+        tile_mma<T, BV>(G1[ct], sdO + 16 * w * LDV, LDV, sST + 16 * ct * LDV, LDV);
+        tile_mma<T, BV>(G2[ct], sdR + 16 * w * LDV, LDV, sST + 16 * ct * LDV, LDV);
+        tile_mma<T, BV>(G3[ct], sU + 16 * w * LDV, LDV, sDT + 16 * ct * LDV, LDV);
+      }
+      for (int idx = tid; idx < DK * BV; idx += kThreads) {
+        const int c = idx / BV, vl = idx % BV;
+        dss += f32(sST[c * LDV + vl]) * f32(sDT[c * LDV + vl]);
+      }
+      __syncthreads();
+    }
+  }
+  sRV[w][l] = rv;
+
+  // ---- phase 3: C x C weights
+  T* sPm = reinterpret_cast<T*>(sR);
+  T* sPmT = sPm + C * LDT;
+  T* sE = sPmT + C * LDT;
+  T* sET = sE + C * LDT;
+  float rowF[4] = {0.f, 0.f, 0.f, 0.f}, rowA[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int J = 0; J < 4; ++J) {
+    const int j = 16 * J + c16;
+    float colF = 0.f, colA = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = 16 * w + 4 * g4 + r;
+      const float e = (J <= w && j <= i) ? __expf(sGam[i] - sGam[j]) : 0.f;
+      const float pm = e * dP[J][r];
+      const float ea = j < i ? -e * dA[J][r] : 0.f;  // (M o dA)_ij
+      const float E = sBeta[i] * ea;
+      const float F = pm * QK[J][r];
+      const float fa = ea * KK[J][r];
+      rowF[r] += F;
+      rowA[r] += fa;
+      colF += F;
+      colA += sBeta[i] * fa;
+      sPm[i * LDT + j] = to<T>(pm);
+      sPmT[j * LDT + i] = to<T>(pm);
+      sE[i * LDT + j] = to<T>(E);
+      sET[j * LDT + i] = to<T>(E);
+    }
+    colF += __shfl_xor(colF, 16);
+    colF += __shfl_xor(colF, 32);
+    colA += __shfl_xor(colA, 16);
+    colA += __shfl_xor(colA, 32);
+    if (g4 == 0) {
+      sColF[w][j] = colF;
+      sColA[w][j] = colA;
+    }
+  }
+  {  // <D, S_r> over the workgroup
+    float x = dss;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+    if (l == 0) sRed[0][w] = x;
+  }
+  __syncthreads();
+
+  // ---- phase 4: dQ, dK and the epilogue (row i = 16w + 4g4 + r, channel c)
+  float dot1[4] = {0.f, 0.f, 0.f, 0.f}, dot2[4] = {0.f, 0.f, 0.f, 0.f}, dot3[4] = {0.f, 0.f, 0.f, 0.f};
+  float dl[4] = {0.f, 0.f, 0.f, 0.f};
+  T* dqc_io = static_cast<T*>(a.dqc_io);
+#pragma unroll
+  for (int ct = 0; ct < NTC; ++ct) {
+    f32x4 x = zero4(), y = zero4();
+    tile_mma<T, C>(x, sPm + 16 * w * LDT, LDT, sKT + 16 * ct * LDT, LDT);
+    tile_mma<T, C>(y, sPmT + 16 * w * LDT, LDT, sQT + 16 * ct * LDT, LDT);
+    tile_mma<T, C>(y, sE + 16 * w * LDT, LDT, sKT + 16 * ct * LDT, LDT);
+    tile_mma<T, C>(y, sET + 16 * w * LDT, LDT, sKT + 16 * ct * LDT, LDT);
+    const int c = 16 * ct + c16;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = 16 * w + 4 * g4 + r;
+      const float G = __expf(sGam[i]);
+      const float qv = f32(sQT[c * LDT + i]), kv = f32(sKT[c * LDT + i]);
+      const float dq = G * G1[ct][r] + x[r];
+      const float dk = y[r] + sDec[i] * G3[ct][r] - sBeta[i] * G * G2[ct][r];
+      dot1[r] += G1[ct][r] * qv;
+      dot2[r] += G2[ct][r] * kv;
+      dot3[r] += G3[ct][r] * kv;
+      if (i < nrow) {
+        const size_t off = tok_off(b, r0 + i, h, a.T, a.H, DK) + c;
+        a.dqc[off] = dq;
+        dqc_io[off] = to<T>(dq);
+        a.dk_bb[off] = dk;
+        dl[r] -= dq * a.corr[off];
+      }
+    }
+  }
+  float xt = 0.f;  // sum over this wave's rows of e^{gamma_C - gamma_i} (G3_i . k_i)
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int i = 16 * w + 4 * g4 + r;
+    const float d1 = row16_sum(dot1[r]), d2 = row16_sum(dot2[r]), d3 = row16_sum(dot3[r]);
+    const float rf = row16_sum(rowF[r]), ra = row16_sum(rowA[r]);
+    const float dlam = row16_sum(dl[r]);
+    const float G = __expf(sGam[i]), bt = sBeta[i];
+    const float colF = sColF[0][i] + sColF[1][i] + sColF[2][i] + sColF[3][i];
+    const float colA = sColA[0][i] + sColA[1][i] + sColA[2][i] + sColA[3][i];
+    const float rvi = sRV[0][i] + sRV[1][i] + sRV[2][i] + sRV[3][i];
+    const float dg = G * d1 + rf - colF - bt * G * d2 + bt * ra - colA - sDec[i] * d3;
+    if (c16 == 0) {
+      sDg[i] = i < nrow ? dg : 0.f;
+      xt += i < nrow ? sDec[i] * d3 : 0.f;
+      if (i < nrow) {
+        const size_t ti = ((size_t)b * a.T + r0 + i) * a.H + h;
+        a.dbeta[ti] = rvi - G * d2 + ra;
+        a.dlam[ti] = dlam;
+      }
+    }
+  }
+  xt += __shfl_xor(xt, 16);
+  xt += __shfl_xor(xt, 32);
+  if (l == 0) sRed[1][w] = xt;
+  __syncthreads();
+  if (w == 0) {
+    // the last row of the chunk also carries the derivative through gamma_C
+    float x = sDg[l];
+    if (l == nrow - 1)
+      x += (sRed[1][0] + sRed[1][1] + sRed[1][2] + sRed[1][3]) +
+           eC * (sRed[0][0] + sRed[0][1] + sRed[0][2] + sRed[0][3]);
+    // suffix sum: dlogalpha_s = sum_{i >= s} dgamma_i
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const float y = __shfl_down(x, off);
+      if (l + off < 64) x += y;
+    }
+    if (l < nrow) a.dlogalpha[((size_t)b * a.T + r0 + l) * a.H + h] = x;
+  }
+}
+
+namespace {
+template <typename T, int DK>
+hipError_t run_prep(const GdnPrepArgs& a, hipStream_t st) {
+  const int nblk = a.B * a.H * ((a.T + kChunk - 1) / kChunk);
+  if (nblk == 0) return hipSuccess;
+  hipLaunchKernelGGL((gdn_bwd_prep_kernel<T, DK>), dim3(nblk), dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
+template <typename T, int DK, int NPR>
+hipError_t run_dstate_v(const GdnDstateArgs& a, hipStream_t st) {
+  const int nblk = a.B * a.H * (a.dv / (16 * NPR));
+  if (nblk == 0) return hipSuccess;
+  hipLaunchKernelGGL((gdn_dstate_kernel<T, DK, NPR>), dim3(nblk), dim3(64 * NPR), 0, st, a);
+  return hipGetLastError();
+}
+// Four value tiles per workgroup where that still gives every compute unit a
+// workgroup, else two.
+template <typename T, int DK>
+hipError_t run_dstate(const GdnDstateArgs& a, hipStream_t st) {
+  if ((long long)a.B * a.H * (a.dv / 64) >= 256) return run_dstate_v<T, DK, 4>(a, st);
+  return run_dstate_v<T, DK, 2>(a, st);
+}
+template <typename T, int DK>
+hipError_t run_bwd_chunk(const GdnBwdArgs& a, hipStream_t st) {
+  const int nblk = a.B * a.H * ((a.T + kChunk - 1) / kChunk);
+  if (nblk == 0) return hipSuccess;
+  constexpr int BV = sizeof(T) == 2 ? 64 : 32;
+  hipLaunchKernelGGL((gdn_bwd_chunk_kernel<T, DK, BV>), dim3(nblk), dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_gdn_bwd_prep(const GdnPrepArgs& a, bool is_bf16, hipStream_t st) {
+  if (is_bf16) {
+    switch (a.dk) {
+      case 64: return run_prep<bf16_t, 64>(a, st);
+      case 128: return run_prep<bf16_t, 128>(a, st);
+    }
+  } else if (a.dk == 64) {
+    return run_prep<float, 64>(a, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_gdn_dstate(const GdnDstateArgs& a, bool is_bf16, hipStream_t st) {
+  if (is_bf16) {
+    switch (a.dk) {
+      case 64: return run_dstate<bf16_t, 64>(a, st);
+      case 128: return run_dstate<bf16_t, 128>(a, st);
+    }
+  } else if (a.dk == 64) {
+    return run_dstate<float, 64>(a, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_gdn_bwd_chunk(const GdnBwdArgs& a, bool is_bf16, hipStream_t st) {
+  if (is_bf16) {
+    switch (a.dk) {
+      case 64: return run_bwd_chunk<bf16_t, 64>(a, st);
+      case 128: return run_bwd_chunk<bf16_t, 128>(a, st);
+    }
+  } else if (a.dk == 64) {
+    return run_bwd_chunk<float, 64>(a, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace ccq

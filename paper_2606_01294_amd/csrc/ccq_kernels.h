@@ -186,6 +186,55 @@ struct CcqDkArgs {
   int centered;
 };
 
+// ---- training step (CCQ-Gated DeltaNet backward) ----
+// Per chunk, with the forward's Tm = (I + A)^{-1}: the decayed causal scores
+// transposed, PT[j][i] = e^{gamma_i - gamma_j} (qc_i . k_j) for j <= i (else 0),
+// plain row-major, and Tm^T with every row in acc_pos order.
+struct GdnPrepArgs {
+  const void* qc;        // [B,T,H,dk] io (cleaned queries)
+  const void* k;         // [B,T,H,dk] io
+  const float* gam;      // forward workspace, as TriArgs
+  const void* Tm;        // forward workspace, as TriArgs
+  void* PT;              // [B*H, N, C, C] io
+  void* TmT;             // [B*H, N, C, C] io
+  int B, T, H, dk, dv;
+};
+
+// Reverse scan of the state adjoint D = dS_{r+1} over the chunks of one head:
+//   dU = PT (s dO) + diag(e^{gamma_C - gamma}) K D^T,   dR = Tm^T dU,
+//   D <- e^{gamma_C} D + (s dO)^T diag(e^gamma) Qc - dR^T diag(beta e^gamma) K.
+// Stores D (the adjoint of the state leaving each chunk) and dR.
+struct GdnDstateArgs {
+  const void* qc; const void* k; const void* dO;
+  const float* gam;      // forward workspace, as TriArgs
+  const void* PT;        // as GdnPrepArgs
+  const void* TmT;       // as GdnPrepArgs
+  void* dstates;         // [B*H, N, dv, dk] io, plain row-major
+  void* dR;              // [B,T,H,dv] io
+  int B, T, H, dk, dv;
+  float scale;
+};
+
+// Chunk-parallel Gated DeltaNet gradients given S_r, U, dS_{r+1} and dR.
+struct GdnBwdArgs {
+  const void* qc; const void* k; const void* v; const void* dO;
+  const float* gam;      // forward workspace, as TriArgs
+  const void* states;    // forward workspace S_r, as GdnArgs (fragment-native)
+  const void* U;         // forward workspace U^T, as GdnArgs (fragment-native)
+  const void* dstates;   // as GdnDstateArgs
+  const void* dR;        // as GdnDstateArgs
+  const float* corr;     // Sigma_t q_t, [B,T,H,dk] fp32
+  float* dqc;            // dL/dq_clean [B,T,H,dk] fp32
+  void* dqc_io;          // same, io dtype
+  float* dk_bb;          // backbone part of dL/dk [B,T,H,dk] fp32
+  void* dv_out;          // [B,T,H,dv] io
+  float* dlogalpha;      // [B,T,H]
+  float* dbeta;          // [B,T,H]
+  float* dlam;           // [B,T,H]
+  int B, T, H, dk, dv;
+  float scale;
+};
+
 // Each launcher returns hipSuccess or the launch error.  is_bf16 selects the
 // io dtype (bf16 or fp32); shapes are validated by the caller.
 hipError_t launch_clean_gram(const CleanArgs& a, bool is_bf16, hipStream_t st);
@@ -218,6 +267,9 @@ hipError_t launch_gla_bwd_chunk(const GlaBwdArgs& a, bool is_bf16, bool gate_bf1
 hipError_t launch_gla_dg(const DgArgs& a, bool gate_bf16, hipStream_t st);
 hipError_t launch_ccq_dk(const CcqDkArgs& a, bool is_bf16, hipStream_t st);
 bool bwd_supported(int dk, int dv, bool is_bf16);
+hipError_t launch_gdn_bwd_prep(const GdnPrepArgs& a, bool is_bf16, hipStream_t st);
+hipError_t launch_gdn_dstate(const GdnDstateArgs& a, bool is_bf16, hipStream_t st);
+hipError_t launch_gdn_bwd_chunk(const GdnBwdArgs& a, bool is_bf16, hipStream_t st);
 
 // Supported-shape predicates (used by validation before any launch).
 bool clean_supported(int dk, bool is_bf16);

@@ -39,7 +39,7 @@ class Workload:
         return self.B * self.T
 
 
-# The five layer shapes the benchmark and the parity tests use.
+# The layer shapes the benchmark and the parity tests use.
 WORKLOADS = {
     "gla_small_fp32": Workload("gla_small_fp32", GLA, 1, 256, 2, 64, 64, torch.float32, 0),
     "gla_500m_t2k": Workload("gla_500m_t2k", GLA, 8, 2048, 4, 128, 256, torch.bfloat16, 1),
@@ -47,6 +47,8 @@ WORKLOADS = {
     "gla_500m_t20k": Workload("gla_500m_t20k", GLA, 1, 20480, 4, 128, 256, torch.bfloat16, 3),
     "gdn_1p3b_t20k": Workload("gdn_1p3b_t20k", GDN, 1, 20480, 8, 256, 256, torch.bfloat16, 3),
     "gla_train_t4k": Workload("gla_train_t4k", GLA, 4, 4096, 8, 128, 256, torch.bfloat16, 4,
+                              train=True),
+    "gdn_train_t4k": Workload("gdn_train_t4k", GDN, 4, 4096, 8, 128, 256, torch.bfloat16, 4,
                               train=True),
 }
 

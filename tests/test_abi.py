@@ -112,7 +112,10 @@ def test_training_entry_point_validation():
     assert ccq.ccq_workspace_size(shape(), ccq.CCQ_GLA, True) > ccq.ccq_workspace_size(
         shape(), ccq.CCQ_GLA, False)
     assert ccq.ccq_workspace_size(shape(dk=256), ccq.CCQ_GDN, True) == 0
-    assert call_bwd(shape(dk=256), bb=1) == 2               # no Gated DeltaNet backward
+    assert ccq.ccq_workspace_size(shape(), ccq.CCQ_GDN, True) > ccq.ccq_workspace_size(
+        shape(), ccq.CCQ_GDN, False)
+    assert call_bwd(shape(dk=256), bb=1) == 2               # no training step at dk = 256
+    assert call_bwd(shape(), bb=1) == 1                     # Gated DeltaNet needs beta, dbeta
     s = shape()
     s.t0 = 5
     assert call_bwd(s) == 1                                 # training starts from zero state
