@@ -182,9 +182,34 @@ FwdLayout fwd_layout(const ccq_shape* s, ccq_backbone bb) {
   return L;
 }
 
+// Suffix statistics of the contraction's key gradient (ccq_dk).
+struct DkWs {
+  size_t hseg = 0, dseg = 0, dchunk = 0;
+};
+
+template <typename Take>
+DkWs take_dk_ws(const ccq_shape* s, Take&& take) {
+  const size_t bh = (size_t)s->B * s->H, dk = s->dk;
+  const size_t nc = (s->T + 63) / 64, seg = ccq::clean_seg((long long)bh, (long long)nc);
+  const size_t ns = (nc + seg - 1) / seg;
+  DkWs d;
+  d.hseg = take(bh * ns * dk * dk * 4);
+  d.dseg = take(bh * ns * dk * 4);
+  d.dchunk = take(bh * nc * dk * 4);
+  return d;
+}
+
+void set_dk_ws(ccq::CcqDkArgs& ka, const ccq_shape* s, char* ws, const DkWs& d) {
+  ka.seg = ccq::clean_seg((long long)s->B * s->H, (s->T + 63) / 64);
+  ka.hseg = reinterpret_cast<float*>(ws + d.hseg);
+  ka.dseg = reinterpret_cast<float*>(ws + d.dseg);
+  ka.dchunk = reinterpret_cast<float*>(ws + d.dchunk);
+}
+
 struct BwdLayout {
   size_t qclean, corr, mdq, mdu, states, dstates, dqc, dqc_io, dkg, db, dbt, total;
   CleanWs clean;
+  DkWs dkws;
 };
 
 BwdLayout bwd_layout(const ccq_shape* s) {
@@ -206,6 +231,7 @@ BwdLayout bwd_layout(const ccq_shape* s) {
   L.db = take(ntok * s->dk * 4);
   L.dbt = take(nchunk * s->dk * 4);
   L.clean = take_clean_ws(s, take);
+  L.dkws = take_dk_ws(s, take);
   L.total = off;
   return L;
 }
@@ -215,6 +241,7 @@ BwdLayout bwd_layout(const ccq_shape* s) {
 struct GdnBwdLayout {
   size_t qclean, corr, mdq, mdu, states, Tm, gam, U, PT, TmT, dstates, dR, dqc, dqc_io, dkb, total;
   CleanWs clean;
+  DkWs dkws;
 };
 
 GdnBwdLayout gdn_bwd_layout(const ccq_shape* s) {
@@ -240,6 +267,7 @@ GdnBwdLayout gdn_bwd_layout(const ccq_shape* s) {
   L.dqc_io = take(ntok * s->dk * e);
   L.dkb = take(ntok * s->dk * 4);
   L.clean = take_clean_ws(s, take);
+  L.dkws = take_dk_ws(s, take);
   L.total = off;
   return L;
 }
@@ -407,6 +435,7 @@ ccq_status gdn_fwd_bwd(const ccq_shape* s, const void* q, const void* k, const v
   if (traced(st, [&] { return ccq::launch_clean_out(c2, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   ccq::CcqDkArgs ka{q, k, ws + L.dqc_io, lam, mdq, mdu, dkb, dk, s->B, s->T, s->H, s->dk,
                     s->centered};
+  set_dk_ws(ka, s, ws, L.dkws);
   if (traced(st, [&] { return ccq::launch_ccq_dk(ka, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   return CCQ_OK;
 }
@@ -515,6 +544,7 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
   if (traced(st, [&] { return ccq::launch_clean_out(c2, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   ccq::CcqDkArgs ka{q, k, ws + L.dqc_io, lam, mdq, mdu, dkg, dk, s->B, s->T, s->H, s->dk,
                     s->centered};
+  set_dk_ws(ka, s, ws, L.dkws);
   if (traced(st, [&] { return ccq::launch_ccq_dk(ka, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   return CCQ_OK;
 }

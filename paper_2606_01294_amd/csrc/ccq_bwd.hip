@@ -69,7 +69,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_dstate_kernel(const DstateArg
   if (N > 0) prefetch(N - 1);
 
   for (int ci = N - 1; ci >= 0; --ci) {
-    __syncthreads();  // (A)
+    lds_barrier();  // (A)
     rg.store_f32(sG, LDG);
     rdo.store_t(sdOT, LDT);
     {  // adjoint of the state leaving chunk ci
@@ -81,7 +81,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_dstate_kernel(const DstateArg
         for (int r = 0; r < 4; ++r) out[(size_t)(16 * tv + 4 * g4 + r) * DK + 16 * tc + c16] = to<T>(dS[u][r]);
       }
     }
-    __syncthreads();  // (B)
+    lds_barrier();  // (B)
     if (tid < DK) {
       float x[C];
 #pragma unroll
@@ -92,7 +92,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_dstate_kernel(const DstateArg
       for (int j = 0; j < C; ++j) sG[j * LDG + tid] = x[j];
       sDec[tid] = __expf(x[C - 1]);
     }
-    __syncthreads();  // (C)
+    lds_barrier();  // (C)
     {  // (qc * e^{b})^T, e^{b} <= 1
       const int j = ChunkTile<T, DK>::row();
 #pragma unroll
@@ -104,7 +104,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_dstate_kernel(const DstateArg
       }
     }
     if (ci > 0) prefetch(ci - 1);
-    __syncthreads();  // (D)
+    lds_barrier();  // (D)
 #pragma unroll
     for (int u = 0; u < NPW; ++u) {
       const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
@@ -180,7 +180,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
     rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), gsk, nrow);
     rg.load(gate + tok_off(b, r0, h, a.T, a.H, DK), gsk, nrow);
     rg.store_f32(sG, LDG);
-    __syncthreads();
+    lds_barrier();
     if (tid < DK) {
       float x[C];
 #pragma unroll
@@ -192,7 +192,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
       sBm[tid] = __expf(x[C / 2 - 1]);
       sBCm[tid] = __expf(x[C - 1] - x[C / 2 - 1]);
     }
-    __syncthreads();
+    lds_barrier();
     const int j = ChunkTile<T, DK>::row();
 #pragma unroll
     for (int u = 0; u < ChunkTile<T, DK>::NV; ++u) {
@@ -211,7 +211,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
       *reinterpret_cast<typename ChunkTile<T, DK>::vec_t*>(sKt + j * LDQ + c0) = ko;
     }
   }
-  __syncthreads();
+  lds_barrier();
 #pragma unroll
   for (int J = 0; J < 4; ++J) {
     f32x4 acc = zero4();
@@ -222,7 +222,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
       sAqkT[jj * LDT + i] = to<T>((J <= w && jj <= i) ? a.scale * acc[r] : 0.f);
     }
   }
-  __syncthreads();  // sQt is dead from here on
+  lds_barrier();  // sQt is dead from here on
 
   // ---- phase 2: loop over value slices
   f32x4 X1[NTC], X2[NTC], Adv[4];
@@ -255,7 +255,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
       rdo.store(sdO, LDV);
       rdo.store_t(sdOT, LDT);
     }
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
     for (int ct = 0; ct < NTC; ++ct) {
       tile_mma<T, BV>(X1[ct], sdO + 16 * w * LDV, LDV, sSrT + 16 * ct * LDV, LDV);
@@ -276,7 +276,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
         if (jr < nrow) dvout[tok_off(b, r0 + jr, h, a.T, a.H, a.dv) + vv0 + 16 * tn + c16] = to<T>(acc[r]);
       }
     }
-    __syncthreads();
+    lds_barrier();
   }
 
   // ---- phase 3: intra terms with A_dv[t][j] = dO_t . v_j (j <= t)
@@ -289,7 +289,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
       sAdv[i * LDT + jj] = val;
       sAdvT[jj * LDT + i] = val;
     }
-  __syncthreads();
+  lds_barrier();
   f32x4 Y2[NTC];
 #pragma unroll
   for (int ct = 0; ct < NTC; ++ct) {
@@ -297,7 +297,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
     Y2[ct] = zero4();
     tile_mma<T, C>(Y2[ct], sAdvT + 16 * w * LDT, LDT, sQtT + 16 * ct * LDT, LDT);
   }
-  __syncthreads();  // sAdv/sAdvT dead: sTot may reuse the region
+  lds_barrier();  // sAdv/sAdvT dead: sTot may reuse the region
 
   // ---- phase 4: epilogue per element (row i of stripe w, key channel c)
   T* dqc_io = static_cast<T*>(a.dqc_io);
@@ -340,7 +340,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
     x += __shfl_xor(x, 32);
     if (g4 == 0) sTot[w * DK + 16 * ct + c16] = x;
   }
-  __syncthreads();
+  lds_barrier();
   if (tid < DK)
     a.db_tot[((size_t)bh * N + ci) * DK + tid] =
         sTot[tid] + sTot[DK + tid] + sTot[2 * DK + tid] + sTot[3 * DK + tid];
@@ -378,23 +378,136 @@ __global__ __launch_bounds__(kThreads) void gla_dg_kernel(const DgArgs a) {
 }
 
 // ----------------------------------------------------------------------------
-// Key gradient of the contraction: reverse scan over chunks per (head, CT
-// output columns).  Carried: H = sum_{later t} rho_t (u_t q_t^T + q_t u_t^T)
-// (rows n0..n0+CT as fp32 accumulators) and the mean-term vector
-// D = sum_{later t} (lam_t/t^2) (u_t (m_t.q_t) + q_t (m_t.u_t)).  Within the
-// chunk, with j <= t:
-//   W1[t][j] = q_t . k_j - (m_t.q_t)/t     applied to rho_t u_t
-//   W2[t][j] = rho_t (u_t . k_j - (m_t.u_t)/t)   applied to q_t
-// so dk_j = H k_j + D + sum_{t>=j} (W1[t][j] rho_t u_t + W2[t][j] q_t).
-template <typename T, int DK, int CT>
+// Key gradient of the contraction, dk_j = H_j k_j + D_j + (within-chunk terms),
+// with the suffix sums over later tokens
+//   H_j = sum_{t > chunk of j} rho_t (u_t q_t^T + q_t u_t^T),  rho_t = -lam_t / t,
+//   D_j = sum_{t > chunk of j} (lam_t/t^2) (u_t (m_t.q_t) + q_t (m_t.u_t)).
+// Both are plain (undecayed) sums, so the chunks are cut into segments of
+// `seg`: ccq_dk_stats_kernel forms every segment's H and D and every chunk's
+// D (one workgroup per segment, all segments in parallel), and
+// ccq_dk_kernel starts each segment from the sum over the later segments and
+// walks the segment's chunks from last to first.
+template <typename T, int DK>
+__global__ __launch_bounds__(kThreads, 1) void ccq_dk_stats_kernel(const CcqDkArgs a) {
+  constexpr int C = kChunk;
+  constexpr int P = Pad<T>::value;
+  constexpr int LDT = C + P;
+  constexpr int NT16 = DK / 16, NPW = NT16 * NT16 / 4;
+  constexpr int NPART = kThreads / DK;
+  static_assert(NPW >= 1 && kThreads % DK == 0, "tile split");
+
+  __shared__ __align__(16) T sQT[DK * LDT];
+  __shared__ __align__(16) T sRUT[DK * LDT];  // (rho u)^T
+  __shared__ float sA[C], sB[C];              // -(m.q)/t and -rho (m.u)/t
+  __shared__ float sDp[kThreads];
+
+  const int N = (a.T + C - 1) / C;
+  const int NS = (N + a.seg - 1) / a.seg;
+  const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int bh = lb / NS, sg = lb % NS;
+  const int b = bh / a.H, h = bh % a.H;
+  const int tid = threadIdx.x, w = wave_id(), l = lane_id();
+  const int g4 = l >> 4, c16 = l & 15;
+  const T* q = static_cast<const T*>(a.q);
+  const T* uu = static_cast<const T*>(a.u);
+  const size_t gs = (size_t)a.H * DK;
+  const int c_begin = sg * a.seg;
+  const int c_end = (c_begin + a.seg) < N ? (c_begin + a.seg) : N;
+
+  f32x4 H[NPW];
+#pragma unroll
+  for (int u = 0; u < NPW; ++u) H[u] = zero4();
+  float dsum = 0.f;
+
+  ChunkTile<T, DK> rq, ru;
+  RowScalar rlam, rmq, rmu;
+  auto prefetch = [&](int ci) {
+    const int r0 = ci * C;
+    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+    rq.load(q + tok_off(b, r0, h, a.T, a.H, DK), gs, nrow);
+    ru.load(uu + tok_off(b, r0, h, a.T, a.H, DK), gs, nrow);
+    const size_t t0i = ((size_t)b * a.T + r0) * a.H + h;
+    const int row = ChunkTile<T, DK>::row();
+    rlam.load(a.lam + t0i, (size_t)a.H, row, nrow);
+    rmq.load(a.mdot_q + t0i, (size_t)a.H, row, nrow);
+    rmu.load(a.mdot_u + t0i, (size_t)a.H, row, nrow);
+  };
+  if (c_begin < c_end) prefetch(c_begin);
+
+  for (int ci = c_begin; ci < c_end; ++ci) {
+    lds_barrier();
+    {
+      const int j = ChunkTile<T, DK>::row();
+      const float tpos = (float)(ci * C + j + 1);
+      const float rho = -rlam.get() / tpos;
+      if (w == 0) {
+        sA[j] = a.centered ? -rmq.get() / tpos : 0.f;
+        sB[j] = a.centered ? -rho * rmu.get() / tpos : 0.f;
+      }
+      rq.store_t(sQT, LDT);
+#pragma unroll
+      for (int u = 0; u < ChunkTile<T, DK>::NV; ++u) {
+        const auto x = ru.get(u);
+        const int c0 = ChunkTile<T, DK>::col(u);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sRUT[(c0 + e) * LDT + j] = to<T>(rho * f32(x[e]));
+      }
+    }
+    if (ci + 1 < c_end) prefetch(ci + 1);
+    lds_barrier();
+#pragma unroll
+    for (int u = 0; u < NPW; ++u) {
+      const int tau = w * NPW + u, tr = tau / NT16, tc = tau % NT16;
+      tile_mma<T, C>(H[u], sRUT + 16 * tr * LDT, LDT, sQT + 16 * tc * LDT, LDT);
+      tile_mma<T, C>(H[u], sQT + 16 * tr * LDT, LDT, sRUT + 16 * tc * LDT, LDT);
+    }
+    {  // this chunk's mean-term vector, NPART threads per key channel
+      const int n = tid % DK, part = tid / DK;
+      float x = 0.f;
+#pragma unroll 8
+      for (int t = part * (C / NPART); t < (part + 1) * (C / NPART); ++t)
+        x += sA[t] * f32(sRUT[n * LDT + t]) + sB[t] * f32(sQT[n * LDT + t]);
+      sDp[tid] = x;
+    }
+    lds_barrier();
+    if (tid < DK) {
+      float x = sDp[tid];
+#pragma unroll
+      for (int p2 = 1; p2 < NPART; ++p2) x += sDp[p2 * DK + tid];
+      a.dchunk[((size_t)bh * N + ci) * DK + tid] = x;
+      dsum += x;
+    }
+  }
+  float* hs = a.hseg + ((size_t)bh * NS + sg) * DK * DK;
+#pragma unroll
+  for (int u = 0; u < NPW; ++u) {
+    const int tau = w * NPW + u, tr = tau / NT16, tc = tau % NT16;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) hs[(size_t)(16 * tr + 4 * g4 + r) * DK + 16 * tc + c16] = H[u][r];
+  }
+  if (tid < DK) a.dseg[((size_t)bh * NS + sg) * DK + tid] = dsum;
+}
+
+// Reverse walk over one segment's chunks per (head, segment).  Wave w owns
+// NTW 16-wide tiles of output columns n and keeps, in MFMA accumulators, the
+// carried H[c][n] for every c (H is symmetric, so these columns are also its
+// rows) and, in registers, D[n]; both start from the sums over the later
+// segments.  Per chunk, with j <= t:
+//   W1[t][j] = q_t . k_j - (m_t.q_t)/t            applied to rho_t u_t
+//   W2[t][j] = rho_t (u_t . k_j - (m_t.u_t)/t)     applied to q_t
+//   dk_j = H k_j + D + sum_{t>=j} (W1[t][j] rho_t u_t + W2[t][j] q_t),
+// then H += sum_t rho_t (u_t q_t^T + q_t u_t^T) and D += the chunk's D.  For
+// bf16, H and the weights W enter the products as a bf16 head plus a bf16 tail.
+template <typename T, int DK>
 __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) {
   constexpr int C = kChunk;
   constexpr int P = Pad<T>::value;
   constexpr bool kSplit = sizeof(T) == 2;
   constexpr int LDQ = DK + P, LDT = C + P, LDA = C + P;
-  constexpr int NTILE_COL = DK / 16;
-  constexpr int NPW = CT * DK / (16 * 16 * 4);
-  static_assert(NPW >= 1, "tile split");
+  constexpr int NCT = DK / 16;  // 16-row tiles of the contraction index c
+  constexpr int NTW = DK / 64;  // output column tiles per wave
+  constexpr int NK = DK / 32;
+  static_assert(NTW >= 1, "column split");
 
   __shared__ __align__(16) T sQ[C * LDQ];
   __shared__ __align__(16) T sU[C * LDQ];
@@ -405,16 +518,12 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
   __shared__ __align__(16) T sW1l[kSplit ? C * LDA : 8];
   __shared__ __align__(16) T sW2h[C * LDA];
   __shared__ __align__(16) T sW2l[kSplit ? C * LDA : 8];
-  __shared__ __align__(16) T sHh[CT * LDQ];
-  __shared__ __align__(16) T sHl[kSplit ? CT * LDQ : 8];
   __shared__ float sRho[C], sMq[C], sMu[C];
-  __shared__ float sD[CT];
 
-  const int ntiles = DK / CT;
   const int N = (a.T + C - 1) / C;
+  const int NS = (N + a.seg - 1) / a.seg;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int bh = lb / ntiles;
-  const int n0 = (lb % ntiles) * CT;
+  const int bh = lb / NS, sg = lb % NS;
   const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
@@ -423,11 +532,40 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
   const T* uu = static_cast<const T*>(a.u);
   T* dk_out = static_cast<T*>(a.dk_out);
   const size_t gs = (size_t)a.H * DK;
+  const int c_begin = sg * a.seg;
+  const int c_end = (c_begin + a.seg) < N ? (c_begin + a.seg) : N;
 
-  f32x4 H[NPW];
+  // the weights' tiles above the diagonal stay zero
+  for (int idx = tid; idx < C * LDA; idx += kThreads) {
+    sW1h[idx] = to<T>(0.f);
+    sW2h[idx] = to<T>(0.f);
+    if constexpr (kSplit) {
+      sW1l[idx] = to<T>(0.f);
+      sW2l[idx] = to<T>(0.f);
+    }
+  }
+
+  // the sums over the later segments
+  f32x4 Hc[NCT][NTW];
+  float dreg[NTW];
 #pragma unroll
-  for (int u = 0; u < NPW; ++u) H[u] = zero4();
-  if (tid < CT) sD[tid] = 0.f;
+  for (int x = 0; x < NTW; ++x) {
+    dreg[x] = 0.f;
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) Hc[ct][x] = zero4();
+  }
+  for (int s2 = sg + 1; s2 < NS; ++s2) {
+    const float* hs = a.hseg + ((size_t)bh * NS + s2) * DK * DK;
+#pragma unroll
+    for (int x = 0; x < NTW; ++x) {
+      const int n = 16 * (w * NTW + x) + c16;
+      dreg[x] += a.dseg[((size_t)bh * NS + s2) * DK + n];
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Hc[ct][x][r] += hs[(size_t)(16 * ct + 4 * g4 + r) * DK + n];
+    }
+  }
 
   ChunkTile<T, DK> rq, ru, rk;
   RowScalar rlam, rmq, rmu;
@@ -443,12 +581,12 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
     rmq.load(a.mdot_q + t0i, (size_t)a.H, row, nrow);
     rmu.load(a.mdot_u + t0i, (size_t)a.H, row, nrow);
   };
-  if (N > 0) prefetch(N - 1);
+  if (c_begin < c_end) prefetch(c_end - 1);
 
-  for (int ci = N - 1; ci >= 0; --ci) {
+  for (int ci = c_end - 1; ci >= c_begin; --ci) {
     const int r0 = ci * C;
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-    __syncthreads();  // (A)
+    lds_barrier();  // (A)
     {
       const int j = ChunkTile<T, DK>::row();
       const float tpos = (float)(r0 + j + 1);
@@ -470,103 +608,135 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
         for (int e = 0; e < 8; ++e) sRUT[(c0 + e) * LDT + j] = to<T>(rho * f32(x[e]));
       }
     }
-    // carried H (later chunks) as the B^T operand of the inter-chunk product
+    float dcv[NTW];  // this chunk's D, added after its outputs
 #pragma unroll
-    for (int u = 0; u < NPW; ++u) {
-      const int tau = w * NPW + u, tr = tau / NTILE_COL, tc = tau % NTILE_COL;
+    for (int x = 0; x < NTW; ++x) dcv[x] = a.dchunk[((size_t)bh * N + ci) * DK + 16 * (w * NTW + x) + c16];
+    // the backbone's part of dk for this wave's outputs, requested before the products
+    float dkg[NTW][4][4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int n = 16 * tr + 4 * g4 + r, c = 16 * tc + c16;
+    for (int x = 0; x < NTW; ++x)
+#pragma unroll
+      for (int J = 0; J < 4; ++J)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int jr = 16 * J + 4 * g4 + r;
+          dkg[x][J][r] = a.dk_gla[tok_off(b, r0 + (jr < nrow ? jr : nrow - 1), h, a.T, a.H, DK) +
+                                  16 * (w * NTW + x) + c16];
+        }
+    if (ci > c_begin) prefetch(ci - 1);
+    lds_barrier();  // (B)
+
+    // intra weights: the ten tiles on or below the diagonal, over the waves
+#pragma unroll
+    for (int s3 = 0; s3 < 3; ++s3) {
+      const int t = w + 4 * s3;
+      if (t < 10) {
+        const int I = intra_tile_row(t), J = intra_tile_col(t);
+        f32x4 s1 = zero4(), s2 = zero4();
+        tile_mma<T, DK>(s1, sQ + 16 * I * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+        tile_mma<T, DK>(s2, sU + 16 * I * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int tt = 16 * I + 4 * g4 + r, jj = 16 * J + c16;
+          const bool on = jj <= tt;
+          const float w1 = on ? s1[r] - sMq[tt] : 0.f;
+          const float w2 = on ? sRho[tt] * (s2[r] - sMu[tt]) : 0.f;
+          if constexpr (kSplit) {
+            bf16_t hi, lo;
+            split_bf16(w1, hi, lo);
+            sW1h[jj * LDA + tt] = hi;
+            sW1l[jj * LDA + tt] = lo;
+            split_bf16(w2, hi, lo);
+            sW2h[jj * LDA + tt] = hi;
+            sW2l[jj * LDA + tt] = lo;
+          } else {
+            sW1h[jj * LDA + tt] = w1;
+            sW2h[jj * LDA + tt] = w2;
+          }
+        }
+      }
+    }
+    lds_barrier();  // (C)
+
+    // dk rows j (all four row tiles), this wave's columns n
+#pragma unroll
+    for (int x = 0; x < NTW; ++x) {
+      const int nt = w * NTW + x;
+      Frag<T> hh[NK], hl[NK];
+#pragma unroll
+      for (int m = 0; m < NK; ++m) {
         if constexpr (kSplit) {
-          bf16_t hi, lo;
-          split_bf16(H[u][r], hi, lo);
-          sHh[n * LDQ + c] = hi;
-          sHl[n * LDQ + c] = lo;
+          const f32x4 p0 = Hc[2 * m][x], p1 = Hc[2 * m + 1][x];
+          hh[m] = acc_pair_frag<T>(p0, p1);
+          f32x4 r0v, r1v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            r0v[e] = p0[e] - f32(hh[m].v[e]);
+            r1v[e] = p1[e] - f32(hh[m].v[4 + e]);
+          }
+          hl[m] = acc_pair_frag<T>(r0v, r1v);
         } else {
-          sHh[n * LDQ + c] = H[u][r];
+          hh[m] = acc_pair_frag<T>(Hc[2 * m][x], Hc[2 * m + 1][x]);
+        }
+      }
+      Frag<T> f1[2], f2[2];
+#pragma unroll
+      for (int m2 = 0; m2 < 2; ++m2) {
+        f1[m2] = ld_frag(sRUT + 16 * nt * LDT + 32 * m2, LDT);
+        f2[m2] = ld_frag(sQT + 16 * nt * LDT + 32 * m2, LDT);
+      }
+#pragma unroll
+      for (int J = 0; J < 4; ++J) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int m = 0; m < NK; ++m) {
+          const Frag<T> kf = ld_frag_acc(sK + 16 * J * LDQ + 32 * m, (size_t)LDQ);
+          mma(acc, kf, hh[m]);
+          if constexpr (kSplit) mma(acc, kf, hl[m]);
+        }
+#pragma unroll
+        for (int m2 = 0; m2 < 2; ++m2) {
+          mma(acc, ld_frag(sW1h + 16 * J * LDA + 32 * m2, LDA), f1[m2]);
+          mma(acc, ld_frag(sW2h + 16 * J * LDA + 32 * m2, LDA), f2[m2]);
+          if constexpr (kSplit) {
+            mma(acc, ld_frag(sW1l + 16 * J * LDA + 32 * m2, LDA), f1[m2]);
+            mma(acc, ld_frag(sW2l + 16 * J * LDA + 32 * m2, LDA), f2[m2]);
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int jr = 16 * J + 4 * g4 + r;
+          if (jr < nrow) {
+            const size_t off = tok_off(b, r0 + jr, h, a.T, a.H, DK) + 16 * nt + c16;
+            dk_out[off] = to<T>(dkg[x][J][r] + acc[r] + dreg[x]);
+          }
         }
       }
     }
-    if (ci > 0) prefetch(ci - 1);
-    __syncthreads();  // (B)
 
-    // intra weights for pairs j <= t (row stripe w of t)
+    // H += (rho u)^T q + q^T (rho u) for this wave's columns; D += this chunk's D
+    Frag<T> bq[NTW][2], bu[NTW][2];
 #pragma unroll
-    for (int J = 0; J < 4; ++J) {
-      f32x4 s1 = zero4(), s2 = zero4();
-      if (J <= w) {
-        tile_mma<T, DK>(s1, sQ + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
-        tile_mma<T, DK>(s2, sU + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+    for (int x = 0; x < NTW; ++x)
+#pragma unroll
+      for (int m2 = 0; m2 < 2; ++m2) {
+        bq[x][m2] = ld_frag(sQT + 16 * (w * NTW + x) * LDT + 32 * m2, LDT);
+        bu[x][m2] = ld_frag(sRUT + 16 * (w * NTW + x) * LDT + 32 * m2, LDT);
       }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int t = 16 * w + 4 * g4 + r, jj = 16 * J + c16;
-        const bool on = J <= w && jj <= t;
-        const float w1 = on ? s1[r] - sMq[t] : 0.f;
-        const float w2 = on ? sRho[t] * (s2[r] - sMu[t]) : 0.f;
-        if constexpr (kSplit) {
-          bf16_t hi, lo;
-          split_bf16(w1, hi, lo);
-          sW1h[jj * LDA + t] = hi;
-          sW1l[jj * LDA + t] = lo;
-          split_bf16(w2, hi, lo);
-          sW2h[jj * LDA + t] = hi;
-          sW2l[jj * LDA + t] = lo;
-        } else {
-          sW1h[jj * LDA + t] = w1;
-          sW2h[jj * LDA + t] = w2;
-        }
-      }
-    }
-    __syncthreads();  // (C)
-
-    // dk rows of stripe w (key index j), columns [n0, n0 + CT)
+    for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-    for (int tn = 0; tn < CT / 16; ++tn) {
-      f32x4 acc = zero4();
+      for (int m2 = 0; m2 < 2; ++m2) {
+        const Frag<T> au = ld_frag(sRUT + 16 * ct * LDT + 32 * m2, LDT);
+        const Frag<T> aq = ld_frag(sQT + 16 * ct * LDT + 32 * m2, LDT);
 #pragma unroll
-      for (int k0 = 0; k0 < DK; k0 += 32) {
-        const Frag<T> fa = ld_frag(sK + 16 * w * LDQ + k0, LDQ);
-        mma(acc, fa, ld_frag(sHh + 16 * tn * LDQ + k0, LDQ));
-        if constexpr (kSplit) mma(acc, fa, ld_frag(sHl + 16 * tn * LDQ + k0, LDQ));
-      }
-      const T* rut = sRUT + (n0 + 16 * tn) * LDT;
-      const T* qt = sQT + (n0 + 16 * tn) * LDT;
-#pragma unroll
-      for (int k0 = 0; k0 < C; k0 += 32) {
-        const Frag<T> f1 = ld_frag(rut + k0, LDT), f2 = ld_frag(qt + k0, LDT);
-        mma(acc, ld_frag(sW1h + 16 * w * LDA + k0, LDA), f1);
-        mma(acc, ld_frag(sW2h + 16 * w * LDA + k0, LDA), f2);
-        if constexpr (kSplit) {
-          mma(acc, ld_frag(sW1l + 16 * w * LDA + k0, LDA), f1);
-          mma(acc, ld_frag(sW2l + 16 * w * LDA + k0, LDA), f2);
+        for (int x = 0; x < NTW; ++x) {
+          mma(Hc[ct][x], au, bq[x][m2]);
+          mma(Hc[ct][x], aq, bu[x][m2]);
         }
       }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int jr = 16 * w + 4 * g4 + r;
-        const int col = n0 + 16 * tn + c16;
-        if (jr < nrow) {
-          const size_t off = tok_off(b, r0 + jr, h, a.T, a.H, DK) + col;
-          dk_out[off] = to<T>(a.dk_gla[off] + acc[r] + sD[16 * tn + c16]);
-        }
-      }
-    }
-    __syncthreads();  // (D) sD and the H tile have been read
-
-    // H += (rho u)^T q + q^T (rho u) for rows [n0, n0+CT); D += this chunk's mean terms
-#pragma unroll
-    for (int u = 0; u < NPW; ++u) {
-      const int tau = w * NPW + u, tr = tau / NTILE_COL, tc = tau % NTILE_COL;
-      tile_mma<T, C>(H[u], sRUT + (n0 + 16 * tr) * LDT, LDT, sQT + 16 * tc * LDT, LDT);
-      tile_mma<T, C>(H[u], sQT + (n0 + 16 * tr) * LDT, LDT, sRUT + 16 * tc * LDT, LDT);
-    }
-    if (tid < CT) {
-      float s = 0.f;
-      for (int t = 0; t < C; ++t)
-        s -= sMq[t] * f32(sRUT[(n0 + tid) * LDT + t]) + sRho[t] * sMu[t] * f32(sQT[(n0 + tid) * LDT + t]);
-      sD[tid] += s;
-    }
+    for (int x = 0; x < NTW; ++x) dreg[x] += dcv[x];
   }
 }
 
@@ -586,11 +756,17 @@ hipError_t run_bwd_chunk(const GlaBwdArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((gla_bwd_chunk_kernel<T, TG, DK, BV>), dim3(nblk), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
-template <typename T, int DK, int CT>
+template <typename T, int DK>
 hipError_t run_ccq_dk(const CcqDkArgs& a, hipStream_t st) {
-  const int nblk = a.B * a.H * (DK / CT);
-  if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((ccq_dk_kernel<T, DK, CT>), dim3(nblk), dim3(kThreads), 0, st, a);
+  const int N = (a.T + kChunk - 1) / kChunk;
+  if (a.seg <= 0) return hipErrorInvalidValue;
+  const int NS = (N + a.seg - 1) / a.seg;
+  const int nseg = a.B * a.H * NS;
+  if (nseg == 0) return hipSuccess;
+  hipLaunchKernelGGL((ccq_dk_stats_kernel<T, DK>), dim3(nseg), dim3(kThreads), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((ccq_dk_kernel<T, DK>), dim3(nseg), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 template <typename T, typename TG>
@@ -643,10 +819,10 @@ hipError_t launch_gla_dg(const DgArgs& a, bool gate_bf16, hipStream_t st) {
 
 hipError_t launch_ccq_dk(const CcqDkArgs& a, bool is_bf16, hipStream_t st) {
   if (is_bf16) {
-    if (a.dk == 64) return run_ccq_dk<bf16_t, 64, 16>(a, st);
-    if (a.dk == 128) return run_ccq_dk<bf16_t, 128, 32>(a, st);
+    if (a.dk == 64) return run_ccq_dk<bf16_t, 64>(a, st);
+    if (a.dk == 128) return run_ccq_dk<bf16_t, 128>(a, st);
   } else {
-    if (a.dk == 64) return run_ccq_dk<float, 64, 16>(a, st);
+    if (a.dk == 64) return run_ccq_dk<float, 64>(a, st);
   }
   return hipErrorInvalidValue;
 }

@@ -63,7 +63,7 @@ __global__ __launch_bounds__(kThreads) void gdn_bwd_prep_kernel(const GdnPrepArg
     rk.store(sK, LDQ);
     rt.store(sTm, LDP);
   }
-  __syncthreads();
+  lds_barrier();
 
   // wave w: rows i of stripe w against every key tile J; P^T stored as rows j
   T* PT = static_cast<T*>(a.PT) + cidx * C * C;
@@ -159,7 +159,7 @@ __global__ __launch_bounds__(64 * NPR, 1) void gdn_dstate_kernel(const GdnDstate
     const int r0 = ci * C;
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
     const size_t cidx = (size_t)bh * N + ci;
-    __syncthreads();  // every wave is done with the previous chunk's LDS
+    lds_barrier();  // every wave is done with the previous chunk's LDS
     st.rk.store(sK, LDQ);
     st.rp.store(sPT, LDP);
     st.rt.store(sTT, LDP);
@@ -193,7 +193,7 @@ __global__ __launch_bounds__(64 * NPR, 1) void gdn_dstate_kernel(const GdnDstate
       for (int tc = 0; tc < NCT; ++tc) store4(out + 16 * tc, D[tc][0], D[tc][1], D[tc][2], D[tc][3]);
     }
     if (ci > 0) prefetch(ci - 1);
-    __syncthreads();
+    lds_barrier();
 
     // X = K D^T (D^T from the accumulators), rows scaled by e^{gamma_C - gamma_i}
     Frag<T> df[NK];
@@ -304,7 +304,7 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
     rk.store(sK, LDQ);
     rq.store_t(sQT, LDT);
     rk.store_t(sKT, LDT);
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
     for (int J = 0; J < 4; ++J) {
       QK[J] = zero4();
@@ -314,7 +314,7 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
         tile_mma<T, DK>(KK[J], sK + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
       }
     }
-    __syncthreads();  // sQ, sK dead
+    lds_barrier();  // sQ, sK dead
   }
 
   // ---- phase 2: value slices
@@ -383,7 +383,7 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
 #pragma unroll
         for (int e = 0; e < 8; ++e) sU[(32 * m + acc_logical(8 * pp + e)) * LDV + vl] = x[e];
       }
-      __syncthreads();
+      lds_barrier();
 #pragma unroll
       for (int J = 0; J < 4; ++J) {
         if (J <= w) {
@@ -401,10 +401,20 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
         const int c = idx / BV, vl = idx % BV;
         dss += f32(sST[c * LDV + vl]) * f32(sDT[c * LDV + vl]);
       }
-      __syncthreads();
+      lds_barrier();
     }
   }
   sRV[w][l] = rv;
+
+  // Sigma_t q_t for this wave's rows, requested now for the epilogue
+  float cr[NTC][4];
+#pragma unroll
+  for (int ct = 0; ct < NTC; ++ct)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = 16 * w + 4 * g4 + r;
+      cr[ct][r] = a.corr[tok_off(b, r0 + (i < nrow ? i : nrow - 1), h, a.T, a.H, DK) + 16 * ct + c16];
+    }
 
   // ---- phase 3: C x C weights
   T* sPm = reinterpret_cast<T*>(sR);
@@ -449,7 +459,7 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
     for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
     if (l == 0) sRed[0][w] = x;
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- phase 4: dQ, dK and the epilogue (row i = 16w + 4g4 + r, channel c)
   float dot1[4] = {0.f, 0.f, 0.f, 0.f}, dot2[4] = {0.f, 0.f, 0.f, 0.f}, dot3[4] = {0.f, 0.f, 0.f, 0.f};
@@ -478,7 +488,7 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
         a.dqc[off] = dq;
         dqc_io[off] = to<T>(dq);
         a.dk_bb[off] = dk;
-        dl[r] -= dq * a.corr[off];
+        dl[r] -= dq * cr[ct][r];
       }
     }
   }
@@ -507,7 +517,7 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
   xt += __shfl_xor(xt, 16);
   xt += __shfl_xor(xt, 32);
   if (l == 0) sRed[1][w] = xt;
-  __syncthreads();
+  lds_barrier();
   if (w == 0) {
     // the last row of the chunk also carries the derivative through gamma_C
     float x = sDg[l];

@@ -172,7 +172,8 @@ struct DgArgs {
   int B, T, H, dk;
 };
 
-// Key gradient of the contraction (reverse scan of an undecayed dk x dk state).
+// Key gradient of the contraction (suffix sums of an undecayed dk x dk state,
+// formed per segment of chunks, then a reverse walk inside every segment).
 struct CcqDkArgs {
   const void* q;        // [B,T,H,dk] io
   const void* k;        // [B,T,H,dk] io
@@ -184,6 +185,10 @@ struct CcqDkArgs {
   void* dk_out;         // [B,T,H,dk] io
   int B, T, H, dk;
   int centered;
+  int seg;              // chunks per segment (NS = ceil(N / seg) segments)
+  float* hseg;          // [B*H, NS, dk, dk] fp32 workspace: each segment's H
+  float* dseg;          // [B*H, NS, dk] fp32 workspace: each segment's D
+  float* dchunk;        // [B*H, N, dk] fp32 workspace: each chunk's D
 };
 
 // ---- training step (CCQ-Gated DeltaNet backward) ----
