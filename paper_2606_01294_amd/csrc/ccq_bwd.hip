@@ -230,7 +230,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
   for (int ct = 0; ct < NTC; ++ct) { X1[ct] = zero4(); X2[ct] = zero4(); }
 #pragma unroll
   for (int J = 0; J < 4; ++J) Adv[J] = zero4();
-  T* dvout = static_cast<T*>(a.dv_out);
+  T* dvrow = static_cast<T*>(a.dv_out) + tok_off(b, r0, h, a.T, a.H, a.dv);
   for (int vv0 = 0; vv0 < a.dv; vv0 += BV) {
     // states: S_r diag(e^{b_m}) transposed, dS_{r+1} diag(e^{b_C - b_m}) and dS_{r+1}^T
     for (int idx = tid; idx < BV * DK / 8; idx += kThreads) {
@@ -273,7 +273,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int jr = 16 * w + 4 * g4 + r;
-        if (jr < nrow) dvout[tok_off(b, r0 + jr, h, a.T, a.H, a.dv) + vv0 + 16 * tn + c16] = to<T>(acc[r]);
+        if (jr < nrow) dvrow[jr * gsv + vv0 + 16 * tn + c16] = to<T>(acc[r]);
       }
     }
     lds_barrier();
@@ -300,7 +300,24 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
   lds_barrier();  // sAdv/sAdvT dead: sTot may reuse the region
 
   // ---- phase 4: epilogue per element (row i of stripe w, key channel c)
-  T* dqc_io = static_cast<T*>(a.dqc_io);
+  // every global operand of the epilogue requested at once (rows clamped into
+  // the sequence), then the per-element arithmetic
+  const size_t rowoff = tok_off(b, r0, h, a.T, a.H, DK);
+  T* dqc_io = static_cast<T*>(a.dqc_io) + rowoff;
+  float* dqc_f = a.dqc + rowoff;
+  float* dkg_f = a.dk_gla + rowoff;
+  float* db_f = a.db + rowoff;
+  float qv[NTC][4], kv[NTC][4], cv[NTC][4];
+#pragma unroll
+  for (int ct = 0; ct < NTC; ++ct)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = 16 * w + 4 * g4 + r;
+      const int off = (i < nrow ? i : nrow - 1) * (int)gsk + 16 * ct + c16;
+      qv[ct][r] = f32(qc[rowoff + off]);
+      kv[ct][r] = f32(k[rowoff + off]);
+      cv[ct][r] = a.corr[rowoff + off];
+    }
   float tot[NTC];
   float dl[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -315,14 +332,14 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
         const float d = sG[i * LDG + c] - bm;
         const float dqc = a.scale * __expf(d) * X1[ct][r];
         const float dkg = __expf(-d) * (Y2[ct][r] * a.scale + X2[ct][r] * sBCm[c]);
-        const size_t off = tok_off(b, r0 + i, h, a.T, a.H, DK) + c;
-        const float db = f32(qc[off]) * dqc - f32(k[off]) * dkg;
-        a.dqc[off] = dqc;
+        const int off = i * (int)gsk + c;
+        const float db = qv[ct][r] * dqc - kv[ct][r] * dkg;
+        dqc_f[off] = dqc;
         dqc_io[off] = to<T>(dqc);
-        a.dk_gla[off] = dkg;
-        a.db[off] = db;
+        dkg_f[off] = dkg;
+        db_f[off] = db;
         tot[ct] += db;
-        dl[r] -= dqc * a.corr[off];
+        dl[r] -= dqc * cv[ct][r];
       }
     }
   }
@@ -488,6 +505,28 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_stats_kernel(const CcqDkAr
   if (tid < DK) a.dseg[((size_t)bh * NS + sg) * DK + tid] = dsum;
 }
 
+// In place, per head: segment s's H and D become the sums over the later
+// segments s' > s (exclusive suffix sums), four elements per thread.
+__global__ __launch_bounds__(kThreads) void ccq_dk_suffix_kernel(const CcqDkArgs a) {
+  const int N = (a.T + kChunk - 1) / kChunk;
+  const int NS = (N + a.seg - 1) / a.seg;
+  const size_t per = (size_t)a.dk * a.dk + a.dk;  // H and D elements of one segment
+  const size_t i4 = ((size_t)blockIdx.x * kThreads + threadIdx.x) * 4;
+  const int bh = blockIdx.y;
+  if (i4 >= per) return;
+  const bool isH = i4 < (size_t)a.dk * a.dk;
+  float* base = isH ? a.hseg + (size_t)bh * NS * a.dk * a.dk + i4
+                    : a.dseg + (size_t)bh * NS * a.dk + (i4 - (size_t)a.dk * a.dk);
+  const size_t stride = isH ? (size_t)a.dk * a.dk : (size_t)a.dk;
+  f32x4 acc = zero4();
+  for (int s2 = NS - 1; s2 >= 0; --s2) {
+    f32x4* p = reinterpret_cast<f32x4*>(base + s2 * stride);
+    const f32x4 x = *p;
+    *p = acc;
+    acc += x;
+  }
+}
+
 // Reverse walk over one segment's chunks per (head, segment).  Wave w owns
 // NTW 16-wide tiles of output columns n and keeps, in MFMA accumulators, the
 // carried H[c][n] for every c (H is symmetric, so these columns are also its
@@ -545,7 +584,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
     }
   }
 
-  // the sums over the later segments
+  // the sums over the later segments (suffix sums formed by ccq_dk_suffix_kernel)
   f32x4 Hc[NCT][NTW];
   float dreg[NTW];
 #pragma unroll
@@ -554,16 +593,15 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct) Hc[ct][x] = zero4();
   }
-  for (int s2 = sg + 1; s2 < NS; ++s2) {
-    const float* hs = a.hseg + ((size_t)bh * NS + s2) * DK * DK;
+  {  // H[c][n] = H[n][c] (H is symmetric): four consecutive c per load
+    const float* hs = a.hseg + ((size_t)bh * NS + sg) * DK * DK;
 #pragma unroll
     for (int x = 0; x < NTW; ++x) {
       const int n = 16 * (w * NTW + x) + c16;
-      dreg[x] += a.dseg[((size_t)bh * NS + s2) * DK + n];
+      dreg[x] = a.dseg[((size_t)bh * NS + sg) * DK + n];
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) Hc[ct][x][r] += hs[(size_t)(16 * ct + 4 * g4 + r) * DK + n];
+        Hc[ct][x] = *reinterpret_cast<const f32x4*>(hs + (size_t)n * DK + 16 * ct + 4 * g4);
     }
   }
 
@@ -612,6 +650,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
 #pragma unroll
     for (int x = 0; x < NTW; ++x) dcv[x] = a.dchunk[((size_t)bh * N + ci) * DK + 16 * (w * NTW + x) + c16];
     // the backbone's part of dk for this wave's outputs, requested before the products
+    const size_t rowoff = tok_off(b, r0, h, a.T, a.H, DK);
     float dkg[NTW][4][4];
 #pragma unroll
     for (int x = 0; x < NTW; ++x)
@@ -620,8 +659,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int jr = 16 * J + 4 * g4 + r;
-          dkg[x][J][r] = a.dk_gla[tok_off(b, r0 + (jr < nrow ? jr : nrow - 1), h, a.T, a.H, DK) +
-                                  16 * (w * NTW + x) + c16];
+          dkg[x][J][r] = a.dk_gla[rowoff + (jr < nrow ? jr : nrow - 1) * (int)gs + 16 * (w * NTW + x) + c16];
         }
     if (ci > c_begin) prefetch(ci - 1);
     lds_barrier();  // (B)
@@ -707,8 +745,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
         for (int r = 0; r < 4; ++r) {
           const int jr = 16 * J + 4 * g4 + r;
           if (jr < nrow) {
-            const size_t off = tok_off(b, r0 + jr, h, a.T, a.H, DK) + 16 * nt + c16;
-            dk_out[off] = to<T>(dkg[x][J][r] + acc[r] + dreg[x]);
+            dk_out[rowoff + jr * (int)gs + 16 * nt + c16] = to<T>(dkg[x][J][r] + acc[r] + dreg[x]);
           }
         }
       }
@@ -765,6 +802,11 @@ hipError_t run_ccq_dk(const CcqDkArgs& a, hipStream_t st) {
   if (nseg == 0) return hipSuccess;
   hipLaunchKernelGGL((ccq_dk_stats_kernel<T, DK>), dim3(nseg), dim3(kThreads), 0, st, a);
   hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t per4 = ((size_t)DK * DK + DK) / 4;
+  hipLaunchKernelGGL(ccq_dk_suffix_kernel, dim3((unsigned)((per4 + kThreads - 1) / kThreads), a.B * a.H),
+                     dim3(kThreads), 0, st, a);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((ccq_dk_kernel<T, DK>), dim3(nseg), dim3(kThreads), 0, st, a);
   return hipGetLastError();

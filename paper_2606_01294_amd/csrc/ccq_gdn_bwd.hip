@@ -215,6 +215,7 @@ __global__ __launch_bounds__(64 * NPR, 1) void gdn_dstate_kernel(const GdnDstate
       mma(dU[I], ld_frag(sPT + 16 * I * LDP, LDP), of0);
       mma(dU[I], ld_frag(sPT + 16 * I * LDP + 32, LDP), of1);
     }
+    T* dRrow = dRg + tok_off(b, r0, h, a.T, a.H, a.dv) + v;
     // dR = Tm^T dU
     const Frag<T> uf0 = acc_pair_frag<T>(dU[0], dU[1]);
     const Frag<T> uf1 = acc_pair_frag<T>(dU[2], dU[3]);
@@ -230,7 +231,7 @@ __global__ __launch_bounds__(64 * NPR, 1) void gdn_dstate_kernel(const GdnDstate
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int i = 16 * I + 4 * g4 + r;
-        if (i < nrow) dRg[tok_off(b, r0 + i, h, a.T, a.H, a.dv) + v] = to<T>(dR[I][r]);
+        if (i < nrow) dRrow[i * a.H * a.dv] = to<T>(dR[I][r]);
       }
     // D <- e^{gamma_C} D + (G Q)^T dO' - K^T diag(beta G) dR
 #pragma unroll
@@ -334,7 +335,7 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
     const T* Sg = static_cast<const T*>(a.states) + cidx * a.dv * DK;
     const T* Ug = static_cast<const T*>(a.U) + cidx * a.dv * C;
     const T* Dg = static_cast<const T*>(a.dstates) + cidx * a.dv * DK;
-    T* dvout = static_cast<T*>(a.dv_out);
+    T* dvrow = static_cast<T*>(a.dv_out) + tok_off(b, r0, h, a.T, a.H, a.dv);
     typedef T v8 __attribute__((ext_vector_type(8)));
     for (int vv0 = 0; vv0 < a.dv; vv0 += BV) {
       {
@@ -358,7 +359,7 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
           *reinterpret_cast<v8*>(sdO + row * LDV + c0) = yo;
           *reinterpret_cast<v8*>(sdR + row * LDV + c0) = xr;
           *reinterpret_cast<v8*>(sV + row * LDV + c0) = xv;
-          if (row < nrow) *reinterpret_cast<v8*>(dvout + tok_off(b, r0 + row, h, a.T, a.H, a.dv) + vv0 + c0) = yd;
+          if (row < nrow) *reinterpret_cast<v8*>(dvrow + row * (int)gsv + vv0 + c0) = yd;
         }
       }
       // S_r and U^T slices (fragment-native: per value tile and 32-wide k
@@ -407,13 +408,14 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
   sRV[w][l] = rv;
 
   // Sigma_t q_t for this wave's rows, requested now for the epilogue
+  const size_t rowoff = tok_off(b, r0, h, a.T, a.H, DK);
   float cr[NTC][4];
 #pragma unroll
   for (int ct = 0; ct < NTC; ++ct)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int i = 16 * w + 4 * g4 + r;
-      cr[ct][r] = a.corr[tok_off(b, r0 + (i < nrow ? i : nrow - 1), h, a.T, a.H, DK) + 16 * ct + c16];
+      cr[ct][r] = a.corr[rowoff + (i < nrow ? i : nrow - 1) * (int)gsk + 16 * ct + c16];
     }
 
   // ---- phase 3: C x C weights
@@ -484,7 +486,7 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
       dot2[r] += G2[ct][r] * kv;
       dot3[r] += G3[ct][r] * kv;
       if (i < nrow) {
-        const size_t off = tok_off(b, r0 + i, h, a.T, a.H, DK) + c;
+        const size_t off = rowoff + i * (int)gsk + c;
         a.dqc[off] = dq;
         dqc_io[off] = to<T>(dq);
         a.dk_bb[off] = dk;
