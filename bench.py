@@ -6,9 +6,9 @@ dk=128, dv=256) plus one CCQ-Gated-DeltaNet forward on the ~1.3B-layer shape
 (B=4, T=4096, H=8, dk=dv=256), bf16 io, fp32 states, chunk 64, inputs resident
 in HBM.  `value` is the tokens of both calls divided by the mean step time.
 The line also carries the per-kernel HIP-event timings, the roofline of the
-dominant kernel, per-workload figures (including T=20480 and the GLA and Gated
-DeltaNet training steps) and the fp64 CPU oracle timed on a bounded sample of
-the same inputs.
+dominant kernel, per-workload figures (including T=20480, the GLA and Gated
+DeltaNet training steps and the one-token recurrent decode step on the cache)
+and the fp64 CPU oracle timed on a bounded sample of the same inputs.
 
     python bench.py [--gpus 1] [--steps 40] [--warmup 5]
 """
@@ -119,6 +119,10 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
         by = ntok * (3 * dk * io_bytes + 5 * dv * io_bytes + 2 * dv * dk * io_bytes // C
                      + 12 * dk + 28)
         fl = ntok * (6 * dk * dv + 4 * C * dv + 12 * C * dk)
+    elif kernel == "decode":        # cache (S, Cbar fp32) read and written once, mu, q, k, v, gates, o
+        gb = dk * gate_bytes if w.backbone == 0 else 8
+        by = BH * (8 * dv * dk + 8 * dk * dk + dk * (2 * io_bytes + 20) + 2 * dv * io_bytes + gb + 4)
+        fl = BH * (5 * dk * dk + 6 * dv * dk)
     elif kernel == "ccq_dk":
         by = ntok * (3 * dk * io_bytes + 12 + 4 * dk + dk * io_bytes)
         fl = ntok * (6 * dk * dk + 8 * C * dk)
@@ -136,7 +140,7 @@ KERNELS = {0: ["gla_state"] + CLEAN + ["clean_out", "gla_out"],
            "gdn_train": CLEAN + ["clean_out_train", "gdn_tri", "gdn_state", "gdn_out",
                                  "gdn_bwd_prep", "gdn_dstate", "gdn_bwd_chunk", "clean_dq",
                                  "ccq_dk"]}
-KERNEL_SYMBOL = {"clean_gram": "clean_gram_kernel",
+KERNEL_SYMBOL = {"decode": "decode_stats_kernel+decode_out_kernel", "clean_gram": "clean_gram_kernel",
                  "clean_prefix": "clean_prefix_kernel", "clean_out": "clean_out_kernel",
                  "clean_out_train": "clean_out_kernel", "clean_dq": "clean_out_kernel",
                  "gla_state": "gla_state_kernel", "gla_scan": "gla_scan_kernel", "gla_out": "gla_out_kernel",
@@ -154,6 +158,8 @@ def _source(kernel: str) -> str:
         return "ccq_gla.hip"
     if kernel in ("gdn_bwd_prep", "gdn_dstate", "gdn_bwd_chunk"):
         return "ccq_gdn_bwd.hip"
+    if kernel == "decode":
+        return "ccq_decode.hip"
     if kernel.startswith("gdn"):
         return "ccq_gdn.hip"
     return "ccq_bwd.hip"
@@ -232,6 +238,36 @@ class Call:
         else:
             self.ccq.ccq_gdn_fwd(d["q"], d["k"], d["v"], d["logalpha"], d["beta"], d["lam"],
                                  out=self.out, workspace=self.ws)
+
+
+class DecodeCall:
+    """One recurrent decode step (one token per sequence) at position T + 1 of a
+    workload's shape, with the cache resident on the GPU (updated in place)."""
+
+    def __init__(self, w, torch, ccq, inputs):
+        import dataclasses
+        self.w = dataclasses.replace(w, name=w.name.replace("_t", "_decode_t"), T=1)
+        self.t0 = w.T
+        d = inputs.make_inputs(w.backbone, w.B, 1, w.H, w.dk, w.dv, w.dtype, seed=w.seed)
+        self.d = {k: v[:, 0].contiguous().cuda() for k, v in d.items()}
+        dev = self.d["q"].device
+        gen = torch.Generator(device="cpu").manual_seed(w.seed)
+        B, H, dk, dv = w.B, w.H, w.dk, w.dv
+        self.S = (0.1 * torch.randn(B, H, dv, dk, generator=gen)).to(dev)
+        self.C = (torch.randn(B, H, dk, dk, generator=gen) / dk).to(dev)
+        self.mu = (torch.randn(B, H, dk, generator=gen) / dk).to(dev)
+        self.o = torch.empty((B, H, dv), dtype=w.dtype, device=dev)
+        self.ws = torch.empty(max(1, ccq.ccq_decode_workspace_size(
+            ccq.make_shape(B, 1, H, dk, dv, w.dtype))), dtype=torch.uint8, device=dev)
+        self.ccq = ccq
+        self.kernels = ["decode"]
+
+    def __call__(self):
+        d = self.d
+        gate = d["g"] if self.w.backbone == 0 else d["logalpha"]
+        self.ccq.ccq_decode(d["q"], d["k"], d["v"], gate, d["lam"], self.S, self.C, self.mu,
+                            self.t0, backbone=self.w.backbone, beta=d.get("beta"), out=self.o,
+                            workspace=self.ws)
 
 
 def time_calls(torch, ccq, calls, steps, warmup):
@@ -399,6 +435,15 @@ def main(argv=None):
             if c not in step_calls:
                 del c
                 torch.cuda.empty_cache()
+        for name in ("gla_500m_t2k", "gdn_1p3b_t4k"):
+            c = DecodeCall(W[name], torch, ccq, inputs)
+            ms, pk = time_calls(torch, ccq, [c], max(20, args.steps), 5)
+            extra[c.w.name] = {"tokens_per_s": round(c.w.B / (ms * 1e-3), 1), "ms": round(ms, 5),
+                               "position": c.t0 + 1,
+                               "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
+                               "roofline": roofline(pk[0], c.w)}
+            del c
+            torch.cuda.empty_cache()
 
     cpu = None if args.no_cpu_baseline else cpu_baseline(step_calls)
 

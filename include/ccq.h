@@ -127,6 +127,27 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
                        size_t ws_bytes, void* stream);
 
 /*
+ * Recurrent inference, one token per sequence (Alg. 2), on the cache triple
+ * of App. C, updated in place:
+ *   Cbar <- Cbar + (k k^T - Cbar)/t,  mu <- mu + (k - mu)/t,  t = s->t0 + 1;
+ *   q_clean = q - lam (Cbar q - mu (mu . q))   (Cbar q alone when centered = 0);
+ *   S <- BackboneUpdate(S; k, v, gates);  o = scale S q_clean.
+ * s->T must be 1; s->t0 is the number of tokens already absorbed (the cache of
+ * a fresh sequence is all zeros with t0 = 0).  q, k [B,H,dk] and v, o [B,H,dv]
+ * in io_dtype (one token, T = 1, of the [B,T,H,d] layout); GLA gate g [B,H,dk]
+ * gate_dtype; Gated DeltaNet log alpha and beta [B,H] fp32 (beta NULL for GLA);
+ * lam [B,H] fp32.  S [B,H,dv,dk], C [B,H,dk,dk] and mu [B,H,dk] are fp32,
+ * caller-owned, read and overwritten.  Supported: dk in {64,128,256}, dv in
+ * {64,128,256,512}, both backbones and both io dtypes.  The workspace holds
+ * ccq_decode_workspace_size(s) bytes (0 for an unsupported shape).
+ */
+size_t ccq_decode_workspace_size(const ccq_shape* s);
+ccq_status ccq_decode(const ccq_shape* s, ccq_backbone bb, const void* q, const void* k,
+                      const void* v, const void* g_or_logalpha, const float* beta,
+                      const float* lam, float* S, float* C, float* mu, void* o, void* workspace,
+                      size_t ws_bytes, void* stream);
+
+/*
  * Per-kernel timing hook (instrumentation for benchmarks and profilers, not
  * part of the method).  `events` points at n_events hipEvent_t handles created
  * by the caller (hipEventCreate).  Until the next ccq_trace_events call from

@@ -23,7 +23,8 @@ CCQ_GLA, CCQ_GDN = 0, 1
 _STATUS = {0: "CCQ_OK", 1: "CCQ_ERR_INVALID_ARG", 2: "CCQ_ERR_UNSUPPORTED",
            3: "CCQ_ERR_WORKSPACE", 4: "CCQ_ERR_HIP"}
 EXPORTS = ("ccq_workspace_size", "ccq_gla_fwd", "ccq_gdn_fwd", "ccq_fwd_bwd",
-           "ccq_trace_events", "ccq_status_string", "ccq_version")
+           "ccq_decode_workspace_size", "ccq_decode", "ccq_trace_events", "ccq_status_string",
+           "ccq_version")
 
 
 class CcqError(RuntimeError):
@@ -64,6 +65,10 @@ def lib() -> ctypes.CDLL:
             L.ccq_gdn_fwd.restype = ctypes.c_int
             L.ccq_fwd_bwd.argtypes = [SP, ctypes.c_int] + [P] * 15 + [S, P]
             L.ccq_fwd_bwd.restype = ctypes.c_int
+            L.ccq_decode_workspace_size.argtypes = [SP]
+            L.ccq_decode_workspace_size.restype = S
+            L.ccq_decode.argtypes = [SP, ctypes.c_int] + [P] * 11 + [S, P]
+            L.ccq_decode.restype = ctypes.c_int
             L.ccq_trace_events.argtypes = [P, ctypes.c_int]
             L.ccq_trace_events.restype = ctypes.c_int
             L.ccq_status_string.argtypes = [ctypes.c_int]
@@ -249,3 +254,46 @@ def ccq_fwd_bwd(q, k, v, g, lam, dO, scale=1.0, centered=True, chunk=64, out=Non
     if rc != 0:
         raise CcqError("ccq_fwd_bwd", rc)
     return out
+
+
+def ccq_decode_workspace_size(shape: Shape) -> int:
+    return int(lib().ccq_decode_workspace_size(ctypes.byref(shape)))
+
+
+def ccq_decode(q, k, v, gate, lam, S, C, mu, t0, backbone=CCQ_GLA, beta=None, scale=1.0,
+               centered=True, out=None, workspace=None, stream=None):
+    """One recurrent CCQ step per sequence (Alg. 2) on the cache (S, C, mu), which is
+    updated in place.  q, k [B,H,dk] and v [B,H,dv] (one token); GLA gate [B,H,dk],
+    Gated DeltaNet log alpha [B,H] fp32 plus beta [B,H] fp32; lam [B,H] fp32;
+    S [B,H,dv,dk], C [B,H,dk,dk], mu [B,H,dk] fp32; t0 = tokens already absorbed.
+    Returns o [B,H,dv]."""
+    B, H, dk = q.shape
+    dv = v.shape[-1]
+    dev = q.device
+    gate_dtype = gate.dtype if backbone == CCQ_GLA else q.dtype
+    shape = make_shape(B, 1, H, dk, dv, q.dtype, gate_dtype, scale, centered, t0)
+    _check(k, "k", (B, H, dk), q.dtype, dev)
+    _check(v, "v", (B, H, dv), q.dtype, dev)
+    _check(lam, "lam", (B, H), torch.float32, dev)
+    if backbone == CCQ_GLA:
+        _check(gate, "g", (B, H, dk), gate.dtype, dev)
+    else:
+        if beta is None:
+            raise ValueError("beta is required for Gated DeltaNet")
+        _check(gate, "logalpha", (B, H), torch.float32, dev)
+        _check(beta, "beta", (B, H), torch.float32, dev)
+    for t, name, shp in ((S, "S", (B, H, dv, dk)), (C, "C", (B, H, dk, dk)), (mu, "mu", (B, H, dk))):
+        if t is None:
+            raise ValueError("%s (the cache) is required" % name)
+        _check(t, name, shp, torch.float32, dev)
+    o = out if out is not None else torch.empty((B, H, dv), dtype=q.dtype, device=dev)
+    _check(o, "o", (B, H, dv), q.dtype, dev)
+    need = ccq_decode_workspace_size(shape)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    rc = lib().ccq_decode(ctypes.byref(shape), int(backbone), _p(q), _p(k), _p(v), _p(gate),
+                          _p(beta), _p(lam), _p(S), _p(C), _p(mu), _p(o), _p(workspace),
+                          workspace.numel(), _stream(stream))
+    if rc != 0:
+        raise CcqError("ccq_decode", rc)
+    return o

@@ -549,6 +549,41 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
   return CCQ_OK;
 }
 
+size_t ccq_decode_workspace_size(const ccq_shape* s) {
+  if (!s || s->B < 0 || s->H < 0 || !ccq::decode_supported(s->dk, s->dv)) return 0;
+  return align_up((size_t)s->B * s->H * s->dk * sizeof(float));
+}
+
+ccq_status ccq_decode(const ccq_shape* s, ccq_backbone bb, const void* q, const void* k,
+                      const void* v, const void* g_or_logalpha, const float* beta,
+                      const float* lam, float* S, float* C, float* mu, void* o, void* workspace,
+                      size_t ws_bytes, void* stream) {
+  if (!s) return CCQ_ERR_INVALID_ARG;
+  if (s->B < 0 || s->H < 0 || s->t0 < 0 || s->T != 1) return CCQ_ERR_INVALID_ARG;
+  if (!dtype_ok(s->io_dtype) || !dtype_ok(s->gate_dtype)) return CCQ_ERR_INVALID_ARG;
+  if (s->centered != 0 && s->centered != 1) return CCQ_ERR_INVALID_ARG;
+  if (bb != CCQ_GLA && bb != CCQ_GDN) return CCQ_ERR_INVALID_ARG;
+  if (!ccq::decode_supported(s->dk, s->dv)) return CCQ_ERR_UNSUPPORTED;
+  if ((long long)s->B * s->H > 65535) return CCQ_ERR_UNSUPPORTED;  // grid y
+  if (s->B == 0 || s->H == 0) return CCQ_OK;
+  const void* req[] = {q, k, v, g_or_logalpha, lam, S, C, mu, o};
+  for (const void* p : req)
+    if (!p || !aligned(p)) return CCQ_ERR_INVALID_ARG;
+  if (bb == CCQ_GDN && (!beta || !aligned(beta))) return CCQ_ERR_INVALID_ARG;
+  if (!workspace || !aligned(workspace) || ws_bytes < ccq_decode_workspace_size(s))
+    return CCQ_ERR_WORKSPACE;
+  ccq::DecodeArgs a{q, k, v, g_or_logalpha, beta, lam, S, C, mu, static_cast<float*>(workspace), o,
+                    s->B, s->H, s->dk, s->dv, s->centered, s->scale, s->t0};
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  trace_begin_call();
+  if (traced(st, [&] {
+        return ccq::launch_decode(a, bb == CCQ_GDN, s->io_dtype == CCQ_BF16,
+                                  s->gate_dtype == CCQ_BF16, st);
+      }) != hipSuccess)
+    return CCQ_ERR_HIP;
+  return CCQ_OK;
+}
+
 ccq_status ccq_trace_events(void* const* events, int n_events) {
   if (events == nullptr || n_events <= 0) {
     g_trace = Trace{};

@@ -240,6 +240,25 @@ struct GdnBwdArgs {
   float scale;
 };
 
+// ---- recurrent decode (one token per sequence, cache updated in place) ----
+struct DecodeArgs {
+  const void* q;         // [B,H,dk] io
+  const void* k;         // [B,H,dk] io
+  const void* v;         // [B,H,dv] io
+  const void* g;         // GLA: [B,H,dk] gate dtype; Gated DeltaNet: [B,H] fp32 log alpha
+  const float* beta;     // Gated DeltaNet: [B,H] fp32
+  const float* lam;      // [B,H] fp32
+  float* S;              // [B,H,dv,dk] fp32, in place
+  float* C;              // [B,H,dk,dk] fp32 (Cbar), in place
+  float* mu;             // [B,H,dk] fp32, in place
+  float* cq;             // [B,H,dk] fp32 workspace: Cbar_t q
+  void* o;               // [B,H,dv] io
+  int B, H, dk, dv;
+  int centered;
+  float scale;
+  int64_t t0;            // tokens before this one (its position is t0 + 1)
+};
+
 // Each launcher returns hipSuccess or the launch error.  is_bf16 selects the
 // io dtype (bf16 or fp32); shapes are validated by the caller.
 hipError_t launch_clean_gram(const CleanArgs& a, bool is_bf16, hipStream_t st);
@@ -275,6 +294,8 @@ bool bwd_supported(int dk, int dv, bool is_bf16);
 hipError_t launch_gdn_bwd_prep(const GdnPrepArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_gdn_dstate(const GdnDstateArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_gdn_bwd_chunk(const GdnBwdArgs& a, bool is_bf16, hipStream_t st);
+hipError_t launch_decode(const DecodeArgs& a, bool gdn, bool is_bf16, bool gate_bf16, hipStream_t st);
+bool decode_supported(int dk, int dv);
 
 // Supported-shape predicates (used by validation before any launch).
 bool clean_supported(int dk, bool is_bf16);

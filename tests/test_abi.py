@@ -121,3 +121,24 @@ def test_training_entry_point_validation():
     assert call_bwd(s) == 1                                 # training starts from zero state
     assert call_bwd(shape(), ws_bytes=100) == 3             # workspace too small
     assert call_bwd(shape(io_dtype=__import__("torch").float32, dk=128)) == 2
+
+
+def call_decode(s, bb=0, ws_bytes=1 << 30, ptr=FAKE, beta=None, ws_ptr=FAKE):
+    P = ctypes.c_void_p
+    return ccq.lib().ccq_decode(ctypes.byref(s), bb, P(ptr), P(ptr), P(ptr), P(ptr),
+                                None if beta is None else P(beta), P(ptr), P(ptr), P(ptr),
+                                P(ptr), P(ptr), None if ws_ptr is None else P(ws_ptr), ws_bytes,
+                                None)
+
+
+def test_decode_entry_point_validation():
+    s = shape(T=1, dk=256, dv=512)
+    assert ccq.ccq_decode_workspace_size(s) == 2 * 3 * 256 * 4
+    assert ccq.ccq_decode_workspace_size(shape(T=1, dk=96)) == 0
+    assert call_decode(shape(T=2)) == 1                      # one token per call
+    assert call_decode(shape(T=1, dk=96)) == 2               # unsupported head size
+    assert call_decode(shape(T=1), bb=1) == 1                # Gated DeltaNet needs beta
+    assert call_decode(shape(T=1), ws_ptr=None) == 3         # no workspace
+    assert call_decode(shape(T=1), ws_bytes=8) == 3          # workspace too small
+    assert call_decode(shape(T=1), ptr=FAKE + 4) == 1        # misaligned tensor
+    assert call_decode(shape(B=0, T=1), ptr=0, ws_ptr=None) == 0
