@@ -4,7 +4,10 @@
 One step = one CCQ-GLA forward on the ~500M-layer shape (B=8, T=2048, H=4,
 dk=128, dv=256) plus one CCQ-Gated-DeltaNet forward on the ~1.3B-layer shape
 (B=4, T=4096, H=8, dk=dv=256), bf16 io, fp32 states, chunk 64, inputs resident
-in HBM.  `value` is the tokens of both calls divided by the mean step time.
+in HBM.  `value` is the tokens of both calls divided by the mean step time of
+`--steps` steps timed without per-kernel events; the same number of steps is
+then timed again with the library's per-kernel HIP events recorded around every
+launch (`ms_per_step_traced`), and those events give the per-kernel durations.
 The line also carries the per-kernel HIP-event timings, the roofline of the
 dominant kernel, per-workload figures (including T=20480, the GLA and Gated
 DeltaNet training steps and the one-token recurrent decode step on the cache)
@@ -270,14 +273,26 @@ class DecodeCall:
                             workspace=self.ws)
 
 
-def time_calls(torch, ccq, calls, steps, warmup):
+def time_calls(torch, ccq, calls, steps, warmup, with_plain=False):
     """Warm up, then time exactly `steps` steps (each step = every call once) between two
     synchronisations; per-kernel durations come from HIP events the library records on
-    its stream around each of its launches."""
+    its stream around each of its launches.  With with_plain, exactly `steps` more steps
+    are timed first without those events (the event records add dispatch gaps of their
+    own), and that time is returned as well."""
     for _ in range(warmup):
         for c in calls:
             c()
     torch.cuda.synchronize()
+    ms_plain = None
+    if with_plain:
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record()
+        for i in range(steps):
+            for c in calls:
+                c()
+        end.record()
+        torch.cuda.synchronize()
+        ms_plain = start.elapsed_time(end) / steps
     ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2 * len(c.kernels))]
            for c in calls] for _ in range(steps)]
     for step_ev in ev:
@@ -295,6 +310,12 @@ def time_calls(torch, ccq, calls, steps, warmup):
     end.record()
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(end) / steps
+    if with_plain:
+        return ms_plain, ms_step, per_kernel_times(calls, ev, steps)
+    return ms_step, per_kernel_times(calls, ev, steps)
+
+
+def per_kernel_times(calls, ev, steps):
     per_kernel = []
     for j, c in enumerate(calls):
         for kidx, name in enumerate(c.kernels):
@@ -304,7 +325,7 @@ def time_calls(torch, ccq, calls, steps, warmup):
                                "ms_mean": sum(ts) / len(ts),
                                "ms_std": (sum((t - sum(ts) / len(ts)) ** 2 for t in ts) /
                                           max(1, len(ts) - 1)) ** 0.5})
-    return ms_step, per_kernel
+    return per_kernel
 
 
 def roofline(entry, w):
@@ -327,6 +348,37 @@ def roofline(entry, w):
     r["algorithmic_flops"] = fl
     r["ms_per_launch"] = round(entry["ms_mean"], 5)
     return r
+
+
+EXTRA = ("gla_500m_t2k", "gdn_1p3b_t4k", "gla_500m_t20k", "gdn_1p3b_t20k", "gla_train_t4k",
+         "gdn_train_t4k", "gla_500m_decode_t2k", "gdn_1p3b_decode_t4k")
+
+
+def measure_extra(name, torch, ccq, inputs, steps, existing):
+    """Figures of one workload on its own: tokens/s from untimed-event steps, per-kernel
+    durations and the dominant kernel's roofline from the traced steps."""
+    W = inputs.WORKLOADS
+    if "_decode_" in name:
+        c = DecodeCall(W[name.replace("_decode_t", "_t")], torch, ccq, inputs)
+        ms, ms_tr, pk = time_calls(torch, ccq, [c], max(20, steps), 5, with_plain=True)
+        res = {"tokens_per_s": round(c.w.B / (ms * 1e-3), 1), "ms": round(ms, 5),
+               "ms_traced": round(ms_tr, 5), "position": c.t0 + 1,
+               "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
+               "roofline": roofline(pk[0], c.w)}
+    else:
+        c = existing.get(name) or Call(W[name], torch, ccq, inputs)
+        ms, ms_tr, pk = time_calls(torch, ccq, [c], max(5, steps // 2), 3, with_plain=True)
+        fl = sum(kernel_cost(e["kernel"], c.w)[1] for e in pk)
+        dom = max(pk, key=lambda e: e["ms_mean"])
+        res = {"tokens_per_s": round(c.w.tokens / (ms * 1e-3), 1), "ms": round(ms, 4),
+               "ms_traced": round(ms_tr, 4),
+               "mfma_frac": round(fl / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+               "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
+               "roofline": roofline(dom, c.w)}
+    if name not in existing:
+        del c
+        torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline(calls):
@@ -373,6 +425,8 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip the per-workload figures")
+    ap.add_argument("--only", metavar="WORKLOAD",
+                    help="time only this per-workload entry (for profiling) and print its figures")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (HBM counter "
                          "calibration for rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -401,8 +455,17 @@ def main(argv=None):
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
     W = inputs.WORKLOADS
+    if args.only:
+        if args.only not in EXTRA:
+            print("--only takes one of: " + ", ".join(EXTRA), file=sys.stderr)
+            return 2
+        res = {"workload": args.only}
+        res.update(measure_extra(args.only, torch, ccq, inputs, args.steps, {}))
+        print(json.dumps(res), flush=True)
+        return 0
     step_calls = [Call(W["gla_500m_t2k"], torch, ccq, inputs), Call(W["gdn_1p3b_t4k"], torch, ccq, inputs)]
-    ms_step, per_kernel = time_calls(torch, ccq, step_calls, args.steps, args.warmup)
+    ms_step, ms_traced, per_kernel = time_calls(torch, ccq, step_calls, args.steps, args.warmup,
+                                                with_plain=True)
     tokens = sum(c.w.tokens for c in step_calls)
     value = tokens / (ms_step * 1e-3)
 
@@ -421,29 +484,9 @@ def main(argv=None):
 
     extra = {}
     if not args.no_extra:
-        for name in ("gla_500m_t2k", "gdn_1p3b_t4k", "gla_500m_t20k", "gdn_1p3b_t20k",
-                     "gla_train_t4k", "gdn_train_t4k"):
-            c = step_calls[0] if name == "gla_500m_t2k" else (
-                step_calls[1] if name == "gdn_1p3b_t4k" else Call(W[name], torch, ccq, inputs))
-            ms, pk = time_calls(torch, ccq, [c], max(5, args.steps // 2), 3)
-            fl = sum(kernel_cost(e["kernel"], c.w)[1] for e in pk)
-            dom = max(pk, key=lambda e: e["ms_mean"])
-            extra[name] = {"tokens_per_s": round(c.w.tokens / (ms * 1e-3), 1), "ms": round(ms, 4),
-                           "mfma_frac": round(fl / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-                           "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
-                           "roofline": roofline(dom, c.w)}
-            if c not in step_calls:
-                del c
-                torch.cuda.empty_cache()
-        for name in ("gla_500m_t2k", "gdn_1p3b_t4k"):
-            c = DecodeCall(W[name], torch, ccq, inputs)
-            ms, pk = time_calls(torch, ccq, [c], max(20, args.steps), 5)
-            extra[c.w.name] = {"tokens_per_s": round(c.w.B / (ms * 1e-3), 1), "ms": round(ms, 5),
-                               "position": c.t0 + 1,
-                               "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
-                               "roofline": roofline(pk[0], c.w)}
-            del c
-            torch.cuda.empty_cache()
+        for name in EXTRA:
+            extra[name] = measure_extra(name, torch, ccq, inputs, args.steps,
+                                        {c.w.name: c for c in step_calls})
 
     cpu = None if args.no_cpu_baseline else cpu_baseline(step_calls)
 
@@ -455,6 +498,7 @@ def main(argv=None):
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 5),
+        "ms_per_step_traced": round(ms_traced, 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
