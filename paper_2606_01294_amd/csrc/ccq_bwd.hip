@@ -137,17 +137,16 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
   __shared__ float sBm[DK], sBCm[DK];
   // phase-local buffers share one region
   constexpr int kR1 = C * LDQ * ES;
-  constexpr int kOffdS = DK * LDV * ES, kOffdST = kOffdS + BV * LDQ * ES,
-                kOffV = kOffdST + DK * LDV * ES, kOffdO = kOffV + C * LDV * ES,
-                kOffdOT = kOffdO + C * LDV * ES, kR2 = kOffdOT + BV * LDT * ES;
+  constexpr int kOffdS = BV * LDQ * ES, kOffV = kOffdS + BV * LDQ * ES,
+                kOffdO = kOffV + C * LDV * ES, kOffdOT = kOffdO + C * LDV * ES,
+                kR2 = kOffdOT + BV * LDT * ES;
   constexpr int kR3 = 2 * C * LDT * ES;
   constexpr int kR4 = 4 * DK * 4;
   constexpr int kR = kR1 > kR2 ? (kR1 > kR3 ? kR1 : kR3) : (kR2 > kR3 ? kR2 : kR3);
   __shared__ __align__(16) char sR[kR > kR4 ? kR : kR4];
   T* sQt = reinterpret_cast<T*>(sR);
-  T* sSrT = reinterpret_cast<T*>(sR);
-  T* sdS = reinterpret_cast<T*>(sR + kOffdS);
-  T* sdST = reinterpret_cast<T*>(sR + kOffdST);
+  T* sS = reinterpret_cast<T*>(sR);  // S_r diag(e^{b_m}) slice, rows v
+  T* sdS = reinterpret_cast<T*>(sR + kOffdS);  // dS_{r+1} diag(e^{b_C - b_m}) slice, rows v
   T* sV = reinterpret_cast<T*>(sR + kOffV);
   T* sdO = reinterpret_cast<T*>(sR + kOffdO);
   T* sdOT = reinterpret_cast<T*>(sR + kOffdOT);
@@ -225,41 +224,62 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
   lds_barrier();  // sQt is dead from here on
 
   // ---- phase 2: loop over value slices
+  // X1 = dO S_r diag(e^{b_m}), X2 = V dS_{r+1} diag(e^{b_C - b_m}), Adv = dO V^T
   f32x4 X1[NTC], X2[NTC], Adv[4];
 #pragma unroll
   for (int ct = 0; ct < NTC; ++ct) { X1[ct] = zero4(); X2[ct] = zero4(); }
 #pragma unroll
   for (int J = 0; J < 4; ++J) Adv[J] = zero4();
   T* dvrow = static_cast<T*>(a.dv_out) + tok_off(b, r0, h, a.T, a.H, a.dv);
+  // every value slice's global operands are requested one slice ahead
+  typedef T v8 __attribute__((ext_vector_type(8)));
+  constexpr int NPS = BV * DK / 8 / kThreads;  // 8-element pieces of S_r (and dS) per thread
+  static_assert(NPS >= 1 && BV * DK / 8 % kThreads == 0, "piece split");
+  struct Slice {
+    v8 s[NPS], d[NPS];
+    ChunkTile<T, BV> rv, rdo;
+  };
+  auto load_slice = [&](Slice& sl, int vv0) {
+#pragma unroll
+    for (int p = 0; p < NPS; ++p) {
+      const int idx = tid + p * kThreads, row = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
+      sl.s[p] = *reinterpret_cast<const v8*>(Sst + (size_t)(vv0 + row) * DK + c0);
+      sl.d[p] = *reinterpret_cast<const v8*>(dSst + (size_t)(vv0 + row) * DK + c0);
+    }
+    sl.rv.load(v + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
+    sl.rdo.load(dO + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
+  };
+  Slice cur;
+  load_slice(cur, 0);
   for (int vv0 = 0; vv0 < a.dv; vv0 += BV) {
-    // states: S_r diag(e^{b_m}) transposed, dS_{r+1} diag(e^{b_C - b_m}) and dS_{r+1}^T
-    for (int idx = tid; idx < BV * DK / 8; idx += kThreads) {
-      const int row = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
-      typedef T v8 __attribute__((ext_vector_type(8)));
-      const v8 sv = *reinterpret_cast<const v8*>(Sst + (size_t)(vv0 + row) * DK + c0);
-      const v8 dv8 = *reinterpret_cast<const v8*>(dSst + (size_t)(vv0 + row) * DK + c0);
-      v8 ds_scaled;
+    // states, rows v: S_r diag(e^{b_m}) and dS_{r+1} diag(e^{b_C - b_m}); the
+    // products over v read them with transposing LDS reads
+#pragma unroll
+    for (int p = 0; p < NPS; ++p) {
+      const int idx = tid + p * kThreads, row = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
+      v8 s_scaled, ds_scaled;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        sSrT[(c0 + e) * LDV + row] = to<T>(f32(sv[e]) * sBm[c0 + e]);
-        sdST[(c0 + e) * LDV + row] = dv8[e];
-        ds_scaled[e] = to<T>(f32(dv8[e]) * sBCm[c0 + e]);
+        s_scaled[e] = to<T>(f32(cur.s[p][e]) * sBm[c0 + e]);
+        ds_scaled[e] = to<T>(f32(cur.d[p][e]) * sBCm[c0 + e]);
       }
+      *reinterpret_cast<v8*>(sS + row * LDQ + c0) = s_scaled;
       *reinterpret_cast<v8*>(sdS + row * LDQ + c0) = ds_scaled;
     }
-    {
-      ChunkTile<T, BV> rv, rdo;
-      rv.load(v + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
-      rdo.load(dO + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
-      rv.store(sV, LDV);
-      rdo.store(sdO, LDV);
-      rdo.store_t(sdOT, LDT);
-    }
+    cur.rv.store(sV, LDV);
+    cur.rdo.store(sdO, LDV);
+    cur.rdo.store_t(sdOT, LDT);
+    if (vv0 + BV < a.dv) load_slice(cur, vv0 + BV);
     lds_barrier();
 #pragma unroll
-    for (int ct = 0; ct < NTC; ++ct) {
-      tile_mma<T, BV>(X1[ct], sdO + 16 * w * LDV, LDV, sSrT + 16 * ct * LDV, LDV);
-      tile_mma<T, BV>(X2[ct], sV + 16 * w * LDV, LDV, sdST + 16 * ct * LDV, LDV);
+    for (int k0 = 0; k0 < BV; k0 += 32) {
+      const Frag<T> fo = ld_frag(sdO + 16 * w * LDV + k0, LDV);
+      const Frag<T> fv = ld_frag(sV + 16 * w * LDV + k0, LDV);
+#pragma unroll
+      for (int ct = 0; ct < NTC; ++ct) {
+        mma(X1[ct], fo, ld_frag_tr(sS + k0 * LDQ + 16 * ct, LDQ));
+        mma(X2[ct], fv, ld_frag_tr(sdS + k0 * LDQ + 16 * ct, LDQ));
+      }
     }
 #pragma unroll
     for (int J = 0; J < 4; ++J)
@@ -331,7 +351,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
       if (i < nrow) {
         const float d = sG[i * LDG + c] - bm;
         const float dqc = a.scale * __expf(d) * X1[ct][r];
-        const float dkg = __expf(-d) * (Y2[ct][r] * a.scale + X2[ct][r] * sBCm[c]);
+        const float dkg = __expf(-d) * (Y2[ct][r] * a.scale + X2[ct][r]);
         const int off = i * (int)gsk + c;
         const float db = qv[ct][r] * dqc - kv[ct][r] * dkg;
         dqc_f[off] = dqc;

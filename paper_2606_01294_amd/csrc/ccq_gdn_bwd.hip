@@ -271,7 +271,7 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
   __shared__ float sDg[C];
   __shared__ float sRed[2][4];
   constexpr int kR1 = 2 * C * LDQ * ES;
-  constexpr int kR2 = 4 * C * LDV * ES + 2 * DK * LDV * ES;
+  constexpr int kR2 = 4 * C * LDV * ES + 2 * BV * LDQ * ES;
   constexpr int kR3 = 4 * C * LDT * ES;
   constexpr int kR = kR1 > kR2 ? (kR1 > kR3 ? kR1 : kR3) : (kR2 > kR3 ? kR2 : kR3);
   __shared__ __align__(16) char sR[kR];
@@ -330,25 +330,52 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
     T* sdR = sdO + C * LDV;
     T* sU = sdR + C * LDV;
     T* sV = sU + C * LDV;
-    T* sST = sV + C * LDV;  // S_r^T [c][v]
-    T* sDT = sST + DK * LDV;  // D^T [c][v]
+    T* sS = sV + C * LDV;     // S_r slice, rows v (read transposed by the products)
+    T* sD = sS + BV * LDQ;    // D slice, rows v
     const T* Sg = static_cast<const T*>(a.states) + cidx * a.dv * DK;
     const T* Ug = static_cast<const T*>(a.U) + cidx * a.dv * C;
     const T* Dg = static_cast<const T*>(a.dstates) + cidx * a.dv * DK;
     T* dvrow = static_cast<T*>(a.dv_out) + tok_off(b, r0, h, a.T, a.H, a.dv);
     typedef T v8 __attribute__((ext_vector_type(8)));
+    // every value slice's global operands are requested one slice ahead
+    constexpr int NPS = BV * DK / 8 / kThreads;  // pieces of S_r and of D per thread
+    constexpr int NPU = BV * C / 8 / kThreads;   // pieces of U^T per thread
+    static_assert(NPS >= 1 && NPU >= 1, "piece split");
+    struct Slice {
+      v8 s[NPS], d[NPS], u[NPU];
+      ChunkTile<T, BV> rdo, rdr, rvv;
+    };
+    auto load_slice = [&](Slice& sl, int vv0) {
+#pragma unroll
+      for (int p = 0; p < NPS; ++p) {
+        const int q = tid + p * kThreads;
+        const int vt = q / (2 * DK), rem = q % (2 * DK);
+        const int m = rem / 64, vr = (rem % 64) / 4, pp = rem % 4;
+        sl.s[p] = *reinterpret_cast<const v8*>(Sg + (size_t)(vv0 / 16 + vt) * 16 * DK + (size_t)(m * 16 + vr) * 32 + 8 * pp);
+        const int vd = q / (DK / 8), cd = (q % (DK / 8)) * 8;
+        sl.d[p] = *reinterpret_cast<const v8*>(Dg + (size_t)(vv0 + vd) * DK + cd);
+      }
+#pragma unroll
+      for (int p = 0; p < NPU; ++p) {
+        const int q = tid + p * kThreads;
+        const int vt = q / 128, rem = q % 128;
+        const int m = rem / 64, vr = (rem % 64) / 4, pp = rem % 4;
+        sl.u[p] = *reinterpret_cast<const v8*>(Ug + (size_t)(vv0 / 16 + vt) * 16 * C + (size_t)(m * 16 + vr) * 32 + 8 * pp);
+      }
+      sl.rdo.load(static_cast<const T*>(a.dO) + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
+      sl.rdr.load(static_cast<const T*>(a.dR) + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
+      sl.rvv.load(static_cast<const T*>(a.v) + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
+    };
+    Slice cur;
+    load_slice(cur, 0);
     for (int vv0 = 0; vv0 < a.dv; vv0 += BV) {
       {
-        ChunkTile<T, BV> rdo, rdr, rvv;
-        rdo.load(static_cast<const T*>(a.dO) + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
-        rdr.load(static_cast<const T*>(a.dR) + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
-        rvv.load(static_cast<const T*>(a.v) + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
         const int row = ChunkTile<T, BV>::row();
         const float bt = sBeta[row];
 #pragma unroll
         for (int u = 0; u < ChunkTile<T, BV>::NV; ++u) {
           const int c0 = ChunkTile<T, BV>::col(u);
-          const v8 xo = rdo.get(u), xr = rdr.get(u), xv = rvv.get(u);
+          const v8 xo = cur.rdo.get(u), xr = cur.rdr.get(u), xv = cur.rvv.get(u);
           v8 yo, yd;
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
@@ -364,26 +391,32 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
       }
       // S_r and U^T slices (fragment-native: per value tile and 32-wide k
       // block, 16 rows of 32 in acc_pos order) and D (plain rows)
-      for (int q = tid; q < BV * DK / 8; q += kThreads) {
+#pragma unroll
+      for (int p = 0; p < NPS; ++p) {
+        const int q = tid + p * kThreads;
         const int vt = q / (2 * DK), rem = q % (2 * DK);
         const int m = rem / 64, vr = (rem % 64) / 4, pp = rem % 4;
-        const v8 x = *reinterpret_cast<const v8*>(Sg + (size_t)(vv0 / 16 + vt) * 16 * DK + (size_t)(m * 16 + vr) * 32 + 8 * pp);
         const int vl = 16 * vt + vr;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sST[(32 * m + acc_logical(8 * pp + e)) * LDV + vl] = x[e];
-        const int vd = q / (DK / 8), cd = (q % (DK / 8)) * 8;
-        const v8 y = *reinterpret_cast<const v8*>(Dg + (size_t)(vv0 + vd) * DK + cd);
+        for (int hh = 0; hh < 2; ++hh) {  // logical columns 4pp.. and 16 + 4pp..
+          T* dst4 = sS + vl * LDQ + 32 * m + 16 * hh + 4 * pp;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sDT[(cd + e) * LDV + vd] = y[e];
+          for (int e = 0; e < 4; ++e) dst4[e] = cur.s[p][4 * hh + e];
+        }
+        const int vd = q / (DK / 8), cd = (q % (DK / 8)) * 8;
+#pragma unroll
+        *reinterpret_cast<v8*>(sD + vd * LDQ + cd) = cur.d[p];
       }
-      for (int q = tid; q < BV * C / 8; q += kThreads) {
+#pragma unroll
+      for (int p = 0; p < NPU; ++p) {
+        const int q = tid + p * kThreads;
         const int vt = q / 128, rem = q % 128;
         const int m = rem / 64, vr = (rem % 64) / 4, pp = rem % 4;
-        const v8 x = *reinterpret_cast<const v8*>(Ug + (size_t)(vv0 / 16 + vt) * 16 * C + (size_t)(m * 16 + vr) * 32 + 8 * pp);
         const int vl = 16 * vt + vr;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sU[(32 * m + acc_logical(8 * pp + e)) * LDV + vl] = x[e];
+        for (int e = 0; e < 8; ++e) sU[(32 * m + acc_logical(8 * pp + e)) * LDV + vl] = cur.u[p][e];
       }
+      if (vv0 + BV < a.dv) load_slice(cur, vv0 + BV);
       lds_barrier();
 #pragma unroll
       for (int J = 0; J < 4; ++J) {
@@ -394,13 +427,17 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
       }
 #pragma unroll
       for (int ct = 0; ct < NTC; ++ct) {
-        tile_mma<T, BV>(G1[ct], sdO + 16 * w * LDV, LDV, sST + 16 * ct * LDV, LDV);
-        tile_mma<T, BV>(G2[ct], sdR + 16 * w * LDV, LDV, sST + 16 * ct * LDV, LDV);
-        tile_mma<T, BV>(G3[ct], sU + 16 * w * LDV, LDV, sDT + 16 * ct * LDV, LDV);
+#pragma unroll
+        for (int k0 = 0; k0 < BV; k0 += 32) {
+          const Frag<T> fs = ld_frag_tr(sS + k0 * LDQ + 16 * ct, LDQ);
+          mma(G1[ct], ld_frag(sdO + 16 * w * LDV + k0, LDV), fs);
+          mma(G2[ct], ld_frag(sdR + 16 * w * LDV + k0, LDV), fs);
+          mma(G3[ct], ld_frag(sU + 16 * w * LDV + k0, LDV), ld_frag_tr(sD + k0 * LDQ + 16 * ct, LDQ));
+        }
       }
       for (int idx = tid; idx < DK * BV; idx += kThreads) {
-        const int c = idx / BV, vl = idx % BV;
-        dss += f32(sST[c * LDV + vl]) * f32(sDT[c * LDV + vl]);
+        const int vl = idx / DK, c = idx % DK;
+        dss += f32(sS[vl * LDQ + c]) * f32(sD[vl * LDQ + c]);
       }
       lds_barrier();
     }
@@ -562,7 +599,7 @@ template <typename T, int DK>
 hipError_t run_bwd_chunk(const GdnBwdArgs& a, hipStream_t st) {
   const int nblk = a.B * a.H * ((a.T + kChunk - 1) / kChunk);
   if (nblk == 0) return hipSuccess;
-  constexpr int BV = sizeof(T) == 2 ? 64 : 32;
+  constexpr int BV = 32;
   hipLaunchKernelGGL((gdn_bwd_chunk_kernel<T, DK, BV>), dim3(nblk), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
