@@ -835,7 +835,7 @@ template <typename T, typename TG>
 hipError_t dstate_dispatch(const DstateArgs& a, hipStream_t st) {
   if constexpr (sizeof(T) == 2) {
     if (a.dk == 64) return run_dstate<T, TG, 64, 64>(a, st);
-    if (a.dk == 128) return run_dstate<T, TG, 128, 64>(a, st);
+    if (a.dk == 128) return run_dstate<T, TG, 128, 32>(a, st);
   } else {
     if (a.dk == 64) return run_dstate<T, TG, 64, 64>(a, st);
   }

@@ -404,7 +404,6 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
           for (int e = 0; e < 4; ++e) dst4[e] = cur.s[p][4 * hh + e];
         }
         const int vd = q / (DK / 8), cd = (q % (DK / 8)) * 8;
-#pragma unroll
         *reinterpret_cast<v8*>(sD + vd * LDQ + cd) = cur.d[p];
       }
 #pragma unroll
