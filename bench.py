@@ -148,7 +148,7 @@ KERNEL_SYMBOL = {"decode": "decode_stats_kernel+decode_out_kernel", "clean_gram"
                  "clean_out_train": "clean_out_kernel", "clean_dq": "clean_out_kernel",
                  "gla_state": "gla_state_kernel", "gla_scan": "gla_scan_kernel", "gla_out": "gla_out_kernel",
                  "gdn_tri": "gdn_tri_kernel", "gdn_state": "gdn_state_dma_kernel",
-                 "gdn_out": "gdn_out_kernel", "gla_dstate": "gla_dstate_kernel",
+                 "gdn_out": "gdn_out_kernel", "gla_dstate": "gla_state_kernel (reverse)",
                  "gla_bwd_chunk": "gla_bwd_chunk_kernel", "gla_dg": "gla_dg_kernel",
                  "gdn_bwd_prep": "gdn_bwd_prep_kernel", "gdn_dstate": "gdn_dstate_kernel",
                  "gdn_bwd_chunk": "gdn_bwd_chunk_kernel", "ccq_dk": "ccq_dk_kernel"}
@@ -157,7 +157,7 @@ KERNEL_SYMBOL = {"decode": "decode_stats_kernel+decode_out_kernel", "clean_gram"
 def _source(kernel: str) -> str:
     if kernel.startswith("clean"):
         return "ccq_clean.hip"
-    if kernel in ("gla_state", "gla_scan", "gla_out"):
+    if kernel in ("gla_state", "gla_scan", "gla_out", "gla_dstate"):
         return "ccq_gla.hip"
     if kernel in ("gdn_bwd_prep", "gdn_dstate", "gdn_bwd_chunk"):
         return "ccq_gdn_bwd.hip"

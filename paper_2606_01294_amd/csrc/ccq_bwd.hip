@@ -18,104 +18,14 @@
 //   dk_j   += sum_{t>=j} rho_t [u_t (q_t . k_j) + q_t (u_t . k_j)]
 //             + sum_{t>=j} (lam_t / t^2) [u_t (m_t . q_t) + q_t (m_t . u_t)],  rho_t = -lam_t / t
 // where the last line is the mean term (absent in the uncentred variant).
+//
+// The reverse scan of dS (first line) is the GLA state kernel run backwards
+// (ccq_gla.hip); this file holds the chunk-parallel gradients, the decay
+// gradient's reverse cumulative sum and the contraction's key gradient.
 #include "ccq_device.h"
 #include "ccq_kernels.h"
 
 namespace ccq {
-
-// ----------------------------------------------------------------------------
-// Reverse scan of dS per (head, BV-row slice), storing dS_{r+1} for every chunk.
-template <typename T, typename TG, int DK, int BV>
-__global__ __launch_bounds__(kThreads, 1) void gla_dstate_kernel(const DstateArgs a) {
-  constexpr int C = kChunk;
-  constexpr int P = Pad<T>::value;
-  constexpr int LDT = C + P, LDG = DK + 1;
-  constexpr int NTC = DK / 16;
-  constexpr int NPW = BV * DK / (16 * 16 * 4);
-  static_assert(NPW >= 1 && DK <= kThreads, "tile split");
-
-  __shared__ __align__(16) T sQeT[DK * LDT];
-  __shared__ __align__(16) T sdOT[BV * LDT];
-  __shared__ float sG[C * LDG];
-  __shared__ float sDec[DK];
-
-  const int nvt = a.dv / BV;
-  const int N = (a.T + C - 1) / C;
-  const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int bh = lb / nvt;
-  const int v0 = (lb % nvt) * BV;
-  const int b = bh / a.H, h = bh % a.H;
-  const int tid = threadIdx.x, w = wave_id(), l = lane_id();
-  const int g4 = l >> 4, c16 = l & 15;
-  const T* qc = static_cast<const T*>(a.qc);
-  const TG* gate = static_cast<const TG*>(a.g);
-  const T* dO = static_cast<const T*>(a.dO);
-  T* dst = static_cast<T*>(a.dstates);
-
-  f32x4 dS[NPW];
-#pragma unroll
-  for (int u = 0; u < NPW; ++u) dS[u] = zero4();
-
-  ChunkTile<T, DK> rq;
-  ChunkTile<TG, DK> rg;
-  ChunkTile<T, BV> rdo;
-  auto prefetch = [&](int ci) {
-    const int r0 = ci * C;
-    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-    rq.load(qc + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
-    rg.load(gate + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
-    rdo.load(dO + tok_off(b, r0, h, a.T, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
-  };
-  if (N > 0) prefetch(N - 1);
-
-  for (int ci = N - 1; ci >= 0; --ci) {
-    lds_barrier();  // (A)
-    rg.store_f32(sG, LDG);
-    rdo.store_t(sdOT, LDT);
-    {  // adjoint of the state leaving chunk ci
-      T* out = dst + (((size_t)bh * N + ci) * a.dv + v0) * DK;
-#pragma unroll
-      for (int u = 0; u < NPW; ++u) {
-        const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) out[(size_t)(16 * tv + 4 * g4 + r) * DK + 16 * tc + c16] = to<T>(dS[u][r]);
-      }
-    }
-    lds_barrier();  // (B)
-    if (tid < DK) {
-      float x[C];
-#pragma unroll
-      for (int j = 0; j < C; ++j) x[j] = sG[j * LDG + tid];
-#pragma unroll
-      for (int j = 1; j < C; ++j) x[j] += x[j - 1];
-#pragma unroll
-      for (int j = 0; j < C; ++j) sG[j * LDG + tid] = x[j];
-      sDec[tid] = __expf(x[C - 1]);
-    }
-    lds_barrier();  // (C)
-    {  // (qc * e^{b})^T, e^{b} <= 1
-      const int j = ChunkTile<T, DK>::row();
-#pragma unroll
-      for (int u = 0; u < ChunkTile<T, DK>::NV; ++u) {
-        const auto x = rq.get(u);
-        const int c0 = ChunkTile<T, DK>::col(u);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) sQeT[(c0 + e) * LDT + j] = to<T>(f32(x[e]) * __expf(sG[j * LDG + c0 + e]));
-      }
-    }
-    if (ci > 0) prefetch(ci - 1);
-    lds_barrier();  // (D)
-#pragma unroll
-    for (int u = 0; u < NPW; ++u) {
-      const int tau = w * NPW + u, tv = tau / NTC, tc = tau % NTC;
-      f32x4 d = zero4();
-      tile_mma<T, C>(d, sdOT + 16 * tv * LDT, LDT, sQeT + 16 * tc * LDT, LDT);
-      const float dec = sDec[16 * tc + c16];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) dS[u][r] = dS[u][r] * dec + a.scale * d[r];
-    }
-  }
-}
 
 // ----------------------------------------------------------------------------
 // One workgroup per chunk: dqc, the GLA part of dk, dv, the decay gradient
@@ -800,13 +710,6 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
 // ----------------------------------------------------------------------------
 namespace {
 template <typename T, typename TG, int DK, int BV>
-hipError_t run_dstate(const DstateArgs& a, hipStream_t st) {
-  const int nblk = a.B * a.H * (a.dv / BV);
-  if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((gla_dstate_kernel<T, TG, DK, BV>), dim3(nblk), dim3(kThreads), 0, st, a);
-  return hipGetLastError();
-}
-template <typename T, typename TG, int DK, int BV>
 hipError_t run_bwd_chunk(const GlaBwdArgs& a, hipStream_t st) {
   const int nblk = a.B * a.H * ((a.T + kChunk - 1) / kChunk);
   if (nblk == 0) return hipSuccess;
@@ -832,16 +735,6 @@ hipError_t run_ccq_dk(const CcqDkArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 template <typename T, typename TG>
-hipError_t dstate_dispatch(const DstateArgs& a, hipStream_t st) {
-  if constexpr (sizeof(T) == 2) {
-    if (a.dk == 64) return run_dstate<T, TG, 64, 64>(a, st);
-    if (a.dk == 128) return run_dstate<T, TG, 128, 32>(a, st);
-  } else {
-    if (a.dk == 64) return run_dstate<T, TG, 64, 64>(a, st);
-  }
-  return hipErrorInvalidValue;
-}
-template <typename T, typename TG>
 hipError_t chunk_dispatch(const GlaBwdArgs& a, hipStream_t st) {
   if constexpr (sizeof(T) == 2) {
     if (a.dk == 64) return run_bwd_chunk<T, TG, 64, 32>(a, st);
@@ -857,11 +750,6 @@ bool bwd_supported(int dk, int dv, bool is_bf16) {
   const bool dv_ok = dv == 64 || dv == 128 || dv == 256 || dv == 512;
   if (is_bf16) return dv_ok && (dk == 64 || dk == 128);
   return dv_ok && dk == 64;
-}
-
-hipError_t launch_gla_dstate(const DstateArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st) {
-  if (is_bf16) return gate_bf16 ? dstate_dispatch<bf16_t, bf16_t>(a, st) : dstate_dispatch<bf16_t, float>(a, st);
-  return gate_bf16 ? dstate_dispatch<float, bf16_t>(a, st) : dstate_dispatch<float, float>(a, st);
 }
 
 hipError_t launch_gla_bwd_chunk(const GlaBwdArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st) {

@@ -30,7 +30,12 @@ namespace ccq {
 // back one iteration late (all vector memory operations share one in-order
 // counter, so a store just before the next loads are waited for would add
 // its latency to every chunk).
-template <typename T, typename TG, int NVT>
+//
+// With kRev the same pass runs backwards for the training step: over the
+// chunks from last to first it carries the state adjoint D = dL/dS_{r+1} and
+// stores it for every chunk, with  D^T <- diag(e^{b_C}) D^T + s (Q e^{b})^T dO
+// (a.k = q_clean, a.v = dO, a.states = the adjoints, a.scale = s).
+template <typename T, typename TG, int NVT, bool kRev = false>
 __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateArgs a) {
   constexpr int C = kChunk, BK = 64, VB = 16 * NVT;
   constexpr int P = Pad<T>::value, PG = Pad<TG>::value;
@@ -81,16 +86,18 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
     for (int tv = 0; tv < NVT; ++tv)
       store4(st + (size_t)(16 * tv + c16) * a.dk, Sr[tv][0], Sr[tv][1], Sr[tv][2], Sr[tv][3]);
   };
-  if (cb < ce) prefetch(cb);
+  const int nch = ce - cb;
+  if (nch > 0) prefetch(kRev ? ce - 1 : cb);
   float le = 0.f;  // log decay of this lane's channel since the segment began
 
-  for (int ci = cb; ci < ce; ++ci) {
-    const int buf = (ci - cb) & 1;  // the other buffer was released at the previous barrier
+  for (int it = 0; it < nch; ++it) {
+    const int ci = kRev ? ce - 1 - it : cb + it;
+    const int buf = it & 1;  // the other buffer was released at the previous barrier
     rk.store(sK[buf], LDK);
     rg.store(sG[buf], LDG);
     rv.store(sV[buf], LDV);
-    if (ci > cb) write_back(ci - 1);
-    if (ci + 1 < ce) prefetch(ci + 1);
+    if (it > 0) write_back(kRev ? ci + 1 : ci - 1);
+    if (it + 1 < nch) prefetch(kRev ? ci - 1 : ci + 1);
 #pragma unroll
     for (int tv = 0; tv < NVT; ++tv) Sr[tv] = S[tv];
     __syncthreads();
@@ -121,12 +128,17 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
     const float bC = half[0] + half[1];
     if (a.cdec && vt == 0 && g4 == 0) a.cdec[((size_t)bh * N + ci) * a.dk + c0 + 16 * w + c16] = __expf(le);
     le += bC;
-    Frag<T> kd0, kd1;
+    Frag<T> kd0, kd1;  // forward: k e^{b_C - b}; reverse: s q e^{b}
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float b0 = ex[0] + pb[0][e], b1 = half[0] + ex[1] + pb[1][e];
-      set_frag_elem(kd0, e, frag_elem(kf0, e) * __expf(bC - b0));
-      set_frag_elem(kd1, e, frag_elem(kf1, e) * __expf(bC - b1));
+      if constexpr (kRev) {
+        set_frag_elem(kd0, e, a.scale * frag_elem(kf0, e) * __expf(b0));
+        set_frag_elem(kd1, e, a.scale * frag_elem(kf1, e) * __expf(b1));
+      } else {
+        set_frag_elem(kd0, e, frag_elem(kf0, e) * __expf(bC - b0));
+        set_frag_elem(kd1, e, frag_elem(kf1, e) * __expf(bC - b1));
+      }
     }
     // S^T <- diag(e^{b_C}) S^T + Kd^T V; row c = 4 g4 + r of the tile needs e^{b_C[c]}
     f32x4 dec;
@@ -140,7 +152,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
     }
   }
 
-  if (cb < ce) write_back(ce - 1);
+  if (nch > 0) write_back(kRev ? cb : ce - 1);
   // the segment's total: the local state at its end and its decay (or, with
   // one segment, the final state)
   float* out = a.segsum ? a.segsum + ((size_t)bh * NS + sg) * a.dv * a.dk
@@ -362,20 +374,20 @@ int gla_nseg(const GlaStateArgs& a) {
   const int N = (a.T + kChunk - 1) / kChunk;
   return a.seg > 0 ? (N + a.seg - 1) / a.seg : 1;
 }
-template <typename T, typename TG, int NVT>
+template <typename T, typename TG, int NVT, bool kRev>
 hipError_t run_gla_state_v(const GlaStateArgs& a, hipStream_t st) {
   const int nblk = a.B * a.H * (a.dk / 64) * (a.dv / (16 * NVT)) * gla_nseg(a);
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((gla_state_kernel<T, TG, NVT>), dim3(nblk), dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((gla_state_kernel<T, TG, NVT, kRev>), dim3(nblk), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 // 64-wide value slices when they still give every SIMD a wave, else 32 or 16.
-template <typename T, typename TG>
+template <typename T, typename TG, bool kRev = false>
 hipError_t run_gla_state(const GlaStateArgs& a, hipStream_t st) {
   const long long waves64 = (long long)a.B * a.H * (a.dk / 64) * (a.dv / 64) * 4 * gla_nseg(a);
-  if (waves64 >= 1024) return run_gla_state_v<T, TG, 4>(a, st);
-  if (waves64 * 2 >= 1024) return run_gla_state_v<T, TG, 2>(a, st);
-  return run_gla_state_v<T, TG, 1>(a, st);
+  if (waves64 >= 1024) return run_gla_state_v<T, TG, 4, kRev>(a, st);
+  if (waves64 * 2 >= 1024) return run_gla_state_v<T, TG, 2, kRev>(a, st);
+  return run_gla_state_v<T, TG, 1, kRev>(a, st);
 }
 template <typename T, typename TG, int DK, int VP, int VPW, int IPW>
 hipError_t run_gla_out_v(const GlaOutArgs& a, hipStream_t st) {
@@ -413,6 +425,23 @@ bool gla_supported(int dk, int dv, bool is_bf16) {
 hipError_t launch_gla_state(const GlaStateArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st) {
   if (is_bf16) return gate_bf16 ? run_gla_state<bf16_t, bf16_t>(a, st) : run_gla_state<bf16_t, float>(a, st);
   return gate_bf16 ? run_gla_state<float, bf16_t>(a, st) : run_gla_state<float, float>(a, st);
+}
+
+// The training step's reverse state scan (kRev), one segment.
+hipError_t launch_gla_dstate(const DstateArgs& d, bool is_bf16, bool gate_bf16, hipStream_t st) {
+  GlaStateArgs a{};
+  a.k = d.qc;
+  a.v = d.dO;
+  a.g = d.g;
+  a.states = d.dstates;
+  a.B = d.B;
+  a.T = d.T;
+  a.H = d.H;
+  a.dk = d.dk;
+  a.dv = d.dv;
+  a.scale = d.scale;
+  if (is_bf16) return gate_bf16 ? run_gla_state<bf16_t, bf16_t, true>(a, st) : run_gla_state<bf16_t, float, true>(a, st);
+  return gate_bf16 ? run_gla_state<float, bf16_t, true>(a, st) : run_gla_state<float, float, true>(a, st);
 }
 
 hipError_t launch_gla_scan(const GlaScanArgs& a, bool is_bf16, hipStream_t st) {

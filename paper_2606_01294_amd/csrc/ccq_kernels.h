@@ -67,6 +67,7 @@ struct GlaStateArgs {
   float* segsum;      // [B*H, NS, dv, dk] fp32: local state at each segment's end (NS > 1)
   float* segdec;      // [B*H, NS, dk] fp32: e^{sum of the segment's log decays}
   float* cdec;        // [B*H, N, dk] fp32: e^{log decays of the segment before each chunk}
+  float scale;        // read scale (the reverse scan of the training step only)
 };
 
 // Entry state of every segment, E_0 = 0 (S0 is inside segment 0's states),
