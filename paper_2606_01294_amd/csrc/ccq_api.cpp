@@ -310,15 +310,22 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   char* ws = static_cast<char*>(workspace);
   const bool bf = s->io_dtype == CCQ_BF16;
   void* qclean = ws + L.qclean;
-  SideStream* sd = nullptr;
-  if (side_stream(&sd) != hipSuccess || fork_to(*sd, st) != hipSuccess) return CCQ_ERR_HIP;
-  hipStream_t ss = sd->s;
-  trace_begin_call();
-
-  // side stream: the backbone's state pass (chunk-entry states S_r)
   const float* la = static_cast<const float*>(g_or_la);
   float* gam = reinterpret_cast<float*>(ws + L.gam);
   const bool gbf = s->gate_dtype == CCQ_BF16;
+  trace_begin_call();
+  // Gated DeltaNet: the chunk transforms first, on the caller's stream with
+  // the whole chip, so that the sequential state pass (the longest branch)
+  // starts as early as possible
+  if (bb == CCQ_GDN) {
+    ccq::TriArgs ta{k, la, beta, ws + L.Tm, gam, s->B, s->T, s->H, s->dk, s->dv};
+    if (traced(st, [&] { return ccq::launch_gdn_tri(ta, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  }
+  SideStream* sd = nullptr;
+  if (side_stream(&sd) != hipSuccess || fork_to(*sd, st) != hipSuccess) return CCQ_ERR_HIP;
+  hipStream_t ss = sd->s;
+
+  // side stream: the backbone's state pass (chunk-entry states S_r)
   if (bb == CCQ_GLA) {
     // segments of the state pass run in parallel; a scan over the segment
     // totals gives every segment's entry state and S_T
@@ -338,8 +345,6 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
       if (traced(ss, [&] { return ccq::launch_gla_scan(ga, bf, ss); }) != hipSuccess) return CCQ_ERR_HIP;
     }
   } else {
-    ccq::TriArgs ta{k, la, beta, ws + L.Tm, gam, s->B, s->T, s->H, s->dk, s->dv};
-    if (traced(ss, [&] { return ccq::launch_gdn_tri(ta, bf, ss); }) != hipSuccess) return CCQ_ERR_HIP;
     ccq::GdnArgs da{k, v, beta, ws + L.Tm, gam, S0, ST, ws + L.states, ws + L.U, s->B, s->T, s->H,
                     s->dk, s->dv};
     if (traced(ss, [&] { return ccq::launch_gdn_state(da, bf, ss); }) != hipSuccess) return CCQ_ERR_HIP;
