@@ -785,3 +785,41 @@ int ccq_oracle_gdn_fwd_bwd(const ccq_oracle_shape* s, int seg, const double* q, 
   }
   return err;
 }
+
+/*
+ * Pre-processing of one layer's raw queries and keys (Alg. 1, the per-chunk
+ * normalisation and gate lines; Eq. clean for the gate):
+ *   qbar = q / max(|q|, 1e-12), kbar = k / max(|k|, 1e-12)   per head;
+ *   lambda[h] = sigmoid(sum_j W[h][j] qraw[j] + b[h]),
+ * where qraw is the token's query before the split into heads (all H*dk
+ * features, head-major) and W is [H, H*dk].  Layouts: q, k [B,T,H,dk];
+ * lambda [B,T,H].  Outputs may alias nothing.
+ */
+int ccq_oracle_prep(int32_t B, int32_t T, int32_t H, int32_t dk, const double* q, const double* k,
+                    const double* W, const double* bias, double* qbar, double* kbar, double* lam) {
+  if (B < 0 || T < 0 || H <= 0 || dk <= 0) return 1;
+  const int64_t ntok = (int64_t)B * T;
+  const int64_t E = (int64_t)H * dk;
+#pragma omp parallel for schedule(static)
+  for (int64_t t = 0; t < ntok; ++t) {
+    const double* qr = q + t * E;
+    const double* kr = k + t * E;
+    for (int h = 0; h < H; ++h) {
+      double qq = 0.0, kk = 0.0;
+      for (int c = 0; c < dk; ++c) {
+        qq += qr[h * dk + c] * qr[h * dk + c];
+        kk += kr[h * dk + c] * kr[h * dk + c];
+      }
+      const double qn = sqrt(qq) > 1e-12 ? sqrt(qq) : 1e-12;
+      const double kn = sqrt(kk) > 1e-12 ? sqrt(kk) : 1e-12;
+      for (int c = 0; c < dk; ++c) {
+        qbar[t * E + h * dk + c] = qr[h * dk + c] / qn;
+        kbar[t * E + h * dk + c] = kr[h * dk + c] / kn;
+      }
+      double z = bias[h];
+      for (int64_t j = 0; j < E; ++j) z += W[h * E + j] * qr[j];
+      lam[t * H + h] = 1.0 / (1.0 + exp(-z));
+    }
+  }
+  return 0;
+}

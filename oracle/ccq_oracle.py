@@ -13,6 +13,8 @@ Functions (all arrays are numpy float64, row-major):
                     chunk forms of the backbone update
   gla_fwd_bwd(...)  reverse pass of CCQ-GLA for L = sum <dO, o>
   gdn_fwd_bwd(...)  reverse pass of CCQ-Gated DeltaNet for L = sum <dO, o>
+  prep(...)         per-head l2 normalisation of raw q, k and the gate
+                    lambda = sigmoid(W qraw + b) from the query before the head split
 """
 from __future__ import annotations
 
@@ -63,6 +65,8 @@ def _load():
             lib.ccq_oracle_chunk_fwd.argtypes = [ctypes.POINTER(Shape), ctypes.c_int] + [P] * 14
             lib.ccq_oracle_gla_fwd_bwd.argtypes = [ctypes.POINTER(Shape), ctypes.c_int] + [P] * 12
             lib.ccq_oracle_gdn_fwd_bwd.argtypes = [ctypes.POINTER(Shape), ctypes.c_int] + [P] * 14
+            lib.ccq_oracle_prep.argtypes = [ctypes.c_int32] * 4 + [P] * 7
+            lib.ccq_oracle_prep.restype = ctypes.c_int
             for f in (lib.ccq_oracle_fwd, lib.ccq_oracle_chunk_fwd, lib.ccq_oracle_gla_fwd_bwd,
                       lib.ccq_oracle_gdn_fwd_bwd):
                 f.restype = ctypes.c_int
@@ -178,3 +182,17 @@ def gdn_fwd_bwd(q, k, v, logalpha, beta, lam, dO, scale=1.0, centered=True, seg=
     if rc != 0:
         raise RuntimeError("ccq_oracle_gdn_fwd_bwd failed with code %d" % rc)
     return dict(o=o, dq=dq, dk=dk, dv=dv, dlogalpha=dla, dbeta=dbeta, dlam=dlam)
+
+
+def prep(q, k, W, b):
+    """Raw q, k [B,T,H,dk], W [H, H*dk], b [H] -> dict q, k (per-head unit rows) and
+    lam [B,T,H] = sigmoid(W qraw + b), qraw the token's query over all heads."""
+    q, k, W, b = _f64(q), _f64(k), _f64(W), _f64(b)
+    B, T, H, dk = q.shape
+    assert k.shape == q.shape and W.shape == (H, H * dk) and b.shape == (H,)
+    qb, kb, lam = np.zeros(q.shape), np.zeros(q.shape), np.zeros((B, T, H))
+    rc = _load().ccq_oracle_prep(B, T, H, dk, _ptr(q), _ptr(k), _ptr(W), _ptr(b), _ptr(qb),
+                                 _ptr(kb), _ptr(lam))
+    if rc != 0:
+        raise RuntimeError("ccq_oracle_prep failed with code %d" % rc)
+    return dict(q=qb, k=kb, lam=lam)

@@ -409,3 +409,51 @@ def test_gdn_reverse_pass_without_contraction_or_decay():
     np.testing.assert_allclose(r["dv"], qk * dO, rtol=1e-14)
     np.testing.assert_allclose(r["dbeta"], dv_ * qk, rtol=1e-14)
     np.testing.assert_allclose(r["dlogalpha"], 0.0, atol=1e-15)
+
+
+# ---------------------------------------------------------------- pre-processing
+
+
+def test_prep_normalises_each_head_and_is_scale_invariant():
+    rng = np.random.default_rng(21)
+    B, T, H, dk = 2, 5, 3, 8
+    q = rng.standard_normal((B, T, H, dk)) * rng.uniform(0.1, 10, (B, T, H, 1))
+    k = rng.standard_normal((B, T, H, dk))
+    W = rng.standard_normal((H, H * dk))
+    b = rng.standard_normal(H)
+    r = O.prep(q, k, W, b)
+    np.testing.assert_allclose(np.linalg.norm(r["q"], axis=-1), 1.0, rtol=1e-14)
+    np.testing.assert_allclose(np.linalg.norm(r["k"], axis=-1), 1.0, rtol=1e-14)
+    s = O.prep(3.5 * q, 0.25 * k, W, b)
+    np.testing.assert_allclose(s["q"], r["q"], rtol=1e-13, atol=1e-15)
+    np.testing.assert_allclose(s["k"], r["k"], rtol=1e-13, atol=1e-15)
+    z = O.prep(np.zeros_like(q), k, W, b)
+    assert np.all(z["q"] == 0.0)
+
+
+def test_prep_gate_reads_the_raw_query_before_the_head_split():
+    """W = 0 gives sigmoid(b); a single unit weight W[h][j] picks raw feature j of the whole
+    token (head j // dk, channel j % dk) for gate h; flipping the sign of W and b gives
+    1 - lambda; scaling q by c and W by 1/c leaves lambda unchanged (the gate uses the raw,
+    unnormalised query)."""
+    rng = np.random.default_rng(22)
+    B, T, H, dk = 1, 4, 3, 4
+    q = rng.standard_normal((B, T, H, dk))
+    k = rng.standard_normal((B, T, H, dk))
+    b = rng.standard_normal(H)
+    r0 = O.prep(q, k, np.zeros((H, H * dk)), b)
+    np.testing.assert_allclose(r0["lam"], np.broadcast_to(1 / (1 + np.exp(-b)), (B, T, H)), rtol=1e-14)
+    W = np.zeros((H, H * dk))
+    W[0, 2 * dk + 1] = 1.0       # gate 0 <- head 2, channel 1
+    W[2, 3] = 1.0                # gate 2 <- head 0, channel 3
+    r1 = O.prep(q, k, W, np.zeros(H))
+    sig = lambda x: 1 / (1 + np.exp(-x))
+    np.testing.assert_allclose(r1["lam"][..., 0], sig(q[:, :, 2, 1]), rtol=1e-14)
+    np.testing.assert_allclose(r1["lam"][..., 1], 0.5, rtol=1e-14)
+    np.testing.assert_allclose(r1["lam"][..., 2], sig(q[:, :, 0, 3]), rtol=1e-14)
+    W = rng.standard_normal((H, H * dk))
+    a = O.prep(q, k, W, b)
+    f = O.prep(q, k, -W, -b)
+    np.testing.assert_allclose(a["lam"] + f["lam"], 1.0, rtol=1e-14)
+    c = O.prep(4.0 * q, k, W / 4.0, b)
+    np.testing.assert_allclose(c["lam"], a["lam"], rtol=1e-13)
