@@ -126,6 +126,9 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
         gb = dk * gate_bytes if w.backbone == 0 else 8
         by = BH * (8 * dv * dk + 8 * dk * dk + dk * (2 * io_bytes + 20) + 2 * dv * io_bytes + gb + 4)
         fl = BH * (5 * dk * dk + 6 * dv * dk)
+    elif kernel == "prep":          # raw q, k in; normalised q, k and the gate out (W_lambda once)
+        by = ntok * (4 * dk * io_bytes + 4) + w.H * w.H * dk * 4 + w.H * 4
+        fl = ntok * (2 * w.H * dk + 6 * dk)
     elif kernel == "ccq_dk":
         by = ntok * (3 * dk * io_bytes + 12 + 4 * dk + dk * io_bytes)
         fl = ntok * (6 * dk * dk + 8 * C * dk)
@@ -143,7 +146,7 @@ KERNELS = {0: ["gla_state"] + CLEAN + ["clean_out", "gla_out"],
            "gdn_train": CLEAN + ["clean_out_train", "gdn_tri", "gdn_state", "gdn_out",
                                  "gdn_bwd_prep", "gdn_dstate", "gdn_bwd_chunk", "clean_dq",
                                  "ccq_dk"]}
-KERNEL_SYMBOL = {"decode": "decode_stats_kernel+decode_out_kernel", "clean_gram": "clean_gram_kernel",
+KERNEL_SYMBOL = {"prep": "prep_kernel", "decode": "decode_stats_kernel+decode_out_kernel", "clean_gram": "clean_gram_kernel",
                  "clean_prefix": "clean_prefix_kernel", "clean_out": "clean_out_kernel",
                  "clean_out_train": "clean_out_kernel", "clean_dq": "clean_out_kernel",
                  "gla_state": "gla_state_kernel", "gla_scan": "gla_scan_kernel", "gla_out": "gla_out_kernel",
@@ -163,6 +166,8 @@ def _source(kernel: str) -> str:
         return "ccq_gdn_bwd.hip"
     if kernel == "decode":
         return "ccq_decode.hip"
+    if kernel == "prep":
+        return "ccq_prep.hip"
     if kernel.startswith("gdn"):
         return "ccq_gdn.hip"
     return "ccq_bwd.hip"
@@ -273,6 +278,28 @@ class DecodeCall:
                             workspace=self.ws)
 
 
+class PrepCall:
+    """Pre-processing of a workload's raw q, k (l2 normalisation per head and the gate
+    from the pre-split query), inputs resident on the GPU."""
+
+    def __init__(self, w, torch, ccq, inputs):
+        import dataclasses
+        self.w = dataclasses.replace(w, name=w.name.replace("_t", "_prep_t"))
+        gen = torch.Generator().manual_seed(w.seed)
+        B, T, H, dk = w.B, w.T, w.H, w.dk
+        self.q = torch.randn(B, T, H, dk, generator=gen).to(w.dtype).cuda()
+        self.k = torch.randn(B, T, H, dk, generator=gen).to(w.dtype).cuda()
+        self.wl = (torch.randn(H, H * dk, generator=gen) / (H * dk) ** 0.5).cuda()
+        self.bl = torch.randn(H, generator=gen).cuda()
+        self.out = {"q": torch.empty_like(self.q), "k": torch.empty_like(self.k),
+                    "lam": torch.empty((B, T, H), dtype=torch.float32, device=self.q.device)}
+        self.ccq = ccq
+        self.kernels = ["prep"]
+
+    def __call__(self):
+        self.ccq.ccq_prep(self.q, self.k, self.wl, self.bl, out=self.out)
+
+
 def time_calls(torch, ccq, calls, steps, warmup, with_plain=False):
     """Warm up, then time exactly `steps` steps (each step = every call once) between two
     synchronisations; per-kernel durations come from HIP events the library records on
@@ -351,14 +378,21 @@ def roofline(entry, w):
 
 
 EXTRA = ("gla_500m_t2k", "gdn_1p3b_t4k", "gla_500m_t20k", "gdn_1p3b_t20k", "gla_train_t4k",
-         "gdn_train_t4k", "gla_500m_decode_t2k", "gdn_1p3b_decode_t4k")
+         "gdn_train_t4k", "gla_500m_decode_t2k", "gdn_1p3b_decode_t4k", "gdn_1p3b_prep_t4k")
 
 
 def measure_extra(name, torch, ccq, inputs, steps, existing):
     """Figures of one workload on its own: tokens/s from untimed-event steps, per-kernel
     durations and the dominant kernel's roofline from the traced steps."""
     W = inputs.WORKLOADS
-    if "_decode_" in name:
+    if "_prep_" in name:
+        c = PrepCall(W[name.replace("_prep_t", "_t")], torch, ccq, inputs)
+        ms, ms_tr, pk = time_calls(torch, ccq, [c], max(20, steps), 5, with_plain=True)
+        res = {"tokens_per_s": round(c.w.tokens / (ms * 1e-3), 1), "ms": round(ms, 5),
+               "ms_traced": round(ms_tr, 5),
+               "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
+               "roofline": roofline(pk[0], c.w)}
+    elif "_decode_" in name:
         c = DecodeCall(W[name.replace("_decode_t", "_t")], torch, ccq, inputs)
         ms, ms_tr, pk = time_calls(torch, ccq, [c], max(20, steps), 5, with_plain=True)
         res = {"tokens_per_s": round(c.w.B / (ms * 1e-3), 1), "ms": round(ms, 5),

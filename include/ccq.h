@@ -148,6 +148,22 @@ ccq_status ccq_decode(const ccq_shape* s, ccq_backbone bb, const void* q, const 
                       size_t ws_bytes, void* stream);
 
 /*
+ * Pre-processing of one layer's raw queries and keys (Alg. 1: the per-chunk
+ * l2 normalisation of Q and K, and the gate Lambda = sigma(Q W_lambda^T +
+ * b_lambda) computed from the query before normalisation; Eq. clean):
+ *   q[b,t,h,:] = q_raw[b,t,h,:] / max(|q_raw[b,t,h,:]|, 1e-12), k likewise;
+ *   lam[b,t,h] = sigmoid(sum_j w_lam[h][j] q_raw[b,t,j] + b_lam[h]),
+ * where j runs over all H*dk features of the token's query before the split
+ * into heads (head-major).  q_raw, k_raw, q, k [B,T,H,dk] io_dtype; w_lam
+ * [H, H*dk] fp32; b_lam [H] fp32; lam [B,T,H] fp32.  q and k may be q_raw and
+ * k_raw (in place).  Uses s->B, T, H, dk and io_dtype.  Supported: dk in
+ * {64,128,256}, H <= 16, H*dk <= 2048 and H*H*dk <= 16384 (W_lambda is
+ * staged on chip); otherwise CCQ_ERR_UNSUPPORTED.  Allocates nothing.
+ */
+ccq_status ccq_prep(const ccq_shape* s, const void* q_raw, const void* k_raw, const float* w_lam,
+                    const float* b_lam, void* q, void* k, float* lam, void* stream);
+
+/*
  * Per-kernel timing hook (instrumentation for benchmarks and profilers, not
  * part of the method).  `events` points at n_events hipEvent_t handles created
  * by the caller (hipEventCreate).  Until the next ccq_trace_events call from

@@ -23,8 +23,8 @@ CCQ_GLA, CCQ_GDN = 0, 1
 _STATUS = {0: "CCQ_OK", 1: "CCQ_ERR_INVALID_ARG", 2: "CCQ_ERR_UNSUPPORTED",
            3: "CCQ_ERR_WORKSPACE", 4: "CCQ_ERR_HIP"}
 EXPORTS = ("ccq_workspace_size", "ccq_gla_fwd", "ccq_gdn_fwd", "ccq_fwd_bwd",
-           "ccq_decode_workspace_size", "ccq_decode", "ccq_trace_events", "ccq_status_string",
-           "ccq_version")
+           "ccq_decode_workspace_size", "ccq_decode", "ccq_prep", "ccq_trace_events",
+           "ccq_status_string", "ccq_version")
 
 
 class CcqError(RuntimeError):
@@ -69,6 +69,8 @@ def lib() -> ctypes.CDLL:
             L.ccq_decode_workspace_size.restype = S
             L.ccq_decode.argtypes = [SP, ctypes.c_int] + [P] * 11 + [S, P]
             L.ccq_decode.restype = ctypes.c_int
+            L.ccq_prep.argtypes = [SP] + [P] * 8
+            L.ccq_prep.restype = ctypes.c_int
             L.ccq_trace_events.argtypes = [P, ctypes.c_int]
             L.ccq_trace_events.restype = ctypes.c_int
             L.ccq_status_string.argtypes = [ctypes.c_int]
@@ -297,3 +299,25 @@ def ccq_decode(q, k, v, gate, lam, S, C, mu, t0, backbone=CCQ_GLA, beta=None, sc
     if rc != 0:
         raise CcqError("ccq_decode", rc)
     return o
+
+
+def ccq_prep(q_raw, k_raw, w_lam, b_lam, out=None, stream=None):
+    """Per-head l2 normalisation of raw q, k [B,T,H,dk] and the gate
+    lam = sigmoid(w_lam qraw + b_lam) [B,T,H] from the token's query before the head
+    split (w_lam [H, H*dk] fp32, b_lam [H] fp32).  Returns dict q, k, lam; pass
+    out=dict(q=q_raw, k=k_raw) to normalise in place."""
+    B, T, H, dk = q_raw.shape
+    dev = q_raw.device
+    _check(k_raw, "k_raw", (B, T, H, dk), q_raw.dtype, dev)
+    _check(w_lam, "w_lam", (H, H * dk), torch.float32, dev)
+    _check(b_lam, "b_lam", (H,), torch.float32, dev)
+    out = dict(out or {})
+    out.setdefault("q", torch.empty_like(q_raw))
+    out.setdefault("k", torch.empty_like(k_raw))
+    out.setdefault("lam", torch.empty((B, T, H), dtype=torch.float32, device=dev))
+    shape = make_shape(B, T, H, dk, dk, q_raw.dtype)
+    rc = lib().ccq_prep(ctypes.byref(shape), _p(q_raw), _p(k_raw), _p(w_lam), _p(b_lam),
+                        _p(out["q"]), _p(out["k"]), _p(out["lam"]), _stream(stream))
+    if rc != 0:
+        raise CcqError("ccq_prep", rc)
+    return out

@@ -589,6 +589,25 @@ ccq_status ccq_decode(const ccq_shape* s, ccq_backbone bb, const void* q, const 
   return CCQ_OK;
 }
 
+ccq_status ccq_prep(const ccq_shape* s, const void* q_raw, const void* k_raw, const float* w_lam,
+                    const float* b_lam, void* q, void* k, float* lam, void* stream) {
+  if (!s) return CCQ_ERR_INVALID_ARG;
+  if (s->B < 0 || s->T < 0 || s->H < 0) return CCQ_ERR_INVALID_ARG;
+  if (!dtype_ok(s->io_dtype)) return CCQ_ERR_INVALID_ARG;
+  if ((long long)s->B * s->T * s->H == 0) return CCQ_OK;
+  if (!ccq::prep_supported(s->H, s->dk)) return CCQ_ERR_UNSUPPORTED;
+  const void* req[] = {q_raw, k_raw, w_lam, b_lam, q, k, lam};
+  for (const void* p : req)
+    if (!p || !aligned(p)) return CCQ_ERR_INVALID_ARG;
+  if ((long long)s->B * s->T / 16 >= (1LL << 31)) return CCQ_ERR_UNSUPPORTED;
+  ccq::PrepArgs a{q_raw, k_raw, w_lam, b_lam, q, k, lam, s->B, s->T, s->H, s->dk};
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  trace_begin_call();
+  if (traced(st, [&] { return ccq::launch_prep(a, s->io_dtype == CCQ_BF16, st); }) != hipSuccess)
+    return CCQ_ERR_HIP;
+  return CCQ_OK;
+}
+
 ccq_status ccq_trace_events(void* const* events, int n_events) {
   if (events == nullptr || n_events <= 0) {
     g_trace = Trace{};

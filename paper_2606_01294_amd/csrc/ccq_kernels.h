@@ -260,6 +260,20 @@ struct DecodeArgs {
   int64_t t0;            // tokens before this one (its position is t0 + 1)
 };
 
+// ---- pre-processing: per-head l2 normalisation and the gate ----
+constexpr int kPrepMaxHeads = 16;
+constexpr size_t kPrepMaxLds = 65536;  // W_lambda staged in LDS (fp32)
+struct PrepArgs {
+  const void* q_raw;     // [B,T,H,dk] io
+  const void* k_raw;     // [B,T,H,dk] io
+  const float* w;        // [H, H*dk] fp32
+  const float* b;        // [H] fp32
+  void* q;               // [B,T,H,dk] io (may be q_raw)
+  void* k;               // [B,T,H,dk] io (may be k_raw)
+  float* lam;            // [B,T,H] fp32
+  int B, T, H, dk;
+};
+
 // Each launcher returns hipSuccess or the launch error.  is_bf16 selects the
 // io dtype (bf16 or fp32); shapes are validated by the caller.
 hipError_t launch_clean_gram(const CleanArgs& a, bool is_bf16, hipStream_t st);
@@ -297,6 +311,8 @@ hipError_t launch_gdn_dstate(const GdnDstateArgs& a, bool is_bf16, hipStream_t s
 hipError_t launch_gdn_bwd_chunk(const GdnBwdArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_decode(const DecodeArgs& a, bool gdn, bool is_bf16, bool gate_bf16, hipStream_t st);
 bool decode_supported(int dk, int dv);
+hipError_t launch_prep(const PrepArgs& a, bool is_bf16, hipStream_t st);
+bool prep_supported(int H, int dk);
 
 // Supported-shape predicates (used by validation before any launch).
 bool clean_supported(int dk, bool is_bf16);

@@ -142,3 +142,16 @@ def test_decode_entry_point_validation():
     assert call_decode(shape(T=1), ws_bytes=8) == 3          # workspace too small
     assert call_decode(shape(T=1), ptr=FAKE + 4) == 1        # misaligned tensor
     assert call_decode(shape(B=0, T=1), ptr=0, ws_ptr=None) == 0
+
+
+def test_prep_entry_point_validation():
+    P = ctypes.c_void_p
+
+    def call(s, ptr=FAKE):
+        return ccq.lib().ccq_prep(ctypes.byref(s), P(ptr), P(ptr), P(ptr), P(ptr), P(ptr), P(ptr),
+                                  P(ptr), None)
+    assert call(shape(H=17, dk=64)) == 2                  # too many heads
+    assert call(shape(H=16, dk=128)) == 2                 # W_lambda does not fit on chip
+    assert call(shape(H=4, dk=96)) == 2
+    assert call(shape(H=4, dk=64), ptr=FAKE + 4) == 1     # misaligned
+    assert call(shape(B=0, H=4, dk=64), ptr=0) == 0
