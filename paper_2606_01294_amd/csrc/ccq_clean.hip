@@ -395,18 +395,30 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
           rs += sv[e + q];
         }
       }
-      const T* xrow = sX + i * LDK + FPT * pp;
-      const float* mrow = sM + FPT * pp;
-      const float* crow = sC + FPT * pp;
+      // this thread's features are the 4-wide groups pp, pp + TPI, ...: the TPI
+      // threads of a token read adjacent 8- and 16-byte pieces (no bank conflicts)
+      const T* xrow = sX + i * LDK + 4 * pp;
+      const float* mrow = sM + 4 * pp;
+      const float* crow = sC + 4 * pp;
 #pragma unroll
-      for (int e = 0; e < FPT; e += 8) {
-        const vec_t xv = *reinterpret_cast<const vec_t*>(xrow + e);
-        const f32x4 m0 = *reinterpret_cast<const f32x4*>(mrow + e), m1 = *reinterpret_cast<const f32x4*>(mrow + e + 4);
-        const f32x4 c0 = *reinterpret_cast<const f32x4*>(crow + e), c1 = *reinterpret_cast<const f32x4*>(crow + e + 4);
+      for (int e = 0; e < FPT; e += 4) {
+        const int f = TPI * e;  // = 4 TPI (e / 4)
+        float xv[4];
+        if constexpr (sizeof(T) == 2) {
+          const bf16x4 x4 = *reinterpret_cast<const bf16x4*>(xrow + f);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) xv[q] = f32(x4[q]);
+        } else {
+          const f32x4 x4 = *reinterpret_cast<const f32x4*>(xrow + f);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) xv[q] = x4[q];
+        }
+        const f32x4 m4 = *reinterpret_cast<const f32x4*>(mrow + f);
+        const f32x4 c4 = *reinterpret_cast<const f32x4*>(crow + f);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          mq += f32(xv[q]) * m0[q] + f32(xv[q + 4]) * m1[q];
-          cx += f32(xv[q]) * c0[q] + f32(xv[q + 4]) * c1[q];
+          mq += xv[q] * m4[q];
+          cx += xv[q] * c4[q];
         }
       }
       rs = group_sum<TPI>(rs);
