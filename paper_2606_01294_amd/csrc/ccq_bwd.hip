@@ -297,28 +297,48 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
 // dg_t = sum_{s >= t} db_s: one workgroup per chunk, one thread per channel.
 template <typename TG>
 __global__ __launch_bounds__(kThreads) void gla_dg_kernel(const DgArgs a) {
-  constexpr int C = kChunk;
+  constexpr int C = kChunk, HC = C / 2;
+  __shared__ float sHalf[kThreads];
   const int N = (a.T + C - 1) / C;
   const int lb = blockIdx.x;
   const int bh = lb / N, ci = lb % N;
   const int b = bh / a.H, h = bh % a.H;
   const int r0 = ci * C;
   const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-  TG* dg = static_cast<TG*>(a.dg);
-  for (int c = threadIdx.x; c < a.dk; c += kThreads) {
-    float acc = 0.f;
-    for (int r = ci + 1; r < N; ++r) acc += a.db_tot[((size_t)bh * N + r) * a.dk + c];
-    float x[C];
-#pragma unroll
-    for (int j = 0; j < C; ++j) {
-      const int jj = j < nrow ? j : nrow - 1;
-      x[j] = a.db[tok_off(b, r0 + jj, h, a.T, a.H, a.dk) + c];
+  const int hd = a.H * a.dk;
+  TG* dg = static_cast<TG*>(a.dg) + tok_off(b, r0, h, a.T, a.H, a.dk);
+  const float* db = a.db + tok_off(b, r0, h, a.T, a.H, a.dk);
+  // thread (c, half): half 1 takes rows 32..63 of channel c, half 0 rows 0..31
+  const int npc = kThreads / 2;  // channels per pass
+  for (int c0 = 0; c0 < a.dk; c0 += npc) {
+    const int c = c0 + (threadIdx.x % npc), half = threadIdx.x / npc;
+    const bool on = c < a.dk;
+    float later = 0.f;  // sum over the later chunks (half 1 only)
+    if (on && half == 1) {
+      const float* tot = a.db_tot + (size_t)bh * N * a.dk + c;
+#pragma unroll 8
+      for (int r = ci + 1; r < N; ++r) later += tot[(size_t)r * a.dk];
     }
+    float x[HC];
 #pragma unroll
-    for (int j = C - 1; j >= 0; --j) {
-      if (j < nrow) {
+    for (int j = 0; j < HC; ++j) {
+      const int row = HC * half + j;
+      x[j] = on ? db[(row < nrow ? row : nrow - 1) * hd + c] : 0.f;
+    }
+    float run = 0.f;  // sum of this half's rows
+#pragma unroll
+    for (int j = 0; j < HC; ++j) run += (HC * half + j < nrow) ? x[j] : 0.f;
+    sHalf[threadIdx.x] = run + later;
+    __syncthreads();
+    // half 0 starts from everything after row 31; half 1 from the later chunks
+    float acc = half == 0 ? sHalf[threadIdx.x + npc] : later;
+    __syncthreads();
+#pragma unroll
+    for (int j = HC - 1; j >= 0; --j) {
+      const int row = HC * half + j;
+      if (on && row < nrow) {
         acc += x[j];
-        dg[tok_off(b, r0 + j, h, a.T, a.H, a.dk) + c] = static_cast<TG>(acc);
+        dg[row * hd + c] = static_cast<TG>(acc);
       }
     }
   }
