@@ -283,15 +283,25 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
     sC[tid] = cen;
     sM[tid] = run - (t0f + (float)((int64_t)cbeg * C)) * cen;
   }
-  // entry moment S'_s: S[nt][mt] is tile (n0 / 16 + nt, mt) of the
-  // fragment-native layout (rows m = 16 mt + 4 (l / 16) + r, column n0 + 16 nt + l % 16)
+  // entry moment S'_s, held with its rows in pair order: accumulator row
+  // 4 g + r of tile mt is feature pair_feat(mt, g, r) = 32 (mt / 2) + 8 g +
+  // 4 (mt % 2) + r, so that two tiles pack into an operand fragment whose k
+  // slots are 8 consecutive features (one 16-byte LDS read for the matching
+  // x fragment).  The stored layout is fragment-native in natural row order
+  // (rows m = 16 mt + 4 (l / 16) + r, column n0 + 16 nt + l % 16): tile mt,
+  // lane group g reads its 4 rows from tile 2 (mt / 2) + g / 2, group
+  // 2 (g % 2) + mt % 2.
   f32x4 S[NNT][NMT];
   {
-    const T* sp = static_cast<const T*>(a.sprime) + so * DK * DK + ((size_t)(n0 / 16) * NMT * 64 + (tid & 63)) * 4;
+    const int lg = (tid & 63) >> 4, lc = tid & 15;
+    const T* sp = static_cast<const T*>(a.sprime) + so * DK * DK + (size_t)(n0 / 16) * NMT * 64 * 4;
 #pragma unroll
     for (int nt = 0; nt < NNT; ++nt)
 #pragma unroll
-      for (int mt = 0; mt < NMT; ++mt) S[nt][mt] = load4f(sp + ((size_t)nt * NMT + mt) * 256);
+      for (int mt = 0; mt < NMT; ++mt) {
+        const int mo = 2 * (mt >> 1) + (lg >> 1), go = 2 * (lg & 1) + (mt & 1);
+        S[nt][mt] = load4f(sp + (((size_t)nt * NMT + mo) * 64 + 16 * go + lc) * 4);
+      }
   }
   if constexpr (kDma) wait_vm_all();
   __syncthreads();  // sC, first chunk
@@ -348,15 +358,17 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
     f32x4 acc[NNT][4];
     {
       const int l_ = opaque(tid & 63), g_ = l_ >> 4, c_ = l_ & 15;
-      const T* pxa = sX + c_ * LDK + 4 * g_;
-      const T* pka = sK + c_ * LDK + 4 * g_;
-      for (int t = w; t < 10; t += NW) {
-        const int I = causal_tile_i(t), J = t - I * (I + 1) / 2;
-        f32x4 sc = zero4();
+      // x fragments in natural feature order: one 16-byte read per lane
+      const T* px8 = sX + c_ * LDK + 8 * g_;
+      {
+        const T* pk8 = sK + c_ * LDK + 8 * g_;
+        for (int t = w; t < 10; t += NW) {
+          const int I = causal_tile_i(t), J = t - I * (I + 1) / 2;
+          f32x4 sc = zero4();
 #pragma unroll
-        for (int p = 0; p < NK; ++p)
-          mma(sc, frag_acc_at(pka + 16 * J * LDK + 32 * p), frag_acc_at(pxa + 16 * I * LDK + 32 * p));
-        *reinterpret_cast<f32x4*>(sS + (16 * I + c_) * LDQ + 16 * J + 4 * g_) = sc;
+          for (int p = 0; p < NK; ++p) mma(sc, frag_at(pk8 + 16 * J * LDK + 32 * p), frag_at(px8 + 16 * I * LDK + 32 * p));
+          *reinterpret_cast<f32x4*>(sS + (16 * I + c_) * LDQ + 16 * J + 4 * g_) = sc;
+        }
       }
 #pragma unroll
       for (int nt = 0; nt < NNT; ++nt)
@@ -366,7 +378,7 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
       for (int p = 0; p < NK; ++p) {
         Frag<T> xf[4], af[NNT];
 #pragma unroll
-        for (int I = 0; I < 4; ++I) xf[I] = frag_acc_at(pxa + 16 * I * LDK + 32 * p);
+        for (int I = 0; I < 4; ++I) xf[I] = frag_at(px8 + 16 * I * LDK + 32 * p);
 #pragma unroll
         for (int nt = 0; nt < NNT; ++nt) af[nt] = acc_pair_frag<T>(S[nt][2 * p], S[nt][2 * p + 1]);
 #pragma unroll
@@ -444,6 +456,8 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
     {
       const int l_ = opaque(tid & 63), g_ = l_ >> 4, c_ = l_ & 15;
       const T* ptr = sK + frag_tr_lane_off<T>(l_, LDK);
+      // K'^T rows in the pair order of the moment's tiles (the update)
+      const T* ptr_pair = sK + frag_tr_pair_lane_off<T>(l_, LDK);
       // K'^T fragments of this wave's columns (intra-chunk product and update)
       Frag<T> kb[NNT][2];
 #pragma unroll
@@ -509,7 +523,10 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
 #pragma unroll
           for (int e = 0; e < G; ++e)
 #pragma unroll
-            for (int q = 0; q < 2; ++q) f[2 * e + q] = frag_tr_any(ptr + 32 * q * LDK + 16 * (G * g + e), LDK);
+            for (int q = 0; q < 2; ++q) {
+              const int mt = G * g + e;
+              f[2 * e + q] = frag_tr_any(ptr_pair + 32 * q * LDK + 32 * (mt >> 1) + 4 * (mt & 1), LDK);
+            }
         };
         load_group(ka[0], 0);
 #pragma unroll

@@ -138,6 +138,46 @@ __device__ __forceinline__ Frag<float> ld_frag_tr_acc<float>(const float* base, 
   return f;
 }
 
+// ld_frag_tr_acc with the fragment's 16 rows (X's columns) taken in pair
+// order: fragment row m is column pair_col(t, m) = 32 (t / 2) + 8 (m / 4) +
+// 4 (t % 2) + m % 4 of X for tile t of a 32-column block pair.  Accumulator
+// tiles 2s and 2s + 1 formed from such operands hold, in lane group g, the 8
+// consecutive columns 32 s + 8 g .. + 7, so acc_pair_frag packs them into an
+// operand whose k slots are in natural order (read by plain ld_frag).  `base`
+// points at X[k0][c0]; t is the 16-column tile index counted from c0 (c0 a
+// multiple of 32).
+template <typename T>
+__device__ __forceinline__ Frag<T> ld_frag_tr_acc_pair(const T* base, int ld, int t);
+
+template <>
+__device__ __forceinline__ Frag<bf16_t> ld_frag_tr_acc_pair<bf16_t>(const bf16_t* base, int ld, int t) {
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  const int l = lane_id(), g = l >> 4, j = l & 15;
+  const bf16_t* p = base + (4 * g + (j >> 2)) * ld + 32 * (t >> 1) + 4 * (t & 1) + 8 * (j & 3);
+  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p));
+  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p + 16 * ld));
+  Frag<bf16_t> f;
+  f.v = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return f;
+}
+
+template <>
+__device__ __forceinline__ Frag<float> ld_frag_tr_acc_pair<float>(const float* base, int ld, int t) {
+  const int l = lane_id(), g = l >> 4, m = l & 15;
+  const int col = 32 * (t >> 1) + 4 * (t & 1) + 8 * (m >> 2) + (m & 3);
+  Frag<float> f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    f.lo[e] = base[(4 * g + e) * ld + col];
+    f.hi[e] = base[(16 + 4 * g + e) * ld + col];
+  }
+  return f;
+}
+
+// Feature held in accumulator row 4 g + r of tile t of a pair-ordered state
+// (ld_frag_tr_acc_pair): 32 (t / 2) + 8 g + 4 (t % 2) + r.
+__host__ __device__ __forceinline__ int pair_feat(int t, int g) { return 32 * (t >> 1) + 8 * g + 4 * (t & 1); }
+
 // Row-operand fragment in the same k-slot order as ld_frag_tr_acc: lane l
 // reads row (l % 16) of a row-major tile at k = 4g .. 4g+3 and 16 + 4g ..
 // 16 + 4g + 3 (g = l / 16).  `tile` points at (row 0, k0); works for LDS or
@@ -549,6 +589,17 @@ __device__ __forceinline__ int frag_tr_lane_off(int l, int ld) {
   const int g = l >> 4, j = l & 15;
   if constexpr (sizeof(T) == 2) return (8 * g + (j >> 2)) * ld + 4 * (j & 3);
   else return 8 * g * ld + j;
+}
+// As frag_tr_lane_off, with the 16 columns of the tile taken in pair order:
+// fragment row m reads column 8 (m / 4) + m % 4 (columns 0..3, 8..11, 16..19,
+// 24..27 of a 32-wide block; add 4 for the other half).  Two such tiles are
+// the rows of a pair of accumulator tiles whose packed fragment has 8
+// consecutive columns per lane group.
+template <typename T>
+__device__ __forceinline__ int frag_tr_pair_lane_off(int l, int ld) {
+  const int g = l >> 4, j = l & 15;
+  if constexpr (sizeof(T) == 2) return (8 * g + (j >> 2)) * ld + 8 * (j & 3);
+  else return 8 * g * ld + 8 * (j >> 2) + (j & 3);
 }
 
 // Sum over aligned groups of n consecutive lanes (n = 2, 4, 8, 16), by

@@ -19,9 +19,11 @@
 // slice of S in MFMA accumulators, and stores S_r and U for every chunk;
 // gdn_out_kernel then forms the outputs of all chunks in parallel.  S_r and
 // U^T are stored fragment-native: per 16-row value tile and 32-wide k step a
-// contiguous 16 x 32 block, each row in accumulator-pair order (acc_pos), so
-// the state kernel writes and the output kernel reads 1 KB per instruction,
-// already in MFMA operand order.
+// contiguous 16 x 32 block, so the state kernel writes and the output kernel
+// reads 1 KB per instruction, already in MFMA operand order.  Rows of S_r are
+// in natural feature order (the state kernel keeps its accumulator tiles in
+// pair order, ld_frag_tr_acc_pair); rows of U^T are in accumulator-pair order
+// (acc_pos) over the chunk's tokens.
 #include "ccq_device.h"
 #include "ccq_kernels.h"
 
@@ -190,12 +192,14 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
   const T* vin = static_cast<const T*>(a.v);
   const T* Tg = static_cast<const T*>(a.Tm);
 
-  // S^T[c][v], c = c0 + 16 tc + 4 g4 + r
+  // S^T[c][v] in pair order: c = c0 + pair_feat(tc, g4) + r, so that the
+  // packed operand of tiles 2m, 2m + 1 holds 8 consecutive features per lane
+  // group (the states are stored so, and K is read with plain 16-byte reads)
   f32x4 S[NCT];
 #pragma unroll
   for (int tc = 0; tc < NCT; ++tc) {
     if (a.S0)
-      S[tc] = *reinterpret_cast<const f32x4*>(a.S0 + ((size_t)bh * a.dv + v) * DK + c0 + 16 * tc + 4 * g4);
+      S[tc] = *reinterpret_cast<const f32x4*>(a.S0 + ((size_t)bh * a.dv + v) * DK + c0 + pair_feat(tc, g4));
     else
       S[tc] = zero4();
   }
@@ -261,12 +265,12 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
     f32x4 R[4];
     Frag<T> kf[2][NKH];
 #pragma unroll
-    for (int m = 0; m < NKH; ++m) kf[0][m] = ld_frag_acc(Kb + c0 + 32 * m, (size_t)LDQ);
+    for (int m = 0; m < NKH; ++m) kf[0][m] = ld_frag(Kb + c0 + 32 * m, LDQ);
 #pragma unroll
     for (int J = 0; J < 4; ++J) {
       if (J + 1 < 4)
 #pragma unroll
-        for (int m = 0; m < NKH; ++m) kf[(J + 1) & 1][m] = ld_frag_acc(Kb + 16 * (J + 1) * LDQ + c0 + 32 * m, (size_t)LDQ);
+        for (int m = 0; m < NKH; ++m) kf[(J + 1) & 1][m] = ld_frag(Kb + 16 * (J + 1) * LDQ + c0 + 32 * m, LDQ);
       __builtin_amdgcn_sched_barrier(0);
       f32x4 acc = zero4();
 #pragma unroll
@@ -322,8 +326,8 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
     Frag<T> tf[2][TB][2];
 #pragma unroll
     for (int t = 0; t < TB; ++t) {
-      tf[0][t][0] = ld_frag_tr_acc(Kb + c0 + 16 * t, LDQ);
-      tf[0][t][1] = ld_frag_tr_acc(Kb + 32 * LDQ + c0 + 16 * t, LDQ);
+      tf[0][t][0] = ld_frag_tr_acc_pair(Kb + c0, LDQ, t);
+      tf[0][t][1] = ld_frag_tr_acc_pair(Kb + 32 * LDQ + c0, LDQ, t);
     }
 #pragma unroll
     for (int tb = 0; tb < NCT / TB; ++tb) {
@@ -331,8 +335,8 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
 #pragma unroll
         for (int t = 0; t < TB; ++t) {
           const int tc = TB * (tb + 1) + t;
-          tf[(tb + 1) & 1][t][0] = ld_frag_tr_acc(Kb + c0 + 16 * tc, LDQ);
-          tf[(tb + 1) & 1][t][1] = ld_frag_tr_acc(Kb + 32 * LDQ + c0 + 16 * tc, LDQ);
+          tf[(tb + 1) & 1][t][0] = ld_frag_tr_acc_pair(Kb + c0, LDQ, tc);
+          tf[(tb + 1) & 1][t][1] = ld_frag_tr_acc_pair(Kb + 32 * LDQ + c0, LDQ, tc);
         }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -352,16 +356,17 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
   if (a.ST) {
 #pragma unroll
     for (int tc = 0; tc < NCT; ++tc)
-      *reinterpret_cast<f32x4*>(a.ST + ((size_t)bh * a.dv + v) * DK + c0 + 16 * tc + 4 * g4) = S[tc];
+      *reinterpret_cast<f32x4*>(a.ST + ((size_t)bh * a.dv + v) * DK + c0 + pair_feat(tc, g4)) = S[tc];
   }
 }
 
 // The same recurrence for bf16 with the chunk operands streamed straight into
-// LDS (global_load_lds_dwordx4), two chunks ahead, through a ring of three
-// stages: K (64 x DK), Tm (64 x 64), the V slice (64 x BVS) and the four
-// coefficient rows.  No registers hold prefetched data and no instructions
-// copy it; the vector-memory counter is waited on explicitly, with the chunk
-// stores of the two previous chunks allowed to remain in flight.  Rows are
+// LDS (global_load_lds_dwordx4), NSTAGE - 1 chunks ahead, through a ring of
+// NSTAGE stages: K (64 x DK), Tm (64 x 64), the V slice (64 x BVS) and the
+// four coefficient rows.  No registers hold prefetched data and no
+// instructions copy it; the vector-memory counter is waited on explicitly,
+// with the chunk stores of the NSTAGE - 1 previous chunks allowed to remain in
+// flight.  Rows are
 // unpadded, so K and Tm are stored with their 16-byte pieces permuted per row
 // (an XOR of the piece index) to keep the fragment reads free of bank
 // conflicts: piece p of K row r sits at p ^ kswz(r), of Tm row r at p ^ tswz(r).
@@ -373,7 +378,7 @@ __device__ __forceinline__ void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(X) : "memory");
 }
 
-template <int DK, int NPR, int NH>
+template <int DK, int NPR, int NH, int NSTAGE>
 __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const GdnArgs a) {
   typedef bf16_t T;
   typedef __attribute__((address_space(3))) void lds_void;
@@ -382,12 +387,14 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
   constexpr int RB = DK * 2;                                  // K row bytes
   constexpr int KB = C * RB, TB = C * C * 2, VB = C * BVS * 2, FB = 4 * C * 4;
   constexpr int NIK = KB / 1024, NIT = TB / 1024, NIV = VB / 1024;
-  constexpr int NIW = (NIK + NIT + NIV) / NW + 1;             // 1 KB pieces per wave and chunk
-  constexpr int SB = KB + TB + VB + FB, NSTAGE = 3;
+  constexpr int NIVW = (NIV + NW - 1) / NW;                   // V pieces per wave (some idle)
+  constexpr int NIW = NIK / NW + NIT / NW + NIVW + 1;         // 1 KB pieces per wave and chunk
+  constexpr int SB = KB + TB + VB + FB;
   constexpr int XB = NH > 1 ? NW * 4 * 64 * 16 : 16;
   constexpr int NSW = NKH + (NH == 1 ? 2 : 1);                // stores per wave per chunk
   static_assert(DK == 128 || DK == 256, "key width");
-  static_assert(NH == 1 || NH == 2, "key split");
+  static_assert(NH == 1 || NH == 2 || NH == 4, "key split");
+  static_assert(NSTAGE == 2 || NSTAGE == 3, "ring depth");
   static_assert(NKH >= 1 && VB % 1024 == 0, "tiles");
   __shared__ __align__(1024) char smem[NSTAGE * SB + XB + 1024];
   f32x4* const sX = reinterpret_cast<f32x4*>(smem + NSTAGE * SB);
@@ -408,12 +415,13 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
   const T* vin = static_cast<const T*>(a.v);
   const T* Tg = static_cast<const T*>(a.Tm);
 
-  // chunk ci into stage ci % 3.  Piece i of each operand goes to wave i % NW,
-  // so every wave issues the same number of pieces of each kind.  Addresses
+  // chunk ci into stage ci % NSTAGE.  Piece i of each operand goes to wave
+  // i % NW, so every wave issues the same number of pieces of each kind (a
+  // wave without a V piece reloads row 0 into the spare area).  Addresses
   // are a per-chunk base (uniform) plus a 32-bit per-lane offset; rows past
   // the end of the sequence read row nrow - 1 (finite data; the chunk
   // transform zeroes their contribution).
-  static_assert(NIK % NW == 0 && NIT % NW == 0 && NIV % NW == 0, "piece split");
+  static_assert(NIK % NW == 0 && NIT % NW == 0, "piece split");
   auto issue = [&](int ci) {
     char* sb = smem + (ci % NSTAGE) * SB;
     const int r0 = ci * C, nrow = min(C, a.T - r0);
@@ -435,41 +443,54 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
       __builtin_amdgcn_global_load_lds((const void*)(tb + off), (lds_void*)(sb + KB + ins * 1024), 16, 0, 0);
     }
 #pragma unroll
-    for (int it = 0; it < NIV / NW; ++it) {
+    for (int it = 0; it < NIVW; ++it) {
       constexpr int CPR = BVS / 8;
       const int ins = it * NW + w, row = ins * (64 / CPR) + l / CPR;
-      const int off = min(row, nrow - 1) * hv + 8 * (l % CPR);
-      __builtin_amdgcn_global_load_lds((const void*)(vb + off), (lds_void*)(sb + KB + TB + ins * 1024), 16, 0, 0);
+      if (NIV % NW == 0 || ins < NIV) {
+        const int off = min(row, nrow - 1) * hv + 8 * (l % CPR);
+        __builtin_amdgcn_global_load_lds((const void*)(vb + off), (lds_void*)(sb + KB + TB + ins * 1024), 16, 0, 0);
+      } else {
+        __builtin_amdgcn_global_load_lds((const void*)(vb + 8 * (l % CPR)), (lds_void*)sDummy, 16, 0, 0);
+      }
     }
     // the coefficient rows (one piece; the other waves load it into a spare area)
     __builtin_amdgcn_global_load_lds((const void*)(a.gam + (((size_t)bh * N + ci) * 5 + 1) * C + 4 * l),
                                      (lds_void*)(w == 0 ? sb + KB + TB + VB : sDummy), 16, 0, 0);
   };
   // wait until chunk ci has landed: the pieces and stores issued after its own
-  // may stay in flight (stores of chunk ci - 2, pieces of ci + 1, stores of ci - 1)
+  // may stay in flight (three stages: stores of chunk ci - 2, pieces of
+  // ci + 1, stores of ci - 1; two stages: stores of ci - 1)
   auto wait_chunk = [&](int ci) {
-    const bool more = ci + 1 < N;
-    if (ci >= 2) {
-      if (more) wait_vm<2 * NSW + NIW>();
-      else wait_vm<2 * NSW>();
-    } else if (ci == 1) {
-      if (more) wait_vm<NSW + NIW>();
-      else wait_vm<NSW>();
+    if constexpr (NSTAGE == 3) {
+      const bool more = ci + 1 < N;
+      if (ci >= 2) {
+        if (more) wait_vm<2 * NSW + NIW>();
+        else wait_vm<2 * NSW>();
+      } else if (ci == 1) {
+        if (more) wait_vm<NSW + NIW>();
+        else wait_vm<NSW>();
+      } else {
+        if (more) wait_vm<NIW>();
+        else wait_vm<0>();
+      }
     } else {
-      if (more) wait_vm<NIW>();
+      if (ci >= 1) wait_vm<NSW>();
       else wait_vm<0>();
     }
   };
 
-  if (N > 0) issue(0);
-  if (N > 1) issue(1);
+#pragma unroll
+  for (int s = 0; s < NSTAGE - 1; ++s)
+    if (s < N) issue(s);
 
-  // S^T[c][v], c = c0 + 16 tc + 4 g4 + r
+  // S^T[c][v] in pair order: c = c0 + pair_feat(tc, g4) + r, so that the
+  // packed operand of tiles 2m, 2m + 1 holds 8 consecutive features per lane
+  // group (the states are stored so, and K is read with plain 16-byte reads)
   f32x4 S[NCT];
 #pragma unroll
   for (int tc = 0; tc < NCT; ++tc) {
     if (a.S0)
-      S[tc] = *reinterpret_cast<const f32x4*>(a.S0 + ((size_t)bh * a.dv + v) * DK + c0 + 16 * tc + 4 * g4);
+      S[tc] = *reinterpret_cast<const f32x4*>(a.S0 + ((size_t)bh * a.dv + v) * DK + c0 + pair_feat(tc, g4));
     else
       S[tc] = zero4();
   }
@@ -485,22 +506,20 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
     const T* Vb = reinterpret_cast<const T*>(sb + KB + TB);
     const float* Fb = reinterpret_cast<const float*>(sb + KB + TB + VB);
     wait_chunk(ci);
-    lds_barrier();  // chunk ci visible; stage (ci + 2) % 3 and the exchange area released
-    if (ci + 2 < N) issue(ci + 2);
+    lds_barrier();  // chunk ci visible; stage (ci - 1) % NSTAGE and the exchange area released
+    if (ci + NSTAGE - 1 < N) issue(ci + NSTAGE - 1);
 
     // P = K S_r^T over this wave's features: K rows 16 J + c16, features in
-    // accumulator-pair order (pieces (c0 + 32 m) / 8 + g4 / 2 and + 2)
+    // natural order (piece (c0 + 32 m) / 8 + g4, one 16-byte read)
     Frag<T> sf[NKH];
 #pragma unroll
     for (int m = 0; m < NKH; ++m) sf[m] = acc_pair_frag<T>(S[2 * m], S[2 * m + 1]);
-    const int ks = kswz(c16), kb8 = (g4 & 1) * 8;
+    const int ks = kswz(c16);
     auto kfrag = [&](int J, int m) {
-      const char* row = Kb + (16 * J + c16) * RB + kb8;
-      const int p0 = (c0 + 32 * m) / 8 + (g4 >> 1);
-      const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row + 16 * (p0 ^ ks));
-      const bf16x4 hi = *reinterpret_cast<const bf16x4*>(row + 16 * ((p0 + 2) ^ ks));
+      const char* row = Kb + (16 * J + c16) * RB;
+      const int p0 = (c0 + 32 * m) / 8 + g4;
       Frag<T> f;
-      f.v = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      f.v = *reinterpret_cast<const bf16x8*>(row + 16 * (p0 ^ ks));
       return f;
     };
     // the V slice, transposed (issued now, waited for where used)
@@ -571,17 +590,18 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
         R[J] = sum;
       }
     }
-    // K^T of this wave's features for the update (rows 4 g4 + j / 4 (+ 16) of
-    // each 32-token half, pieces (c0 + 16 t) / 8 + (j % 4) / 2), issued now so
-    // that they arrive while R and U are formed
+    // K^T of this wave's features for the update, in the pair order of the
+    // state tiles (rows 4 g4 + j / 4 (+ 16) of each 32-token half, features
+    // c0 + pair_feat(t, j % 4): piece (c0 + 32 (t / 2)) / 8 + j % 4, half t % 2),
+    // issued now so that they arrive while R and U are formed
     Frag<T> tf[NCT][2];
     {
-      const int j = c16, rr = 4 * g4 + (j >> 2), rs = kswz(rr), hb = (j & 1) * 8;
+      const int j = c16, rr = 4 * g4 + (j >> 2), rs = kswz(rr);
 #pragma unroll
       for (int t = 0; t < NCT; ++t)
 #pragma unroll
         for (int kq = 0; kq < 2; ++kq) {
-          const int p = (c0 + 16 * t) / 8 + ((j & 3) >> 1);
+          const int p = (c0 + 32 * (t >> 1)) / 8 + (j & 3), hb = (t & 1) * 8;
           const char* pl = Kb + (32 * kq + rr) * RB + 16 * (p ^ rs) + hb;
           const bf16x4 lo = ds_read_tr16_asm(pl);
           const bf16x4 hi = ds_read_tr16_asm(pl + 16 * RB);
@@ -633,8 +653,13 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
       if constexpr (NH == 1) {
         store_frag(u_out, uf[0]);
         store_frag(u_out + 16 * 32, uf[1]);
-      } else {
+      } else if constexpr (NH == 2) {
         store_frag(u_out + 16 * 32 * hq, hq == 0 ? uf[0] : uf[1]);
+      } else {
+        // four waves: one 8-byte half of one fragment each
+        const bf16x8 x = (hq >> 1) == 0 ? uf[0].v : uf[1].v;
+        const bf16x4 y = (hq & 1) == 0 ? bf16x4{x[0], x[1], x[2], x[3]} : bf16x4{x[4], x[5], x[6], x[7]};
+        *reinterpret_cast<bf16x4*>(u_out + 16 * 32 * (hq >> 1) + 4 * (hq & 1)) = y;
       }
     }
   }
@@ -643,7 +668,7 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
     wait_vm<0>();
 #pragma unroll
     for (int tc = 0; tc < NCT; ++tc)
-      *reinterpret_cast<f32x4*>(a.ST + ((size_t)bh * a.dv + v) * DK + c0 + 16 * tc + 4 * g4) = S[tc];
+      *reinterpret_cast<f32x4*>(a.ST + ((size_t)bh * a.dv + v) * DK + c0 + pair_feat(tc, g4)) = S[tc];
   }
 }
 
@@ -738,7 +763,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
     for (int vt = 0; vt < VPW; ++vt) acc[vt] = zero4();
 #pragma unroll
     for (int m = 0; m < NK; ++m) {
-      const Frag<T> qf = ld_frag_acc(sQ + 16 * I * LDQ + 32 * m, (size_t)LDQ);
+      const Frag<T> qf = ld_frag(sQ + 16 * I * LDQ + 32 * m, LDQ);
 #pragma unroll
       for (int vt = 0; vt < VPW; ++vt) mma(acc[vt], sfr[vt][m], qf);
     }
@@ -778,11 +803,18 @@ hipError_t run_gdn_state_v(const GdnArgs& a, hipStream_t st) {
 // Split the key features over as many waves (1, 2, 4 or 8, at least 32
 // features each) as it takes to give every SIMD of the chip a wave, with four
 // waves per workgroup where the split allows.
+// LDS of the streamed kernel with a ring of `ns` stages
+constexpr size_t gdn_dma_lds(int dk, int npr, int nh, int ns) {
+  return (size_t)ns * (kChunk * dk * 2 + kChunk * kChunk * 2 + kChunk * 16 * npr * 2 + 4 * kChunk * 4) +
+         (nh > 1 ? (size_t)npr * nh * 4 * 64 * 16 : 16) + 1024;
+}
 template <int DK, int NPR, int NH>
 hipError_t run_gdn_state_dma(const GdnArgs& a, hipStream_t st) {
   const int nblk = a.B * a.H * (a.dv / (16 * NPR));
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((gdn_state_dma_kernel<DK, NPR, NH>), dim3(nblk), dim3(64 * NPR * NH), 0, st, a);
+  // three stages where they fit in the compute unit's 160 KB of LDS
+  constexpr int NS = gdn_dma_lds(DK, NPR, NH, 3) <= 160 * 1024 ? 3 : 2;
+  hipLaunchKernelGGL((gdn_state_dma_kernel<DK, NPR, NH, NS>), dim3(nblk), dim3(64 * NPR * NH), 0, st, a);
   return hipGetLastError();
 }
 template <typename T, int DK>
@@ -790,7 +822,7 @@ hipError_t run_gdn_state(const GdnArgs& a, hipStream_t st) {
   const long long slices = (long long)a.B * a.H * (a.dv / 16);
   constexpr int kSimds = 1024;
   if constexpr (sizeof(T) == 2 && (DK == 128 || DK == 256)) {
-    if (slices * 2 >= kSimds && a.dv % 32 == 0) return run_gdn_state_dma<DK, 2, 2>(a, st);
+    if (slices * 2 >= kSimds && a.dv % 32 == 0) return run_gdn_state_dma<DK, 2, 4>(a, st);
   }
   if (slices >= kSimds || DK < 64) return run_gdn_state_v<T, DK, 4, 1>(a, st);
   if (slices * 2 >= kSimds || DK < 128) return run_gdn_state_v<T, DK, 2, 2>(a, st);

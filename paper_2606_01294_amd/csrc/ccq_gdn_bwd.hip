@@ -390,19 +390,15 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
         }
       }
       // S_r and U^T slices (fragment-native: per value tile and 32-wide k
-      // block, 16 rows of 32 in acc_pos order) and D (plain rows)
+      // block, 16 rows of 32; S_r rows in natural order, U^T rows in acc_pos
+      // order) and D (plain rows)
 #pragma unroll
       for (int p = 0; p < NPS; ++p) {
         const int q = tid + p * kThreads;
         const int vt = q / (2 * DK), rem = q % (2 * DK);
         const int m = rem / 64, vr = (rem % 64) / 4, pp = rem % 4;
         const int vl = 16 * vt + vr;
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {  // logical columns 4pp.. and 16 + 4pp..
-          T* dst4 = sS + vl * LDQ + 32 * m + 16 * hh + 4 * pp;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) dst4[e] = cur.s[p][4 * hh + e];
-        }
+        *reinterpret_cast<v8*>(sS + vl * LDQ + 32 * m + 8 * pp) = cur.s[p];
         const int vd = q / (DK / 8), cd = (q % (DK / 8)) * 8;
         *reinterpret_cast<v8*>(sD + vd * LDQ + cd) = cur.d[p];
       }
