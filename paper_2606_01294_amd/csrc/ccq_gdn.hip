@@ -235,8 +235,9 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
   Frag<T> sf[NKH], uf[2];
   auto write_back = [&](int cw) {
     T* st_out = st_base + ((size_t)bh * N + cw) * a.dv * DK;
+    if (cw % a.sstride == 0)
 #pragma unroll
-    for (int m = 0; m < NKH; ++m) store_frag(st_out + 16 * 32 * m, sf[m]);
+      for (int m = 0; m < NKH; ++m) store_frag(st_out + 16 * 32 * m, sf[m]);
     if (hq == 0) {
       T* u_out = u_base + ((size_t)bh * N + cw) * a.dv * C;
       store_frag(u_out, uf[0]);
@@ -377,6 +378,25 @@ template <int X>
 __device__ __forceinline__ void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(X) : "memory");
 }
+// s_waitcnt vmcnt(n) for a wave-uniform n in 0..47 (the counter field is an
+// immediate: one scalar branch to the matching wait)
+__device__ __forceinline__ void wait_vm_n(int n) {
+  switch (n) {
+#define CCQ_WAIT_CASE(i) \
+  case i:                \
+    wait_vm<i>();        \
+    break;
+#define CCQ_WAIT_CASE8(i) \
+  CCQ_WAIT_CASE(i) CCQ_WAIT_CASE(i + 1) CCQ_WAIT_CASE(i + 2) CCQ_WAIT_CASE(i + 3) CCQ_WAIT_CASE(i + 4) \
+  CCQ_WAIT_CASE(i + 5) CCQ_WAIT_CASE(i + 6) CCQ_WAIT_CASE(i + 7)
+    CCQ_WAIT_CASE8(0) CCQ_WAIT_CASE8(8) CCQ_WAIT_CASE8(16) CCQ_WAIT_CASE8(24) CCQ_WAIT_CASE8(32) CCQ_WAIT_CASE8(40)
+#undef CCQ_WAIT_CASE8
+#undef CCQ_WAIT_CASE
+    default:
+      wait_vm<0>();
+      break;
+  }
+}
 
 template <int DK, int NPR, int NH, int NSTAGE>
 __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const GdnArgs a) {
@@ -391,7 +411,7 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
   constexpr int NIW = NIK / NW + NIT / NW + NIVW + 1;         // 1 KB pieces per wave and chunk
   constexpr int SB = KB + TB + VB + FB;
   constexpr int XB = NH > 1 ? NW * 4 * 64 * 16 : 16;
-  constexpr int NSW = NKH + (NH == 1 ? 2 : 1);                // stores per wave per chunk
+  constexpr int NSU = NH == 1 ? 2 : 1;                         // U^T stores per wave per chunk
   static_assert(DK == 128 || DK == 256, "key width");
   static_assert(NH == 1 || NH == 2 || NH == 4, "key split");
   static_assert(NSTAGE == 2 || NSTAGE == 3, "ring depth");
@@ -457,26 +477,15 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
     __builtin_amdgcn_global_load_lds((const void*)(a.gam + (((size_t)bh * N + ci) * 5 + 1) * C + 4 * l),
                                      (lds_void*)(w == 0 ? sb + KB + TB + VB : sDummy), 16, 0, 0);
   };
+  // stores per wave of chunk c: S_r (every sstride-th chunk) and U^T
+  auto nstore = [&](int c) { return (c % a.sstride == 0 ? NKH : 0) + NSU; };
   // wait until chunk ci has landed: the pieces and stores issued after its own
   // may stay in flight (three stages: stores of chunk ci - 2, pieces of
   // ci + 1, stores of ci - 1; two stages: stores of ci - 1)
   auto wait_chunk = [&](int ci) {
-    if constexpr (NSTAGE == 3) {
-      const bool more = ci + 1 < N;
-      if (ci >= 2) {
-        if (more) wait_vm<2 * NSW + NIW>();
-        else wait_vm<2 * NSW>();
-      } else if (ci == 1) {
-        if (more) wait_vm<NSW + NIW>();
-        else wait_vm<NSW>();
-      } else {
-        if (more) wait_vm<NIW>();
-        else wait_vm<0>();
-      }
-    } else {
-      if (ci >= 1) wait_vm<NSW>();
-      else wait_vm<0>();
-    }
+    int n = ci >= 1 ? nstore(ci - 1) : 0;
+    if constexpr (NSTAGE == 3) n += (ci >= 2 ? nstore(ci - 2) : 0) + (ci + 1 < N ? NIW : 0);
+    wait_vm_n(n);
   };
 
 #pragma unroll
@@ -647,8 +656,9 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
     // S_r and U^T of this chunk, fragment-native (1 KB per value tile and k step)
     {
       T* st_out = st_base + ((size_t)bh * N + ci) * a.dv * DK;
+      if (ci % a.sstride == 0)
 #pragma unroll
-      for (int m = 0; m < NKH; ++m) store_frag(st_out + 16 * 32 * m, sf[m]);
+        for (int m = 0; m < NKH; ++m) store_frag(st_out + 16 * 32 * m, sf[m]);
       T* u_out = u_base + ((size_t)bh * N + ci) * a.dv * C;
       if constexpr (NH == 1) {
         store_frag(u_out, uf[0]);
@@ -672,12 +682,21 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
   }
 }
 
-// Outputs of one chunk (eight waves).  The decayed, masked scores
+// Outputs of a group of consecutive chunks (eight waves).  Per chunk the
+// decayed, masked scores
 //   P_ij = e^{gamma_i - gamma_j} (q_i . k_j)  (j <= i)
 // are formed once (ten nonzero 16 x 16 tiles over the waves) and kept in LDS;
 // wave w then owns VPW value tiles for IPW token tiles and forms, transposed,
 //   O^T = e^{gamma_i} (S_r Q^T) + U^T P^T,
-// with rows of S_r and U^T read straight from global memory as MFMA operands.
+// with rows of U^T read straight from global memory as MFMA operands.  S_r
+// of the group's first chunk is read the same way; for the later chunks each
+// wave carries its rows of S forward itself,
+//   S_{r+1} = e^{gamma_C} S_r + U^T diag(e^{gamma_C - gamma}) K,
+// so the state pass stores one state per group.  S is held as bf16 operand
+// fragments in natural feature order; a fragment's 8 elements are exactly
+// the lane's entries of two pair-ordered accumulator tiles (tiles 2m, 2m + 1
+// of ld_frag_tr_acc_pair), so the update unpacks, accumulates and repacks in
+// place.
 template <typename T, int DK, int VPW, int IPW>
 __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArgs a) {
   constexpr int C = kChunk;
@@ -692,95 +711,159 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
   __shared__ __align__(16) T sK[C * LDQ];
   __shared__ __align__(16) T sP[C * LDP];  // P[i][acc_pos(j)]
   __shared__ __align__(16) float sGam[C];
+  __shared__ __align__(16) float sDd[C + 4];  // e^{gamma_C - gamma_j}; e^{gamma_C} at C
 
   const int N = (a.T + C - 1) / C;
+  const int R = a.group, NGR = (N + R - 1) / R;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int bh = lb / N, ci = lb % N;
+  const int bh = lb / NGR, cb = (lb % NGR) * R, ce = min(N, cb + R);
   const int b = bh / a.H, h = bh % a.H;
-  const int r0 = ci * C;
-  const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
   const int tid = threadIdx.x, w = tid >> 6, l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
   const int vg = w % NVG, ig = w / NVG;
   const size_t gstride = (size_t)a.H * DK;
-
-  {
-    RowTile<T, DK, kOutThreads> rq, rk;
-    rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-    rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-    if (tid < C) sGam[tid] = a.gam[((size_t)bh * N + ci) * 5 * C + tid];
-    rq.store(sQ, LDQ);
-    rk.store(sK, LDQ);
-  }
-  __syncthreads();
-
-  // this wave's S_r and U^T fragments (fragment-native, 1 KB each), issued
-  // after the staging of q and k so that the two sets of registers are not
-  // live at once (two workgroups fit on a compute unit); they arrive while the
-  // score tiles are formed
-  const T* Sg = static_cast<const T*>(a.states) + ((size_t)bh * N + ci) * a.dv * DK;
-  const T* Ug = static_cast<const T*>(a.U) + ((size_t)bh * N + ci) * a.dv * C;
-  Frag<T> sfr[VPW][NK], ufr[VPW][2];
-#pragma unroll
-  for (int vt = 0; vt < VPW; ++vt) {
-    const int vtile = vg * VPW + vt;
-#pragma unroll
-    for (int m = 0; m < NK; ++m) sfr[vt][m] = ld_frag_global(Sg + ((size_t)vtile * NK + m) * 16 * 32, 32);
-#pragma unroll
-    for (int m = 0; m < 2; ++m) ufr[vt][m] = ld_frag_global(Ug + ((size_t)vtile * 2 + m) * 16 * 32, 32);
-  }
-
-  // P tiles: ten lower tiles (I >= J) over the waves, the six upper ones zero;
-  // computed transposed (row j, column i) and stored as rows i
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const int t = w + 8 * s;
-    const int I = intra_tile_row(t), J = intra_tile_col(t);
-    const int i = 16 * I + c16;
-    float x[4] = {0.f, 0.f, 0.f, 0.f};
-    if (t < 10) {
-      f32x4 sc = zero4();
-      tile_mma<T, DK>(sc, sK + 16 * J * LDQ, LDQ, sQ + 16 * I * LDQ, LDQ);
-      const float gi = sGam[i];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int j = 16 * J + 4 * g4 + r;
-        x[r] = j <= i ? sc[r] * __expf(gi - sGam[j]) : 0.f;
-      }
-    }
-    store4(sP + i * LDP + acc_pos(16 * J + 4 * g4), x[0], x[1], x[2], x[3]);
-  }
-  __syncthreads();
-
   T* o = static_cast<T*>(a.o);
-#pragma unroll
-  for (int it = 0; it < IPW; ++it) {
-    const int I = ig * IPW + it;
-    const int i = 16 * I + c16;
-    // S_r Q^T one k step at a time (one q fragment live), both value tiles
-    f32x4 acc[VPW];
-#pragma unroll
-    for (int vt = 0; vt < VPW; ++vt) acc[vt] = zero4();
-#pragma unroll
-    for (int m = 0; m < NK; ++m) {
-      const Frag<T> qf = ld_frag(sQ + 16 * I * LDQ + 32 * m, LDQ);
-#pragma unroll
-      for (int vt = 0; vt < VPW; ++vt) mma(acc[vt], sfr[vt][m], qf);
+
+  Frag<T> sfr[VPW][NK];
+  for (int ci = cb; ci < ce; ++ci) {
+    const int r0 = ci * C;
+    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+    const bool carry = ci + 1 < ce;
+    {
+      RowTile<T, DK, kOutThreads> rq, rk;
+      rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+      rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+      const float* gm = a.gam + ((size_t)bh * N + ci) * 5 * C;
+      if (tid < C) sGam[tid] = gm[tid];
+      if (carry && tid < C + 1) sDd[tid] = tid < C ? gm[3 * C + tid] : gm[4 * C];
+      rq.store(sQ, LDQ);
+      rk.store(sK, LDQ);
     }
-    const Frag<T> pf0 = ld_frag(sP + 16 * I * LDP, LDP);
-    const Frag<T> pf1 = ld_frag(sP + 16 * I * LDP + 32, LDP);
-    const float ei = __expf(sGam[i]);
+    __syncthreads();
+
+    // this wave's S_r (first chunk of the group) and U^T fragments
+    // (fragment-native, 1 KB each), issued after the staging of q and k so
+    // that they arrive while the score tiles are formed
+    if (ci == cb) {
+      const T* Sg = static_cast<const T*>(a.states) + ((size_t)bh * N + ci) * a.dv * DK;
 #pragma unroll
-    for (int vt = 0; vt < VPW; ++vt) {
-      acc[vt] *= ei;
-      mma(acc[vt], ufr[vt][0], pf0);
-      if (I >= 2) mma(acc[vt], ufr[vt][1], pf1);  // keys 32..63 precede row i only for I >= 2
-      if (i < nrow) {
-        const int vcol = 16 * (vg * VPW + vt) + 4 * g4;
-        store4(o + tok_off(b, r0 + i, h, a.T, a.H, a.dv) + vcol, a.scale * acc[vt][0], a.scale * acc[vt][1],
-               a.scale * acc[vt][2], a.scale * acc[vt][3]);
+      for (int vt = 0; vt < VPW; ++vt)
+#pragma unroll
+        for (int m = 0; m < NK; ++m)
+          sfr[vt][m] = ld_frag_global(Sg + ((size_t)(vg * VPW + vt) * NK + m) * 16 * 32, 32);
+    }
+    const T* Ug = static_cast<const T*>(a.U) + ((size_t)bh * N + ci) * a.dv * C;
+    Frag<T> ufr[VPW][2];
+#pragma unroll
+    for (int vt = 0; vt < VPW; ++vt)
+#pragma unroll
+      for (int m = 0; m < 2; ++m) ufr[vt][m] = ld_frag_global(Ug + ((size_t)(vg * VPW + vt) * 2 + m) * 16 * 32, 32);
+
+    // P tiles: ten lower tiles (I >= J) over the waves, the six upper ones zero;
+    // computed transposed (row j, column i) and stored as rows i
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int t = w + 8 * s;
+      const int I = intra_tile_row(t), J = intra_tile_col(t);
+      const int i = 16 * I + c16;
+      float x[4] = {0.f, 0.f, 0.f, 0.f};
+      if (t < 10) {
+        f32x4 sc = zero4();
+        tile_mma<T, DK>(sc, sK + 16 * J * LDQ, LDQ, sQ + 16 * I * LDQ, LDQ);
+        const float gi = sGam[i];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int j = 16 * J + 4 * g4 + r;
+          x[r] = j <= i ? sc[r] * __expf(gi - sGam[j]) : 0.f;
+        }
+      }
+      store4(sP + i * LDP + acc_pos(16 * J + 4 * g4), x[0], x[1], x[2], x[3]);
+    }
+    __syncthreads();
+
+#pragma unroll
+    for (int it = 0; it < IPW; ++it) {
+      const int I = ig * IPW + it;
+      const int i = 16 * I + c16;
+      // S_r Q^T one k step at a time (one q fragment live), all value tiles
+      f32x4 acc[VPW];
+#pragma unroll
+      for (int vt = 0; vt < VPW; ++vt) acc[vt] = zero4();
+#pragma unroll
+      for (int m = 0; m < NK; ++m) {
+        const Frag<T> qf = ld_frag(sQ + 16 * I * LDQ + 32 * m, LDQ);
+#pragma unroll
+        for (int vt = 0; vt < VPW; ++vt) mma(acc[vt], sfr[vt][m], qf);
+      }
+      const Frag<T> pf0 = ld_frag(sP + 16 * I * LDP, LDP);
+      const Frag<T> pf1 = ld_frag(sP + 16 * I * LDP + 32, LDP);
+      const float ei = __expf(sGam[i]);
+#pragma unroll
+      for (int vt = 0; vt < VPW; ++vt) {
+        acc[vt] *= ei;
+        mma(acc[vt], ufr[vt][0], pf0);
+        if (I >= 2) mma(acc[vt], ufr[vt][1], pf1);  // keys 32..63 precede row i only for I >= 2
+        if (i < nrow) {
+          const int vcol = 16 * (vg * VPW + vt) + 4 * g4;
+          store4(o + tok_off(b, r0 + i, h, a.T, a.H, a.dv) + vcol, a.scale * acc[vt][0], a.scale * acc[vt][1],
+                 a.scale * acc[vt][2], a.scale * acc[vt][3]);
+        }
       }
     }
+
+    if (carry) {
+      // S_{r+1}^T = e^{gamma_C} S_r^T + K^T (diag(e^{gamma_C - gamma}) U): the
+      // U^T fragments scaled per token (k slot 8 g4 + e is token 32 m + 4 g4 + e,
+      // or + 16 for e >= 4), then per 32-feature block m the two pair-ordered
+      // tiles of every value tile
+      const float eC = sDd[C];
+      Frag<T> ud[VPW][2];
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        const f32x4 d0 = *reinterpret_cast<const f32x4*>(sDd + 32 * m + 4 * g4);
+        const f32x4 d1 = *reinterpret_cast<const f32x4*>(sDd + 32 * m + 16 + 4 * g4);
+#pragma unroll
+        for (int vt = 0; vt < VPW; ++vt) {
+          f32x4 x, y;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            x[r] = frag_elem(ufr[vt][m], r) * d0[r];
+            y[r] = frag_elem(ufr[vt][m], 4 + r) * d1[r];
+          }
+          ud[vt][m] = acc_pair_frag<T>(x, y);
+        }
+      }
+      // K^T fragments of block m + 1 are read while block m is updated (the
+      // scheduling barrier keeps later blocks' reads from being hoisted)
+      Frag<T> tf[2][2][2];
+      auto load_tf = [&](Frag<T>(&f)[2][2], int m) {
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+          for (int kq = 0; kq < 2; ++kq) f[hh][kq] = ld_frag_tr_acc_pair(sK + 32 * kq * LDQ, LDQ, 2 * m + hh);
+      };
+      load_tf(tf[0], 0);
+#pragma unroll
+      for (int m = 0; m < NK; ++m) {
+        if (m + 1 < NK) load_tf(tf[(m + 1) & 1], m + 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int vt = 0; vt < VPW; ++vt) {
+          f32x4 x, y;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            x[r] = eC * frag_elem(sfr[vt][m], r);
+            y[r] = eC * frag_elem(sfr[vt][m], 4 + r);
+          }
+          mma(x, tf[m & 1][0][0], ud[vt][0]);
+          mma(x, tf[m & 1][0][1], ud[vt][1]);
+          mma(y, tf[m & 1][1][0], ud[vt][0]);
+          mma(y, tf[m & 1][1][1], ud[vt][1]);
+          sfr[vt][m] = acc_pair_frag<T>(x, y);
+        }
+      }
+    }
+    __syncthreads();  // q, k, P and the coefficients of this chunk released
   }
 }
 
@@ -834,7 +917,9 @@ hipError_t run_gdn_state(const GdnArgs& a, hipStream_t st) {
 }
 template <typename T, int DK, int VPW, int IPW>
 hipError_t run_gdn_out_v(const GdnOutArgs& a, hipStream_t st) {
-  const int nblk = a.B * a.H * ((a.T + kChunk - 1) / kChunk);
+  if (a.group < 1) return hipErrorInvalidValue;
+  const int N = (a.T + kChunk - 1) / kChunk;
+  const int nblk = a.B * a.H * ((N + a.group - 1) / a.group);
   if (nblk == 0) return hipSuccess;
   hipLaunchKernelGGL((gdn_out_kernel<T, DK, VPW, IPW>), dim3(nblk), dim3(kOutThreads), 0, st, a);
   return hipGetLastError();
@@ -850,6 +935,16 @@ hipError_t run_gdn_out(const GdnOutArgs& a, hipStream_t st) {
   return hipErrorInvalidValue;
 }
 }  // namespace
+
+int gdn_out_group(int B, int H, int T) {
+  // the largest group (4 or 2 chunks) that still gives two workgroups per
+  // compute unit
+  const long long bh = (long long)B * H;
+  const int N = (T + kChunk - 1) / kChunk;
+  for (int g = 4; g >= 2; g /= 2)
+    if (bh * ((N + g - 1) / g) >= 512) return g;
+  return 1;
+}
 
 bool gdn_supported(int dk, int dv, bool is_bf16) {
   const bool dv_ok = dv == 64 || dv == 128 || dv == 256 || dv == 512;

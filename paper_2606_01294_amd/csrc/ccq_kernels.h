@@ -118,13 +118,17 @@ struct GdnArgs {
   const float* gam;      // workspace, as TriArgs
   const float* S0;       // [B,H,dv,dk] or null
   float* ST;             // [B,H,dv,dk] or null
-  void* states;          // [B*H, N, dv/16, dk/32, 16, 32] io (workspace): S_r, rows
-                         // in acc_pos order (fragment-native)
-  void* U;               // [B*H, N, dv/16, 2, 16, 32] io (workspace): U^T, likewise
+  void* states;          // [B*H, N, dv/16, dk/32, 16, 32] io (workspace): S_r
+                         // (fragment-native, rows in natural feature order),
+                         // stored for chunks r with r % sstride == 0
+  void* U;               // [B*H, N, dv/16, 2, 16, 32] io (workspace): U^T, rows in
+                         // acc_pos order (fragment-native), every chunk
   int B, T, H, dk, dv;
+  int sstride = 1;
 };
 
-// Gated DeltaNet output, one workgroup per chunk.
+// Gated DeltaNet output, one workgroup per group of `group` chunks (the
+// state pass stored S_r for the first chunk of every group: sstride = group).
 struct GdnOutArgs {
   const void* qc;        // [B,T,H,dk] io (cleaned queries)
   const void* k;         // [B,T,H,dk] io
@@ -134,6 +138,7 @@ struct GdnOutArgs {
   void* o;               // [B,T,H,dv] io
   int B, T, H, dk, dv;
   float scale;
+  int group = 1;
 };
 
 // ---- training step (CCQ-GLA backward) ----
@@ -318,5 +323,7 @@ bool prep_supported(int H, int dk);
 bool clean_supported(int dk, bool is_bf16);
 bool gla_supported(int dk, int dv, bool is_bf16);
 bool gdn_supported(int dk, int dv, bool is_bf16);
+// Chunks per output workgroup (and state stride) for a forward pass.
+int gdn_out_group(int B, int H, int T);
 
 }  // namespace ccq

@@ -119,6 +119,27 @@ def test_gdn_parity_state_splits(case):
     compare(GDN, d, dtype)
 
 
+# With enough (batch, head) pairs the Gated DeltaNet output kernel takes
+# groups of 4 or 2 chunks per workgroup, carrying S from one stored state
+# through the group; these shapes reach both group sizes with a partial last
+# group and a ragged last chunk.
+GDN_GROUP_CASES = [
+    # dtype, B, T, H, dk, dv -> chunks, group
+    (BF16, 16, 337, 16, 64, 64),   # 6 chunks, groups of 4: {0..3}, {4, 5}
+    (BF16, 16, 150, 16, 64, 128),  # 3 chunks, groups of 2: {0, 1}, {2}
+    (F32, 16, 337, 16, 64, 64),
+]
+
+
+@pytest.mark.parametrize("case", GDN_GROUP_CASES, ids=lambda c: "%s-B%dT%dH%d-dk%d-dv%d" % (
+    str(c[0]).split(".")[-1], c[1], c[2], c[3], c[4], c[5]))
+def test_gdn_parity_output_groups(case):
+    dtype, B, T, H, dk, dv = case
+    say("gdn groups", case)
+    d = make_inputs(GDN, B, T, H, dk, dv, dtype, seed=400 + T + dv, keys="aniso", lam="random")
+    compare(GDN, d, dtype)
+
+
 @pytest.mark.parametrize("backbone", [GLA, GDN])
 @pytest.mark.parametrize("dtype", [F32, BF16])
 def test_uncentred_scaled_with_initial_states(backbone, dtype):
