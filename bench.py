@@ -52,6 +52,18 @@ def clean_seg(bh: int, nc: int) -> int:
     return seg
 
 
+def gdn_group(w) -> int:
+    """Chunks per Gated DeltaNet output workgroup (one stored state per group):
+    the largest of 4, 2 that still gives 512 workgroups; 1 for training."""
+    if getattr(w, "train", False):
+        return 1
+    nc = -(-w.T // CHUNK)
+    for g in (4, 2):
+        if w.B * w.H * -(-nc // g) >= 512:
+            return g
+    return 1
+
+
 def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     """Algorithmic (bytes, flops) of one launch of `kernel` on workload w: every
     input read once, every output written once; products counted at 2 flops per
@@ -93,13 +105,16 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     elif kernel == "gdn_tri":       # k, log alpha, beta in; chunk transforms Tm and decays out
         by = ntok * (dk * io_bytes + 8 + C * io_bytes + 4)
         fl = ntok * (2 * C * dk)
-    elif kernel == "gdn_state":     # k, v, Tm, decays, beta in; chunk states, U, final state out
-        by = ntok * (dk * io_bytes + dv * io_bytes + C * io_bytes + 8 + dv * dk * io_bytes // C
-                     + dv * io_bytes) + (0 if getattr(w, "train", False) else BH * dv * dk * 4)
+    elif kernel == "gdn_state":     # k, v, Tm, decays, beta in; group-entry states, U, final state out
+        G = gdn_group(w)
+        by = ntok * (dk * io_bytes + dv * io_bytes + C * io_bytes + 8 + dv * io_bytes) \
+            + BH * -(-NC // G) * dv * dk * io_bytes + (0 if getattr(w, "train", False) else BH * dv * dk * 4)
         fl = ntok * (4 * dk * dv + 2 * C * dv)
-    elif kernel == "gdn_out":       # q_clean, k, chunk states, U, decays in; o out
-        by = ntok * (2 * dk * io_bytes + dv * dk * io_bytes // C + 2 * dv * io_bytes + 4)
-        fl = ntok * (2 * C * dk + 2 * dk * dv + 2 * C * dv)
+    elif kernel == "gdn_out":       # q_clean, k, group-entry states, U, decays in; o out
+        G = gdn_group(w)
+        by = ntok * (2 * dk * io_bytes + 2 * dv * io_bytes + 4) + BH * -(-NC // G) * dv * dk * io_bytes
+        # plus the state carried through each group: S <- e^{gamma_C} S + U^T diag(.) K
+        fl = ntok * (2 * C * dk + 2 * dk * dv + 2 * C * dv) + BH * (NC - -(-NC // G)) * 2 * C * dk * dv
     elif kernel == "gla_dstate":
         by = ntok * (dk * io_bytes + dk * gate_bytes + dv * io_bytes + dv * dk * io_bytes // C)
         fl = ntok * (2 * dk * dv)
