@@ -164,6 +164,48 @@ ccq_status ccq_prep(const ccq_shape* s, const void* q_raw, const void* k_raw, co
                     const float* b_lam, void* q, void* k, float* lam, void* stream);
 
 /*
+ * Packed batches of sequences of different lengths: Alg. 1 (and its
+ * training step) applied to every sequence on its own, each an independent
+ * recurrence with its own states, exactly as if each were a call of its own.
+ * Sequence b occupies rows cu_seqlens[b] .. cu_seqlens[b+1] - 1 of the packed
+ * tensors: q, k, dq, dk [rows,H,dk] and v, o, dO, dv [rows,H,dv] in io_dtype,
+ * the GLA gate g / dg [rows,H,dk] in gate_dtype, Gated DeltaNet log alpha,
+ * beta and their gradients [rows,H] fp32, lam / dlam [rows,H] fp32.
+ * cu_seqlens is a DEVICE array of B + 1 int32 (0 = cu[0] <= cu[1] <= ...);
+ * s->B is the number of sequences and s->T an upper bound on their lengths
+ * (a longer sequence is cut at T; the device offsets are not validated by
+ * the host: the packed tensors must hold cu[B] rows).  S0, C0, mu0, ST, CT,
+ * muT are per sequence, as in the padded calls; a sequence of length 0 with
+ * t0 = 0 returns its initial states (or zeros).  Internally the sequences are
+ * laid out as a padded [B,T,...] batch in the workspace (rows past a
+ * sequence's end are zero, which leaves every state unchanged and no output
+ * of the sequence's own rows), the padded path runs, and the results are
+ * copied back; the caches' running means are rescaled to each sequence's own
+ * token count.  q_clean export is not offered here.  The workspace holds
+ * ccq_varlen_workspace_size(s, bb, with_bwd) bytes (0: unsupported shape),
+ * which includes the padded copies.  Errors as for the padded entry points;
+ * B > 65535 is CCQ_ERR_UNSUPPORTED.
+ */
+size_t ccq_varlen_workspace_size(const ccq_shape* s, ccq_backbone bb, int with_bwd);
+ccq_status ccq_gla_fwd_varlen(const ccq_shape* s, const int32_t* cu_seqlens, const void* q,
+                              const void* k, const void* v, const void* g, const float* lam,
+                              const float* S0, const float* C0, const float* mu0, void* o,
+                              float* ST, float* CT, float* muT, void* workspace, size_t ws_bytes,
+                              void* stream);
+ccq_status ccq_gdn_fwd_varlen(const ccq_shape* s, const int32_t* cu_seqlens, const void* q,
+                              const void* k, const void* v, const float* logalpha,
+                              const float* beta, const float* lam, const float* S0,
+                              const float* C0, const float* mu0, void* o, float* ST, float* CT,
+                              float* muT, void* workspace, size_t ws_bytes, void* stream);
+/* Training step on a packed batch (as ccq_fwd_bwd, t0 = 0). */
+ccq_status ccq_fwd_bwd_varlen(const ccq_shape* s, ccq_backbone bb, const int32_t* cu_seqlens,
+                              const void* q, const void* k, const void* v,
+                              const void* g_or_logalpha, const float* beta, const float* lam,
+                              const void* dO, void* o, void* dq, void* dk, void* dv,
+                              void* dg_or_dlogalpha, float* dbeta, float* dlam, void* workspace,
+                              size_t ws_bytes, void* stream);
+
+/*
  * Per-kernel timing hook (instrumentation for benchmarks and profilers, not
  * part of the method).  `events` points at n_events hipEvent_t handles created
  * by the caller (hipEventCreate).  Until the next ccq_trace_events call from

@@ -15,6 +15,9 @@ Functions (all arrays are numpy float64, row-major):
   gdn_fwd_bwd(...)  reverse pass of CCQ-Gated DeltaNet for L = sum <dO, o>
   prep(...)         per-head l2 normalisation of raw q, k and the gate
                     lambda = sigmoid(W qraw + b) from the query before the head split
+  varlen_fwd(...), varlen_fwd_bwd(...)
+                    packed batches: the per-sequence forward / reverse pass applied
+                    to each sequence of the batch on its own
 """
 from __future__ import annotations
 
@@ -196,3 +199,62 @@ def prep(q, k, W, b):
     if rc != 0:
         raise RuntimeError("ccq_oracle_prep failed with code %d" % rc)
     return dict(q=qb, k=kb, lam=lam)
+
+
+def _seq_slices(cu):
+    cu = [int(x) for x in np.asarray(cu).reshape(-1)]
+    return [(cu[b], cu[b + 1]) for b in range(len(cu) - 1)]
+
+
+def varlen_fwd(q, k, v, gate, lam, cu, beta=None, backbone=GLA, S0=None, C0=None, mu0=None,
+               scale=1.0, centered=True, t0=0):
+    """Forward of a packed batch: sequence b is rows cu[b]..cu[b+1]-1 of q, k
+    [rows,H,dk], v [rows,H,dv], gate, lam (and beta); each runs through fwd on its
+    own, from its own initial states.  Returns o [rows,H,dv] and the per-sequence
+    ST, CT, muT."""
+    q, k, v, gate, lam = _f64(q), _f64(k), _f64(v), _f64(gate), _f64(lam)
+    beta = _f64(beta) if backbone == GDN else None
+    rows, H, dk = q.shape
+    dv = v.shape[-1]
+    sl = _seq_slices(cu)
+    B = len(sl)
+    o = np.zeros((rows, H, dv))
+    ST, CT, muT = np.zeros((B, H, dv, dk)), np.zeros((B, H, dk, dk)), np.zeros((B, H, dk))
+    for b, (r0, r1) in enumerate(sl):
+        init = [None if x is None else _f64(x)[b:b + 1] for x in (S0, C0, mu0)]
+        if r1 == r0:
+            ST[b] = 0.0 if init[0] is None else init[0][0]
+            CT[b] = 0.0 if init[1] is None else init[1][0]
+            muT[b] = 0.0 if init[2] is None else init[2][0]
+            continue
+        r = fwd(q[None, r0:r1], k[None, r0:r1], v[None, r0:r1], gate[None, r0:r1], lam[None, r0:r1],
+                beta=None if beta is None else beta[None, r0:r1], backbone=backbone, S0=init[0],
+                C0=init[1], mu0=init[2], scale=scale, centered=centered, t0=t0)
+        o[r0:r1] = r["o"][0]
+        ST[b], CT[b], muT[b] = r["ST"][0], r["CT"][0], r["muT"][0]
+    return dict(o=o, ST=ST, CT=CT, muT=muT)
+
+
+def varlen_fwd_bwd(q, k, v, gate, lam, dO, cu, beta=None, backbone=GLA, scale=1.0, centered=True):
+    """Reverse pass of a packed batch (L = sum <dO, o>), each sequence on its own from
+    zero states.  Returns packed o, dq, dk, dv, dg, dlam (and dbeta for Gated DeltaNet)."""
+    arrs = {"q": _f64(q), "k": _f64(k), "v": _f64(v), "g": _f64(gate), "lam": _f64(lam),
+            "dO": _f64(dO)}
+    if backbone == GDN:
+        arrs["beta"] = _f64(beta)
+    keys = ("o", "dq", "dk", "dv", "dg", "dlam") + (("dbeta",) if backbone == GDN else ())
+    like = {"o": "dO", "dq": "q", "dk": "k", "dv": "v", "dg": "g", "dlam": "lam", "dbeta": "lam"}
+    out = {key: np.zeros_like(arrs[like[key]]) for key in keys}
+    for r0, r1 in _seq_slices(cu):
+        if r1 == r0:
+            continue
+        a = {n: x[None, r0:r1] for n, x in arrs.items()}
+        if backbone == GLA:
+            r = gla_fwd_bwd(a["q"], a["k"], a["v"], a["g"], a["lam"], a["dO"], scale=scale,
+                            centered=centered)
+        else:
+            r = gdn_fwd_bwd(a["q"], a["k"], a["v"], a["g"], a["beta"], a["lam"], a["dO"],
+                            scale=scale, centered=centered)
+        for key in keys:
+            out[key][r0:r1] = r["dlogalpha" if (key == "dg" and backbone == GDN) else key][0]
+    return out

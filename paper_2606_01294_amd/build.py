@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libccq.so")
-SOURCES = ["ccq_clean.hip", "ccq_gla.hip", "ccq_gdn.hip", "ccq_bwd.hip", "ccq_gdn_bwd.hip", "ccq_decode.hip", "ccq_prep.hip", "ccq_util.hip",
+SOURCES = ["ccq_clean.hip", "ccq_gla.hip", "ccq_gdn.hip", "ccq_bwd.hip", "ccq_gdn_bwd.hip", "ccq_decode.hip", "ccq_prep.hip", "ccq_varlen.hip", "ccq_util.hip",
            "ccq_api.cpp"]
 ARCH = "gfx950"
 

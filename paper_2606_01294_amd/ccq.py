@@ -23,8 +23,9 @@ CCQ_GLA, CCQ_GDN = 0, 1
 _STATUS = {0: "CCQ_OK", 1: "CCQ_ERR_INVALID_ARG", 2: "CCQ_ERR_UNSUPPORTED",
            3: "CCQ_ERR_WORKSPACE", 4: "CCQ_ERR_HIP"}
 EXPORTS = ("ccq_workspace_size", "ccq_gla_fwd", "ccq_gdn_fwd", "ccq_fwd_bwd",
-           "ccq_decode_workspace_size", "ccq_decode", "ccq_prep", "ccq_trace_events",
-           "ccq_status_string", "ccq_version")
+           "ccq_varlen_workspace_size", "ccq_gla_fwd_varlen", "ccq_gdn_fwd_varlen",
+           "ccq_fwd_bwd_varlen", "ccq_decode_workspace_size", "ccq_decode", "ccq_prep",
+           "ccq_trace_events", "ccq_status_string", "ccq_version")
 
 
 class CcqError(RuntimeError):
@@ -65,6 +66,14 @@ def lib() -> ctypes.CDLL:
             L.ccq_gdn_fwd.restype = ctypes.c_int
             L.ccq_fwd_bwd.argtypes = [SP, ctypes.c_int] + [P] * 15 + [S, P]
             L.ccq_fwd_bwd.restype = ctypes.c_int
+            L.ccq_varlen_workspace_size.argtypes = [SP, ctypes.c_int, ctypes.c_int]
+            L.ccq_varlen_workspace_size.restype = S
+            L.ccq_gla_fwd_varlen.argtypes = [SP] + [P] * 14 + [S, P]
+            L.ccq_gla_fwd_varlen.restype = ctypes.c_int
+            L.ccq_gdn_fwd_varlen.argtypes = [SP] + [P] * 15 + [S, P]
+            L.ccq_gdn_fwd_varlen.restype = ctypes.c_int
+            L.ccq_fwd_bwd_varlen.argtypes = [SP, ctypes.c_int] + [P] * 16 + [S, P]
+            L.ccq_fwd_bwd_varlen.restype = ctypes.c_int
             L.ccq_decode_workspace_size.argtypes = [SP]
             L.ccq_decode_workspace_size.restype = S
             L.ccq_decode.argtypes = [SP, ctypes.c_int] + [P] * 11 + [S, P]
@@ -255,6 +264,133 @@ def ccq_fwd_bwd(q, k, v, g, lam, dO, scale=1.0, centered=True, chunk=64, out=Non
                            _p(out["dlam"]), _p(workspace), workspace.numel(), _stream(stream))
     if rc != 0:
         raise CcqError("ccq_fwd_bwd", rc)
+    return out
+
+
+def ccq_varlen_workspace_size(shape: Shape, backbone: int, with_bwd: bool = False) -> int:
+    return int(lib().ccq_varlen_workspace_size(ctypes.byref(shape), int(backbone),
+                                               int(bool(with_bwd))))
+
+
+def _varlen_shape(backbone, q, v, gate, cu_seqlens, max_len, scale, centered, t0):
+    if cu_seqlens.dtype != torch.int32 or cu_seqlens.dim() != 1 or cu_seqlens.numel() < 1:
+        raise TypeError("cu_seqlens must be a 1-D int32 tensor of B + 1 offsets")
+    if cu_seqlens.device != q.device or not cu_seqlens.is_contiguous():
+        raise ValueError("cu_seqlens must be contiguous on the device of q")
+    rows, H, dk = q.shape
+    B = cu_seqlens.numel() - 1
+    gate_dtype = gate.dtype if backbone == CCQ_GLA else q.dtype
+    return make_shape(B, max_len, H, dk, v.shape[-1], q.dtype, gate_dtype, scale, centered, t0)
+
+
+def _varlen_ws(shape, backbone, with_bwd, workspace, device):
+    need = ccq_varlen_workspace_size(shape, backbone, with_bwd)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+    return workspace
+
+
+def _varlen_fwd(backbone, q, k, v, gate, beta, lam, cu_seqlens, max_len, S0, C0, mu0, scale,
+                centered, t0, want_states, out, workspace, stream):
+    rows, H, dk = q.shape
+    dv = v.shape[-1]
+    dev = q.device
+    shape = _varlen_shape(backbone, q, v, gate, cu_seqlens, max_len, scale, centered, t0)
+    B = shape.B
+    _check(k, "k", (rows, H, dk), q.dtype, dev)
+    _check(v, "v", (rows, H, dv), q.dtype, dev)
+    if backbone == CCQ_GLA:
+        _check(gate, "g", (rows, H, dk), gate.dtype, dev)
+    else:
+        if beta is None:
+            raise ValueError("beta is required for Gated DeltaNet")
+        _check(gate, "logalpha", (rows, H), torch.float32, dev)
+        _check(beta, "beta", (rows, H), torch.float32, dev)
+    _check(lam, "lam", (rows, H), torch.float32, dev)
+    _check(S0, "S0", (B, H, dv, dk), torch.float32, dev)
+    _check(C0, "C0", (B, H, dk, dk), torch.float32, dev)
+    _check(mu0, "mu0", (B, H, dk), torch.float32, dev)
+    out = dict(out or {})
+    out.setdefault("o", torch.empty((rows, H, dv), dtype=q.dtype, device=dev))
+    if want_states:
+        out.setdefault("ST", torch.empty((B, H, dv, dk), dtype=torch.float32, device=dev))
+        out.setdefault("CT", torch.empty((B, H, dk, dk), dtype=torch.float32, device=dev))
+        out.setdefault("muT", torch.empty((B, H, dk), dtype=torch.float32, device=dev))
+    workspace = _varlen_ws(shape, backbone, False, workspace, dev)
+    st = _stream(stream)
+    if backbone == CCQ_GLA:
+        rc = lib().ccq_gla_fwd_varlen(ctypes.byref(shape), _p(cu_seqlens), _p(q), _p(k), _p(v),
+                                      _p(gate), _p(lam), _p(S0), _p(C0), _p(mu0), _p(out["o"]),
+                                      _p(out.get("ST")), _p(out.get("CT")), _p(out.get("muT")),
+                                      _p(workspace), workspace.numel(), st)
+        fn = "ccq_gla_fwd_varlen"
+    else:
+        rc = lib().ccq_gdn_fwd_varlen(ctypes.byref(shape), _p(cu_seqlens), _p(q), _p(k), _p(v),
+                                      _p(gate), _p(beta), _p(lam), _p(S0), _p(C0), _p(mu0),
+                                      _p(out["o"]), _p(out.get("ST")), _p(out.get("CT")),
+                                      _p(out.get("muT")), _p(workspace), workspace.numel(), st)
+        fn = "ccq_gdn_fwd_varlen"
+    if rc != 0:
+        raise CcqError(fn, rc)
+    return out
+
+
+def ccq_gla_fwd_varlen(q, k, v, g, lam, cu_seqlens, max_len, S0=None, C0=None, mu0=None,
+                       scale=1.0, centered=True, t0=0, want_states=True, out=None,
+                       workspace=None, stream=None):
+    """CCQ-GLA forward on a packed batch: q, k, g [rows,H,dk], v [rows,H,dv], lam
+    [rows,H]; sequence b is rows cu_seqlens[b]..cu_seqlens[b+1]-1 (int32 device
+    tensor of B + 1 offsets), at most max_len rows long.  Returns dict o
+    [rows,H,dv][, ST, CT, muT per sequence]."""
+    return _varlen_fwd(CCQ_GLA, q, k, v, g, None, lam, cu_seqlens, max_len, S0, C0, mu0, scale,
+                       centered, t0, want_states, out, workspace, stream)
+
+
+def ccq_gdn_fwd_varlen(q, k, v, logalpha, beta, lam, cu_seqlens, max_len, S0=None, C0=None,
+                       mu0=None, scale=1.0, centered=True, t0=0, want_states=True, out=None,
+                       workspace=None, stream=None):
+    """CCQ-Gated-DeltaNet forward on a packed batch (layout as ccq_gla_fwd_varlen;
+    logalpha, beta [rows,H] fp32)."""
+    return _varlen_fwd(CCQ_GDN, q, k, v, logalpha, beta, lam, cu_seqlens, max_len, S0, C0, mu0,
+                       scale, centered, t0, want_states, out, workspace, stream)
+
+
+def ccq_fwd_bwd_varlen(q, k, v, g, lam, dO, cu_seqlens, max_len, scale=1.0, centered=True,
+                       out=None, workspace=None, stream=None, backbone=CCQ_GLA, beta=None):
+    """Training step on a packed batch (layout as ccq_gla_fwd_varlen; dO [rows,H,dv]).
+    Returns the same dict as ccq_fwd_bwd, packed."""
+    rows, H, dk = q.shape
+    dv = v.shape[-1]
+    dev = q.device
+    shape = _varlen_shape(backbone, q, v, g, cu_seqlens, max_len, scale, centered, 0)
+    if backbone == CCQ_GLA:
+        _check(g, "g", (rows, H, dk), g.dtype, dev)
+    else:
+        if beta is None:
+            raise ValueError("beta is required for the Gated DeltaNet training step")
+        _check(g, "logalpha", (rows, H), torch.float32, dev)
+        _check(beta, "beta", (rows, H), torch.float32, dev)
+    _check(k, "k", (rows, H, dk), q.dtype, dev)
+    _check(v, "v", (rows, H, dv), q.dtype, dev)
+    _check(dO, "dO", (rows, H, dv), q.dtype, dev)
+    _check(lam, "lam", (rows, H), torch.float32, dev)
+    out = dict(out or {})
+    out.setdefault("o", torch.empty((rows, H, dv), dtype=q.dtype, device=dev))
+    out.setdefault("dq", torch.empty((rows, H, dk), dtype=q.dtype, device=dev))
+    out.setdefault("dk", torch.empty((rows, H, dk), dtype=q.dtype, device=dev))
+    out.setdefault("dv", torch.empty((rows, H, dv), dtype=q.dtype, device=dev))
+    out.setdefault("dg", torch.empty(tuple(g.shape), dtype=g.dtype, device=dev))
+    out.setdefault("dlam", torch.empty((rows, H), dtype=torch.float32, device=dev))
+    if backbone == CCQ_GDN:
+        out.setdefault("dbeta", torch.empty((rows, H), dtype=torch.float32, device=dev))
+    workspace = _varlen_ws(shape, backbone, True, workspace, dev)
+    rc = lib().ccq_fwd_bwd_varlen(ctypes.byref(shape), int(backbone), _p(cu_seqlens), _p(q),
+                                  _p(k), _p(v), _p(g), _p(beta), _p(lam), _p(dO), _p(out["o"]),
+                                  _p(out["dq"]), _p(out["dk"]), _p(out["dv"]), _p(out["dg"]),
+                                  _p(out.get("dbeta")), _p(out["dlam"]), _p(workspace),
+                                  workspace.numel(), _stream(stream))
+    if rc != 0:
+        raise CcqError("ccq_fwd_bwd_varlen", rc)
     return out
 
 

@@ -447,9 +447,127 @@ ccq_status gdn_fwd_bwd(const ccq_shape* s, const void* q, const void* k, const v
   return CCQ_OK;
 }
 
+// Padded copies of a packed batch, ahead of the padded path's own workspace.
+struct VarlenLayout {
+  size_t q = 0, k = 0, v = 0, gate = 0, beta = 0, lam = 0, o = 0;
+  size_t dO = 0, dq = 0, dk = 0, dv = 0, dgate = 0, dbeta = 0, dlam = 0;
+  size_t inner = 0, total = 0;
+};
+VarlenLayout varlen_layout(const ccq_shape* s, ccq_backbone bb, bool bwd) {
+  VarlenLayout L;
+  size_t off = 0;
+  auto take = [&](size_t n) {
+    const size_t o = off;
+    off += align_up(n);
+    return o;
+  };
+  const size_t ntok = (size_t)s->B * s->T * s->H, e = esize(s->io_dtype), eg = esize(s->gate_dtype);
+  const size_t gate = bb == CCQ_GLA ? ntok * s->dk * eg : ntok * 4;
+  L.q = take(ntok * s->dk * e);
+  L.k = take(ntok * s->dk * e);
+  L.v = take(ntok * s->dv * e);
+  L.gate = take(gate);
+  if (bb == CCQ_GDN) L.beta = take(ntok * 4);
+  L.lam = take(ntok * 4);
+  L.o = take(ntok * s->dv * e);
+  if (bwd) {
+    L.dO = take(ntok * s->dv * e);
+    L.dq = take(ntok * s->dk * e);
+    L.dk = take(ntok * s->dk * e);
+    L.dv = take(ntok * s->dv * e);
+    L.dgate = take(gate);
+    if (bb == CCQ_GDN) L.dbeta = take(ntok * 4);
+    L.dlam = take(ntok * 4);
+  }
+  L.inner = off;
+  const size_t inner = bwd ? (bb == CCQ_GLA ? bwd_layout(s).total : gdn_bwd_layout(s).total)
+                           : fwd_layout(s, bb).total;
+  L.total = off + inner;
+  return L;
+}
+
+// Row bytes of the packed tensors: q/k, v, the gate (GLA [.., dk] in the gate
+// dtype, Gated DeltaNet log alpha [..] fp32) and the per-head scalars.
+struct VarlenRows {
+  size_t qk, v, gate, scalar;
+};
+VarlenRows varlen_rows(const ccq_shape* s, ccq_backbone bb) {
+  const size_t e = esize(s->io_dtype);
+  return {(size_t)s->H * s->dk * e, (size_t)s->H * s->dv * e,
+          bb == CCQ_GLA ? (size_t)s->H * s->dk * esize(s->gate_dtype) : (size_t)s->H * 4, (size_t)s->H * 4};
+}
+
+ccq_status check_varlen(const ccq_shape* s, ccq_backbone bb, const int32_t* cu) {
+  ccq_status rc = check_shape(s, bb);
+  if (rc != CCQ_OK) return rc;
+  if (s->B > 65535) return CCQ_ERR_UNSUPPORTED;  // one grid row per sequence
+  if (s->B > 0 && (!cu || (reinterpret_cast<uintptr_t>(cu) & 3u))) return CCQ_ERR_INVALID_ARG;
+  return CCQ_OK;
+}
+
+ccq_status varlen_forward(ccq_backbone bb, const ccq_shape* s, const int32_t* cu, const void* q,
+                          const void* k, const void* v, const void* g_or_la, const float* beta,
+                          const float* lam, const float* S0, const float* C0, const float* mu0, void* o,
+                          float* ST, float* CT, float* muT, void* workspace, size_t ws_bytes,
+                          void* stream) {
+  ccq_status rc = check_varlen(s, bb, cu);
+  if (rc != CCQ_OK) return rc;
+  const void* ptrs[] = {S0, C0, mu0, ST, CT, muT, workspace};
+  for (const void* p : ptrs)
+    if (p && !aligned(p)) return CCQ_ERR_INVALID_ARG;
+  if (s->B == 0 || s->H == 0) return CCQ_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (s->T == 0) return copy_initial_states(s, S0, C0, mu0, ST, CT, muT, st);
+  const void* req[] = {q, k, v, g_or_la, lam, o};
+  for (const void* p : req)
+    if (!p || !aligned(p)) return CCQ_ERR_INVALID_ARG;
+  if (bb == CCQ_GDN && (!beta || !aligned(beta))) return CCQ_ERR_INVALID_ARG;
+  const VarlenLayout L = varlen_layout(s, bb, false);
+  if (!workspace || ws_bytes < L.total) return CCQ_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  const VarlenRows R = varlen_rows(s, bb);
+  auto gather = [&](size_t dst, const void* src, size_t rb) {
+    return ccq::launch_varlen_copy(ws + dst, src, cu, s->B, s->T, rb, true, st) == hipSuccess;
+  };
+  if (!gather(L.q, q, R.qk) || !gather(L.k, k, R.qk) || !gather(L.v, v, R.v) || !gather(L.gate, g_or_la, R.gate) ||
+      (bb == CCQ_GDN && !gather(L.beta, beta, R.scalar)) || !gather(L.lam, lam, R.scalar))
+    return CCQ_ERR_HIP;
+  rc = run_forward(bb, s, ws + L.q, ws + L.k, ws + L.v, ws + L.gate,
+                   bb == CCQ_GDN ? reinterpret_cast<const float*>(ws + L.beta) : nullptr,
+                   reinterpret_cast<const float*>(ws + L.lam), S0, C0, mu0, ws + L.o, ST, CT, muT, nullptr,
+                   ws + L.inner, ws_bytes - L.inner, stream);
+  if (rc != CCQ_OK) return rc;
+  if (ccq::launch_varlen_copy(o, ws + L.o, cu, s->B, s->T, R.v, false, st) != hipSuccess) return CCQ_ERR_HIP;
+  if (ccq::launch_varlen_cache_fix(CT, muT, C0, mu0, cu, s->B, s->H, s->dk, s->T, s->t0, st) != hipSuccess)
+    return CCQ_ERR_HIP;
+  return CCQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+size_t ccq_varlen_workspace_size(const ccq_shape* s, ccq_backbone bb, int with_bwd) {
+  if (check_shape(s, bb) != CCQ_OK) return 0;
+  if (with_bwd && !ccq::bwd_supported(s->dk, s->dv, s->io_dtype == CCQ_BF16)) return 0;
+  return varlen_layout(s, bb, with_bwd != 0).total;
+}
+
+ccq_status ccq_gla_fwd_varlen(const ccq_shape* s, const int32_t* cu_seqlens, const void* q, const void* k,
+                              const void* v, const void* g, const float* lam, const float* S0,
+                              const float* C0, const float* mu0, void* o, float* ST, float* CT, float* muT,
+                              void* workspace, size_t ws_bytes, void* stream) {
+  return varlen_forward(CCQ_GLA, s, cu_seqlens, q, k, v, g, nullptr, lam, S0, C0, mu0, o, ST, CT, muT,
+                        workspace, ws_bytes, stream);
+}
+
+ccq_status ccq_gdn_fwd_varlen(const ccq_shape* s, const int32_t* cu_seqlens, const void* q, const void* k,
+                              const void* v, const float* logalpha, const float* beta, const float* lam,
+                              const float* S0, const float* C0, const float* mu0, void* o, float* ST,
+                              float* CT, float* muT, void* workspace, size_t ws_bytes, void* stream) {
+  return varlen_forward(CCQ_GDN, s, cu_seqlens, q, k, v, logalpha, beta, lam, S0, C0, mu0, o, ST, CT, muT,
+                        workspace, ws_bytes, stream);
+}
 
 size_t ccq_workspace_size(const ccq_shape* s, ccq_backbone bb, int with_bwd) {
   if (check_shape(s, bb) != CCQ_OK) return 0;
@@ -553,6 +671,47 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
                     s->centered};
   set_dk_ws(ka, s, ws, L.dkws);
   if (traced(st, [&] { return ccq::launch_ccq_dk(ka, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
+  return CCQ_OK;
+}
+
+ccq_status ccq_fwd_bwd_varlen(const ccq_shape* s, ccq_backbone bb, const int32_t* cu_seqlens, const void* q,
+                              const void* k, const void* v, const void* g_or_logalpha, const float* beta,
+                              const float* lam, const void* dO, void* o, void* dq, void* dk, void* dv,
+                              void* dg_or_dlogalpha, float* dbeta, float* dlam, void* workspace,
+                              size_t ws_bytes, void* stream) {
+  ccq_status rc = check_varlen(s, bb, cu_seqlens);
+  if (rc != CCQ_OK) return rc;
+  if (s->t0 != 0) return CCQ_ERR_INVALID_ARG;
+  if (!ccq::bwd_supported(s->dk, s->dv, s->io_dtype == CCQ_BF16)) return CCQ_ERR_UNSUPPORTED;
+  if (workspace && !aligned(workspace)) return CCQ_ERR_INVALID_ARG;
+  if ((size_t)s->B * s->T * s->H == 0) return CCQ_OK;
+  const void* req[] = {q, k, v, g_or_logalpha, lam, dO, o, dq, dk, dv, dg_or_dlogalpha, dlam};
+  for (const void* p : req)
+    if (!p || !aligned(p)) return CCQ_ERR_INVALID_ARG;
+  if (bb == CCQ_GDN && (!beta || !aligned(beta) || !dbeta || !aligned(dbeta))) return CCQ_ERR_INVALID_ARG;
+  const VarlenLayout L = varlen_layout(s, bb, true);
+  if (!workspace || ws_bytes < L.total) return CCQ_ERR_WORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  const VarlenRows R = varlen_rows(s, bb);
+  const int32_t* cu = cu_seqlens;
+  auto copy = [&](void* dst, const void* src, size_t rb, bool to_padded) {
+    return ccq::launch_varlen_copy(dst, src, cu, s->B, s->T, rb, to_padded, st) == hipSuccess;
+  };
+  if (!copy(ws + L.q, q, R.qk, true) || !copy(ws + L.k, k, R.qk, true) || !copy(ws + L.v, v, R.v, true) ||
+      !copy(ws + L.gate, g_or_logalpha, R.gate, true) || (bb == CCQ_GDN && !copy(ws + L.beta, beta, R.scalar, true)) ||
+      !copy(ws + L.lam, lam, R.scalar, true) || !copy(ws + L.dO, dO, R.v, true))
+    return CCQ_ERR_HIP;
+  rc = ccq_fwd_bwd(s, bb, ws + L.q, ws + L.k, ws + L.v, ws + L.gate,
+                   bb == CCQ_GDN ? reinterpret_cast<const float*>(ws + L.beta) : nullptr,
+                   reinterpret_cast<const float*>(ws + L.lam), ws + L.dO, ws + L.o, ws + L.dq, ws + L.dk,
+                   ws + L.dv, ws + L.dgate, bb == CCQ_GDN ? reinterpret_cast<float*>(ws + L.dbeta) : nullptr,
+                   reinterpret_cast<float*>(ws + L.dlam), ws + L.inner, ws_bytes - L.inner, stream);
+  if (rc != CCQ_OK) return rc;
+  if (!copy(o, ws + L.o, R.v, false) || !copy(dq, ws + L.dq, R.qk, false) || !copy(dk, ws + L.dk, R.qk, false) ||
+      !copy(dv, ws + L.dv, R.v, false) || !copy(dg_or_dlogalpha, ws + L.dgate, R.gate, false) ||
+      (bb == CCQ_GDN && !copy(dbeta, ws + L.dbeta, R.scalar, false)) || !copy(dlam, ws + L.dlam, R.scalar, false))
+    return CCQ_ERR_HIP;
   return CCQ_OK;
 }
 

@@ -319,6 +319,16 @@ bool decode_supported(int dk, int dv);
 hipError_t launch_prep(const PrepArgs& a, bool is_bf16, hipStream_t st);
 bool prep_supported(int H, int dk);
 
+// Packed batches: rows of sequence b are cu[b] .. cu[b+1] - 1 of a [rows, ...]
+// tensor whose rows are row_bytes wide (a multiple of 4).  to_padded: packed
+// -> [B, T, ...] with the rows past each sequence's end zeroed; else the
+// sequences' rows back from padded to packed.
+hipError_t launch_varlen_copy(void* dst, const void* src, const int* cu, int B, int T, size_t row_bytes,
+                              bool to_padded, hipStream_t st);
+// Cbar_T, mu_T of a padded forward rescaled from count t0 + T to t0 + len_b.
+hipError_t launch_varlen_cache_fix(float* CT, float* muT, const float* C0, const float* mu0, const int* cu,
+                                   int B, int H, int dk, int T, long long t0, hipStream_t st);
+
 // Supported-shape predicates (used by validation before any launch).
 bool clean_supported(int dk, bool is_bf16);
 bool gla_supported(int dk, int dv, bool is_bf16);

@@ -155,3 +155,41 @@ def test_prep_entry_point_validation():
     assert call(shape(H=4, dk=96)) == 2
     assert call(shape(H=4, dk=64), ptr=FAKE + 4) == 1     # misaligned
     assert call(shape(B=0, H=4, dk=64), ptr=0) == 0
+
+
+def test_varlen_entry_point_validation():
+    P = ctypes.c_void_p
+    s = shape(dk=128)
+    assert ccq.ccq_varlen_workspace_size(s, ccq.CCQ_GLA) > ccq.ccq_workspace_size(s, ccq.CCQ_GLA)
+    assert ccq.ccq_varlen_workspace_size(s, ccq.CCQ_GDN, True) > ccq.ccq_workspace_size(
+        s, ccq.CCQ_GDN, True)
+    assert ccq.ccq_varlen_workspace_size(shape(dk=96), ccq.CCQ_GLA) == 0
+
+    def call(s, cu=FAKE, ptr=FAKE, ws_bytes=1 << 34):
+        return ccq.lib().ccq_gla_fwd_varlen(ctypes.byref(s), None if cu is None else P(cu), P(ptr),
+                                            P(ptr), P(ptr), P(ptr), P(ptr), None, None, None,
+                                            P(ptr), None, None, None, P(FAKE), ws_bytes, None)
+    assert call(shape(), cu=None) == 1                      # offsets required
+    assert call(shape(), cu=FAKE + 2) == 1                  # misaligned offsets
+    assert call(shape(B=70000)) == 2                        # one grid row per sequence
+    assert call(shape(dk=96)) == 2
+    assert call(shape(), ptr=FAKE + 4) == 1
+    assert call(shape(), ws_bytes=64) == 3
+    assert call(shape(B=0), cu=None, ptr=0) == 0
+
+    def call_gdn(s, beta=FAKE):
+        return ccq.lib().ccq_gdn_fwd_varlen(ctypes.byref(s), P(FAKE), P(FAKE), P(FAKE), P(FAKE),
+                                            P(FAKE), None if beta is None else P(beta), P(FAKE),
+                                            None, None, None, P(FAKE), None, None, None, P(FAKE),
+                                            1 << 34, None)
+    assert call_gdn(shape(dk=256), beta=None) == 1
+
+    def call_bwd(s, bb=0, t0=0):
+        s.t0 = t0
+        return ccq.lib().ccq_fwd_bwd_varlen(ctypes.byref(s), bb, P(FAKE), P(FAKE), P(FAKE), P(FAKE),
+                                            P(FAKE), None, P(FAKE), P(FAKE), P(FAKE), P(FAKE),
+                                            P(FAKE), P(FAKE), P(FAKE), None, P(FAKE), P(FAKE),
+                                            1 << 34, None)
+    assert call_bwd(shape(), t0=3) == 1
+    assert call_bwd(shape(), bb=1) == 1                     # Gated DeltaNet needs beta, dbeta
+    assert call_bwd(shape(dk=256), bb=1) == 2

@@ -457,3 +457,76 @@ def test_prep_gate_reads_the_raw_query_before_the_head_split():
     np.testing.assert_allclose(a["lam"] + f["lam"], 1.0, rtol=1e-14)
     c = O.prep(4.0 * q, k, W / 4.0, b)
     np.testing.assert_allclose(c["lam"], a["lam"], rtol=1e-13)
+
+
+# ---------------------------------------------------------------- packed batches
+
+
+def _pack(d, lens):
+    """Rows of sequences b = 0.. (lengths lens) of a batched input dict, packed."""
+    out = {}
+    for n, x in d.items():
+        if x is None:
+            out[n] = None
+            continue
+        out[n] = np.concatenate([x[b, :L] for b, L in enumerate(lens)], axis=0)
+    return out, np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+
+
+@pytest.mark.parametrize("backbone", [O.GLA, O.GDN])
+def test_packed_batch_of_equal_lengths_is_the_batched_call(backbone):
+    """With every length equal, the packed forward (one call per sequence) reproduces the
+    batched C path, which walks the (batch, head) pairs itself."""
+    rng = np.random.default_rng(40)
+    B, T = 3, 23
+    d = rnd_inputs(rng, B, T, 2, 6, 4, backbone=backbone)
+    S0 = rng.standard_normal((B, 2, 4, 6))
+    ref = run(d, backbone=backbone, S0=S0)
+    p, cu = _pack(d, [T] * B)
+    r = O.varlen_fwd(p["q"], p["k"], p["v"], p["gate"], p["lam"], cu, beta=p["beta"],
+                     backbone=backbone, S0=S0)
+    np.testing.assert_allclose(r["o"], ref["o"].reshape(B * T, 2, 4), rtol=0, atol=1e-12)
+    for key in ("ST", "CT", "muT"):
+        np.testing.assert_allclose(r[key], ref[key], rtol=0, atol=1e-12)
+
+
+def test_packed_batch_sequences_are_independent():
+    """Reordering the sequences of a packed batch reorders its outputs and nothing
+    else; an empty sequence returns its initial cache."""
+    rng = np.random.default_rng(41)
+    lens = [11, 0, 30, 5]
+    d = rnd_inputs(rng, 4, 30, 2, 5, 3)
+    C0 = rng.standard_normal((4, 2, 5, 5))
+    mu0 = rng.standard_normal((4, 2, 5))
+    p, cu = _pack(d, lens)
+    r = O.varlen_fwd(p["q"], p["k"], p["v"], p["gate"], p["lam"], cu, C0=C0, mu0=mu0, t0=7)
+    perm = [2, 0, 3, 1]
+    dp = {n: (None if x is None else x[perm]) for n, x in d.items()}
+    pp, cup = _pack(dp, [lens[i] for i in perm])
+    rp = O.varlen_fwd(pp["q"], pp["k"], pp["v"], pp["gate"], pp["lam"], cup, C0=C0[perm],
+                      mu0=mu0[perm], t0=7)
+    for j, b in enumerate(perm):
+        np.testing.assert_array_equal(rp["o"][cup[j]:cup[j + 1]], r["o"][cu[b]:cu[b + 1]])
+        for key in ("ST", "CT", "muT"):
+            np.testing.assert_array_equal(rp[key][j], r[key][b])
+    np.testing.assert_array_equal(r["CT"][1], C0[1])
+    np.testing.assert_array_equal(r["muT"][1], mu0[1])
+
+
+@pytest.mark.parametrize("backbone", [O.GLA, O.GDN])
+def test_packed_reverse_pass_of_equal_lengths_is_the_batched_call(backbone):
+    rng = np.random.default_rng(42)
+    B, T = 2, 17
+    d = rnd_inputs(rng, B, T, 1, 4, 3, backbone=backbone)
+    dO = rng.standard_normal((B, T, 1, 3))
+    if backbone == O.GLA:
+        ref = O.gla_fwd_bwd(d["q"], d["k"], d["v"], d["gate"], d["lam"], dO)
+    else:
+        ref = O.gdn_fwd_bwd(d["q"], d["k"], d["v"], d["gate"], d["beta"], d["lam"], dO)
+        ref["dg"] = ref["dlogalpha"]
+    d["dO"] = dO
+    p, cu = _pack(d, [T] * B)
+    r = O.varlen_fwd_bwd(p["q"], p["k"], p["v"], p["gate"], p["lam"], p["dO"], cu, beta=p["beta"],
+                         backbone=backbone)
+    for key in ("o", "dq", "dk", "dv", "dg", "dlam") + (("dbeta",) if backbone == O.GDN else ()):
+        np.testing.assert_allclose(r[key], ref[key].reshape(r[key].shape), rtol=0, atol=1e-12)
