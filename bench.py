@@ -44,12 +44,15 @@ def gla_seg(bh: int, nc: int, dk: int, dv: int) -> int:
 
 
 def clean_seg(bh: int, nc: int) -> int:
-    """Chunks per segment of the query contraction (the library's policy: the
-    longest of 8, 4, 2 that still gives every compute unit a workgroup)."""
-    seg = 8
-    while seg > 2 and bh * (-(-nc // seg)) < 256:
-        seg //= 2
-    return seg
+    """Chunks per segment of the query contraction (the library's policy: the length
+    from 2 to 64 minimising rounds of 256 workgroups x chunks per segment, the longest
+    on a tie)."""
+    best, best_cost = 2, None
+    for seg in range(2, 65):
+        cost = -(-(bh * -(-nc // seg)) // 256) * min(seg, nc)
+        if best_cost is None or cost <= best_cost:
+            best, best_cost = seg, cost
+    return best
 
 
 def gdn_group(w) -> int:
@@ -147,6 +150,19 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     elif kernel == "ccq_dk":
         by = ntok * (3 * dk * io_bytes + 12 + 4 * dk + dk * io_bytes)
         fl = ntok * (6 * dk * dk + 8 * C * dk)
+    elif kernel.startswith("varlen_"):
+        # packed rows read and padded rows written (gathers), padded rows read and
+        # packed rows written (scatter); rows of H heads
+        real = getattr(w, "packed_rows", w.B * w.T)
+        pad = w.B * w.T
+        rb = {"varlen_gather_qk": dk * io_bytes, "varlen_gather_v": dv * io_bytes,
+              "varlen_gather_scalar": 4, "varlen_scatter_o": dv * io_bytes}.get(kernel, 0) * w.H
+        if kernel == "varlen_fix":
+            by, fl = BH * (dk * dk + dk) * 8, 0
+        elif kernel == "varlen_scatter_o":
+            by, fl = 2 * real * rb, 0
+        else:
+            by, fl = (real + pad) * rb, 0
     else:
         raise KeyError(kernel)
     return by, fl
@@ -161,7 +177,11 @@ KERNELS = {0: ["gla_state"] + CLEAN + ["clean_out", "gla_out"],
            "gdn_train": CLEAN + ["clean_out_train", "gdn_tri", "gdn_state", "gdn_out",
                                  "gdn_bwd_prep", "gdn_dstate", "gdn_bwd_chunk", "clean_dq",
                                  "ccq_dk"]}
-KERNEL_SYMBOL = {"prep": "prep_kernel", "decode": "decode_stats_kernel+decode_out_kernel", "clean_gram": "clean_gram_kernel",
+VARLEN_GDN = ["varlen_gather_qk", "varlen_gather_qk", "varlen_gather_v", "varlen_gather_scalar",
+              "varlen_gather_scalar", "varlen_gather_scalar"] + KERNELS[1] + ["varlen_scatter_o", "varlen_fix"]
+KERNEL_SYMBOL = {"varlen_gather_qk": "varlen_copy_kernel", "varlen_gather_v": "varlen_copy_kernel",
+                 "varlen_gather_scalar": "varlen_copy_kernel", "varlen_scatter_o": "varlen_copy_kernel",
+                 "varlen_fix": "varlen_cache_fix_kernel", "prep": "prep_kernel", "decode": "decode_stats_kernel+decode_out_kernel", "clean_gram": "clean_gram_kernel",
                  "clean_prefix": "clean_prefix_kernel", "clean_out": "clean_out_kernel",
                  "clean_out_train": "clean_out_kernel", "clean_dq": "clean_out_kernel",
                  "gla_state": "gla_state_kernel", "gla_scan": "gla_scan_kernel", "gla_out": "gla_out_kernel",
@@ -183,6 +203,8 @@ def _source(kernel: str) -> str:
         return "ccq_decode.hip"
     if kernel == "prep":
         return "ccq_prep.hip"
+    if kernel.startswith("varlen"):
+        return "ccq_varlen.hip"
     if kernel.startswith("gdn"):
         return "ccq_gdn.hip"
     return "ccq_bwd.hip"
@@ -315,6 +337,42 @@ class PrepCall:
         self.ccq.ccq_prep(self.q, self.k, self.wl, self.bl, out=self.out)
 
 
+class VarlenCall:
+    """The Gated DeltaNet forward on a packed batch: 2B sequences of lengths uniform in
+    [T/4, 3T/4] (about the tokens of the B x T workload), carried through the padded
+    path (inputs resident on the GPU)."""
+
+    def __init__(self, w, torch, ccq, inputs):
+        import dataclasses
+        lens = inputs.varlen_lengths(w)
+        self.lens = lens
+        T = max(lens)
+        self.w = dataclasses.replace(w, name=w.name.replace("_t", "_varlen_t"), B=len(lens), T=T)
+        object.__setattr__(self.w, "packed_rows", sum(lens))  # rows of H heads actually present
+        d = inputs.make_inputs(w.backbone, len(lens), T, w.H, w.dk, w.dv, w.dtype, seed=w.seed)
+        self.d = inputs.to_device(inputs.pack(d, lens))
+        dev = self.d["q"].device
+        offs = [0]
+        for L in lens:
+            offs.append(offs[-1] + L)
+        self.cu = torch.tensor(offs, dtype=torch.int32, device=dev)
+        B, H, dk, dv = len(lens), w.H, w.dk, w.dv
+        self.out = {"o": torch.empty((sum(lens), H, dv), dtype=w.dtype, device=dev),
+                    "ST": torch.empty((B, H, dv, dk), dtype=torch.float32, device=dev),
+                    "CT": torch.empty((B, H, dk, dk), dtype=torch.float32, device=dev),
+                    "muT": torch.empty((B, H, dk), dtype=torch.float32, device=dev)}
+        shape = ccq.make_shape(B, T, H, dk, dv, w.dtype, w.dtype)
+        self.ws = torch.empty(max(1, ccq.ccq_varlen_workspace_size(shape, w.backbone)),
+                              dtype=torch.uint8, device=dev)
+        self.ccq = ccq
+        self.kernels = VARLEN_GDN
+
+    def __call__(self):
+        d = self.d
+        self.ccq.ccq_gdn_fwd_varlen(d["q"], d["k"], d["v"], d["logalpha"], d["beta"], d["lam"],
+                                    self.cu, self.w.T, out=self.out, workspace=self.ws)
+
+
 def time_calls(torch, ccq, calls, steps, warmup, with_plain=False):
     """Warm up, then time exactly `steps` steps (each step = every call once) between two
     synchronisations; per-kernel durations come from HIP events the library records on
@@ -393,7 +451,8 @@ def roofline(entry, w):
 
 
 EXTRA = ("gla_500m_t2k", "gdn_1p3b_t4k", "gla_500m_t20k", "gdn_1p3b_t20k", "gla_train_t4k",
-         "gdn_train_t4k", "gla_500m_decode_t2k", "gdn_1p3b_decode_t4k", "gdn_1p3b_prep_t4k")
+         "gdn_train_t4k", "gla_500m_decode_t2k", "gdn_1p3b_decode_t4k", "gdn_1p3b_prep_t4k",
+         "gdn_1p3b_varlen_t4k")
 
 
 def measure_extra(name, torch, ccq, inputs, steps, existing):
@@ -407,6 +466,15 @@ def measure_extra(name, torch, ccq, inputs, steps, existing):
                "ms_traced": round(ms_tr, 5),
                "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
                "roofline": roofline(pk[0], c.w)}
+    elif "_varlen_" in name:
+        c = VarlenCall(W[name.replace("_varlen_t", "_t")], torch, ccq, inputs)
+        ms, ms_tr, pk = time_calls(torch, ccq, [c], max(5, steps // 2), 3, with_plain=True)
+        dom = max(pk, key=lambda e: e["ms_mean"])
+        res = {"tokens_per_s": round(sum(c.lens) / (ms * 1e-3), 1), "ms": round(ms, 4),
+               "ms_traced": round(ms_tr, 4), "sequences": len(c.lens),
+               "packed_tokens": sum(c.lens), "padded_tokens": c.w.B * c.w.T,
+               "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
+               "roofline": roofline(dom, c.w)}
     elif "_decode_" in name:
         c = DecodeCall(W[name.replace("_decode_t", "_t")], torch, ccq, inputs)
         ms, ms_tr, pk = time_calls(torch, ccq, [c], max(20, steps), 5, with_plain=True)

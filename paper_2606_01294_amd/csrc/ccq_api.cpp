@@ -14,10 +14,22 @@ struct Trace {
   hipEvent_t* ev = nullptr;
   int n = 0;
   int next = 0;
+  bool nested = false;  // inside an entry point that wraps another one
 };
 thread_local Trace g_trace;
 
-void trace_begin_call() { g_trace.next = 0; }
+void trace_begin_call() {
+  if (!g_trace.nested) g_trace.next = 0;
+}
+// An entry point built on another one numbers its own launches and the inner
+// call's in one sequence.
+struct TraceScope {
+  TraceScope() {
+    trace_begin_call();
+    g_trace.nested = true;
+  }
+  ~TraceScope() { g_trace.nested = false; }
+};
 
 // Runs one launcher between the trace events of its slot, if tracing is on.
 template <typename F>
@@ -526,8 +538,10 @@ ccq_status varlen_forward(ccq_backbone bb, const ccq_shape* s, const int32_t* cu
   if (!workspace || ws_bytes < L.total) return CCQ_ERR_WORKSPACE;
   char* ws = static_cast<char*>(workspace);
   const VarlenRows R = varlen_rows(s, bb);
+  TraceScope scope;
   auto gather = [&](size_t dst, const void* src, size_t rb) {
-    return ccq::launch_varlen_copy(ws + dst, src, cu, s->B, s->T, rb, true, st) == hipSuccess;
+    return traced(st, [&] { return ccq::launch_varlen_copy(ws + dst, src, cu, s->B, s->T, rb, true, st); }) ==
+           hipSuccess;
   };
   if (!gather(L.q, q, R.qk) || !gather(L.k, k, R.qk) || !gather(L.v, v, R.v) || !gather(L.gate, g_or_la, R.gate) ||
       (bb == CCQ_GDN && !gather(L.beta, beta, R.scalar)) || !gather(L.lam, lam, R.scalar))
@@ -537,8 +551,13 @@ ccq_status varlen_forward(ccq_backbone bb, const ccq_shape* s, const int32_t* cu
                    reinterpret_cast<const float*>(ws + L.lam), S0, C0, mu0, ws + L.o, ST, CT, muT, nullptr,
                    ws + L.inner, ws_bytes - L.inner, stream);
   if (rc != CCQ_OK) return rc;
-  if (ccq::launch_varlen_copy(o, ws + L.o, cu, s->B, s->T, R.v, false, st) != hipSuccess) return CCQ_ERR_HIP;
-  if (ccq::launch_varlen_cache_fix(CT, muT, C0, mu0, cu, s->B, s->H, s->dk, s->T, s->t0, st) != hipSuccess)
+  if (traced(st, [&] { return ccq::launch_varlen_copy(o, ws + L.o, cu, s->B, s->T, R.v, false, st); }) !=
+      hipSuccess)
+    return CCQ_ERR_HIP;
+  if ((CT || muT) &&
+      traced(st, [&] {
+        return ccq::launch_varlen_cache_fix(CT, muT, C0, mu0, cu, s->B, s->H, s->dk, s->T, s->t0, st);
+      }) != hipSuccess)
     return CCQ_ERR_HIP;
   return CCQ_OK;
 }
@@ -695,8 +714,10 @@ ccq_status ccq_fwd_bwd_varlen(const ccq_shape* s, ccq_backbone bb, const int32_t
   char* ws = static_cast<char*>(workspace);
   const VarlenRows R = varlen_rows(s, bb);
   const int32_t* cu = cu_seqlens;
+  TraceScope scope;
   auto copy = [&](void* dst, const void* src, size_t rb, bool to_padded) {
-    return ccq::launch_varlen_copy(dst, src, cu, s->B, s->T, rb, to_padded, st) == hipSuccess;
+    return traced(st, [&] { return ccq::launch_varlen_copy(dst, src, cu, s->B, s->T, rb, to_padded, st); }) ==
+           hipSuccess;
   };
   if (!copy(ws + L.q, q, R.qk, true) || !copy(ws + L.k, k, R.qk, true) || !copy(ws + L.v, v, R.v, true) ||
       !copy(ws + L.gate, g_or_logalpha, R.gate, true) || (bb == CCQ_GDN && !copy(ws + L.beta, beta, R.scalar, true)) ||

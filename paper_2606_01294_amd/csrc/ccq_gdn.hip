@@ -905,6 +905,11 @@ hipError_t run_gdn_state(const GdnArgs& a, hipStream_t st) {
   const long long slices = (long long)a.B * a.H * (a.dv / 16);
   constexpr int kSimds = 1024;
   if constexpr (sizeof(T) == 2 && (DK == 128 || DK == 256)) {
+    // one workgroup per compute unit: at dk = 128, 64-wide value slices once
+    // there are enough of them, so that the chip takes every slice in one
+    // round (at dk = 256 that split would not fit the registers)
+    if constexpr (DK == 128)
+      if (slices >= kSimds && a.dv % 64 == 0) return run_gdn_state_dma<DK, 4, 2>(a, st);
     if (slices * 2 >= kSimds && a.dv % 32 == 0) return run_gdn_state_dma<DK, 2, 4>(a, st);
   }
   if (slices >= kSimds || DK < 64) return run_gdn_state_v<T, DK, 4, 1>(a, st);

@@ -284,12 +284,23 @@ struct PrepArgs {
 hipError_t launch_clean_gram(const CleanArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_clean_prefix(const CleanArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_clean_out(const CleanArgs& a, bool is_bf16, hipStream_t st);
-// Chunks per segment of the query contraction for bh heads of nc chunks: the
-// longest of 8, 4, 2 that still gives every compute unit a workgroup.
+// Chunks per segment of the query contraction for bh heads of nc chunks.  Each
+// segment is one workgroup walking its chunks in order, one workgroup per
+// compute unit at a time, so the pass takes about (rounds of 256 workgroups) x
+// (chunks per segment) chunk steps: the segment length (2 to 64) that
+// minimises that, the longest on a tie (fewer segment statistics).
 inline int clean_seg(long long bh, long long nc) {
-  int seg = 8;
-  while (seg > 2 && bh * ((nc + seg - 1) / seg) < 256) seg /= 2;
-  return seg;
+  int best = 2;
+  long long best_cost = -1;
+  for (int seg = 2; seg <= 64; ++seg) {
+    const long long wgs = bh * ((nc + seg - 1) / seg);
+    const long long cost = ((wgs + 255) / 256) * (seg < nc ? seg : nc);
+    if (best_cost < 0 || cost <= best_cost) {
+      best_cost = cost;
+      best = seg;
+    }
+  }
+  return best;
 }
 hipError_t launch_gla_state(const GlaStateArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
 hipError_t launch_gla_out(const GlaOutArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);

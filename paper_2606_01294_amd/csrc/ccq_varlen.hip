@@ -46,26 +46,25 @@ __global__ void varlen_copy_kernel(V* dst, const V* src, const int* cu, int T, l
   }
 }
 
-// Cbar_T and mu_T of (sequence b, head h) = blockIdx.x: counts t0 + T ->
-// t0 + len_b; a sequence with no tokens at all returns the initial cache.
+// Cbar_T and mu_T of (sequence b, head h) = blockIdx.y: counts t0 + T ->
+// t0 + len_b, blockIdx.x taking 256 of the head's dk * dk + dk values; a
+// sequence with no tokens at all returns the initial cache.
 __global__ void varlen_cache_fix_kernel(float* CT, float* muT, const float* C0, const float* mu0,
                                         const int* cu, int H, int dk, int T, long long t0) {
-  const int bh = blockIdx.x, b = bh / H;
+  const int bh = blockIdx.y, b = bh / H;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int nc = dk * dk;
+  if (i >= nc + dk) return;
   const int len = seq_len(cu, b, T);
   const long long cnt = t0 + len;
-  const size_t cbase = (size_t)bh * dk * dk, mbase = (size_t)bh * dk;
+  float* dst = i < nc ? (CT ? CT + (size_t)bh * nc + i : nullptr) : (muT ? muT + (size_t)bh * dk + (i - nc) : nullptr);
+  if (!dst) return;
   if (cnt == 0) {
-    if (CT)
-      for (int i = threadIdx.x; i < dk * dk; i += blockDim.x) CT[cbase + i] = C0 ? C0[cbase + i] : 0.f;
-    if (muT)
-      for (int i = threadIdx.x; i < dk; i += blockDim.x) muT[mbase + i] = mu0 ? mu0[mbase + i] : 0.f;
+    const float* src = i < nc ? (C0 ? C0 + (size_t)bh * nc + i : nullptr) : (mu0 ? mu0 + (size_t)bh * dk + (i - nc) : nullptr);
+    *dst = src ? *src : 0.f;
     return;
   }
-  const float f = (float)((double)(t0 + T) / (double)cnt);
-  if (CT)
-    for (int i = threadIdx.x; i < dk * dk; i += blockDim.x) CT[cbase + i] *= f;
-  if (muT)
-    for (int i = threadIdx.x; i < dk; i += blockDim.x) muT[mbase + i] *= f;
+  *dst *= (float)((double)(t0 + T) / (double)cnt);
 }
 
 }  // namespace
@@ -103,8 +102,9 @@ hipError_t launch_varlen_copy(void* dst, const void* src, const int* cu, int B, 
 hipError_t launch_varlen_cache_fix(float* CT, float* muT, const float* C0, const float* mu0, const int* cu,
                                    int B, int H, int dk, int T, long long t0, hipStream_t st) {
   if (B == 0 || H == 0 || (!CT && !muT)) return hipSuccess;
-  hipLaunchKernelGGL(varlen_cache_fix_kernel, dim3((unsigned)(B * H)), dim3(256), 0, st, CT, muT, C0, mu0, cu, H,
-                     dk, T, t0);
+  const unsigned nx = (unsigned)((dk * dk + dk + 255) / 256);
+  hipLaunchKernelGGL(varlen_cache_fix_kernel, dim3(nx, (unsigned)(B * H)), dim3(256), 0, st, CT, muT, C0, mu0, cu,
+                     H, dk, T, t0);
   return hipGetLastError();
 }
 

@@ -112,6 +112,19 @@ def workload_inputs(w: Workload, **kw) -> dict:
     return make_inputs(w.backbone, w.B, w.T, w.H, w.dk, w.dv, w.dtype, seed=w.seed, **kw)
 
 
+def varlen_lengths(w: Workload) -> list:
+    """Sequence lengths of the packed-batch form of workload w: 2B sequences with
+    lengths uniform in [T/4, 3T/4] (seeded), about as many tokens as w itself."""
+    rng = np.random.default_rng(w.seed)
+    return [int(x) for x in rng.integers(w.T // 4, 3 * w.T // 4 + 1, size=2 * w.B)]
+
+
+def pack(inputs: dict, lens) -> dict:
+    """Rows 0..lens[b]-1 of every sequence b of a [B, T, ...] input dict, packed."""
+    return {k: torch.cat([t[b, :L] for b, L in enumerate(lens)], dim=0).contiguous()
+            for k, t in inputs.items()}
+
+
 def to_f64(inputs: dict) -> dict:
     """Exact fp64 copies (numpy) of the same values, for the oracle."""
     return {k: t.double().numpy() for k, t in inputs.items()}
