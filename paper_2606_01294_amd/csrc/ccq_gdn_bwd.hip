@@ -89,18 +89,23 @@ __global__ __launch_bounds__(kThreads) void gdn_bwd_prep_kernel(const GdnPrepArg
 
 // ----------------------------------------------------------------------------
 // Reverse scan of D = dL/dS_{r+1} over the chunks of one head.  A workgroup
-// owns NPR value tiles of 16; wave p keeps D^T[c][v] for all key features c
-// of its tile in MFMA accumulators.  Per chunk (last to first):
-//   store D;  X = diag(e^{gamma_C - gamma}) K D^T;  dU = X + PT dO';
-//   dR = Tm^T dU -> stored;  D <- e^{gamma_C} D + (G Q)^T dO' - K^T diag(beta G) dR.
+// owns NPR value tiles of 16, each split over NH waves by key feature: wave
+// (p, hq) keeps D^T[c][v] for its DK / NH features c of tile p in MFMA
+// accumulators.  Per chunk (last to first):
+//   store D;  X = diag(e^{gamma_C - gamma}) K D^T (partial over each wave's
+//   features, summed over the NH waves through LDS in a fixed order);
+//   dU = X + PT dO';  dR = Tm^T dU -> stored;
+//   D <- e^{gamma_C} D + (G Q)^T dO' - K^T diag(beta G) dR.
 // The chunk's K, G Q, PT, Tm^T and dO' slice are prefetched into registers
 // one chunk ahead and staged through LDS.
-template <typename T, int DK, int NPR>
-__global__ __launch_bounds__(64 * NPR, 1) void gdn_dstate_kernel(const GdnDstateArgs a) {
-  constexpr int C = kChunk, NT = 64 * NPR, BVS = 16 * NPR;
+template <typename T, int DK, int NPR, int NH>
+__global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_dstate_kernel(const GdnDstateArgs a) {
+  constexpr int C = kChunk, NW = NPR * NH, NT = 64 * NW, BVS = 16 * NPR;
   constexpr int P = Pad<T>::value;
   constexpr int LDQ = DK + P, LDP = C + P;
-  constexpr int NCT = DK / 16, NK = DK / 32;
+  constexpr int DKH = DK / NH, NCT = DKH / 16, NK = DKH / 32;
+  constexpr int NTO = NT < C * BVS / 8 ? NT : C * BVS / 8;  // threads staging the dO' slice
+  static_assert(NK >= 1, "key split");
 
   __shared__ __align__(16) T sK[C * LDQ];
   __shared__ __align__(16) T sQ[C * LDQ];      // e^{gamma_i} qc_i
@@ -108,6 +113,7 @@ __global__ __launch_bounds__(64 * NPR, 1) void gdn_dstate_kernel(const GdnDstate
   __shared__ __align__(16) T sTT[C * LDP];     // Tm^T, rows in acc_pos order
   __shared__ __align__(16) T sdOT[BVS * LDP];  // (s dO)^T of the workgroup's values
   __shared__ __align__(16) float sCf[3][C];    // e^{gamma_C - gamma}, beta e^gamma, e^{gamma_C}
+  __shared__ __align__(16) f32x4 sX[NH > 1 ? NW * 4 * 64 : 1];  // partial X of every wave
 
   const int nvt = a.dv / BVS;
   const int N = (a.T + C - 1) / C;
@@ -115,9 +121,11 @@ __global__ __launch_bounds__(64 * NPR, 1) void gdn_dstate_kernel(const GdnDstate
   const int bh = lb / nvt;
   const int v0 = (lb % nvt) * BVS;
   const int b = bh / a.H, h = bh % a.H;
-  const int tid = threadIdx.x, pr = wave_id(), l = lane_id();
+  const int tid = threadIdx.x, w = wave_id(), l = lane_id();
+  const int pr = w / NH, hq = w % NH;
   const int g4 = l >> 4, c16 = l & 15;
   const int v = v0 + 16 * pr + c16;
+  const int c0 = hq * DKH;  // first key feature of this wave
   const T* qc = static_cast<const T*>(a.qc);
   const T* k = static_cast<const T*>(a.k);
   const T* dO = static_cast<const T*>(a.dO);
@@ -132,7 +140,7 @@ __global__ __launch_bounds__(64 * NPR, 1) void gdn_dstate_kernel(const GdnDstate
     RowTile<T, DK, NT> rk;
     ChunkTile<T, DK, NT> rq;   // lane = token row, so one decay per lane
     RowTile<T, C, NT> rp, rt;
-    ChunkTile<T, BVS, NT> rdo;
+    ChunkTile<T, BVS, NTO> rdo;
     float gq;                  // gamma of this lane's token row
     RowScalar cf[3];
   };
@@ -145,7 +153,7 @@ __global__ __launch_bounds__(64 * NPR, 1) void gdn_dstate_kernel(const GdnDstate
     st.rq.load(qc + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
     st.rp.load(static_cast<const T*>(a.PT) + cidx * C * C, (size_t)C, C);
     st.rt.load(static_cast<const T*>(a.TmT) + cidx * C * C, (size_t)C, C);
-    st.rdo.load(dO + tok_off(b, r0, h, a.T, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
+    if (tid < NTO) st.rdo.load(dO + tok_off(b, r0, h, a.T, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
     st.gq = a.gam[cidx * 5 * C + (tid & 63)];
     if (tid < C) {
       st.cf[0].load(a.gam + (cidx * 5 + 3) * C, 1, tid, C);
@@ -175,20 +183,21 @@ __global__ __launch_bounds__(64 * NPR, 1) void gdn_dstate_kernel(const GdnDstate
         for (int e = 0; e < 8; ++e) y[e] = to<T>(eg * f32(x[e]));
         *reinterpret_cast<vq*>(sQ + row * LDQ + ChunkTile<T, DK, NT>::col(u)) = y;
       }
+      if (tid < NTO)
 #pragma unroll
-      for (int u = 0; u < ChunkTile<T, BVS, NT>::NV; ++u) {
-        const auto x = st.rdo.get(u);
-        const int c0 = ChunkTile<T, BVS, NT>::col(u);
+        for (int u = 0; u < ChunkTile<T, BVS, NTO>::NV; ++u) {
+          const auto x = st.rdo.get(u);
+          const int cc = ChunkTile<T, BVS, NTO>::col(u);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sdOT[(c0 + e) * LDP + row] = to<T>(a.scale * f32(x[e]));
-      }
+          for (int e = 0; e < 8; ++e) sdOT[(cc + e) * LDP + row] = to<T>(a.scale * f32(x[e]));
+        }
     }
     if (tid < C) {
 #pragma unroll
       for (int q = 0; q < 3; ++q) sCf[q][tid] = st.cf[q].get();
     }
     {  // D is the adjoint of the state leaving chunk ci
-      T* out = dst + (cidx * a.dv + v) * DK + 4 * g4;
+      T* out = dst + (cidx * a.dv + v) * DK + c0 + 4 * g4;
 #pragma unroll
       for (int tc = 0; tc < NCT; ++tc) store4(out + 16 * tc, D[tc][0], D[tc][1], D[tc][2], D[tc][3]);
     }
@@ -204,9 +213,25 @@ __global__ __launch_bounds__(64 * NPR, 1) void gdn_dstate_kernel(const GdnDstate
     for (int I = 0; I < 4; ++I) {
       dU[I] = zero4();
 #pragma unroll
-      for (int m = 0; m < NK; ++m) mma(dU[I], ld_frag_acc(sK + 16 * I * LDQ + 32 * m, (size_t)LDQ), df[m]);
-      dU[I] *= *reinterpret_cast<const f32x4*>(&sCf[0][16 * I + 4 * g4]);
+      for (int m = 0; m < NK; ++m)
+        mma(dU[I], ld_frag_acc(sK + 16 * I * LDQ + c0 + 32 * m, (size_t)LDQ), df[m]);
     }
+    if constexpr (NH > 1) {
+      // sum the NH partial products of this value tile, in a fixed order so
+      // every wave of the tile holds bit-identical X
+#pragma unroll
+      for (int I = 0; I < 4; ++I) sX[(w * 4 + I) * 64 + l] = dU[I];
+      lds_barrier();
+#pragma unroll
+      for (int I = 0; I < 4; ++I) {
+        f32x4 sum = sX[((pr * NH) * 4 + I) * 64 + l];
+#pragma unroll
+        for (int hh = 1; hh < NH; ++hh) sum += sX[((pr * NH + hh) * 4 + I) * 64 + l];
+        dU[I] = sum;
+      }
+    }
+#pragma unroll
+    for (int I = 0; I < 4; ++I) dU[I] *= *reinterpret_cast<const f32x4*>(&sCf[0][16 * I + 4 * g4]);
     // dU += PT dO'
     const Frag<T> of0 = ld_frag(sdOT + 16 * pr * LDP, LDP);
     const Frag<T> of1 = ld_frag(sdOT + 16 * pr * LDP + 32, LDP);
@@ -226,13 +251,14 @@ __global__ __launch_bounds__(64 * NPR, 1) void gdn_dstate_kernel(const GdnDstate
       mma(dR[I], ld_frag(sTT + 16 * I * LDP, LDP), uf0);
       mma(dR[I], ld_frag(sTT + 16 * I * LDP + 32, LDP), uf1);
     }
+    if (hq == 0)
 #pragma unroll
-    for (int I = 0; I < 4; ++I)
+      for (int I = 0; I < 4; ++I)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i = 16 * I + 4 * g4 + r;
-        if (i < nrow) dRrow[i * a.H * a.dv] = to<T>(dR[I][r]);
-      }
+        for (int r = 0; r < 4; ++r) {
+          const int i = 16 * I + 4 * g4 + r;
+          if (i < nrow) dRrow[i * a.H * a.dv] = to<T>(dR[I][r]);
+        }
     // D <- e^{gamma_C} D + (G Q)^T dO' - K^T diag(beta G) dR
 #pragma unroll
     for (int I = 0; I < 4; ++I) dR[I] *= -*reinterpret_cast<const f32x4*>(&sCf[1][16 * I + 4 * g4]);
@@ -242,10 +268,10 @@ __global__ __launch_bounds__(64 * NPR, 1) void gdn_dstate_kernel(const GdnDstate
 #pragma unroll
     for (int tc = 0; tc < NCT; ++tc) {
       D[tc] *= eC;
-      mma(D[tc], ld_frag_tr(sQ + 16 * tc, LDQ), of0);
-      mma(D[tc], ld_frag_tr(sQ + 32 * LDQ + 16 * tc, LDQ), of1);
-      mma(D[tc], ld_frag_tr_acc(sK + 16 * tc, LDQ), rf0);
-      mma(D[tc], ld_frag_tr_acc(sK + 32 * LDQ + 16 * tc, LDQ), rf1);
+      mma(D[tc], ld_frag_tr(sQ + c0 + 16 * tc, LDQ), of0);
+      mma(D[tc], ld_frag_tr(sQ + 32 * LDQ + c0 + 16 * tc, LDQ), of1);
+      mma(D[tc], ld_frag_tr_acc(sK + c0 + 16 * tc, LDQ), rf0);
+      mma(D[tc], ld_frag_tr_acc(sK + 32 * LDQ + c0 + 16 * tc, LDQ), rf1);
     }
   }
 }
@@ -576,19 +602,23 @@ hipError_t run_prep(const GdnPrepArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((gdn_bwd_prep_kernel<T, DK>), dim3(nblk), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
-template <typename T, int DK, int NPR>
+template <typename T, int DK, int NPR, int NH>
 hipError_t run_dstate_v(const GdnDstateArgs& a, hipStream_t st) {
   const int nblk = a.B * a.H * (a.dv / (16 * NPR));
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((gdn_dstate_kernel<T, DK, NPR>), dim3(nblk), dim3(64 * NPR), 0, st, a);
+  hipLaunchKernelGGL((gdn_dstate_kernel<T, DK, NPR, NH>), dim3(nblk), dim3(64 * NPR * NH), 0, st, a);
   return hipGetLastError();
 }
-// Four value tiles per workgroup where that still gives every compute unit a
-// workgroup, else two.
+// Value tiles per workgroup (4 or 2) and key split: with fewer value slices
+// than SIMDs the features of a slice are split over two waves (measured at
+// 512 slices of dk = 128: a two-way split takes 7% less time than a four-way
+// one, 17% less than none).
 template <typename T, int DK>
 hipError_t run_dstate(const GdnDstateArgs& a, hipStream_t st) {
-  if ((long long)a.B * a.H * (a.dv / 64) >= 256) return run_dstate_v<T, DK, 4>(a, st);
-  return run_dstate_v<T, DK, 2>(a, st);
+  const long long slices = (long long)a.B * a.H * (a.dv / 16);
+  if (slices >= 2048) return run_dstate_v<T, DK, 4, 1>(a, st);
+  if (slices >= 1024) return run_dstate_v<T, DK, 2, 1>(a, st);
+  return run_dstate_v<T, DK, 2, 2>(a, st);
 }
 template <typename T, int DK>
 hipError_t run_bwd_chunk(const GdnBwdArgs& a, hipStream_t st) {
