@@ -60,6 +60,9 @@ def gdn_group(w) -> int:
     the largest of 4, 2 that still gives 512 workgroups; 1 for training."""
     if getattr(w, "train", False):
         return 1
+    vpw = max(1, w.dv // 128)   # the output kernel carries S only where it fits the registers
+    if w.dk * vpw * (2 if w.dtype == __import__("torch").bfloat16 else 4) > 1024:
+        return 1
     nc = -(-w.T // CHUNK)
     for g in (4, 2):
         if w.B * w.H * -(-nc // g) >= 512:

@@ -359,7 +359,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   } else {
     ccq::GdnArgs da{k, v, beta, ws + L.Tm, gam, S0, ST, ws + L.states, ws + L.U, s->B, s->T, s->H,
                     s->dk, s->dv};
-    da.sstride = ccq::gdn_out_group(s->B, s->H, s->T);  // one state per output group
+    da.sstride = ccq::gdn_out_group(s->B, s->H, s->T, s->dk, s->dv, bf);  // one state per output group
     if (traced(ss, [&] { return ccq::launch_gdn_state(da, bf, ss); }) != hipSuccess) return CCQ_ERR_HIP;
   }
 
@@ -390,7 +390,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   } else {
     ccq::GdnOutArgs oa{qclean, k, gam, ws + L.states, ws + L.U, o, s->B, s->T, s->H, s->dk, s->dv,
                        s->scale};
-    oa.group = ccq::gdn_out_group(s->B, s->H, s->T);
+    oa.group = ccq::gdn_out_group(s->B, s->H, s->T, s->dk, s->dv, bf);
     if (traced(st, [&] { return ccq::launch_gdn_out(oa, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   }
   return CCQ_OK;

@@ -697,7 +697,7 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
 // the lane's entries of two pair-ordered accumulator tiles (tiles 2m, 2m + 1
 // of ld_frag_tr_acc_pair), so the update unpacks, accumulates and repacks in
 // place.
-template <typename T, int DK, int VPW, int IPW>
+template <typename T, int DK, int VPW, int IPW, bool CARRY>
 __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArgs a) {
   constexpr int C = kChunk;
   constexpr int P = Pad<T>::value;
@@ -714,7 +714,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
   __shared__ __align__(16) float sDd[C + 4];  // e^{gamma_C - gamma_j}; e^{gamma_C} at C
 
   const int N = (a.T + C - 1) / C;
-  const int R = a.group, NGR = (N + R - 1) / R;
+  const int R = CARRY ? a.group : 1, NGR = (N + R - 1) / R;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
   const int bh = lb / NGR, cb = (lb % NGR) * R, ce = min(N, cb + R);
   const int b = bh / a.H, h = bh % a.H;
@@ -728,7 +728,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
   for (int ci = cb; ci < ce; ++ci) {
     const int r0 = ci * C;
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-    const bool carry = ci + 1 < ce;
+    const bool carry = CARRY && ci + 1 < ce;
     {
       RowTile<T, DK, kOutThreads> rq, rk;
       rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
@@ -811,7 +811,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
       }
     }
 
-    if (carry) {
+    if constexpr (CARRY) if (carry) {
       // S_{r+1}^T = e^{gamma_C} S_r^T + K^T (diag(e^{gamma_C - gamma}) U): the
       // U^T fragments scaled per token (k slot 8 g4 + e is token 32 m + 4 g4 + e,
       // or + 16 for e >= 4), then per 32-feature block m the two pair-ordered
@@ -923,10 +923,12 @@ hipError_t run_gdn_state(const GdnArgs& a, hipStream_t st) {
 template <typename T, int DK, int VPW, int IPW>
 hipError_t run_gdn_out_v(const GdnOutArgs& a, hipStream_t st) {
   if (a.group < 1) return hipErrorInvalidValue;
+  constexpr bool kCarry = DK * VPW * (int)sizeof(T) <= 1024;  // as gdn_out_carries
+  if (!kCarry && a.group != 1) return hipErrorInvalidValue;
   const int N = (a.T + kChunk - 1) / kChunk;
   const int nblk = a.B * a.H * ((N + a.group - 1) / a.group);
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((gdn_out_kernel<T, DK, VPW, IPW>), dim3(nblk), dim3(kOutThreads), 0, st, a);
+  hipLaunchKernelGGL((gdn_out_kernel<T, DK, VPW, IPW, kCarry>), dim3(nblk), dim3(kOutThreads), 0, st, a);
   return hipGetLastError();
 }
 template <typename T, int DK>
@@ -941,14 +943,23 @@ hipError_t run_gdn_out(const GdnOutArgs& a, hipStream_t st) {
 }
 }  // namespace
 
-int gdn_out_group(int B, int H, int T) {
+int gdn_out_group(int B, int H, int T, int dk, int dv, bool is_bf16) {
   // the largest group (4 or 2 chunks) that still gives two workgroups per
-  // compute unit
+  // compute unit; none where a wave's share of S would not fit its registers
+  // beside the output's
+  if (!gdn_out_carries(dk, dv, is_bf16)) return 1;
   const long long bh = (long long)B * H;
   const int N = (T + kChunk - 1) / kChunk;
   for (int g = 4; g >= 2; g /= 2)
     if (bh * ((N + g - 1) / g) >= 512) return g;
   return 1;
+}
+
+bool gdn_out_carries(int dk, int dv, bool is_bf16) {
+  // a wave holds S for its value tiles (dv / 128 of them, at least one) and
+  // all dk features as operand fragments: up to 64 registers
+  const int vpw = dv / 128;
+  return dk * (vpw < 1 ? 1 : vpw) * (is_bf16 ? 2 : 4) <= 1024;
 }
 
 bool gdn_supported(int dk, int dv, bool is_bf16) {

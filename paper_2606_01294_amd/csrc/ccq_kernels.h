@@ -345,6 +345,8 @@ bool clean_supported(int dk, bool is_bf16);
 bool gla_supported(int dk, int dv, bool is_bf16);
 bool gdn_supported(int dk, int dv, bool is_bf16);
 // Chunks per output workgroup (and state stride) for a forward pass.
-int gdn_out_group(int B, int H, int T);
+int gdn_out_group(int B, int H, int T, int dk, int dv, bool is_bf16);
+// Whether the output kernel can carry S through a group at this shape.
+bool gdn_out_carries(int dk, int dv, bool is_bf16);
 
 }  // namespace ccq

@@ -128,6 +128,9 @@ GDN_GROUP_CASES = [
     (BF16, 16, 337, 16, 64, 64),   # 6 chunks, groups of 4: {0..3}, {4, 5}
     (BF16, 16, 150, 16, 64, 128),  # 3 chunks, groups of 2: {0, 1}, {2}
     (F32, 16, 337, 16, 64, 64),
+    (BF16, 16, 150, 16, 128, 512),  # four value tiles per wave, groups of 2
+    (F32, 16, 150, 16, 128, 256),
+    (BF16, 16, 150, 16, 256, 512),  # S too large to carry: one chunk per workgroup
 ]
 
 
