@@ -56,18 +56,20 @@ def clean_seg(bh: int, nc: int) -> int:
 
 
 def gdn_group(w) -> int:
-    """Chunks per Gated DeltaNet output workgroup (one stored state per group):
-    the largest of 4, 2 that still gives 512 workgroups; 1 for training."""
+    """Chunks per Gated DeltaNet output workgroup (one stored state per group), as
+    the library picks it; 1 for training."""
     if getattr(w, "train", False):
         return 1
     vpw = max(1, w.dv // 128)   # the output kernel carries S only where it fits the registers
     if w.dk * vpw * (2 if w.dtype == __import__("torch").bfloat16 else 4) > 1024:
         return 1
     nc = -(-w.T // CHUNK)
-    for g in (4, 2):
-        if w.B * w.H * -(-nc // g) >= 512:
-            return g
-    return 1
+    best, best_cost = 1, None
+    for g in (1, 2, 4, 8):   # rounds of 256 workgroups x (group + 1), the largest on a tie
+        cost = -(-(w.B * w.H * -(-nc // g)) // 256) * (g + 1)
+        if best_cost is None or cost <= best_cost:
+            best, best_cost = g, cost
+    return best
 
 
 def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):

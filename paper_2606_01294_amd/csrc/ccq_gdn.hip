@@ -944,15 +944,26 @@ hipError_t run_gdn_out(const GdnOutArgs& a, hipStream_t st) {
 }  // namespace
 
 int gdn_out_group(int B, int H, int T, int dk, int dv, bool is_bf16) {
-  // the largest group (4 or 2 chunks) that still gives two workgroups per
-  // compute unit; none where a wave's share of S would not fit its registers
-  // beside the output's
+  // One workgroup (a compute unit's worth) walks its group's chunks in order
+  // after reading one stored state, so the kernel takes about (rounds of 256
+  // workgroups) x (group + 1) chunk steps: the group of 8, 4, 2 or 1 chunks
+  // that minimises that, the largest on a tie (fewer stored states).  No
+  // groups where a wave's share of S would not fit its registers beside the
+  // output's.
   if (!gdn_out_carries(dk, dv, is_bf16)) return 1;
   const long long bh = (long long)B * H;
-  const int N = (T + kChunk - 1) / kChunk;
-  for (int g = 4; g >= 2; g /= 2)
-    if (bh * ((N + g - 1) / g) >= 512) return g;
-  return 1;
+  const long long N = (T + kChunk - 1) / kChunk;
+  int best = 1;
+  long long best_cost = -1;
+  for (int g = 1; g <= 8; g *= 2) {
+    const long long rounds = (bh * ((N + g - 1) / g) + 255) / 256;
+    const long long cost = rounds * (g + 1);
+    if (best_cost < 0 || cost <= best_cost) {
+      best_cost = cost;
+      best = g;
+    }
+  }
+  return best;
 }
 
 bool gdn_out_carries(int dk, int dv, bool is_bf16) {

@@ -120,15 +120,18 @@ def test_gdn_parity_state_splits(case):
 
 
 # With enough (batch, head) pairs the Gated DeltaNet output kernel takes
-# groups of 4 or 2 chunks per workgroup, carrying S from one stored state
-# through the group; these shapes reach both group sizes with a partial last
-# group and a ragged last chunk.
+# groups of chunks per workgroup, carrying S from one stored state through the
+# group (the group size follows from B * H and the chunk count); these shapes
+# reach groups of 8 (here all 6 chunks of a head, one partial group), 4 (3
+# chunks) and 2 (groups {0, 1} and {2}) with ragged last chunks, four value
+# tiles per wave with and without the carry, and fp32.  The full-size
+# workloads below add groups of 8 and 4 over many groups per head.
 GDN_GROUP_CASES = [
-    # dtype, B, T, H, dk, dv -> chunks, group
-    (BF16, 16, 337, 16, 64, 64),   # 6 chunks, groups of 4: {0..3}, {4, 5}
-    (BF16, 16, 150, 16, 64, 128),  # 3 chunks, groups of 2: {0, 1}, {2}
+    # dtype, B, T, H, dk, dv
+    (BF16, 16, 337, 16, 64, 64),    # 6 chunks, one group
+    (BF16, 8, 150, 16, 64, 128),    # 3 chunks, groups of 2
     (F32, 16, 337, 16, 64, 64),
-    (BF16, 16, 150, 16, 128, 512),  # four value tiles per wave, groups of 2
+    (BF16, 16, 150, 16, 128, 512),  # four value tiles per wave, one group of 3
     (F32, 16, 150, 16, 128, 256),
     (BF16, 16, 150, 16, 256, 512),  # S too large to carry: one chunk per workgroup
 ]
