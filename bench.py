@@ -38,9 +38,18 @@ CHUNK = 64
 
 def gla_seg(bh: int, nc: int, dk: int, dv: int) -> int:
     """Chunks per segment of the GLA state pass (the library's policy; 0 = one
-    segment): segments only when the unsegmented pass leaves SIMDs idle."""
-    waves = bh * (dk // 64) * (dv // 64) * 4
-    return 8 if (waves < 1024 and nc > 8) else 0
+    segment): the segment count minimising rounds of 512 workgroups x chunks per
+    segment (+2 for the scan when segmented), the fewest segments on a tie."""
+    tiles = bh * (dk // 64) * (dv // 64)
+    best_ns, best_cost = 1, None
+    for ns in range(1, min(64, nc) + 1):
+        sl = -(-nc // ns)
+        if -(-nc // sl) != ns or (ns > 1 and sl < 4):
+            continue
+        cost = -(-(tiles * ns) // 512) * sl + (2 if ns > 1 else 0)
+        if best_cost is None or cost < best_cost:
+            best_ns, best_cost = ns, cost
+    return -(-nc // best_ns) if best_ns > 1 else 0
 
 
 def clean_seg(bh: int, nc: int) -> int:

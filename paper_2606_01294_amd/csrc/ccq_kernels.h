@@ -306,11 +306,24 @@ hipError_t launch_gla_state(const GlaStateArgs& a, bool is_bf16, bool gate_bf16,
 hipError_t launch_gla_out(const GlaOutArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
 hipError_t launch_gla_scan(const GlaScanArgs& a, bool is_bf16, hipStream_t st);
 // Chunks per segment of the GLA state pass (0: one segment) for bh heads of
-// nc chunks: segments only when the unsegmented pass (four waves per 64 x 64
-// tile of S) would not give every SIMD of the chip a wave.
+// nc chunks.  A workgroup carries one 64 x (16 NVT) tile of S through its
+// segment's chunks, two workgroups per compute unit; the segments then meet
+// in a scan.  The segment count minimises rounds of 512 workgroups x chunks
+// per segment, plus two chunk steps for the scan when there is more than one
+// segment (of at least 4 chunks); the fewest segments on a tie.
 inline int gla_seg(long long bh, long long nc, int dk, int dv) {
-  const long long waves = bh * (dk / 64) * (dv / 64) * 4;
-  return (waves < 1024 && nc > 8) ? 8 : 0;
+  const long long tiles = bh * (dk / 64) * (dv / 64);
+  long long best_ns = 1, best_cost = -1;
+  for (long long ns = 1; ns <= 64 && ns <= nc; ++ns) {
+    const long long sl = (nc + ns - 1) / ns;
+    if ((nc + sl - 1) / sl != ns || (ns > 1 && sl < 4)) continue;  // ns segments of sl >= 4 chunks
+    const long long cost = ((tiles * ns + 511) / 512) * sl + (ns > 1 ? 2 : 0);
+    if (best_cost < 0 || cost < best_cost) {
+      best_cost = cost;
+      best_ns = ns;
+    }
+  }
+  return best_ns > 1 ? (int)((nc + best_ns - 1) / best_ns) : 0;
 }
 hipError_t launch_gdn_tri(const TriArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_gdn_state(const GdnArgs& a, bool is_bf16, hipStream_t st);
