@@ -48,7 +48,7 @@ extern "C" {
 typedef enum {
   CCQ_OK = 0,
   CCQ_ERR_INVALID_ARG = 1, /* NULL where a tensor is required, negative sizes, misalignment */
-  CCQ_ERR_UNSUPPORTED = 2, /* a head size, chunk or dtype this build has no kernel for */
+  CCQ_ERR_UNSUPPORTED = 2, /* a head size, chunk or dtype the library has no kernel for */
   CCQ_ERR_WORKSPACE = 3,   /* workspace NULL or smaller than ccq_workspace_size() */
   CCQ_ERR_HIP = 4          /* the HIP runtime reported an error at launch */
 } ccq_status;
