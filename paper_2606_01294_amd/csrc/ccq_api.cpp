@@ -296,11 +296,13 @@ ccq_status copy_initial_states(const ccq_shape* s, const float* S0, const float*
   return e == hipSuccess ? CCQ_OK : CCQ_ERR_HIP;
 }
 
+// cu: offsets of a packed batch laid out padded (the Gated DeltaNet chunk
+// transform, state pass and output then skip each sequence's padding), or null.
 ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const void* k,
                        const void* v, const void* g_or_la, const float* beta, const float* lam,
                        const float* S0, const float* C0, const float* mu0, void* o, float* ST,
                        float* CT, float* muT, float* q_clean_dbg, void* workspace,
-                       size_t ws_bytes, void* stream) {
+                       size_t ws_bytes, void* stream, const int32_t* cu = nullptr) {
   ccq_status rc = check_shape(s, bb);
   if (rc != CCQ_OK) return rc;
   const size_t ntok = (size_t)s->B * s->T * s->H;
@@ -331,6 +333,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   // starts as early as possible
   if (bb == CCQ_GDN) {
     ccq::TriArgs ta{k, la, beta, ws + L.Tm, gam, s->B, s->T, s->H, s->dk, s->dv};
+    ta.cu = cu;
     if (traced(st, [&] { return ccq::launch_gdn_tri(ta, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   }
   SideStream* sd = nullptr;
@@ -360,6 +363,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
     ccq::GdnArgs da{k, v, beta, ws + L.Tm, gam, S0, ST, ws + L.states, ws + L.U, s->B, s->T, s->H,
                     s->dk, s->dv};
     da.sstride = ccq::gdn_out_group(s->B, s->H, s->T, s->dk, s->dv, bf);  // one state per output group
+    da.cu = cu;
     if (traced(ss, [&] { return ccq::launch_gdn_state(da, bf, ss); }) != hipSuccess) return CCQ_ERR_HIP;
   }
 
@@ -391,6 +395,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
     ccq::GdnOutArgs oa{qclean, k, gam, ws + L.states, ws + L.U, o, s->B, s->T, s->H, s->dk, s->dv,
                        s->scale};
     oa.group = ccq::gdn_out_group(s->B, s->H, s->T, s->dk, s->dv, bf);
+    oa.cu = cu;
     if (traced(st, [&] { return ccq::launch_gdn_out(oa, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   }
   return CCQ_OK;
@@ -549,7 +554,7 @@ ccq_status varlen_forward(ccq_backbone bb, const ccq_shape* s, const int32_t* cu
   rc = run_forward(bb, s, ws + L.q, ws + L.k, ws + L.v, ws + L.gate,
                    bb == CCQ_GDN ? reinterpret_cast<const float*>(ws + L.beta) : nullptr,
                    reinterpret_cast<const float*>(ws + L.lam), S0, C0, mu0, ws + L.o, ST, CT, muT, nullptr,
-                   ws + L.inner, ws_bytes - L.inner, stream);
+                   ws + L.inner, ws_bytes - L.inner, stream, cu);
   if (rc != CCQ_OK) return rc;
   if (traced(st, [&] { return ccq::launch_varlen_copy(o, ws + L.o, cu, s->B, s->T, R.v, false, st); }) !=
       hipSuccess)

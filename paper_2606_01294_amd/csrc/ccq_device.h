@@ -602,6 +602,18 @@ __device__ __forceinline__ int frag_tr_pair_lane_off(int l, int ld) {
   else return 8 * g * ld + 8 * (j >> 2) + (j & 3);
 }
 
+// Chunks of sequence b that hold tokens.  Without offsets, all N chunks of the
+// [B, T] batch; with the offsets cu of a packed batch laid out padded (rows
+// past each sequence's end zero), ceil(len_b / 64) with len_b = cu[b+1] - cu[b]
+// clamped to [0, T]: the chunks past them hold only zero rows, which leave
+// every state unchanged, so the state and output passes may skip them.
+__device__ __forceinline__ int live_chunks(const int* cu, int b, int T, int N) {
+  if (!cu) return N;
+  int len = cu[b + 1] - cu[b];
+  len = len < 0 ? 0 : (len > T ? T : len);
+  return (len + kChunk - 1) / kChunk;
+}
+
 // Sum over aligned groups of n consecutive lanes (n = 2, 4, 8, 16), by
 // swizzles (no address registers).
 template <int N>

@@ -54,6 +54,7 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
   const int bh = lb / N, ci = lb % N;
   const int b = bh / a.H, h = bh % a.H;
+  if (ci >= live_chunks(a.cu, b, a.T, N)) return;  // padding of a packed batch: not read
   const int r0 = ci * C;
   const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
   const int tid = threadIdx.x, w = wave_id(), l = lane_id();
@@ -179,7 +180,11 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
   const int nvt = a.dv / BVS;
   const int N = (a.T + C - 1) / C;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int bh = lb / nvt;
+  // heads in head-major order: the workgroups of consecutive logical blocks
+  // (one compute-unit cluster) then hold one head of every sequence, which
+  // balances the clusters when a packed batch's sequences differ in length
+  const int hm = lb / nvt;
+  const int bh = (hm % a.B) * a.H + hm / a.B;
   const int tid = threadIdx.x, w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
   const int pr = w / NH, hq = w % NH;
@@ -188,6 +193,7 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
   const int v = v0 + vs;
   const int c0 = hq * DKH;          // first key feature of this wave
   const int b = bh / a.H, h = bh % a.H;
+  const int NL = live_chunks(a.cu, b, a.T, N);  // chunks walked (all but a packed batch's padding)
   const T* k = static_cast<const T*>(a.k);
   const T* vin = static_cast<const T*>(a.v);
   const T* Tg = static_cast<const T*>(a.Tm);
@@ -256,7 +262,7 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
       for (int q = 0; q < 4; ++q) sCf[buf][q][tid] = sg.cf[q].get();
     }
     if (ci > 0) write_back(ci - 1);
-    if (ci + 1 < N) prefetch(sg, ci + 1);
+    if (ci + 1 < NL) prefetch(sg, ci + 1);
     __syncthreads();
     const T* Kb = sK[buf];
 
@@ -350,10 +356,10 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
     }
   };
 
-  if (N > 0) prefetch(st, 0);
-  for (int ci = 0; ci < N; ++ci) step(st, ci);
+  if (NL > 0) prefetch(st, 0);
+  for (int ci = 0; ci < NL; ++ci) step(st, ci);
 
-  if (N > 0) write_back(N - 1);
+  if (NL > 0) write_back(NL - 1);
   if (a.ST) {
 #pragma unroll
     for (int tc = 0; tc < NCT; ++tc)
@@ -423,7 +429,11 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
   const int nvt = a.dv / BVS;
   const int N = (a.T + C - 1) / C;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int bh = lb / nvt;
+  // heads in head-major order: the workgroups of consecutive logical blocks
+  // (one compute-unit cluster) then hold one head of every sequence, which
+  // balances the clusters when a packed batch's sequences differ in length
+  const int hm = lb / nvt;
+  const int bh = (hm % a.B) * a.H + hm / a.B;
   const int l = lane_id(), g4 = l >> 4, c16 = l & 15;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int pr = w / NH, hq = w % NH;
@@ -431,6 +441,7 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
   const int v = v0 + 16 * pr + c16;
   const int c0 = hq * DKH;
   const int b = bh / a.H, h = bh % a.H;
+  const int NL = live_chunks(a.cu, b, a.T, N);  // chunks walked (all but a packed batch's padding)
   const T* k = static_cast<const T*>(a.k);
   const T* vin = static_cast<const T*>(a.v);
   const T* Tg = static_cast<const T*>(a.Tm);
@@ -484,13 +495,13 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
   // ci + 1, stores of ci - 1; two stages: stores of ci - 1)
   auto wait_chunk = [&](int ci) {
     int n = ci >= 1 ? nstore(ci - 1) : 0;
-    if constexpr (NSTAGE == 3) n += (ci >= 2 ? nstore(ci - 2) : 0) + (ci + 1 < N ? NIW : 0);
+    if constexpr (NSTAGE == 3) n += (ci >= 2 ? nstore(ci - 2) : 0) + (ci + 1 < NL ? NIW : 0);
     wait_vm_n(n);
   };
 
 #pragma unroll
   for (int s = 0; s < NSTAGE - 1; ++s)
-    if (s < N) issue(s);
+    if (s < NL) issue(s);
 
   // S^T[c][v] in pair order: c = c0 + pair_feat(tc, g4) + r, so that the
   // packed operand of tiles 2m, 2m + 1 holds 8 consecutive features per lane
@@ -508,7 +519,7 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
   T* st_base = static_cast<T*>(a.states) + (((size_t)vt * (DK / 32) + hq * NKH) * 16 + c16) * 32 + 8 * g4;
   T* u_base = static_cast<T*>(a.U) + ((size_t)vt * 2 * 16 + c16) * 32 + 8 * g4;
 
-  for (int ci = 0; ci < N; ++ci) {
+  for (int ci = 0; ci < NL; ++ci) {
     const char* sb = smem + (ci % NSTAGE) * SB;
     const char* Kb = sb;
     const T* Tb = reinterpret_cast<const T*>(sb + KB);
@@ -516,7 +527,7 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
     const float* Fb = reinterpret_cast<const float*>(sb + KB + TB + VB);
     wait_chunk(ci);
     lds_barrier();  // chunk ci visible; stage (ci - 1) % NSTAGE and the exchange area released
-    if (ci + NSTAGE - 1 < N) issue(ci + NSTAGE - 1);
+    if (ci + NSTAGE - 1 < NL) issue(ci + NSTAGE - 1);
 
     // P = K S_r^T over this wave's features: K rows 16 J + c16, features in
     // natural order (piece (c0 + 32 m) / 8 + g4, one 16-byte read)
@@ -716,8 +727,11 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
   const int N = (a.T + C - 1) / C;
   const int R = CARRY ? a.group : 1, NGR = (N + R - 1) / R;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int bh = lb / NGR, cb = (lb % NGR) * R, ce = min(N, cb + R);
+  const int hm = lb / NGR, cb = (lb % NGR) * R;
+  const int bh = (hm % a.B) * a.H + hm / a.B;  // head-major, as the state pass
   const int b = bh / a.H, h = bh % a.H;
+  const int ce = min(live_chunks(a.cu, b, a.T, N), cb + R);  // a packed batch's padding is skipped
+  if (cb >= ce) return;
   const int tid = threadIdx.x, w = tid >> 6, l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
   const int vg = w % NVG, ig = w / NVG;

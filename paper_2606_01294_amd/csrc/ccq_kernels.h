@@ -106,6 +106,7 @@ struct TriArgs {
                          // decay in the chunk), beta_j e^{gamma_j}, beta_j,
                          // e^{gamma_C - gamma_j}, e^{gamma_C}
   int B, T, H, dk, dv;
+  const int* cu = nullptr;  // packed-batch offsets [B+1] (device) or null: see live_chunks
 };
 
 // Gated DeltaNet state recurrence (sequential over chunks): writes the
@@ -125,6 +126,7 @@ struct GdnArgs {
                          // acc_pos order (fragment-native), every chunk
   int B, T, H, dk, dv;
   int sstride = 1;
+  const int* cu = nullptr;  // as TriArgs
 };
 
 // Gated DeltaNet output, one workgroup per group of `group` chunks (the
@@ -139,6 +141,7 @@ struct GdnOutArgs {
   int B, T, H, dk, dv;
   float scale;
   int group = 1;
+  const int* cu = nullptr;  // as TriArgs
 };
 
 // ---- training step (CCQ-GLA backward) ----
