@@ -154,7 +154,8 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
         by = ntok * (3 * dk * io_bytes + 5 * dv * io_bytes + 2 * dv * dk * io_bytes // C
                      + 12 * dk + 28)
         fl = ntok * (6 * dk * dv + 4 * C * dv + 12 * C * dk)
-    elif kernel == "decode":        # cache (S, Cbar fp32) read and written once, mu, q, k, v, gates, o
+    elif kernel in ("decode", "decode_split"):  # cache (S, Cbar fp32) read and written once,
+        # mu, q, k, v, gates, o
         gb = dk * gate_bytes if w.backbone == 0 else 8
         by = BH * (8 * dv * dk + 8 * dk * dk + dk * (2 * io_bytes + 20) + 2 * dv * io_bytes + gb + 4)
         fl = BH * (5 * dk * dk + 6 * dv * dk)
@@ -195,7 +196,7 @@ VARLEN_GDN = ["varlen_gather_qk", "varlen_gather_qk", "varlen_gather_v", "varlen
               "varlen_gather_scalar", "varlen_gather_scalar"] + KERNELS[1] + ["varlen_scatter_o", "varlen_fix"]
 KERNEL_SYMBOL = {"varlen_gather_qk": "varlen_copy_kernel", "varlen_gather_v": "varlen_copy_kernel",
                  "varlen_gather_scalar": "varlen_copy_kernel", "varlen_scatter_o": "varlen_copy_kernel",
-                 "varlen_fix": "varlen_cache_fix_kernel", "prep": "prep_kernel", "decode": "decode_stats_kernel+decode_out_kernel", "clean_gram": "clean_gram_kernel",
+                 "varlen_fix": "varlen_cache_fix_kernel", "prep": "prep_kernel", "decode": "decode_kernel", "decode_split": "decode_cbar_kernel+decode_s_kernel", "clean_gram": "clean_gram_kernel",
                  "clean_prefix": "clean_prefix_kernel", "clean_out": "clean_out_kernel",
                  "clean_out_train": "clean_out_kernel", "clean_dq": "clean_out_kernel",
                  "gla_state": "gla_state_kernel", "gla_scan": "gla_scan_kernel", "gla_out": "gla_out_kernel",
@@ -213,7 +214,7 @@ def _source(kernel: str) -> str:
         return "ccq_gla.hip"
     if kernel in ("gdn_bwd_prep", "gdn_dstate", "gdn_bwd_chunk"):
         return "ccq_gdn_bwd.hip"
-    if kernel == "decode":
+    if kernel.startswith("decode"):
         return "ccq_decode.hip"
     if kernel == "prep":
         return "ccq_prep.hip"
@@ -316,10 +317,12 @@ class DecodeCall:
         self.C = (torch.randn(B, H, dk, dk, generator=gen) / dk).to(dev)
         self.mu = (torch.randn(B, H, dk, generator=gen) / dk).to(dev)
         self.o = torch.empty((B, H, dv), dtype=w.dtype, device=dev)
-        self.ws = torch.empty(max(1, ccq.ccq_decode_workspace_size(
-            ccq.make_shape(B, 1, H, dk, dv, w.dtype))), dtype=torch.uint8, device=dev)
+        # the decode workspace is allocated once and kept, as a serving loop would
+        need = ccq.ccq_decode_workspace_size(ccq.make_shape(B, 1, H, dk, dv, w.dtype))
+        self.ws = torch.empty(max(1, need), dtype=torch.uint8, device=dev)
         self.ccq = ccq
-        self.kernels = ["decode"]
+        # a workspace is needed exactly when the step is split into two launches
+        self.kernels = ["decode_split" if need else "decode"]
 
     def __call__(self):
         d = self.d

@@ -138,8 +138,10 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
  * gate_dtype; Gated DeltaNet log alpha and beta [B,H] fp32 (beta NULL for GLA);
  * lam [B,H] fp32.  S [B,H,dv,dk], C [B,H,dk,dk] and mu [B,H,dk] are fp32,
  * caller-owned, read and overwritten.  Supported: dk in {64,128,256}, dv in
- * {64,128,256,512}, both backbones and both io dtypes.  The workspace holds
- * ccq_decode_workspace_size(s) bytes (0 for an unsupported shape).
+ * {64,128,256,512}, both backbones and both io dtypes.
+ * The workspace holds ccq_decode_workspace_size(s) bytes, B*H*dk*4 rounded
+ * up when the step is split into two launches (fewer than 256 heads of large
+ * caches), else 0, and workspace may then be NULL.
  */
 size_t ccq_decode_workspace_size(const ccq_shape* s);
 ccq_status ccq_decode(const ccq_shape* s, ccq_backbone bb, const void* q, const void* k,

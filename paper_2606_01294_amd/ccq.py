@@ -427,11 +427,11 @@ def ccq_decode(q, k, v, gate, lam, S, C, mu, t0, backbone=CCQ_GLA, beta=None, sc
     o = out if out is not None else torch.empty((B, H, dv), dtype=q.dtype, device=dev)
     _check(o, "o", (B, H, dv), q.dtype, dev)
     need = ccq_decode_workspace_size(shape)
-    if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
     rc = lib().ccq_decode(ctypes.byref(shape), int(backbone), _p(q), _p(k), _p(v), _p(gate),
                           _p(beta), _p(lam), _p(S), _p(C), _p(mu), _p(o), _p(workspace),
-                          workspace.numel(), _stream(stream))
+                          0 if workspace is None else workspace.numel(), _stream(stream))
     if rc != 0:
         raise CcqError("ccq_decode", rc)
     return o

@@ -741,9 +741,13 @@ ccq_status ccq_fwd_bwd_varlen(const ccq_shape* s, ccq_backbone bb, const int32_t
   return CCQ_OK;
 }
 
+// Decode workspace: Cbar_t q [B,H,dk] fp32 when the step is split into two
+// launches (a few large heads), else none.
 size_t ccq_decode_workspace_size(const ccq_shape* s) {
   if (!s || s->B < 0 || s->H < 0 || !ccq::decode_supported(s->dk, s->dv)) return 0;
-  return align_up((size_t)s->B * s->H * s->dk * sizeof(float));
+  const long long bh = (long long)s->B * s->H;
+  if (!ccq::decode_split(bh, s->dk, s->dv)) return 0;
+  return align_up((size_t)bh * s->dk * sizeof(float));
 }
 
 ccq_status ccq_decode(const ccq_shape* s, ccq_backbone bb, const void* q, const void* k,
@@ -756,16 +760,17 @@ ccq_status ccq_decode(const ccq_shape* s, ccq_backbone bb, const void* q, const 
   if (s->centered != 0 && s->centered != 1) return CCQ_ERR_INVALID_ARG;
   if (bb != CCQ_GLA && bb != CCQ_GDN) return CCQ_ERR_INVALID_ARG;
   if (!ccq::decode_supported(s->dk, s->dv)) return CCQ_ERR_UNSUPPORTED;
-  if ((long long)s->B * s->H > 65535) return CCQ_ERR_UNSUPPORTED;  // grid y
+  if ((long long)s->B * s->H > 0x7fffffffLL) return CCQ_ERR_UNSUPPORTED;  // one workgroup per head
   if (s->B == 0 || s->H == 0) return CCQ_OK;
   const void* req[] = {q, k, v, g_or_logalpha, lam, S, C, mu, o};
   for (const void* p : req)
     if (!p || !aligned(p)) return CCQ_ERR_INVALID_ARG;
   if (bb == CCQ_GDN && (!beta || !aligned(beta))) return CCQ_ERR_INVALID_ARG;
-  if (!workspace || !aligned(workspace) || ws_bytes < ccq_decode_workspace_size(s))
-    return CCQ_ERR_WORKSPACE;
-  ccq::DecodeArgs a{q, k, v, g_or_logalpha, beta, lam, S, C, mu, static_cast<float*>(workspace), o,
-                    s->B, s->H, s->dk, s->dv, s->centered, s->scale, s->t0};
+  const size_t need = ccq_decode_workspace_size(s);
+  if (need && (!workspace || !aligned(workspace) || ws_bytes < need)) return CCQ_ERR_WORKSPACE;
+  ccq::DecodeArgs a{q, k, v, g_or_logalpha, beta, lam, S, C, mu,
+                    need ? static_cast<float*>(workspace) : nullptr,
+                    o, s->B, s->H, s->dk, s->dv, s->centered, s->scale, s->t0};
   hipStream_t st = static_cast<hipStream_t>(stream);
   trace_begin_call();
   if (traced(st, [&] {

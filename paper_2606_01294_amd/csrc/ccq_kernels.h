@@ -260,7 +260,7 @@ struct DecodeArgs {
   float* S;              // [B,H,dv,dk] fp32, in place
   float* C;              // [B,H,dk,dk] fp32 (Cbar), in place
   float* mu;             // [B,H,dk] fp32, in place
-  float* cq;             // [B,H,dk] fp32 workspace: Cbar_t q
+  float* cq;             // [B,H,dk] fp32 workspace: Cbar_t q (split step only)
   void* o;               // [B,H,dv] io
   int B, H, dk, dv;
   int centered;
@@ -343,6 +343,7 @@ hipError_t launch_gdn_dstate(const GdnDstateArgs& a, bool is_bf16, hipStream_t s
 hipError_t launch_gdn_bwd_chunk(const GdnBwdArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_decode(const DecodeArgs& a, bool gdn, bool is_bf16, bool gate_bf16, hipStream_t st);
 bool decode_supported(int dk, int dv);
+bool decode_split(long long bh, int dk, int dv);  // two launches over 16-row blocks (needs the workspace)
 hipError_t launch_prep(const PrepArgs& a, bool is_bf16, hipStream_t st);
 bool prep_supported(int H, int dk);
 

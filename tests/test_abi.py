@@ -132,15 +132,19 @@ def call_decode(s, bb=0, ws_bytes=1 << 30, ptr=FAKE, beta=None, ws_ptr=FAKE):
 
 
 def test_decode_entry_point_validation():
+    # six heads: the step is split into two launches that pass Cbar q through it
     s = shape(T=1, dk=256, dv=512)
-    assert ccq.ccq_decode_workspace_size(s) == 2 * 3 * 256 * 4
+    need = ccq.ccq_decode_workspace_size(s)
+    assert need == 6 * 256 * 4
+    # 256 heads have a workgroup each and need no workspace
+    assert ccq.ccq_decode_workspace_size(shape(B=64, H=4, T=1)) == 0
     assert ccq.ccq_decode_workspace_size(shape(T=1, dk=96)) == 0
     assert call_decode(shape(T=2)) == 1                      # one token per call
     assert call_decode(shape(T=1, dk=96)) == 2               # unsupported head size
     assert call_decode(shape(T=1), bb=1) == 1                # Gated DeltaNet needs beta
-    assert call_decode(shape(T=1), ws_ptr=None) == 3         # no workspace
-    assert call_decode(shape(T=1), ws_bytes=8) == 3          # workspace too small
     assert call_decode(shape(T=1), ptr=FAKE + 4) == 1        # misaligned tensor
+    assert call_decode(s, ws_ptr=None) == 3                  # no workspace
+    assert call_decode(s, ws_bytes=need - 4) == 3            # workspace too small
     assert call_decode(shape(B=0, T=1), ptr=0, ws_ptr=None) == 0
 
 

@@ -62,6 +62,12 @@ CASES = [
     (GDN, F32, 2, 2, 64, 128, "iso"),
     (GDN, BF16, 2, 2, 256, 256, "aniso"),
     (GDN, BF16, 1, 3, 128, 64, "meanshift"),
+    # S in several register batches (dk = 256, dv = 512), one short batch (dv = 64),
+    # and a narrow head with a tall S (dk = 64, dv = 512)
+    (GDN, BF16, 1, 2, 256, 512, "iso"),
+    (GDN, F32, 1, 2, 256, 64, "aniso"),
+    (GLA, F32, 1, 2, 64, 512, "aniso"),
+    (GLA, BF16, 2, 2, 256, 128, "iso"),
 ]
 
 
@@ -81,7 +87,10 @@ def test_decode_continues_a_prefix(case):
     S = torch.from_numpy(pre["ST"]).float().cuda()
     C = torch.from_numpy(pre["CT"]).float().cuda()
     mu = torch.from_numpy(pre["muT"]).float().cuda()
-    o = decode_steps(backbone, {k: v[:, P:] for k, v in d.items()}, S, C, mu, P, n)
+    # one workspace for all the steps, as a serving loop would keep
+    need = ccq.ccq_decode_workspace_size(ccq.make_shape(B, 1, H, dk, dv, dtype))
+    ws = torch.zeros(max(need, 1), dtype=torch.uint8, device="cuda")
+    o = decode_steps(backbone, {k: v[:, P:] for k, v in d.items()}, S, C, mu, P, n, workspace=ws)
     errs = {"o": nerr(o, full["o"][:, P:]), "S": nerr(np64(S), full["ST"]),
             "C": nerr(np64(C), full["CT"]), "mu": nerr(np64(mu), full["muT"])}
     say("  errors", errs)
