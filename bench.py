@@ -13,7 +13,7 @@ dominant kernel, per-workload figures (including T=20480, the GLA and Gated
 DeltaNet training steps and the one-token recurrent decode step on the cache)
 and the fp64 CPU oracle timed on a bounded sample of the same inputs.
 
-    python bench.py [--gpus 1] [--steps 40] [--warmup 5]
+    python bench.py [--gpus 1] [--steps 40] [--warmup 20]
 """
 from __future__ import annotations
 
@@ -556,7 +556,7 @@ def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=40)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip the per-workload figures")
     ap.add_argument("--only", metavar="WORKLOAD",
