@@ -138,6 +138,10 @@ def test_decode_entry_point_validation():
     assert need == 6 * 256 * 4
     # 256 heads have a workgroup each and need no workspace
     assert ccq.ccq_decode_workspace_size(shape(B=64, H=4, T=1)) == 0
+    # the two decode workloads: 32 GLA heads (dk = 128, dv = 256) keep a workgroup per
+    # head; 32 Gated DeltaNet heads of dk = dv = 256 take the two-launch split
+    assert ccq.ccq_decode_workspace_size(shape(B=8, H=4, T=1, dk=128, dv=256)) == 0
+    assert ccq.ccq_decode_workspace_size(shape(B=4, H=8, T=1, dk=256, dv=256)) == 32 * 256 * 4
     assert ccq.ccq_decode_workspace_size(shape(T=1, dk=96)) == 0
     assert call_decode(shape(T=2)) == 1                      # one token per call
     assert call_decode(shape(T=1, dk=96)) == 2               # unsupported head size
