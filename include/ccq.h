@@ -26,10 +26,13 @@
  *  * The library allocates and frees nothing.  Scratch comes from the caller's
  *    `workspace` of at least ccq_workspace_size() bytes (16-byte aligned).
  *  * Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
- *    stream).  Arguments are validated before anything is launched; on an
- *    error nothing is launched and nothing is written.  A failed launch
- *    returns CCQ_ERR_HIP.  Nothing aborts, nothing throws, nothing is kept
- *    between calls: concurrent calls on different workspaces are safe.
+ *    stream): every kernel of a call is launched on that stream, in order.
+ *    The library creates no streams or events.  Arguments are validated
+ *    before anything is launched; on an error nothing is launched and nothing
+ *    is written.  A failed launch returns CCQ_ERR_HIP.  Nothing aborts,
+ *    nothing throws, and nothing is kept between calls except the per-thread
+ *    setting of the timing hook ccq_trace_events (off unless a caller sets
+ *    it): concurrent calls on different workspaces are safe.
  *  * q and k are used as given (the caller applies any l2-normalisation, as
  *    Alg. 1 does before the cleaning lines).  NaN/Inf inputs propagate.
  *  * Statistics (Cbar, mu) and the backbone state are fp32 whatever io_dtype

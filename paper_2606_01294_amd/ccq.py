@@ -142,6 +142,21 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def _record(stream, *objs):
+    """Tensors the binding allocated on torch's current stream but handed to the
+    library on another stream `stream`: mark them as used there, so that the caching
+    allocator does not give their memory to a later allocation on the current stream
+    while the library's kernels on `stream` may still use it (the workspace is freed
+    when the call returns)."""
+    if stream is None:
+        return
+    for o in objs:
+        for t in (o.values() if isinstance(o, dict) else (o,)):
+            if isinstance(t, torch.Tensor) and t.is_cuda and \
+                    stream != torch.cuda.current_stream(t.device):
+                t.record_stream(stream)
+
+
 def _check(t, name, shape, dtype, device):
     if t is None:
         return
@@ -203,6 +218,7 @@ def _fwd(backbone, q, k, v, gate, lam, beta, S0, C0, mu0, scale, centered, t0, c
                                _p(out.get("ST")), _p(out.get("CT")), _p(out.get("muT")),
                                _p(out.get("qclean")), _p(workspace), workspace.numel(), st)
         fn = "ccq_gdn_fwd"
+    _record(stream, workspace, out)
     if rc != 0:
         raise CcqError(fn, rc)
     return out
@@ -262,6 +278,7 @@ def ccq_fwd_bwd(q, k, v, g, lam, dO, scale=1.0, centered=True, chunk=64, out=Non
                            _p(beta), _p(lam), _p(dO), _p(out["o"]), _p(out["dq"]),
                            _p(out["dk"]), _p(out["dv"]), _p(out["dg"]), _p(out.get("dbeta")),
                            _p(out["dlam"]), _p(workspace), workspace.numel(), _stream(stream))
+    _record(stream, workspace, out)
     if rc != 0:
         raise CcqError("ccq_fwd_bwd", rc)
     return out
@@ -330,6 +347,7 @@ def _varlen_fwd(backbone, q, k, v, gate, beta, lam, cu_seqlens, max_len, S0, C0,
                                       _p(out["o"]), _p(out.get("ST")), _p(out.get("CT")),
                                       _p(out.get("muT")), _p(workspace), workspace.numel(), st)
         fn = "ccq_gdn_fwd_varlen"
+    _record(stream, workspace, out)
     if rc != 0:
         raise CcqError(fn, rc)
     return out
@@ -389,6 +407,7 @@ def ccq_fwd_bwd_varlen(q, k, v, g, lam, dO, cu_seqlens, max_len, scale=1.0, cent
                                   _p(out["dq"]), _p(out["dk"]), _p(out["dv"]), _p(out["dg"]),
                                   _p(out.get("dbeta")), _p(out["dlam"]), _p(workspace),
                                   workspace.numel(), _stream(stream))
+    _record(stream, workspace, out)
     if rc != 0:
         raise CcqError("ccq_fwd_bwd_varlen", rc)
     return out
@@ -432,6 +451,7 @@ def ccq_decode(q, k, v, gate, lam, S, C, mu, t0, backbone=CCQ_GLA, beta=None, sc
     rc = lib().ccq_decode(ctypes.byref(shape), int(backbone), _p(q), _p(k), _p(v), _p(gate),
                           _p(beta), _p(lam), _p(S), _p(C), _p(mu), _p(o), _p(workspace),
                           0 if workspace is None else workspace.numel(), _stream(stream))
+    _record(stream, workspace, o)
     if rc != 0:
         raise CcqError("ccq_decode", rc)
     return o
@@ -454,6 +474,7 @@ def ccq_prep(q_raw, k_raw, w_lam, b_lam, out=None, stream=None):
     shape = make_shape(B, T, H, dk, dk, q_raw.dtype)
     rc = lib().ccq_prep(ctypes.byref(shape), _p(q_raw), _p(k_raw), _p(w_lam), _p(b_lam),
                         _p(out["q"]), _p(out["k"]), _p(out["lam"]), _stream(stream))
+    _record(stream, out)
     if rc != 0:
         raise CcqError("ccq_prep", rc)
     return out

@@ -43,51 +43,6 @@ hipError_t traced(hipStream_t st, F&& launch) {
   return e;
 }
 
-// A second stream per (host thread, device).  The backbone's state pass does
-// not read q_clean, so it runs on this stream concurrently with the query
-// contraction, which it barely competes with (a latency-bound sequential
-// loop next to chunk-parallel work); the caller's stream waits for it through
-// an event before the output kernel.  Created on first use with default
-// priority; lives as long as the thread.
-struct SideStream {
-  hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
-};
-constexpr int kMaxDevices = 64;
-thread_local SideStream g_side[kMaxDevices];
-
-hipError_t side_stream(SideStream** out) {
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-  SideStream& sd = g_side[dev];
-  if (!sd.s) {
-    SideStream n;
-    e = hipStreamCreateWithFlags(&n.s, hipStreamNonBlocking);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&n.fork, hipEventDisableTiming);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&n.join, hipEventDisableTiming);
-    if (e != hipSuccess) return e;
-    sd = n;
-  }
-  *out = &sd;
-  return hipSuccess;
-}
-
-// Make `side` start after everything already enqueued on `st`.
-hipError_t fork_to(const SideStream& sd, hipStream_t st) {
-  hipError_t e = hipEventRecord(sd.fork, st);
-  if (e == hipSuccess) e = hipStreamWaitEvent(sd.s, sd.fork, 0);
-  return e;
-}
-
-// Make `st` wait for everything enqueued on `side` so far.
-hipError_t join_from(const SideStream& sd, hipStream_t st) {
-  hipError_t e = hipEventRecord(sd.join, sd.s);
-  if (e == hipSuccess) e = hipStreamWaitEvent(st, sd.join, 0);
-  return e;
-}
-
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -328,19 +283,13 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   float* gam = reinterpret_cast<float*>(ws + L.gam);
   const bool gbf = s->gate_dtype == CCQ_BF16;
   trace_begin_call();
-  // Gated DeltaNet: the chunk transforms first, on the caller's stream with
-  // the whole chip, so that the sequential state pass (the longest branch)
-  // starts as early as possible
+  // the backbone's chunk transforms (Gated DeltaNet) and state pass: chunk-entry
+  // states S_r (and U)
   if (bb == CCQ_GDN) {
     ccq::TriArgs ta{k, la, beta, ws + L.Tm, gam, s->B, s->T, s->H, s->dk, s->dv};
     ta.cu = cu;
     if (traced(st, [&] { return ccq::launch_gdn_tri(ta, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   }
-  SideStream* sd = nullptr;
-  if (side_stream(&sd) != hipSuccess || fork_to(*sd, st) != hipSuccess) return CCQ_ERR_HIP;
-  hipStream_t ss = sd->s;
-
-  // side stream: the backbone's state pass (chunk-entry states S_r)
   if (bb == CCQ_GLA) {
     // segments of the state pass run in parallel; a scan over the segment
     // totals gives every segment's entry state and S_T
@@ -352,22 +301,22 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
       sa.segdec = reinterpret_cast<float*>(ws + L.segdec);
       sa.cdec = reinterpret_cast<float*>(ws + L.cdec);
     }
-    if (traced(ss, [&] { return ccq::launch_gla_state(sa, bf, gbf, ss); }) != hipSuccess) return CCQ_ERR_HIP;
+    if (traced(st, [&] { return ccq::launch_gla_state(sa, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
     if (L.gla_seg > 0) {
       const int nc = (s->T + 63) / 64;
       ccq::GlaScanArgs ga{sa.segsum, sa.segdec, ws + L.entries, ST, s->B, s->H, s->dk, s->dv,
                           (nc + L.gla_seg - 1) / L.gla_seg};
-      if (traced(ss, [&] { return ccq::launch_gla_scan(ga, bf, ss); }) != hipSuccess) return CCQ_ERR_HIP;
+      if (traced(st, [&] { return ccq::launch_gla_scan(ga, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
     }
   } else {
     ccq::GdnArgs da{k, v, beta, ws + L.Tm, gam, S0, ST, ws + L.states, ws + L.U, s->B, s->T, s->H,
                     s->dk, s->dv};
     da.sstride = ccq::gdn_out_group(s->B, s->H, s->T, s->dk, s->dv, bf);  // one state per output group
     da.cu = cu;
-    if (traced(ss, [&] { return ccq::launch_gdn_state(da, bf, ss); }) != hipSuccess) return CCQ_ERR_HIP;
+    if (traced(st, [&] { return ccq::launch_gdn_state(da, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   }
 
-  // caller's stream: the query contraction
+  // the query contraction
   ccq::CleanArgs ca = clean_args(s, ws, L.clean);
   ca.q = q;
   ca.k = k;
@@ -381,8 +330,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   if (run_clean_stats(ca, bf, st) != hipSuccess) return CCQ_ERR_HIP;
   if (traced(st, [&] { return ccq::launch_clean_out(ca, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
 
-  // both halves meet at the output kernel
-  if (join_from(*sd, st) != hipSuccess) return CCQ_ERR_HIP;
+  // outputs from q_clean and the chunk-entry states
   if (bb == CCQ_GLA) {
     ccq::GlaOutArgs oa{qclean, k, v, g_or_la, ws + L.states, o, s->B, s->T, s->H, s->dk, s->dv, s->scale};
     if (L.gla_seg > 0) {
