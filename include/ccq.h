@@ -108,6 +108,29 @@ ccq_status ccq_gdn_fwd(const ccq_shape* s, const void* q, const void* k, const v
                        size_t ws_bytes, void* stream);
 
 /*
+ * Allocation-free form of ccq_gdn_fwd, for callers that cannot allocate device
+ * memory or pass a workspace: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same arguments and results as
+ * ccq_gdn_fwd without the workspace: the kernels use a scratch array of
+ * CCQ_NOALLOC_SCRATCH_BYTES that the library holds in device memory, one copy
+ * per device, from the first call on that device until the process ends.  The
+ * call allocates nothing (no hipMalloc, hipFree or allocating library call).
+ * Shapes whose ccq_workspace_size(s, CCQ_GDN, 0) exceeds
+ * CCQ_NOALLOC_SCRATCH_BYTES return CCQ_ERR_WORKSPACE before anything is
+ * launched (at dk = dv = 256 that is about 10,000 token-heads, B*T*H, per call).
+ * All calls on one device share its scratch: calls that may overlap on one
+ * device (two streams, two host threads) race and must be ordered by the
+ * caller; calls ordered on one stream are safe.  The scratch keeps the last
+ * call's contents, and no call reads what an earlier call left there.
+ */
+#define CCQ_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+ccq_status ccq_gdn_fwd_noalloc(const ccq_shape* s, const void* q, const void* k, const void* v,
+                               const float* logalpha, const float* beta, const float* lam,
+                               const float* S0, const float* C0, const float* mu0, void* o,
+                               float* ST, float* CT, float* muT, float* q_clean_dbg,
+                               void* stream);
+
+/*
  * Training step: forward and the gradients of L = sum_t <dO_t, o_t> with
  * respect to q, k, v, the gates and lambda (fresh sequence: zero initial
  * states, t0 must be 0).

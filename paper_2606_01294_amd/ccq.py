@@ -22,7 +22,7 @@ CCQ_F32, CCQ_BF16 = 0, 1
 CCQ_GLA, CCQ_GDN = 0, 1
 _STATUS = {0: "CCQ_OK", 1: "CCQ_ERR_INVALID_ARG", 2: "CCQ_ERR_UNSUPPORTED",
            3: "CCQ_ERR_WORKSPACE", 4: "CCQ_ERR_HIP"}
-EXPORTS = ("ccq_workspace_size", "ccq_gla_fwd", "ccq_gdn_fwd", "ccq_fwd_bwd",
+EXPORTS = ("ccq_workspace_size", "ccq_gla_fwd", "ccq_gdn_fwd", "ccq_gdn_fwd_noalloc", "ccq_fwd_bwd",
            "ccq_varlen_workspace_size", "ccq_gla_fwd_varlen", "ccq_gdn_fwd_varlen",
            "ccq_fwd_bwd_varlen", "ccq_decode_workspace_size", "ccq_decode", "ccq_prep",
            "ccq_trace_events", "ccq_status_string", "ccq_version")
@@ -64,6 +64,8 @@ def lib() -> ctypes.CDLL:
             L.ccq_gla_fwd.restype = ctypes.c_int
             L.ccq_gdn_fwd.argtypes = [SP] + [P] * 15 + [S, P]
             L.ccq_gdn_fwd.restype = ctypes.c_int
+            L.ccq_gdn_fwd_noalloc.argtypes = [SP] + [P] * 15
+            L.ccq_gdn_fwd_noalloc.restype = ctypes.c_int
             L.ccq_fwd_bwd.argtypes = [SP, ctypes.c_int] + [P] * 15 + [S, P]
             L.ccq_fwd_bwd.restype = ctypes.c_int
             L.ccq_varlen_workspace_size.argtypes = [SP, ctypes.c_int, ctypes.c_int]
@@ -238,6 +240,48 @@ def ccq_gdn_fwd(q, k, v, logalpha, beta, lam, S0=None, C0=None, mu0=None, scale=
     """CCQ-Gated-DeltaNet chunkwise forward.  Returns dict o[, ST, CT, muT][, qclean]."""
     return _fwd(CCQ_GDN, q, k, v, logalpha, lam, beta, S0, C0, mu0, scale, centered, t0, chunk,
                 want_states, want_qclean, out, workspace, stream)
+
+
+# CCQ_NOALLOC_SCRATCH_BYTES of include/ccq.h
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def ccq_gdn_fwd_noalloc(q, k, v, logalpha, beta, lam, S0=None, C0=None, mu0=None, scale=1.0,
+                        centered=True, t0=0, chunk=64, want_states=True, want_qclean=False,
+                        out=None, stream=None):
+    """CCQ-Gated-DeltaNet forward without a workspace: the library's own per-device
+    scratch (CCQ_NOALLOC_SCRATCH_BYTES) serves the kernels.  The binding allocates
+    only the outputs it is not given; pass every output in `out` to allocate nothing.
+    Returns dict o[, ST, CT, muT][, qclean]."""
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    dev = q.device
+    shape = make_shape(B, T, H, dk, dv, q.dtype, q.dtype, scale, centered, t0, chunk)
+    _check(k, "k", (B, T, H, dk), q.dtype, dev)
+    _check(v, "v", (B, T, H, dv), q.dtype, dev)
+    _check(logalpha, "logalpha", (B, T, H), torch.float32, dev)
+    _check(beta, "beta", (B, T, H), torch.float32, dev)
+    _check(lam, "lam", (B, T, H), torch.float32, dev)
+    _check(S0, "S0", (B, H, dv, dk), torch.float32, dev)
+    _check(C0, "C0", (B, H, dk, dk), torch.float32, dev)
+    _check(mu0, "mu0", (B, H, dk), torch.float32, dev)
+    out = dict(out or {})
+    if "o" not in out:
+        out["o"] = torch.empty((B, T, H, dv), dtype=q.dtype, device=dev)
+    if want_states:
+        out.setdefault("ST", torch.empty((B, H, dv, dk), dtype=torch.float32, device=dev))
+        out.setdefault("CT", torch.empty((B, H, dk, dk), dtype=torch.float32, device=dev))
+        out.setdefault("muT", torch.empty((B, H, dk), dtype=torch.float32, device=dev))
+    if want_qclean:
+        out.setdefault("qclean", torch.empty((B, T, H, dk), dtype=torch.float32, device=dev))
+    rc = lib().ccq_gdn_fwd_noalloc(ctypes.byref(shape), _p(q), _p(k), _p(v), _p(logalpha),
+                                   _p(beta), _p(lam), _p(S0), _p(C0), _p(mu0), _p(out["o"]),
+                                   _p(out.get("ST")), _p(out.get("CT")), _p(out.get("muT")),
+                                   _p(out.get("qclean")), _stream(stream))
+    _record(stream, out)
+    if rc != 0:
+        raise CcqError("ccq_gdn_fwd_noalloc", rc)
+    return out
 
 
 def ccq_fwd_bwd(q, k, v, g, lam, dO, scale=1.0, centered=True, chunk=64, out=None,

@@ -3,9 +3,16 @@
 // launch, so an error return means nothing was enqueued.
 #include "ccq.h"
 
-#include <hip/hip_runtime_api.h>
+#include <hip/hip_runtime.h>
+
+#include <mutex>
 
 #include "ccq_kernels.h"
+
+// Scratch of the allocation-free forward (ccq_gdn_fwd_noalloc), one copy per
+// device; see scratch_on_current_device below.
+static constexpr size_t kScratchBytes = CCQ_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 namespace {
 
@@ -251,13 +258,12 @@ ccq_status copy_initial_states(const ccq_shape* s, const float* S0, const float*
   return e == hipSuccess ? CCQ_OK : CCQ_ERR_HIP;
 }
 
-// cu: offsets of a packed batch laid out padded (the Gated DeltaNet chunk
-// transform, state pass and output then skip each sequence's padding), or null.
-ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const void* k,
-                       const void* v, const void* g_or_la, const float* beta, const float* lam,
-                       const float* S0, const float* C0, const float* mu0, void* o, float* ST,
-                       float* CT, float* muT, float* q_clean_dbg, void* workspace,
-                       size_t ws_bytes, void* stream, const int32_t* cu = nullptr) {
+// Argument checks of the forward entry points (nothing is launched).
+ccq_status check_forward_args(ccq_backbone bb, const ccq_shape* s, const void* q, const void* k,
+                              const void* v, const void* g_or_la, const float* beta,
+                              const float* lam, const float* S0, const float* C0,
+                              const float* mu0, const void* o, const float* ST, const float* CT,
+                              const float* muT, const float* q_clean_dbg, const void* workspace) {
   ccq_status rc = check_shape(s, bb);
   if (rc != CCQ_OK) return rc;
   const size_t ntok = (size_t)s->B * s->T * s->H;
@@ -270,6 +276,19 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
       if (!p || !aligned(p)) return CCQ_ERR_INVALID_ARG;
     if (bb == CCQ_GDN && (!beta || !aligned(beta))) return CCQ_ERR_INVALID_ARG;
   }
+  return CCQ_OK;
+}
+
+// cu: offsets of a packed batch laid out padded (the Gated DeltaNet chunk
+// transform, state pass and output then skip each sequence's padding), or null.
+ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const void* k,
+                       const void* v, const void* g_or_la, const float* beta, const float* lam,
+                       const float* S0, const float* C0, const float* mu0, void* o, float* ST,
+                       float* CT, float* muT, float* q_clean_dbg, void* workspace,
+                       size_t ws_bytes, void* stream, const int32_t* cu = nullptr) {
+  ccq_status rc = check_forward_args(bb, s, q, k, v, g_or_la, beta, lam, S0, C0, mu0, o, ST, CT,
+                                     muT, q_clean_dbg, workspace);
+  if (rc != CCQ_OK) return rc;
   const FwdLayout L = fwd_layout(s, bb);
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (s->B == 0 || s->H == 0) return CCQ_OK;
@@ -515,6 +534,34 @@ ccq_status varlen_forward(ccq_backbone bb, const ccq_shape* s, const int32_t* cu
   return CCQ_OK;
 }
 
+// Scratch of the allocation-free forward (ccq_gdn_fwd_noalloc): a device array
+// of kScratchBytes, one copy on every device the library runs on, held until the
+// process ends.  In host code `scratch` names a host-side stand-in, not device
+// memory: its device address is looked up once per device with
+// hipGetSymbolAddress (with that device current) and only that address is
+// handed to kernels.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// Device address of the current device's scratch (looked up on its first use).
+hipError_t scratch_on_current_device(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
@@ -565,6 +612,26 @@ ccq_status ccq_gdn_fwd(const ccq_shape* s, const void* q, const void* k, const v
                        size_t ws_bytes, void* stream) {
   return run_forward(CCQ_GDN, s, q, k, v, logalpha, beta, lam, S0, C0, mu0, o, ST, CT, muT,
                      q_clean_dbg, workspace, ws_bytes, stream);
+}
+
+ccq_status ccq_gdn_fwd_noalloc(const ccq_shape* s, const void* q, const void* k, const void* v,
+                               const float* logalpha, const float* beta, const float* lam,
+                               const float* S0, const float* C0, const float* mu0, void* o,
+                               float* ST, float* CT, float* muT, float* q_clean_dbg,
+                               void* stream) {
+  ccq_status rc = check_forward_args(CCQ_GDN, s, q, k, v, logalpha, beta, lam, S0, C0, mu0, o,
+                                     ST, CT, muT, q_clean_dbg, nullptr);
+  if (rc != CCQ_OK) return rc;
+  // every buffer the kernels read is written first in the same call, so the
+  // previous call's contents need no clearing
+  if (fwd_layout(s, CCQ_GDN).total > kScratchBytes) return CCQ_ERR_WORKSPACE;
+  if (s->B == 0 || s->H == 0 || s->T == 0)  // no scratch needed
+    return run_forward(CCQ_GDN, s, q, k, v, logalpha, beta, lam, S0, C0, mu0, o, ST, CT, muT,
+                       q_clean_dbg, nullptr, 0, stream);
+  void* ws = nullptr;
+  if (scratch_on_current_device(&ws) != hipSuccess) return CCQ_ERR_HIP;
+  return run_forward(CCQ_GDN, s, q, k, v, logalpha, beta, lam, S0, C0, mu0, o, ST, CT, muT,
+                     q_clean_dbg, ws, kScratchBytes, stream);
 }
 
 ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const void* k,

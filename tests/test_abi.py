@@ -94,6 +94,26 @@ def test_gdn_requires_beta():
     assert rc == 1
 
 
+def call_gdn_noalloc(s, ptr=FAKE, beta_ptr=FAKE):
+    P = ctypes.c_void_p
+    return ccq.lib().ccq_gdn_fwd_noalloc(ctypes.byref(s) if s is not None else None, P(ptr),
+                                         P(ptr), P(ptr), P(ptr), P(beta_ptr), P(ptr), None, None,
+                                         None, P(ptr), None, None, None, None, None)
+
+
+def test_noalloc_validation_before_launch():
+    """The allocation-free forward validates like ccq_gdn_fwd, and a shape whose workspace
+    exceeds its scratch returns CCQ_ERR_WORKSPACE, all before any HIP call."""
+    assert call_gdn_noalloc(None) == 1
+    assert call_gdn_noalloc(shape(dk=96)) == 2
+    assert call_gdn_noalloc(shape(dk=256), beta_ptr=0) == 1
+    assert call_gdn_noalloc(shape(dk=256), ptr=FAKE + 4) == 1
+    big = shape(B=4, T=4096, H=8, dk=256, dv=256)
+    assert ccq.ccq_workspace_size(big, ccq.CCQ_GDN) > ccq.NOALLOC_SCRATCH_BYTES
+    assert call_gdn_noalloc(big) == 3
+    assert call_gdn_noalloc(shape(B=0, dk=256), ptr=0, beta_ptr=0) == 0
+
+
 def test_binding_rejects_wrong_dtype_before_calling():
     import torch
     q = torch.zeros(1, 4, 1, 64)
