@@ -183,6 +183,76 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     return by, fl
 
 
+def method_cost(w, io_bytes=None, gate_bytes=None):
+    """Algorithmic (bytes, flops) of the method itself on workload w, per forward call
+    (the work the call must do, whatever the kernels): per token and head
+      F_CCQ = 4 dk^2 + 4 C dk                               (statistics and contraction)
+      F_GLA = 2 C (dk + dv) + 4 dk dv                       (chunk read and write)
+      F_GDN = 6 C dk + 4 C dv + 6 dk dv + C^2 / 3           (WY/UT transform, read, write)
+    with the C x C blocks counted dense; bytes = q, k, v, o, the gates and lambda read or
+    written once, plus the final (S, Cbar, mu) in fp32.  A training step counts three
+    times the forward flops (the backward taken as twice the forward) and also reads dO
+    and writes dq, dk, dv, the gate gradients and dlambda once."""
+    import torch
+    io_bytes = io_bytes or (2 if w.dtype == torch.bfloat16 else 4)
+    gate_bytes = gate_bytes or io_bytes
+    BH = w.B * w.H
+    n = getattr(w, "packed_rows", w.B * w.T) * w.H   # a packed batch: its real tokens only
+    dk, dv, C = w.dk, w.dv, CHUNK
+    f = 4 * dk * dk + 4 * C * dk
+    if w.backbone == 0:
+        f += 2 * C * (dk + dv) + 4 * dk * dv
+        gates = dk * gate_bytes
+    else:
+        f += 6 * C * dk + 4 * C * dv + 6 * dk * dv + C * C / 3
+        gates = 8
+    tok = (2 * dk + 2 * dv) * io_bytes + gates + 4
+    states = BH * (dv * dk + dk * dk + dk) * 4
+    if getattr(w, "train", False):
+        return n * (2 * tok + 4) + states, 3 * f * n
+    return n * tok + states, f * n
+
+
+def method_roofline(w, ms, traffic=None):
+    """Roofline of one whole call (all of its kernels) on the method's own work: the
+    bound is whichever of flops / MFMA peak and bytes / HBM peak is longer; `achieved`
+    is that work over the measured call time; `traffic` the rocprofv3 HBM bytes summed
+    over the call's kernels (None when any is missing or stale)."""
+    by, fl = method_cost(w)
+    sec = ms * 1e-3
+    t_mfma = fl / (PEAK_BF16_TFLOPS * 1e12)
+    t_hbm = by / (PEAK_HBM_GBS * 1e9)
+    if t_mfma >= t_hbm:
+        ach = fl / sec / 1e12
+        r = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
+             "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4)}
+    else:
+        ach = by / sec / 1e9
+        r = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+             "frac": round(ach / PEAK_HBM_GBS, 4)}
+    r["traffic"] = traffic
+    r["traffic_ratio"] = round(traffic / by, 3) if traffic else None
+    r["method_bytes"] = by
+    r["method_flops"] = int(fl)
+    r["roofline_us"] = round(max(t_mfma, t_hbm) * 1e6, 2)
+    r["ms_per_call"] = round(ms, 5)
+    r["mfma_frac"] = round(fl / sec / 1e12 / PEAK_BF16_TFLOPS, 4)
+    r["hbm_frac"] = round(by / sec / 1e9 / PEAK_HBM_GBS, 4)
+    return r
+
+
+def call_traffic(kernels, workload):
+    """rocprofv3 HBM bytes of one call: the committed per-kernel counter figures summed,
+    or None when any kernel's figure is missing or stale."""
+    tot = 0
+    for k in kernels:
+        t = measured_traffic(k, workload)
+        if t is None:
+            return None
+        tot += t
+    return tot
+
+
 CLEAN = ["clean_gram", "clean_prefix"]
 KERNELS = {0: ["gla_state"] + CLEAN + ["clean_out", "gla_out"],
            "gla_seg": ["gla_state", "gla_scan"] + CLEAN + ["clean_out", "gla_out"],
@@ -394,8 +464,10 @@ def time_calls(torch, ccq, calls, steps, warmup, with_plain=False):
     """Warm up, then time exactly `steps` steps (each step = every call once) between two
     synchronisations; per-kernel durations come from HIP events the library records on
     its stream around each of its launches.  With with_plain, exactly `steps` more steps
-    are timed first without those events (the event records add dispatch gaps of their
-    own), and that time is returned as well."""
+    are timed first without any events (the event records add dispatch gaps of their
+    own), and that time is returned as well, then `steps` more with one pair of events
+    around each whole call (every launch of a call is on torch's current stream), whose
+    mean durations are stored as `ms_call` on each call."""
     for _ in range(warmup):
         for c in calls:
             c()
@@ -410,6 +482,16 @@ def time_calls(torch, ccq, calls, steps, warmup, with_plain=False):
         end.record()
         torch.cuda.synchronize()
         ms_plain = start.elapsed_time(end) / steps
+        cev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                for _ in calls] for _ in range(steps)]
+        for i in range(steps):
+            for j, c in enumerate(calls):
+                cev[i][j][0].record()
+                c()
+                cev[i][j][1].record()
+        torch.cuda.synchronize()
+        for j, c in enumerate(calls):
+            c.ms_call = sum(cev[i][j][0].elapsed_time(cev[i][j][1]) for i in range(steps)) / steps
     ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2 * len(c.kernels))]
            for c in calls] for _ in range(steps)]
     for step_ev in ev:
@@ -491,7 +573,8 @@ def measure_extra(name, torch, ccq, inputs, steps, existing):
                "ms_traced": round(ms_tr, 4), "sequences": len(c.lens),
                "packed_tokens": sum(c.lens), "padded_tokens": c.w.B * c.w.T,
                "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
-               "roofline": roofline(dom, c.w)}
+               "roofline": method_roofline(c.w, c.ms_call),
+               "dominant_kernel": roofline(dom, c.w)}
     elif "_decode_" in name:
         c = DecodeCall(W[name.replace("_decode_t", "_t")], torch, ccq, inputs)
         ms, ms_tr, pk = time_calls(torch, ccq, [c], max(20, steps), 5, with_plain=True)
@@ -502,54 +585,51 @@ def measure_extra(name, torch, ccq, inputs, steps, existing):
     else:
         c = existing.get(name) or Call(W[name], torch, ccq, inputs)
         ms, ms_tr, pk = time_calls(torch, ccq, [c], max(5, steps // 2), 3, with_plain=True)
-        fl = sum(kernel_cost(e["kernel"], c.w)[1] for e in pk)
         dom = max(pk, key=lambda e: e["ms_mean"])
         res = {"tokens_per_s": round(c.w.tokens / (ms * 1e-3), 1), "ms": round(ms, 4),
                "ms_traced": round(ms_tr, 4),
-               "mfma_frac": round(fl / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
                "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
-               "roofline": roofline(dom, c.w)}
+               "roofline": method_roofline(c.w, c.ms_call, call_traffic(c.kernels, c.w.name)),
+               "dominant_kernel": roofline(dom, c.w)}
     if name not in existing:
         del c
         torch.cuda.empty_cache()
     return res
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(calls):
-    """The fp64 oracle on the host cores, on the first n (batch, head) sequences of each
-    workload (n = min(oracle threads, B*H)), scaled to the whole step by the number of
-    sequence waves."""
+    """The fp64 oracle on the host cores (OpenMP over the (batch, head) sequences), run on
+    the whole step: every sequence of every workload of the step, on the same inputs."""
     from oracle import ccq_oracle as O
-    import numpy as np
 
     thr = O.threads()
     total = 0.0
     parts = []
-    used = 1
     for c in calls:
         w = c.w
-        nseq = w.B * w.H
-        n = min(thr, nseq)
-        used = max(used, n)
-        pairs = [(b, h) for b in range(w.B) for h in range(w.H)][:n]
-
-        def pick(t):
-            a = t.double().numpy()
-            return np.ascontiguousarray(np.stack([a[b, :, h] for b, h in pairs])[:, :, None])
-
-        d = {k: pick(v) for k, v in c.cpu.items()}
+        d = {k: v.double().numpy() for k, v in c.cpu.items()}
         t0 = time.perf_counter()
         if w.backbone == 0:
             O.fwd(d["q"], d["k"], d["v"], d["g"], d["lam"], backbone=O.GLA)
         else:
             O.fwd(d["q"], d["k"], d["v"], d["logalpha"], d["lam"], beta=d["beta"], backbone=O.GDN)
         dt = time.perf_counter() - t0
-        total += dt * math.ceil(nseq / n)
-        parts.append("%s: %d of %d sequences in %.2f s" % (w.name, n, nseq, dt))
+        total += dt
+        parts.append("%s: all %d sequences in %.2f s" % (w.name, w.B * w.H, dt))
     tokens = sum(c.w.tokens for c in calls)
-    return {"value": round(tokens / total, 1), "unit": "tokens/s", "cores": used,
-            "kind": "oracle",
-            "sample": "; ".join(parts) + "; whole-step time = sample time x ceil(B*H / n)"}
+    return {"value": round(tokens / total, 1), "unit": "tokens/s", "cores": thr,
+            "kind": "oracle", "cpu_model": cpu_model(), "nproc": os.cpu_count(),
+            "sample": "the whole step (no extrapolation): " + "; ".join(parts)}
 
 
 def main(argv=None):
@@ -604,10 +684,17 @@ def main(argv=None):
     value = tokens / (ms_step * 1e-3)
 
     wl = {c.w.name: c.w for c in step_calls}
+    # the roofline of the call that dominates the step, on the method's own work
+    dom_call = max(step_calls, key=lambda c: c.ms_call)
+    roof = method_roofline(dom_call.w, dom_call.ms_call, call_traffic(dom_call.kernels, dom_call.w.name))
+    roof = dict({"kernel": "ccq_%s_fwd" % ("gla" if dom_call.w.backbone == 0 else "gdn"),
+                 "scope": "one whole forward call (%d launches: %s)" % (
+                     len(dom_call.kernels), ", ".join(dom_call.kernels)),
+                 "workload": dom_call.w.name}, **roof)
     dominant = max(per_kernel, key=lambda e: e["ms_mean"])
-    roof = roofline(dominant, wl[dominant["workload"]])
-    step_flops = sum(kernel_cost(e["kernel"], wl[e["workload"]])[1] for e in per_kernel)
-    step_bytes = sum(kernel_cost(e["kernel"], wl[e["workload"]])[0] for e in per_kernel)
+    step_roof_us = sum(method_roofline(c.w, c.ms_call)["roofline_us"] for c in step_calls)
+    step_bytes = sum(method_cost(c.w)[0] for c in step_calls)
+    step_flops = sum(method_cost(c.w)[1] for c in step_calls)
     kernels = []
     for e in per_kernel:
         by, fl = kernel_cost(e["kernel"], wl[e["workload"]])
@@ -645,6 +732,10 @@ def main(argv=None):
         "mfma_frac": round(step_flops / (ms_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "hbm_frac": round(step_bytes / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
         "roofline": roof,
+        "step_roofline": {"roofline_us": round(step_roof_us, 2),
+                          "frac": round(step_roof_us * 1e-3 / ms_step, 4),
+                          "calls_ms": {c.w.name: round(c.ms_call, 5) for c in step_calls}},
+        "dominant_kernel": roofline(dominant, wl[dominant["workload"]]),
         "kernels": kernels,
         "cpu_baseline": cpu,
         "extra": extra,
