@@ -144,7 +144,8 @@ ccq_status ccq_gdn_fwd_noalloc(const ccq_shape* s, const void* q, const void* k,
  *   dO [B,T,H,dv] io_dtype upstream gradient; o, dq, dk, dv io_dtype;
  *   dlam [B,T,H] fp32.
  * Supported: chunk = 64, dv in {64,128,256,512}, and dk in {64,128} for bf16
- * io or dk = 64 for fp32 io; other shapes return CCQ_ERR_UNSUPPORTED.
+ * io (also 256 for CCQ_GDN) or dk = 64 for fp32 io; other shapes return
+ * CCQ_ERR_UNSUPPORTED.
  */
 ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const void* k,
                        const void* v, const void* g_or_logalpha, const float* beta,

@@ -568,7 +568,7 @@ extern "C" {
 
 size_t ccq_varlen_workspace_size(const ccq_shape* s, ccq_backbone bb, int with_bwd) {
   if (check_shape(s, bb) != CCQ_OK) return 0;
-  if (with_bwd && !ccq::bwd_supported(s->dk, s->dv, s->io_dtype == CCQ_BF16)) return 0;
+  if (with_bwd && !ccq::bwd_supported(s->dk, s->dv, s->io_dtype == CCQ_BF16, bb == CCQ_GDN)) return 0;
   return varlen_layout(s, bb, with_bwd != 0).total;
 }
 
@@ -591,7 +591,7 @@ ccq_status ccq_gdn_fwd_varlen(const ccq_shape* s, const int32_t* cu_seqlens, con
 size_t ccq_workspace_size(const ccq_shape* s, ccq_backbone bb, int with_bwd) {
   if (check_shape(s, bb) != CCQ_OK) return 0;
   if (with_bwd) {
-    if (!ccq::bwd_supported(s->dk, s->dv, s->io_dtype == CCQ_BF16)) return 0;
+    if (!ccq::bwd_supported(s->dk, s->dv, s->io_dtype == CCQ_BF16, bb == CCQ_GDN)) return 0;
     return bb == CCQ_GLA ? bwd_layout(s).total : gdn_bwd_layout(s).total;
   }
   return fwd_layout(s, bb).total;
@@ -644,7 +644,7 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
   if (s->t0 != 0) return CCQ_ERR_INVALID_ARG;     // a training step starts from zero states
   const bool bf = s->io_dtype == CCQ_BF16;
   const bool gbf = s->gate_dtype == CCQ_BF16;
-  if (!ccq::bwd_supported(s->dk, s->dv, bf)) return CCQ_ERR_UNSUPPORTED;
+  if (!ccq::bwd_supported(s->dk, s->dv, bf, bb == CCQ_GDN)) return CCQ_ERR_UNSUPPORTED;
   const size_t ntok = (size_t)s->B * s->T * s->H;
   if (workspace && !aligned(workspace)) return CCQ_ERR_INVALID_ARG;
   if (ntok > 0) {
@@ -721,7 +721,7 @@ ccq_status ccq_fwd_bwd_varlen(const ccq_shape* s, ccq_backbone bb, const int32_t
   ccq_status rc = check_varlen(s, bb, cu_seqlens);
   if (rc != CCQ_OK) return rc;
   if (s->t0 != 0) return CCQ_ERR_INVALID_ARG;
-  if (!ccq::bwd_supported(s->dk, s->dv, s->io_dtype == CCQ_BF16)) return CCQ_ERR_UNSUPPORTED;
+  if (!ccq::bwd_supported(s->dk, s->dv, s->io_dtype == CCQ_BF16, bb == CCQ_GDN)) return CCQ_ERR_UNSUPPORTED;
   if (workspace && !aligned(workspace)) return CCQ_ERR_INVALID_ARG;
   if ((size_t)s->B * s->T * s->H == 0) return CCQ_OK;
   const void* req[] = {q, k, v, g_or_logalpha, lam, dO, o, dq, dk, dv, dg_or_dlogalpha, dlam};

@@ -353,13 +353,15 @@ __global__ __launch_bounds__(kThreads) void gla_dg_kernel(const DgArgs a) {
 // `seg`: ccq_dk_stats_kernel forms every segment's H and D and every chunk's
 // D (one workgroup per segment, all segments in parallel), and
 // ccq_dk_kernel starts each segment from the sum over the later segments and
-// walks the segment's chunks from last to first.
-template <typename T, int DK>
+// walks the segment's chunks from last to first.  For large DK the 16 x 16
+// tiles of H (and the output columns of ccq_dk_kernel) are split over NSPLIT
+// workgroups per segment (blockIdx.y); each stages the whole chunk.
+template <typename T, int DK, int NSPLIT>
 __global__ __launch_bounds__(kThreads, 1) void ccq_dk_stats_kernel(const CcqDkArgs a) {
   constexpr int C = kChunk;
   constexpr int P = Pad<T>::value;
   constexpr int LDT = C + P;
-  constexpr int NT16 = DK / 16, NPW = NT16 * NT16 / 4;
+  constexpr int NT16 = DK / 16, NPW = NT16 * NT16 / (4 * NSPLIT);
   constexpr int NPART = kThreads / DK;
   static_assert(NPW >= 1 && kThreads % DK == 0, "tile split");
 
@@ -375,6 +377,8 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_stats_kernel(const CcqDkAr
   const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
+  const int split = NSPLIT > 1 ? (int)blockIdx.y : 0;  // this workgroup's share of the tiles
+  const int tw0 = (split * (kThreads / 64) + w) * NPW;  // first tile of this wave
   const T* q = static_cast<const T*>(a.q);
   const T* uu = static_cast<const T*>(a.u);
   const size_t gs = (size_t)a.H * DK;
@@ -424,11 +428,11 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_stats_kernel(const CcqDkAr
     lds_barrier();
 #pragma unroll
     for (int u = 0; u < NPW; ++u) {
-      const int tau = w * NPW + u, tr = tau / NT16, tc = tau % NT16;
+      const int tau = tw0 + u, tr = tau / NT16, tc = tau % NT16;
       tile_mma<T, C>(H[u], sRUT + 16 * tr * LDT, LDT, sQT + 16 * tc * LDT, LDT);
       tile_mma<T, C>(H[u], sQT + 16 * tr * LDT, LDT, sRUT + 16 * tc * LDT, LDT);
     }
-    {  // this chunk's mean-term vector, NPART threads per key channel
+    if (split == 0) {  // this chunk's mean-term vector, NPART threads per key channel
       const int n = tid % DK, part = tid / DK;
       float x = 0.f;
 #pragma unroll 8
@@ -437,7 +441,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_stats_kernel(const CcqDkAr
       sDp[tid] = x;
     }
     lds_barrier();
-    if (tid < DK) {
+    if (split == 0 && tid < DK) {
       float x = sDp[tid];
 #pragma unroll
       for (int p2 = 1; p2 < NPART; ++p2) x += sDp[p2 * DK + tid];
@@ -448,11 +452,11 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_stats_kernel(const CcqDkAr
   float* hs = a.hseg + ((size_t)bh * NS + sg) * DK * DK;
 #pragma unroll
   for (int u = 0; u < NPW; ++u) {
-    const int tau = w * NPW + u, tr = tau / NT16, tc = tau % NT16;
+    const int tau = tw0 + u, tr = tau / NT16, tc = tau % NT16;
 #pragma unroll
     for (int r = 0; r < 4; ++r) hs[(size_t)(16 * tr + 4 * g4 + r) * DK + 16 * tc + c16] = H[u][r];
   }
-  if (tid < DK) a.dseg[((size_t)bh * NS + sg) * DK + tid] = dsum;
+  if (split == 0 && tid < DK) a.dseg[((size_t)bh * NS + sg) * DK + tid] = dsum;
 }
 
 // In place, per head: segment s's H and D become the sums over the later
@@ -487,19 +491,25 @@ __global__ __launch_bounds__(kThreads) void ccq_dk_suffix_kernel(const CcqDkArgs
 //   dk_j = H k_j + D + sum_{t>=j} (W1[t][j] rho_t u_t + W2[t][j] q_t),
 // then H += sum_t rho_t (u_t q_t^T + q_t u_t^T) and D += the chunk's D.  For
 // bf16, H and the weights W enter the products as a bf16 head plus a bf16 tail.
-template <typename T, int DK>
+// The output columns are split over NSPLIT workgroups per segment (blockIdx.y).
+// Without the row-major copies of q and u (kRowQU false, DK = 256, where they
+// would not fit in LDS beside the rest), the intra weights read q and rho u
+// from their transposed tiles with transposing LDS reads.
+template <typename T, int DK, int NSPLIT>
 __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) {
   constexpr int C = kChunk;
   constexpr int P = Pad<T>::value;
   constexpr bool kSplit = sizeof(T) == 2;
+  constexpr bool kRowQU = DK <= 128;
   constexpr int LDQ = DK + P, LDT = C + P, LDA = C + P;
   constexpr int NCT = DK / 16;  // 16-row tiles of the contraction index c
-  constexpr int NTW = DK / 64;  // output column tiles per wave
+  constexpr int NTW = DK / (64 * NSPLIT);  // output column tiles per wave
   constexpr int NK = DK / 32;
   static_assert(NTW >= 1, "column split");
+  static_assert(kRowQU || sizeof(T) == 2, "transposing reads are bf16 only");
 
-  __shared__ __align__(16) T sQ[C * LDQ];
-  __shared__ __align__(16) T sU[C * LDQ];
+  __shared__ __align__(16) T sQ[kRowQU ? C * LDQ : 8];
+  __shared__ __align__(16) T sU[kRowQU ? C * LDQ : 8];
   __shared__ __align__(16) T sK[C * LDQ];
   __shared__ __align__(16) T sQT[DK * LDT];
   __shared__ __align__(16) T sRUT[DK * LDT];  // (rho u)^T
@@ -516,6 +526,8 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
   const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
+  const int split = NSPLIT > 1 ? (int)blockIdx.y : 0;
+  const int nt0 = (split * (kThreads / 64) + w) * NTW;  // first output column tile of this wave
   const T* q = static_cast<const T*>(a.q);
   const T* k = static_cast<const T*>(a.k);
   const T* uu = static_cast<const T*>(a.u);
@@ -547,7 +559,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
     const float* hs = a.hseg + ((size_t)bh * NS + sg) * DK * DK;
 #pragma unroll
     for (int x = 0; x < NTW; ++x) {
-      const int n = 16 * (w * NTW + x) + c16;
+      const int n = 16 * (nt0 + x) + c16;
       dreg[x] = a.dseg[((size_t)bh * NS + sg) * DK + n];
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct)
@@ -584,9 +596,11 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
         sMq[j] = a.centered ? rmq.get() / tpos : 0.f;
         sMu[j] = a.centered ? rmu.get() / tpos : 0.f;
       }
-      rq.store(sQ, LDQ);
+      if constexpr (kRowQU) {
+        rq.store(sQ, LDQ);
+        ru.store(sU, LDQ);
+      }
       rq.store_t(sQT, LDT);
-      ru.store(sU, LDQ);
       rk.store(sK, LDQ);
 #pragma unroll
       for (int u = 0; u < ChunkTile<T, DK>::NV; ++u) {
@@ -598,7 +612,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
     }
     float dcv[NTW];  // this chunk's D, added after its outputs
 #pragma unroll
-    for (int x = 0; x < NTW; ++x) dcv[x] = a.dchunk[((size_t)bh * N + ci) * DK + 16 * (w * NTW + x) + c16];
+    for (int x = 0; x < NTW; ++x) dcv[x] = a.dchunk[((size_t)bh * N + ci) * DK + 16 * (nt0 + x) + c16];
     // the backbone's part of dk for this wave's outputs, requested before the products
     const size_t rowoff = tok_off(b, r0, h, a.T, a.H, DK);
     float dkg[NTW][4][4];
@@ -609,7 +623,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int jr = 16 * J + 4 * g4 + r;
-          dkg[x][J][r] = a.dk_gla[rowoff + (jr < nrow ? jr : nrow - 1) * (int)gs + 16 * (w * NTW + x) + c16];
+          dkg[x][J][r] = a.dk_gla[rowoff + (jr < nrow ? jr : nrow - 1) * (int)gs + 16 * (nt0 + x) + c16];
         }
     if (ci > c_begin) prefetch(ci - 1);
     lds_barrier();  // (B)
@@ -621,14 +635,23 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
       if (t < 10) {
         const int I = intra_tile_row(t), J = intra_tile_col(t);
         f32x4 s1 = zero4(), s2 = zero4();
-        tile_mma<T, DK>(s1, sQ + 16 * I * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
-        tile_mma<T, DK>(s2, sU + 16 * I * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+        if constexpr (kRowQU) {
+          tile_mma<T, DK>(s1, sQ + 16 * I * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+          tile_mma<T, DK>(s2, sU + 16 * I * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+        } else {  // s2 = (rho u) . k here
+#pragma unroll
+          for (int k0 = 0; k0 < DK; k0 += 32) {
+            const Frag<T> kf = ld_frag(sK + 16 * J * LDQ + k0, LDQ);
+            mma(s1, ld_frag_tr(sQT + k0 * LDT + 16 * I, LDT), kf);
+            mma(s2, ld_frag_tr(sRUT + k0 * LDT + 16 * I, LDT), kf);
+          }
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int tt = 16 * I + 4 * g4 + r, jj = 16 * J + c16;
           const bool on = jj <= tt;
           const float w1 = on ? s1[r] - sMq[tt] : 0.f;
-          const float w2 = on ? sRho[tt] * (s2[r] - sMu[tt]) : 0.f;
+          const float w2 = on ? (kRowQU ? sRho[tt] * (s2[r] - sMu[tt]) : s2[r] - sRho[tt] * sMu[tt]) : 0.f;
           if constexpr (kSplit) {
             bf16_t hi, lo;
             split_bf16(w1, hi, lo);
@@ -649,7 +672,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
     // dk rows j (all four row tiles), this wave's columns n
 #pragma unroll
     for (int x = 0; x < NTW; ++x) {
-      const int nt = w * NTW + x;
+      const int nt = nt0 + x;
       Frag<T> hh[NK], hl[NK];
 #pragma unroll
       for (int m = 0; m < NK; ++m) {
@@ -707,8 +730,8 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
     for (int x = 0; x < NTW; ++x)
 #pragma unroll
       for (int m2 = 0; m2 < 2; ++m2) {
-        bq[x][m2] = ld_frag(sQT + 16 * (w * NTW + x) * LDT + 32 * m2, LDT);
-        bu[x][m2] = ld_frag(sRUT + 16 * (w * NTW + x) * LDT + 32 * m2, LDT);
+        bq[x][m2] = ld_frag(sQT + 16 * (nt0 + x) * LDT + 32 * m2, LDT);
+        bu[x][m2] = ld_frag(sRUT + 16 * (nt0 + x) * LDT + 32 * m2, LDT);
       }
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct)
@@ -743,7 +766,11 @@ hipError_t run_ccq_dk(const CcqDkArgs& a, hipStream_t st) {
   const int NS = (N + a.seg - 1) / a.seg;
   const int nseg = a.B * a.H * NS;
   if (nseg == 0) return hipSuccess;
-  hipLaunchKernelGGL((ccq_dk_stats_kernel<T, DK>), dim3(nseg), dim3(kThreads), 0, st, a);
+  // at DK = 256 H's tiles are split over two workgroups per segment and the
+  // output columns over four, so that a wave's share of H fits its registers
+  // (no spills)
+  constexpr int NSPLIT_S = DK >= 256 ? 2 : 1, NSPLIT = DK >= 256 ? 4 : 1;
+  hipLaunchKernelGGL((ccq_dk_stats_kernel<T, DK, NSPLIT_S>), dim3(nseg, NSPLIT_S), dim3(kThreads), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t per4 = ((size_t)DK * DK + DK) / 4;
@@ -751,7 +778,7 @@ hipError_t run_ccq_dk(const CcqDkArgs& a, hipStream_t st) {
                      dim3(kThreads), 0, st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((ccq_dk_kernel<T, DK>), dim3(nseg), dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((ccq_dk_kernel<T, DK, NSPLIT>), dim3(nseg, NSPLIT), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 template <typename T, typename TG>
@@ -766,9 +793,9 @@ hipError_t chunk_dispatch(const GlaBwdArgs& a, hipStream_t st) {
 }
 }  // namespace
 
-bool bwd_supported(int dk, int dv, bool is_bf16) {
+bool bwd_supported(int dk, int dv, bool is_bf16, bool gdn) {
   const bool dv_ok = dv == 64 || dv == 128 || dv == 256 || dv == 512;
-  if (is_bf16) return dv_ok && (dk == 64 || dk == 128);
+  if (is_bf16) return dv_ok && (dk == 64 || dk == 128 || (gdn && dk == 256));
   return dv_ok && dk == 64;
 }
 
@@ -791,6 +818,7 @@ hipError_t launch_ccq_dk(const CcqDkArgs& a, bool is_bf16, hipStream_t st) {
   if (is_bf16) {
     if (a.dk == 64) return run_ccq_dk<bf16_t, 64>(a, st);
     if (a.dk == 128) return run_ccq_dk<bf16_t, 128>(a, st);
+    if (a.dk == 256) return run_ccq_dk<bf16_t, 256>(a, st);
   } else {
     if (a.dk == 64) return run_ccq_dk<float, 64>(a, st);
   }

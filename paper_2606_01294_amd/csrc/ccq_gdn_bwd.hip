@@ -635,6 +635,7 @@ hipError_t launch_gdn_bwd_prep(const GdnPrepArgs& a, bool is_bf16, hipStream_t s
     switch (a.dk) {
       case 64: return run_prep<bf16_t, 64>(a, st);
       case 128: return run_prep<bf16_t, 128>(a, st);
+      case 256: return run_prep<bf16_t, 256>(a, st);
     }
   } else if (a.dk == 64) {
     return run_prep<float, 64>(a, st);
@@ -647,6 +648,7 @@ hipError_t launch_gdn_dstate(const GdnDstateArgs& a, bool is_bf16, hipStream_t s
     switch (a.dk) {
       case 64: return run_dstate<bf16_t, 64>(a, st);
       case 128: return run_dstate<bf16_t, 128>(a, st);
+      case 256: return run_dstate<bf16_t, 256>(a, st);
     }
   } else if (a.dk == 64) {
     return run_dstate<float, 64>(a, st);
@@ -659,6 +661,7 @@ hipError_t launch_gdn_bwd_chunk(const GdnBwdArgs& a, bool is_bf16, hipStream_t s
     switch (a.dk) {
       case 64: return run_bwd_chunk<bf16_t, 64>(a, st);
       case 128: return run_bwd_chunk<bf16_t, 128>(a, st);
+      case 256: return run_bwd_chunk<bf16_t, 256>(a, st);
     }
   } else if (a.dk == 64) {
     return run_bwd_chunk<float, 64>(a, st);

@@ -337,7 +337,8 @@ hipError_t launch_gla_dstate(const DstateArgs& a, bool is_bf16, bool gate_bf16, 
 hipError_t launch_gla_bwd_chunk(const GlaBwdArgs& a, bool is_bf16, bool gate_bf16, hipStream_t st);
 hipError_t launch_gla_dg(const DgArgs& a, bool gate_bf16, hipStream_t st);
 hipError_t launch_ccq_dk(const CcqDkArgs& a, bool is_bf16, hipStream_t st);
-bool bwd_supported(int dk, int dv, bool is_bf16);
+// Training-step shapes: bf16 dk in {64, 128} (and 256 for Gated DeltaNet), fp32 dk = 64.
+bool bwd_supported(int dk, int dv, bool is_bf16, bool gdn);
 hipError_t launch_gdn_bwd_prep(const GdnPrepArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_gdn_dstate(const GdnDstateArgs& a, bool is_bf16, hipStream_t st);
 hipError_t launch_gdn_bwd_chunk(const GdnBwdArgs& a, bool is_bf16, hipStream_t st);

@@ -48,7 +48,7 @@ WORKLOADS = {
     "gdn_1p3b_t20k": Workload("gdn_1p3b_t20k", GDN, 1, 20480, 8, 256, 256, torch.bfloat16, 3),
     "gla_train_t4k": Workload("gla_train_t4k", GLA, 4, 4096, 8, 128, 256, torch.bfloat16, 4,
                               train=True),
-    "gdn_train_t4k": Workload("gdn_train_t4k", GDN, 4, 4096, 8, 128, 256, torch.bfloat16, 4,
+    "gdn_train_t4k": Workload("gdn_train_t4k", GDN, 4, 4096, 8, 256, 256, torch.bfloat16, 4,
                               train=True),
 }
 

@@ -131,11 +131,15 @@ def call_bwd(s, bb=0, ws_bytes=1 << 34, ptr=FAKE):
 def test_training_entry_point_validation():
     assert ccq.ccq_workspace_size(shape(), ccq.CCQ_GLA, True) > ccq.ccq_workspace_size(
         shape(), ccq.CCQ_GLA, False)
-    assert ccq.ccq_workspace_size(shape(dk=256), ccq.CCQ_GDN, True) == 0
+    # dk = 256: a Gated DeltaNet training step (the 1.3B layer's head size), no GLA one
+    assert ccq.ccq_workspace_size(shape(dk=256), ccq.CCQ_GDN, True) > ccq.ccq_workspace_size(
+        shape(dk=256), ccq.CCQ_GDN, False)
+    assert ccq.ccq_workspace_size(shape(dk=256), ccq.CCQ_GLA, True) == 0
     assert ccq.ccq_workspace_size(shape(), ccq.CCQ_GDN, True) > ccq.ccq_workspace_size(
         shape(), ccq.CCQ_GDN, False)
-    assert call_bwd(shape(dk=256), bb=1) == 2               # no training step at dk = 256
-    assert call_bwd(shape(), bb=1) == 1                     # Gated DeltaNet needs beta, dbeta
+    assert call_bwd(shape(dk=256), bb=0) == 2               # no GLA training step at dk = 256
+    assert call_bwd(shape(dk=256), bb=1) == 1               # Gated DeltaNet needs beta, dbeta
+    assert call_bwd(shape(), bb=1) == 1
     s = shape()
     s.t0 = 5
     assert call_bwd(s) == 1                                 # training starts from zero state
@@ -220,4 +224,5 @@ def test_varlen_entry_point_validation():
                                             1 << 34, None)
     assert call_bwd(shape(), t0=3) == 1
     assert call_bwd(shape(), bb=1) == 1                     # Gated DeltaNet needs beta, dbeta
-    assert call_bwd(shape(dk=256), bb=1) == 2
+    assert call_bwd(shape(dk=256), bb=0) == 2                # no GLA training step at dk = 256
+    assert call_bwd(shape(dk=256), bb=1) == 1                # Gated DeltaNet at dk = 256 needs beta

@@ -63,7 +63,25 @@ CASES = [
     (BF16, 1, 64, 2, 128, 128, "iso", "const"),
     (BF16, 1, 3, 2, 64, 64, "iso", "random"),
     (BF16, 3, 330, 3, 128, 64, "iso", "random"),
+    # dk = 256, the 1.3B layer's head size
+    (BF16, 1, 200, 2, 256, 256, "iso", "random"),
+    (BF16, 2, 130, 2, 256, 128, "aniso", "random"),
+    (BF16, 1, 97, 1, 256, 512, "meanshift", "random"),
+    (BF16, 1, 3, 2, 256, 64, "iso", "const"),
+    (BF16, 1, 600, 1, 256, 256, "aniso", "random"),
 ]
+
+
+# The reverse state scan at dk = 256 splits value slices by how many there are
+# (B * H * dv / 16): >= 2048 (four tiles per workgroup), >= 1024 (two), fewer
+# (two, each over two waves); these shapes reach the first two, the cases above
+# the third.
+@pytest.mark.parametrize("B,H", [(8, 16), (4, 16)])
+def test_gdn_fwd_bwd_dk256_state_splits(B, H):
+    say("gdn fwd_bwd dk256 split", B, H)
+    d = make_inputs(GDN, B, 70, H, 256, 256, BF16, seed=500 + B * H, keys="aniso", lam="random",
+                    with_dO=True)
+    check(d, BF16)
 
 
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "%s-B%d-T%d-dk%d-dv%d-%s" % (
