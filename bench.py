@@ -262,8 +262,7 @@ KERNELS = {0: ["gla_state"] + CLEAN + ["clean_out", "gla_out"],
            "gdn_train": CLEAN + ["clean_out_train", "gdn_tri", "gdn_state", "gdn_out",
                                  "gdn_bwd_prep", "gdn_dstate", "gdn_bwd_chunk", "clean_dq",
                                  "ccq_dk"]}
-VARLEN_GDN = ["varlen_gather_qk", "varlen_gather_qk", "varlen_gather_v", "varlen_gather_scalar",
-              "varlen_gather_scalar", "varlen_gather_scalar"] + KERNELS[1] + ["varlen_scatter_o", "varlen_fix"]
+VARLEN_GDN = KERNELS[1]  # the forward kernels read the packed rows themselves
 KERNEL_SYMBOL = {"varlen_gather_qk": "varlen_copy_kernel", "varlen_gather_v": "varlen_copy_kernel",
                  "varlen_gather_scalar": "varlen_copy_kernel", "varlen_scatter_o": "varlen_copy_kernel",
                  "varlen_fix": "varlen_cache_fix_kernel", "prep": "prep_kernel", "decode": "decode_kernel", "decode_split": "decode_cbar_kernel+decode_s_kernel", "clean_gram": "clean_gram_kernel",
@@ -426,8 +425,8 @@ class PrepCall:
 
 class VarlenCall:
     """The Gated DeltaNet forward on a packed batch: 2B sequences of lengths uniform in
-    [T/4, 3T/4] (about the tokens of the B x T workload), carried through the padded
-    path (inputs resident on the GPU)."""
+    [T/4, 3T/4] (about the tokens of the B x T workload), read by the kernels straight
+    from the packed rows (inputs resident on the GPU)."""
 
     def __init__(self, w, torch, ccq, inputs):
         import dataclasses

@@ -205,15 +205,16 @@ ccq_status ccq_prep(const ccq_shape* s, const void* q_raw, const void* k_raw, co
  * (a longer sequence is cut at T; the device offsets are not validated by
  * the host: the packed tensors must hold cu[B] rows).  S0, C0, mu0, ST, CT,
  * muT are per sequence, as in the padded calls; a sequence of length 0 with
- * t0 = 0 returns its initial states (or zeros).  Internally the sequences are
- * laid out as a padded [B,T,...] batch in the workspace (rows past a
- * sequence's end are zero, which leaves every state unchanged and no output
- * of the sequence's own rows), the padded path runs, and the results are
- * copied back; the caches' running means are rescaled to each sequence's own
- * token count.  q_clean export is not offered here.  The workspace holds
- * ccq_varlen_workspace_size(s, bb, with_bwd) bytes (0: unsupported shape),
- * which includes the padded copies.  Errors as for the padded entry points;
- * B > 65535 is CCQ_ERR_UNSUPPORTED.
+ * t0 = 0 returns its initial states (or zeros).  The forward kernels read and
+ * write the packed rows directly, through the offsets, and walk only each
+ * sequence's own chunks.  The training step lays the sequences out as a
+ * padded [B,T,...] batch in the workspace (rows past a sequence's end are
+ * zero, which leaves every state unchanged and no output of the sequence's
+ * own rows), runs the padded path and copies the results back.  q_clean
+ * export is not offered here.  The workspace holds
+ * ccq_varlen_workspace_size(s, bb, with_bwd) bytes (0: unsupported shape):
+ * the padded call's for the forward, plus the padded copies for training.
+ * Errors as for the padded entry points; B > 65535 is CCQ_ERR_UNSUPPORTED.
  */
 size_t ccq_varlen_workspace_size(const ccq_shape* s, ccq_backbone bb, int with_bwd);
 ccq_status ccq_gla_fwd_varlen(const ccq_shape* s, const int32_t* cu_seqlens, const void* q,

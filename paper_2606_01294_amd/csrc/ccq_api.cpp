@@ -279,8 +279,10 @@ ccq_status check_forward_args(ccq_backbone bb, const ccq_shape* s, const void* q
   return CCQ_OK;
 }
 
-// cu: offsets of a packed batch laid out padded (the Gated DeltaNet chunk
-// transform, state pass and output then skip each sequence's padding), or null.
+// cu: device offsets of a packed batch (sequence b is rows cu[b] .. cu[b+1] - 1
+// of the token tensors, cut at s->T), or null for a padded [B, T, ...] batch.
+// Every kernel reads and writes the packed rows directly and walks only each
+// sequence's own chunks; the workspace keeps its padded per-chunk layout.
 ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const void* k,
                        const void* v, const void* g_or_la, const float* beta, const float* lam,
                        const float* S0, const float* C0, const float* mu0, void* o, float* ST,
@@ -313,6 +315,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
     // segments of the state pass run in parallel; a scan over the segment
     // totals gives every segment's entry state and S_T
     ccq::GlaStateArgs sa{k, v, g_or_la, S0, ST, ws + L.states, s->B, s->T, s->H, s->dk, s->dv};
+    sa.cu = cu;
     if (L.gla_seg > 0) {
       sa.seg = L.gla_seg;
       sa.ST = nullptr;
@@ -342,6 +345,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   ca.lam = lam;
   ca.C0 = C0;
   ca.mu0 = mu0;
+  ca.cu = cu;
   ca.qclean = qclean;
   ca.qclean_dbg = q_clean_dbg;
   ca.CT = CT;
@@ -352,6 +356,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   // outputs from q_clean and the chunk-entry states
   if (bb == CCQ_GLA) {
     ccq::GlaOutArgs oa{qclean, k, v, g_or_la, ws + L.states, o, s->B, s->T, s->H, s->dk, s->dv, s->scale};
+    oa.cu = cu;
     if (L.gla_seg > 0) {
       oa.seg = L.gla_seg;
       oa.entries = ws + L.entries;
@@ -506,32 +511,10 @@ ccq_status varlen_forward(ccq_backbone bb, const ccq_shape* s, const int32_t* cu
   for (const void* p : req)
     if (!p || !aligned(p)) return CCQ_ERR_INVALID_ARG;
   if (bb == CCQ_GDN && (!beta || !aligned(beta))) return CCQ_ERR_INVALID_ARG;
-  const VarlenLayout L = varlen_layout(s, bb, false);
-  if (!workspace || ws_bytes < L.total) return CCQ_ERR_WORKSPACE;
-  char* ws = static_cast<char*>(workspace);
-  const VarlenRows R = varlen_rows(s, bb);
-  TraceScope scope;
-  auto gather = [&](size_t dst, const void* src, size_t rb) {
-    return traced(st, [&] { return ccq::launch_varlen_copy(ws + dst, src, cu, s->B, s->T, rb, true, st); }) ==
-           hipSuccess;
-  };
-  if (!gather(L.q, q, R.qk) || !gather(L.k, k, R.qk) || !gather(L.v, v, R.v) || !gather(L.gate, g_or_la, R.gate) ||
-      (bb == CCQ_GDN && !gather(L.beta, beta, R.scalar)) || !gather(L.lam, lam, R.scalar))
-    return CCQ_ERR_HIP;
-  rc = run_forward(bb, s, ws + L.q, ws + L.k, ws + L.v, ws + L.gate,
-                   bb == CCQ_GDN ? reinterpret_cast<const float*>(ws + L.beta) : nullptr,
-                   reinterpret_cast<const float*>(ws + L.lam), S0, C0, mu0, ws + L.o, ST, CT, muT, nullptr,
-                   ws + L.inner, ws_bytes - L.inner, stream, cu);
-  if (rc != CCQ_OK) return rc;
-  if (traced(st, [&] { return ccq::launch_varlen_copy(o, ws + L.o, cu, s->B, s->T, R.v, false, st); }) !=
-      hipSuccess)
-    return CCQ_ERR_HIP;
-  if ((CT || muT) &&
-      traced(st, [&] {
-        return ccq::launch_varlen_cache_fix(CT, muT, C0, mu0, cu, s->B, s->H, s->dk, s->T, s->t0, st);
-      }) != hipSuccess)
-    return CCQ_ERR_HIP;
-  return CCQ_OK;
+  if (!workspace || ws_bytes < fwd_layout(s, bb).total) return CCQ_ERR_WORKSPACE;
+  // the kernels read the packed rows through the offsets themselves
+  return run_forward(bb, s, q, k, v, g_or_la, beta, lam, S0, C0, mu0, o, ST, CT, muT, nullptr,
+                     workspace, ws_bytes, stream, cu);
 }
 
 // Scratch of the allocation-free forward (ccq_gdn_fwd_noalloc): a device array
@@ -569,7 +552,8 @@ extern "C" {
 size_t ccq_varlen_workspace_size(const ccq_shape* s, ccq_backbone bb, int with_bwd) {
   if (check_shape(s, bb) != CCQ_OK) return 0;
   if (with_bwd && !ccq::bwd_supported(s->dk, s->dv, s->io_dtype == CCQ_BF16, bb == CCQ_GDN)) return 0;
-  return varlen_layout(s, bb, with_bwd != 0).total;
+  // the forward reads packed rows directly; the training step runs on padded copies
+  return with_bwd ? varlen_layout(s, bb, true).total : fwd_layout(s, bb).total;
 }
 
 ccq_status ccq_gla_fwd_varlen(const ccq_shape* s, const int32_t* cu_seqlens, const void* q, const void* k,

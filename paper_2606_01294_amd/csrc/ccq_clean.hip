@@ -69,7 +69,9 @@ __global__ __launch_bounds__(64 * (DK >= 128 ? 8 : 4), 1) void clean_gram_kernel
   const int a0 = w * RW;
   const T* k = static_cast<const T*>(a.k);
   const size_t gstride = (size_t)a.H * DK;
-  const int cbeg = s * a.seg, cend = min(NC, cbeg + a.seg);
+  const Seq sq = seq_of(a.cu, b, a.T);
+  // a packed sequence's segments past its end are empty: zero sums
+  const int cbeg = s * a.seg, cend = min(n_chunks(sq.len), cbeg + a.seg);
 
   f32x4 acc[RT][CT], stot[RT];
 #pragma unroll
@@ -81,9 +83,9 @@ __global__ __launch_bounds__(64 * (DK >= 128 ? 8 : 4), 1) void clean_gram_kernel
 
   RowTile<T, DK, NTG> rk;
   auto load = [&](int c) {
-    rk.load(k + tok_off(b, c * C, h, a.T, a.H, DK), gstride, min(C, a.T - c * C));
+    rk.load(k + seq_off(sq, c * C, h, a.H, DK), gstride, min(C, sq.len - c * C));
   };
-  load(cbeg);
+  if (cbeg < cend) load(cbeg);
   const Frag<T> ones = ones_col_frag<T>();
 
   for (int c = cbeg; c < cend; ++c) {
@@ -147,17 +149,19 @@ __global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
   const int l = g & 63, tile = g >> 6;
   const int n = 16 * (tile / NMT) + (l & 15);
   const int m = 16 * (tile % NMT) + 4 * (l >> 4);
-  const int NS = n_segs(a.T, a.seg), NC = n_chunks(a.T);
+  const int NS = n_segs(a.T, a.seg);
+  const Seq sq = seq_of(a.cu, bh / a.H, a.T);
+  const int NSL = n_segs(sq.len, a.seg), NCL = n_chunks(sq.len);  // this sequence's own
   const float t0f = (float)a.t0;
   f32x4 acc = zero4();
   if (a.C0) acc = *reinterpret_cast<const f32x4*>(a.C0 + ((size_t)bh * DK + n) * DK + m) * t0f;
   float run_a = a.mu0 ? t0f * a.mu0[(size_t)bh * DK + n] : 0.f;  // raw key sums before s
   f32x4 run_b = a.mu0 ? *reinterpret_cast<const f32x4*>(a.mu0 + (size_t)bh * DK + m) * t0f : zero4();
   T* Sp = static_cast<T*>(a.sprime);
-  for (int s = 0; s < NS; ++s) {
+  for (int s = 0; s < NSL; ++s) {
     const size_t so = (size_t)bh * NS + s;
-    const int cbeg = s * a.seg, cend = min(NC, cbeg + a.seg);
-    const float len = (float)(min(a.T, cend * kChunk) - cbeg * kChunk);
+    const int cbeg = s * a.seg, cend = min(NCL, cbeg + a.seg);
+    const float len = (float)(min(sq.len, cend * kChunk) - cbeg * kChunk);
     const float ns = t0f + (float)((int64_t)cbeg * kChunk);
     const float tot_a = a.ssum[so * DK + n];
     const f32x4 tot_b = *reinterpret_cast<const f32x4*>(a.ssum + so * DK + m);
@@ -174,7 +178,16 @@ __global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
     run_a += tot_a;
     run_b += tot_b;
   }
-  const float inv = 1.f / (t0f + (float)a.T);
+  if (a.t0 + sq.len == 0) {  // no token at all (an empty packed sequence): the initial cache
+    if (a.CT)
+      *reinterpret_cast<f32x4*>(a.CT + ((size_t)bh * DK + n) * DK + m) =
+          a.C0 ? *reinterpret_cast<const f32x4*>(a.C0 + ((size_t)bh * DK + n) * DK + m) : zero4();
+    if (a.muT && n == 0)
+      *reinterpret_cast<f32x4*>(a.muT + (size_t)bh * DK + m) =
+          a.mu0 ? *reinterpret_cast<const f32x4*>(a.mu0 + (size_t)bh * DK + m) : zero4();
+    return;
+  }
+  const float inv = 1.f / (t0f + (float)sq.len);
   if (a.CT) *reinterpret_cast<f32x4*>(a.CT + ((size_t)bh * DK + n) * DK + m) = acc * inv;
   if (a.muT && n == 0) *reinterpret_cast<f32x4*>(a.muT + (size_t)bh * DK + m) = run_b * inv;
 }
@@ -244,7 +257,13 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
   const int bh = lb / NS, s = lb % NS;
   const int b = bh / a.H, h = bh % a.H;
-  const int cbeg = s * a.seg, cend = min(NC, cbeg + a.seg);
+  const Seq sq = seq_of(a.cu, b, a.T);
+  // rows of the token tensors this kernel writes (q_clean and, in training,
+  // Sigma x, m . x and the base), which live in the workspace in a padded
+  // [B, T, ...] layout whatever the layout of the inputs
+  const Seq sw{(long long)b * a.T, sq.len};
+  const int cbeg = s * a.seg, cend = min(n_chunks(sq.len), cbeg + a.seg);
+  if (cbeg >= cend) return;  // a segment past a packed sequence's end
   const int tid = threadIdx.x;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n0 = w * NCW;
@@ -258,15 +277,15 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
   Tile rx, rk;
   RowScalar rl;
   auto prefetch = [&](int c) {
-    const int r0 = c * C, n = min(C, a.T - r0);
+    const int r0 = c * C, n = min(C, sq.len - r0);
     if constexpr (kDma) {
-      LdsStream<DK, NW>::load(x + tok_off(b, r0, h, a.T, a.H, DK), gstride, n, sSt);
-      LdsStream<DK, NW>::load(k + tok_off(b, r0, h, a.T, a.H, DK), gstride, n, sSt + C * DK);
+      LdsStream<DK, NW>::load(x + seq_off(sq, r0, h, a.H, DK), gstride, n, sSt);
+      LdsStream<DK, NW>::load(k + seq_off(sq, r0, h, a.H, DK), gstride, n, sSt + C * DK);
     } else {
-      rx.load(x + tok_off(b, r0, h, a.T, a.H, DK), gstride, n);
-      rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), gstride, n);
+      rx.load(x + seq_off(sq, r0, h, a.H, DK), gstride, n);
+      rk.load(k + seq_off(sq, r0, h, a.H, DK), gstride, n);
     }
-    if (tid < C) rl.load(a.lam + ((size_t)b * a.T + r0) * a.H + h, (size_t)a.H, tid, n);
+    if (tid < C) rl.load(a.lam + seq_idx(sq, r0, h, a.H), (size_t)a.H, tid, n);
   };
   prefetch(cbeg);
 
@@ -278,7 +297,7 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
     float run = a.mu0 ? t0f * a.mu0[(size_t)bh * DK + tid] : 0.f;
 #pragma unroll 8
     for (int p = 0; p < s; ++p) run += ss[(size_t)p * DK];
-    const float len = (float)(min(a.T, cend * C) - cbeg * C);
+    const float len = (float)(min(sq.len, cend * C) - cbeg * C);
     cen = a.centered ? ss[(size_t)s * DK] / len : 0.f;
     sC[tid] = cen;
     sM[tid] = run - (t0f + (float)((int64_t)cbeg * C)) * cen;
@@ -308,7 +327,7 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
 
   float csum = 0.f;  // key sum of the current chunk, feature tid
   for (int c = cbeg; c < cend; ++c) {
-    const int r0 = c * C, nrow = min(C, a.T - r0);
+    const int r0 = c * C, nrow = min(C, sq.len - r0);
     // per-token and per-feature values first: waiting for their loads costs
     // nothing here, while after the stores below it would also wait for those
     if (tid < C) sLam[tid] = rl.get();
@@ -337,7 +356,7 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
         const int e = t_ + NT * u, row = e / VPR, col = (e % VPR) * 8;
         T* px = sX + row * LDK + col;
         if (c > cbeg)
-          *reinterpret_cast<vec_t*>(qc + tok_off(b, r0 - C + row, h, a.T, a.H, DK) + col) =
+          *reinterpret_cast<vec_t*>(qc + seq_off(sw, r0 - C + row, h, a.H, DK) + col) =
               *reinterpret_cast<const vec_t*>(px);
         vec_t y;
 #pragma unroll
@@ -448,7 +467,7 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
       }
       if (pp == 0) {
         sCq[i] = cqp;
-        if (TRAIN && a.mdot && i < nrow) a.mdot[((size_t)b * a.T + r0 + i) * a.H + h] = cqp + ti * cx;  // raw m . x
+        if (TRAIN && a.mdot && i < nrow) a.mdot[seq_idx(sw, r0 + i, h, a.H)] = cqp + ti * cx;  // raw m . x
       }
     }
     lds_barrier();  // (3) shifted scores complete
@@ -487,7 +506,7 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
         for (int nt = 0; nt < NNT; ++nt) {
           const int n = n0 + 16 * nt + 4 * g_;
           if constexpr (TRAIN)
-            xb[nt] = a.base ? *reinterpret_cast<const f32x4*>(a.base + tok_off(b, r0 + min(i, nrow - 1), h, a.T, a.H, DK) + n)
+            xb[nt] = a.base ? *reinterpret_cast<const f32x4*>(a.base + seq_off(sw, r0 + min(i, nrow - 1), h, a.H, DK) + n)
                             : load4f(sX + i * LDK + n);
           else
             xb[nt] = load4f(sX + i * LDK + n);
@@ -507,7 +526,7 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
           }
           store4(sX + i * LDK + n, o[0], o[1], o[2], o[3]);
           if (TRAIN && i < nrow) {
-            const size_t off = tok_off(b, r0 + i, h, a.T, a.H, DK) + n;
+            const size_t off = seq_off(sw, r0 + i, h, a.H, DK) + n;
             if (a.qclean_dbg) *reinterpret_cast<f32x4*>(a.qclean_dbg + off) = o;
             if (a.corr) *reinterpret_cast<f32x4*>(a.corr + off) = cr;
           }
@@ -551,12 +570,12 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
 
   // copy out the last chunk
   {
-    const int r0 = (cend - 1) * C, nrow = min(C, a.T - r0);
+    const int r0 = (cend - 1) * C, nrow = min(C, sq.len - r0);
 #pragma unroll
     for (int u = 0; u < NV; ++u) {
       const int e = tid + NT * u, row = e / VPR, col = (e % VPR) * 8;
       if (row < nrow)
-        *reinterpret_cast<vec_t*>(qc + tok_off(b, r0 + row, h, a.T, a.H, DK) + col) =
+        *reinterpret_cast<vec_t*>(qc + seq_off(sw, r0 + row, h, a.H, DK) + col) =
             *reinterpret_cast<const vec_t*>(sX + row * LDK + col);
     }
   }

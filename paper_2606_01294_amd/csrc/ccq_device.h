@@ -614,6 +614,29 @@ __device__ __forceinline__ int live_chunks(const int* cu, int b, int T, int N) {
   return (len + kChunk - 1) / kChunk;
 }
 
+// Sequence b of a batch: its first row in the token tensors and its length.
+// Without offsets (cu null) the batch is padded, [B, T, ...], and every
+// sequence has T tokens; with offsets it is packed: sequence b is rows
+// cu[b] .. cu[b + 1] - 1 of [rows, ...] tensors, its length cut at T.
+struct Seq {
+  long long row0;
+  int len;
+};
+__device__ __forceinline__ Seq seq_of(const int* cu, int b, int T) {
+  if (!cu) return Seq{(long long)b * T, T};
+  int len = cu[b + 1] - cu[b];
+  len = len < 0 ? 0 : (len > T ? T : len);
+  return Seq{(long long)cu[b], len};
+}
+// Offset of token t of sequence q, head h, in a [rows, H, D] tensor (elements).
+__device__ __forceinline__ size_t seq_off(const Seq& q, int t, int h, int H, int D) {
+  return ((size_t)(q.row0 + t) * H + h) * (size_t)D;
+}
+// Index of token t of sequence q, head h, in a [rows, H] tensor.
+__device__ __forceinline__ size_t seq_idx(const Seq& q, int t, int h, int H) {
+  return (size_t)(q.row0 + t) * H + h;
+}
+
 // Sum over aligned groups of n consecutive lanes (n = 2, 4, 8, 16), by
 // swizzles (no address registers).
 template <int N>

@@ -54,18 +54,19 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
   const int bh = lb / N, ci = lb % N;
   const int b = bh / a.H, h = bh % a.H;
-  if (ci >= live_chunks(a.cu, b, a.T, N)) return;  // padding of a packed batch: not read
+  const Seq sq = seq_of(a.cu, b, a.T);
   const int r0 = ci * C;
-  const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+  if (r0 >= sq.len) return;  // past a packed sequence's end
+  const int nrow = (sq.len - r0) < C ? (sq.len - r0) : C;
   const int tid = threadIdx.x, w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
 
   // all global loads first (K, the log decays and beta), one round trip
   RowTile<T, DK> rk;
-  rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+  rk.load(static_cast<const T*>(a.k) + seq_off(sq, r0, h, a.H, DK), (size_t)a.H * DK, nrow);
   float la = 0.f, bt = 0.f;
   if (tid < C) {
-    const size_t ti = ((size_t)b * a.T + r0 + (tid < nrow ? tid : nrow - 1)) * a.H + h;
+    const size_t ti = seq_idx(sq, r0 + (tid < nrow ? tid : nrow - 1), h, a.H);
     la = a.logalpha[ti];
     bt = a.beta[ti];
   }
@@ -193,7 +194,8 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
   const int v = v0 + vs;
   const int c0 = hq * DKH;          // first key feature of this wave
   const int b = bh / a.H, h = bh % a.H;
-  const int NL = live_chunks(a.cu, b, a.T, N);  // chunks walked (all but a packed batch's padding)
+  const Seq sq = seq_of(a.cu, b, a.T);
+  const int NL = (sq.len + C - 1) / C;  // chunks walked (a packed sequence's own)
   const T* k = static_cast<const T*>(a.k);
   const T* vin = static_cast<const T*>(a.v);
   const T* Tg = static_cast<const T*>(a.Tm);
@@ -220,10 +222,10 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
   Stage st;
   auto prefetch = [&](Stage& sg, int ci) {
     const int r0 = ci * C;
-    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-    sg.rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), (size_t)a.H * DK, nrow);
+    const int nrow = (sq.len - r0) < C ? (sq.len - r0) : C;
+    sg.rk.load(k + seq_off(sq, r0, h, a.H, DK), (size_t)a.H * DK, nrow);
     sg.rt.load(Tg + ((size_t)bh * N + ci) * C * C, (size_t)C, C);
-    sg.rv.load(vin + tok_off(b, r0, h, a.T, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
+    sg.rv.load(vin + seq_off(sq, r0, h, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
     if (tid < C) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) sg.cf[q].load(a.gam + (((size_t)bh * N + ci) * 5 + 1 + q) * C, 1, tid, C);
@@ -441,7 +443,8 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
   const int v = v0 + 16 * pr + c16;
   const int c0 = hq * DKH;
   const int b = bh / a.H, h = bh % a.H;
-  const int NL = live_chunks(a.cu, b, a.T, N);  // chunks walked (all but a packed batch's padding)
+  const Seq sq = seq_of(a.cu, b, a.T);
+  const int NL = (sq.len + C - 1) / C;  // chunks walked (a packed sequence's own)
   const T* k = static_cast<const T*>(a.k);
   const T* vin = static_cast<const T*>(a.v);
   const T* Tg = static_cast<const T*>(a.Tm);
@@ -455,11 +458,11 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
   static_assert(NIK % NW == 0 && NIT % NW == 0, "piece split");
   auto issue = [&](int ci) {
     char* sb = smem + (ci % NSTAGE) * SB;
-    const int r0 = ci * C, nrow = min(C, a.T - r0);
+    const int r0 = ci * C, nrow = min(C, sq.len - r0);
     const int hs = a.H * DK, hv = a.H * a.dv;
-    const T* kb = k + tok_off(b, r0, h, a.T, a.H, DK);
+    const T* kb = k + seq_off(sq, r0, h, a.H, DK);
     const T* tb = Tg + ((size_t)bh * N + ci) * C * C;
-    const T* vb = vin + tok_off(b, r0, h, a.T, a.H, a.dv) + v0;
+    const T* vb = vin + seq_off(sq, r0, h, a.H, a.dv) + v0;
 #pragma unroll
     for (int it = 0; it < NIK / NW; ++it) {
       constexpr int CPR = DK / 8;
@@ -730,7 +733,8 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
   const int hm = lb / NGR, cb = (lb % NGR) * R;
   const int bh = (hm % a.B) * a.H + hm / a.B;  // head-major, as the state pass
   const int b = bh / a.H, h = bh % a.H;
-  const int ce = min(live_chunks(a.cu, b, a.T, N), cb + R);  // a packed batch's padding is skipped
+  const Seq sq = seq_of(a.cu, b, a.T);
+  const int ce = min((sq.len + C - 1) / C, cb + R);  // a packed sequence's own chunks
   if (cb >= ce) return;
   const int tid = threadIdx.x, w = tid >> 6, l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
@@ -741,12 +745,13 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
   Frag<T> sfr[VPW][NK];
   for (int ci = cb; ci < ce; ++ci) {
     const int r0 = ci * C;
-    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+    const int nrow = (sq.len - r0) < C ? (sq.len - r0) : C;
     const bool carry = CARRY && ci + 1 < ce;
     {
       RowTile<T, DK, kOutThreads> rq, rk;
-      rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-      rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+      rq.load(static_cast<const T*>(a.qc) + seq_off(Seq{(long long)b * a.T, sq.len}, r0, h, a.H, DK), gstride,
+              nrow);  // q_clean: the workspace's padded rows
+      rk.load(static_cast<const T*>(a.k) + seq_off(sq, r0, h, a.H, DK), gstride, nrow);
       const float* gm = a.gam + ((size_t)bh * N + ci) * 5 * C;
       if (tid < C) sGam[tid] = gm[tid];
       if (carry && tid < C + 1) sDd[tid] = tid < C ? gm[3 * C + tid] : gm[4 * C];
@@ -819,7 +824,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
         if (I >= 2) mma(acc[vt], ufr[vt][1], pf1);  // keys 32..63 precede row i only for I >= 2
         if (i < nrow) {
           const int vcol = 16 * (vg * VPW + vt) + 4 * g4;
-          store4(o + tok_off(b, r0 + i, h, a.T, a.H, a.dv) + vcol, a.scale * acc[vt][0], a.scale * acc[vt][1],
+          store4(o + seq_off(sq, r0 + i, h, a.H, a.dv) + vcol, a.scale * acc[vt][0], a.scale * acc[vt][1],
                  a.scale * acc[vt][2], a.scale * acc[vt][3]);
         }
       }

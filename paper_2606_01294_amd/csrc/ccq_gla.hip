@@ -51,8 +51,11 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
   const int vt = lb % nvt, kt = (lb / nvt) % nkt, sg = (lb / (nvt * nkt)) % NS, bh = lb / (nvt * nkt * NS);
   const int c0 = kt * BK, v0 = vt * VB;
-  const int cb = sg * SL, ce = min(N, cb + SL);  // this segment's chunks
   const int b = bh / a.H, h = bh % a.H;
+  const Seq sq = seq_of(a.cu, b, a.T);
+  // this segment's chunks (none past a packed sequence's end: the segment then
+  // passes its entry state through unchanged, zero sum and unit decay)
+  const int cb = sg * SL, ce = min((sq.len + C - 1) / C, cb + SL);
   const int w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
   const T* k = static_cast<const T*>(a.k);
@@ -74,10 +77,10 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
   RowTile<T, VB> rv;
   auto prefetch = [&](int ci) {
     const int r0 = ci * C;
-    const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-    rk.load(k + tok_off(b, r0, h, a.T, a.H, a.dk) + c0, (size_t)a.H * a.dk, nrow);
-    rg.load(gate + tok_off(b, r0, h, a.T, a.H, a.dk) + c0, (size_t)a.H * a.dk, nrow);
-    rv.load(v + tok_off(b, r0, h, a.T, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
+    const int nrow = (sq.len - r0) < C ? (sq.len - r0) : C;
+    rk.load(k + seq_off(sq, r0, h, a.H, a.dk) + c0, (size_t)a.H * a.dk, nrow);
+    rg.load(gate + seq_off(sq, r0, h, a.H, a.dk) + c0, (size_t)a.H * a.dk, nrow);
+    rv.load(v + seq_off(sq, r0, h, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
   };
   f32x4 Sr[NVT];  // S_r kept for the deferred write-back
   auto write_back = [&](int cw) {
@@ -222,8 +225,10 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
   const int bh = lb / N, ci = lb % N;
   const int b = bh / a.H, h = bh % a.H;
+  const Seq sq = seq_of(a.cu, b, a.T);
   const int r0 = ci * C;
-  const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
+  if (r0 >= sq.len) return;  // past a packed sequence's end
+  const int nrow = (sq.len - r0) < C ? (sq.len - r0) : C;
   const int tid = threadIdx.x, w = tid >> 6, l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
   const int vg = w % NVG, ig = w / NVG;
@@ -235,9 +240,10 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
 
   RowTile<T, DK, NT> rq, rk;
   RowTile<TG, DK, NT> rg;
-  rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-  rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
-  rg.load(static_cast<const TG*>(a.g) + tok_off(b, r0, h, a.T, a.H, DK), gstride, nrow);
+  const Seq sw{(long long)b * a.T, sq.len};  // q_clean: the workspace's padded rows
+  rq.load(static_cast<const T*>(a.qc) + seq_off(sw, r0, h, a.H, DK), gstride, nrow);
+  rk.load(static_cast<const T*>(a.k) + seq_off(sq, r0, h, a.H, DK), gstride, nrow);
+  rg.load(static_cast<const TG*>(a.g) + seq_off(sq, r0, h, a.H, DK), gstride, nrow);
 #pragma unroll
   for (int u = 0; u < RowTile<TG, DK, NT>::NV; ++u) {  // gates as fp32 rows
     const auto x = rg.get(u);
@@ -309,7 +315,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
     if (vp > 0) __syncthreads();  // every wave is done with the previous V slice
     {
       RowTile<T, VP, NT> rv;
-      rv.load(static_cast<const T*>(a.v) + tok_off(b, r0, h, a.T, a.H, a.dv) + vp, (size_t)a.H * a.dv, nrow);
+      rv.load(static_cast<const T*>(a.v) + seq_off(sq, r0, h, a.H, a.dv) + vp, (size_t)a.H * a.dv, nrow);
       rv.store(sV, LDV);
     }
     // this wave's rows of S_r (k = key channel), scaled by e^{b_m}
@@ -362,7 +368,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
         mma(acc[vt], ld_frag_tr_acc(sV + vl, LDV), pf0);
         if (I >= 2) mma(acc[vt], ld_frag_tr_acc(sV + 32 * LDV + vl, LDV), pf1);  // keys 32..63 precede row i
         if (i < nrow)
-          store4(o + tok_off(b, r0 + i, h, a.T, a.H, a.dv) + vp + vl + 4 * g4, a.scale * acc[vt][0],
+          store4(o + seq_off(sq, r0 + i, h, a.H, a.dv) + vp + vl + 4 * g4, a.scale * acc[vt][0],
                  a.scale * acc[vt][1], a.scale * acc[vt][2], a.scale * acc[vt][3]);
       }
     }

@@ -44,6 +44,10 @@ struct CleanArgs {
   int centered;
   int seg;            // chunks per segment
   int64_t t0;
+  // packed batch: sequence b is rows cu[b] .. cu[b+1] - 1 of [rows, H, d] token
+  // tensors (length cut at T), or null for a padded [B, T, H, d] batch; the
+  // workspace keeps its padded per-chunk layout either way
+  const int* cu = nullptr;
 };
 
 // GLA state recurrence (sequential over chunks) for one 64-channel tile of S.
@@ -68,6 +72,7 @@ struct GlaStateArgs {
   float* segdec;      // [B*H, NS, dk] fp32: e^{sum of the segment's log decays}
   float* cdec;        // [B*H, N, dk] fp32: e^{log decays of the segment before each chunk}
   float scale;        // read scale (the reverse scan of the training step only)
+  const int* cu = nullptr;  // packed-batch offsets (device), as CleanArgs
 };
 
 // Entry state of every segment, E_0 = 0 (S0 is inside segment 0's states),
@@ -93,6 +98,7 @@ struct GlaOutArgs {
   int seg;              // chunks per segment of the state pass (0 = one segment)
   const void* entries;  // [B*H, NS, dv, dk] io, or null with one segment
   const float* cdec;    // [B*H, N, dk] fp32, or null with one segment
+  const int* cu = nullptr;  // packed-batch offsets (device), as CleanArgs
 };
 
 // Gated DeltaNet chunk transform (chunk-parallel): Tm = (I + A)^{-1} and the
@@ -106,7 +112,7 @@ struct TriArgs {
                          // decay in the chunk), beta_j e^{gamma_j}, beta_j,
                          // e^{gamma_C - gamma_j}, e^{gamma_C}
   int B, T, H, dk, dv;
-  const int* cu = nullptr;  // packed-batch offsets [B+1] (device) or null: see live_chunks
+  const int* cu = nullptr;  // packed-batch offsets [B+1] (device), as CleanArgs, or null
 };
 
 // Gated DeltaNet state recurrence (sequential over chunks): writes the
@@ -354,9 +360,6 @@ bool prep_supported(int H, int dk);
 // sequences' rows back from padded to packed.
 hipError_t launch_varlen_copy(void* dst, const void* src, const int* cu, int B, int T, size_t row_bytes,
                               bool to_padded, hipStream_t st);
-// Cbar_T, mu_T of a padded forward rescaled from count t0 + T to t0 + len_b.
-hipError_t launch_varlen_cache_fix(float* CT, float* muT, const float* C0, const float* mu0, const int* cu,
-                                   int B, int H, int dk, int T, long long t0, hipStream_t st);
 
 // Supported-shape predicates (used by validation before any launch).
 bool clean_supported(int dk, bool is_bf16);

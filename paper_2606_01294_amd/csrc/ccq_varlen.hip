@@ -1,17 +1,15 @@
-// ccq_varlen.hip -- packed batches of sequences of different lengths.
+// ccq_varlen.hip -- padded copies of packed batches for the training step.
 //
 // Sequence b of a packed batch holds rows cu[b] .. cu[b+1] - 1 of every
-// [rows, H, d] tensor.  Every sequence is independent (its own states), so
-// the packed batch is carried through the chunkwise path as a padded batch
-// [B, T, H, d] (T the longest length): row t of sequence b is copied to
-// padded row b T + t, and the rows past the sequence's end hold zeros.  A
-// zero row leaves every state unchanged (k = v = 0 writes nothing; a zero
-// log-gate or log-decay keeps S; beta = 0 makes the delta rule the identity)
-// and, the path being causal, changes no output of the sequence's own rows.
-// The only quantities the padding reaches are the running means of the
-// contraction cache, Cbar_T = S^K / (t0 + T) and mu_T = m / (t0 + T), whose
-// sums are unchanged but whose counts are not: varlen_cache_fix rescales
-// them to the sequence's own count t0 + len_b.
+// [rows, H, d] tensor.  The forward kernels read packed rows directly; the
+// training step (ccq_fwd_bwd_varlen) runs on a padded batch [B, T, H, d] (T
+// the longest length): row t of sequence b is copied to padded row b T + t
+// and the rows past the sequence's end hold zeros.  A zero row leaves every
+// state unchanged (k = v = 0 writes nothing; a zero log-gate or log-decay
+// keeps S; beta = 0 makes the delta rule the identity) and, the path being
+// causal, changes no output or gradient of the sequence's own rows; the
+// training step returns no caches, so the padding's effect on the running
+// means' counts does not arise.
 #include "ccq_device.h"
 #include "ccq_kernels.h"
 
@@ -46,27 +44,6 @@ __global__ void varlen_copy_kernel(V* dst, const V* src, const int* cu, int T, l
   }
 }
 
-// Cbar_T and mu_T of (sequence b, head h) = blockIdx.y: counts t0 + T ->
-// t0 + len_b, blockIdx.x taking 256 of the head's dk * dk + dk values; a
-// sequence with no tokens at all returns the initial cache.
-__global__ void varlen_cache_fix_kernel(float* CT, float* muT, const float* C0, const float* mu0,
-                                        const int* cu, int H, int dk, int T, long long t0) {
-  const int bh = blockIdx.y, b = bh / H;
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  const int nc = dk * dk;
-  if (i >= nc + dk) return;
-  const int len = seq_len(cu, b, T);
-  const long long cnt = t0 + len;
-  float* dst = i < nc ? (CT ? CT + (size_t)bh * nc + i : nullptr) : (muT ? muT + (size_t)bh * dk + (i - nc) : nullptr);
-  if (!dst) return;
-  if (cnt == 0) {
-    const float* src = i < nc ? (C0 ? C0 + (size_t)bh * nc + i : nullptr) : (mu0 ? mu0 + (size_t)bh * dk + (i - nc) : nullptr);
-    *dst = src ? *src : 0.f;
-    return;
-  }
-  *dst *= (float)((double)(t0 + T) / (double)cnt);
-}
-
 }  // namespace
 
 hipError_t launch_varlen_copy(void* dst, const void* src, const int* cu, int B, int T, size_t row_bytes,
@@ -96,15 +73,6 @@ hipError_t launch_varlen_copy(void* dst, const void* src, const int* cu, int B, 
       hipLaunchKernelGGL((varlen_copy_kernel<V, false>), grid, dim3(256), 0, st, static_cast<V*>(dst),
                          static_cast<const V*>(src), cu, T, units);
   }
-  return hipGetLastError();
-}
-
-hipError_t launch_varlen_cache_fix(float* CT, float* muT, const float* C0, const float* mu0, const int* cu,
-                                   int B, int H, int dk, int T, long long t0, hipStream_t st) {
-  if (B == 0 || H == 0 || (!CT && !muT)) return hipSuccess;
-  const unsigned nx = (unsigned)((dk * dk + dk + 255) / 256);
-  hipLaunchKernelGGL(varlen_cache_fix_kernel, dim3(nx, (unsigned)(B * H)), dim3(256), 0, st, CT, muT, C0, mu0, cu,
-                     H, dk, T, t0);
   return hipGetLastError();
 }
 

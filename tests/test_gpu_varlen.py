@@ -67,6 +67,10 @@ FWD_CASES = [
     (GLA, F32, [5, 70, 128], 2, 64, 128, 40, True),
     (GDN, BF16, [150, 1, 64, 0, 90], 2, 256, 256, 0, True),
     (GDN, F32, [66, 130], 2, 64, 64, 8, False),
+    # few heads and many chunks: the GLA state pass runs in segments, the
+    # shorter sequences' last segments are empty
+    (GLA, BF16, [1100, 300, 0, 700], 1, 128, 256, 0, True),
+    (GDN, BF16, [700, 64, 333], 1, 128, 128, 0, False),
 ]
 
 
@@ -144,3 +148,52 @@ def test_varlen_training_step(case):
     say("  errors", errs)
     tol = TOL[dtype]
     assert all(v <= tol for v in errs.values()), errs
+
+
+def test_varlen_sequence_cut_at_max_len():
+    """A sequence longer than max_len is cut there: only its first max_len rows are read
+    and written, and the next sequence's packed rows (which start past B * max_len) are
+    still found through the offsets."""
+    lens, max_len, H, dk, dv = [200, 50, 90], 100, 2, 64, 128
+    for backbone in (GLA, GDN):
+        p, cu = packed(backbone, lens, H, dk, dv, BF16, seed=88)
+        gout = run_fwd(backbone, p, cu, max_len, None, 0)
+        cut = [min(L, max_len) for L in lens]
+        keep = np.concatenate([np.arange(cu[b], cu[b] + cut[b]) for b in range(len(lens))])
+        f = to_f64(p)
+        fc = {n: x[keep] for n, x in f.items()}
+        cuc = np.concatenate([[0], np.cumsum(cut)]).astype(np.int32)
+        gate = fc["g"] if backbone == GLA else fc["logalpha"]
+        ref = O.varlen_fwd(fc["q"], fc["k"], fc["v"], gate, fc["lam"], cuc, beta=fc.get("beta"),
+                           backbone=backbone)
+        errs = {"o": nerr(gout["o"][keep], ref["o"])}
+        errs.update({n: nerr(gout[n], ref[n]) for n in ("ST", "CT", "muT")})
+        say("  cut", backbone, errs)
+        assert all(v <= TOL[BF16] for v in errs.values()), errs
+
+
+def test_varlen_full_size_gdn():
+    """The packed Gated DeltaNet workload of the benchmark: 8 sequences of 1024 to 3072
+    tokens, H=8, dk=dv=256, bf16, every sequence compared with the oracle."""
+    from paper_2606_01294_amd.inputs import WORKLOADS, varlen_lengths
+    w = WORKLOADS["gdn_1p3b_t4k"]
+    lens = varlen_lengths(w)
+    say("varlen full size", lens)
+    T = max(lens)
+    d = make_inputs(GDN, len(lens), T, w.H, w.dk, w.dv, w.dtype, seed=w.seed)
+    p = {n: torch.cat([x[b, :L] for b, L in enumerate(lens)], dim=0).contiguous()
+         for n, x in d.items()}
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    gout = run_fwd(GDN, p, cu, T, None, 0)
+    f = to_f64(p)
+    ref = O.varlen_fwd(f["q"], f["k"], f["v"], f["logalpha"], f["lam"], cu, beta=f["beta"],
+                       backbone=GDN)
+    worst = {}
+    for b in range(len(lens)):
+        sl = slice(cu[b], cu[b + 1])
+        e = {"o": nerr(gout["o"][sl], ref["o"][sl]), "ST": nerr(gout["ST"][b], ref["ST"][b]),
+             "CT": nerr(gout["CT"][b], ref["CT"][b]), "muT": nerr(gout["muT"][b], ref["muT"][b])}
+        for n, v in e.items():
+            worst[n] = max(worst.get(n, 0.0), v)
+        assert all(v <= TOL[w.dtype] for v in e.values()), (b, e)
+    say("  worst", worst)
