@@ -162,6 +162,9 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     elif kernel == "prep":          # raw q, k in; normalised q, k and the gate out (W_lambda once)
         by = ntok * (4 * dk * io_bytes + 4) + w.H * w.H * dk * 4 + w.H * 4
         fl = ntok * (2 * w.H * dk + 6 * dk)
+    elif kernel == "prep_scales":   # raw q, k in; the two row scales and the gate out
+        by = ntok * (2 * dk * io_bytes + 12) + w.H * w.H * dk * 4 + w.H * 4
+        fl = ntok * (2 * w.H * dk + 4 * dk)
     elif kernel == "ccq_dk":
         by = ntok * (3 * dk * io_bytes + 12 + 4 * dk + dk * io_bytes)
         fl = ntok * (6 * dk * dk + 8 * C * dk)
@@ -263,7 +266,7 @@ KERNELS = {0: ["gla_state"] + CLEAN + ["clean_out", "gla_out"],
                                  "gdn_bwd_prep", "gdn_dstate", "gdn_bwd_chunk", "clean_dq",
                                  "ccq_dk"]}
 VARLEN_GDN = KERNELS[1]  # the forward kernels read the packed rows themselves
-KERNEL_SYMBOL = {"varlen_gather_qk": "varlen_copy_kernel", "varlen_gather_v": "varlen_copy_kernel",
+KERNEL_SYMBOL = {"prep_scales": "prep_kernel (row scales)", "varlen_gather_qk": "varlen_copy_kernel", "varlen_gather_v": "varlen_copy_kernel",
                  "varlen_gather_scalar": "varlen_copy_kernel", "varlen_scatter_o": "varlen_copy_kernel",
                  "varlen_fix": "varlen_cache_fix_kernel", "prep": "prep_kernel", "decode": "decode_kernel", "decode_split": "decode_cbar_kernel+decode_s_kernel", "clean_gram": "clean_gram_kernel",
                  "clean_prefix": "clean_prefix_kernel", "clean_out": "clean_out_kernel",
@@ -285,7 +288,7 @@ def _source(kernel: str) -> str:
         return "ccq_gdn_bwd.hip"
     if kernel.startswith("decode"):
         return "ccq_decode.hip"
-    if kernel == "prep":
+    if kernel in ("prep", "prep_scales"):
         return "ccq_prep.hip"
     if kernel.startswith("varlen"):
         return "ccq_varlen.hip"
@@ -423,6 +426,37 @@ class PrepCall:
         self.ccq.ccq_prep(self.q, self.k, self.wl, self.bl, out=self.out)
 
 
+class RawCall:
+    """The Gated DeltaNet forward from raw q, k (ccq_fwd_raw: the l2 normalisation and
+    the gate folded into the forward), inputs resident on the GPU; the same raw tensors
+    as the pre-processing workload."""
+
+    def __init__(self, w, torch, ccq, inputs):
+        import dataclasses
+        self.w = dataclasses.replace(w, name=w.name.replace("_t", "_raw_t"))
+        gen = torch.Generator().manual_seed(w.seed)
+        B, T, H, dk, dv = w.B, w.T, w.H, w.dk, w.dv
+        self.q = torch.randn(B, T, H, dk, generator=gen).to(w.dtype).cuda()
+        self.k = torch.randn(B, T, H, dk, generator=gen).to(w.dtype).cuda()
+        self.wl = (torch.randn(H, H * dk, generator=gen) / (H * dk) ** 0.5).cuda()
+        self.bl = torch.randn(H, generator=gen).cuda()
+        d = inputs.workload_inputs(w)
+        self.v, self.la, self.beta = d["v"].cuda(), d["logalpha"].cuda(), d["beta"].cuda()
+        self.out = {"o": torch.empty((B, T, H, dv), dtype=w.dtype, device="cuda"),
+                    "ST": torch.empty((B, H, dv, dk), dtype=torch.float32, device="cuda"),
+                    "CT": torch.empty((B, H, dk, dk), dtype=torch.float32, device="cuda"),
+                    "muT": torch.empty((B, H, dk), dtype=torch.float32, device="cuda")}
+        shape = ccq.make_shape(B, T, H, dk, dv, w.dtype, w.dtype)
+        self.ws = torch.empty(max(1, ccq.ccq_fwd_raw_workspace_size(shape, 1)), dtype=torch.uint8,
+                              device="cuda")
+        self.ccq = ccq
+        self.kernels = ["prep_scales"] + KERNELS[1]
+
+    def __call__(self):
+        self.ccq.ccq_fwd_raw(self.q, self.k, self.wl, self.bl, self.v, self.la, self.beta,
+                             backbone=1, out=self.out, workspace=self.ws)
+
+
 class VarlenCall:
     """The Gated DeltaNet forward on a packed batch: 2B sequences of lengths uniform in
     [T/4, 3T/4] (about the tokens of the B x T workload), read by the kernels straight
@@ -550,7 +584,7 @@ def roofline(entry, w):
 
 EXTRA = ("gla_500m_t2k", "gdn_1p3b_t4k", "gla_500m_t20k", "gdn_1p3b_t20k", "gla_train_t4k",
          "gdn_train_t4k", "gla_500m_decode_t2k", "gdn_1p3b_decode_t4k", "gdn_1p3b_prep_t4k",
-         "gdn_1p3b_varlen_t4k")
+         "gdn_1p3b_raw_t4k", "gdn_1p3b_varlen_t4k")
 
 
 def measure_extra(name, torch, ccq, inputs, steps, existing):
@@ -564,6 +598,14 @@ def measure_extra(name, torch, ccq, inputs, steps, existing):
                "ms_traced": round(ms_tr, 5),
                "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
                "roofline": roofline(pk[0], c.w)}
+    elif "_raw_" in name:
+        c = RawCall(W[name.replace("_raw_t", "_t")], torch, ccq, inputs)
+        ms, ms_tr, pk = time_calls(torch, ccq, [c], max(5, steps // 2), 3, with_plain=True)
+        dom = max(pk, key=lambda e: e["ms_mean"])
+        res = {"tokens_per_s": round(c.w.tokens / (ms * 1e-3), 1), "ms": round(ms, 4),
+               "ms_traced": round(ms_tr, 4),
+               "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
+               "roofline": method_roofline(c.w, c.ms_call), "dominant_kernel": roofline(dom, c.w)}
     elif "_varlen_" in name:
         c = VarlenCall(W[name.replace("_varlen_t", "_t")], torch, ccq, inputs)
         ms, ms_tr, pk = time_calls(torch, ccq, [c], max(5, steps // 2), 3, with_plain=True)

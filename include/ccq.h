@@ -193,6 +193,31 @@ ccq_status ccq_prep(const ccq_shape* s, const void* q_raw, const void* k_raw, co
                     const float* b_lam, void* q, void* k, float* lam, void* stream);
 
 /*
+ * Forward from the raw queries and keys: Alg. 1's per-chunk l2 normalisation
+ * of Q and K and the gate Lambda = sigma(Q W_lambda^T + b_lambda) (Eq. clean)
+ * folded into the forward, with the results of ccq_prep followed by
+ * ccq_gla_fwd (bb = CCQ_GLA) or ccq_gdn_fwd (bb = CCQ_GDN), but without the
+ * normalised q and k ever being written: a first pass reads the raw rows once
+ * and writes only the per-row scales 1 / max(|x|, 1e-12) and the gate
+ * (3 floats per token and head, in the workspace), and every kernel of the
+ * forward scales the raw rows as it stages them.
+ *   q_raw, k_raw [B,T,H,dk] io_dtype; w_lam [H, H*dk] fp32; b_lam [H] fp32 (as
+ *   ccq_prep); v, the gates, S0, C0, mu0, o, ST, CT, muT as in the forward
+ *   entry points (beta required for CCQ_GDN, NULL for CCQ_GLA);
+ *   lam_out [B,T,H] fp32 or NULL: the gate, if the caller wants it.
+ * The workspace holds ccq_fwd_raw_workspace_size(s, bb) bytes (0 for an
+ * unsupported shape).  Shape limits are those of both the forward and
+ * ccq_prep (H <= 16, H*dk <= 2048, H*H*dk <= 16384); q_clean export is not
+ * offered here.
+ */
+size_t ccq_fwd_raw_workspace_size(const ccq_shape* s, ccq_backbone bb);
+ccq_status ccq_fwd_raw(const ccq_shape* s, ccq_backbone bb, const void* q_raw, const void* k_raw,
+                       const float* w_lam, const float* b_lam, const void* v,
+                       const void* g_or_logalpha, const float* beta, const float* S0,
+                       const float* C0, const float* mu0, void* o, float* ST, float* CT, float* muT,
+                       float* lam_out, void* workspace, size_t ws_bytes, void* stream);
+
+/*
  * Packed batches of sequences of different lengths: Alg. 1 (and its
  * training step) applied to every sequence on its own, each an independent
  * recurrence with its own states, exactly as if each were a call of its own.

@@ -25,6 +25,7 @@ _STATUS = {0: "CCQ_OK", 1: "CCQ_ERR_INVALID_ARG", 2: "CCQ_ERR_UNSUPPORTED",
 EXPORTS = ("ccq_workspace_size", "ccq_gla_fwd", "ccq_gdn_fwd", "ccq_gdn_fwd_noalloc", "ccq_fwd_bwd",
            "ccq_varlen_workspace_size", "ccq_gla_fwd_varlen", "ccq_gdn_fwd_varlen",
            "ccq_fwd_bwd_varlen", "ccq_decode_workspace_size", "ccq_decode", "ccq_prep",
+           "ccq_fwd_raw_workspace_size", "ccq_fwd_raw",
            "ccq_trace_events", "ccq_status_string", "ccq_version")
 
 
@@ -82,6 +83,10 @@ def lib() -> ctypes.CDLL:
             L.ccq_decode.restype = ctypes.c_int
             L.ccq_prep.argtypes = [SP] + [P] * 8
             L.ccq_prep.restype = ctypes.c_int
+            L.ccq_fwd_raw_workspace_size.argtypes = [SP, ctypes.c_int]
+            L.ccq_fwd_raw_workspace_size.restype = S
+            L.ccq_fwd_raw.argtypes = [SP, ctypes.c_int] + [P] * 15 + [P, S, P]
+            L.ccq_fwd_raw.restype = ctypes.c_int
             L.ccq_trace_events.argtypes = [P, ctypes.c_int]
             L.ccq_trace_events.restype = ctypes.c_int
             L.ccq_status_string.argtypes = [ctypes.c_int]
@@ -521,4 +526,55 @@ def ccq_prep(q_raw, k_raw, w_lam, b_lam, out=None, stream=None):
     _record(stream, out)
     if rc != 0:
         raise CcqError("ccq_prep", rc)
+    return out
+
+
+def ccq_fwd_raw_workspace_size(shape: Shape, backbone: int) -> int:
+    return int(lib().ccq_fwd_raw_workspace_size(ctypes.byref(shape), int(backbone)))
+
+
+def ccq_fwd_raw(q_raw, k_raw, w_lam, b_lam, v, gate, beta=None, backbone=CCQ_GLA, S0=None, C0=None,
+                mu0=None, scale=1.0, centered=True, t0=0, chunk=64, want_states=True,
+                want_lam=False, out=None, workspace=None, stream=None):
+    """Forward from raw q, k [B,T,H,dk]: the l2 normalisation and the gate
+    lam = sigmoid(w_lam qraw + b_lam) (w_lam [H, H*dk], b_lam [H] fp32) folded into the
+    forward.  gate: the GLA log-forget gate [B,T,H,dk], or Gated DeltaNet log alpha
+    [B,T,H] fp32 with beta [B,T,H] fp32.  Returns dict o[, ST, CT, muT][, lam]."""
+    B, T, H, dk = q_raw.shape
+    dv = v.shape[-1]
+    dev = q_raw.device
+    gate_dtype = gate.dtype if backbone == CCQ_GLA else q_raw.dtype
+    shape = make_shape(B, T, H, dk, dv, q_raw.dtype, gate_dtype, scale, centered, t0, chunk)
+    _check(k_raw, "k_raw", (B, T, H, dk), q_raw.dtype, dev)
+    _check(v, "v", (B, T, H, dv), q_raw.dtype, dev)
+    _check(w_lam, "w_lam", (H, H * dk), torch.float32, dev)
+    _check(b_lam, "b_lam", (H,), torch.float32, dev)
+    if backbone == CCQ_GLA:
+        _check(gate, "g", (B, T, H, dk), gate.dtype, dev)
+    else:
+        if beta is None:
+            raise ValueError("beta is required for Gated DeltaNet")
+        _check(gate, "logalpha", (B, T, H), torch.float32, dev)
+        _check(beta, "beta", (B, T, H), torch.float32, dev)
+    _check(S0, "S0", (B, H, dv, dk), torch.float32, dev)
+    _check(C0, "C0", (B, H, dk, dk), torch.float32, dev)
+    _check(mu0, "mu0", (B, H, dk), torch.float32, dev)
+    out = dict(out or {})
+    out.setdefault("o", torch.empty((B, T, H, dv), dtype=q_raw.dtype, device=dev))
+    if want_states:
+        out.setdefault("ST", torch.empty((B, H, dv, dk), dtype=torch.float32, device=dev))
+        out.setdefault("CT", torch.empty((B, H, dk, dk), dtype=torch.float32, device=dev))
+        out.setdefault("muT", torch.empty((B, H, dk), dtype=torch.float32, device=dev))
+    if want_lam:
+        out.setdefault("lam", torch.empty((B, T, H), dtype=torch.float32, device=dev))
+    need = ccq_fwd_raw_workspace_size(shape, backbone)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    rc = lib().ccq_fwd_raw(ctypes.byref(shape), int(backbone), _p(q_raw), _p(k_raw), _p(w_lam),
+                           _p(b_lam), _p(v), _p(gate), _p(beta), _p(S0), _p(C0), _p(mu0),
+                           _p(out["o"]), _p(out.get("ST")), _p(out.get("CT")), _p(out.get("muT")),
+                           _p(out.get("lam")), _p(workspace), workspace.numel(), _stream(stream))
+    _record(stream, workspace, out)
+    if rc != 0:
+        raise CcqError("ccq_fwd_raw", rc)
     return out

@@ -287,7 +287,8 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
                        const void* v, const void* g_or_la, const float* beta, const float* lam,
                        const float* S0, const float* C0, const float* mu0, void* o, float* ST,
                        float* CT, float* muT, float* q_clean_dbg, void* workspace,
-                       size_t ws_bytes, void* stream, const int32_t* cu = nullptr) {
+                       size_t ws_bytes, void* stream, const int32_t* cu = nullptr,
+                       const float* rq = nullptr, const float* rk = nullptr) {
   ccq_status rc = check_forward_args(bb, s, q, k, v, g_or_la, beta, lam, S0, C0, mu0, o, ST, CT,
                                      muT, q_clean_dbg, workspace);
   if (rc != CCQ_OK) return rc;
@@ -309,6 +310,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   if (bb == CCQ_GDN) {
     ccq::TriArgs ta{k, la, beta, ws + L.Tm, gam, s->B, s->T, s->H, s->dk, s->dv};
     ta.cu = cu;
+    ta.rk = rk;
     if (traced(st, [&] { return ccq::launch_gdn_tri(ta, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   }
   if (bb == CCQ_GLA) {
@@ -316,6 +318,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
     // totals gives every segment's entry state and S_T
     ccq::GlaStateArgs sa{k, v, g_or_la, S0, ST, ws + L.states, s->B, s->T, s->H, s->dk, s->dv};
     sa.cu = cu;
+    sa.rk = rk;
     if (L.gla_seg > 0) {
       sa.seg = L.gla_seg;
       sa.ST = nullptr;
@@ -346,6 +349,8 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   ca.C0 = C0;
   ca.mu0 = mu0;
   ca.cu = cu;
+  ca.rq = rq;
+  ca.rk = rk;
   ca.qclean = qclean;
   ca.qclean_dbg = q_clean_dbg;
   ca.CT = CT;
@@ -357,6 +362,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   if (bb == CCQ_GLA) {
     ccq::GlaOutArgs oa{qclean, k, v, g_or_la, ws + L.states, o, s->B, s->T, s->H, s->dk, s->dv, s->scale};
     oa.cu = cu;
+    oa.rk = rk;
     if (L.gla_seg > 0) {
       oa.seg = L.gla_seg;
       oa.entries = ws + L.entries;
@@ -368,6 +374,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
                        s->scale};
     oa.group = ccq::gdn_out_group(s->B, s->H, s->T, s->dk, s->dv, bf);
     oa.cu = cu;
+    oa.rk = rk;
     if (traced(st, [&] { return ccq::launch_gdn_out(oa, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   }
   return CCQ_OK;
@@ -517,6 +524,21 @@ ccq_status varlen_forward(ccq_backbone bb, const ccq_shape* s, const int32_t* cu
                      workspace, ws_bytes, stream, cu);
 }
 
+// Forward from raw q, k: the row scales 1 / |q|, 1 / |k| and the gate, then
+// the forward workspace.
+struct RawLayout {
+  size_t rq = 0, rk = 0, lam = 0, inner = 0;
+};
+RawLayout raw_layout(const ccq_shape* s) {
+  RawLayout L;
+  const size_t n = (size_t)s->B * s->T * s->H * sizeof(float);
+  L.rq = 0;
+  L.rk = align_up(n);
+  L.lam = 2 * align_up(n);
+  L.inner = 3 * align_up(n);
+  return L;
+}
+
 // Scratch of the allocation-free forward (ccq_gdn_fwd_noalloc): a device array
 // of kScratchBytes, one copy on every device the library runs on, held until the
 // process ends.  In host code `scratch` names a host-side stand-in, not device
@@ -596,6 +618,51 @@ ccq_status ccq_gdn_fwd(const ccq_shape* s, const void* q, const void* k, const v
                        size_t ws_bytes, void* stream) {
   return run_forward(CCQ_GDN, s, q, k, v, logalpha, beta, lam, S0, C0, mu0, o, ST, CT, muT,
                      q_clean_dbg, workspace, ws_bytes, stream);
+}
+
+size_t ccq_fwd_raw_workspace_size(const ccq_shape* s, ccq_backbone bb) {
+  if (check_shape(s, bb) != CCQ_OK || !ccq::prep_supported(s->H, s->dk)) return 0;
+  return raw_layout(s).inner + fwd_layout(s, bb).total;
+}
+
+ccq_status ccq_fwd_raw(const ccq_shape* s, ccq_backbone bb, const void* q_raw, const void* k_raw,
+                       const float* w_lam, const float* b_lam, const void* v,
+                       const void* g_or_logalpha, const float* beta, const float* S0,
+                       const float* C0, const float* mu0, void* o, float* ST, float* CT, float* muT,
+                       float* lam_out, void* workspace, size_t ws_bytes, void* stream) {
+  ccq_status rc = check_shape(s, bb);
+  if (rc != CCQ_OK) return rc;
+  const size_t ntok = (size_t)s->B * s->T * s->H;
+  const void* opt[] = {S0, C0, mu0, ST, CT, muT, lam_out, workspace};
+  for (const void* p : opt)
+    if (p && !aligned(p)) return CCQ_ERR_INVALID_ARG;
+  if (ntok > 0) {
+    const void* req[] = {q_raw, k_raw, w_lam, b_lam, v, g_or_logalpha, o};
+    for (const void* p : req)
+      if (!p || !aligned(p)) return CCQ_ERR_INVALID_ARG;
+    if (bb == CCQ_GDN && (!beta || !aligned(beta))) return CCQ_ERR_INVALID_ARG;
+    if (!ccq::prep_supported(s->H, s->dk)) return CCQ_ERR_UNSUPPORTED;
+    if ((long long)s->B * s->T / 16 >= (1LL << 31)) return CCQ_ERR_UNSUPPORTED;
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (s->B == 0 || s->H == 0) return CCQ_OK;
+  if (s->T == 0) return copy_initial_states(s, S0, C0, mu0, ST, CT, muT, st);
+  const RawLayout R = raw_layout(s);
+  if (!workspace || ws_bytes < R.inner + fwd_layout(s, bb).total) return CCQ_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  float* rq = reinterpret_cast<float*>(ws + R.rq);
+  float* rk = reinterpret_cast<float*>(ws + R.rk);
+  float* lam = lam_out ? lam_out : reinterpret_cast<float*>(ws + R.lam);
+  TraceScope scope;
+  // the gate and the row scales (no normalised rows are written) ...
+  ccq::PrepArgs pa{q_raw, k_raw, w_lam, b_lam, nullptr, nullptr, lam, s->B, s->T, s->H, s->dk};
+  pa.rq = rq;
+  pa.rk = rk;
+  if (traced(st, [&] { return ccq::launch_prep(pa, s->io_dtype == CCQ_BF16, st); }) != hipSuccess)
+    return CCQ_ERR_HIP;
+  // ... then the forward, every kernel scaling the raw rows as it stages them
+  return run_forward(bb, s, q_raw, k_raw, v, g_or_logalpha, beta, lam, S0, C0, mu0, o, ST, CT, muT,
+                     nullptr, ws + R.inner, ws_bytes - R.inner, stream, nullptr, rq, rk);
 }
 
 ccq_status ccq_gdn_fwd_noalloc(const ccq_shape* s, const void* q, const void* k, const void* v,

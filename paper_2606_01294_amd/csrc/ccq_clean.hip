@@ -82,14 +82,17 @@ __global__ __launch_bounds__(64 * (DK >= 128 ? 8 : 4), 1) void clean_gram_kernel
   }
 
   RowTile<T, DK, NTG> rk;
+  RowScales<RowTile<T, DK, NTG>> fk;
   auto load = [&](int c) {
     rk.load(k + seq_off(sq, c * C, h, a.H, DK), gstride, min(C, sq.len - c * C));
+    if (a.rk) fk.load(a.rk + seq_idx(sq, c * C, h, a.H), (size_t)a.H, min(C, sq.len - c * C));
   };
   if (cbeg < cend) load(cbeg);
   const Frag<T> ones = ones_col_frag<T>();
 
   for (int c = cbeg; c < cend; ++c) {
     T* buf = sK[(c - cbeg) & 1];  // the other buffer may still be read by a slower wave
+    if (a.rk) fk.apply(rk);
     rk.store(buf, LDK);
     if (c + 1 < cend) load(c + 1);
     __syncthreads();
@@ -276,8 +279,19 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
 
   Tile rx, rk;
   RowScalar rl;
+  // row scales of raw q and k (l2 normalisation folded in), for the rows of
+  // this thread's staged vectors
+  float fq[NV], fk[NV];
   auto prefetch = [&](int c) {
     const int r0 = c * C, n = min(C, sq.len - r0);
+    if (a.rq) {
+#pragma unroll
+      for (int u = 0; u < NV; ++u) {
+        const int row = min((tid + NT * u) / VPR, n - 1);
+        fq[u] = a.rq[seq_idx(sq, r0 + row, h, a.H)];
+        fk[u] = a.rk[seq_idx(sq, r0 + row, h, a.H)];
+      }
+    }
     if constexpr (kDma) {
       LdsStream<DK, NW>::load(x + seq_off(sq, r0, h, a.H, DK), gstride, n, sSt);
       LdsStream<DK, NW>::load(k + seq_off(sq, r0, h, a.H, DK), gstride, n, sSt + C * DK);
@@ -359,6 +373,13 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
           *reinterpret_cast<vec_t*>(qc + seq_off(sw, r0 - C + row, h, a.H, DK) + col) =
               *reinterpret_cast<const vec_t*>(px);
         vec_t y;
+        if (a.rq) {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            xv[u][q] = to<T>(f32(xv[u][q]) * fq[u]);
+            kv[u][q] = to<T>(f32(kv[u][q]) * fk[u]);
+          }
+        }
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
           xv[u][q] = row < nrow ? xv[u][q] : to<T>(0.f);

@@ -437,6 +437,7 @@ struct RowTile {
   static constexpr int TOT = kChunk * VPR;            // vectors in the tile
   static constexpr int NV = (TOT + NT - 1) / NT;      // vectors per thread
   static_assert(D % VE == 0, "row split");
+  typedef T elem_t;
   typedef T vec_t __attribute__((ext_vector_type(VE)));
   vec_t v[NV];
   uint32_t ok;  // bit u: vector u exists and its row lies inside the sequence
@@ -465,6 +466,30 @@ struct RowTile {
 #pragma unroll
     for (int u = 0; u < NV; ++u)
       if (mine(u)) *reinterpret_cast<vec_t*>(dst + row(u) * ld + col(u)) = get(u);
+  }
+};
+
+// Per-row scale factors of a RowTile's vectors (a row's l2 normalisation
+// 1 / |x|), loaded beside the tile so that their latency overlaps its own.
+// `sc` points at the factor of the tile's row 0 and consecutive rows are
+// `stride` apart; rows >= n repeat row n - 1, as the tile does.
+template <typename Tile>
+struct RowScales {
+  float f[Tile::NV];
+  __device__ __forceinline__ void load(const float* sc, size_t stride, int n) {
+#pragma unroll
+    for (int u = 0; u < Tile::NV; ++u)
+      if (Tile::mine(u)) {
+        const int r = Tile::row(u);
+        f[u] = sc[(size_t)(r < n ? r : n - 1) * stride];
+      }
+  }
+  __device__ __forceinline__ void apply(Tile& t) const {
+#pragma unroll
+    for (int u = 0; u < Tile::NV; ++u)
+      if (Tile::mine(u))
+#pragma unroll
+        for (int e = 0; e < Tile::VE; ++e) t.v[u][e] = to<typename Tile::elem_t>(f32(t.v[u][e]) * f[u]);
   }
 };
 

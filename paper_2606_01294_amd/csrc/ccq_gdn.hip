@@ -63,13 +63,17 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
 
   // all global loads first (K, the log decays and beta), one round trip
   RowTile<T, DK> rk;
+  RowScales<RowTile<T, DK>> fk;  // raw keys: row scales (l2 normalisation)
   rk.load(static_cast<const T*>(a.k) + seq_off(sq, r0, h, a.H, DK), (size_t)a.H * DK, nrow);
-  float la = 0.f, bt = 0.f;
+  if (a.rk) fk.load(a.rk + seq_idx(sq, r0, h, a.H), (size_t)a.H, nrow);
+  float la = 0.f, bt = 0.f, rkt = 1.f;
   if (tid < C) {
     const size_t ti = seq_idx(sq, r0 + (tid < nrow ? tid : nrow - 1), h, a.H);
     la = a.logalpha[ti];
     bt = a.beta[ti];
+    if (a.rk) rkt = a.rk[ti];
   }
+  if (a.rk) fk.apply(rk);
   rk.store(sK, LDQ);
   if (tid < C) {
     float x = tid < nrow ? la : 0.f;
@@ -84,9 +88,11 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
     sBeta[tid] = bt;
     float* cf = a.gam + ((size_t)bh * N + ci) * 5 * C + tid;
     cf[0] = x;                      // gamma_j
-    cf[C] = bt * __expf(x);         // beta_j e^{gamma_j}
+    // (with raw keys the two coefficients that multiply key rows carry the
+    // row's l2 normalisation)
+    cf[C] = bt * __expf(x) * rkt;   // beta_j e^{gamma_j}
     cf[2 * C] = bt;                 // beta_j
-    cf[3 * C] = __expf(gC - x);     // e^{gamma_C - gamma_j}
+    cf[3 * C] = __expf(gC - x) * rkt;  // e^{gamma_C - gamma_j}
     cf[4 * C] = __expf(gC);         // e^{gamma_C}
   }
   __syncthreads();
@@ -726,6 +732,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
   __shared__ __align__(16) T sP[C * LDP];  // P[i][acc_pos(j)]
   __shared__ __align__(16) float sGam[C];
   __shared__ __align__(16) float sDd[C + 4];  // e^{gamma_C - gamma_j}; e^{gamma_C} at C
+  __shared__ float sRk[C];                    // raw keys: row scales of the scores
 
   const int N = (a.T + C - 1) / C;
   const int R = CARRY ? a.group : 1, NGR = (N + R - 1) / R;
@@ -754,6 +761,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
       rk.load(static_cast<const T*>(a.k) + seq_off(sq, r0, h, a.H, DK), gstride, nrow);
       const float* gm = a.gam + ((size_t)bh * N + ci) * 5 * C;
       if (tid < C) sGam[tid] = gm[tid];
+      if (a.rk && tid < C) sRk[tid] = a.rk[seq_idx(sq, r0 + (tid < nrow ? tid : nrow - 1), h, a.H)];
       if (carry && tid < C + 1) sDd[tid] = tid < C ? gm[3 * C + tid] : gm[4 * C];
       rq.store(sQ, LDQ);
       rk.store(sK, LDQ);
@@ -793,7 +801,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int j = 16 * J + 4 * g4 + r;
-          x[r] = j <= i ? sc[r] * __expf(gi - sGam[j]) : 0.f;
+          x[r] = j <= i ? sc[r] * __expf(gi - sGam[j]) * (a.rk ? sRk[j] : 1.f) : 0.f;
         }
       }
       store4(sP + i * LDP + acc_pos(16 * J + 4 * g4), x[0], x[1], x[2], x[3]);

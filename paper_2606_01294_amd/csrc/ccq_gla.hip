@@ -73,12 +73,14 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
   }
 
   RowTile<T, BK> rk;
+  RowScales<RowTile<T, BK>> fk;  // raw keys: row scales (l2 normalisation)
   RowTile<TG, BK> rg;
   RowTile<T, VB> rv;
   auto prefetch = [&](int ci) {
     const int r0 = ci * C;
     const int nrow = (sq.len - r0) < C ? (sq.len - r0) : C;
     rk.load(k + seq_off(sq, r0, h, a.H, a.dk) + c0, (size_t)a.H * a.dk, nrow);
+    if (a.rk) fk.load(a.rk + seq_idx(sq, r0, h, a.H), (size_t)a.H, nrow);
     rg.load(gate + seq_off(sq, r0, h, a.H, a.dk) + c0, (size_t)a.H * a.dk, nrow);
     rv.load(v + seq_off(sq, r0, h, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
   };
@@ -96,6 +98,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
   for (int it = 0; it < nch; ++it) {
     const int ci = kRev ? ce - 1 - it : cb + it;
     const int buf = it & 1;  // the other buffer was released at the previous barrier
+    if (a.rk) fk.apply(rk);
     rk.store(sK[buf], LDK);
     rg.store(sG[buf], LDG);
     rv.store(sV[buf], LDV);
@@ -239,10 +242,12 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
   const bool ent = sg > 0 && a.entries;
 
   RowTile<T, DK, NT> rq, rk;
+  RowScales<RowTile<T, DK, NT>> fk;  // raw keys: row scales (l2 normalisation)
   RowTile<TG, DK, NT> rg;
   const Seq sw{(long long)b * a.T, sq.len};  // q_clean: the workspace's padded rows
   rq.load(static_cast<const T*>(a.qc) + seq_off(sw, r0, h, a.H, DK), gstride, nrow);
   rk.load(static_cast<const T*>(a.k) + seq_off(sq, r0, h, a.H, DK), gstride, nrow);
+  if (a.rk) fk.load(a.rk + seq_idx(sq, r0, h, a.H), (size_t)a.H, nrow);
   rg.load(static_cast<const TG*>(a.g) + seq_off(sq, r0, h, a.H, DK), gstride, nrow);
 #pragma unroll
   for (int u = 0; u < RowTile<TG, DK, NT>::NV; ++u) {  // gates as fp32 rows
@@ -274,6 +279,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
     }
   }
   __syncthreads();
+  if (a.rk) fk.apply(rk);
   // Qt = q e^{b - b_m}, Kt = k e^{b_m - b}
 #pragma unroll
   for (int u = 0; u < RowTile<T, DK, NT>::NV; ++u) {

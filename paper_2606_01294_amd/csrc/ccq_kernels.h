@@ -48,6 +48,10 @@ struct CleanArgs {
   // tensors (length cut at T), or null for a padded [B, T, H, d] batch; the
   // workspace keeps its padded per-chunk layout either way
   const int* cu = nullptr;
+  // raw q, k with per-row l2 normalisation folded in: token t, head h is scaled
+  // by rq / rk [rows, H] fp32 (1 / max(|x|, eps)) as it is staged, or null
+  const float* rq = nullptr;
+  const float* rk = nullptr;
 };
 
 // GLA state recurrence (sequential over chunks) for one 64-channel tile of S.
@@ -73,6 +77,7 @@ struct GlaStateArgs {
   float* cdec;        // [B*H, N, dk] fp32: e^{log decays of the segment before each chunk}
   float scale;        // read scale (the reverse scan of the training step only)
   const int* cu = nullptr;  // packed-batch offsets (device), as CleanArgs
+  const float* rk = nullptr;  // key row scales, as CleanArgs
 };
 
 // Entry state of every segment, E_0 = 0 (S0 is inside segment 0's states),
@@ -99,6 +104,7 @@ struct GlaOutArgs {
   const void* entries;  // [B*H, NS, dv, dk] io, or null with one segment
   const float* cdec;    // [B*H, N, dk] fp32, or null with one segment
   const int* cu = nullptr;  // packed-batch offsets (device), as CleanArgs
+  const float* rk = nullptr;  // key row scales, as CleanArgs
 };
 
 // Gated DeltaNet chunk transform (chunk-parallel): Tm = (I + A)^{-1} and the
@@ -113,6 +119,10 @@ struct TriArgs {
                          // e^{gamma_C - gamma_j}, e^{gamma_C}
   int B, T, H, dk, dv;
   const int* cu = nullptr;  // packed-batch offsets [B+1] (device), as CleanArgs, or null
+  // key row scales, as CleanArgs: the keys of A are scaled as staged, and the
+  // coefficients beta e^gamma and e^{gamma_C - gamma} that multiply key rows
+  // in the state pass and the output kernel's carry are stored times rk
+  const float* rk = nullptr;
 };
 
 // Gated DeltaNet state recurrence (sequential over chunks): writes the
@@ -148,6 +158,7 @@ struct GdnOutArgs {
   float scale;
   int group = 1;
   const int* cu = nullptr;  // as TriArgs
+  const float* rk = nullptr;  // key row scales (the scores'; the carry's come with the coefficients)
 };
 
 // ---- training step (CCQ-GLA backward) ----
@@ -282,10 +293,13 @@ struct PrepArgs {
   const void* k_raw;     // [B,T,H,dk] io
   const float* w;        // [H, H*dk] fp32
   const float* b;        // [H] fp32
-  void* q;               // [B,T,H,dk] io (may be q_raw)
-  void* k;               // [B,T,H,dk] io (may be k_raw)
+  void* q;               // [B,T,H,dk] io (may be q_raw), or null with rq
+  void* k;               // [B,T,H,dk] io (may be k_raw), or null with rk
   float* lam;            // [B,T,H] fp32
   int B, T, H, dk;
+  // instead of the normalised rows: the row scales 1 / max(|x|, 1e-12) [B,T,H]
+  float* rq = nullptr;
+  float* rk = nullptr;
 };
 
 // Each launcher returns hipSuccess or the launch error.  is_bf16 selects the

@@ -7,7 +7,9 @@
 // squared norms over the aligned lane group holding that head, writes the
 // normalised pieces and accumulates every gate's partial dot product
 // z[h'] += W[h'][j] q[j] over its pieces; the H partial dots are then reduced
-// over the wave and lane h' writes lambda[h'].  W (H x H dk, fp32) is staged
+// over the wave and lane h' writes lambda[h'].  Without output rows (q and k
+// null) the kernel writes the row scales 1 / max(|x|, 1e-12) instead, for a
+// forward that normalises as it stages the raw rows.  W (H x H dk, fp32) is staged
 // in LDS once per workgroup and shared by its 16 tokens.  A wave reads each raw row before it writes the
 // normalised one, so the outputs may overwrite the inputs.
 #include "ccq_device.h"
@@ -104,14 +106,19 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(const PrepArgs a) {
       kk = lane_group_sum<(PPH < 64 ? PPH : 64)>(kk);
       if (p < NP) {
         const float iq = 1.f / fmaxf(sqrtf(qq), 1e-12f), ik = 1.f / fmaxf(sqrtf(kk), 1e-12f);
-        v8 yq, yk;
+        if (qo) {
+          v8 yq, yk;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          yq[e] = to<T>(qf[e] * iq);
-          yk[e] = to<T>(kf[e] * ik);
+          for (int e = 0; e < 8; ++e) {
+            yq[e] = to<T>(qf[e] * iq);
+            yk[e] = to<T>(kf[e] * ik);
+          }
+          *reinterpret_cast<v8*>(qo + base + 8 * p) = yq;
+          *reinterpret_cast<v8*>(ko + base + 8 * p) = yk;
+        } else if (p % PPH == 0) {  // the row scales instead, from the head's first lane
+          a.rq[(size_t)tok * H + p / PPH] = iq;
+          a.rk[(size_t)tok * H + p / PPH] = ik;
         }
-        *reinterpret_cast<v8*>(qo + base + 8 * p) = yq;
-        *reinterpret_cast<v8*>(ko + base + 8 * p) = yk;
 #pragma unroll
         for (int g = 0; g < HMAX; ++g) {
           if (g < H) {

@@ -114,6 +114,25 @@ def test_noalloc_validation_before_launch():
     assert call_gdn_noalloc(shape(B=0, dk=256), ptr=0, beta_ptr=0) == 0
 
 
+def test_forward_from_raw_validation():
+    """ccq_fwd_raw: workspace = the forward's plus three floats per token and head; the
+    pre-processing limits apply; errors before any launch."""
+    P = ctypes.c_void_p
+    s = shape(dk=128)
+    ws = ccq.ccq_fwd_raw_workspace_size(s, ccq.CCQ_GLA)
+    assert ws >= ccq.ccq_workspace_size(s, ccq.CCQ_GLA) + 3 * 2 * 100 * 3 * 4
+    assert ccq.ccq_fwd_raw_workspace_size(shape(H=32, dk=64), ccq.CCQ_GLA) == 0  # W_lambda too large
+
+    def call(s, bb=0, w=FAKE, beta=None, ws_bytes=1 << 30):
+        return ccq.lib().ccq_fwd_raw(ctypes.byref(s), bb, P(FAKE), P(FAKE), P(w), P(FAKE), P(FAKE),
+                                     P(FAKE), P(beta), None, None, None, P(FAKE), None, None, None,
+                                     None, P(FAKE), ws_bytes, None)
+    assert call(shape(), w=0) == 1                          # W_lambda required
+    assert call(shape(dk=256), bb=1) == 1                   # Gated DeltaNet needs beta
+    assert call(shape(H=32, dk=64)) == 2                    # W_lambda does not fit on chip
+    assert call(shape(), ws_bytes=64) == 3
+
+
 def test_binding_rejects_wrong_dtype_before_calling():
     import torch
     q = torch.zeros(1, 4, 1, 64)
