@@ -2,12 +2,13 @@
 // the l2 normalisation of Q and K and the gate Lambda = sigma(Q W_lambda^T + b_lambda)
 // from the query before the head split; Eq. clean for the gate).
 //
-// One wave per token: it requests the token's whole q and k rows at once
+// Each wave takes four tokens: it requests their whole q and k rows at once
 // (16-byte pieces, consecutive lanes along the row), reduces each head's
-// squared norms over the aligned lane group holding that head, writes the
-// normalised pieces and accumulates every gate's partial dot product
-// z[h'] += W[h'][j] q[j] over its pieces; the H partial dots are then reduced
-// over the wave and lane h' writes lambda[h'].  Without output rows (q and k
+// squared norms over the aligned lane group holding that head and writes the
+// normalised pieces; then every gate's partial dot products
+// z[h'] += W[h'][j] q[j] over the lane's pieces, each piece of W read from LDS
+// once for the four tokens; the H partial dots are reduced over the wave and
+// lane h' writes lambda[h'].  Without output rows (q and k
 // null) the kernel writes the row scales 1 / max(|x|, 1e-12) instead, for a
 // forward that normalises as it stages the raw rows.  W (H x H dk, fp32) is staged
 // in LDS once per workgroup and shared by its 16 tokens.  A wave reads each raw row before it writes the
@@ -80,24 +81,20 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(const PrepArgs a) {
       }
     }
   }
+  // norms of every token's head rows; normalised rows (or the row scales) out
 #pragma unroll
   for (int tt = 0; tt < TPW; ++tt) {
     const long long tok = (long long)blockIdx.x * kPrepTokens + w * TPW + tt;
     if (tok >= ntok) break;
     const size_t base = (size_t)tok * E;
-    const v8* qv = qa[tt];
-    const v8* kv = ka[tt];
-    float z[HMAX];
-#pragma unroll
-    for (int g = 0; g < HMAX; ++g) z[g] = 0.f;
 #pragma unroll
     for (int i = 0; i < NPMAX; ++i) {
       const int p = l + 64 * i;
       float qf[8], kf[8], qq = 0.f, kk = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        qf[e] = p < NP ? f32(qv[i][e]) : 0.f;
-        kf[e] = p < NP ? f32(kv[i][e]) : 0.f;
+        qf[e] = p < NP ? f32(qa[tt][i][e]) : 0.f;
+        kf[e] = p < NP ? f32(ka[tt][i][e]) : 0.f;
         qq += qf[e] * qf[e];
         kk += kf[e] * kf[e];
       }
@@ -119,24 +116,66 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(const PrepArgs a) {
           a.rq[(size_t)tok * H + p / PPH] = iq;
           a.rk[(size_t)tok * H + p / PPH] = ik;
         }
+      }
+    }
+  }
+  // the gates: every W piece read from LDS serves all TPW tokens of the wave
+  float z[TPW][HMAX];
 #pragma unroll
-        for (int g = 0; g < HMAX; ++g) {
-          if (g < H) {
-            const f32x4 w0 = *reinterpret_cast<const f32x4*>(sW + g * E + 4 * p);
-            const f32x4 w1 = *reinterpret_cast<const f32x4*>(sW + g * E + E / 2 + 4 * p);
+  for (int tt = 0; tt < TPW; ++tt)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) z[g] += w0[e] * qf[e] + w1[e] * qf[4 + e];
-          }
+    for (int g = 0; g < HMAX; ++g) z[tt][g] = 0.f;
+#pragma unroll
+  for (int i = 0; i < NPMAX; ++i) {
+    const int p = l + 64 * i;
+    if (p < NP) {
+      float qf[TPW][8];
+#pragma unroll
+      for (int tt = 0; tt < TPW; ++tt)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qf[tt][e] = f32(qa[tt][i][e]);
+#pragma unroll
+      for (int g = 0; g < HMAX; ++g) {
+        if (g < H) {
+          const f32x4 w0 = *reinterpret_cast<const f32x4*>(sW + g * E + 4 * p);
+          const f32x4 w1 = *reinterpret_cast<const f32x4*>(sW + g * E + E / 2 + 4 * p);
+#pragma unroll
+          for (int tt = 0; tt < TPW; ++tt)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) z[tt][g] += w0[e] * qf[tt][e] + w1[e] * qf[tt][4 + e];
         }
       }
     }
+  }
+  // sums over the wave of the TPW x HMAX partial dots by a reduce-scatter
+  // butterfly: at each step a lane keeps half of its values, adds its
+  // partner's copy of them and hands over the other half, so that after
+  // log2(TPW HMAX) steps lane l holds the partial sum of value l % (TPW HMAX)
+  // over the lanes that share its low bits; one more exchange (when 64 lanes
+  // exceed the values) completes the sum
+  constexpr int NZ = TPW * HMAX;  // 64
+  static_assert(NZ == 64, "one value per lane after the butterfly");
+  float zz[NZ];
 #pragma unroll
-    for (int g = 0; g < HMAX; ++g) {
-      if (g < H) {
-        const float sgz = lane_group_sum<64>(z[g]);
-        if (l == g) a.lam[(size_t)tok * H + g] = 1.f / (1.f + __expf(-(sgz + a.b[g])));
-      }
+  for (int tt = 0; tt < TPW; ++tt)
+#pragma unroll
+    for (int g = 0; g < HMAX; ++g) zz[tt * HMAX + g] = z[tt][g];
+#pragma unroll
+  for (int half = NZ / 2; half >= 1; half >>= 1) {
+    // lanes with bit `half` set keep the upper half of their current values
+    const bool up = (l & half) != 0;
+#pragma unroll
+    for (int j = 0; j < half; ++j) {
+      const float mine = up ? zz[half + j] : zz[j];
+      const float other = up ? zz[j] : zz[half + j];
+      zz[j] = mine + __shfl_xor(other, half);
     }
+  }
+  // lane l now holds value l (token l / HMAX, gate l % HMAX), summed over the wave
+  {
+    const int tt = l / HMAX, g = l % HMAX;
+    const long long tok = (long long)blockIdx.x * kPrepTokens + w * TPW + tt;
+    if (g < H && tok < ntok) a.lam[(size_t)tok * H + g] = 1.f / (1.f + __expf(-(zz[0] + a.b[g])));
   }
 }
 
