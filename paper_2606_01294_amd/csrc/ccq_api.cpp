@@ -181,7 +181,7 @@ void set_dk_ws(ccq::CcqDkArgs& ka, const ccq_shape* s, char* ws, const DkWs& d) 
 }
 
 struct BwdLayout {
-  size_t qclean, corr, mdq, mdu, states, dstates, dqc, dqc_io, dkg, db, dbt, total;
+  size_t qclean, corr, mdq, mdu, states, dstates, dqc, dqc_io, dkg, db, dgn, total;
   CleanWs clean;
   DkWs dkws;
 };
@@ -203,7 +203,7 @@ BwdLayout bwd_layout(const ccq_shape* s) {
   L.dqc_io = take(ntok * s->dk * e);
   L.dkg = take(ntok * s->dk * 4);
   L.db = take(ntok * s->dk * 4);
-  L.dbt = take(nchunk * s->dk * 4);
+  L.dgn = take(nchunk * s->dk * 4);  // dg at each next chunk's first token
   L.clean = take_clean_ws(s, take);
   L.dkws = take_dk_ws(s, take);
   L.total = off;
@@ -720,7 +720,7 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
   float* dqc = reinterpret_cast<float*>(ws + L.dqc);
   float* dkg = reinterpret_cast<float*>(ws + L.dkg);
   float* db = reinterpret_cast<float*>(ws + L.db);
-  float* dbt = reinterpret_cast<float*>(ws + L.dbt);
+  float* dgn = reinterpret_cast<float*>(ws + L.dgn);
   trace_begin_call();
 
   // forward: cleaned queries (with Sigma q and m.q kept), then GLA keeping S_r
@@ -744,10 +744,10 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
                      s->dv, s->scale};
   if (traced(st, [&] { return ccq::launch_gla_dstate(da, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   ccq::GlaBwdArgs ba{ws + L.qclean, k, v, g_or_logalpha, dO, ws + L.states, ws + L.dstates, corr,
-                     dqc, ws + L.dqc_io, dkg, dv, db, dbt, dlam, s->B, s->T, s->H, s->dk, s->dv,
+                     dqc, ws + L.dqc_io, dkg, dv, db, dgn, dlam, s->B, s->T, s->H, s->dk, s->dv,
                      s->scale};
   if (traced(st, [&] { return ccq::launch_gla_bwd_chunk(ba, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
-  ccq::DgArgs ga2{db, dbt, dg_or_dlogalpha, s->B, s->T, s->H, s->dk};
+  ccq::DgArgs ga2{db, dgn, dg_or_dlogalpha, s->B, s->T, s->H, s->dk};
   if (traced(st, [&] { return ccq::launch_gla_dg(ga2, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   ccq::CleanArgs c2 = clean_args(s, ws, L.clean);  // same keys: statistics reused
   c2.q = ws + L.dqc_io;

@@ -11,6 +11,15 @@
 //   dv_j    = s sum_{t>=j} (qc_t . k_j e^{b_t - b_j}) dO_t + dS_{r+1} (k_j * e^{b_C - b_j})
 //   dg_s    = sum_{t>=s} (qc_t * dqc_t - k_t * dk_t)     (dk: the GLA part only)
 // (all exponentials taken relative to a mid-chunk reference, as in the forward).
+// The sum over the later chunks is not accumulated token by token: the decay
+// gradient at the first token of chunk r + 1 equals, per key channel c,
+//   dg_{(r+1)C}[c] = sum_v S_{r+1}[c, v] dS_{r+1}[c, v]
+//                  = e^{b_C[c]} sum_v S_r[c, v] dS_{r+1}[c, v] + sum_j k_j[c] dk_j^inter[c],
+// (the gradient of a gate is the state it multiplies times that state's
+// adjoint), with dk_j^inter = e^{b_C - b_j} * (dS_{r+1}^T v_j) the inter-chunk
+// part of dk_j; every term is formed from the chunk's own operands, so the
+// rounding errors of the bf16 states and products enter once per chunk
+// instead of adding up over the whole sequence.
 //
 // Contraction part, u_t = dqc_t:
 //   dq_t    = (I - lam_t Sigma_t) u_t                     (Sigma_t is symmetric)
@@ -21,7 +30,8 @@
 //
 // The reverse scan of dS (first line) is the GLA state kernel run backwards
 // (ccq_gla.hip); this file holds the chunk-parallel gradients, the decay
-// gradient's reverse cumulative sum and the contraction's key gradient.
+// gradient (each chunk's rows summed in reverse from the value at the next
+// chunk's first token) and the contraction's key gradient.
 #include "ccq_device.h"
 #include "ccq_kernels.h"
 
@@ -29,7 +39,8 @@ namespace ccq {
 
 // ----------------------------------------------------------------------------
 // One workgroup per chunk: dqc, the GLA part of dk, dv, the decay gradient
-// db and dlam, looping over BV-wide slices of the value dimension.
+// db, dlam and the decay gradient at the next chunk's first token, looping
+// over BV-wide slices of the value dimension.
 template <typename T, typename TG, int DK, int BV>
 __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwdArgs a) {
   constexpr int C = kChunk;
@@ -51,7 +62,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
                 kOffdO = kOffV + C * LDV * ES, kOffdOT = kOffdO + C * LDV * ES,
                 kR2 = kOffdOT + BV * LDT * ES;
   constexpr int kR3 = 2 * C * LDT * ES;
-  constexpr int kR4 = 4 * DK * 4;
+  constexpr int kR4 = 8 * DK * 4;
   constexpr int kR = kR1 > kR2 ? (kR1 > kR3 ? kR1 : kR3) : (kR2 > kR3 ? kR2 : kR3);
   __shared__ __align__(16) char sR[kR > kR4 ? kR : kR4];
   T* sQt = reinterpret_cast<T*>(sR);
@@ -161,6 +172,12 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
   };
   Slice cur;
   load_slice(cur, 0);
+  // sum_v S_r[c][v] dS_{r+1}[c][v] for this thread's 8 channels (every piece
+  // of a thread covers the same channels)
+  static_assert(kThreads % (DK / 8) == 0, "channels per thread");
+  float rdot[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) rdot[e] = 0.f;
   for (int vv0 = 0; vv0 < a.dv; vv0 += BV) {
     // states, rows v: S_r diag(e^{b_m}) and dS_{r+1} diag(e^{b_C - b_m}); the
     // products over v read them with transposing LDS reads
@@ -172,6 +189,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
       for (int e = 0; e < 8; ++e) {
         s_scaled[e] = to<T>(f32(cur.s[p][e]) * sBm[c0 + e]);
         ds_scaled[e] = to<T>(f32(cur.d[p][e]) * sBCm[c0 + e]);
+        rdot[e] += f32(cur.s[p][e]) * f32(cur.d[p][e]);
       }
       *reinterpret_cast<v8*>(sS + row * LDQ + c0) = s_scaled;
       *reinterpret_cast<v8*>(sdS + row * LDQ + c0) = ds_scaled;
@@ -248,11 +266,11 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
       kv[ct][r] = f32(k[rowoff + off]);
       cv[ct][r] = a.corr[rowoff + off];
     }
-  float tot[NTC];
+  float kdk[NTC];  // sum over the chunk's rows of k * dk^inter
   float dl[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int ct = 0; ct < NTC; ++ct) {
-    tot[ct] = 0.f;
+    kdk[ct] = 0.f;
     const int c = 16 * ct + c16;
     const float bm = sG[(C / 2 - 1) * LDG + c];
 #pragma unroll
@@ -261,14 +279,15 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
       if (i < nrow) {
         const float d = sG[i * LDG + c] - bm;
         const float dqc = a.scale * __expf(d) * X1[ct][r];
-        const float dkg = __expf(-d) * (Y2[ct][r] * a.scale + X2[ct][r]);
+        const float inter = __expf(-d) * X2[ct][r];
+        const float dkg = __expf(-d) * (Y2[ct][r] * a.scale) + inter;
         const int off = i * (int)gsk + c;
         const float db = qv[ct][r] * dqc - kv[ct][r] * dkg;
         dqc_f[off] = dqc;
         dqc_io[off] = to<T>(dqc);
         dkg_f[off] = dkg;
         db_f[off] = db;
-        tot[ct] += db;
+        kdk[ct] += kv[ct][r] * inter;
         dl[r] -= dqc * cv[ct][r];
       }
     }
@@ -279,22 +298,39 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
     const int i = 16 * w + 4 * g4 + r;
     if (c16 == 0 && i < nrow) a.dlam[((size_t)b * a.T + r0 + i) * a.H + h] = s;
   }
-  // per-chunk column sums of db (for the reverse cumulative sum across chunks)
+  // decay gradient at the next chunk's first token:
+  //   e^{b_C} sum_v S_r dS_{r+1} + sum_j k_j * dk_j^inter
+  // (zero after the last chunk, where dS_{r+1} = 0); wave sums in a fixed order
+  float* sRow = sTot + 4 * DK;
 #pragma unroll
   for (int ct = 0; ct < NTC; ++ct) {
-    float x = tot[ct];
+    float x = kdk[ct];
     x += __shfl_xor(x, 16);
     x += __shfl_xor(x, 32);
     if (g4 == 0) sTot[w * DK + 16 * ct + c16] = x;
   }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    float x = rdot[e];
+#pragma unroll
+    for (int m = DK / 8; m < 64; m *= 2) x += __shfl_xor(x, m);
+    rdot[e] = x;
+  }
+  if (l < DK / 8)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sRow[w * DK + 8 * l + e] = rdot[e];
   lds_barrier();
-  if (tid < DK)
-    a.db_tot[((size_t)bh * N + ci) * DK + tid] =
-        sTot[tid] + sTot[DK + tid] + sTot[2 * DK + tid] + sTot[3 * DK + tid];
+  if (tid < DK) {
+    const float kd = sTot[tid] + sTot[DK + tid] + sTot[2 * DK + tid] + sTot[3 * DK + tid];
+    const float sd = sRow[tid] + sRow[DK + tid] + sRow[2 * DK + tid] + sRow[3 * DK + tid];
+    a.dg_next[((size_t)bh * N + ci) * DK + tid] = __expf(sG[(C - 1) * LDG + tid]) * sd + kd;
+  }
 }
 
 // ----------------------------------------------------------------------------
-// dg_t = sum_{s >= t} db_s: one workgroup per chunk, one thread per channel.
+// dg_t = sum_{s >= t} db_s: one workgroup per chunk, one thread per channel;
+// the rows of the chunk are summed here and the later chunks enter through the
+// decay gradient at the next chunk's first token (dg_next).
 template <typename TG>
 __global__ __launch_bounds__(kThreads) void gla_dg_kernel(const DgArgs a) {
   constexpr int C = kChunk, HC = C / 2;
@@ -313,12 +349,8 @@ __global__ __launch_bounds__(kThreads) void gla_dg_kernel(const DgArgs a) {
   for (int c0 = 0; c0 < a.dk; c0 += npc) {
     const int c = c0 + (threadIdx.x % npc), half = threadIdx.x / npc;
     const bool on = c < a.dk;
-    float later = 0.f;  // sum over the later chunks (half 1 only)
-    if (on && half == 1) {
-      const float* tot = a.db_tot + (size_t)bh * N * a.dk + c;
-#pragma unroll 8
-      for (int r = ci + 1; r < N; ++r) later += tot[(size_t)r * a.dk];
-    }
+    // sum over the later chunks (half 1 only)
+    const float later = (on && half == 1) ? a.dg_next[((size_t)bh * N + ci) * a.dk + c] : 0.f;
     float x[HC];
 #pragma unroll
     for (int j = 0; j < HC; ++j) {

@@ -184,16 +184,16 @@ struct GlaBwdArgs {
   float* dk_gla;        // GLA part of dL/dk [B,T,H,dk] fp32
   void* dv_out;         // [B,T,H,dv] io
   float* db;            // dL/d(cumulative log decay) [B,T,H,dk] fp32
-  float* db_tot;        // per-chunk column sums of db [B*H, N, dk]
+  float* dg_next;       // decay gradient at the first token of the next chunk [B*H, N, dk]
   float* dlam;          // [B,T,H]
   int B, T, H, dk, dv;
   float scale;
 };
 
-// dg_s = sum_{t >= s} db_t (reverse cumulative sum over the sequence).
+// dg_s = sum_{t >= s} db_t: the chunk's own rows plus dg_next.
 struct DgArgs {
   const float* db;
-  const float* db_tot;
+  const float* dg_next;
   void* dg;             // [B,T,H,dk] gate dtype
   int B, T, H, dk;
 };
