@@ -938,6 +938,11 @@ hipError_t run_gdn_state(const GdnArgs& a, hipStream_t st) {
     if constexpr (DK == 128)
       if (slices >= kSimds && a.dv % 64 == 0) return run_gdn_state_dma<DK, 4, 2>(a, st);
     if (slices * 2 >= kSimds && a.dv % 32 == 0) return run_gdn_state_dma<DK, 2, 4>(a, st);
+    // at most one value tile per compute unit at dk = 256 (long sequences of
+    // few heads): one tile per workgroup over four waves, which beats eight
+    // waves of the register-prefetch form (fewer partial products to exchange)
+    if constexpr (DK == 256)
+      if (slices <= kSimds / 4) return run_gdn_state_dma<DK, 1, 4>(a, st);
   }
   if (slices >= kSimds || DK < 64) return run_gdn_state_v<T, DK, 4, 1>(a, st);
   if (slices * 2 >= kSimds || DK < 128) return run_gdn_state_v<T, DK, 2, 2>(a, st);
