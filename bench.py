@@ -81,6 +81,21 @@ def gdn_group(w) -> int:
     return best
 
 
+def gla_group(w) -> int:
+    """Chunks per GLA output workgroup (one stored state per group), as the library
+    picks it; 1 for training, fp32 and dv > 256."""
+    import torch
+    if getattr(w, "train", False) or w.dtype != torch.bfloat16 or w.dv > 256 or w.dk not in (64, 128):
+        return 1
+    nc, bh = -(-w.T // CHUNK), w.B * w.H
+    best, best_cost = 1, -(-(bh * nc) // 512) * 3   # one chunk per workgroup, two per compute unit
+    for g in (2, 4, 8):   # rounds of 256 workgroups x (group + 1), the largest on a tie
+        cost = -(-(bh * -(-nc // g)) // 256) * (g + 1)
+        if cost <= best_cost:
+            best, best_cost = g, cost
+    return best
+
+
 def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
     """Algorithmic (bytes, flops) of one launch of `kernel` on workload w: every
     input read once, every output written once; products counted at 2 flops per
@@ -108,17 +123,20 @@ def kernel_cost(kernel: str, w, io_bytes: int = 2, gate_bytes: int = 2):
         elif kernel == "clean_dq":
             by += ntok * (4 * dk + 4)
         fl = ntok * (2 * dk * dk + 4 * C * dk)
-    elif kernel == "gla_state":     # k, g, v in; chunk-entry (segment-local) states, segment totals out
-        by = ntok * (dk * io_bytes + dk * gate_bytes + dv * io_bytes + dv * dk * io_bytes // C) \
+    elif kernel == "gla_state":     # k, g, v in; group-entry (segment-local) states, segment totals out
+        NG = -(-NC // gla_group(w))
+        by = ntok * (dk * io_bytes + dk * gate_bytes + dv * io_bytes) + BH * NG * dv * dk * io_bytes \
             + BH * GS * dv * dk * 4 + (BH * (GS + NC) * dk * 4 if GS > 1 else 0)
         fl = ntok * (2 * dk * dv)
     elif kernel == "gla_scan":      # segment totals in; segment entry states and final state out
         by = BH * GS * (dv * dk * 4 + dk * 4) + BH * (GS - 1) * dv * dk * io_bytes + BH * dv * dk * 4
         fl = BH * GS * dv * dk * 2
-    elif kernel == "gla_out":       # q_clean, k, g, v, chunk states, segment entry states in; o out
-        by = ntok * (2 * dk * io_bytes + dk * gate_bytes + 2 * dv * io_bytes + dv * dk * io_bytes // C) \
-            + (BH * (GS - 1) * dv * dk * io_bytes + BH * NC * dk * 4 if GS > 1 else 0)
-        fl = ntok * (2 * C * dk + 2 * dk * dv + 2 * C * dv)
+    elif kernel == "gla_out":       # q_clean, k, g, v, group-entry states, segment entry states in; o out
+        NG = -(-NC // gla_group(w))
+        by = ntok * (2 * dk * io_bytes + dk * gate_bytes + 2 * dv * io_bytes) + BH * NG * dv * dk * io_bytes \
+            + (BH * (GS - 1) * dv * dk * io_bytes + BH * NG * dk * 4 if GS > 1 else 0)
+        # plus the state carried through each group: S <- S diag(e^{b_C}) + V Kd^T
+        fl = ntok * (2 * C * dk + 2 * dk * dv + 2 * C * dv) + BH * (NC - NG) * 2 * C * dk * dv
     elif kernel == "gdn_tri":       # k, log alpha, beta in; chunk transforms Tm and decays out
         by = ntok * (dk * io_bytes + 8 + C * io_bytes + 4)
         fl = ntok * (2 * C * dk)

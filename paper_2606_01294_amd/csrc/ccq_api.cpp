@@ -319,6 +319,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
     ccq::GlaStateArgs sa{k, v, g_or_la, S0, ST, ws + L.states, s->B, s->T, s->H, s->dk, s->dv};
     sa.cu = cu;
     sa.rk = rk;
+    sa.group = ccq::gla_out_group(s->B, s->H, s->T, s->dk, s->dv, bf);  // one state per output group
     if (L.gla_seg > 0) {
       sa.seg = L.gla_seg;
       sa.ST = nullptr;
@@ -363,6 +364,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
     ccq::GlaOutArgs oa{qclean, k, v, g_or_la, ws + L.states, o, s->B, s->T, s->H, s->dk, s->dv, s->scale};
     oa.cu = cu;
     oa.rk = rk;
+    oa.group = ccq::gla_out_group(s->B, s->H, s->T, s->dk, s->dv, bf);  // as the state pass stored
     if (L.gla_seg > 0) {
       oa.seg = L.gla_seg;
       oa.entries = ws + L.entries;

@@ -9,8 +9,9 @@
 //
 // gla_state_kernel carries a 64-channel tile of S through the chunks of a
 // head (rows and columns of S evolve independently under the GLA write) and
-// stores S_r for every chunk; gla_out_kernel forms every chunk's outputs in
-// parallel.  The output uses a mid-chunk reference m = C/2: Qt = q * e^{b - b_m},
+// stores S_r for every chunk (a forward pass: for the first chunk of every
+// output group); gla_out_kernel forms the outputs of every chunk, or of every
+// group of chunks, in parallel.  The output uses a mid-chunk reference m = C/2: Qt = q * e^{b - b_m},
 // Kt = k * e^{b_m - b}, so Qt Kt^T carries e^{b_i - b_j} with factors of at most
 // e^{|b_m - b_i|} (a 32-token log-decay), and the inter-chunk read is
 // Qt (S_r diag(e^{b_m}))^T.
@@ -85,7 +86,10 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
     rv.load(v + seq_off(sq, r0, h, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
   };
   f32x4 Sr[NVT];  // S_r kept for the deferred write-back
+  // only the first chunk of each output group (a.group chunks) is read back
+  const int grp = (!kRev && a.group > 1) ? a.group : 1;
   auto write_back = [&](int cw) {
+    if (cw % grp != 0) return;
     T* st = static_cast<T*>(a.states) + (((size_t)bh * N + cw) * a.dv + v0) * a.dk + c0 + 16 * w + 4 * g4;
 #pragma unroll
     for (int tv = 0; tv < NVT; ++tv)
@@ -201,7 +205,18 @@ __global__ __launch_bounds__(256) void gla_scan_kernel(const GlaScanArgs a) {
 // value tiles for IPW token tiles, transposed: O^T = S_r' Qt^T + V^T P^T, with
 // rows of S_r read straight from global memory and scaled by e^{b_m} per key
 // channel.  V is staged VP columns at a time.
-template <typename T, typename TG, int DK, int VP, int VPW, int IPW>
+//
+// CARRY (bf16, all value columns in one slice): one workgroup walks a group of
+// a.group consecutive chunks and reads S_r for the first one only.  Each wave
+// holds its value tiles of S_r^T, all key channels, in fp32 accumulators in
+// pair order (tile t, row 4 g + r is channel pair_feat(t, g) + r), so that two
+// tiles pack into the operand of the output product with 8 consecutive
+// channels per lane group.  Per chunk
+//   S^T <- S^T diag(e^{b_m})                    (the output's operand)
+//   S^T <- diag(e^{b_C - b_m}) (S^T + Kt^T V)   (= e^{b_C} S_r^T + Kd^T V)
+// with Kt^T read transposed in the same pair order and V in the matching
+// token order; both factors are at most 1.
+template <typename T, typename TG, int DK, int VP, int VPW, int IPW, bool CARRY>
 __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArgs a) {
   constexpr int C = kChunk, NT = kOutThreads;
   constexpr int P = Pad<T>::value;
@@ -221,21 +236,31 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
   float* sB = reinterpret_cast<float*>(sBPV);     // gates, then their prefix b
   T* sP = reinterpret_cast<T*>(sBPV);             // masked scores, once sB is dead
   T* sV = reinterpret_cast<T*>(sBPV + kPBytes);   // V slice, once sB is dead
-  __shared__ __align__(16) float sBm[DK], sBe[DK];  // e^{b_m}; the same times the decay since the segment began
+  // e^{b_m}; the same times the decay since the segment began (CARRY: the decay alone)
+  __shared__ __align__(16) float sBm[DK], sBe[DK];
+  __shared__ __align__(16) float sDc[CARRY ? DK : 4];  // CARRY: e^{b_C - b_m}
   __shared__ float sTot[TPC][DK];
+  static_assert(!CARRY || sizeof(T) == 2, "carried state: bf16 path");
 
   const int N = (a.T + C - 1) / C;
+  const int R = CARRY ? a.group : 1, NGR = (N + R - 1) / R;
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
-  const int bh = lb / N, ci = lb % N;
+  const int bh = lb / NGR, cb = (lb % NGR) * R;
   const int b = bh / a.H, h = bh % a.H;
   const Seq sq = seq_of(a.cu, b, a.T);
-  const int r0 = ci * C;
-  if (r0 >= sq.len) return;  // past a packed sequence's end
-  const int nrow = (sq.len - r0) < C ? (sq.len - r0) : C;
+  const int ce = min((sq.len + C - 1) / C, cb + R);  // a packed sequence's own chunks
+  if (cb >= ce) return;
   const int tid = threadIdx.x, w = tid >> 6, l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
   const int vg = w % NVG, ig = w / NVG;
   const size_t gstride = (size_t)a.H * DK;
+  constexpr int NTS = CARRY ? VPW : 1, NPT = CARRY ? 2 * NK : 1;
+  f32x4 Sc[NTS][NPT];  // CARRY: this wave's value tiles of S^T, pair order
+
+  for (int ci = cb; ci < ce; ++ci) {
+  if (ci > cb) __syncthreads();  // every wave is done with the previous chunk
+  const int r0 = ci * C;
+  const int nrow = (sq.len - r0) < C ? (sq.len - r0) : C;
   // past the first segment of the state pass, S_r = local state + the
   // segment's entry state decayed to this chunk (per key channel)
   const int sg = a.seg > 0 ? ci / a.seg : 0;
@@ -275,10 +300,11 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
     if (j0 <= C / 2 - 1 && C / 2 - 1 < j0 + TOK) {
       const float bm = __expf(x[C / 2 - 1 - j0] + off);
       sBm[c] = bm;
-      if (ent) sBe[c] = bm * a.cdec[((size_t)bh * N + ci) * DK + c];
+      if (ent) sBe[c] = (CARRY ? 1.f : bm) * a.cdec[((size_t)bh * N + ci) * DK + c];
     }
   }
   __syncthreads();
+  if (CARRY && tid < DK) sDc[tid] = __expf(sB[(C - 1) * LDB + tid] - sB[(C / 2 - 1) * LDB + tid]);
   if (a.rk) fk.apply(rk);
   // Qt = q e^{b - b_m}, Kt = k e^{b_m - b}
 #pragma unroll
@@ -317,6 +343,110 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
   const int NS = a.seg > 0 ? (N + a.seg - 1) / a.seg : 1;
   const T* Eg = ent ? static_cast<const T*>(a.entries) + ((size_t)bh * NS + sg) * a.dv * DK : nullptr;
   T* o = static_cast<T*>(a.o);
+  if constexpr (CARRY) {
+    {
+      RowTile<T, VP, NT> rv;
+      rv.load(static_cast<const T*>(a.v) + seq_off(sq, r0, h, a.H, a.dv), (size_t)a.H * a.dv, nrow);
+      rv.store(sV, LDV);
+    }
+    if (ci == cb) {
+      // S_r of the group's first chunk (plus the segment entry decayed to it):
+      // lane (g, j) of value tile vt reads channels 32 m + 8 g .. + 7 of value
+      // row 16 vt' + j, which are rows 4 g .. 4 g + 3 of tiles 2 m and 2 m + 1
+#pragma unroll
+      for (int vt = 0; vt < VPW; ++vt) {
+        const int vr = 16 * (vg * VPW + vt);
+#pragma unroll
+        for (int m = 0; m < NK; ++m) {
+          const Frag<T> f = ld_frag_global(Sg + (size_t)vr * DK + 32 * m, (size_t)DK);
+          f32x4 x, y;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            x[r] = frag_elem(f, r);
+            y[r] = frag_elem(f, 4 + r);
+          }
+          if (ent) {
+            const Frag<T> fe = ld_frag_global(Eg + (size_t)vr * DK + 32 * m, (size_t)DK);
+            const f32x4 d0 = *reinterpret_cast<const f32x4*>(sBe + 32 * m + 8 * g4);
+            const f32x4 d1 = *reinterpret_cast<const f32x4*>(sBe + 32 * m + 8 * g4 + 4);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              x[r] += frag_elem(fe, r) * d0[r];
+              y[r] += frag_elem(fe, 4 + r) * d1[r];
+            }
+          }
+          Sc[vt][2 * m] = x;
+          Sc[vt][2 * m + 1] = y;
+        }
+      }
+    }
+    // S^T diag(e^{b_m}) in place, the output's operand
+#pragma unroll
+    for (int m = 0; m < NK; ++m) {
+      const f32x4 e0 = *reinterpret_cast<const f32x4*>(sBm + 32 * m + 8 * g4);
+      const f32x4 e1 = *reinterpret_cast<const f32x4*>(sBm + 32 * m + 8 * g4 + 4);
+#pragma unroll
+      for (int vt = 0; vt < VPW; ++vt) {
+        Sc[vt][2 * m] *= e0;
+        Sc[vt][2 * m + 1] *= e1;
+      }
+    }
+    __syncthreads();  // sV and sP are ready
+    // V in the token order of the accumulator pairs (for both products)
+    Frag<T> vf[VPW][2];
+#pragma unroll
+    for (int vt = 0; vt < VPW; ++vt)
+#pragma unroll
+      for (int kq = 0; kq < 2; ++kq) vf[vt][kq] = ld_frag_tr_acc(sV + 32 * kq * LDV + 16 * (vg * VPW + vt), LDV);
+#pragma unroll
+    for (int it = 0; it < IPW; ++it) {
+      const int I = ig * IPW + it;
+      const int i = 16 * I + c16;
+      f32x4 acc[VPW];
+#pragma unroll
+      for (int vt = 0; vt < VPW; ++vt) acc[vt] = zero4();
+#pragma unroll
+      for (int m = 0; m < NK; ++m) {
+        const Frag<T> qf = ld_frag(sQt + 16 * I * LDQ + 32 * m, LDQ);
+#pragma unroll
+        for (int vt = 0; vt < VPW; ++vt) mma(acc[vt], acc_pair_frag<T>(Sc[vt][2 * m], Sc[vt][2 * m + 1]), qf);
+      }
+      const Frag<T> pf0 = ld_frag(sP + 16 * I * LDP, LDP);
+      const Frag<T> pf1 = ld_frag(sP + 16 * I * LDP + 32, LDP);
+#pragma unroll
+      for (int vt = 0; vt < VPW; ++vt) {
+        const int vl = 16 * (vg * VPW + vt);
+        mma(acc[vt], vf[vt][0], pf0);
+        if (I >= 2) mma(acc[vt], vf[vt][1], pf1);  // keys 32..63 precede row i
+        if (i < nrow)
+          store4(o + seq_off(sq, r0 + i, h, a.H, a.dv) + vl + 4 * g4, a.scale * acc[vt][0], a.scale * acc[vt][1],
+                 a.scale * acc[vt][2], a.scale * acc[vt][3]);
+      }
+    }
+    if (ci + 1 < ce) {
+      // S^T <- diag(e^{b_C - b_m}) (S^T + Kt^T V), per 32-channel block
+#pragma unroll
+      for (int m = 0; m < NK; ++m) {
+        Frag<T> kf[2][2];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+          for (int kq = 0; kq < 2; ++kq) kf[hh][kq] = ld_frag_tr_acc_pair(sKt + 32 * kq * LDQ, LDQ, 2 * m + hh);
+        const f32x4 d0 = *reinterpret_cast<const f32x4*>(sDc + 32 * m + 8 * g4);
+        const f32x4 d1 = *reinterpret_cast<const f32x4*>(sDc + 32 * m + 8 * g4 + 4);
+#pragma unroll
+        for (int vt = 0; vt < VPW; ++vt) {
+#pragma unroll
+          for (int kq = 0; kq < 2; ++kq) {
+            mma(Sc[vt][2 * m], kf[0][kq], vf[vt][kq]);
+            mma(Sc[vt][2 * m + 1], kf[1][kq], vf[vt][kq]);
+          }
+          Sc[vt][2 * m] *= d0;
+          Sc[vt][2 * m + 1] *= d1;
+        }
+      }
+    }
+  } else
   for (int vp = 0; vp < a.dv; vp += VP) {
     if (vp > 0) __syncthreads();  // every wave is done with the previous V slice
     {
@@ -379,6 +509,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
       }
     }
   }
+  }  // chunks of the group
 }
 
 namespace {
@@ -403,9 +534,19 @@ hipError_t run_gla_state(const GlaStateArgs& a, hipStream_t st) {
 }
 template <typename T, typename TG, int DK, int VP, int VPW, int IPW>
 hipError_t run_gla_out_v(const GlaOutArgs& a, hipStream_t st) {
-  const int nblk = a.B * a.H * ((a.T + kChunk - 1) / kChunk);
+  const int N = (a.T + kChunk - 1) / kChunk;
+  if constexpr (sizeof(T) == 2) {
+    if (a.group > 1) {
+      if (a.dv != VP) return hipErrorInvalidValue;  // the carried state covers every value column
+      const int nblk = a.B * a.H * ((N + a.group - 1) / a.group);
+      if (nblk == 0) return hipSuccess;
+      hipLaunchKernelGGL((gla_out_kernel<T, TG, DK, VP, VPW, IPW, true>), dim3(nblk), dim3(kOutThreads), 0, st, a);
+      return hipGetLastError();
+    }
+  }
+  const int nblk = a.B * a.H * N;
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((gla_out_kernel<T, TG, DK, VP, VPW, IPW>), dim3(nblk), dim3(kOutThreads), 0, st, a);
+  hipLaunchKernelGGL((gla_out_kernel<T, TG, DK, VP, VPW, IPW, false>), dim3(nblk), dim3(kOutThreads), 0, st, a);
   return hipGetLastError();
 }
 // V is staged at most 256 columns (fp32: 128) at a time.
@@ -427,6 +568,31 @@ hipError_t run_gla_out(const GlaOutArgs& a, hipStream_t st) {
   return hipErrorInvalidValue;
 }
 }  // namespace
+
+int gla_out_group(int B, int H, int T, int dk, int dv, bool is_bf16) {
+  // The carried form needs every value column in one staged slice (bf16:
+  // dv <= 256).  A group of G chunks takes a compute unit and costs about
+  // G + 1 chunk steps (the stored state read once); a workgroup of the
+  // one-chunk form (two per compute unit) about 3, its state read and the
+  // state pass's store of every chunk included.  The G of least rounds x cost
+  // wins, the largest on a tie.  Measured per call: T = 2048 with 32 heads
+  // 142 us (one chunk each), 128 (G = 2), 118.5 (4), 140 (8); T = 20480 with 4
+  // heads 203, 188.5, 192, 185.
+  if (!is_bf16 || dv > 256 || (dk != 64 && dk != 128)) return 1;
+  const long long bh = (long long)B * H;
+  const long long N = (T + kChunk - 1) / kChunk;
+  int best = 1;
+  long long best_cost = ((bh * N + 511) / 512) * 3;
+  for (int g = 2; g <= 8; g *= 2) {
+    const long long rounds = (bh * ((N + g - 1) / g) + 255) / 256;
+    const long long cost = rounds * (g + 1);
+    if (cost <= best_cost) {
+      best_cost = cost;
+      best = g;
+    }
+  }
+  return best;
+}
 
 bool gla_supported(int dk, int dv, bool is_bf16) {
   const bool dv_ok = dv == 64 || dv == 128 || dv == 256 || dv == 512;

@@ -78,6 +78,7 @@ struct GlaStateArgs {
   float scale;        // read scale (the reverse scan of the training step only)
   const int* cu = nullptr;  // packed-batch offsets (device), as CleanArgs
   const float* rk = nullptr;  // key row scales, as CleanArgs
+  int group = 1;  // forward: S_r stored for every group-th chunk only (the output groups)
 };
 
 // Entry state of every segment, E_0 = 0 (S0 is inside segment 0's states),
@@ -105,6 +106,7 @@ struct GlaOutArgs {
   const float* cdec;    // [B*H, N, dk] fp32, or null with one segment
   const int* cu = nullptr;  // packed-batch offsets (device), as CleanArgs
   const float* rk = nullptr;  // key row scales, as CleanArgs
+  int group = 1;  // chunks per workgroup, S carried between them (gla_out_group)
 };
 
 // Gated DeltaNet chunk transform (chunk-parallel): Tm = (I + A)^{-1} and the
@@ -378,6 +380,8 @@ hipError_t launch_varlen_copy(void* dst, const void* src, const int* cu, int B, 
 // Supported-shape predicates (used by validation before any launch).
 bool clean_supported(int dk, bool is_bf16);
 bool gla_supported(int dk, int dv, bool is_bf16);
+// Chunks per output workgroup of the GLA forward (1: one chunk each).
+int gla_out_group(int B, int H, int T, int dk, int dv, bool is_bf16);
 bool gdn_supported(int dk, int dv, bool is_bf16);
 // Chunks per output workgroup (and state stride) for a forward pass.
 int gdn_out_group(int B, int H, int T, int dk, int dv, bool is_bf16);

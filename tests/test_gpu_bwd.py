@@ -76,14 +76,31 @@ def test_fwd_bwd_uncentred_scaled(dtype):
     check(d, dtype, centered=False, scale=0.25)
 
 
-def test_fwd_bwd_matches_forward_entry_point():
-    """The training step's o equals ccq_gla_fwd's o bit for bit (same kernels)."""
-    d = make_inputs(GLA, 2, 190, 2, 128, 256, BF16, seed=19, lam="random", with_dO=True)
+def _both_o(dtype, dk, dv):
+    d = make_inputs(GLA, 2, 190, 2, dk, dv, dtype, seed=19, lam="random", with_dO=True)
     g = to_device(d)
     a = ccq.ccq_fwd_bwd(g["q"], g["k"], g["v"], g["g"], g["lam"], g["dO"])
     b = ccq.ccq_gla_fwd(g["q"], g["k"], g["v"], g["g"], g["lam"])
     torch.cuda.synchronize()
-    assert torch.equal(a["o"], b["o"])
+    return a["o"], b["o"]
+
+
+@pytest.mark.parametrize("dtype, dk, dv", [(BF16, 128, 512), (F32, 64, 128)])
+def test_fwd_bwd_matches_forward_entry_point(dtype, dk, dv):
+    """Where the forward also takes one chunk per output workgroup (bf16 with dv = 512,
+    fp32), the training step's o equals ccq_gla_fwd's o bit for bit (same kernels)."""
+    a, b = _both_o(dtype, dk, dv)
+    assert torch.equal(a, b)
+
+
+def test_fwd_bwd_o_near_grouped_forward():
+    """bf16 with dv <= 256: the forward carries S through groups of chunks in fp32,
+    while the training step reads every chunk's stored bf16 state; the two o agree to
+    the bf16 bar (each is held to the oracle by the parity tests)."""
+    a, b = _both_o(BF16, 128, 256)
+    e = nerr(np64(a), np64(b))
+    say("  training o against the grouped forward's o: %.2e" % e)
+    assert 0 < e <= TOL[BF16]
 
 
 def test_fwd_bwd_deterministic():

@@ -75,6 +75,30 @@ def test_gla_parity_segments(case):
     compare(GLA, d, dtype, S0=S0.astype(np.float32).astype(np.float64))
 
 
+# The bf16 GLA forward (dv <= 256) carries S through groups of chunks per
+# output workgroup, reading one stored state per group (the group size follows
+# from B * H and the chunk count): the small and segment cases above take
+# groups of 2 (across segment entries in the segment cases), these shapes
+# groups of 8 (all 6 chunks of a head, one partial group), 4 (16 chunks, the
+# last ragged) and 4 (one group of 3 chunks); the full-size workloads below add
+# groups of 4 (T = 2048) and 8 (T = 20480, across the state pass's segments).
+GLA_GROUP_CASES = [
+    # dtype, B, T, H, dk, dv
+    (BF16, 16, 337, 16, 64, 64),
+    (BF16, 8, 1000, 8, 128, 128),
+    (BF16, 16, 150, 16, 64, 128),
+]
+
+
+@pytest.mark.parametrize("case", GLA_GROUP_CASES, ids=lambda c: "%s-B%dT%dH%d-dk%d-dv%d" % (
+    str(c[0]).split(".")[-1], c[1], c[2], c[3], c[4], c[5]))
+def test_gla_parity_output_groups(case):
+    dtype, B, T, H, dk, dv = case
+    say("gla groups", case)
+    d = make_inputs(GLA, B, T, H, dk, dv, dtype, seed=500 + T, keys="aniso", lam="random")
+    compare(GLA, d, dtype)
+
+
 GDN_CASES = [
     (F32, 1, 200, 2, 64, 64, "iso", "const"),
     (F32, 1, 130, 2, 128, 256, "aniso", "random"),
