@@ -37,6 +37,17 @@
  *     (App. B, mean term), and P^prev's row i is S^K_r q_i.
  *   * centered = 0 selects the uncentred ablation Sigma := Cbar (App. E).
  *   * o is multiplied by `scale` (1.0 reproduces the paper).
+ *   * decay = 1 selects the decay-aligned covariance Sigma^gamma that App. J
+ *     names as future work for forgetting backbones, read for the scalar decay
+ *     of Gated DeltaNet: key j enters the statistics of token t with the
+ *     backbone's own factor gamma_{j,t} = prod_{s=j+1..t} alpha_s, normalised
+ *     by the decayed count W_t = sum_{j<=t} gamma_{j,t} = alpha_t W_{t-1} + 1:
+ *       Cbar^gamma_t = (1/W_t) sum_j gamma_{j,t} k_j k_j^T,
+ *       mu^gamma_t   = (1/W_t) sum_j gamma_{j,t} k_j,
+ *       Sigma^gamma_t = Cbar^gamma_t - mu^gamma_t mu^gamma_t^T,
+ *     i.e. Alg. 2's running-mean updates with t replaced by W_t.  With
+ *     alpha = 1 this is Sigma_t.  Forward only, from empty statistics (t0 = 0,
+ *     no C0 / mu0); CT, muT are then Cbar^gamma_T, mu^gamma_T.
  *
  * Layouts: q,k [B,T,H,dk]; v,o [B,T,H,dv]; GLA g [B,T,H,dk]; GDN logalpha,
  * beta [B,T,H]; lambda [B,T,H]; states S [B,H,dv,dk], C [B,H,dk,dk],
@@ -54,7 +65,7 @@ typedef struct {
   int32_t B, T, H, dk, dv;
   int32_t backbone; /* 0 = GLA, 1 = Gated DeltaNet */
   int32_t centered; /* 1 = Sigma = Cbar - mu mu^T, 0 = Cbar */
-  int32_t pad_;
+  int32_t decay;    /* 1 = decay-aligned statistics (Gated DeltaNet), 0 = undecayed */
   double scale;     /* read scale */
   int64_t t0;       /* tokens already absorbed into C0, mu0 */
 } ccq_oracle_shape;
@@ -116,6 +127,7 @@ int ccq_oracle_fwd(const ccq_oracle_shape* s, int form, const double* q, const d
                    double* CT, double* muT, double* qclean) {
   if (!s || s->B < 0 || s->T < 0 || s->H < 0 || s->dk <= 0 || s->dv <= 0 || s->t0 < 0) return 1;
   if (s->backbone == 1 && !beta) return 1;
+  if (s->decay && (s->backbone != 1 || s->t0 != 0 || C0 || mu0)) return 1;
   const int B = s->B, T = s->T, H = s->H, dk = s->dk, dv = s->dv;
   int err = 0;
 #pragma omp parallel for schedule(dynamic, 1)
@@ -141,12 +153,14 @@ int ccq_oracle_fwd(const ccq_oracle_shape* s, int form, const double* q, const d
         const size_t ti = tok(s, b, t, h);
         const double* kt = k + ti * dk;
         const double* qt = q + ti * dk;
-        tau += 1.0;
+        /* the weight of every earlier key falls by alpha_t (decay = 1) */
+        const double al = s->decay ? exp(gate[ti]) : 1.0;
+        tau = al * tau + 1.0;
         /* statistics include the current key (Alg. 2 updates before the read) */
         if (form == 0) {
           for (int a = 0; a < dk; ++a)
-            for (int bb = 0; bb < dk; ++bb) K[a * dk + bb] += kt[a] * kt[bb];
-          for (int a = 0; a < dk; ++a) m[a] += kt[a];
+            for (int bb = 0; bb < dk; ++bb) K[a * dk + bb] = al * K[a * dk + bb] + kt[a] * kt[bb];
+          for (int a = 0; a < dk; ++a) m[a] = al * m[a] + kt[a];
           /* c = Sigma_t q = (K q)/t - m (m.q)/t^2 */
           double mq = 0.0;
           for (int a = 0; a < dk; ++a) mq += m[a] * qt[a];
@@ -323,6 +337,7 @@ int ccq_oracle_chunk_fwd(const ccq_oracle_shape* s, int C, const double* q, cons
                          const double* lam, const double* S0, const double* C0,
                          const double* mu0, double* o, double* ST, double* CT, double* muT,
                          double* qclean) {
+  if (s && s->decay) return 1; /* the decay-aligned statistics: token forward only */
   if (!s || C <= 0 || s->B < 0 || s->T < 0 || s->H < 0 || s->dk <= 0 || s->dv <= 0) return 1;
   if (s->backbone == 1 && !beta) return 1;
   const int B = s->B, T = s->T, H = s->H, dk = s->dk, dv = s->dv;
@@ -438,6 +453,7 @@ int ccq_oracle_gla_fwd_bwd(const ccq_oracle_shape* s, int seg, const double* q, 
                            const double* v, const double* g, const double* lam,
                            const double* dO, double* o, double* dq, double* dk_out,
                            double* dv_out, double* dg, double* dlam) {
+  if (s && s->decay) return 1; /* the decay-aligned statistics: token forward only */
   if (!s || seg <= 0 || s->backbone != 0 || s->t0 != 0 || s->B < 0 || s->T < 0 || s->H < 0 ||
       s->dk <= 0 || s->dv <= 0)
     return 1;
@@ -617,6 +633,7 @@ int ccq_oracle_gdn_fwd_bwd(const ccq_oracle_shape* s, int seg, const double* q, 
                            const double* lam, const double* dO, double* o, double* dq,
                            double* dk_out, double* dv_out, double* dlogalpha, double* dbeta,
                            double* dlam) {
+  if (s && s->decay) return 1; /* the decay-aligned statistics: token forward only */
   if (!s || seg <= 0 || s->backbone != 1 || s->t0 != 0 || s->B < 0 || s->T < 0 || s->H < 0 ||
       s->dk <= 0 || s->dv <= 0)
     return 1;

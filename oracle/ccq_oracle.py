@@ -41,7 +41,7 @@ class Shape(ctypes.Structure):
     _fields_ = [
         ("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
         ("dk", ctypes.c_int32), ("dv", ctypes.c_int32),
-        ("backbone", ctypes.c_int32), ("centered", ctypes.c_int32), ("pad_", ctypes.c_int32),
+        ("backbone", ctypes.c_int32), ("centered", ctypes.c_int32), ("decay", ctypes.c_int32),
         ("scale", ctypes.c_double), ("t0", ctypes.c_int64),
     ]
 
@@ -94,10 +94,10 @@ def _ptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
 
-def _shape(q, v, backbone, centered, scale, t0):
+def _shape(q, v, backbone, centered, scale, t0, decay=False):
     B, T, H, dk = q.shape
     dv = v.shape[-1]
-    return Shape(B, T, H, dk, dv, backbone, int(centered), 0, float(scale), int(t0))
+    return Shape(B, T, H, dk, dv, backbone, int(centered), int(decay), float(scale), int(t0))
 
 
 def _inputs(q, k, v, gate, beta, lam, backbone):
@@ -120,12 +120,15 @@ def _outputs(q, v):
 
 
 def fwd(q, k, v, gate, lam, beta=None, backbone=GLA, S0=None, C0=None, mu0=None,
-        scale=1.0, centered=True, t0=0, form=0):
-    """Token-by-token CCQ forward.  Returns dict o, ST, CT, muT, qclean."""
+        scale=1.0, centered=True, t0=0, form=0, decay=False):
+    """Token-by-token CCQ forward.  Returns dict o, ST, CT, muT, qclean.
+    decay=True (Gated DeltaNet, t0 = 0, no C0/mu0): the decay-aligned statistics,
+    each key weighted by the product of the later alphas and t replaced by the
+    decayed count W_t = alpha_t W_{t-1} + 1."""
     q, k, v, gate, beta, lam = _inputs(q, k, v, gate, beta, lam, backbone)
     S0, C0, mu0 = _f64(S0), _f64(C0), _f64(mu0)
     o, ST, CT, muT, qc = _outputs(q, v)
-    sh = _shape(q, v, backbone, centered, scale, t0)
+    sh = _shape(q, v, backbone, centered, scale, t0, decay)
     rc = _load().ccq_oracle_fwd(ctypes.byref(sh), int(form), _ptr(q), _ptr(k), _ptr(v), _ptr(gate),
                                 _ptr(beta), _ptr(lam), _ptr(S0), _ptr(C0), _ptr(mu0), _ptr(o),
                                 _ptr(ST), _ptr(CT), _ptr(muT), _ptr(qc))

@@ -530,3 +530,84 @@ def test_packed_reverse_pass_of_equal_lengths_is_the_batched_call(backbone):
                          backbone=backbone)
     for key in ("o", "dq", "dk", "dv", "dg", "dlam") + (("dbeta",) if backbone == O.GDN else ()):
         np.testing.assert_allclose(r[key], ref[key].reshape(r[key].shape), rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------- decay-aligned statistics (App. J)
+# The reading: for Gated DeltaNet's scalar decay, key j enters token t's
+# statistics with weight gamma_{j,t} = prod_{s=j+1..t} alpha_s, normalised by
+# W_t = sum_j gamma_{j,t}.  These pins hold the oracle's decay=True path to
+# numpy's weighted covariance, to the undecayed path at alpha = 1, to its own
+# running-mean form, and to a restart where alpha vanishes.
+
+def _gdn_decay_inputs(rng, T, dk, dv, H=1, B=1, logalpha=None):
+    d = rnd_inputs(rng, B, T, H, dk, dv, backbone=O.GDN)
+    if logalpha is not None:
+        d["gate"] = logalpha
+    return d
+
+
+def test_decay_aligned_is_numpy_weighted_covariance():
+    rng = np.random.default_rng(51)
+    T, dk, dv = 14, 3, 2
+    d = _gdn_decay_inputs(rng, T, dk, dv)
+    d["gate"] = -rng.uniform(0.05, 1.5, size=(1, T, 1))      # strong forgetting
+    d["k"] = d["k"] + 2.0                                     # a common key mean
+    r = run(d, backbone=O.GDN, decay=True)
+    L = np.cumsum(d["gate"][0, :, 0])
+    k, q, lam = d["k"][0, :, 0], d["q"][0, :, 0], d["lam"][0, :, 0]
+    for t in range(T):
+        w = np.exp(L[t] - L[:t + 1])                          # gamma_{j,t}, j <= t
+        if t == 0:
+            sig = np.zeros((dk, dk))
+        else:
+            sig = np.cov(k[:t + 1].T, aweights=w, bias=True)
+        qc = q[t] - lam[t] * sig @ q[t]
+        np.testing.assert_allclose(r["qclean"][0, t, 0], qc, rtol=0, atol=1e-12)
+    W = np.exp(L[-1] - L).sum()
+    wT = np.exp(L[-1] - L)
+    np.testing.assert_allclose(r["muT"][0, 0], (wT[:, None] * k).sum(0) / W, atol=1e-12)
+    np.testing.assert_allclose(r["CT"][0, 0], np.einsum("j,ja,jb->ab", wT, k, k) / W, atol=1e-12)
+
+
+def test_decay_aligned_without_decay_is_sigma():
+    rng = np.random.default_rng(52)
+    d = _gdn_decay_inputs(rng, 40, 5, 4, H=2)
+    d["gate"] = np.zeros((1, 40, 2))                          # alpha = 1
+    a = run(d, backbone=O.GDN, decay=True)
+    b = run(d, backbone=O.GDN)
+    for key in ("o", "qclean", "CT", "muT", "ST"):
+        np.testing.assert_array_equal(a[key], b[key])
+
+
+def test_decay_aligned_running_mean_form_agrees():
+    rng = np.random.default_rng(53)
+    d = _gdn_decay_inputs(rng, 50, 6, 5, H=2)
+    a = run(d, backbone=O.GDN, decay=True, form=0)
+    b = run(d, backbone=O.GDN, decay=True, form=1)
+    for key in ("o", "qclean", "CT", "muT"):
+        np.testing.assert_allclose(a[key], b[key], rtol=1e-10, atol=1e-12)
+
+
+def test_decay_aligned_vanishing_alpha_restarts_the_statistics():
+    """alpha_t = 0 at t* erases every earlier key from the statistics (and the Gated
+    DeltaNet state), so from t* on the outputs are those of a fresh run on the suffix."""
+    rng = np.random.default_rng(54)
+    T, ts = 45, 17
+    d = _gdn_decay_inputs(rng, T, 6, 4, H=2)
+    d["gate"][:, ts] = -1e4                                   # exp(-1e4) == 0 in fp64
+    full = run(d, backbone=O.GDN, decay=True)
+    tail = {k_: (None if v is None else v[:, ts:]) for k_, v in d.items()}
+    part = run(tail, backbone=O.GDN, decay=True)
+    # Sigma^gamma = k k^T - k k^T = 0 there (up to the rounding of the two products)
+    np.testing.assert_allclose(full["qclean"][:, ts], d["q"][:, ts], rtol=0, atol=1e-14)
+    np.testing.assert_allclose(full["qclean"][:, ts:], part["qclean"], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(full["o"][:, ts:], part["o"], rtol=1e-12, atol=1e-13)
+
+
+def test_decay_aligned_rejected_where_not_defined():
+    rng = np.random.default_rng(55)
+    d = _gdn_decay_inputs(rng, 8, 4, 4)
+    with pytest.raises(RuntimeError):
+        run(rnd_inputs(rng, 1, 8, 1, 4, 4), backbone=O.GLA, decay=True)   # per-channel decay
+    with pytest.raises(RuntimeError):
+        run(d, backbone=O.GDN, decay=True, t0=5)                          # no decayed count cached
