@@ -390,6 +390,15 @@ class Call:
                                  out=self.out, workspace=self.ws)
 
 
+class DecayCall(Call):
+    """The Gated DeltaNet forward with the decay-aligned statistics (ccq_shape.decay_aligned)."""
+
+    def __call__(self):
+        d = self.d
+        self.ccq.ccq_gdn_fwd(d["q"], d["k"], d["v"], d["logalpha"], d["beta"], d["lam"],
+                             out=self.out, workspace=self.ws, decay_aligned=True)
+
+
 class DecodeCall:
     """One recurrent decode step (one token per sequence) at position T + 1 of a
     workload's shape, with the cache resident on the GPU (updated in place)."""
@@ -602,7 +611,7 @@ def roofline(entry, w):
 
 EXTRA = ("gla_500m_t2k", "gdn_1p3b_t4k", "gla_500m_t20k", "gdn_1p3b_t20k", "gla_train_t4k",
          "gdn_train_t4k", "gla_500m_decode_t2k", "gdn_1p3b_decode_t4k", "gdn_1p3b_prep_t4k",
-         "gdn_1p3b_raw_t4k", "gdn_1p3b_varlen_t4k")
+         "gdn_1p3b_raw_t4k", "gdn_1p3b_varlen_t4k", "gdn_1p3b_decay_t4k")
 
 
 def measure_extra(name, torch, ccq, inputs, steps, existing):
@@ -642,13 +651,17 @@ def measure_extra(name, torch, ccq, inputs, steps, existing):
                "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
                "roofline": roofline(pk[0], c.w)}
     else:
-        c = existing.get(name) or Call(W[name], torch, ccq, inputs)
+        if "_decay_" in name:
+            c = DecayCall(W[name.replace("_decay_t", "_t")], torch, ccq, inputs)
+        else:
+            c = existing.get(name) or Call(W[name], torch, ccq, inputs)
         ms, ms_tr, pk = time_calls(torch, ccq, [c], max(5, steps // 2), 3, with_plain=True)
         dom = max(pk, key=lambda e: e["ms_mean"])
         res = {"tokens_per_s": round(c.w.tokens / (ms * 1e-3), 1), "ms": round(ms, 4),
                "ms_traced": round(ms_tr, 4),
                "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
-               "roofline": method_roofline(c.w, c.ms_call, call_traffic(c.kernels, c.w.name)),
+               "roofline": method_roofline(c.w, c.ms_call,
+                                           call_traffic(c.kernels, name if "_decay_" in name else c.w.name)),
                "dominant_kernel": roofline(dom, c.w)}
     if name not in existing:
         del c

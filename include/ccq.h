@@ -68,6 +68,15 @@ typedef struct {
   ccq_dtype gate_dtype; /* dtype of the GLA gate g (and of dg); ignored for GDN */
   float scale;          /* o = scale * S q_clean; the paper's read uses 1.0 */
   int32_t centered;     /* 1: Sigma = Cbar - mu mu^T (the paper); 0: Sigma = Cbar (App. E ablation) */
+  int32_t decay_aligned;/* 0: the paper's undecayed statistics.  1 (Gated DeltaNet forward only):
+                         * the decay-aligned covariance Sigma^gamma that App. J names as future
+                         * work for forgetting backbones, read as key j entering token t's
+                         * statistics with the backbone's own decay prod_{s=j+1..t} alpha_s and
+                         * t replaced by the decayed count W_t = alpha_t W_{t-1} + 1 (Alg. 2's
+                         * running means with W_t for t); alpha = 1 gives Sigma_t.  Needs t0 = 0
+                         * and no C0 / mu0 (the cache holds no W); CT, muT are then the
+                         * weighted means.  Else CCQ_ERR_UNSUPPORTED (GLA, whose decay is per
+                         * channel; ccq_fwd_bwd; ccq_decode). */
   int64_t t0;           /* tokens already absorbed into C0/mu0; positions are t0+1 .. t0+T */
 } ccq_shape;
 

@@ -41,7 +41,8 @@ class Shape(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("dk", ctypes.c_int32), ("dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
                 ("io_dtype", ctypes.c_int32), ("gate_dtype", ctypes.c_int32),
-                ("scale", ctypes.c_float), ("centered", ctypes.c_int32), ("t0", ctypes.c_int64)]
+                ("scale", ctypes.c_float), ("centered", ctypes.c_int32),
+                ("decay_aligned", ctypes.c_int32), ("t0", ctypes.c_int64)]
 
 
 _lib = None
@@ -130,10 +131,10 @@ def _dt(t: torch.dtype) -> int:
 
 
 def make_shape(B, T, H, dk, dv, io_dtype, gate_dtype=None, scale=1.0, centered=True, t0=0,
-               chunk=64) -> Shape:
+               chunk=64, decay_aligned=False) -> Shape:
     gd = io_dtype if gate_dtype is None else gate_dtype
     return Shape(int(B), int(T), int(H), int(dk), int(dv), int(chunk), _dt(io_dtype), _dt(gd),
-                 float(scale), int(bool(centered)), int(t0))
+                 float(scale), int(bool(centered)), int(bool(decay_aligned)), int(t0))
 
 
 def ccq_workspace_size(shape: Shape, backbone: int, with_bwd: bool = False) -> int:
@@ -185,12 +186,13 @@ def _workspace(shape, backbone, with_bwd, workspace, device):
 
 
 def _fwd(backbone, q, k, v, gate, lam, beta, S0, C0, mu0, scale, centered, t0, chunk,
-         want_states, want_qclean, out, workspace, stream):
+         want_states, want_qclean, out, workspace, stream, decay_aligned=False):
     B, T, H, dk = q.shape
     dv = v.shape[-1]
     dev = q.device
     gate_dtype = gate.dtype if backbone == CCQ_GLA else q.dtype
-    shape = make_shape(B, T, H, dk, dv, q.dtype, gate_dtype, scale, centered, t0, chunk)
+    shape = make_shape(B, T, H, dk, dv, q.dtype, gate_dtype, scale, centered, t0, chunk,
+                       decay_aligned)
     _check(k, "k", (B, T, H, dk), q.dtype, dev)
     _check(v, "v", (B, T, H, dv), q.dtype, dev)
     if backbone == CCQ_GLA:
@@ -241,10 +243,11 @@ def ccq_gla_fwd(q, k, v, g, lam, S0=None, C0=None, mu0=None, scale=1.0, centered
 
 def ccq_gdn_fwd(q, k, v, logalpha, beta, lam, S0=None, C0=None, mu0=None, scale=1.0,
                 centered=True, t0=0, chunk=64, want_states=True, want_qclean=False, out=None,
-                workspace=None, stream=None):
-    """CCQ-Gated-DeltaNet chunkwise forward.  Returns dict o[, ST, CT, muT][, qclean]."""
+                workspace=None, stream=None, decay_aligned=False):
+    """CCQ-Gated-DeltaNet chunkwise forward.  Returns dict o[, ST, CT, muT][, qclean].
+    decay_aligned=True: the decay-aligned statistics (ccq_shape.decay_aligned)."""
     return _fwd(CCQ_GDN, q, k, v, logalpha, lam, beta, S0, C0, mu0, scale, centered, t0, chunk,
-                want_states, want_qclean, out, workspace, stream)
+                want_states, want_qclean, out, workspace, stream, decay_aligned)
 
 
 # CCQ_NOALLOC_SCRATCH_BYTES of include/ccq.h
@@ -338,7 +341,8 @@ def ccq_varlen_workspace_size(shape: Shape, backbone: int, with_bwd: bool = Fals
                                                int(bool(with_bwd))))
 
 
-def _varlen_shape(backbone, q, v, gate, cu_seqlens, max_len, scale, centered, t0):
+def _varlen_shape(backbone, q, v, gate, cu_seqlens, max_len, scale, centered, t0,
+                  decay_aligned=False):
     if cu_seqlens.dtype != torch.int32 or cu_seqlens.dim() != 1 or cu_seqlens.numel() < 1:
         raise TypeError("cu_seqlens must be a 1-D int32 tensor of B + 1 offsets")
     if cu_seqlens.device != q.device or not cu_seqlens.is_contiguous():
@@ -346,7 +350,8 @@ def _varlen_shape(backbone, q, v, gate, cu_seqlens, max_len, scale, centered, t0
     rows, H, dk = q.shape
     B = cu_seqlens.numel() - 1
     gate_dtype = gate.dtype if backbone == CCQ_GLA else q.dtype
-    return make_shape(B, max_len, H, dk, v.shape[-1], q.dtype, gate_dtype, scale, centered, t0)
+    return make_shape(B, max_len, H, dk, v.shape[-1], q.dtype, gate_dtype, scale, centered, t0,
+                      decay_aligned=decay_aligned)
 
 
 def _varlen_ws(shape, backbone, with_bwd, workspace, device):
@@ -357,11 +362,12 @@ def _varlen_ws(shape, backbone, with_bwd, workspace, device):
 
 
 def _varlen_fwd(backbone, q, k, v, gate, beta, lam, cu_seqlens, max_len, S0, C0, mu0, scale,
-                centered, t0, want_states, out, workspace, stream):
+                centered, t0, want_states, out, workspace, stream, decay_aligned=False):
     rows, H, dk = q.shape
     dv = v.shape[-1]
     dev = q.device
-    shape = _varlen_shape(backbone, q, v, gate, cu_seqlens, max_len, scale, centered, t0)
+    shape = _varlen_shape(backbone, q, v, gate, cu_seqlens, max_len, scale, centered, t0,
+                          decay_aligned)
     B = shape.B
     _check(k, "k", (rows, H, dk), q.dtype, dev)
     _check(v, "v", (rows, H, dv), q.dtype, dev)
@@ -415,11 +421,11 @@ def ccq_gla_fwd_varlen(q, k, v, g, lam, cu_seqlens, max_len, S0=None, C0=None, m
 
 def ccq_gdn_fwd_varlen(q, k, v, logalpha, beta, lam, cu_seqlens, max_len, S0=None, C0=None,
                        mu0=None, scale=1.0, centered=True, t0=0, want_states=True, out=None,
-                       workspace=None, stream=None):
+                       workspace=None, stream=None, decay_aligned=False):
     """CCQ-Gated-DeltaNet forward on a packed batch (layout as ccq_gla_fwd_varlen;
-    logalpha, beta [rows,H] fp32)."""
+    logalpha, beta [rows,H] fp32).  decay_aligned as ccq_gdn_fwd."""
     return _varlen_fwd(CCQ_GDN, q, k, v, logalpha, beta, lam, cu_seqlens, max_len, S0, C0, mu0,
-                       scale, centered, t0, want_states, out, workspace, stream)
+                       scale, centered, t0, want_states, out, workspace, stream, decay_aligned)
 
 
 def ccq_fwd_bwd_varlen(q, k, v, g, lam, dO, cu_seqlens, max_len, scale=1.0, centered=True,

@@ -63,7 +63,10 @@ ccq_status check_shape(const ccq_shape* s, ccq_backbone bb) {
   if (s->B < 0 || s->T < 0 || s->H < 0 || s->t0 < 0) return CCQ_ERR_INVALID_ARG;
   if (!dtype_ok(s->io_dtype) || !dtype_ok(s->gate_dtype)) return CCQ_ERR_INVALID_ARG;
   if (s->centered != 0 && s->centered != 1) return CCQ_ERR_INVALID_ARG;
+  if (s->decay_aligned != 0 && s->decay_aligned != 1) return CCQ_ERR_INVALID_ARG;
   if (bb != CCQ_GLA && bb != CCQ_GDN) return CCQ_ERR_INVALID_ARG;
+  // the decay-aligned statistics: scalar decay (Gated DeltaNet), from empty statistics
+  if (s->decay_aligned && (bb != CCQ_GDN || s->t0 != 0)) return CCQ_ERR_UNSUPPORTED;
   if (s->chunk != 64) return CCQ_ERR_UNSUPPORTED;
   const bool bf = s->io_dtype == CCQ_BF16;
   if (!ccq::clean_supported(s->dk, bf)) return CCQ_ERR_UNSUPPORTED;
@@ -78,7 +81,7 @@ ccq_status check_shape(const ccq_shape* s, ccq_backbone bb) {
 
 // Workspace of the query contraction: segment and chunk key statistics.
 struct CleanWs {
-  size_t gram = 0, sprime = 0, csum = 0, ssum = 0;
+  size_t gram = 0, sprime = 0, csum = 0, ssum = 0, sdec = 0;
 };
 
 template <typename Take>
@@ -91,6 +94,7 @@ CleanWs take_clean_ws(const ccq_shape* s, Take&& take) {
   c.sprime = take(bh * ns * dk * dk * esize(s->io_dtype));
   c.csum = take(bh * nc * dk * 4);
   c.ssum = take(bh * ns * dk * 4);
+  c.sdec = take(bh * ns * 2 * 4);  // decay-aligned statistics: segment weight sums and decays
   return c;
 }
 
@@ -100,6 +104,7 @@ ccq::CleanArgs clean_args(const ccq_shape* s, char* ws, const CleanWs& c) {
   a.sprime = ws + c.sprime;
   a.csum = reinterpret_cast<float*>(ws + c.csum);
   a.ssum = reinterpret_cast<float*>(ws + c.ssum);
+  a.sdec = reinterpret_cast<float*>(ws + c.sdec);
   a.B = s->B;
   a.T = s->T;
   a.H = s->H;
@@ -266,6 +271,7 @@ ccq_status check_forward_args(ccq_backbone bb, const ccq_shape* s, const void* q
                               const float* muT, const float* q_clean_dbg, const void* workspace) {
   ccq_status rc = check_shape(s, bb);
   if (rc != CCQ_OK) return rc;
+  if (s->decay_aligned && (C0 || mu0)) return CCQ_ERR_UNSUPPORTED;  // no cached W to continue from
   const size_t ntok = (size_t)s->B * s->T * s->H;
   const void* ptrs[] = {S0, C0, mu0, ST, CT, muT, q_clean_dbg, workspace};
   for (const void* p : ptrs)
@@ -356,6 +362,7 @@ ccq_status run_forward(ccq_backbone bb, const ccq_shape* s, const void* q, const
   ca.qclean_dbg = q_clean_dbg;
   ca.CT = CT;
   ca.muT = muT;
+  if (s->decay_aligned) ca.la = la;  // keys weighted by the backbone's decay (check_shape: GDN)
   if (run_clean_stats(ca, bf, st) != hipSuccess) return CCQ_ERR_HIP;
   if (traced(st, [&] { return ccq::launch_clean_out(ca, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
 
@@ -695,6 +702,7 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
   ccq_status rc = check_shape(s, bb);
   if (rc != CCQ_OK) return rc;
   if (s->t0 != 0) return CCQ_ERR_INVALID_ARG;     // a training step starts from zero states
+  if (s->decay_aligned) return CCQ_ERR_UNSUPPORTED;  // the decay-aligned statistics: forward only
   const bool bf = s->io_dtype == CCQ_BF16;
   const bool gbf = s->gate_dtype == CCQ_BF16;
   if (!ccq::bwd_supported(s->dk, s->dv, bf, bb == CCQ_GDN)) return CCQ_ERR_UNSUPPORTED;
@@ -774,6 +782,7 @@ ccq_status ccq_fwd_bwd_varlen(const ccq_shape* s, ccq_backbone bb, const int32_t
   ccq_status rc = check_varlen(s, bb, cu_seqlens);
   if (rc != CCQ_OK) return rc;
   if (s->t0 != 0) return CCQ_ERR_INVALID_ARG;
+  if (s->decay_aligned) return CCQ_ERR_UNSUPPORTED;  // the decay-aligned statistics: forward only
   if (!ccq::bwd_supported(s->dk, s->dv, s->io_dtype == CCQ_BF16, bb == CCQ_GDN)) return CCQ_ERR_UNSUPPORTED;
   if (workspace && !aligned(workspace)) return CCQ_ERR_INVALID_ARG;
   if ((size_t)s->B * s->T * s->H == 0) return CCQ_OK;
@@ -826,7 +835,9 @@ ccq_status ccq_decode(const ccq_shape* s, ccq_backbone bb, const void* q, const 
   if (s->B < 0 || s->H < 0 || s->t0 < 0 || s->T != 1) return CCQ_ERR_INVALID_ARG;
   if (!dtype_ok(s->io_dtype) || !dtype_ok(s->gate_dtype)) return CCQ_ERR_INVALID_ARG;
   if (s->centered != 0 && s->centered != 1) return CCQ_ERR_INVALID_ARG;
+  if (s->decay_aligned != 0 && s->decay_aligned != 1) return CCQ_ERR_INVALID_ARG;
   if (bb != CCQ_GLA && bb != CCQ_GDN) return CCQ_ERR_INVALID_ARG;
+  if (s->decay_aligned) return CCQ_ERR_UNSUPPORTED;  // the cache holds no decayed count
   if (!ccq::decode_supported(s->dk, s->dv)) return CCQ_ERR_UNSUPPORTED;
   if ((long long)s->B * s->H > 0x7fffffffLL) return CCQ_ERR_UNSUPPORTED;  // one workgroup per head
   if (s->B == 0 || s->H == 0) return CCQ_OK;

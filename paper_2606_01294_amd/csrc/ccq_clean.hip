@@ -27,6 +27,19 @@
 //                 chunks) held in MFMA accumulators
 // Without centring (Sigma = Cbar) the same kernels run with c_s = 0 and no
 // mean terms.
+//
+// Decay-aligned statistics (DECAY; Gated DeltaNet's scalar decay alpha_t):
+// key j enters token t's sums with weight w_{j,t} = e^{L_t - L_j} (L the
+// cumulative log decay) and t becomes W_t = sum_{j<=t} w_{j,t}.  Every sum
+// is kept decayed to the point it is taken at: the Gram and key sums of a
+// chunk or segment to its end, the carried moment of clean_out to the chunk
+// it enters; a sum moves on by one chunk as  X <- e^{gamma_C} X + (the chunk's
+// terms weighted e^{gamma_C - gamma_j})  (gamma the chunk's inclusive log-decay
+// prefix), and within a chunk token i sees e^{gamma_i} times the chunk-entry
+// sums plus its keys weighted e^{gamma_i - gamma_j}.  The shift invariance
+// above holds for the weighted covariance too (with W in place of t), so the
+// segment centring is unchanged; c_s is the segment's weighted mean.  Every
+// factor is at most 1.
 #include "ccq_device.h"
 #include "ccq_kernels.h"
 
@@ -52,7 +65,12 @@ __device__ __forceinline__ f32x4 load4f(const T* p) {
 // (head, segment); wave w owns rows [w RW, (w+1) RW) and all columns, so each
 // chunk of keys is read from memory once.  The chunk and segment key sums come
 // from the same products (a ones column).
-template <typename T, int DK>
+// DECAY: each chunk's rows are staged times sqrt(e^{gamma_C - gamma_j}) (so the
+// product of two of them carries the weight once), the ones column becomes
+// the column of those square roots, and the sums so far are decayed by the
+// chunk's e^{gamma_C} before its terms are added; also each segment's weight
+// sum and decay (sdec).
+template <typename T, int DK, bool DECAY>
 __global__ __launch_bounds__(64 * (DK >= 128 ? 8 : 4), 1) void clean_gram_kernel(const CleanArgs a) {
   constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P;
   constexpr int NWG = DK >= 128 ? 8 : 4, NTG = 64 * NWG;
@@ -60,6 +78,9 @@ __global__ __launch_bounds__(64 * (DK >= 128 ? 8 : 4), 1) void clean_gram_kernel
   constexpr int RT = RW / 16;   // row tiles per wave
   constexpr int CT = DK / 16;   // column tiles
   __shared__ __align__(16) T sK[2][C * LDK];
+  // DECAY, per chunk parity: sqrt of each row's weight, and the chunk's decay
+  __shared__ __align__(16) float sW[2][DECAY ? C : 1];
+  __shared__ float sDc[2];
 
   const int NC = n_chunks(a.T), NS = n_segs(a.T, a.seg);
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
@@ -83,29 +104,81 @@ __global__ __launch_bounds__(64 * (DK >= 128 ? 8 : 4), 1) void clean_gram_kernel
 
   RowTile<T, DK, NTG> rk;
   RowScales<RowTile<T, DK, NTG>> fk;
+  float lav = 0.f;    // DECAY, wave 0: the log decay of row l of the next chunk
+  float om = 0.f;     // DECAY, wave 0: the segment's weight sum so far
+  float lseg = 0.f;   // DECAY, wave 0: the segment's log decay so far
   auto load = [&](int c) {
-    rk.load(k + seq_off(sq, c * C, h, a.H, DK), gstride, min(C, sq.len - c * C));
-    if (a.rk) fk.load(a.rk + seq_idx(sq, c * C, h, a.H), (size_t)a.H, min(C, sq.len - c * C));
+    const int n = min(C, sq.len - c * C);
+    rk.load(k + seq_off(sq, c * C, h, a.H, DK), gstride, n);
+    if (a.rk) fk.load(a.rk + seq_idx(sq, c * C, h, a.H), (size_t)a.H, n);
+    if constexpr (DECAY)
+      if (w == 0) lav = l < n ? a.la[seq_idx(sq, c * C + l, h, a.H)] : 0.f;
   };
   if (cbeg < cend) load(cbeg);
   const Frag<T> ones = ones_col_frag<T>();
 
   for (int c = cbeg; c < cend; ++c) {
-    T* buf = sK[(c - cbeg) & 1];  // the other buffer may still be read by a slower wave
-    if (a.rk) fk.apply(rk);
+    const int par = (c - cbeg) & 1;
+    T* buf = sK[par];  // the other buffer may still be read by a slower wave
+    if constexpr (DECAY) {
+      if (w == 0) {
+        // inclusive log-decay prefix over the chunk's rows (lane = row)
+        float g = lav;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const float u = __shfl_up(g, o);
+          if (l >= o) g += u;
+        }
+        const float gC = __shfl(g, 63);  // rows past the end add nothing
+        const int n = min(C, sq.len - c * C);
+        const float wj = l < n ? __expf(gC - g) : 0.f;
+        sW[par][l] = l < n ? __expf(0.5f * (gC - g)) : 0.f;
+        float ws = wj;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) ws += __shfl_xor(ws, o);
+        om = __expf(gC) * om + ws;
+        lseg += gC;
+        if (l == 0) sDc[par] = __expf(gC);
+      }
+      __syncthreads();  // the chunk's weights
+#pragma unroll
+      for (int u = 0; u < RowTile<T, DK, NTG>::NV; ++u)
+        if (RowTile<T, DK, NTG>::mine(u)) {
+          const float f = sW[par][RowTile<T, DK, NTG>::row(u)] * (a.rk ? fk.f[u] : 1.f);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) rk.v[u][e] = to<T>(f32(rk.v[u][e]) * f);
+        }
+    } else {
+      if (a.rk) fk.apply(rk);
+    }
     rk.store(buf, LDK);
     if (c + 1 < cend) load(c + 1);
     __syncthreads();
+    if constexpr (DECAY) {  // the sums so far, decayed to this chunk's end
+      const float dc = sDc[par];
+#pragma unroll
+      for (int v = 0; v < RT; ++v) {
+        stot[v] *= dc;
+#pragma unroll
+        for (int t = 0; t < CT; ++t) acc[v][t] *= dc;
+      }
+    }
     f32x4 msum[RT];
 #pragma unroll
     for (int v = 0; v < RT; ++v) msum[v] = zero4();
 #pragma unroll
     for (int k0 = 0; k0 < C; k0 += 32) {
+      Frag<T> col = ones;  // DECAY: column 0 holds the square roots of the rows' weights
+      if constexpr (DECAY) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          set_frag_elem(col, e, c16 == 0 ? sW[par][k0 + 8 * g4 + e] : 0.f);
+      }
       Frag<T> fa[RT];
 #pragma unroll
       for (int v = 0; v < RT; ++v) {
         fa[v] = ld_frag_tr(buf + k0 * LDK + a0 + 16 * v, LDK);
-        mma(msum[v], fa[v], ones);
+        mma(msum[v], fa[v], col);
       }
 #pragma unroll
       for (int t = 0; t < CT; ++t) {
@@ -127,6 +200,11 @@ __global__ __launch_bounds__(64 * (DK >= 128 ? 8 : 4), 1) void clean_gram_kernel
     for (int v = 0; v < RT; ++v)
       *reinterpret_cast<f32x4*>(a.ssum + ((size_t)bh * NS + s) * DK + a0 + 16 * v + 4 * g4) = stot[v];
   }
+  if constexpr (DECAY)
+    if (w == 0 && l == 0) {  // (an empty segment: no weight, no decay)
+      a.sdec[((size_t)bh * NS + s) * 2] = om;
+      a.sdec[((size_t)bh * NS + s) * 2 + 1] = __expf(lseg);
+    }
   // acc[v][t] is accumulator tile (rows m = a0 + 16 v .., columns n = 16 t ..),
   // stored fragment-native: 1 KB per tile, lane-contiguous
   float* G = a.gram + ((size_t)bh * NS + s) * DK * DK;
@@ -143,7 +221,10 @@ __global__ __launch_bounds__(64 * (DK >= 128 ? 8 : 4), 1) void clean_gram_kernel
 // sum before it about c_s (running sums of the segment key sums).  Each thread
 // owns four consecutive fragment-native elements, (m .. m + 3, n): one scalar
 // index n and a vector of four m.  Also the final Cbar_T and mu_T.
-template <typename T, int DK>
+// DECAY: the prefix runs over the segments decayed, X <- E_s X + (segment s's
+// sum, decayed to its end), and the segment's and the earlier tokens' decayed
+// weight sums take the place of the token counts (t0 = 0, no C0 / mu0).
+template <typename T, int DK, bool DECAY>
 __global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
   constexpr int PER = DK * DK / 4 / 256;  // workgroups per head
   constexpr int NMT = DK / 16;
@@ -161,11 +242,18 @@ __global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
   float run_a = a.mu0 ? t0f * a.mu0[(size_t)bh * DK + n] : 0.f;  // raw key sums before s
   f32x4 run_b = a.mu0 ? *reinterpret_cast<const f32x4*>(a.mu0 + (size_t)bh * DK + m) * t0f : zero4();
   T* Sp = static_cast<T*>(a.sprime);
+  float wb = 0.f;  // DECAY: decayed weight of the tokens before segment s
   for (int s = 0; s < NSL; ++s) {
     const size_t so = (size_t)bh * NS + s;
     const int cbeg = s * a.seg, cend = min(NCL, cbeg + a.seg);
-    const float len = (float)(min(sq.len, cend * kChunk) - cbeg * kChunk);
-    const float ns = t0f + (float)((int64_t)cbeg * kChunk);
+    float len = (float)(min(sq.len, cend * kChunk) - cbeg * kChunk);
+    float ns = t0f + (float)((int64_t)cbeg * kChunk);
+    float E = 1.f;
+    if constexpr (DECAY) {
+      len = a.sdec[so * 2];
+      E = a.sdec[so * 2 + 1];
+      ns = wb;
+    }
     const float tot_a = a.ssum[so * DK + n];
     const f32x4 tot_b = *reinterpret_cast<const f32x4*>(a.ssum + so * DK + m);
     const f32x4 gm = *reinterpret_cast<const f32x4*>(a.gram + so * DK * DK + 4 * (size_t)g);
@@ -177,9 +265,16 @@ __global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) o[q] = acc[q] - ma * cb4[q] - ca * mb4[q] - ns * ca * cb4[q];
     store4(Sp + so * DK * DK + 4 * (size_t)g, o[0], o[1], o[2], o[3]);
-    acc += gm;
-    run_a += tot_a;
-    run_b += tot_b;
+    if constexpr (DECAY) {
+      acc = acc * E + gm;
+      run_a = run_a * E + tot_a;
+      run_b = run_b * E + tot_b;
+      wb = wb * E + len;
+    } else {
+      acc += gm;
+      run_a += tot_a;
+      run_b += tot_b;
+    }
   }
   if (a.t0 + sq.len == 0) {  // no token at all (an empty packed sequence): the initial cache
     if (a.CT)
@@ -190,7 +285,7 @@ __global__ __launch_bounds__(256) void clean_prefix_kernel(const CleanArgs a) {
           a.mu0 ? *reinterpret_cast<const f32x4*>(a.mu0 + (size_t)bh * DK + m) : zero4();
     return;
   }
-  const float inv = 1.f / (t0f + (float)sq.len);
+  const float inv = 1.f / (DECAY ? wb : t0f + (float)sq.len);  // W_T for the decayed sums
   if (a.CT) *reinterpret_cast<f32x4*>(a.CT + ((size_t)bh * DK + n) * DK + m) = acc * inv;
   if (a.muT && n == 0) *reinterpret_cast<f32x4*>(a.muT + (size_t)bh * DK + m) = run_b * inv;
 }
@@ -225,7 +320,14 @@ __device__ __forceinline__ int causal_tile_i(int t) { return t >= 6 ? 3 : t >= 3
 // cq'_i = m'_i . x_i comes from the score row sums and M'_r . x_i.  x and K'
 // are staged in LDS once per chunk; q_clean is formed in place over x and is
 // copied out with row-contiguous stores while the next chunk is staged.
-template <typename T, int DK, int NW, bool TRAIN>
+// DECAY (the decay-aligned statistics): with gamma the chunk's inclusive
+// log-decay prefix and W_i token i's decayed count,
+//   out^T  = diag(e^{gamma_i}) S'_r x^T + K'^T sc,   sc_ij scaled e^{gamma_i - gamma_j}
+//   cq'_i  = e^{gamma_i} M'_r . x_i + sum_{j <= i} sc_ij,  shift cq'_i / W_i (times
+//            the weight), mean term e^{gamma_i} (cq'_i / W_i) M'_r, all over W_i
+//   S'_{r+1} = e^{gamma_C} S'_r + K'^T diag(e^{gamma_C - gamma}) K',
+//   M'_{r+1} = e^{gamma_C} M'_r + (the chunk's weighted key sum about c_s).
+template <typename T, int DK, int NW, bool TRAIN, bool DECAY>
 __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a) {
   constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P, LDP = C + P, LDQ = C + 4;
   constexpr int NT = 64 * NW, VPR = DK / 8;
@@ -243,7 +345,8 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
   constexpr bool kDma = sizeof(T) == 2;
   constexpr int oX = 0, oK = oX + C * LDK * (int)sizeof(T), oS = oK + C * LDK * (int)sizeof(T);
   constexpr int oP = oS + C * LDQ * 4, oC = oP + C * LDP * (int)sizeof(T), oM = oC + DK * 4;
-  constexpr int oCq = oM + DK * 4, oLam = oCq + C * 4, oSt = oLam + C * 4;
+  constexpr int oCq = oM + DK * 4, oLam = oCq + C * 4, oDec = oLam + C * 4;
+  constexpr int oSt = oDec + (DECAY ? (3 * C + 4) * 4 : 0);
   constexpr int oEnd = oSt + (kDma ? 2 * C * DK * (int)sizeof(T) : 16);
   __shared__ __align__(16) char smem[oEnd];
   T* const sX = reinterpret_cast<T*>(smem + oX);         // x rows, then q_clean rows
@@ -255,6 +358,14 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
   float* const sCq = reinterpret_cast<float*>(smem + oCq);
   float* const sLam = reinterpret_cast<float*>(smem + oLam);
   T* const sSt = reinterpret_cast<T*>(smem + oSt);
+  // DECAY: gamma_i, e^{gamma_i}, W_i of the chunk's tokens, and [0] W entering the
+  // chunk, [1] e^{gamma_C} and [2] the weight sum of the previous chunk, [3] W
+  // leaving this chunk
+  float* const sGm = reinterpret_cast<float*>(smem + oDec);
+  float* const sEg = sGm + C;
+  float* const sWt = sGm + 2 * C;
+  float* const sSc = sGm + 3 * C;
+  static_assert(!(DECAY && sizeof(T) == 2 && DK == 256 && oEnd > 160 * 1024), "LDS");
 
   const int NC = n_chunks(a.T), NS = n_segs(a.T, a.seg);
   const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
@@ -278,7 +389,7 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
   const size_t so = (size_t)bh * NS + s;
 
   Tile rx, rk;
-  RowScalar rl;
+  RowScalar rl, rla;  // lambda and (DECAY) the log decay of token tid
   // row scales of raw q and k (l2 normalisation folded in), for the rows of
   // this thread's staged vectors
   float fq[NV], fk[NV];
@@ -300,6 +411,7 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
       rk.load(k + seq_off(sq, r0, h, a.H, DK), gstride, n);
     }
     if (tid < C) rl.load(a.lam + seq_idx(sq, r0, h, a.H), (size_t)a.H, tid, n);
+    if (DECAY && tid < C) rla.load(a.la + seq_idx(sq, r0, h, a.H), (size_t)a.H, tid, n);
   };
   prefetch(cbeg);
 
@@ -308,13 +420,28 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
   float cen = 0.f;
   if (tid < DK) {
     const float* ss = a.ssum + (size_t)bh * NS * DK + tid;
-    float run = a.mu0 ? t0f * a.mu0[(size_t)bh * DK + tid] : 0.f;
+    if constexpr (DECAY) {
+      // decayed key sum and weight before the segment (segment sums decayed
+      // to their ends, carried through the later segments' decays)
+      const float* sd = a.sdec + (size_t)bh * NS * 2;
+      float run = 0.f, wb = 0.f;
+      for (int p = 0; p < s; ++p) {
+        run = run * sd[2 * p + 1] + ss[(size_t)p * DK];
+        wb = wb * sd[2 * p + 1] + sd[2 * p];
+      }
+      cen = a.centered ? ss[(size_t)s * DK] / sd[2 * s] : 0.f;
+      sC[tid] = cen;
+      sM[tid] = run - wb * cen;
+      if (tid == 0) sSc[3] = wb;  // W entering the segment's first chunk
+    } else {
+      float run = a.mu0 ? t0f * a.mu0[(size_t)bh * DK + tid] : 0.f;
 #pragma unroll 8
-    for (int p = 0; p < s; ++p) run += ss[(size_t)p * DK];
-    const float len = (float)(min(sq.len, cend * C) - cbeg * C);
-    cen = a.centered ? ss[(size_t)s * DK] / len : 0.f;
-    sC[tid] = cen;
-    sM[tid] = run - (t0f + (float)((int64_t)cbeg * C)) * cen;
+      for (int p = 0; p < s; ++p) run += ss[(size_t)p * DK];
+      const float len = (float)(min(sq.len, cend * C) - cbeg * C);
+      cen = a.centered ? ss[(size_t)s * DK] / len : 0.f;
+      sC[tid] = cen;
+      sM[tid] = run - (t0f + (float)((int64_t)cbeg * C)) * cen;
+    }
   }
   // entry moment S'_s, held with its rows in pair order: accumulator row
   // 4 g + r of tile mt is feature pair_feat(mt, g, r) = 32 (mt / 2) + 8 g +
@@ -345,8 +472,24 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
     // per-token and per-feature values first: waiting for their loads costs
     // nothing here, while after the stores below it would also wait for those
     if (tid < C) sLam[tid] = rl.get();
+    if constexpr (DECAY) {
+      if (tid < 64) {  // wave 0: the chunk's inclusive log-decay prefix (lane = token)
+        float g = rla.get();
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const float u = __shfl_up(g, o);
+          if (tid >= o) g += u;
+        }
+        sGm[tid] = g;
+        sEg[tid] = __expf(g);
+      }
+      if (tid == 0) sSc[0] = sSc[3];  // W entering this chunk
+    }
     if (tid < DK) {
-      if (c > cbeg) sM[tid] += csum - (float)C * cen;  // M'_c
+      if (c > cbeg) {  // M'_c
+        if constexpr (DECAY) sM[tid] = sSc[1] * sM[tid] + (csum - sSc[2] * cen);
+        else sM[tid] += csum - (float)C * cen;
+      }
       csum = a.csum[((size_t)bh * NC + c) * DK + tid];
     }
     // stage chunk c; each thread first copies out the q_clean of chunk c - 1
@@ -434,16 +577,23 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
     {
       const int t_ = opaque(tid);
       const int i = t_ / TPI, pp = t_ % TPI;
-      const float ti = t0f + (float)(r0 + i + 1);
+      float ti = t0f + (float)(r0 + i + 1);  // DECAY: becomes W_i below
       float sv[JPT];
-      float rs = 0.f, mq = 0.f, cx = 0.f;
+      float rs = 0.f, mq = 0.f, cx = 0.f, ws = 0.f;
       const float* srow = sS + i * LDQ + JPT * pp;
 #pragma unroll
       for (int e = 0; e < JPT; e += 4) {
         const f32x4 v4 = *reinterpret_cast<const f32x4*>(srow + e);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          sv[e + q] = JPT * pp + e + q <= i ? v4[q] : 0.f;
+          const int j = JPT * pp + e + q;
+          if constexpr (DECAY) {  // weight e^{gamma_i - gamma_j} (0 past the diagonal)
+            const float f = j <= i ? __expf(sGm[i] - sGm[j]) : 0.f;
+            ws += f;
+            sv[e + q] = f * v4[q];
+          } else {
+            sv[e + q] = j <= i ? v4[q] : 0.f;
+          }
           rs += sv[e + q];
         }
       }
@@ -476,6 +626,11 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
       rs = group_sum<TPI>(rs);
       mq = group_sum<TPI>(mq);
       cx = group_sum<TPI>(cx);
+      if constexpr (DECAY) {
+        const float eg = sEg[i];
+        mq *= eg;                               // the chunk-entry sum decayed to token i
+        ti = eg * sSc[0] + group_sum<TPI>(ws);  // W_i
+      }
       const float cqp = mq + rs;
       const float sub = a.centered ? cqp / ti : 0.f;
       T* prow = sP + i * LDP + JPT * pp;
@@ -483,11 +638,25 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
       for (int e = 0; e < JPT; e += 8) {
         vec_t y;
 #pragma unroll
-        for (int q = 0; q < 8; ++q) y[q] = to<T>(JPT * pp + e + q <= i ? sv[e + q] - sub : 0.f);
+        for (int q = 0; q < 8; ++q) {
+          if constexpr (DECAY) {  // the weight again (zero past the diagonal)
+            const int j = JPT * pp + e + q;
+            y[q] = to<T>(j <= i ? sv[e + q] - __expf(sGm[i] - sGm[j]) * sub : 0.f);
+          }
+          else y[q] = to<T>(JPT * pp + e + q <= i ? sv[e + q] - sub : 0.f);
+        }
         *reinterpret_cast<vec_t*>(prow + e) = y;
       }
       if (pp == 0) {
         sCq[i] = cqp;
+        if constexpr (DECAY) {
+          sWt[i] = ti;
+          if (i == C - 1) {  // W leaving the chunk, its decay and its own weight sum
+            sSc[3] = ti;
+            sSc[1] = sEg[C - 1];
+            sSc[2] = ti - sEg[C - 1] * sSc[0];
+          }
+        }
         if (TRAIN && a.mdot && i < nrow) a.mdot[seq_idx(sw, r0 + i, h, a.H)] = cqp + ti * cx;  // raw m . x
       }
     }
@@ -507,6 +676,13 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
       if constexpr (kDma)
 #pragma unroll
         for (int nt = 0; nt < NNT; ++nt) lds_wait(kb[nt]);
+      if constexpr (DECAY)  // the chunk-entry moment's part, decayed to each token
+#pragma unroll
+        for (int I = 0; I < 4; ++I) {
+          const float eg = sEg[16 * I + c_];
+#pragma unroll
+          for (int nt = 0; nt < NNT; ++nt) acc[nt][I] *= eg;
+        }
       // out^T += K'^T sc (keys 32..63 only reach tokens 32..63)
       const T* pp_ = sP + c_ * LDP + 8 * g_;
 #pragma unroll
@@ -532,8 +708,8 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
           else
             xb[nt] = load4f(sX + i * LDK + n);
         }
-        const float inv = 1.f / (t0f + (float)(r0 + i + 1));
-        const float msub = a.centered ? sCq[i] * inv : 0.f;
+        const float inv = 1.f / (DECAY ? sWt[i] : t0f + (float)(r0 + i + 1));
+        const float msub = a.centered ? (DECAY ? sEg[i] : 1.f) * sCq[i] * inv : 0.f;
         const float lam = sLam[i];
 #pragma unroll
         for (int nt = 0; nt < NNT; ++nt) {
@@ -557,6 +733,21 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
       // S'_{r+1} = S'_r + K'^T K' (not needed after the segment's last chunk);
       // transposed key reads two m tiles ahead of their products
       if (c + 1 < cend) {
+        if constexpr (DECAY) {
+          // S' decayed over the chunk; the keys of this wave's columns weighted
+          // e^{gamma_C - gamma_j} (k slot e of kb[nt][q] is token 32 q + 8 g + e)
+          const float eC = sEg[C - 1], gC = sGm[C - 1];
+#pragma unroll
+          for (int nt = 0; nt < NNT; ++nt) {
+#pragma unroll
+            for (int mt = 0; mt < NMT; ++mt) S[nt][mt] *= eC;
+#pragma unroll
+            for (int q = 0; q < 2; ++q)
+#pragma unroll
+              for (int e = 0; e < 8; ++e)
+                set_frag_elem(kb[nt][q], e, frag_elem(kb[nt][q], e) * __expf(gC - sGm[32 * q + 8 * g_ + e]));
+          }
+        }
         constexpr int G = 2, NG = NMT / G;
         Frag<T> ka[2][2 * G];
         auto load_group = [&](Frag<T>(&f)[2 * G], int g) {
@@ -603,19 +794,28 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
 }
 
 namespace {
+// The decay-aligned forms (a.la set) run forward only: no initial statistics,
+// no training outputs of the contraction (base, m . x).
 template <typename T, int DK>
 hipError_t run_gram(const CleanArgs& a, hipStream_t st) {
   const long long nblk = (long long)a.B * a.H * n_segs(a.T, a.seg);
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((clean_gram_kernel<T, DK>), dim3((unsigned)nblk), dim3(64 * (DK >= 128 ? 8 : 4)), 0,
-                     st, a);
+  if (a.la && !a.sdec) return hipErrorInvalidValue;
+  if (a.la)
+    hipLaunchKernelGGL((clean_gram_kernel<T, DK, true>), dim3((unsigned)nblk), dim3(64 * (DK >= 128 ? 8 : 4)),
+                       0, st, a);
+  else
+    hipLaunchKernelGGL((clean_gram_kernel<T, DK, false>), dim3((unsigned)nblk), dim3(64 * (DK >= 128 ? 8 : 4)),
+                       0, st, a);
   return hipGetLastError();
 }
 template <typename T, int DK>
 hipError_t run_prefix(const CleanArgs& a, hipStream_t st) {
   const long long nblk = (long long)a.B * a.H * (DK * DK / 1024);
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((clean_prefix_kernel<T, DK>), dim3((unsigned)nblk), dim3(256), 0, st, a);
+  if (a.la && (a.t0 != 0 || a.C0 || a.mu0 || !a.sdec)) return hipErrorInvalidValue;
+  if (a.la) hipLaunchKernelGGL((clean_prefix_kernel<T, DK, true>), dim3((unsigned)nblk), dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((clean_prefix_kernel<T, DK, false>), dim3((unsigned)nblk), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 template <typename T, int DK>
@@ -623,10 +823,18 @@ hipError_t run_out(const CleanArgs& a, hipStream_t st) {
   const long long nblk = (long long)a.B * a.H * n_segs(a.T, a.seg);
   if (nblk == 0) return hipSuccess;
   constexpr int NW = DK >= 128 ? 8 : 4;
-  if (a.base || a.corr || a.mdot || a.qclean_dbg)
-    hipLaunchKernelGGL((clean_out_kernel<T, DK, NW, true>), dim3((unsigned)nblk), dim3(64 * NW), 0, st, a);
-  else
-    hipLaunchKernelGGL((clean_out_kernel<T, DK, NW, false>), dim3((unsigned)nblk), dim3(64 * NW), 0, st, a);
+  const bool train = a.base || a.corr || a.mdot || a.qclean_dbg;
+  if (a.la) {
+    if (a.base || a.mdot || a.t0 != 0 || a.mu0 || !a.sdec) return hipErrorInvalidValue;
+    if (train)
+      hipLaunchKernelGGL((clean_out_kernel<T, DK, NW, true, true>), dim3((unsigned)nblk), dim3(64 * NW), 0, st, a);
+    else
+      hipLaunchKernelGGL((clean_out_kernel<T, DK, NW, false, true>), dim3((unsigned)nblk), dim3(64 * NW), 0, st, a);
+  } else if (train) {
+    hipLaunchKernelGGL((clean_out_kernel<T, DK, NW, true, false>), dim3((unsigned)nblk), dim3(64 * NW), 0, st, a);
+  } else {
+    hipLaunchKernelGGL((clean_out_kernel<T, DK, NW, false, false>), dim3((unsigned)nblk), dim3(64 * NW), 0, st, a);
+  }
   return hipGetLastError();
 }
 

@@ -52,6 +52,13 @@ struct CleanArgs {
   // by rq / rk [rows, H] fp32 (1 / max(|x|, eps)) as it is staged, or null
   const float* rq = nullptr;
   const float* rk = nullptr;
+  // decay-aligned statistics (Gated DeltaNet): the per-token log decays
+  // [rows, H] fp32, or null for the undecayed statistics of the paper; every
+  // sum above is then weighted by the decay from the key to the point it is
+  // taken at (the end of a chunk or segment) and token counts become the
+  // decayed counts
+  const float* la = nullptr;
+  float* sdec = nullptr;  // [B*H, NS, 2] workspace: each segment's weight sum and decay
 };
 
 // GLA state recurrence (sequential over chunks) for one 64-channel tile of S.

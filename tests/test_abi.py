@@ -246,3 +246,29 @@ def test_varlen_entry_point_validation():
     assert call_bwd(shape(), bb=1) == 1                     # Gated DeltaNet needs beta, dbeta
     assert call_bwd(shape(dk=256), bb=0) == 2                # no GLA training step at dk = 256
     assert call_bwd(shape(dk=256), bb=1) == 1                # Gated DeltaNet at dk = 256 needs beta
+
+
+def test_decay_aligned_validation():
+    """ccq_shape.decay_aligned: Gated DeltaNet forward only, from empty statistics; every
+    other use is refused before any launch.  The field sits in the padding before t0, so
+    the struct keeps its size and t0 its offset."""
+    assert ctypes.sizeof(ccq.Shape) == 56 and ccq.Shape.t0.offset == 48
+    P = ctypes.c_void_p
+
+    def call_gdn(s, C0=None):
+        return ccq.lib().ccq_gdn_fwd(ctypes.byref(s), P(FAKE), P(FAKE), P(FAKE), P(FAKE),
+                                     P(FAKE), P(FAKE), None, None if C0 is None else P(C0), None,
+                                     P(FAKE), None, None, None, None, P(FAKE), 1 << 34, None)
+
+    d = dict(dk=256, decay_aligned=True)
+    assert call_gla(shape(decay_aligned=True)) == 2         # GLA: per-channel decay
+    s = shape(**d)
+    s.decay_aligned = 3
+    assert call_gdn(s) == 1
+    assert call_gdn(shape(t0=7, **d)) == 2                  # no cached decayed count
+    assert call_gdn(shape(**d), C0=FAKE) == 2
+    assert call_bwd(shape(**d), bb=1) == 2                  # forward only
+    assert call_decode(shape(T=1, **d), bb=1, beta=FAKE) == 2
+    # the flag does not change the workspace
+    assert ccq.ccq_workspace_size(shape(**d), ccq.CCQ_GDN) == ccq.ccq_workspace_size(
+        shape(dk=256), ccq.CCQ_GDN)
