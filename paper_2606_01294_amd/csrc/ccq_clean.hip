@@ -329,7 +329,9 @@ __device__ __forceinline__ int causal_tile_i(int t) { return t >= 6 ? 3 : t >= 3
 //   M'_{r+1} = e^{gamma_C} M'_r + (the chunk's weighted key sum about c_s).
 template <typename T, int DK, int NW, bool TRAIN, bool DECAY>
 __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a) {
-  constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P, LDP = C + P, LDQ = C + 4;
+  // 16-byte row padding here (the other kernels use 32 bytes): at dk = 256 the
+  // 32-byte form would not fit beside the staging area in the 160 KB of LDS
+  constexpr int C = kChunk, P = 16 / (int)sizeof(T), LDK = DK + P, LDP = C + P, LDQ = C + 4;
   constexpr int NT = 64 * NW, VPR = DK / 8;
   constexpr int NCW = DK / NW, NNT = NCW / 16, NMT = DK / 16, NK = DK / 32;
   constexpr int TPI = NT / C, JPT = C / TPI, FPT = DK / TPI;  // per-token split of the row sums

@@ -32,7 +32,7 @@ __device__ __forceinline__ int intra_tile_row(int t) { return (int)((0x940ffa94u
 __device__ __forceinline__ int intra_tile_col(int t) { return (int)((0xfb9e4910ull >> (2 * t)) & 3); }
 
 template <typename T>
-struct Pad { static constexpr int value = 16 / (int)sizeof(T); };  // 16-byte row padding
+struct Pad { static constexpr int value = 32 / (int)sizeof(T); };  // 32-byte row padding
 
 template <typename T> struct Frag;
 template <> struct Frag<bf16_t> { bf16x8 v; };
