@@ -412,7 +412,13 @@ __device__ __forceinline__ void wait_vm_n(int n) {
   }
 }
 
-template <int DK, int NPR, int NH, int NSTAGE>
+// RS (reduce-scatter exchange): instead of every wave of a value tile reading
+// all NH x 4 partial products and forming all of R, wave hq sums the partials
+// of its own 4 / NH token tiles (the same fixed order), forms those tiles of R
+// from its own rows of V and of the coefficients, and writes them as bf16 in
+// the layout of the operand fragments of U = Tm R; after a second barrier every
+// wave reads the two fragments.  R enters the product as bf16 either way.
+template <int DK, int NPR, int NH, int NSTAGE, bool RS = false>
 __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const GdnArgs a) {
   typedef bf16_t T;
   typedef __attribute__((address_space(3))) void lds_void;
@@ -425,14 +431,17 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
   constexpr int NIW = NIK / NW + NIT / NW + NIVW + 1;         // 1 KB pieces per wave and chunk
   constexpr int SB = KB + TB + VB + FB;
   constexpr int XB = NH > 1 ? NW * 4 * 64 * 16 : 16;
+  constexpr int XR = RS ? NPR * 2 * 64 * 16 : 0;              // RS: bf16 R fragments
   constexpr int NSU = NH == 1 ? 2 : 1;                         // U^T stores per wave per chunk
   static_assert(DK == 128 || DK == 256, "key width");
   static_assert(NH == 1 || NH == 2 || NH == 4, "key split");
   static_assert(NSTAGE == 2 || NSTAGE == 3, "ring depth");
   static_assert(NKH >= 1 && VB % 1024 == 0, "tiles");
-  __shared__ __align__(1024) char smem[NSTAGE * SB + XB + 1024];
+  static_assert(!RS || NH > 1, "the reduce-scatter exchange splits the keys");
+  __shared__ __align__(1024) char smem[NSTAGE * SB + XB + 1024 + XR];
   f32x4* const sX = reinterpret_cast<f32x4*>(smem + NSTAGE * SB);
   char* const sDummy = smem + NSTAGE * SB + XB;
+  T* const sR = reinterpret_cast<T*>(smem + NSTAGE * SB + XB + 1024);
 
   const int nvt = a.dv / BVS;
   const int N = (a.T + C - 1) / C;
@@ -551,16 +560,25 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
       f.v = *reinterpret_cast<const bf16x8*>(row + 16 * (p0 ^ ks));
       return f;
     };
-    // the V slice, transposed (issued now, waited for where used)
+    // the V slice, transposed (issued now, waited for where used); RS: the
+    // rows of this wave's token tiles only (tile J is rows 16 J + 4 g4 + r)
+    constexpr int JPW = RS ? 4 / NH : 4;
+    const int J0 = RS ? hq * JPW : 0;
     Frag<T> vf[2];
+    bf16x4 vw[RS ? JPW : 1];
     {
       const int j = c16;
       const char* pv = reinterpret_cast<const char*>(Vb) + (4 * g4 + (j >> 2)) * (2 * BVS) + 32 * pr + 8 * (j & 3);
+      if constexpr (RS) {
 #pragma unroll
-      for (int m = 0; m < 2; ++m) {
-        const bf16x4 lo = ds_read_tr16_asm(pv + 32 * m * 2 * BVS);
-        const bf16x4 hi = ds_read_tr16_asm(pv + (32 * m + 16) * 2 * BVS);
-        vf[m].v = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        for (int jj = 0; jj < JPW; ++jj) vw[jj] = ds_read_tr16_asm(pv + 16 * (J0 + jj) * 2 * BVS);
+      } else {
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+          const bf16x4 lo = ds_read_tr16_asm(pv + 32 * m * 2 * BVS);
+          const bf16x4 hi = ds_read_tr16_asm(pv + (32 * m + 16) * 2 * BVS);
+          vf[m].v = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        }
       }
     }
     f32x4 R[4];
@@ -583,13 +601,14 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
     // coefficients and Tm rows, read now so that their latency overlaps the
     // exchange
     Frag<T> tfr[4][2];
-    f32x4 bg[4], bj[4], dd[4];
+    f32x4 bg[JPW], bj[JPW], dd[4];  // bg, bj: the token tiles this wave forms R for
 #pragma unroll
-    for (int J = 0; J < 4; ++J) {
-      bg[J] = *reinterpret_cast<const f32x4*>(Fb + 16 * J + 4 * g4);
-      bj[J] = *reinterpret_cast<const f32x4*>(Fb + C + 16 * J + 4 * g4);
-      dd[J] = *reinterpret_cast<const f32x4*>(Fb + 2 * C + 16 * J + 4 * g4);
+    for (int jj = 0; jj < JPW; ++jj) {
+      bg[jj] = *reinterpret_cast<const f32x4*>(Fb + 16 * (J0 + jj) + 4 * g4);
+      bj[jj] = *reinterpret_cast<const f32x4*>(Fb + C + 16 * (J0 + jj) + 4 * g4);
     }
+#pragma unroll
+    for (int J = 0; J < 4; ++J) dd[J] = *reinterpret_cast<const f32x4*>(Fb + 2 * C + 16 * J + 4 * g4);
     const float eC = Fb[3 * C];
     {
       const int ts = tswz(c16);
@@ -600,7 +619,31 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
           tfr[I][q].v = *reinterpret_cast<const bf16x8*>(reinterpret_cast<const char*>(Tb) + (16 * I + c16) * 128 +
                                                          16 * ((4 * q + g4) ^ ts));
     }
-    if constexpr (NH > 1) {
+    Frag<T> rf0, rf1;  // R as the bf16 operand of U = Tm R (tiles 0, 1 and 2, 3)
+    if constexpr (RS) {
+      // this wave's token tiles: the NH partials summed in the fixed order,
+      // R = beta V - beta e^gamma P, written as bf16 where fragment J / 2 of the
+      // slice keeps tile J in its lane's elements 4 (J % 2) .. + 3
+#pragma unroll
+      for (int J = 0; J < 4; ++J) sX[(w * 4 + J) * 64 + l] = R[J];
+      lds_barrier();  // (also completes this wave's V and coefficient reads)
+#pragma unroll
+      for (int jj = 0; jj < JPW; ++jj) asm volatile("" : "+v"(vw[jj]));
+#pragma unroll
+      for (int jj = 0; jj < JPW; ++jj) {
+        const int J = J0 + jj;
+        f32x4 sum = sX[((pr * NH) * 4 + J) * 64 + l];
+#pragma unroll
+        for (int hh = 1; hh < NH; ++hh) sum += sX[((pr * NH + hh) * 4 + J) * 64 + l];
+        bf16x4 y;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) y[r] = static_cast<bf16_t>(bj[jj][r] * f32(vw[jj][r]) - bg[jj][r] * sum[r]);
+        *reinterpret_cast<bf16x4*>(sR + ((pr * 2 + (J >> 1)) * 64 + l) * 8 + 4 * (J & 1)) = y;
+      }
+      lds_barrier();
+      rf0.v = *reinterpret_cast<const bf16x8*>(sR + ((pr * 2) * 64 + l) * 8);
+      rf1.v = *reinterpret_cast<const bf16x8*>(sR + ((pr * 2 + 1) * 64 + l) * 8);
+    } else if constexpr (NH > 1) {
       // sum the NH partial products of this value slice, in a fixed order so
       // every wave of the slice holds bit-identical P
 #pragma unroll
@@ -637,19 +680,21 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
           tf[t][kq].v = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         }
     }
-    lds_wait_but<(4 * NCT < 15 ? 4 * NCT : 15)>(vf);  // at most 15 LDS reads stay in flight
-    // R = beta V - beta e^gamma P
+    if constexpr (!RS) {
+      lds_wait_but<(4 * NCT < 15 ? 4 * NCT : 15)>(vf);  // at most 15 LDS reads stay in flight
+      // R = beta V - beta e^gamma P
 #pragma unroll
-    for (int m = 0; m < 2; ++m)
+      for (int m = 0; m < 2; ++m)
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int J = 2 * m + hh;
+        for (int hh = 0; hh < 2; ++hh) {
+          const int J = 2 * m + hh;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) R[J][r] = bj[J][r] * frag_elem(vf[m], 4 * hh + r) - bg[J][r] * R[J][r];
-      }
+          for (int r = 0; r < 4; ++r) R[J][r] = bj[J][r] * frag_elem(vf[m], 4 * hh + r) - bg[J][r] * R[J][r];
+        }
+      rf0 = acc_pair_frag<T>(R[0], R[1]);
+      rf1 = acc_pair_frag<T>(R[2], R[3]);
+    }
     // U = Tm R (Tm rows are stored in acc_pos order)
-    const Frag<T> rf0 = acc_pair_frag<T>(R[0], R[1]);
-    const Frag<T> rf1 = acc_pair_frag<T>(R[2], R[3]);
     f32x4 U[4];
 #pragma unroll
     for (int I = 0; I < 4; ++I) {
@@ -914,17 +959,20 @@ hipError_t run_gdn_state_v(const GdnArgs& a, hipStream_t st) {
 // features each) as it takes to give every SIMD of the chip a wave, with four
 // waves per workgroup where the split allows.
 // LDS of the streamed kernel with a ring of `ns` stages
-constexpr size_t gdn_dma_lds(int dk, int npr, int nh, int ns) {
+constexpr size_t gdn_dma_lds(int dk, int npr, int nh, int ns, bool rs) {
   return (size_t)ns * (kChunk * dk * 2 + kChunk * kChunk * 2 + kChunk * 16 * npr * 2 + 4 * kChunk * 4) +
-         (nh > 1 ? (size_t)npr * nh * 4 * 64 * 16 : 16) + 1024;
+         (nh > 1 ? (size_t)npr * nh * 4 * 64 * 16 : 16) + 1024 + (rs ? (size_t)npr * 2 * 64 * 16 : 0);
 }
-template <int DK, int NPR, int NH>
+// With a key split the exchange is the reduce-scatter form: bit-identical, and
+// measured on the 1.3B shape 380 -> 362 us per forward call at T = 4096 and
+// 915 -> 865 us at T = 20480.
+template <int DK, int NPR, int NH, bool RS = (NH > 1)>
 hipError_t run_gdn_state_dma(const GdnArgs& a, hipStream_t st) {
   const int nblk = a.B * a.H * (a.dv / (16 * NPR));
   if (nblk == 0) return hipSuccess;
   // three stages where they fit in the compute unit's 160 KB of LDS
-  constexpr int NS = gdn_dma_lds(DK, NPR, NH, 3) <= 160 * 1024 ? 3 : 2;
-  hipLaunchKernelGGL((gdn_state_dma_kernel<DK, NPR, NH, NS>), dim3(nblk), dim3(64 * NPR * NH), 0, st, a);
+  constexpr int NS = gdn_dma_lds(DK, NPR, NH, 3, RS) <= 160 * 1024 ? 3 : 2;
+  hipLaunchKernelGGL((gdn_state_dma_kernel<DK, NPR, NH, NS, RS>), dim3(nblk), dim3(64 * NPR * NH), 0, st, a);
   return hipGetLastError();
 }
 template <typename T, int DK>
