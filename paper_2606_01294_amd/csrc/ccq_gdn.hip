@@ -418,7 +418,10 @@ __device__ __forceinline__ void wait_vm_n(int n) {
 // from its own rows of V and of the coefficients, and writes them as bf16 in
 // the layout of the operand fragments of U = Tm R; after a second barrier every
 // wave reads the two fragments.  R enters the product as bf16 either way.
-template <int DK, int NPR, int NH, int NSTAGE, bool RS = false>
+// RSU (with RS): U = Tm R is split the same way: wave hq forms only the rows
+// of its own token tiles, stores them as its part of U^T, and shares them,
+// times e^{gamma_C - gamma}, as bf16 operand fragments for the state update.
+template <int DK, int NPR, int NH, int NSTAGE, bool RS = false, bool RSU = false>
 __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const GdnArgs a) {
   typedef bf16_t T;
   typedef __attribute__((address_space(3))) void lds_void;
@@ -431,17 +434,19 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
   constexpr int NIW = NIK / NW + NIT / NW + NIVW + 1;         // 1 KB pieces per wave and chunk
   constexpr int SB = KB + TB + VB + FB;
   constexpr int XB = NH > 1 ? NW * 4 * 64 * 16 : 16;
-  constexpr int XR = RS ? NPR * 2 * 64 * 16 : 0;              // RS: bf16 R fragments
+  constexpr int XR = (RS ? NPR * 2 * 64 * 16 : 0) * (RSU ? 2 : 1);  // bf16 R (RSU: and U) fragments
   constexpr int NSU = NH == 1 ? 2 : 1;                         // U^T stores per wave per chunk
   static_assert(DK == 128 || DK == 256, "key width");
   static_assert(NH == 1 || NH == 2 || NH == 4, "key split");
   static_assert(NSTAGE == 2 || NSTAGE == 3, "ring depth");
   static_assert(NKH >= 1 && VB % 1024 == 0, "tiles");
   static_assert(!RS || NH > 1, "the reduce-scatter exchange splits the keys");
+  static_assert(!RSU || RS, "the split U builds on the split R");
   __shared__ __align__(1024) char smem[NSTAGE * SB + XB + 1024 + XR];
   f32x4* const sX = reinterpret_cast<f32x4*>(smem + NSTAGE * SB);
   char* const sDummy = smem + NSTAGE * SB + XB;
   T* const sR = reinterpret_cast<T*>(smem + NSTAGE * SB + XB + 1024);
+  T* const sU = sR + NPR * 2 * 64 * 8;  // RSU: fragments of U diag(e^{gamma_C - gamma})
 
   const int nvt = a.dv / BVS;
   const int N = (a.T + C - 1) / C;
@@ -600,24 +605,26 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
     }
     // coefficients and Tm rows, read now so that their latency overlaps the
     // exchange
-    Frag<T> tfr[4][2];
-    f32x4 bg[JPW], bj[JPW], dd[4];  // bg, bj: the token tiles this wave forms R for
+    constexpr int IPW = RSU ? JPW : 4;  // the token tiles of U this wave forms
+    const int I0 = RSU ? J0 : 0;
+    Frag<T> tfr[IPW][2];
+    f32x4 bg[JPW], bj[JPW], dd[IPW];  // bg, bj: the token tiles this wave forms R for
 #pragma unroll
     for (int jj = 0; jj < JPW; ++jj) {
       bg[jj] = *reinterpret_cast<const f32x4*>(Fb + 16 * (J0 + jj) + 4 * g4);
       bj[jj] = *reinterpret_cast<const f32x4*>(Fb + C + 16 * (J0 + jj) + 4 * g4);
     }
 #pragma unroll
-    for (int J = 0; J < 4; ++J) dd[J] = *reinterpret_cast<const f32x4*>(Fb + 2 * C + 16 * J + 4 * g4);
+    for (int ii = 0; ii < IPW; ++ii) dd[ii] = *reinterpret_cast<const f32x4*>(Fb + 2 * C + 16 * (I0 + ii) + 4 * g4);
     const float eC = Fb[3 * C];
     {
       const int ts = tswz(c16);
 #pragma unroll
-      for (int I = 0; I < 4; ++I)
+      for (int ii = 0; ii < IPW; ++ii)
 #pragma unroll
         for (int q = 0; q < 2; ++q)
-          tfr[I][q].v = *reinterpret_cast<const bf16x8*>(reinterpret_cast<const char*>(Tb) + (16 * I + c16) * 128 +
-                                                         16 * ((4 * q + g4) ^ ts));
+          tfr[ii][q].v = *reinterpret_cast<const bf16x8*>(reinterpret_cast<const char*>(Tb) +
+                                                          (16 * (I0 + ii) + c16) * 128 + 16 * ((4 * q + g4) ^ ts));
     }
     Frag<T> rf0, rf1;  // R as the bf16 operand of U = Tm R (tiles 0, 1 and 2, 3)
     if constexpr (RS) {
@@ -695,20 +702,39 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
       rf1 = acc_pair_frag<T>(R[2], R[3]);
     }
     // U = Tm R (Tm rows are stored in acc_pos order)
-    f32x4 U[4];
+    f32x4 U[IPW];
 #pragma unroll
-    for (int I = 0; I < 4; ++I) {
-      U[I] = zero4();
-      mma(U[I], tfr[I][0], rf0);
-      mma(U[I], tfr[I][1], rf1);
+    for (int ii = 0; ii < IPW; ++ii) {
+      U[ii] = zero4();
+      mma(U[ii], tfr[ii][0], rf0);
+      mma(U[ii], tfr[ii][1], rf1);
     }
-    Frag<T> uf[2];
-    uf[0] = acc_pair_frag<T>(U[0], U[1]);
-    uf[1] = acc_pair_frag<T>(U[2], U[3]);
+    Frag<T> uf[2], ud0, ud1;
+    bf16x4 uw[IPW];  // RSU: this wave's tiles of U as bf16, its part of U^T
+    if constexpr (RSU) {
+      // tile I lives in elements 4 (I % 2) .. + 3 of fragment I / 2
 #pragma unroll
-    for (int I = 0; I < 4; ++I) U[I] *= dd[I];
-    const Frag<T> ud0 = acc_pair_frag<T>(U[0], U[1]);
-    const Frag<T> ud1 = acc_pair_frag<T>(U[2], U[3]);
+      for (int ii = 0; ii < IPW; ++ii) {
+        const int I = I0 + ii;
+        bf16x4 y;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          uw[ii][r] = static_cast<bf16_t>(U[ii][r]);
+          y[r] = static_cast<bf16_t>(U[ii][r] * dd[ii][r]);
+        }
+        *reinterpret_cast<bf16x4*>(sU + ((pr * 2 + (I >> 1)) * 64 + l) * 8 + 4 * (I & 1)) = y;
+      }
+      lds_barrier();
+      ud0.v = *reinterpret_cast<const bf16x8*>(sU + ((pr * 2) * 64 + l) * 8);
+      ud1.v = *reinterpret_cast<const bf16x8*>(sU + ((pr * 2 + 1) * 64 + l) * 8);
+    } else {
+      uf[0] = acc_pair_frag<T>(U[0], U[1]);
+      uf[1] = acc_pair_frag<T>(U[2], U[3]);
+#pragma unroll
+      for (int I = 0; I < 4; ++I) U[I] *= dd[I];
+      ud0 = acc_pair_frag<T>(U[0], U[1]);
+      ud1 = acc_pair_frag<T>(U[2], U[3]);
+    }
     // S^T <- e^{gamma_C} S^T + K^T diag(e^{gamma_C - gamma}) U
 #pragma unroll
     for (int t = 1; t < NCT; ++t) lds_wait(tf[t]);
@@ -725,7 +751,13 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
 #pragma unroll
         for (int m = 0; m < NKH; ++m) store_frag(st_out + 16 * 32 * m, sf[m]);
       T* u_out = u_base + ((size_t)bh * N + ci) * a.dv * C;
-      if constexpr (NH == 1) {
+      if constexpr (RSU && IPW == 2) {
+        // two waves: fragment hq whole
+        *reinterpret_cast<bf16x8*>(u_out + 16 * 32 * hq) =
+            bf16x8{uw[0][0], uw[0][1], uw[0][2], uw[0][3], uw[1][0], uw[1][1], uw[1][2], uw[1][3]};
+      } else if constexpr (RSU) {
+        *reinterpret_cast<bf16x4*>(u_out + 16 * 32 * (I0 >> 1) + 4 * (I0 & 1)) = uw[0];
+      } else if constexpr (NH == 1) {
         store_frag(u_out, uf[0]);
         store_frag(u_out + 16 * 32, uf[1]);
       } else if constexpr (NH == 2) {
@@ -959,20 +991,21 @@ hipError_t run_gdn_state_v(const GdnArgs& a, hipStream_t st) {
 // features each) as it takes to give every SIMD of the chip a wave, with four
 // waves per workgroup where the split allows.
 // LDS of the streamed kernel with a ring of `ns` stages
-constexpr size_t gdn_dma_lds(int dk, int npr, int nh, int ns, bool rs) {
+constexpr size_t gdn_dma_lds(int dk, int npr, int nh, int ns, bool rs, bool rsu) {
   return (size_t)ns * (kChunk * dk * 2 + kChunk * kChunk * 2 + kChunk * 16 * npr * 2 + 4 * kChunk * 4) +
-         (nh > 1 ? (size_t)npr * nh * 4 * 64 * 16 : 16) + 1024 + (rs ? (size_t)npr * 2 * 64 * 16 : 0);
+         (nh > 1 ? (size_t)npr * nh * 4 * 64 * 16 : 16) + 1024 +
+         (rs ? (size_t)npr * 2 * 64 * 16 * (rsu ? 2 : 1) : 0);
 }
 // With a key split the exchange is the reduce-scatter form: bit-identical, and
 // measured on the 1.3B shape 380 -> 362 us per forward call at T = 4096 and
 // 915 -> 865 us at T = 20480.
-template <int DK, int NPR, int NH, bool RS = (NH > 1)>
+template <int DK, int NPR, int NH, bool RS = (NH > 1), bool RSU = (NH > 1)>
 hipError_t run_gdn_state_dma(const GdnArgs& a, hipStream_t st) {
   const int nblk = a.B * a.H * (a.dv / (16 * NPR));
   if (nblk == 0) return hipSuccess;
   // three stages where they fit in the compute unit's 160 KB of LDS
-  constexpr int NS = gdn_dma_lds(DK, NPR, NH, 3, RS) <= 160 * 1024 ? 3 : 2;
-  hipLaunchKernelGGL((gdn_state_dma_kernel<DK, NPR, NH, NS, RS>), dim3(nblk), dim3(64 * NPR * NH), 0, st, a);
+  constexpr int NS = gdn_dma_lds(DK, NPR, NH, 3, RS, RSU) <= 160 * 1024 ? 3 : 2;
+  hipLaunchKernelGGL((gdn_state_dma_kernel<DK, NPR, NH, NS, RS, RSU>), dim3(nblk), dim3(64 * NPR * NH), 0, st, a);
   return hipGetLastError();
 }
 template <typename T, int DK>

@@ -35,8 +35,8 @@ def expected(DK, NPR, NH):
     return NIW + alt, NKH + NSU
 
 
-# the instantiations the library launches (template <DK, NPR, NH, NSTAGE, RS>)
-INSTANCES = [(256, 2, 4, 2, 1), (256, 1, 4, 3, 1), (128, 4, 2, 3, 1), (128, 2, 4, 3, 1)]
+# the instantiations the library launches (template <DK, NPR, NH, NSTAGE, RS, RSU>)
+INSTANCES = [(256, 2, 4, 2, 1, 1), (256, 1, 4, 3, 1, 1), (128, 4, 2, 3, 1, 1), (128, 2, 4, 3, 1, 1)]
 
 
 @pytest.fixture(scope="module")
@@ -64,10 +64,10 @@ def chunk_loop(asm, sym):
     return [line.split(";")[0].strip() for line in body[head[0]:max(back) + 1]]
 
 
-@pytest.mark.parametrize("inst", INSTANCES, ids=lambda t: "dk%d-npr%d-nh%d-ns%d-rs%d" % t)
+@pytest.mark.parametrize("inst", INSTANCES, ids=lambda t: "dk%d-npr%d-nh%d-ns%d-rs%d-rsu%d" % t)
 def test_state_pass_loop_issues_the_counted_vector_memory_ops(gdn_asm, inst):
-    DK, NPR, NH, NS, RS = inst
-    sym = "_ZN3ccq20gdn_state_dma_kernelILi%dELi%dELi%dELi%dELb%dEEEvNS_7GdnArgsE" % inst
+    DK, NPR, NH, NS, RS, RSU = inst
+    sym = "_ZN3ccq20gdn_state_dma_kernelILi%dELi%dELi%dELi%dELb%dELb%dEEEvNS_7GdnArgsE" % inst
     assert ("\n" + sym + ":") in gdn_asm, "instantiation %s not emitted" % sym
     loop = chunk_loop(gdn_asm, sym)
     mnem = [line.split()[0] for line in loop if line and not line.startswith((".", ";"))]
