@@ -329,15 +329,19 @@ __device__ __forceinline__ int causal_tile_i(int t) { return t >= 6 ? 3 : t >= 3
 //   M'_{r+1} = e^{gamma_C} M'_r + (the chunk's weighted key sum about c_s).
 template <typename T, int DK, int NW, bool TRAIN, bool DECAY>
 __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a) {
-  // 16-byte row padding here (the other kernels use 32 bytes): at dk = 256 the
-  // 32-byte form would not fit beside the staging area in the 160 KB of LDS
-  constexpr int C = kChunk, P = 16 / (int)sizeof(T), LDK = DK + P, LDP = C + P, LDQ = C + 4;
+  // the shifted scores overwrite the raw ones in place (row i of both is
+  // written and read only by the threads of token i, one wave, whose LDS
+  // accesses complete in order), which leaves room at dk = 256 for the 32-byte
+  // row padding; a row of raw scores is 288 bytes, so the shifted scores'
+  // fragment reads see the same conflict-free 32 mod 256 pitch
+  constexpr int C = kChunk, P = Pad<T>::value, LDK = DK + P, LDQ = C + 8;
+  constexpr int LDP = LDQ * 4 / (int)sizeof(T);
   constexpr int NT = 64 * NW, VPR = DK / 8;
   constexpr int NCW = DK / NW, NNT = NCW / 16, NMT = DK / 16, NK = DK / 32;
   constexpr int TPI = NT / C, JPT = C / TPI, FPT = DK / TPI;  // per-token split of the row sums
   constexpr int NV = C * VPR / NT;                            // staged vectors per thread
   static_assert(NCW % 16 == 0 && NNT >= 1, "column split");
-  static_assert(NT >= DK && JPT % 8 == 0 && FPT % 8 == 0 && C * VPR % NT == 0, "thread split");
+  static_assert(NT >= DK && JPT % 8 == 0 && FPT % 8 == 0 && C * VPR % NT == 0 && NT % VPR == 0, "thread split");
   typedef RowTile<T, DK, NT> Tile;
   typedef typename Tile::vec_t vec_t;
   // bf16 chunks are prefetched straight into LDS (x then k, unpadded); fp32
@@ -346,7 +350,7 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
   // instructions' immediate field.
   constexpr bool kDma = sizeof(T) == 2;
   constexpr int oX = 0, oK = oX + C * LDK * (int)sizeof(T), oS = oK + C * LDK * (int)sizeof(T);
-  constexpr int oP = oS + C * LDQ * 4, oC = oP + C * LDP * (int)sizeof(T), oM = oC + DK * 4;
+  constexpr int oC = oS + C * LDQ * 4, oM = oC + DK * 4;
   constexpr int oCq = oM + DK * 4, oLam = oCq + C * 4, oDec = oLam + C * 4;
   constexpr int oSt = oDec + (DECAY ? (3 * C + 4) * 4 : 0);
   constexpr int oEnd = oSt + (kDma ? 2 * C * DK * (int)sizeof(T) : 16);
@@ -354,7 +358,7 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
   T* const sX = reinterpret_cast<T*>(smem + oX);         // x rows, then q_clean rows
   T* const sK = reinterpret_cast<T*>(smem + oK);         // centred keys
   float* const sS = reinterpret_cast<float*>(smem + oS); // raw scores, [i][j]
-  T* const sP = reinterpret_cast<T*>(smem + oP);         // masked, shifted scores, [i][j]
+  T* const sP = reinterpret_cast<T*>(smem + oS);         // masked, shifted scores, [i][j], over sS
   float* const sC = reinterpret_cast<float*>(smem + oC);
   float* const sM = reinterpret_cast<float*>(smem + oM);
   float* const sCq = reinterpret_cast<float*>(smem + oCq);
@@ -495,42 +499,58 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
       csum = a.csum[((size_t)bh * NC + c) * DK + tid];
     }
     // stage chunk c; each thread first copies out the q_clean of chunk c - 1
-    // (always a full chunk) held at the same places.  The streamed chunk is
-    // read before any store is issued, so that no wait on it can cover a store.
+    // (always a full chunk) held at the same places.  The outgoing rows and the
+    // centre are read together and stored before the streamed chunk is read
+    // (two LDS round trips per chunk, few registers); a register-prefetched
+    // chunk is taken first instead, so that its wait covers no store.
     {
       const int t_ = opaque(tid);
+      const int col = (t_ % VPR) * 8;  // the same for every vector of a thread
       vec_t xv[NV], kv[NV];
+      auto take = [&]() {
 #pragma unroll
-      for (int u = 0; u < NV; ++u) {
-        if constexpr (kDma) {
-          xv[u] = *reinterpret_cast<const vec_t*>(sSt + 8 * (t_ + NT * u));
-          kv[u] = *reinterpret_cast<const vec_t*>(sSt + C * DK + 8 * (t_ + NT * u));
-        } else {
-          xv[u] = rx.get(u);
-          kv[u] = rk.get(u);
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < NV; ++u) {
-        const int e = t_ + NT * u, row = e / VPR, col = (e % VPR) * 8;
-        T* px = sX + row * LDK + col;
-        if (c > cbeg)
-          *reinterpret_cast<vec_t*>(qc + seq_off(sw, r0 - C + row, h, a.H, DK) + col) =
-              *reinterpret_cast<const vec_t*>(px);
-        vec_t y;
-        if (a.rq) {
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            xv[u][q] = to<T>(f32(xv[u][q]) * fq[u]);
-            kv[u][q] = to<T>(f32(kv[u][q]) * fk[u]);
+        for (int u = 0; u < NV; ++u) {
+          if constexpr (kDma) {
+            xv[u] = *reinterpret_cast<const vec_t*>(sSt + 8 * (t_ + NT * u));
+            kv[u] = *reinterpret_cast<const vec_t*>(sSt + C * DK + 8 * (t_ + NT * u));
+          } else {
+            xv[u] = rx.get(u);
+            kv[u] = rk.get(u);
           }
         }
+        if (a.rq)
+#pragma unroll
+          for (int u = 0; u < NV; ++u)
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              xv[u][q] = to<T>(f32(xv[u][q]) * fq[u]);
+              kv[u][q] = to<T>(f32(kv[u][q]) * fk[u]);
+            }
+      };
+      if constexpr (!kDma) take();
+      const f32x4 ca = *reinterpret_cast<const f32x4*>(sC + col);
+      const f32x4 cb = *reinterpret_cast<const f32x4*>(sC + col + 4);
+      if (c > cbeg) {
+        vec_t qo[NV];
+#pragma unroll
+        for (int u = 0; u < NV; ++u) qo[u] = *reinterpret_cast<const vec_t*>(sX + ((t_ + NT * u) / VPR) * LDK + col);
+#pragma unroll
+        for (int u = 0; u < NV; ++u)
+          *reinterpret_cast<vec_t*>(qc + seq_off(sw, r0 - C + (t_ + NT * u) / VPR, h, a.H, DK) + col) = qo[u];
+      }
+      if constexpr (kDma) take();
+#pragma unroll
+      for (int u = 0; u < NV; ++u) {
+        const int row = (t_ + NT * u) / VPR;
+        const bool live = row < nrow;
+        const float keep = live ? 1.f : 0.f;  // (a product, not a select: no branch per element)
+        vec_t y;
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-          xv[u][q] = row < nrow ? xv[u][q] : to<T>(0.f);
-          y[q] = to<T>(row < nrow ? f32(kv[u][q]) - sC[col + q] : 0.f);
+          xv[u][q] = live ? xv[u][q] : to<T>(0.f);
+          y[q] = to<T>((f32(kv[u][q]) - (q < 4 ? ca[q] : cb[q - 4])) * keep);
         }
-        *reinterpret_cast<vec_t*>(px) = xv[u];
+        *reinterpret_cast<vec_t*>(sX + row * LDK + col) = xv[u];
         *reinterpret_cast<vec_t*>(sK + row * LDK + col) = y;
       }
     }
@@ -635,6 +655,8 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
       }
       const float cqp = mq + rs;
       const float sub = a.centered ? cqp / ti : 0.f;
+      // the shifted row goes over the raw one: keep these stores after the reads
+      asm volatile("" ::: "memory");
       T* prow = sP + i * LDP + JPT * pp;
 #pragma unroll
       for (int e = 0; e < JPT; e += 8) {
