@@ -40,6 +40,8 @@
 // above holds for the weighted covariance too (with W in place of t), so the
 // segment centring is unchanged; c_s is the segment's weighted mean.  Every
 // factor is at most 1.
+#include <type_traits>
+
 #include "ccq_device.h"
 #include "ccq_kernels.h"
 
@@ -539,20 +541,30 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
           *reinterpret_cast<vec_t*>(qc + seq_off(sw, r0 - C + (t_ + NT * u) / VPR, h, a.H, DK) + col) = qo[u];
       }
       if constexpr (kDma) take();
+      auto put = [&](auto masked) {
 #pragma unroll
-      for (int u = 0; u < NV; ++u) {
-        const int row = (t_ + NT * u) / VPR;
-        const bool live = row < nrow;
-        const float keep = live ? 1.f : 0.f;  // (a product, not a select: no branch per element)
-        vec_t y;
+        for (int u = 0; u < NV; ++u) {
+          const int row = (t_ + NT * u) / VPR;
+          const bool live = row < nrow;
+          const float keep = live ? 1.f : 0.f;  // (a product, not a select: no branch per element)
+          vec_t y;
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          xv[u][q] = live ? xv[u][q] : to<T>(0.f);
-          y[q] = to<T>((f32(kv[u][q]) - (q < 4 ? ca[q] : cb[q - 4])) * keep);
+          for (int q = 0; q < 8; ++q) {
+            const float d = f32(kv[u][q]) - (q < 4 ? ca[q] : cb[q - 4]);
+            if constexpr (decltype(masked)::value) {
+              xv[u][q] = live ? xv[u][q] : to<T>(0.f);
+              y[q] = to<T>(d * keep);
+            } else {
+              y[q] = to<T>(d);
+            }
+          }
+          *reinterpret_cast<vec_t*>(sX + row * LDK + col) = xv[u];
+          *reinterpret_cast<vec_t*>(sK + row * LDK + col) = y;
         }
-        *reinterpret_cast<vec_t*>(sX + row * LDK + col) = xv[u];
-        *reinterpret_cast<vec_t*>(sK + row * LDK + col) = y;
-      }
+      };
+      // rows past the end exist only in a sequence's last chunk
+      if (nrow == C) put(std::false_type{});
+      else put(std::true_type{});
     }
     lds_barrier();  // (1) x, K', M'_c staged; the staging area is free
     if (c + 1 < cend) prefetch(c + 1);
@@ -734,16 +746,17 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
         }
         const float inv = 1.f / (DECAY ? sWt[i] : t0f + (float)(r0 + i + 1));
         const float msub = a.centered ? (DECAY ? sEg[i] : 1.f) * sCq[i] * inv : 0.f;
-        const float lam = sLam[i];
+        const float lam = sLam[i], li = lam * inv, lm = li * msub;
 #pragma unroll
         for (int nt = 0; nt < NNT; ++nt) {
           const int n = n0 + 16 * nt + 4 * g_;
           const f32x4 mr = *reinterpret_cast<const f32x4*>(sM + n);
+          // o = base - (lam / t) out + (lam / t) msub M'_r, two products per element
           f32x4 cr, o;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            cr[r] = (acc[nt][I][r] - msub * mr[r]) * inv;  // Sigma_t x_t
-            o[r] = xb[nt][r] - lam * cr[r];
+            o[r] = fmaf(-li, acc[nt][I][r], fmaf(lm, mr[r], xb[nt][r]));
+            if constexpr (TRAIN) cr[r] = (acc[nt][I][r] - msub * mr[r]) * inv;  // Sigma_t x_t
           }
           store4(sX + i * LDK + n, o[0], o[1], o[2], o[3]);
           if (TRAIN && i < nrow) {

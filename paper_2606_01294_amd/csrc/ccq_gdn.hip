@@ -105,12 +105,24 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
     if (J <= w) tile_mma<T, DK>(acc[J], sK + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
   }
   __syncthreads();
+  {
+    // the coefficients read whole and every entry formed before the mask is
+    // applied as a select (reads under the mask compile to a branch and a wait
+    // each); e^{gamma_i - gamma_j} may overflow above the diagonal, where the
+    // select discards it
+    const f32x4 gi = *reinterpret_cast<const f32x4*>(sGam + 16 * w + 4 * g4);
+    const f32x4 bi = *reinterpret_cast<const f32x4*>(sBeta + 16 * w + 4 * g4);
+    float gj[4];
 #pragma unroll
-  for (int J = 0; J < 4; ++J) {
+    for (int J = 0; J < 4; ++J) gj[J] = sGam[16 * J + c16];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int i = 16 * w + 4 * g4 + r, j = 16 * J + c16;
-      sA[i * LDA + j] = j < i ? sBeta[i] * __expf(sGam[i] - sGam[j]) * acc[J][r] : 0.f;
+    for (int J = 0; J < 4; ++J) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = 16 * w + 4 * g4 + r, j = 16 * J + c16;
+        const float v = bi[r] * __expf(gi[r] - gj[J]) * acc[J][r];
+        sA[i * LDA + j] = j < i ? v : 0.f;
+      }
     }
   }
   __syncthreads();
@@ -820,9 +832,9 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
   const Seq sq = seq_of(a.cu, b, a.T);
   const int ce = min((sq.len + C - 1) / C, cb + R);  // a packed sequence's own chunks
   if (cb >= ce) return;
-  const int tid = threadIdx.x, w = tid >> 6, l = lane_id();
+  const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
-  const int vg = w % NVG, ig = w / NVG;
+  const int vg = w % NVG, ig = NIG == 1 ? 0 : w / NVG;  // (uniform: no lane-masked branch on the tile)
   const size_t gstride = (size_t)a.H * DK;
   T* o = static_cast<T*>(a.o);
 

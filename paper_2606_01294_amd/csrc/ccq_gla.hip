@@ -250,9 +250,9 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
   const Seq sq = seq_of(a.cu, b, a.T);
   const int ce = min((sq.len + C - 1) / C, cb + R);  // a packed sequence's own chunks
   if (cb >= ce) return;
-  const int tid = threadIdx.x, w = tid >> 6, l = lane_id();
+  const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
-  const int vg = w % NVG, ig = w / NVG;
+  const int vg = w % NVG, ig = NIG == 1 ? 0 : w / NVG;  // (uniform: no lane-masked branch on the tile)
   const size_t gstride = (size_t)a.H * DK;
   constexpr int NTS = CARRY ? VPW : 1, NPT = CARRY ? 2 * NK : 1;
   f32x4 Sc[NTS][NPT];  // CARRY: this wave's value tiles of S^T, pair order
