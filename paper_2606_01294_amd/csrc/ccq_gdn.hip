@@ -454,10 +454,10 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
   static_assert(NKH >= 1 && VB % 1024 == 0, "tiles");
   static_assert(!RS || NH > 1, "the reduce-scatter exchange splits the keys");
   static_assert(!RSU || RS, "the split U builds on the split R");
-  __shared__ __align__(1024) char smem[NSTAGE * SB + XB + 1024 + XR];
+  static_assert(NIV % NW == 0 || NW % NIV == 0, "V pieces over the waves");
+  __shared__ __align__(1024) char smem[NSTAGE * SB + XB + XR];
   f32x4* const sX = reinterpret_cast<f32x4*>(smem + NSTAGE * SB);
-  char* const sDummy = smem + NSTAGE * SB + XB;
-  T* const sR = reinterpret_cast<T*>(smem + NSTAGE * SB + XB + 1024);
+  T* const sR = reinterpret_cast<T*>(smem + NSTAGE * SB + XB);
   T* const sU = sR + NPR * 2 * 64 * 8;  // RSU: fragments of U diag(e^{gamma_C - gamma})
 
   const int nvt = a.dv / BVS;
@@ -483,11 +483,11 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
 
   // chunk ci into stage ci % NSTAGE.  Piece i of each operand goes to wave
   // i % NW, so every wave issues the same number of pieces of each kind (a
-  // wave without a V piece reloads row 0 into the spare area).  Addresses
+  // piece that not every wave can have is shared out by lanes).  Addresses
   // are a per-chunk base (uniform) plus a 32-bit per-lane offset; rows past
   // the end of the sequence read row nrow - 1 (finite data; the chunk
   // transform zeroes their contribution).
-  static_assert(NIK % NW == 0 && NIT % NW == 0, "piece split");
+  static_assert(NIK % NW == 0 && NIT % NW == 0 && 64 % NW == 0, "piece split");
   auto issue = [&](int ci) {
     char* sb = smem + (ci % NSTAGE) * SB;
     const int r0 = ci * C, nrow = min(C, sq.len - r0);
@@ -508,20 +508,24 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
       const int off = row * C + 8 * ((l % 8) ^ tswz(row));
       __builtin_amdgcn_global_load_lds((const void*)(tb + off), (lds_void*)(sb + KB + ins * 1024), 16, 0, 0);
     }
+    {
+      // with fewer V pieces than waves, NW / NIV waves share a piece, each
+      // loading its own lanes of it (lane i of a piece lands at its base + 16 i
+      // whichever lanes are active)
+      constexpr int CPR = BVS / 8, SH = NIV >= NW ? 1 : NW / NIV, LPW = 64 / SH;
 #pragma unroll
-    for (int it = 0; it < NIVW; ++it) {
-      constexpr int CPR = BVS / 8;
-      const int ins = it * NW + w, row = ins * (64 / CPR) + l / CPR;
-      if (NIV % NW == 0 || ins < NIV) {
-        const int off = min(row, nrow - 1) * hv + 8 * (l % CPR);
-        __builtin_amdgcn_global_load_lds((const void*)(vb + off), (lds_void*)(sb + KB + TB + ins * 1024), 16, 0, 0);
-      } else {
-        __builtin_amdgcn_global_load_lds((const void*)(vb + 8 * (l % CPR)), (lds_void*)sDummy, 16, 0, 0);
+      for (int it = 0; it < NIVW; ++it) {
+        const int ins = SH == 1 ? it * NW + w : w / SH, row = ins * (64 / CPR) + l / CPR;
+        if (SH == 1 || l / LPW == w % SH) {
+          const int off = min(row, nrow - 1) * hv + 8 * (l % CPR);
+          __builtin_amdgcn_global_load_lds((const void*)(vb + off), (lds_void*)(sb + KB + TB + ins * 1024), 16, 0, 0);
+        }
       }
     }
-    // the coefficient rows (one piece; the other waves load it into a spare area)
-    __builtin_amdgcn_global_load_lds((const void*)(a.gam + (((size_t)bh * N + ci) * 5 + 1) * C + 4 * l),
-                                     (lds_void*)(w == 0 ? sb + KB + TB + VB : sDummy), 16, 0, 0);
+    // the coefficient rows, one piece shared the same way by all the waves
+    if (l / (64 / NW) == w)
+      __builtin_amdgcn_global_load_lds((const void*)(a.gam + (((size_t)bh * N + ci) * 5 + 1) * C + 4 * l),
+                                       (lds_void*)(sb + KB + TB + VB), 16, 0, 0);
   };
   // stores per wave of chunk c: S_r (every sstride-th chunk) and U^T
   auto nstore = [&](int c) { return (c % a.sstride == 0 ? NKH : 0) + NSU; };
@@ -1005,8 +1009,7 @@ hipError_t run_gdn_state_v(const GdnArgs& a, hipStream_t st) {
 // LDS of the streamed kernel with a ring of `ns` stages
 constexpr size_t gdn_dma_lds(int dk, int npr, int nh, int ns, bool rs, bool rsu) {
   return (size_t)ns * (kChunk * dk * 2 + kChunk * kChunk * 2 + kChunk * 16 * npr * 2 + 4 * kChunk * 4) +
-         (nh > 1 ? (size_t)npr * nh * 4 * 64 * 16 : 16) + 1024 +
-         (rs ? (size_t)npr * 2 * 64 * 16 * (rsu ? 2 : 1) : 0);
+         (nh > 1 ? (size_t)npr * nh * 4 * 64 * 16 : 16) + (rs ? (size_t)npr * 2 * 64 * 16 * (rsu ? 2 : 1) : 0);
 }
 // With a key split the exchange is the reduce-scatter form: bit-identical, and
 // measured on the 1.3B shape 380 -> 362 us per forward call at T = 4096 and

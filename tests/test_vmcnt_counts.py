@@ -23,16 +23,15 @@ C = 64
 
 def expected(DK, NPR, NH):
     """(stream-load instructions in the loop, stores in the loop) from the kernel's
-    constants; a V piece that only some waves have is an if/else of one load each."""
+    constants; a piece shared by several waves is one lane-masked load in each."""
     NW, BVS = NPR * NH, 16 * NPR
     DKH = DK // NH
     NKH = DKH // 32
     NIK, NIT, NIV = C * DK * 2 // 1024, C * C * 2 // 1024, C * BVS * 2 // 1024
     NIVW = (NIV + NW - 1) // NW
     NIW = NIK // NW + NIT // NW + NIVW + 1
-    alt = 1 if NIV % NW != 0 else 0
     NSU = 2 if NH == 1 else 1
-    return NIW + alt, NKH + NSU
+    return NIW, NKH + NSU
 
 
 # the instantiations the library launches (template <DK, NPR, NH, NSTAGE, RS, RSU>)
