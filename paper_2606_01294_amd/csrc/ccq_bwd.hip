@@ -387,30 +387,46 @@ __global__ __launch_bounds__(kThreads) void gla_dg_kernel(const DgArgs a) {
 // ccq_dk_kernel starts each segment from the sum over the later segments and
 // walks the segment's chunks from last to first.  For large DK the 16 x 16
 // tiles of H (and the output columns of ccq_dk_kernel) are split over NSPLIT
-// workgroups per segment (blockIdx.y); each stages the whole chunk.
-template <typename T, int DK, int NSPLIT>
-__global__ __launch_bounds__(kThreads, 1) void ccq_dk_stats_kernel(const CcqDkArgs a) {
+// workgroups per segment; each stages the whole chunk.
+// Product of two 16-wide column blocks of row-major chunk tiles over the
+// chunk's rows: acc += A[:, a0..]^T B[:, b0..], both operands taken with
+// transposing LDS reads (at = A + a0, bt = B + b0).
+template <typename T, int K>
+__device__ __forceinline__ void tile_mma_tr(f32x4& acc, const T* at, int lda, const T* bt, int ldb) {
+#pragma unroll
+  for (int k0 = 0; k0 < K; k0 += 32) mma(acc, ld_frag_tr(at + k0 * lda, lda), ld_frag_tr(bt + k0 * ldb, ldb));
+}
+
+// Both kernels stage q and rho u as row-major chunk tiles (16-byte writes) and
+// read them feature-major with transposing reads where a product runs over the
+// chunk's rows.
+template <typename T, int DK, int NSPLIT, int NWV>
+__global__ __launch_bounds__(64 * NWV, 1) void ccq_dk_stats_kernel(const CcqDkArgs a) {
   constexpr int C = kChunk;
   constexpr int P = Pad<T>::value;
-  constexpr int LDT = C + P;
-  constexpr int NT16 = DK / 16, NPW = NT16 * NT16 / (4 * NSPLIT);
-  constexpr int NPART = kThreads / DK;
-  static_assert(NPW >= 1 && kThreads % DK == 0, "tile split");
+  constexpr int LDQ = DK + P;
+  constexpr int NTHR = 64 * NWV;
+  constexpr int NT16 = DK / 16, NPW = NT16 * NT16 / (NWV * NSPLIT);
+  constexpr int NPART = NTHR / DK;
+  static_assert(NPW >= 1 && NTHR % DK == 0, "tile split");
+  typedef ChunkTile<T, DK, NTHR> Tile;
 
-  __shared__ __align__(16) T sQT[DK * LDT];
-  __shared__ __align__(16) T sRUT[DK * LDT];  // (rho u)^T
-  __shared__ float sA[C], sB[C];              // -(m.q)/t and -rho (m.u)/t
-  __shared__ float sDp[kThreads];
+  __shared__ __align__(16) T sQ[C * LDQ];
+  __shared__ __align__(16) T sRU[C * LDQ];  // rho u
+  __shared__ float sA[C], sB[C];            // -(m.q)/t and -rho (m.u)/t
+  __shared__ float sDp[NTHR];
 
   const int N = (a.T + C - 1) / C;
   const int NS = (N + a.seg - 1) / a.seg;
-  const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
+  // the NSPLIT workgroups of a segment are consecutive logical blocks: one
+  // XCD (one L2) at about the same time, so each chunk comes from HBM once
+  const int lbs = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int split = lbs % NSPLIT, lb = lbs / NSPLIT;  // split: this workgroup's share of the tiles
   const int bh = lb / NS, sg = lb % NS;
   const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
-  const int split = NSPLIT > 1 ? (int)blockIdx.y : 0;  // this workgroup's share of the tiles
-  const int tw0 = (split * (kThreads / 64) + w) * NPW;  // first tile of this wave
+  const int tw0 = (split * NWV + w) * NPW;  // first tile of this wave
   const T* q = static_cast<const T*>(a.q);
   const T* uu = static_cast<const T*>(a.u);
   const size_t gs = (size_t)a.H * DK;
@@ -422,7 +438,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_stats_kernel(const CcqDkAr
   for (int u = 0; u < NPW; ++u) H[u] = zero4();
   float dsum = 0.f;
 
-  ChunkTile<T, DK> rq, ru;
+  Tile rq, ru;
   RowScalar rlam, rmq, rmu;
   auto prefetch = [&](int ci) {
     const int r0 = ci * C;
@@ -430,7 +446,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_stats_kernel(const CcqDkAr
     rq.load(q + tok_off(b, r0, h, a.T, a.H, DK), gs, nrow);
     ru.load(uu + tok_off(b, r0, h, a.T, a.H, DK), gs, nrow);
     const size_t t0i = ((size_t)b * a.T + r0) * a.H + h;
-    const int row = ChunkTile<T, DK>::row();
+    const int row = Tile::row();
     rlam.load(a.lam + t0i, (size_t)a.H, row, nrow);
     rmq.load(a.mdot_q + t0i, (size_t)a.H, row, nrow);
     rmu.load(a.mdot_u + t0i, (size_t)a.H, row, nrow);
@@ -440,20 +456,21 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_stats_kernel(const CcqDkAr
   for (int ci = c_begin; ci < c_end; ++ci) {
     lds_barrier();
     {
-      const int j = ChunkTile<T, DK>::row();
+      const int j = Tile::row();
       const float tpos = (float)(ci * C + j + 1);
       const float rho = -rlam.get() / tpos;
       if (w == 0) {
         sA[j] = a.centered ? -rmq.get() / tpos : 0.f;
         sB[j] = a.centered ? -rho * rmu.get() / tpos : 0.f;
       }
-      rq.store_t(sQT, LDT);
+      rq.store(sQ, LDQ);
 #pragma unroll
-      for (int u = 0; u < ChunkTile<T, DK>::NV; ++u) {
+      for (int u = 0; u < Tile::NV; ++u) {
         const auto x = ru.get(u);
-        const int c0 = ChunkTile<T, DK>::col(u);
+        typename Tile::vec_t y;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sRUT[(c0 + e) * LDT + j] = to<T>(rho * f32(x[e]));
+        for (int e = 0; e < 8; ++e) y[e] = to<T>(rho * f32(x[e]));
+        *reinterpret_cast<typename Tile::vec_t*>(sRU + j * LDQ + Tile::col(u)) = y;
       }
     }
     if (ci + 1 < c_end) prefetch(ci + 1);
@@ -461,15 +478,15 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_stats_kernel(const CcqDkAr
 #pragma unroll
     for (int u = 0; u < NPW; ++u) {
       const int tau = tw0 + u, tr = tau / NT16, tc = tau % NT16;
-      tile_mma<T, C>(H[u], sRUT + 16 * tr * LDT, LDT, sQT + 16 * tc * LDT, LDT);
-      tile_mma<T, C>(H[u], sQT + 16 * tr * LDT, LDT, sRUT + 16 * tc * LDT, LDT);
+      tile_mma_tr<T, C>(H[u], sRU + 16 * tr, LDQ, sQ + 16 * tc, LDQ);
+      tile_mma_tr<T, C>(H[u], sQ + 16 * tr, LDQ, sRU + 16 * tc, LDQ);
     }
     if (split == 0) {  // this chunk's mean-term vector, NPART threads per key channel
       const int n = tid % DK, part = tid / DK;
       float x = 0.f;
 #pragma unroll 8
       for (int t = part * (C / NPART); t < (part + 1) * (C / NPART); ++t)
-        x += sA[t] * f32(sRUT[n * LDT + t]) + sB[t] * f32(sQT[n * LDT + t]);
+        x += sA[t] * f32(sRU[t * LDQ + n]) + sB[t] * f32(sQ[t * LDQ + n]);
       sDp[tid] = x;
     }
     lds_barrier();
@@ -523,28 +540,24 @@ __global__ __launch_bounds__(kThreads) void ccq_dk_suffix_kernel(const CcqDkArgs
 //   dk_j = H k_j + D + sum_{t>=j} (W1[t][j] rho_t u_t + W2[t][j] q_t),
 // then H += sum_t rho_t (u_t q_t^T + q_t u_t^T) and D += the chunk's D.  For
 // bf16, H and the weights W enter the products as a bf16 head plus a bf16 tail.
-// The output columns are split over NSPLIT workgroups per segment (blockIdx.y).
-// Without the row-major copies of q and u (kRowQU false, DK = 256, where they
-// would not fit in LDS beside the rest), the intra weights read q and rho u
-// from their transposed tiles with transposing LDS reads.
-template <typename T, int DK, int NSPLIT>
-__global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) {
+// The output columns are split over NSPLIT workgroups per segment.
+// W2 is formed from the staged rho u (rho_t u_t . k_j - rho_t (m_t.u_t)/t).
+template <typename T, int DK, int NSPLIT, int NWV>
+__global__ __launch_bounds__(64 * NWV, 1) void ccq_dk_kernel(const CcqDkArgs a) {
   constexpr int C = kChunk;
   constexpr int P = Pad<T>::value;
   constexpr bool kSplit = sizeof(T) == 2;
-  constexpr bool kRowQU = DK <= 128;
-  constexpr int LDQ = DK + P, LDT = C + P, LDA = C + P;
+  constexpr int LDQ = DK + P, LDA = C + P;
   constexpr int NCT = DK / 16;  // 16-row tiles of the contraction index c
-  constexpr int NTW = DK / (64 * NSPLIT);  // output column tiles per wave
+  constexpr int NTHR = 64 * NWV;
+  constexpr int NTW = DK / (16 * NWV * NSPLIT);  // output column tiles per wave
+  typedef ChunkTile<T, DK, NTHR> Tile;
   constexpr int NK = DK / 32;
   static_assert(NTW >= 1, "column split");
-  static_assert(kRowQU || sizeof(T) == 2, "transposing reads are bf16 only");
 
-  __shared__ __align__(16) T sQ[kRowQU ? C * LDQ : 8];
-  __shared__ __align__(16) T sU[kRowQU ? C * LDQ : 8];
+  __shared__ __align__(16) T sQ[C * LDQ];
+  __shared__ __align__(16) T sRU[C * LDQ];  // rho u
   __shared__ __align__(16) T sK[C * LDQ];
-  __shared__ __align__(16) T sQT[DK * LDT];
-  __shared__ __align__(16) T sRUT[DK * LDT];  // (rho u)^T
   __shared__ __align__(16) T sW1h[C * LDA];   // transposed: [j][t]
   __shared__ __align__(16) T sW1l[kSplit ? C * LDA : 8];
   __shared__ __align__(16) T sW2h[C * LDA];
@@ -553,13 +566,14 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
 
   const int N = (a.T + C - 1) / C;
   const int NS = (N + a.seg - 1) / a.seg;
-  const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
+  // the NSPLIT workgroups of a segment are consecutive logical blocks (one L2)
+  const int lbs = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int split = lbs % NSPLIT, lb = lbs / NSPLIT;
   const int bh = lb / NS, sg = lb % NS;
   const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, w = wave_id(), l = lane_id();
   const int g4 = l >> 4, c16 = l & 15;
-  const int split = NSPLIT > 1 ? (int)blockIdx.y : 0;
-  const int nt0 = (split * (kThreads / 64) + w) * NTW;  // first output column tile of this wave
+  const int nt0 = (split * NWV + w) * NTW;  // first output column tile of this wave
   const T* q = static_cast<const T*>(a.q);
   const T* k = static_cast<const T*>(a.k);
   const T* uu = static_cast<const T*>(a.u);
@@ -569,7 +583,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
   const int c_end = (c_begin + a.seg) < N ? (c_begin + a.seg) : N;
 
   // the weights' tiles above the diagonal stay zero
-  for (int idx = tid; idx < C * LDA; idx += kThreads) {
+  for (int idx = tid; idx < C * LDA; idx += NTHR) {
     sW1h[idx] = to<T>(0.f);
     sW2h[idx] = to<T>(0.f);
     if constexpr (kSplit) {
@@ -599,7 +613,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
     }
   }
 
-  ChunkTile<T, DK> rq, ru, rk;
+  Tile rq, ru, rk;
   RowScalar rlam, rmq, rmu;
   auto prefetch = [&](int ci) {
     const int r0 = ci * C;
@@ -608,7 +622,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
     ru.load(uu + tok_off(b, r0, h, a.T, a.H, DK), gs, nrow);
     rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), gs, nrow);
     const size_t t0i = ((size_t)b * a.T + r0) * a.H + h;
-    const int row = ChunkTile<T, DK>::row();
+    const int row = Tile::row();
     rlam.load(a.lam + t0i, (size_t)a.H, row, nrow);
     rmq.load(a.mdot_q + t0i, (size_t)a.H, row, nrow);
     rmu.load(a.mdot_u + t0i, (size_t)a.H, row, nrow);
@@ -620,7 +634,7 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
     const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
     lds_barrier();  // (A)
     {
-      const int j = ChunkTile<T, DK>::row();
+      const int j = Tile::row();
       const float tpos = (float)(r0 + j + 1);
       const float rho = -rlam.get() / tpos;
       if (w == 0) {
@@ -628,28 +642,27 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
         sMq[j] = a.centered ? rmq.get() / tpos : 0.f;
         sMu[j] = a.centered ? rmu.get() / tpos : 0.f;
       }
-      if constexpr (kRowQU) {
-        rq.store(sQ, LDQ);
-        ru.store(sU, LDQ);
-      }
-      rq.store_t(sQT, LDT);
+      rq.store(sQ, LDQ);
       rk.store(sK, LDQ);
 #pragma unroll
-      for (int u = 0; u < ChunkTile<T, DK>::NV; ++u) {
+      for (int u = 0; u < Tile::NV; ++u) {
         const auto x = ru.get(u);
-        const int c0 = ChunkTile<T, DK>::col(u);
+        typename Tile::vec_t y;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sRUT[(c0 + e) * LDT + j] = to<T>(rho * f32(x[e]));
+        for (int e = 0; e < 8; ++e) y[e] = to<T>(rho * f32(x[e]));
+        *reinterpret_cast<typename Tile::vec_t*>(sRU + j * LDQ + Tile::col(u)) = y;
       }
     }
     float dcv[NTW];  // this chunk's D, added after its outputs
 #pragma unroll
     for (int x = 0; x < NTW; ++x) dcv[x] = a.dchunk[((size_t)bh * N + ci) * DK + 16 * (nt0 + x) + c16];
-    // the backbone's part of dk for this wave's outputs, requested before the products
+    // the backbone's part of dk for this wave's outputs, requested before the
+    // products: here at DK = 256 (fewer registers live in the dk-row products),
+    // else at the start of those products (measured faster there)
     const size_t rowoff = tok_off(b, r0, h, a.T, a.H, DK);
+    constexpr bool kEarlyDkg = DK >= 256;
     float dkg[NTW][4][4];
-#pragma unroll
-    for (int x = 0; x < NTW; ++x)
+    auto load_dkg = [&](int x) {
 #pragma unroll
       for (int J = 0; J < 4; ++J)
 #pragma unroll
@@ -657,33 +670,32 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
           const int jr = 16 * J + 4 * g4 + r;
           dkg[x][J][r] = a.dk_gla[rowoff + (jr < nrow ? jr : nrow - 1) * (int)gs + 16 * (nt0 + x) + c16];
         }
+    };
+    if constexpr (kEarlyDkg)
+#pragma unroll
+      for (int x = 0; x < NTW; ++x) load_dkg(x);
     if (ci > c_begin) prefetch(ci - 1);
     lds_barrier();  // (B)
 
     // intra weights: the ten tiles on or below the diagonal, over the waves
 #pragma unroll
-    for (int s3 = 0; s3 < 3; ++s3) {
-      const int t = w + 4 * s3;
+    for (int s3 = 0; s3 < (10 + NWV - 1) / NWV; ++s3) {
+      const int t = w + NWV * s3;
       if (t < 10) {
         const int I = intra_tile_row(t), J = intra_tile_col(t);
-        f32x4 s1 = zero4(), s2 = zero4();
-        if constexpr (kRowQU) {
-          tile_mma<T, DK>(s1, sQ + 16 * I * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
-          tile_mma<T, DK>(s2, sU + 16 * I * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
-        } else {  // s2 = (rho u) . k here
+        f32x4 s1 = zero4(), s2 = zero4();  // q . k and (rho u) . k
 #pragma unroll
-          for (int k0 = 0; k0 < DK; k0 += 32) {
-            const Frag<T> kf = ld_frag(sK + 16 * J * LDQ + k0, LDQ);
-            mma(s1, ld_frag_tr(sQT + k0 * LDT + 16 * I, LDT), kf);
-            mma(s2, ld_frag_tr(sRUT + k0 * LDT + 16 * I, LDT), kf);
-          }
+        for (int k0 = 0; k0 < DK; k0 += 32) {
+          const Frag<T> kf = ld_frag(sK + 16 * J * LDQ + k0, LDQ);
+          mma(s1, ld_frag(sQ + 16 * I * LDQ + k0, LDQ), kf);
+          mma(s2, ld_frag(sRU + 16 * I * LDQ + k0, LDQ), kf);
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int tt = 16 * I + 4 * g4 + r, jj = 16 * J + c16;
           const bool on = jj <= tt;
           const float w1 = on ? s1[r] - sMq[tt] : 0.f;
-          const float w2 = on ? (kRowQU ? sRho[tt] * (s2[r] - sMu[tt]) : s2[r] - sRho[tt] * sMu[tt]) : 0.f;
+          const float w2 = on ? s2[r] - sRho[tt] * sMu[tt] : 0.f;
           if constexpr (kSplit) {
             bf16_t hi, lo;
             split_bf16(w1, hi, lo);
@@ -701,56 +713,62 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
     }
     lds_barrier();  // (C)
 
-    // dk rows j (all four row tiles), this wave's columns n
+    // dk rows j (all four row tiles), this wave's columns n.  H enters one k
+    // step at a time (its bf16 head and tail formed just before use), the four
+    // row tiles accumulating side by side: each tile sums the same products in
+    // the same order as a tile-by-tile walk, with a quarter of the registers.
 #pragma unroll
     for (int x = 0; x < NTW; ++x) {
       const int nt = nt0 + x;
-      Frag<T> hh[NK], hl[NK];
+      if constexpr (!kEarlyDkg) load_dkg(x);
+      f32x4 acc[4];
+#pragma unroll
+      for (int J = 0; J < 4; ++J) acc[J] = zero4();
 #pragma unroll
       for (int m = 0; m < NK; ++m) {
+        Frag<T> hh, hl;
         if constexpr (kSplit) {
           const f32x4 p0 = Hc[2 * m][x], p1 = Hc[2 * m + 1][x];
-          hh[m] = acc_pair_frag<T>(p0, p1);
+          hh = acc_pair_frag<T>(p0, p1);
           f32x4 r0v, r1v;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            r0v[e] = p0[e] - f32(hh[m].v[e]);
-            r1v[e] = p1[e] - f32(hh[m].v[4 + e]);
+            r0v[e] = p0[e] - f32(hh.v[e]);
+            r1v[e] = p1[e] - f32(hh.v[4 + e]);
           }
-          hl[m] = acc_pair_frag<T>(r0v, r1v);
+          hl = acc_pair_frag<T>(r0v, r1v);
         } else {
-          hh[m] = acc_pair_frag<T>(Hc[2 * m][x], Hc[2 * m + 1][x]);
+          hh = acc_pair_frag<T>(Hc[2 * m][x], Hc[2 * m + 1][x]);
+        }
+#pragma unroll
+        for (int J = 0; J < 4; ++J) {
+          const Frag<T> kf = ld_frag_acc(sK + 16 * J * LDQ + 32 * m, (size_t)LDQ);
+          mma(acc[J], kf, hh);
+          if constexpr (kSplit) mma(acc[J], kf, hl);
         }
       }
       Frag<T> f1[2], f2[2];
 #pragma unroll
       for (int m2 = 0; m2 < 2; ++m2) {
-        f1[m2] = ld_frag(sRUT + 16 * nt * LDT + 32 * m2, LDT);
-        f2[m2] = ld_frag(sQT + 16 * nt * LDT + 32 * m2, LDT);
+        f1[m2] = ld_frag_tr(sRU + 32 * m2 * LDQ + 16 * nt, LDQ);
+        f2[m2] = ld_frag_tr(sQ + 32 * m2 * LDQ + 16 * nt, LDQ);
       }
 #pragma unroll
       for (int J = 0; J < 4; ++J) {
-        f32x4 acc = zero4();
-#pragma unroll
-        for (int m = 0; m < NK; ++m) {
-          const Frag<T> kf = ld_frag_acc(sK + 16 * J * LDQ + 32 * m, (size_t)LDQ);
-          mma(acc, kf, hh[m]);
-          if constexpr (kSplit) mma(acc, kf, hl[m]);
-        }
 #pragma unroll
         for (int m2 = 0; m2 < 2; ++m2) {
-          mma(acc, ld_frag(sW1h + 16 * J * LDA + 32 * m2, LDA), f1[m2]);
-          mma(acc, ld_frag(sW2h + 16 * J * LDA + 32 * m2, LDA), f2[m2]);
+          mma(acc[J], ld_frag(sW1h + 16 * J * LDA + 32 * m2, LDA), f1[m2]);
+          mma(acc[J], ld_frag(sW2h + 16 * J * LDA + 32 * m2, LDA), f2[m2]);
           if constexpr (kSplit) {
-            mma(acc, ld_frag(sW1l + 16 * J * LDA + 32 * m2, LDA), f1[m2]);
-            mma(acc, ld_frag(sW2l + 16 * J * LDA + 32 * m2, LDA), f2[m2]);
+            mma(acc[J], ld_frag(sW1l + 16 * J * LDA + 32 * m2, LDA), f1[m2]);
+            mma(acc[J], ld_frag(sW2l + 16 * J * LDA + 32 * m2, LDA), f2[m2]);
           }
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int jr = 16 * J + 4 * g4 + r;
           if (jr < nrow) {
-            dk_out[rowoff + jr * (int)gs + 16 * nt + c16] = to<T>(dkg[x][J][r] + acc[r] + dreg[x]);
+            dk_out[rowoff + jr * (int)gs + 16 * nt + c16] = to<T>(dkg[x][J][r] + acc[J][r] + dreg[x]);
           }
         }
       }
@@ -762,15 +780,15 @@ __global__ __launch_bounds__(kThreads, 1) void ccq_dk_kernel(const CcqDkArgs a) 
     for (int x = 0; x < NTW; ++x)
 #pragma unroll
       for (int m2 = 0; m2 < 2; ++m2) {
-        bq[x][m2] = ld_frag(sQT + 16 * (nt0 + x) * LDT + 32 * m2, LDT);
-        bu[x][m2] = ld_frag(sRUT + 16 * (nt0 + x) * LDT + 32 * m2, LDT);
+        bq[x][m2] = ld_frag_tr(sQ + 32 * m2 * LDQ + 16 * (nt0 + x), LDQ);
+        bu[x][m2] = ld_frag_tr(sRU + 32 * m2 * LDQ + 16 * (nt0 + x), LDQ);
       }
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
       for (int m2 = 0; m2 < 2; ++m2) {
-        const Frag<T> au = ld_frag(sRUT + 16 * ct * LDT + 32 * m2, LDT);
-        const Frag<T> aq = ld_frag(sQT + 16 * ct * LDT + 32 * m2, LDT);
+        const Frag<T> au = ld_frag_tr(sRU + 32 * m2 * LDQ + 16 * ct, LDQ);
+        const Frag<T> aq = ld_frag_tr(sQ + 32 * m2 * LDQ + 16 * ct, LDQ);
 #pragma unroll
         for (int x = 0; x < NTW; ++x) {
           mma(Hc[ct][x], au, bq[x][m2]);
@@ -798,11 +816,16 @@ hipError_t run_ccq_dk(const CcqDkArgs& a, hipStream_t st) {
   const int NS = (N + a.seg - 1) / a.seg;
   const int nseg = a.B * a.H * NS;
   if (nseg == 0) return hipSuccess;
-  // at DK = 256 H's tiles are split over two workgroups per segment and the
-  // output columns over four, so that a wave's share of H fits its registers
-  // (no spills)
-  constexpr int NSPLIT_S = DK >= 256 ? 2 : 1, NSPLIT = DK >= 256 ? 4 : 1;
-  hipLaunchKernelGGL((ccq_dk_stats_kernel<T, DK, NSPLIT_S>), dim3(nseg, NSPLIT_S), dim3(kThreads), 0, st, a);
+  // eight waves per workgroup (two per SIMD) for ccq_dk_kernel from DK = 128
+  // and ccq_dk_stats_kernel at DK = 256 (measured: at DK = 128 the statistics
+  // run faster with four); at DK = 256 H's tiles (ccq_dk_stats_kernel) and the
+  // output columns (ccq_dk_kernel, each wave carrying one 16-column tile of H)
+  // are split over two workgroups per segment, so that a wave's share of H
+  // fits its registers
+  constexpr int NSPLIT_S = DK >= 256 ? 2 : 1, NSPLIT = DK >= 256 ? 2 : 1;
+  constexpr int NWV_S = DK >= 256 ? 8 : 4, NWV = DK >= 128 ? 8 : 4;
+  hipLaunchKernelGGL((ccq_dk_stats_kernel<T, DK, NSPLIT_S, NWV_S>), dim3(nseg * NSPLIT_S), dim3(64 * NWV_S), 0, st,
+                     a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t per4 = ((size_t)DK * DK + DK) / 4;
@@ -810,7 +833,7 @@ hipError_t run_ccq_dk(const CcqDkArgs& a, hipStream_t st) {
                      dim3(kThreads), 0, st, a);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((ccq_dk_kernel<T, DK, NSPLIT>), dim3(nseg, NSPLIT), dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((ccq_dk_kernel<T, DK, NSPLIT, NWV>), dim3(nseg * NSPLIT), dim3(64 * NWV), 0, st, a);
   return hipGetLastError();
 }
 template <typename T, typename TG>
