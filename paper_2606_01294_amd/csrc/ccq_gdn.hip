@@ -488,20 +488,28 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
   // the end of the sequence read row nrow - 1 (finite data; the chunk
   // transform zeroes their contribution).
   static_assert(NIK % NW == 0 && NIT % NW == 0 && 64 % NW == 0, "piece split");
-  auto issue = [&](int ci) {
+  // the K pieces [it0, it1) of this wave
+  auto issue_k = [&](int ci, int it0, int it1) {
     char* sb = smem + (ci % NSTAGE) * SB;
     const int r0 = ci * C, nrow = min(C, sq.len - r0);
-    const int hs = a.H * DK, hv = a.H * a.dv;
+    const int hs = a.H * DK;
     const T* kb = k + seq_off(sq, r0, h, a.H, DK);
-    const T* tb = Tg + ((size_t)bh * N + ci) * C * C;
-    const T* vb = vin + seq_off(sq, r0, h, a.H, a.dv) + v0;
 #pragma unroll
     for (int it = 0; it < NIK / NW; ++it) {
+      if (it < it0 || it >= it1) continue;
       constexpr int CPR = DK / 8;
       const int ins = it * NW + w, row = ins * (64 / CPR) + l / CPR;
       const int off = min(row, nrow - 1) * hs + 8 * ((l % CPR) ^ kswz(row));
       __builtin_amdgcn_global_load_lds((const void*)(kb + off), (lds_void*)(sb + ins * 1024), 16, 0, 0);
     }
+  };
+  // the Tm, V and coefficient pieces of this wave
+  auto issue_rest = [&](int ci) {
+    char* sb = smem + (ci % NSTAGE) * SB;
+    const int r0 = ci * C, nrow = min(C, sq.len - r0);
+    const int hv = a.H * a.dv;
+    const T* tb = Tg + ((size_t)bh * N + ci) * C * C;
+    const T* vb = vin + seq_off(sq, r0, h, a.H, a.dv) + v0;
 #pragma unroll
     for (int it = 0; it < NIT / NW; ++it) {
       const int ins = it * NW + w, row = ins * 8 + l / 8;
@@ -526,6 +534,10 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
     if (l / (64 / NW) == w)
       __builtin_amdgcn_global_load_lds((const void*)(a.gam + (((size_t)bh * N + ci) * 5 + 1) * C + 4 * l),
                                        (lds_void*)(sb + KB + TB + VB), 16, 0, 0);
+  };
+  auto issue = [&](int ci) {
+    issue_k(ci, 0, NIK / NW);
+    issue_rest(ci);
   };
   // stores per wave of chunk c: S_r (every sstride-th chunk) and U^T
   auto nstore = [&](int c) { return (c % a.sstride == 0 ? NKH : 0) + NSU; };
@@ -566,7 +578,11 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
     const float* Fb = reinterpret_cast<const float*>(sb + KB + TB + VB);
     wait_chunk(ci);
     lds_barrier();  // chunk ci visible; stage (ci - 1) % NSTAGE and the exchange area released
-    if (ci + NSTAGE - 1 < NL) issue(ci + NSTAGE - 1);
+    // chunk ci + NSTAGE - 1 goes out in pieces between this chunk's first
+    // products (their issue then overlaps the matrix cores' work), all of it
+    // before this chunk's stores, so the counted waits stay as they are
+    const bool ahead = ci + NSTAGE - 1 < NL;
+    constexpr int KPJ = (NIK / NW + 3) / 4;  // K pieces after each token tile of P
 
     // P = K S_r^T over this wave's features: K rows 16 J + c16, features in
     // natural order (piece (c0 + 32 m) / 8 + g4, one 16-byte read)
@@ -617,8 +633,10 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_dma_kernel(const G
 #pragma unroll
         for (int m = 0; m < NKH; ++m) mma(acc, kf[J & 1][m], sf[m]);
         R[J] = acc;
+        if (ahead) issue_k(ci + NSTAGE - 1, J * KPJ, (J + 1) * KPJ);
       }
     }
+    if (ahead) issue_rest(ci + NSTAGE - 1);
     // coefficients and Tm rows, read now so that their latency overlaps the
     // exchange
     constexpr int IPW = RSU ? JPW : 4;  // the token tiles of U this wave forms
