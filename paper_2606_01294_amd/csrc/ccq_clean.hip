@@ -401,7 +401,18 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
   // row scales of raw q and k (l2 normalisation folded in), for the rows of
   // this thread's staged vectors
   float fq[NV], fk[NV];
-  auto prefetch = [&](int c) {
+  // streamed chunk: piece i of the x rows for i < NI, of the key rows after
+  typedef LdsStream<DK, NW> Stream;
+  auto stream_piece = [&](int c, int i) {
+    if constexpr (kDma) {
+      const int r0 = c * C, n = min(C, sq.len - r0);
+      if (i < Stream::NI) Stream::load_one(x + seq_off(sq, r0, h, a.H, DK), gstride, n, sSt, i);
+      else Stream::load_one(k + seq_off(sq, r0, h, a.H, DK), gstride, n, sSt + C * DK, i - Stream::NI);
+    }
+  };
+  // everything but the streamed pieces when `spread` (those then go out one
+  // or two at a time between the next products)
+  auto prefetch = [&](int c, bool spread) {
     const int r0 = c * C, n = min(C, sq.len - r0);
     if (a.rq) {
 #pragma unroll
@@ -412,8 +423,9 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
       }
     }
     if constexpr (kDma) {
-      LdsStream<DK, NW>::load(x + seq_off(sq, r0, h, a.H, DK), gstride, n, sSt);
-      LdsStream<DK, NW>::load(k + seq_off(sq, r0, h, a.H, DK), gstride, n, sSt + C * DK);
+      if (!spread)
+#pragma unroll
+        for (int i = 0; i < 2 * Stream::NI; ++i) stream_piece(c, i);
     } else {
       rx.load(x + seq_off(sq, r0, h, a.H, DK), gstride, n);
       rk.load(k + seq_off(sq, r0, h, a.H, DK), gstride, n);
@@ -421,7 +433,7 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
     if (tid < C) rl.load(a.lam + seq_idx(sq, r0, h, a.H), (size_t)a.H, tid, n);
     if (DECAY && tid < C) rla.load(a.la + seq_idx(sq, r0, h, a.H), (size_t)a.H, tid, n);
   };
-  prefetch(cbeg);
+  prefetch(cbeg, false);
 
   // segment centre c_s and key sum before the segment about it, M'_s; one
   // thread per feature
@@ -567,7 +579,8 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
       else put(std::true_type{});
     }
     lds_barrier();  // (1) x, K', M'_c staged; the staging area is free
-    if (c + 1 < cend) prefetch(c + 1);
+    const bool more = c + 1 < cend;
+    if (more) prefetch(c + 1, true);
 
     // raw scores of the causal tiles this wave owns, to sS[i][j]; then
     // out^T = S'_r x^T: acc[nt][I] holds features n0 + 16 nt + 4 (l / 16) + r
@@ -602,6 +615,13 @@ __global__ __launch_bounds__(64 * NW, 1) void clean_out_kernel(const CleanArgs a
         for (int I = 0; I < 4; ++I)
 #pragma unroll
           for (int nt = 0; nt < NNT; ++nt) mma(acc[nt][I], af[nt], xf[I]);
+        // the next chunk's streamed pieces, spread over these products
+        if constexpr (kDma) {
+          constexpr int PPS = (2 * Stream::NI + NK - 1) / NK;
+#pragma unroll
+          for (int i = PPS * p; i < PPS * (p + 1); ++i)
+            if (i < 2 * Stream::NI && more) stream_piece(c + 1, i);
+        }
       }
     }
     lds_barrier();  // (2) scores complete

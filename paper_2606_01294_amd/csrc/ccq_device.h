@@ -506,16 +506,18 @@ struct LdsStream {
   static constexpr int RPI = 64 / VPR;     // rows per wave instruction
   static constexpr int NI = kChunk / RPI / NW;  // instructions per wave
   static_assert(VPR <= 64 && 64 % VPR == 0 && kChunk % (RPI * NW) == 0, "stream split");
-  __device__ __forceinline__ static void load(const bf16_t* src, size_t gstride, int n, bf16_t* dst) {
+  // instruction it (< NI) of this wave
+  __device__ __forceinline__ static void load_one(const bf16_t* src, size_t gstride, int n, bf16_t* dst, int it) {
     typedef __attribute__((address_space(3))) void lds_void;
     const int l = lane_id(), w = wave_id();
+    const int ins = w * NI + it;
+    const int row = ins * RPI + l / VPR;
+    const bf16_t* p = src + (size_t)(row < n ? row : n - 1) * gstride + (l % VPR) * 8;
+    __builtin_amdgcn_global_load_lds((const void*)p, (lds_void*)(dst + ins * RPI * D), 16, 0, 0);
+  }
+  __device__ __forceinline__ static void load(const bf16_t* src, size_t gstride, int n, bf16_t* dst) {
 #pragma unroll
-    for (int it = 0; it < NI; ++it) {
-      const int ins = w * NI + it;
-      const int row = ins * RPI + l / VPR;
-      const bf16_t* p = src + (size_t)(row < n ? row : n - 1) * gstride + (l % VPR) * 8;
-      __builtin_amdgcn_global_load_lds((const void*)p, (lds_void*)(dst + ins * RPI * D), 16, 0, 0);
-    }
+    for (int it = 0; it < NI; ++it) load_one(src, gstride, n, dst, it);
   }
 };
 
