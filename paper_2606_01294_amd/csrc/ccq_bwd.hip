@@ -388,15 +388,6 @@ __global__ __launch_bounds__(kThreads) void gla_dg_kernel(const DgArgs a) {
 // walks the segment's chunks from last to first.  For large DK the 16 x 16
 // tiles of H (and the output columns of ccq_dk_kernel) are split over NSPLIT
 // workgroups per segment; each stages the whole chunk.
-// Product of two 16-wide column blocks of row-major chunk tiles over the
-// chunk's rows: acc += A[:, a0..]^T B[:, b0..], both operands taken with
-// transposing LDS reads (at = A + a0, bt = B + b0).
-template <typename T, int K>
-__device__ __forceinline__ void tile_mma_tr(f32x4& acc, const T* at, int lda, const T* bt, int ldb) {
-#pragma unroll
-  for (int k0 = 0; k0 < K; k0 += 32) mma(acc, ld_frag_tr(at + k0 * lda, lda), ld_frag_tr(bt + k0 * ldb, ldb));
-}
-
 // Both kernels stage q and rho u as row-major chunk tiles (16-byte writes) and
 // read them feature-major with transposing reads where a product runs over the
 // chunk's rows.

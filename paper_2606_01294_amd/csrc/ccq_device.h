@@ -328,6 +328,22 @@ __device__ __forceinline__ void tile_mma(f32x4& acc, const T* a, int lda, const 
   for (int k0 = 0; k0 < K; k0 += 32) mma(acc, ld_frag(a + k0, lda), ld_frag(bt + k0, ldb));
 }
 
+// The same product over the chunk index with operands in row-major chunk
+// tiles (rows = the chunk's tokens): tile_mma_tr takes both operands with
+// transposing LDS reads, acc += A[:, a0..]^T B[:, b0..] (at = A + a0,
+// bt = B + b0); tile_mma_bt only the second, acc += A B for a 16-row block of
+// A and a 16-column block of B (b = B + b0).
+template <typename T, int K>
+__device__ __forceinline__ void tile_mma_tr(f32x4& acc, const T* at, int lda, const T* bt, int ldb) {
+#pragma unroll
+  for (int k0 = 0; k0 < K; k0 += 32) mma(acc, ld_frag_tr(at + k0 * lda, lda), ld_frag_tr(bt + k0 * ldb, ldb));
+}
+template <typename T, int K>
+__device__ __forceinline__ void tile_mma_bt(f32x4& acc, const T* a, int lda, const T* b, int ldb) {
+#pragma unroll
+  for (int k0 = 0; k0 < K; k0 += 32) mma(acc, ld_frag(a + k0, lda), ld_frag_tr(b + k0 * ldb, ldb));
+}
+
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
 template <typename T> __device__ __forceinline__ T to(float x) { return static_cast<T>(x); }

@@ -304,16 +304,15 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
   constexpr int ES = (int)sizeof(T);
   static_assert(BV % 32 == 0 && DK % 32 == 0, "tiles");
 
-  __shared__ __align__(16) T sQT[DK * LDT];  // qc^T (key channel rows)
-  __shared__ __align__(16) T sKT[DK * LDT];
+  __shared__ __align__(16) T sQ[C * LDQ];  // qc rows (kept to the end; read transposed there)
+  __shared__ __align__(16) T sK[C * LDQ];
   __shared__ float sGam[C], sBeta[C], sDec[C];
   __shared__ float sColF[4][C], sColA[4][C], sRV[4][C];
   __shared__ float sDg[C];
   __shared__ float sRed[2][4];
-  constexpr int kR1 = 2 * C * LDQ * ES;
   constexpr int kR2 = 4 * C * LDV * ES + 2 * BV * LDQ * ES;
-  constexpr int kR3 = 4 * C * LDT * ES;
-  constexpr int kR = kR1 > kR2 ? (kR1 > kR3 ? kR1 : kR3) : (kR2 > kR3 ? kR2 : kR3);
+  constexpr int kR3 = 2 * C * LDT * ES;
+  constexpr int kR = kR2 > kR3 ? kR2 : kR3;
   __shared__ __align__(16) char sR[kR];
 
   const int N = (a.T + C - 1) / C;
@@ -331,8 +330,6 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
   // ---- phase 1: Q K^T and K K^T (rows of stripe w, tiles J <= w)
   f32x4 QK[4], KK[4];
   {
-    T* sQ = reinterpret_cast<T*>(sR);
-    T* sK = sQ + C * LDQ;
     ChunkTile<T, DK> rq, rk;
     rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gsk, nrow);
     rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gsk, nrow);
@@ -343,8 +340,6 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
     }
     rq.store(sQ, LDQ);
     rk.store(sK, LDQ);
-    rq.store_t(sQT, LDT);
-    rk.store_t(sKT, LDT);
     lds_barrier();
 #pragma unroll
     for (int J = 0; J < 4; ++J) {
@@ -355,7 +350,6 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
         tile_mma<T, DK>(KK[J], sK + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
       }
     }
-    lds_barrier();  // sQ, sK dead
   }
 
   // ---- phase 2: value slices
@@ -470,9 +464,12 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
           mma(G3[ct], ld_frag(sU + 16 * w * LDV + k0, LDV), ld_frag_tr(sD + k0 * LDQ + 16 * ct, LDQ));
         }
       }
-      for (int idx = tid; idx < DK * BV; idx += kThreads) {
-        const int vl = idx / DK, c = idx % DK;
-        dss += f32(sS[vl * LDQ + c]) * f32(sD[vl * LDQ + c]);
+      for (int idx = tid; idx < DK * BV / 8; idx += kThreads) {
+        const int vl = idx / (DK / 8), c = (idx % (DK / 8)) * 8;
+        const v8 xs = *reinterpret_cast<const v8*>(sS + vl * LDQ + c);
+        const v8 xd = *reinterpret_cast<const v8*>(sD + vl * LDQ + c);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dss += f32(xs[e]) * f32(xd[e]);
       }
       lds_barrier();
     }
@@ -491,10 +488,8 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
     }
 
   // ---- phase 3: C x C weights
-  T* sPm = reinterpret_cast<T*>(sR);
-  T* sPmT = sPm + C * LDT;
-  T* sE = sPmT + C * LDT;
-  T* sET = sE + C * LDT;
+  T* sPm = reinterpret_cast<T*>(sR);  // rows i (the products over i read it transposed)
+  T* sE = sPm + C * LDT;
   float rowF[4] = {0.f, 0.f, 0.f, 0.f}, rowA[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int J = 0; J < 4; ++J) {
@@ -514,9 +509,7 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
       colF += F;
       colA += sBeta[i] * fa;
       sPm[i * LDT + j] = to<T>(pm);
-      sPmT[j * LDT + i] = to<T>(pm);
       sE[i * LDT + j] = to<T>(E);
-      sET[j * LDT + i] = to<T>(E);
     }
     colF += __shfl_xor(colF, 16);
     colF += __shfl_xor(colF, 32);
@@ -542,16 +535,16 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
 #pragma unroll
   for (int ct = 0; ct < NTC; ++ct) {
     f32x4 x = zero4(), y = zero4();
-    tile_mma<T, C>(x, sPm + 16 * w * LDT, LDT, sKT + 16 * ct * LDT, LDT);
-    tile_mma<T, C>(y, sPmT + 16 * w * LDT, LDT, sQT + 16 * ct * LDT, LDT);
-    tile_mma<T, C>(y, sE + 16 * w * LDT, LDT, sKT + 16 * ct * LDT, LDT);
-    tile_mma<T, C>(y, sET + 16 * w * LDT, LDT, sKT + 16 * ct * LDT, LDT);
+    tile_mma_bt<T, C>(x, sPm + 16 * w * LDT, LDT, sK + 16 * ct, LDQ);
+    tile_mma_tr<T, C>(y, sPm + 16 * w, LDT, sQ + 16 * ct, LDQ);
+    tile_mma_bt<T, C>(y, sE + 16 * w * LDT, LDT, sK + 16 * ct, LDQ);
+    tile_mma_tr<T, C>(y, sE + 16 * w, LDT, sK + 16 * ct, LDQ);
     const int c = 16 * ct + c16;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int i = 16 * w + 4 * g4 + r;
       const float G = __expf(sGam[i]);
-      const float qv = f32(sQT[c * LDT + i]), kv = f32(sKT[c * LDT + i]);
+      const float qv = f32(sQ[i * LDQ + c]), kv = f32(sK[i * LDQ + c]);
       const float dq = G * G1[ct][r] + x[r];
       const float dk = y[r] + sDec[i] * G3[ct][r] - sBeta[i] * G * G2[ct][r];
       dot1[r] += G1[ct][r] * qv;
