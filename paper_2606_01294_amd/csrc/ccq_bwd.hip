@@ -51,28 +51,24 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
   static_assert(DK <= kThreads, "one thread per key channel in the scan");
 
   __shared__ float sG[C * LDG];  // inclusive log-decay prefix b
-  __shared__ __align__(16) T sQtT[DK * LDT];
-  __shared__ __align__(16) T sKtT[DK * LDT];
+  // the rescaled Qt and Kt stay as row-major tiles to the end: the products
+  // over the chunk index take them with transposing reads
+  __shared__ __align__(16) T sQt[C * LDQ];
   __shared__ __align__(16) T sKt[C * LDQ];
   __shared__ __align__(16) T sAqkT[C * LDT];  // s (Qt Kt^T masked)^T
   __shared__ float sBm[DK], sBCm[DK];
   // phase-local buffers share one region
-  constexpr int kR1 = C * LDQ * ES;
   constexpr int kOffdS = BV * LDQ * ES, kOffV = kOffdS + BV * LDQ * ES,
-                kOffdO = kOffV + C * LDV * ES, kOffdOT = kOffdO + C * LDV * ES,
-                kR2 = kOffdOT + BV * LDT * ES;
-  constexpr int kR3 = 2 * C * LDT * ES;
+                kOffdO = kOffV + C * LDV * ES, kR2 = kOffdO + C * LDV * ES;
+  constexpr int kR3 = C * LDT * ES;
   constexpr int kR4 = 8 * DK * 4;
-  constexpr int kR = kR1 > kR2 ? (kR1 > kR3 ? kR1 : kR3) : (kR2 > kR3 ? kR2 : kR3);
+  constexpr int kR = kR2 > kR3 ? kR2 : kR3;
   __shared__ __align__(16) char sR[kR > kR4 ? kR : kR4];
-  T* sQt = reinterpret_cast<T*>(sR);
   T* sS = reinterpret_cast<T*>(sR);  // S_r diag(e^{b_m}) slice, rows v
   T* sdS = reinterpret_cast<T*>(sR + kOffdS);  // dS_{r+1} diag(e^{b_C - b_m}) slice, rows v
   T* sV = reinterpret_cast<T*>(sR + kOffV);
   T* sdO = reinterpret_cast<T*>(sR + kOffdO);
-  T* sdOT = reinterpret_cast<T*>(sR + kOffdOT);
-  T* sAdv = reinterpret_cast<T*>(sR);
-  T* sAdvT = reinterpret_cast<T*>(sR + C * LDT * ES);
+  T* sAdv = reinterpret_cast<T*>(sR);  // rows t (the products over t read it transposed)
   float* sTot = reinterpret_cast<float*>(sR);
 
   const int N = (a.T + C - 1) / C;
@@ -124,8 +120,6 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
         const float d = sG[j * LDG + c0 + e] - sG[(C / 2 - 1) * LDG + c0 + e];
         qo[e] = to<T>(f32(xq[e]) * __expf(d));
         ko[e] = to<T>(f32(xk[e]) * __expf(-d));
-        sQtT[(c0 + e) * LDT + j] = qo[e];
-        sKtT[(c0 + e) * LDT + j] = ko[e];
       }
       *reinterpret_cast<typename ChunkTile<T, DK>::vec_t*>(sQt + j * LDQ + c0) = qo;
       *reinterpret_cast<typename ChunkTile<T, DK>::vec_t*>(sKt + j * LDQ + c0) = ko;
@@ -142,7 +136,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
       sAqkT[jj * LDT + i] = to<T>((J <= w && jj <= i) ? a.scale * acc[r] : 0.f);
     }
   }
-  lds_barrier();  // sQt is dead from here on
+  lds_barrier();
 
   // ---- phase 2: loop over value slices
   // X1 = dO S_r diag(e^{b_m}), X2 = V dS_{r+1} diag(e^{b_C - b_m}), Adv = dO V^T
@@ -196,7 +190,6 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
     }
     cur.rv.store(sV, LDV);
     cur.rdo.store(sdO, LDV);
-    cur.rdo.store_t(sdOT, LDT);
     if (vv0 + BV < a.dv) load_slice(cur, vv0 + BV);
     lds_barrier();
 #pragma unroll
@@ -216,7 +209,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
 #pragma unroll
     for (int tn = 0; tn < BV / 16; ++tn) {
       f32x4 acc = zero4();
-      tile_mma<T, C>(acc, sAqkT + 16 * w * LDT, LDT, sdOT + 16 * tn * LDT, LDT);
+      tile_mma_bt<T, C>(acc, sAqkT + 16 * w * LDT, LDT, sdO + 16 * tn, LDV);
       tile_mma<T, DK>(acc, sKt + 16 * w * LDQ, LDQ, sdS + 16 * tn * LDQ, LDQ);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -233,19 +226,17 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int i = 16 * w + 4 * g4 + r, jj = 16 * J + c16;
-      const T val = to<T>((J <= w && jj <= i) ? Adv[J][r] : 0.f);
-      sAdv[i * LDT + jj] = val;
-      sAdvT[jj * LDT + i] = val;
+      sAdv[i * LDT + jj] = to<T>((J <= w && jj <= i) ? Adv[J][r] : 0.f);
     }
   lds_barrier();
   f32x4 Y2[NTC];
 #pragma unroll
   for (int ct = 0; ct < NTC; ++ct) {
-    tile_mma<T, C>(X1[ct], sAdv + 16 * w * LDT, LDT, sKtT + 16 * ct * LDT, LDT);
+    tile_mma_bt<T, C>(X1[ct], sAdv + 16 * w * LDT, LDT, sKt + 16 * ct, LDQ);
     Y2[ct] = zero4();
-    tile_mma<T, C>(Y2[ct], sAdvT + 16 * w * LDT, LDT, sQtT + 16 * ct * LDT, LDT);
+    tile_mma_tr<T, C>(Y2[ct], sAdv + 16 * w, LDT, sQt + 16 * ct, LDQ);
   }
-  lds_barrier();  // sAdv/sAdvT dead: sTot may reuse the region
+  lds_barrier();  // sAdv dead: sTot may reuse the region
 
   // ---- phase 4: epilogue per element (row i of stripe w, key channel c)
   // every global operand of the epilogue requested at once (rows clamped into
