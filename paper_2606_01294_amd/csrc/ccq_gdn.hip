@@ -877,7 +877,9 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
       rq.store(sQ, LDQ);
       rk.store(sK, LDQ);
     }
-    __syncthreads();
+    // (the barriers order LDS only: a __syncthreads() fence would also wait
+    // for the output stores in flight)
+    lds_barrier();
 
     // this wave's S_r (first chunk of the group) and U^T fragments
     // (fragment-native, 1 KB each), issued after the staging of q and k so
@@ -917,7 +919,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
       }
       store4(sP + i * LDP + acc_pos(16 * J + 4 * g4), x[0], x[1], x[2], x[3]);
     }
-    __syncthreads();
+    lds_barrier();
 
 #pragma unroll
     for (int it = 0; it < IPW; ++it) {
@@ -1001,7 +1003,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gdn_out_kernel(const GdnOutArg
         }
       }
     }
-    __syncthreads();  // q, k, P and the coefficients of this chunk released
+    lds_barrier();  // q, k, P and the coefficients of this chunk released
   }
 }
 
