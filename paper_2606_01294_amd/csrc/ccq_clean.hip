@@ -142,7 +142,7 @@ __global__ __launch_bounds__(64 * (DK >= 128 ? 8 : 4), 1) void clean_gram_kernel
         lseg += gC;
         if (l == 0) sDc[par] = __expf(gC);
       }
-      __syncthreads();  // the chunk's weights
+      lds_barrier();  // the chunk's weights
 #pragma unroll
       for (int u = 0; u < RowTile<T, DK, NTG>::NV; ++u)
         if (RowTile<T, DK, NTG>::mine(u)) {
@@ -155,7 +155,7 @@ __global__ __launch_bounds__(64 * (DK >= 128 ? 8 : 4), 1) void clean_gram_kernel
     }
     rk.store(buf, LDK);
     if (c + 1 < cend) load(c + 1);
-    __syncthreads();
+    lds_barrier();  // (LDS only: a __syncthreads() fence would wait for the load just issued)
     if constexpr (DECAY) {  // the sums so far, decayed to this chunk's end
       const float dc = sDc[par];
 #pragma unroll

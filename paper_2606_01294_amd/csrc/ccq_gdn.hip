@@ -283,7 +283,9 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
     }
     if (ci > 0) write_back(ci - 1);
     if (ci + 1 < NL) prefetch(sg, ci + 1);
-    __syncthreads();
+    // the barriers of the step order LDS only: a __syncthreads() fence would
+    // wait for the prefetch just issued and for the stores
+    lds_barrier();
     const T* Kb = sK[buf];
 
     // P = K S_r^T over this wave's features; LDS reads run one row tile ahead
@@ -309,7 +311,7 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_state_kernel(const GdnAr
       // every wave of the slice holds bit-identical P
 #pragma unroll
       for (int J = 0; J < 4; ++J) sX[(w * 4 + J) * 64 + l] = R[J];
-      __syncthreads();
+      lds_barrier();
 #pragma unroll
       for (int J = 0; J < 4; ++J) {
         f32x4 sum = sX[((pr * NH) * 4 + J) * 64 + l];

@@ -110,7 +110,9 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
     if (it + 1 < nch) prefetch(kRev ? ci - 1 : ci + 1);
 #pragma unroll
     for (int tv = 0; tv < NVT; ++tv) Sr[tv] = S[tv];
-    __syncthreads();
+    // orders LDS only: a __syncthreads() fence would wait for the prefetch
+    // just issued and for the state stores
+    lds_barrier();
 
     // gates and keys of this wave's channels: lane = channel c0 + 16 w + c16,
     // tokens 32 m + 8 g4 + e
@@ -258,7 +260,9 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
   f32x4 Sc[NTS][NPT];  // CARRY: this wave's value tiles of S^T, pair order
 
   for (int ci = cb; ci < ce; ++ci) {
-  if (ci > cb) __syncthreads();  // every wave is done with the previous chunk
+  // (the barriers of this loop order LDS only: a __syncthreads() fence would
+  // also wait for the loads in flight and the output stores)
+  if (ci > cb) lds_barrier();  // every wave is done with the previous chunk
   const int r0 = ci * C;
   const int nrow = (sq.len - r0) < C ? (sq.len - r0) : C;
   // past the first segment of the state pass, S_r = local state + the
@@ -281,7 +285,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
     *reinterpret_cast<f32x4*>(dst) = f32x4{f32(x[0]), f32(x[1]), f32(x[2]), f32(x[3])};
     *reinterpret_cast<f32x4*>(dst + 4) = f32x4{f32(x[4]), f32(x[5]), f32(x[6]), f32(x[7])};
   }
-  __syncthreads();
+  lds_barrier();
   {  // inclusive prefix over the chunk, TPC threads per channel
     const int c = tid % DK, part = tid / DK, j0 = part * TOK;
     float x[TOK];
@@ -290,7 +294,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
 #pragma unroll
     for (int j = 1; j < TOK; ++j) x[j] += x[j - 1];
     sTot[part][c] = x[TOK - 1];
-    __syncthreads();
+    lds_barrier();
     float off = 0.f;
 #pragma unroll
     for (int p2 = 0; p2 < TPC - 1; ++p2)
@@ -303,7 +307,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
       if (ent) sBe[c] = (CARRY ? 1.f : bm) * a.cdec[((size_t)bh * N + ci) * DK + c];
     }
   }
-  __syncthreads();
+  lds_barrier();
   if (CARRY && tid < DK) sDc[tid] = __expf(sB[(C - 1) * LDB + tid] - sB[(C / 2 - 1) * LDB + tid]);
   if (a.rk) fk.apply(rk);
   // Qt = q e^{b - b_m}, Kt = k e^{b_m - b}
@@ -321,7 +325,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
     *reinterpret_cast<typename RowTile<T, DK, NT>::vec_t*>(sQt + j * LDQ + cc) = qo;
     *reinterpret_cast<typename RowTile<T, DK, NT>::vec_t*>(sKt + j * LDQ + cc) = ko;
   }
-  __syncthreads();  // sB is dead from here on
+  lds_barrier();  // sB is dead from here on
 
   // masked score tiles, transposed (row j, column i), stored as rows i
 #pragma unroll
@@ -391,7 +395,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
         Sc[vt][2 * m + 1] *= e1;
       }
     }
-    __syncthreads();  // sV and sP are ready
+    lds_barrier();  // sV and sP are ready
     // V in the token order of the accumulator pairs (for both products)
     Frag<T> vf[VPW][2];
 #pragma unroll
@@ -448,7 +452,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
     }
   } else
   for (int vp = 0; vp < a.dv; vp += VP) {
-    if (vp > 0) __syncthreads();  // every wave is done with the previous V slice
+    if (vp > 0) lds_barrier();  // every wave is done with the previous V slice
     {
       RowTile<T, VP, NT> rv;
       rv.load(static_cast<const T*>(a.v) + seq_off(sq, r0, h, a.H, a.dv) + vp, (size_t)a.H * a.dv, nrow);
@@ -481,7 +485,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
         sfr[vt][m] = f;
       }
     }
-    __syncthreads();  // sV and sP are ready
+    lds_barrier();  // sV and sP are ready
 #pragma unroll
     for (int it = 0; it < IPW; ++it) {
       const int I = ig * IPW + it;
