@@ -445,8 +445,11 @@ struct ChunkTile {
 // e / (D / 8), column 8 (e % (D / 8)), so consecutive lanes read consecutive
 // 16- or 32-byte pieces of a row and one wave instruction covers whole rows.
 // Rows >= n read row n - 1 and are zeroed at use, so issuing the loads never
-// waits for data.
-template <typename T, int D, int NT = kThreads>
+// waits for data.  With kWhole, a tile whose rows all lie inside the sequence
+// (n >= 64, uniform over the workgroup) takes a branch without the clamping
+// and the masks (fewer vector instructions per chunk in a loop over chunks;
+// in a kernel that stages one chunk the branch only adds code).
+template <typename T, int D, int NT = kThreads, bool kWhole = false>
 struct RowTile {
   static constexpr int VE = 8;
   static constexpr int VPR = D / VE;                  // vectors per row
@@ -457,6 +460,7 @@ struct RowTile {
   typedef T vec_t __attribute__((ext_vector_type(VE)));
   vec_t v[NV];
   uint32_t ok;  // bit u: vector u exists and its row lies inside the sequence
+  bool full;    // kWhole: every row lies inside the sequence (uniform)
 
   __device__ __forceinline__ static bool mine(int u) { return TOT % NT == 0 || (int)threadIdx.x + NT * u < TOT; }
   __device__ __forceinline__ static int row(int u) { return ((int)threadIdx.x + NT * u) / VPR; }
@@ -464,6 +468,13 @@ struct RowTile {
 
   __device__ __forceinline__ void load(const T* src, size_t gstride, int n) {
     ok = 0;
+    full = kWhole && n >= kChunk;
+    if (full) {  // whole chunk: no clamping (the row offsets do not depend on n)
+#pragma unroll
+      for (int u = 0; u < NV; ++u)
+        if (mine(u)) v[u] = *reinterpret_cast<const vec_t*>(src + (size_t)row(u) * gstride + col(u));
+      return;
+    }
 #pragma unroll
     for (int u = 0; u < NV; ++u) {
       if (!mine(u)) continue;
@@ -476,9 +487,15 @@ struct RowTile {
     vec_t z;
 #pragma unroll
     for (int e = 0; e < VE; ++e) z[e] = static_cast<T>(0.f);
-    return ((ok >> u) & 1u) ? v[u] : z;
+    return (full || ((ok >> u) & 1u)) ? v[u] : z;
   }
   __device__ __forceinline__ void store(T* dst, int ld) const {
+    if (full) {
+#pragma unroll
+      for (int u = 0; u < NV; ++u)
+        if (mine(u)) *reinterpret_cast<vec_t*>(dst + row(u) * ld + col(u)) = v[u];
+      return;
+    }
 #pragma unroll
     for (int u = 0; u < NV; ++u)
       if (mine(u)) *reinterpret_cast<vec_t*>(dst + row(u) * ld + col(u)) = get(u);

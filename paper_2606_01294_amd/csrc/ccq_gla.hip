@@ -73,17 +73,22 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
                 : zero4();
   }
 
-  RowTile<T, BK> rk;
-  RowScales<RowTile<T, BK>> fk;  // raw keys: row scales (l2 normalisation)
-  RowTile<TG, BK> rg;
-  RowTile<T, VB> rv;
-  auto prefetch = [&](int ci) {
+  // a chunk's keys, gates and values, prefetched into registers two chunks
+  // ahead (two sets, alternating)
+  struct Stage {
+    RowTile<T, BK, kThreads, true> rk;
+    RowScales<RowTile<T, BK, kThreads, true>> fk;  // raw keys: row scales (l2 normalisation)
+    RowTile<TG, BK, kThreads, true> rg;
+    RowTile<T, VB, kThreads, true> rv;
+  };
+  Stage sa, sb;
+  auto prefetch = [&](Stage& st, int ci) {
     const int r0 = ci * C;
     const int nrow = (sq.len - r0) < C ? (sq.len - r0) : C;
-    rk.load(k + seq_off(sq, r0, h, a.H, a.dk) + c0, (size_t)a.H * a.dk, nrow);
-    if (a.rk) fk.load(a.rk + seq_idx(sq, r0, h, a.H), (size_t)a.H, nrow);
-    rg.load(gate + seq_off(sq, r0, h, a.H, a.dk) + c0, (size_t)a.H * a.dk, nrow);
-    rv.load(v + seq_off(sq, r0, h, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
+    st.rk.load(k + seq_off(sq, r0, h, a.H, a.dk) + c0, (size_t)a.H * a.dk, nrow);
+    if (a.rk) st.fk.load(a.rk + seq_idx(sq, r0, h, a.H), (size_t)a.H, nrow);
+    st.rg.load(gate + seq_off(sq, r0, h, a.H, a.dk) + c0, (size_t)a.H * a.dk, nrow);
+    st.rv.load(v + seq_off(sq, r0, h, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
   };
   f32x4 Sr[NVT];  // S_r kept for the deferred write-back
   // only the first chunk of each output group (a.group chunks) is read back
@@ -96,18 +101,20 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
       store4(st + (size_t)(16 * tv + c16) * a.dk, Sr[tv][0], Sr[tv][1], Sr[tv][2], Sr[tv][3]);
   };
   const int nch = ce - cb;
-  if (nch > 0) prefetch(kRev ? ce - 1 : cb);
+  auto chunk = [&](int it) { return kRev ? ce - 1 - it : cb + it; };
+  if (nch > 0) prefetch(sa, chunk(0));
+  if (nch > 1) prefetch(sb, chunk(1));
   float le = 0.f;  // log decay of this lane's channel since the segment began
 
-  for (int it = 0; it < nch; ++it) {
-    const int ci = kRev ? ce - 1 - it : cb + it;
+  auto step = [&](Stage& st, int it) {
+    const int ci = chunk(it);
     const int buf = it & 1;  // the other buffer was released at the previous barrier
-    if (a.rk) fk.apply(rk);
-    rk.store(sK[buf], LDK);
-    rg.store(sG[buf], LDG);
-    rv.store(sV[buf], LDV);
+    if (a.rk) st.fk.apply(st.rk);
+    st.rk.store(sK[buf], LDK);
+    st.rg.store(sG[buf], LDG);
+    st.rv.store(sV[buf], LDV);
     if (it > 0) write_back(kRev ? ci + 1 : ci - 1);
-    if (it + 1 < nch) prefetch(kRev ? ci - 1 : ci + 1);
+    if (it + 2 < nch) prefetch(st, chunk(it + 2));
 #pragma unroll
     for (int tv = 0; tv < NVT; ++tv) Sr[tv] = S[tv];
     // orders LDS only: a __syncthreads() fence would wait for the prefetch
@@ -162,6 +169,10 @@ __global__ __launch_bounds__(kThreads, 1) void gla_state_kernel(const GlaStateAr
       mma(S[tv], kd0, ld_frag_tr(sV[buf] + 16 * tv, LDV));
       mma(S[tv], kd1, ld_frag_tr(sV[buf] + 32 * LDV + 16 * tv, LDV));
     }
+  };
+  for (int it = 0; it < nch; it += 2) {
+    step(sa, it);
+    if (it + 1 < nch) step(sb, it + 1);
   }
 
   if (nch > 0) write_back(kRev ? cb : ce - 1);
