@@ -270,6 +270,78 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
   constexpr int NTS = CARRY ? VPW : 1, NPT = CARRY ? 2 * NK : 1;
   f32x4 Sc[NTS][NPT];  // CARRY: this wave's value tiles of S^T, pair order
 
+  // a chunk's q_clean, keys and gates (and, CARRY, values).  CARRY loads each
+  // tile of the next chunk as soon as the current chunk is done with its own,
+  // so that the loads are in flight while the products run.
+  RowTile<T, DK, NT, CARRY> rq, rk;
+  RowScales<RowTile<T, DK, NT, CARRY>> fk;  // raw keys: row scales (l2 normalisation)
+  RowTile<TG, DK, NT, CARRY> rg;
+  RowTile<T, VP, NT, CARRY> rv;
+  const Seq sw{(long long)b * a.T, sq.len};  // q_clean: the workspace's padded rows
+  auto rows = [&](int c) { return (sq.len - c * C) < C ? (sq.len - c * C) : C; };
+  auto load_qk = [&](int c) {
+    rq.load(static_cast<const T*>(a.qc) + seq_off(sw, c * C, h, a.H, DK), gstride, rows(c));
+    rk.load(static_cast<const T*>(a.k) + seq_off(sq, c * C, h, a.H, DK), gstride, rows(c));
+    if (a.rk) fk.load(a.rk + seq_idx(sq, c * C, h, a.H), (size_t)a.H, rows(c));
+  };
+  auto load_g = [&](int c) { rg.load(static_cast<const TG*>(a.g) + seq_off(sq, c * C, h, a.H, DK), gstride, rows(c)); };
+  auto load_v = [&](int c) {
+    rv.load(static_cast<const T*>(a.v) + seq_off(sq, c * C, h, a.H, a.dv), (size_t)a.H * a.dv, rows(c));
+  };
+  if constexpr (CARRY) {
+    // S_r of the group's first chunk plus the segment's entry state decayed to
+    // it, requested before the chunk's inputs so that the two latencies
+    // overlap: lane (g, j) of value tile vt reads channels 32 m + 8 g .. + 7 of
+    // value row 16 vt' + j, which are rows 4 g .. 4 g + 3 of tiles 2 m and 2 m + 1
+    const int sg0 = a.seg > 0 ? cb / a.seg : 0;
+    const bool ent0 = sg0 > 0 && a.entries;
+    const T* Sg = static_cast<const T*>(a.states) + ((size_t)bh * N + cb) * a.dv * DK;
+    const int NS = a.seg > 0 ? (N + a.seg - 1) / a.seg : 1;
+    const T* Eg = static_cast<const T*>(a.entries) + ((size_t)bh * NS + sg0) * a.dv * DK;
+    const float* cd = a.cdec + ((size_t)bh * N + cb) * DK;  // decay since the segment began
+    Frag<T> fs[VPW][NK], fe[VPW][NK];
+    f32x4 de[NK][2];
+#pragma unroll
+    for (int vt = 0; vt < VPW; ++vt)
+#pragma unroll
+      for (int m = 0; m < NK; ++m) fs[vt][m] = ld_frag_global(Sg + (size_t)(16 * (vg * VPW + vt)) * DK + 32 * m, (size_t)DK);
+    if (ent0) {
+#pragma unroll
+      for (int m = 0; m < NK; ++m) {
+        de[m][0] = *reinterpret_cast<const f32x4*>(cd + 32 * m + 8 * g4);
+        de[m][1] = *reinterpret_cast<const f32x4*>(cd + 32 * m + 8 * g4 + 4);
+      }
+#pragma unroll
+      for (int vt = 0; vt < VPW; ++vt)
+#pragma unroll
+        for (int m = 0; m < NK; ++m)
+          fe[vt][m] = ld_frag_global(Eg + (size_t)(16 * (vg * VPW + vt)) * DK + 32 * m, (size_t)DK);
+    }
+    load_g(cb);
+    load_qk(cb);
+    load_v(cb);
+#pragma unroll
+    for (int vt = 0; vt < VPW; ++vt)
+#pragma unroll
+      for (int m = 0; m < NK; ++m) {
+        f32x4 x, y;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          x[r] = frag_elem(fs[vt][m], r);
+          y[r] = frag_elem(fs[vt][m], 4 + r);
+        }
+        if (ent0) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            x[r] += frag_elem(fe[vt][m], r) * de[m][0][r];
+            y[r] += frag_elem(fe[vt][m], 4 + r) * de[m][1][r];
+          }
+        }
+        Sc[vt][2 * m] = x;
+        Sc[vt][2 * m + 1] = y;
+      }
+  }
+
   for (int ci = cb; ci < ce; ++ci) {
   // (the barriers of this loop order LDS only: a __syncthreads() fence would
   // also wait for the loads in flight and the output stores)
@@ -281,14 +353,10 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
   const int sg = a.seg > 0 ? ci / a.seg : 0;
   const bool ent = sg > 0 && a.entries;
 
-  RowTile<T, DK, NT> rq, rk;
-  RowScales<RowTile<T, DK, NT>> fk;  // raw keys: row scales (l2 normalisation)
-  RowTile<TG, DK, NT> rg;
-  const Seq sw{(long long)b * a.T, sq.len};  // q_clean: the workspace's padded rows
-  rq.load(static_cast<const T*>(a.qc) + seq_off(sw, r0, h, a.H, DK), gstride, nrow);
-  rk.load(static_cast<const T*>(a.k) + seq_off(sq, r0, h, a.H, DK), gstride, nrow);
-  if (a.rk) fk.load(a.rk + seq_idx(sq, r0, h, a.H), (size_t)a.H, nrow);
-  rg.load(static_cast<const TG*>(a.g) + seq_off(sq, r0, h, a.H, DK), gstride, nrow);
+  if constexpr (!CARRY) {
+    load_qk(ci);
+    load_g(ci);
+  }
 #pragma unroll
   for (int u = 0; u < RowTile<TG, DK, NT>::NV; ++u) {  // gates as fp32 rows
     const auto x = rg.get(u);
@@ -296,6 +364,8 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
     *reinterpret_cast<f32x4*>(dst) = f32x4{f32(x[0]), f32(x[1]), f32(x[2]), f32(x[3])};
     *reinterpret_cast<f32x4*>(dst + 4) = f32x4{f32(x[4]), f32(x[5]), f32(x[6]), f32(x[7])};
   }
+  if constexpr (CARRY)
+    if (ci + 1 < ce) load_g(ci + 1);
   lds_barrier();
   {  // inclusive prefix over the chunk, TPC threads per channel
     const int c = tid % DK, part = tid / DK, j0 = part * TOK;
@@ -315,7 +385,7 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
     if (j0 <= C / 2 - 1 && C / 2 - 1 < j0 + TOK) {
       const float bm = __expf(x[C / 2 - 1 - j0] + off);
       sBm[c] = bm;
-      if (ent) sBe[c] = (CARRY ? 1.f : bm) * a.cdec[((size_t)bh * N + ci) * DK + c];
+      if (!CARRY && ent) sBe[c] = bm * a.cdec[((size_t)bh * N + ci) * DK + c];
     }
   }
   lds_barrier();
@@ -336,6 +406,8 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
     *reinterpret_cast<typename RowTile<T, DK, NT>::vec_t*>(sQt + j * LDQ + cc) = qo;
     *reinterpret_cast<typename RowTile<T, DK, NT>::vec_t*>(sKt + j * LDQ + cc) = ko;
   }
+  if constexpr (CARRY)
+    if (ci + 1 < ce) load_qk(ci + 1);
   lds_barrier();  // sB is dead from here on
 
   // masked score tiles, transposed (row j, column i), stored as rows i
@@ -359,42 +431,8 @@ __global__ __launch_bounds__(kOutThreads, 1) void gla_out_kernel(const GlaOutArg
   const T* Eg = ent ? static_cast<const T*>(a.entries) + ((size_t)bh * NS + sg) * a.dv * DK : nullptr;
   T* o = static_cast<T*>(a.o);
   if constexpr (CARRY) {
-    {
-      RowTile<T, VP, NT> rv;
-      rv.load(static_cast<const T*>(a.v) + seq_off(sq, r0, h, a.H, a.dv), (size_t)a.H * a.dv, nrow);
-      rv.store(sV, LDV);
-    }
-    if (ci == cb) {
-      // S_r of the group's first chunk (plus the segment entry decayed to it):
-      // lane (g, j) of value tile vt reads channels 32 m + 8 g .. + 7 of value
-      // row 16 vt' + j, which are rows 4 g .. 4 g + 3 of tiles 2 m and 2 m + 1
-#pragma unroll
-      for (int vt = 0; vt < VPW; ++vt) {
-        const int vr = 16 * (vg * VPW + vt);
-#pragma unroll
-        for (int m = 0; m < NK; ++m) {
-          const Frag<T> f = ld_frag_global(Sg + (size_t)vr * DK + 32 * m, (size_t)DK);
-          f32x4 x, y;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            x[r] = frag_elem(f, r);
-            y[r] = frag_elem(f, 4 + r);
-          }
-          if (ent) {
-            const Frag<T> fe = ld_frag_global(Eg + (size_t)vr * DK + 32 * m, (size_t)DK);
-            const f32x4 d0 = *reinterpret_cast<const f32x4*>(sBe + 32 * m + 8 * g4);
-            const f32x4 d1 = *reinterpret_cast<const f32x4*>(sBe + 32 * m + 8 * g4 + 4);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              x[r] += frag_elem(fe, r) * d0[r];
-              y[r] += frag_elem(fe, 4 + r) * d1[r];
-            }
-          }
-          Sc[vt][2 * m] = x;
-          Sc[vt][2 * m + 1] = y;
-        }
-      }
-    }
+    rv.store(sV, LDV);
+    if (ci + 1 < ce) load_v(ci + 1);
     // S^T diag(e^{b_m}) in place, the output's operand
 #pragma unroll
     for (int m = 0; m < NK; ++m) {
