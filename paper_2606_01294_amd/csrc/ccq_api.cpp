@@ -425,6 +425,9 @@ ccq_status gdn_fwd_bwd(const ccq_shape* s, const void* q, const void* k, const v
   if (traced(st, [&] { return ccq::launch_gdn_state(sa, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   ccq::GdnOutArgs oa{ws + L.qclean, k, gam, ws + L.states, ws + L.U, o, s->B, s->T, s->H, s->dk,
                      s->dv, s->scale};
+  // every S_r is stored (the backward reads them); the output kernel still
+  // reads only each group's first and carries S through the group
+  oa.group = ccq::gdn_out_group(s->B, s->H, s->T, s->dk, s->dv, bf);
   if (traced(st, [&] { return ccq::launch_gdn_out(oa, bf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   // backward: PT and Tm^T, the reverse state scan, chunk gradients, dq, dk
   ccq::GdnPrepArgs pa{ws + L.qclean, k, gam, ws + L.Tm, ws + L.PT, ws + L.TmT, s->B, s->T, s->H,
@@ -748,6 +751,9 @@ ccq_status ccq_fwd_bwd(const ccq_shape* s, ccq_backbone bb, const void* q, const
   if (traced(st, [&] { return ccq::launch_gla_state(sa, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   ccq::GlaOutArgs oa{ws + L.qclean, k, v, g_or_logalpha, ws + L.states, o, s->B, s->T, s->H, s->dk,
                      s->dv, s->scale};
+  // every S_r is stored (the backward reads them); the output kernel still
+  // reads only each group's first and carries S through the group
+  oa.group = ccq::gla_out_group(s->B, s->H, s->T, s->dk, s->dv, bf);
   if (traced(st, [&] { return ccq::launch_gla_out(oa, bf, gbf, st); }) != hipSuccess) return CCQ_ERR_HIP;
   // backward: dS scan, chunk gradients, decay gradient, dq, dk
   ccq::DstateArgs da{ws + L.qclean, g_or_logalpha, dO, ws + L.dstates, s->B, s->T, s->H, s->dk,
