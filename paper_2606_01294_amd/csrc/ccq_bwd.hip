@@ -40,15 +40,20 @@ namespace ccq {
 // ----------------------------------------------------------------------------
 // One workgroup per chunk: dqc, the GLA part of dk, dv, the decay gradient
 // db, dlam and the decay gradient at the next chunk's first token, looping
-// over BV-wide slices of the value dimension.
-template <typename T, typename TG, int DK, int BV>
-__global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwdArgs a) {
-  constexpr int C = kChunk;
+// over BV-wide slices of the value dimension.  Wave w owns the 16-row stripe
+// w % 4 of the chunk; with eight waves (NW = 8) the two waves of a stripe
+// split its key-channel tiles (and the stripe's dO V^T tiles, the dv tiles
+// and the intra block's tiles), so that every SIMD holds two waves.
+template <typename T, typename TG, int DK, int BV, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void gla_bwd_chunk_kernel(const GlaBwdArgs a) {
+  constexpr int C = kChunk, NT = 64 * NW;
+  constexpr int HW = NW / 4;  // waves per stripe
   constexpr int P = Pad<T>::value;
   constexpr int LDQ = DK + P, LDT = C + P, LDG = DK + 1, LDV = BV + P;
-  constexpr int NTC = DK / 16;
+  constexpr int NTC = DK / 16, NTW = NTC / HW;  // key-channel tiles, per wave
   constexpr int ES = (int)sizeof(T);
-  static_assert(DK <= kThreads, "one thread per key channel in the scan");
+  static_assert((NW == 4 || NW == 8) && NTW * HW == NTC && (BV / 16) % HW == 0, "wave split");
+  static_assert(DK <= NT, "one thread per key channel in the scan");
 
   __shared__ float sG[C * LDG];  // inclusive log-decay prefix b
   // the rescaled Qt and Kt stay as row-major tiles to the end: the products
@@ -57,11 +62,12 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
   __shared__ __align__(16) T sKt[C * LDQ];
   __shared__ __align__(16) T sAqkT[C * LDT];  // s (Qt Kt^T masked)^T
   __shared__ float sBm[DK], sBCm[DK];
+  __shared__ float sDl[HW > 1 ? C : 1];  // the second half's share of dlam
   // phase-local buffers share one region
   constexpr int kOffdS = BV * LDQ * ES, kOffV = kOffdS + BV * LDQ * ES,
                 kOffdO = kOffV + C * LDV * ES, kR2 = kOffdO + C * LDV * ES;
   constexpr int kR3 = C * LDT * ES;
-  constexpr int kR4 = 8 * DK * 4;
+  constexpr int kR4 = (4 + NW) * DK * 4;
   constexpr int kR = kR2 > kR3 ? kR2 : kR3;
   __shared__ __align__(16) char sR[kR > kR4 ? kR : kR4];
   T* sS = reinterpret_cast<T*>(sR);  // S_r diag(e^{b_m}) slice, rows v
@@ -77,7 +83,9 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
   const int b = bh / a.H, h = bh % a.H;
   const int r0 = ci * C;
   const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-  const int tid = threadIdx.x, w = wave_id(), l = lane_id();
+  const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6), l = lane_id();
+  const int sw = w & 3, hh = w >> 2;  // stripe, half (uniform)
+  const int ct0 = hh * NTW;           // this wave's first key-channel tile
   const int g4 = l >> 4, c16 = l & 15;
   const T* qc = static_cast<const T*>(a.qc);
   const T* k = static_cast<const T*>(a.k);
@@ -90,8 +98,8 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
 
   // ---- phase 1: decay prefix, rescaled Qt / Kt, intra block
   {
-    ChunkTile<T, DK> rq, rk;
-    ChunkTile<TG, DK> rg;
+    ChunkTile<T, DK, NT> rq, rk;
+    ChunkTile<TG, DK, NT> rg;
     rq.load(qc + tok_off(b, r0, h, a.T, a.H, DK), gsk, nrow);
     rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), gsk, nrow);
     rg.load(gate + tok_off(b, r0, h, a.T, a.H, DK), gsk, nrow);
@@ -109,55 +117,57 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
       sBCm[tid] = __expf(x[C - 1] - x[C / 2 - 1]);
     }
     lds_barrier();
-    const int j = ChunkTile<T, DK>::row();
+    const int j = ChunkTile<T, DK, NT>::row();
 #pragma unroll
-    for (int u = 0; u < ChunkTile<T, DK>::NV; ++u) {
-      const int c0 = ChunkTile<T, DK>::col(u);
+    for (int u = 0; u < ChunkTile<T, DK, NT>::NV; ++u) {
+      const int c0 = ChunkTile<T, DK, NT>::col(u);
       const auto xq = rq.get(u), xk = rk.get(u);
-      typename ChunkTile<T, DK>::vec_t qo, ko;
+      typename ChunkTile<T, DK, NT>::vec_t qo, ko;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float d = sG[j * LDG + c0 + e] - sG[(C / 2 - 1) * LDG + c0 + e];
         qo[e] = to<T>(f32(xq[e]) * __expf(d));
         ko[e] = to<T>(f32(xk[e]) * __expf(-d));
       }
-      *reinterpret_cast<typename ChunkTile<T, DK>::vec_t*>(sQt + j * LDQ + c0) = qo;
-      *reinterpret_cast<typename ChunkTile<T, DK>::vec_t*>(sKt + j * LDQ + c0) = ko;
+      *reinterpret_cast<typename ChunkTile<T, DK, NT>::vec_t*>(sQt + j * LDQ + c0) = qo;
+      *reinterpret_cast<typename ChunkTile<T, DK, NT>::vec_t*>(sKt + j * LDQ + c0) = ko;
     }
   }
   lds_barrier();
 #pragma unroll
   for (int J = 0; J < 4; ++J) {
+    if (J % HW != hh) continue;  // the stripe's other wave takes it
     f32x4 acc = zero4();
-    if (J <= w) tile_mma<T, DK>(acc, sQt + 16 * w * LDQ, LDQ, sKt + 16 * J * LDQ, LDQ);
+    if (J <= sw) tile_mma<T, DK>(acc, sQt + 16 * sw * LDQ, LDQ, sKt + 16 * J * LDQ, LDQ);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int i = 16 * w + 4 * g4 + r, jj = 16 * J + c16;
-      sAqkT[jj * LDT + i] = to<T>((J <= w && jj <= i) ? a.scale * acc[r] : 0.f);
+      const int i = 16 * sw + 4 * g4 + r, jj = 16 * J + c16;
+      sAqkT[jj * LDT + i] = to<T>((J <= sw && jj <= i) ? a.scale * acc[r] : 0.f);
     }
   }
   lds_barrier();
 
   // ---- phase 2: loop over value slices
   // X1 = dO S_r diag(e^{b_m}), X2 = V dS_{r+1} diag(e^{b_C - b_m}), Adv = dO V^T
-  f32x4 X1[NTC], X2[NTC], Adv[4];
+  // (this wave's key-channel tiles ct0 .. ct0 + NTW - 1 and dO V^T tiles J % HW = hh)
+  f32x4 X1[NTW], X2[NTW], Adv[4];
 #pragma unroll
-  for (int ct = 0; ct < NTC; ++ct) { X1[ct] = zero4(); X2[ct] = zero4(); }
+  for (int ct = 0; ct < NTW; ++ct) { X1[ct] = zero4(); X2[ct] = zero4(); }
 #pragma unroll
   for (int J = 0; J < 4; ++J) Adv[J] = zero4();
   T* dvrow = static_cast<T*>(a.dv_out) + tok_off(b, r0, h, a.T, a.H, a.dv);
   // every value slice's global operands are requested one slice ahead
   typedef T v8 __attribute__((ext_vector_type(8)));
-  constexpr int NPS = BV * DK / 8 / kThreads;  // 8-element pieces of S_r (and dS) per thread
-  static_assert(NPS >= 1 && BV * DK / 8 % kThreads == 0, "piece split");
+  constexpr int NPS = BV * DK / 8 / NT;  // 8-element pieces of S_r (and dS) per thread
+  static_assert(NPS >= 1 && BV * DK / 8 % NT == 0, "piece split");
   struct Slice {
     v8 s[NPS], d[NPS];
-    ChunkTile<T, BV> rv, rdo;
+    ChunkTile<T, BV, NT> rv, rdo;
   };
   auto load_slice = [&](Slice& sl, int vv0) {
 #pragma unroll
     for (int p = 0; p < NPS; ++p) {
-      const int idx = tid + p * kThreads, row = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
+      const int idx = tid + p * NT, row = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
       sl.s[p] = *reinterpret_cast<const v8*>(Sst + (size_t)(vv0 + row) * DK + c0);
       sl.d[p] = *reinterpret_cast<const v8*>(dSst + (size_t)(vv0 + row) * DK + c0);
     }
@@ -168,7 +178,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
   load_slice(cur, 0);
   // sum_v S_r[c][v] dS_{r+1}[c][v] for this thread's 8 channels (every piece
   // of a thread covers the same channels)
-  static_assert(kThreads % (DK / 8) == 0, "channels per thread");
+  static_assert(NT % (DK / 8) == 0, "channels per thread");
   float rdot[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) rdot[e] = 0.f;
@@ -177,7 +187,7 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
     // products over v read them with transposing LDS reads
 #pragma unroll
     for (int p = 0; p < NPS; ++p) {
-      const int idx = tid + p * kThreads, row = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
+      const int idx = tid + p * NT, row = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
       v8 s_scaled, ds_scaled;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -194,26 +204,27 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
     lds_barrier();
 #pragma unroll
     for (int k0 = 0; k0 < BV; k0 += 32) {
-      const Frag<T> fo = ld_frag(sdO + 16 * w * LDV + k0, LDV);
-      const Frag<T> fv = ld_frag(sV + 16 * w * LDV + k0, LDV);
+      const Frag<T> fo = ld_frag(sdO + 16 * sw * LDV + k0, LDV);
+      const Frag<T> fv = ld_frag(sV + 16 * sw * LDV + k0, LDV);
 #pragma unroll
-      for (int ct = 0; ct < NTC; ++ct) {
-        mma(X1[ct], fo, ld_frag_tr(sS + k0 * LDQ + 16 * ct, LDQ));
-        mma(X2[ct], fv, ld_frag_tr(sdS + k0 * LDQ + 16 * ct, LDQ));
+      for (int ct = 0; ct < NTW; ++ct) {
+        mma(X1[ct], fo, ld_frag_tr(sS + k0 * LDQ + 16 * (ct0 + ct), LDQ));
+        mma(X2[ct], fv, ld_frag_tr(sdS + k0 * LDQ + 16 * (ct0 + ct), LDQ));
       }
     }
 #pragma unroll
     for (int J = 0; J < 4; ++J)
-      if (J <= w) tile_mma<T, BV>(Adv[J], sdO + 16 * w * LDV, LDV, sV + 16 * J * LDV, LDV);
-    // dv = s (Qt Kt^T masked)^T dO + Kt (dS e^{b_C - b_m})^T  for rows of stripe w
+      if (J <= sw && J % HW == hh) tile_mma<T, BV>(Adv[J], sdO + 16 * sw * LDV, LDV, sV + 16 * J * LDV, LDV);
+    // dv = s (Qt Kt^T masked)^T dO + Kt (dS e^{b_C - b_m})^T  for rows of stripe sw
 #pragma unroll
-    for (int tn = 0; tn < BV / 16; ++tn) {
+    for (int tq = 0; tq < BV / 16 / HW; ++tq) {
+      const int tn = HW * tq + hh;
       f32x4 acc = zero4();
-      tile_mma_bt<T, C>(acc, sAqkT + 16 * w * LDT, LDT, sdO + 16 * tn, LDV);
-      tile_mma<T, DK>(acc, sKt + 16 * w * LDQ, LDQ, sdS + 16 * tn * LDQ, LDQ);
+      tile_mma_bt<T, C>(acc, sAqkT + 16 * sw * LDT, LDT, sdO + 16 * tn, LDV);
+      tile_mma<T, DK>(acc, sKt + 16 * sw * LDQ, LDQ, sdS + 16 * tn * LDQ, LDQ);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int jr = 16 * w + 4 * g4 + r;
+        const int jr = 16 * sw + 4 * g4 + r;
         if (jr < nrow) dvrow[jr * gsv + vv0 + 16 * tn + c16] = to<T>(acc[r]);
       }
     }
@@ -222,23 +233,25 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
 
   // ---- phase 3: intra terms with A_dv[t][j] = dO_t . v_j (j <= t)
 #pragma unroll
-  for (int J = 0; J < 4; ++J)
+  for (int J = 0; J < 4; ++J) {
+    if (J % HW != hh) continue;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int i = 16 * w + 4 * g4 + r, jj = 16 * J + c16;
-      sAdv[i * LDT + jj] = to<T>((J <= w && jj <= i) ? Adv[J][r] : 0.f);
+      const int i = 16 * sw + 4 * g4 + r, jj = 16 * J + c16;
+      sAdv[i * LDT + jj] = to<T>((J <= sw && jj <= i) ? Adv[J][r] : 0.f);
     }
+  }
   lds_barrier();
-  f32x4 Y2[NTC];
+  f32x4 Y2[NTW];
 #pragma unroll
-  for (int ct = 0; ct < NTC; ++ct) {
-    tile_mma_bt<T, C>(X1[ct], sAdv + 16 * w * LDT, LDT, sKt + 16 * ct, LDQ);
+  for (int ct = 0; ct < NTW; ++ct) {
+    tile_mma_bt<T, C>(X1[ct], sAdv + 16 * sw * LDT, LDT, sKt + 16 * (ct0 + ct), LDQ);
     Y2[ct] = zero4();
-    tile_mma_tr<T, C>(Y2[ct], sAdv + 16 * w, LDT, sQt + 16 * ct, LDQ);
+    tile_mma_tr<T, C>(Y2[ct], sAdv + 16 * sw, LDT, sQt + 16 * (ct0 + ct), LDQ);
   }
   lds_barrier();  // sAdv dead: sTot may reuse the region
 
-  // ---- phase 4: epilogue per element (row i of stripe w, key channel c)
+  // ---- phase 4: epilogue per element (row i of stripe sw, key channel c)
   // every global operand of the epilogue requested at once (rows clamped into
   // the sequence), then the per-element arithmetic
   const size_t rowoff = tok_off(b, r0, h, a.T, a.H, DK);
@@ -246,27 +259,27 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
   float* dqc_f = a.dqc + rowoff;
   float* dkg_f = a.dk_gla + rowoff;
   float* db_f = a.db + rowoff;
-  float qv[NTC][4], kv[NTC][4], cv[NTC][4];
+  float qv[NTW][4], kv[NTW][4], cv[NTW][4];
 #pragma unroll
-  for (int ct = 0; ct < NTC; ++ct)
+  for (int ct = 0; ct < NTW; ++ct)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int i = 16 * w + 4 * g4 + r;
-      const int off = (i < nrow ? i : nrow - 1) * (int)gsk + 16 * ct + c16;
+      const int i = 16 * sw + 4 * g4 + r;
+      const int off = (i < nrow ? i : nrow - 1) * (int)gsk + 16 * (ct0 + ct) + c16;
       qv[ct][r] = f32(qc[rowoff + off]);
       kv[ct][r] = f32(k[rowoff + off]);
       cv[ct][r] = a.corr[rowoff + off];
     }
-  float kdk[NTC];  // sum over the chunk's rows of k * dk^inter
+  float kdk[NTW];  // sum over the chunk's rows of k * dk^inter
   float dl[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int ct = 0; ct < NTC; ++ct) {
+  for (int ct = 0; ct < NTW; ++ct) {
     kdk[ct] = 0.f;
-    const int c = 16 * ct + c16;
+    const int c = 16 * (ct0 + ct) + c16;
     const float bm = sG[(C / 2 - 1) * LDG + c];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int i = 16 * w + 4 * g4 + r;
+      const int i = 16 * sw + 4 * g4 + r;
       if (i < nrow) {
         const float d = sG[i * LDG + c] - bm;
         const float dqc = a.scale * __expf(d) * X1[ct][r];
@@ -283,22 +296,35 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
       }
     }
   }
+  // dlam: this wave's channels summed over the 16-lane row group, then (two
+  // waves per stripe) the second half's share added through LDS
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const float s = row16_sum(dl[r]);
-    const int i = 16 * w + 4 * g4 + r;
-    if (c16 == 0 && i < nrow) a.dlam[((size_t)b * a.T + r0 + i) * a.H + h] = s;
+  for (int r = 0; r < 4; ++r) dl[r] = row16_sum(dl[r]);
+  if constexpr (HW > 1) {
+    if (hh == 1 && c16 == 0)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sDl[16 * sw + 4 * g4 + r] = dl[r];
+    lds_barrier();
+    if (hh == 0)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dl[r] += sDl[16 * sw + 4 * g4 + r];
   }
+  if (hh == 0)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = 16 * sw + 4 * g4 + r;
+      if (c16 == 0 && i < nrow) a.dlam[((size_t)b * a.T + r0 + i) * a.H + h] = dl[r];
+    }
   // decay gradient at the next chunk's first token:
   //   e^{b_C} sum_v S_r dS_{r+1} + sum_j k_j * dk_j^inter
   // (zero after the last chunk, where dS_{r+1} = 0); wave sums in a fixed order
   float* sRow = sTot + 4 * DK;
 #pragma unroll
-  for (int ct = 0; ct < NTC; ++ct) {
+  for (int ct = 0; ct < NTW; ++ct) {
     float x = kdk[ct];
     x += __shfl_xor(x, 16);
     x += __shfl_xor(x, 32);
-    if (g4 == 0) sTot[w * DK + 16 * ct + c16] = x;
+    if (g4 == 0) sTot[sw * DK + 16 * (ct0 + ct) + c16] = x;
   }
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -313,7 +339,9 @@ __global__ __launch_bounds__(kThreads, 1) void gla_bwd_chunk_kernel(const GlaBwd
   lds_barrier();
   if (tid < DK) {
     const float kd = sTot[tid] + sTot[DK + tid] + sTot[2 * DK + tid] + sTot[3 * DK + tid];
-    const float sd = sRow[tid] + sRow[DK + tid] + sRow[2 * DK + tid] + sRow[3 * DK + tid];
+    float sd = 0.f;
+#pragma unroll
+    for (int ww = 0; ww < NW; ++ww) sd += sRow[ww * DK + tid];
     a.dg_next[((size_t)bh * N + ci) * DK + tid] = __expf(sG[(C - 1) * LDG + tid]) * sd + kd;
   }
 }
@@ -784,11 +812,11 @@ __global__ __launch_bounds__(64 * NWV, 1) void ccq_dk_kernel(const CcqDkArgs a) 
 
 // ----------------------------------------------------------------------------
 namespace {
-template <typename T, typename TG, int DK, int BV>
+template <typename T, typename TG, int DK, int BV, int NW = 4>
 hipError_t run_bwd_chunk(const GlaBwdArgs& a, hipStream_t st) {
   const int nblk = a.B * a.H * ((a.T + kChunk - 1) / kChunk);
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL((gla_bwd_chunk_kernel<T, TG, DK, BV>), dim3(nblk), dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((gla_bwd_chunk_kernel<T, TG, DK, BV, NW>), dim3(nblk), dim3(64 * NW), 0, st, a);
   return hipGetLastError();
 }
 template <typename T, int DK>
@@ -822,7 +850,9 @@ template <typename T, typename TG>
 hipError_t chunk_dispatch(const GlaBwdArgs& a, hipStream_t st) {
   if constexpr (sizeof(T) == 2) {
     if (a.dk == 64) return run_bwd_chunk<T, TG, 64, 32>(a, st);
-    if (a.dk == 128) return run_bwd_chunk<T, TG, 128, 32>(a, st);
+    // eight waves (two per SIMD: the kernel takes a compute unit's LDS) and
+    // 64-wide value slices at dk = 128
+    if (a.dk == 128) return run_bwd_chunk<T, TG, 128, 64, 8>(a, st);
   } else {
     if (a.dk == 64) return run_bwd_chunk<T, TG, 64, 32>(a, st);
   }
