@@ -291,25 +291,32 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_dstate_kernel(const GdnD
 }
 
 // ----------------------------------------------------------------------------
-// One workgroup per chunk (four waves, wave w owning token rows 16w..16w+15):
-// the C x C products Q K^T and K K^T, then a loop over BV-wide value slices
+// One workgroup per chunk (wave w owning token rows 16 (w % 4) .. + 15): the
+// C x C products Q K^T and K K^T, then a loop over BV-wide value slices
 // accumulating G1 = dO' S_r, G2 = dR S_r, G3 = U D, dO' U^T and dR U^T, then
-// the C x C-weighted sums and the per-element and per-row epilogue.
-template <typename T, int DK, int BV>
-__global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwdArgs a) {
-  constexpr int C = kChunk;
+// the C x C-weighted sums and the per-element and per-row epilogue.  With
+// eight waves (NW = 8) the two waves of a stripe split its key-channel tiles
+// and its C x C tiles (J of the same parity as the wave's half); their
+// per-row sums meet through LDS.
+template <typename T, int DK, int BV, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void gdn_bwd_chunk_kernel(const GdnBwdArgs a) {
+  constexpr int C = kChunk, NT = 64 * NW;
+  constexpr int HW = NW / 4;  // waves per stripe
+  constexpr int NJ = 4 / HW;  // C x C tiles J of a wave: J = HW jj + hh
   constexpr int P = Pad<T>::value;
   constexpr int LDQ = DK + P, LDT = C + P, LDV = BV + P;
-  constexpr int NTC = DK / 16;
+  constexpr int NTC = DK / 16, NTW = NTC / HW;  // key-channel tiles, per wave
   constexpr int ES = (int)sizeof(T);
   static_assert(BV % 32 == 0 && DK % 32 == 0, "tiles");
+  static_assert((NW == 4 || NW == 8) && NTW * HW == NTC, "wave split");
 
   __shared__ __align__(16) T sQ[C * LDQ];  // qc rows (kept to the end; read transposed there)
   __shared__ __align__(16) T sK[C * LDQ];
   __shared__ float sGam[C], sBeta[C], sDec[C];
-  __shared__ float sColF[4][C], sColA[4][C], sRV[4][C];
+  __shared__ float sColF[4][C], sColA[4][C], sRV[C];
   __shared__ float sDg[C];
-  __shared__ float sRed[2][4];
+  __shared__ float sRed[2][NW];
+  __shared__ float sHalf[HW > 1 ? 6 : 1][C];  // the second half's per-row sums
   constexpr int kR2 = 4 * C * LDV * ES + 2 * BV * LDQ * ES;
   constexpr int kR3 = 2 * C * LDT * ES;
   constexpr int kR = kR2 > kR3 ? kR2 : kR3;
@@ -321,16 +328,18 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
   const int b = bh / a.H, h = bh % a.H;
   const int r0 = ci * C;
   const int nrow = (a.T - r0) < C ? (a.T - r0) : C;
-  const int tid = threadIdx.x, w = wave_id(), l = lane_id();
+  const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6), l = lane_id();
+  const int sw = w & 3, hh = w >> 2;  // stripe, half (uniform)
+  const int ct0 = hh * NTW;           // this wave's first key-channel tile
   const int g4 = l >> 4, c16 = l & 15;
   const size_t cidx = (size_t)bh * N + ci;
   const size_t gsk = (size_t)a.H * DK, gsv = (size_t)a.H * a.dv;
   const float eC = a.gam[(cidx * 5 + 4) * C];
 
-  // ---- phase 1: Q K^T and K K^T (rows of stripe w, tiles J <= w)
-  f32x4 QK[4], KK[4];
+  // ---- phase 1: Q K^T and K K^T (rows of stripe sw, this wave's tiles J <= sw)
+  f32x4 QK[NJ], KK[NJ];
   {
-    ChunkTile<T, DK> rq, rk;
+    ChunkTile<T, DK, NT> rq, rk;
     rq.load(static_cast<const T*>(a.qc) + tok_off(b, r0, h, a.T, a.H, DK), gsk, nrow);
     rk.load(static_cast<const T*>(a.k) + tok_off(b, r0, h, a.T, a.H, DK), gsk, nrow);
     if (tid < C) {
@@ -342,23 +351,28 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
     rk.store(sK, LDQ);
     lds_barrier();
 #pragma unroll
-    for (int J = 0; J < 4; ++J) {
-      QK[J] = zero4();
-      KK[J] = zero4();
-      if (J <= w) {
-        tile_mma<T, DK>(QK[J], sQ + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
-        tile_mma<T, DK>(KK[J], sK + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+    for (int jj = 0; jj < NJ; ++jj) {
+      const int J = HW * jj + hh;
+      QK[jj] = zero4();
+      KK[jj] = zero4();
+      if (J <= sw) {
+        tile_mma<T, DK>(QK[jj], sQ + 16 * sw * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+        tile_mma<T, DK>(KK[jj], sK + 16 * sw * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
       }
     }
   }
 
   // ---- phase 2: value slices
-  f32x4 G1[NTC], G2[NTC], G3[NTC], dP[4], dA[4];
+  f32x4 G1[NTW], G2[NTW], G3[NTW], dP[NJ], dA[NJ];
 #pragma unroll
-  for (int ct = 0; ct < NTC; ++ct) { G1[ct] = zero4(); G2[ct] = zero4(); G3[ct] = zero4(); }
+  for (int ct = 0; ct < NTW; ++ct) { G1[ct] = zero4(); G2[ct] = zero4(); G3[ct] = zero4(); }
 #pragma unroll
-  for (int J = 0; J < 4; ++J) { dP[J] = zero4(); dA[J] = zero4(); }
+  for (int jj = 0; jj < NJ; ++jj) { dP[jj] = zero4(); dA[jj] = zero4(); }
   float rv = 0.f, dss = 0.f;
+  // the slices of dO, dR and V: 8-element pieces, four per row
+  typedef RowTile<T, BV, NT> VTile;
+  static_assert(VTile::NV == 1, "one piece per thread");
+  const int vrow = VTile::row(0), vcol = VTile::col(0);
   {
     T* sdO = reinterpret_cast<T*>(sR);
     T* sdR = sdO + C * LDV;
@@ -372,17 +386,18 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
     T* dvrow = static_cast<T*>(a.dv_out) + tok_off(b, r0, h, a.T, a.H, a.dv);
     typedef T v8 __attribute__((ext_vector_type(8)));
     // every value slice's global operands are requested one slice ahead
-    constexpr int NPS = BV * DK / 8 / kThreads;  // pieces of S_r and of D per thread
-    constexpr int NPU = BV * C / 8 / kThreads;   // pieces of U^T per thread
-    static_assert(NPS >= 1 && NPU >= 1, "piece split");
+    constexpr int NPS = BV * DK / 8 / NT;              // pieces of S_r and of D per thread
+    constexpr int TPU = BV * C / 8;                    // pieces of U^T
+    constexpr int NPU = (TPU + NT - 1) / NT;           // per thread
+    static_assert(NPS >= 1 && BV * DK / 8 % NT == 0, "piece split");
     struct Slice {
       v8 s[NPS], d[NPS], u[NPU];
-      ChunkTile<T, BV> rdo, rdr, rvv;
+      VTile rdo, rdr, rvv;
     };
     auto load_slice = [&](Slice& sl, int vv0) {
 #pragma unroll
       for (int p = 0; p < NPS; ++p) {
-        const int q = tid + p * kThreads;
+        const int q = tid + p * NT;
         const int vt = q / (2 * DK), rem = q % (2 * DK);
         const int m = rem / 64, vr = (rem % 64) / 4, pp = rem % 4;
         sl.s[p] = *reinterpret_cast<const v8*>(Sg + (size_t)(vv0 / 16 + vt) * 16 * DK + (size_t)(m * 16 + vr) * 32 + 8 * pp);
@@ -391,10 +406,12 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
       }
 #pragma unroll
       for (int p = 0; p < NPU; ++p) {
-        const int q = tid + p * kThreads;
-        const int vt = q / 128, rem = q % 128;
-        const int m = rem / 64, vr = (rem % 64) / 4, pp = rem % 4;
-        sl.u[p] = *reinterpret_cast<const v8*>(Ug + (size_t)(vv0 / 16 + vt) * 16 * C + (size_t)(m * 16 + vr) * 32 + 8 * pp);
+        const int q = tid + p * NT;
+        if (TPU % NT == 0 || q < TPU) {
+          const int vt = q / 128, rem = q % 128;
+          const int m = rem / 64, vr = (rem % 64) / 4, pp = rem % 4;
+          sl.u[p] = *reinterpret_cast<const v8*>(Ug + (size_t)(vv0 / 16 + vt) * 16 * C + (size_t)(m * 16 + vr) * 32 + 8 * pp);
+        }
       }
       sl.rdo.load(static_cast<const T*>(a.dO) + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
       sl.rdr.load(static_cast<const T*>(a.dR) + tok_off(b, r0, h, a.T, a.H, a.dv) + vv0, gsv, nrow);
@@ -403,32 +420,27 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
     Slice cur;
     load_slice(cur, 0);
     for (int vv0 = 0; vv0 < a.dv; vv0 += BV) {
-      {
-        const int row = ChunkTile<T, BV>::row();
-        const float bt = sBeta[row];
+      if (VTile::mine(0)) {
+        const float bt = sBeta[vrow];
+        const v8 xo = cur.rdo.get(0), xr = cur.rdr.get(0), xv = cur.rvv.get(0);
+        v8 yo, yd;
 #pragma unroll
-        for (int u = 0; u < ChunkTile<T, BV>::NV; ++u) {
-          const int c0 = ChunkTile<T, BV>::col(u);
-          const v8 xo = cur.rdo.get(u), xr = cur.rdr.get(u), xv = cur.rvv.get(u);
-          v8 yo, yd;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            yo[e] = to<T>(a.scale * f32(xo[e]));
-            yd[e] = to<T>(bt * f32(xr[e]));
-            rv += f32(xr[e]) * f32(xv[e]);
-          }
-          *reinterpret_cast<v8*>(sdO + row * LDV + c0) = yo;
-          *reinterpret_cast<v8*>(sdR + row * LDV + c0) = xr;
-          *reinterpret_cast<v8*>(sV + row * LDV + c0) = xv;
-          if (row < nrow) *reinterpret_cast<v8*>(dvrow + row * (int)gsv + vv0 + c0) = yd;
+        for (int e = 0; e < 8; ++e) {
+          yo[e] = to<T>(a.scale * f32(xo[e]));
+          yd[e] = to<T>(bt * f32(xr[e]));
+          rv += f32(xr[e]) * f32(xv[e]);
         }
+        *reinterpret_cast<v8*>(sdO + vrow * LDV + vcol) = yo;
+        *reinterpret_cast<v8*>(sdR + vrow * LDV + vcol) = xr;
+        *reinterpret_cast<v8*>(sV + vrow * LDV + vcol) = xv;
+        if (vrow < nrow) *reinterpret_cast<v8*>(dvrow + vrow * (int)gsv + vv0 + vcol) = yd;
       }
       // S_r and U^T slices (fragment-native: per value tile and 32-wide k
       // block, 16 rows of 32; S_r rows in natural order, U^T rows in acc_pos
       // order) and D (plain rows)
 #pragma unroll
       for (int p = 0; p < NPS; ++p) {
-        const int q = tid + p * kThreads;
+        const int q = tid + p * NT;
         const int vt = q / (2 * DK), rem = q % (2 * DK);
         const int m = rem / 64, vr = (rem % 64) / 4, pp = rem % 4;
         const int vl = 16 * vt + vr;
@@ -438,33 +450,36 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
       }
 #pragma unroll
       for (int p = 0; p < NPU; ++p) {
-        const int q = tid + p * kThreads;
-        const int vt = q / 128, rem = q % 128;
-        const int m = rem / 64, vr = (rem % 64) / 4, pp = rem % 4;
-        const int vl = 16 * vt + vr;
+        const int q = tid + p * NT;
+        if (TPU % NT == 0 || q < TPU) {
+          const int vt = q / 128, rem = q % 128;
+          const int m = rem / 64, vr = (rem % 64) / 4, pp = rem % 4;
+          const int vl = 16 * vt + vr;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sU[(32 * m + acc_logical(8 * pp + e)) * LDV + vl] = cur.u[p][e];
+          for (int e = 0; e < 8; ++e) sU[(32 * m + acc_logical(8 * pp + e)) * LDV + vl] = cur.u[p][e];
+        }
       }
       if (vv0 + BV < a.dv) load_slice(cur, vv0 + BV);
       lds_barrier();
 #pragma unroll
-      for (int J = 0; J < 4; ++J) {
-        if (J <= w) {
-          tile_mma<T, BV>(dP[J], sdO + 16 * w * LDV, LDV, sU + 16 * J * LDV, LDV);
-          tile_mma<T, BV>(dA[J], sdR + 16 * w * LDV, LDV, sU + 16 * J * LDV, LDV);
+      for (int jj = 0; jj < NJ; ++jj) {
+        const int J = HW * jj + hh;
+        if (J <= sw) {
+          tile_mma<T, BV>(dP[jj], sdO + 16 * sw * LDV, LDV, sU + 16 * J * LDV, LDV);
+          tile_mma<T, BV>(dA[jj], sdR + 16 * sw * LDV, LDV, sU + 16 * J * LDV, LDV);
         }
       }
 #pragma unroll
-      for (int ct = 0; ct < NTC; ++ct) {
+      for (int ct = 0; ct < NTW; ++ct) {
 #pragma unroll
         for (int k0 = 0; k0 < BV; k0 += 32) {
-          const Frag<T> fs = ld_frag_tr(sS + k0 * LDQ + 16 * ct, LDQ);
-          mma(G1[ct], ld_frag(sdO + 16 * w * LDV + k0, LDV), fs);
-          mma(G2[ct], ld_frag(sdR + 16 * w * LDV + k0, LDV), fs);
-          mma(G3[ct], ld_frag(sU + 16 * w * LDV + k0, LDV), ld_frag_tr(sD + k0 * LDQ + 16 * ct, LDQ));
+          const Frag<T> fs = ld_frag_tr(sS + k0 * LDQ + 16 * (ct0 + ct), LDQ);
+          mma(G1[ct], ld_frag(sdO + 16 * sw * LDV + k0, LDV), fs);
+          mma(G2[ct], ld_frag(sdR + 16 * sw * LDV + k0, LDV), fs);
+          mma(G3[ct], ld_frag(sU + 16 * sw * LDV + k0, LDV), ld_frag_tr(sD + k0 * LDQ + 16 * (ct0 + ct), LDQ));
         }
       }
-      for (int idx = tid; idx < DK * BV / 8; idx += kThreads) {
+      for (int idx = tid; idx < DK * BV / 8; idx += NT) {
         const int vl = idx / (DK / 8), c = (idx % (DK / 8)) * 8;
         const v8 xs = *reinterpret_cast<const v8*>(sS + vl * LDQ + c);
         const v8 xd = *reinterpret_cast<const v8*>(sD + vl * LDQ + c);
@@ -474,17 +489,20 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
       lds_barrier();
     }
   }
-  sRV[w][l] = rv;
+  // dR . v per row: the row's four pieces meet in adjacent lanes
+  rv += __shfl_xor(rv, 1);
+  rv += __shfl_xor(rv, 2);
+  if (VTile::mine(0) && (tid & 3) == 0) sRV[vrow] = rv;
 
   // Sigma_t q_t for this wave's rows, requested now for the epilogue
   const size_t rowoff = tok_off(b, r0, h, a.T, a.H, DK);
-  float cr[NTC][4];
+  float cr[NTW][4];
 #pragma unroll
-  for (int ct = 0; ct < NTC; ++ct)
+  for (int ct = 0; ct < NTW; ++ct)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int i = 16 * w + 4 * g4 + r;
-      cr[ct][r] = a.corr[rowoff + (i < nrow ? i : nrow - 1) * (int)gsk + 16 * ct + c16];
+      const int i = 16 * sw + 4 * g4 + r;
+      cr[ct][r] = a.corr[rowoff + (i < nrow ? i : nrow - 1) * (int)gsk + 16 * (ct0 + ct) + c16];
     }
 
   // ---- phase 3: C x C weights
@@ -492,18 +510,19 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
   T* sE = sPm + C * LDT;
   float rowF[4] = {0.f, 0.f, 0.f, 0.f}, rowA[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int J = 0; J < 4; ++J) {
+  for (int jj = 0; jj < NJ; ++jj) {
+    const int J = HW * jj + hh;
     const int j = 16 * J + c16;
     float colF = 0.f, colA = 0.f;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int i = 16 * w + 4 * g4 + r;
-      const float e = (J <= w && j <= i) ? __expf(sGam[i] - sGam[j]) : 0.f;
-      const float pm = e * dP[J][r];
-      const float ea = j < i ? -e * dA[J][r] : 0.f;  // (M o dA)_ij
+      const int i = 16 * sw + 4 * g4 + r;
+      const float e = (J <= sw && j <= i) ? __expf(sGam[i] - sGam[j]) : 0.f;
+      const float pm = e * dP[jj][r];
+      const float ea = j < i ? -e * dA[jj][r] : 0.f;  // (M o dA)_ij
       const float E = sBeta[i] * ea;
-      const float F = pm * QK[J][r];
-      const float fa = ea * KK[J][r];
+      const float F = pm * QK[jj][r];
+      const float fa = ea * KK[jj][r];
       rowF[r] += F;
       rowA[r] += fa;
       colF += F;
@@ -516,8 +535,8 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
     colA += __shfl_xor(colA, 16);
     colA += __shfl_xor(colA, 32);
     if (g4 == 0) {
-      sColF[w][j] = colF;
-      sColA[w][j] = colA;
+      sColF[sw][j] = colF;
+      sColA[sw][j] = colA;
     }
   }
   {  // <D, S_r> over the workgroup
@@ -528,21 +547,22 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
   }
   lds_barrier();
 
-  // ---- phase 4: dQ, dK and the epilogue (row i = 16w + 4g4 + r, channel c)
+  // ---- phase 4: dQ, dK and the epilogue (row i = 16 sw + 4 g4 + r, channel c)
   float dot1[4] = {0.f, 0.f, 0.f, 0.f}, dot2[4] = {0.f, 0.f, 0.f, 0.f}, dot3[4] = {0.f, 0.f, 0.f, 0.f};
   float dl[4] = {0.f, 0.f, 0.f, 0.f};
   T* dqc_io = static_cast<T*>(a.dqc_io);
 #pragma unroll
-  for (int ct = 0; ct < NTC; ++ct) {
+  for (int ct = 0; ct < NTW; ++ct) {
     f32x4 x = zero4(), y = zero4();
-    tile_mma_bt<T, C>(x, sPm + 16 * w * LDT, LDT, sK + 16 * ct, LDQ);
-    tile_mma_tr<T, C>(y, sPm + 16 * w, LDT, sQ + 16 * ct, LDQ);
-    tile_mma_bt<T, C>(y, sE + 16 * w * LDT, LDT, sK + 16 * ct, LDQ);
-    tile_mma_tr<T, C>(y, sE + 16 * w, LDT, sK + 16 * ct, LDQ);
-    const int c = 16 * ct + c16;
+    const int cc = 16 * (ct0 + ct);
+    tile_mma_bt<T, C>(x, sPm + 16 * sw * LDT, LDT, sK + cc, LDQ);
+    tile_mma_tr<T, C>(y, sPm + 16 * sw, LDT, sQ + cc, LDQ);
+    tile_mma_bt<T, C>(y, sE + 16 * sw * LDT, LDT, sK + cc, LDQ);
+    tile_mma_tr<T, C>(y, sE + 16 * sw, LDT, sK + cc, LDQ);
+    const int c = cc + c16;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int i = 16 * w + 4 * g4 + r;
+      const int i = 16 * sw + 4 * g4 + r;
       const float G = __expf(sGam[i]);
       const float qv = f32(sQ[i * LDQ + c]), kv = f32(sK[i * LDQ + c]);
       const float dq = G * G1[ct][r] + x[r];
@@ -559,38 +579,76 @@ __global__ __launch_bounds__(kThreads, 1) void gdn_bwd_chunk_kernel(const GdnBwd
       }
     }
   }
-  float xt = 0.f;  // sum over this wave's rows of e^{gamma_C - gamma_i} (G3_i . k_i)
+  // per-row sums over this wave's channels (and C x C tiles); with two waves
+  // per stripe the second half's sums are added through LDS
+  float d1[4], d2[4], d3[4], rf[4], ra[4], dlam[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    const int i = 16 * w + 4 * g4 + r;
-    const float d1 = row16_sum(dot1[r]), d2 = row16_sum(dot2[r]), d3 = row16_sum(dot3[r]);
-    const float rf = row16_sum(rowF[r]), ra = row16_sum(rowA[r]);
-    const float dlam = row16_sum(dl[r]);
-    const float G = __expf(sGam[i]), bt = sBeta[i];
-    const float colF = sColF[0][i] + sColF[1][i] + sColF[2][i] + sColF[3][i];
-    const float colA = sColA[0][i] + sColA[1][i] + sColA[2][i] + sColA[3][i];
-    const float rvi = sRV[0][i] + sRV[1][i] + sRV[2][i] + sRV[3][i];
-    const float dg = G * d1 + rf - colF - bt * G * d2 + bt * ra - colA - sDec[i] * d3;
-    if (c16 == 0) {
-      sDg[i] = i < nrow ? dg : 0.f;
-      xt += i < nrow ? sDec[i] * d3 : 0.f;
-      if (i < nrow) {
-        const size_t ti = ((size_t)b * a.T + r0 + i) * a.H + h;
-        a.dbeta[ti] = rvi - G * d2 + ra;
-        a.dlam[ti] = dlam;
+    d1[r] = row16_sum(dot1[r]);
+    d2[r] = row16_sum(dot2[r]);
+    d3[r] = row16_sum(dot3[r]);
+    rf[r] = row16_sum(rowF[r]);
+    ra[r] = row16_sum(rowA[r]);
+    dlam[r] = row16_sum(dl[r]);
+  }
+  if constexpr (HW > 1) {
+    if (hh == 1 && c16 == 0)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = 16 * sw + 4 * g4 + r;
+        sHalf[0][i] = d1[r];
+        sHalf[1][i] = d2[r];
+        sHalf[2][i] = d3[r];
+        sHalf[3][i] = rf[r];
+        sHalf[4][i] = ra[r];
+        sHalf[5][i] = dlam[r];
+      }
+    lds_barrier();
+    if (hh == 0)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = 16 * sw + 4 * g4 + r;
+        d1[r] += sHalf[0][i];
+        d2[r] += sHalf[1][i];
+        d3[r] += sHalf[2][i];
+        rf[r] += sHalf[3][i];
+        ra[r] += sHalf[4][i];
+        dlam[r] += sHalf[5][i];
+      }
+  }
+  float xt = 0.f;  // sum over this stripe's rows of e^{gamma_C - gamma_i} (G3_i . k_i)
+  if (hh == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = 16 * sw + 4 * g4 + r;
+      const float G = __expf(sGam[i]), bt = sBeta[i];
+      const float colF = sColF[0][i] + sColF[1][i] + sColF[2][i] + sColF[3][i];
+      const float colA = sColA[0][i] + sColA[1][i] + sColA[2][i] + sColA[3][i];
+      const float dg = G * d1[r] + rf[r] - colF - bt * G * d2[r] + bt * ra[r] - colA - sDec[i] * d3[r];
+      if (c16 == 0) {
+        sDg[i] = i < nrow ? dg : 0.f;
+        xt += i < nrow ? sDec[i] * d3[r] : 0.f;
+        if (i < nrow) {
+          const size_t ti = ((size_t)b * a.T + r0 + i) * a.H + h;
+          a.dbeta[ti] = sRV[i] - G * d2[r] + ra[r];
+          a.dlam[ti] = dlam[r];
+        }
       }
     }
+    xt += __shfl_xor(xt, 16);
+    xt += __shfl_xor(xt, 32);
+    if (l == 0) sRed[1][sw] = xt;
   }
-  xt += __shfl_xor(xt, 16);
-  xt += __shfl_xor(xt, 32);
-  if (l == 0) sRed[1][w] = xt;
   lds_barrier();
   if (w == 0) {
     // the last row of the chunk also carries the derivative through gamma_C
     float x = sDg[l];
-    if (l == nrow - 1)
-      x += (sRed[1][0] + sRed[1][1] + sRed[1][2] + sRed[1][3]) +
-           eC * (sRed[0][0] + sRed[0][1] + sRed[0][2] + sRed[0][3]);
+    if (l == nrow - 1) {
+      float sd = 0.f;
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) sd += sRed[0][ww];
+      x += (sRed[1][0] + sRed[1][1] + sRed[1][2] + sRed[1][3]) + eC * sd;
+    }
     // suffix sum: dlogalpha_s = sum_{i >= s} dgamma_i
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
@@ -629,12 +687,12 @@ hipError_t run_dstate(const GdnDstateArgs& a, hipStream_t st) {
   if constexpr (DK >= 256) return run_dstate_v<T, DK, 2, 4>(a, st);
   return run_dstate_v<T, DK, 2, 2>(a, st);
 }
-template <typename T, int DK>
+template <typename T, int DK, int NW = 4>
 hipError_t run_bwd_chunk(const GdnBwdArgs& a, hipStream_t st) {
   const int nblk = a.B * a.H * ((a.T + kChunk - 1) / kChunk);
   if (nblk == 0) return hipSuccess;
   constexpr int BV = 32;
-  hipLaunchKernelGGL((gdn_bwd_chunk_kernel<T, DK, BV>), dim3(nblk), dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL((gdn_bwd_chunk_kernel<T, DK, BV, NW>), dim3(nblk), dim3(64 * NW), 0, st, a);
   return hipGetLastError();
 }
 }  // namespace
@@ -670,7 +728,9 @@ hipError_t launch_gdn_bwd_chunk(const GdnBwdArgs& a, bool is_bf16, hipStream_t s
     switch (a.dk) {
       case 64: return run_bwd_chunk<bf16_t, 64>(a, st);
       case 128: return run_bwd_chunk<bf16_t, 128>(a, st);
-      case 256: return run_bwd_chunk<bf16_t, 256>(a, st);
+      // eight waves at dk = 256 (the kernel takes a compute unit's LDS: two
+      // waves per SIMD instead of one)
+      case 256: return run_bwd_chunk<bf16_t, 256, 8>(a, st);
     }
   } else if (a.dk == 64) {
     return run_bwd_chunk<float, 64>(a, st);
