@@ -587,7 +587,10 @@ def per_kernel_times(calls, ev, steps):
     return per_kernel
 
 
-def roofline(entry, w):
+def roofline(entry, w, name=None):
+    """The kernel's own roofline on workload w (`name`: the workload's label when it
+    differs from w's, e.g. a variant of the statistics on w's shape)."""
+    wn = name or w.name
     by, fl = kernel_cost(entry["kernel"], w)
     sec = entry["ms_mean"] * 1e-3
     intensity = fl / by
@@ -600,9 +603,9 @@ def roofline(entry, w):
         ach = fl / sec / 1e12
         r = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
              "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4)}
-    r["traffic"] = measured_traffic(entry["kernel"], w.name)
+    r["traffic"] = measured_traffic(entry["kernel"], wn)
     r["kernel"] = entry["symbol"]
-    r["workload"] = w.name
+    r["workload"] = wn
     r["algorithmic_bytes"] = by
     r["algorithmic_flops"] = fl
     r["ms_per_launch"] = round(entry["ms_mean"], 5)
@@ -662,7 +665,7 @@ def measure_extra(name, torch, ccq, inputs, steps, existing):
                "kernels_ms": [[e["kernel"], e["symbol"], round(e["ms_mean"], 5)] for e in pk],
                "roofline": method_roofline(c.w, c.ms_call,
                                            call_traffic(c.kernels, name if "_decay_" in name else c.w.name)),
-               "dominant_kernel": roofline(dom, c.w)}
+               "dominant_kernel": roofline(dom, c.w, name)}
     if name not in existing:
         del c
         torch.cuda.empty_cache()
