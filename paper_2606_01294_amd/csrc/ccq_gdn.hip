@@ -97,32 +97,35 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
   }
   __syncthreads();
 
-  // A (strictly lower), row tile w; written once every wave is done with K
-  f32x4 acc[4];
+  // A (strictly lower): the ten tiles I >= J dealt to the waves in turn (three,
+  // three, two, two); written once every wave is done with K (the upper
+  // tiles are never read)
+  f32x4 acc[3];
 #pragma unroll
-  for (int J = 0; J < 4; ++J) {
-    acc[J] = zero4();
-    if (J <= w) tile_mma<T, DK>(acc[J], sK + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+  for (int s3 = 0; s3 < 3; ++s3) {
+    const int t = w + 4 * s3;
+    acc[s3] = zero4();
+    if (t < 10)
+      tile_mma<T, DK>(acc[s3], sK + 16 * intra_tile_row(t) * LDQ, LDQ, sK + 16 * intra_tile_col(t) * LDQ, LDQ);
   }
   __syncthreads();
-  {
+#pragma unroll
+  for (int s3 = 0; s3 < 3; ++s3) {
+    const int t = w + 4 * s3;
+    if (t >= 10) continue;
+    const int I = intra_tile_row(t), J = intra_tile_col(t);
     // the coefficients read whole and every entry formed before the mask is
     // applied as a select (reads under the mask compile to a branch and a wait
     // each); e^{gamma_i - gamma_j} may overflow above the diagonal, where the
     // select discards it
-    const f32x4 gi = *reinterpret_cast<const f32x4*>(sGam + 16 * w + 4 * g4);
-    const f32x4 bi = *reinterpret_cast<const f32x4*>(sBeta + 16 * w + 4 * g4);
-    float gj[4];
+    const f32x4 gi = *reinterpret_cast<const f32x4*>(sGam + 16 * I + 4 * g4);
+    const f32x4 bi = *reinterpret_cast<const f32x4*>(sBeta + 16 * I + 4 * g4);
+    const float gj = sGam[16 * J + c16];
 #pragma unroll
-    for (int J = 0; J < 4; ++J) gj[J] = sGam[16 * J + c16];
-#pragma unroll
-    for (int J = 0; J < 4; ++J) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i = 16 * w + 4 * g4 + r, j = 16 * J + c16;
-        const float v = bi[r] * __expf(gi[r] - gj[J]) * acc[J][r];
-        sA[i * LDA + j] = j < i ? v : 0.f;
-      }
+    for (int r = 0; r < 4; ++r) {
+      const int i = 16 * I + 4 * g4 + r, j = 16 * J + c16;
+      const float v = bi[r] * __expf(gi[r] - gj) * acc[s3][r];
+      sA[i * LDA + j] = j < i ? v : 0.f;
     }
   }
   __syncthreads();
@@ -160,11 +163,16 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
   }
   __syncthreads();
 
-  // Tm rows i, each 32-column block in acc_pos order
+  // Tm rows i, each 32-column block in acc_pos order: positions 8q .. 8q + 7
+  // of a row hold logical columns b + 4 (q % 4) .. + 3 and b + 16 + 4 (q % 4)
+  // .. + 3 (b = the block's first column), two 16-byte LDS reads per piece
   T* Tout = static_cast<T*>(a.Tm) + ((size_t)bh * N + ci) * C * C;
-  for (int idx = tid; idx < C * C; idx += kThreads) {
-    const int i = idx / C, p = idx % C;
-    Tout[idx] = to<T>(sX[i * LDA + acc_logical(p)]);
+  for (int idx = tid; idx < C * C / 8; idx += kThreads) {
+    const int i = idx / (C / 8), q = idx % (C / 8);
+    const int lc = ((8 * q) & ~31) + 4 * (q & 3);
+    const f32x4 lo = *reinterpret_cast<const f32x4*>(sX + i * LDA + lc);
+    const f32x4 hi = *reinterpret_cast<const f32x4*>(sX + i * LDA + lc + 16);
+    store_acc_pair(Tout + i * C + 8 * q, lo, hi);
   }
 }
 
