@@ -130,24 +130,23 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
   }
   __syncthreads();
 
-  // diagonal blocks: lane l < 16 of wave w solves column l of block w
+  // diagonal blocks: lane l < 16 of wave w solves column l of block w; each
+  // row's sum is kept in four partial sums (terms m mod 4), so that x_i waits
+  // for one product with x_{i-1} and two additions instead of the whole row
   if (l < 16) {
     float x[16];
     const float* Ab = sA + 16 * w * LDA + 16 * w;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      float s = i == l ? 1.f : 0.f;
+      float p[4] = {i == l ? 1.f : 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int m = 0; m < i; ++m) s -= Ab[i * LDA + m] * x[m];
-      x[i] = s;
+      for (int m = 0; m < i; ++m) p[m & 3] -= Ab[i * LDA + m] * x[m];
+      x[i] = (p[0] + p[1]) + (p[2] + p[3]);
     }
 #pragma unroll
     for (int i = 0; i < 16; ++i) sX[(16 * w + i) * LDA + 16 * w + l] = x[i];
   }
-  for (int idx = tid; idx < C * C; idx += kThreads) {
-    const int i = idx / C, j = idx % C;
-    if ((j >> 4) > (i >> 4)) sX[i * LDA + j] = 0.f;
-  }
+  // (the blocks above the diagonal are never written: the output selects zero there)
   __syncthreads();
 
   // off-diagonal blocks of column block w (LDS traffic local to the wave)
@@ -170,8 +169,10 @@ __global__ __launch_bounds__(kThreads) void gdn_tri_kernel(const TriArgs a) {
   for (int idx = tid; idx < C * C / 8; idx += kThreads) {
     const int i = idx / (C / 8), q = idx % (C / 8);
     const int lc = ((8 * q) & ~31) + 4 * (q & 3);
-    const f32x4 lo = *reinterpret_cast<const f32x4*>(sX + i * LDA + lc);
-    const f32x4 hi = *reinterpret_cast<const f32x4*>(sX + i * LDA + lc + 16);
+    f32x4 lo = *reinterpret_cast<const f32x4*>(sX + i * LDA + lc);
+    f32x4 hi = *reinterpret_cast<const f32x4*>(sX + i * LDA + lc + 16);
+    if ((lc >> 4) > (i >> 4)) lo = zero4();  // above the diagonal blocks
+    if (((lc + 16) >> 4) > (i >> 4)) hi = zero4();
     store_acc_pair(Tout + i * C + 8 * q, lo, hi);
   }
 }
