@@ -65,25 +65,34 @@ __global__ __launch_bounds__(kThreads) void gdn_bwd_prep_kernel(const GdnPrepArg
   }
   lds_barrier();
 
-  // wave w: rows i of stripe w against every key tile J; P^T stored as rows j
+  // the 16 score tiles (rows i of tile I against keys of tile J) dealt to the
+  // waves in turn, the ten with J <= I first; P^T stored as rows j (zero
+  // tiles above the diagonal)
   T* PT = static_cast<T*>(a.PT) + cidx * C * C;
 #pragma unroll
-  for (int J = 0; J < 4; ++J) {
+  for (int s4 = 0; s4 < 4; ++s4) {
+    const int t = w + 4 * s4;
+    const int I = intra_tile_row(t), J = intra_tile_col(t);
     f32x4 acc = zero4();
-    if (J <= w) tile_mma<T, DK>(acc, sQ + 16 * w * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
+    if (t < 10) tile_mma<T, DK>(acc, sQ + 16 * I * LDQ, LDQ, sK + 16 * J * LDQ, LDQ);
     const int j = 16 * J + c16;
     float x[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int i = 16 * w + 4 * g4 + r;
-      x[r] = (J <= w && j <= i) ? acc[r] * __expf(sGam[i] - sGam[j]) : 0.f;
+      const int i = 16 * I + 4 * g4 + r;
+      x[r] = (t < 10 && j <= i) ? acc[r] * __expf(sGam[i] - sGam[j]) : 0.f;
     }
-    store4(PT + (size_t)j * C + 16 * w + 4 * g4, x[0], x[1], x[2], x[3]);
+    store4(PT + (size_t)j * C + 16 * I + 4 * g4, x[0], x[1], x[2], x[3]);
   }
+  // Tm^T: 8 consecutive elements of a row per 16-byte store
   T* TmT = static_cast<T*>(a.TmT) + cidx * C * C;
-  for (int idx = tid; idx < C * C; idx += kThreads) {
-    const int i = idx / C, p = idx % C;
-    TmT[idx] = sTm[acc_logical(p) * LDP + acc_pos(i)];
+  for (int idx = tid; idx < C * C / 8; idx += kThreads) {
+    const int i = idx / (C / 8), p0 = (idx % (C / 8)) * 8;
+    typedef T v8 __attribute__((ext_vector_type(8)));
+    v8 y;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) y[e] = sTm[acc_logical(p0 + e) * LDP + acc_pos(i)];
+    *reinterpret_cast<v8*>(TmT + (size_t)i * C + p0) = y;
   }
 }
 
