@@ -440,6 +440,13 @@ struct ChunkTile {
   }
 };
 
+// x, opaque to the optimiser: addresses derived from it are formed where they
+// are used instead of being hoisted out of a loop and held in registers.
+__device__ __forceinline__ int opaque(int x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
 // One 64-row chunk of a [*, D] token tensor staged for a row-major LDS copy,
 // with coalesced global loads: vector e = tid + NT u (8 elements) is row
 // e / (D / 8), column 8 (e % (D / 8)), so consecutive lanes read consecutive
@@ -481,6 +488,21 @@ struct RowTile {
       const int r = row(u);
       ok |= (r < n ? 1u : 0u) << u;
       v[u] = *reinterpret_cast<const vec_t*>(src + (size_t)(r < n ? r : n - 1) * gstride + col(u));
+    }
+  }
+  // load() with the thread index passed through opaque(): the row offsets are
+  // formed at the loads instead of being hoisted out of a loop over chunks and
+  // held in registers (for kernels short of registers)
+  __device__ __forceinline__ void load_opaque(const T* src, size_t gstride, int n) {
+    const int t = opaque((int)threadIdx.x);
+    ok = 0;
+    full = false;
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      if (!(TOT % NT == 0 || t + NT * u < TOT)) continue;
+      const int r = (t + NT * u) / VPR, c = ((t + NT * u) % VPR) * VE;
+      ok |= (r < n ? 1u : 0u) << u;
+      v[u] = *reinterpret_cast<const vec_t*>(src + (size_t)(r < n ? r : n - 1) * gstride + c);
     }
   }
   __device__ __forceinline__ vec_t get(int u) const {
@@ -591,12 +613,6 @@ __device__ __forceinline__ void lds_wait_but(Frag<bf16_t> (&f)[N]) {
   for (int i = 0; i < N; ++i) asm volatile("" : "+v"(f[i].v));
 }
 
-// x, opaque to the optimiser: addresses derived from it are formed where they
-// are used instead of being hoisted out of a loop and held in registers.
-__device__ __forceinline__ int opaque(int x) {
-  asm volatile("" : "+v"(x));
-  return x;
-}
 
 // Fragment loads from a pointer that already includes the lane's offset.
 // frag_at: 8 contiguous elements (ld_frag with p = tile + (l % 16) ld + 8 (l / 16)).
