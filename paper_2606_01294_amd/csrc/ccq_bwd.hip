@@ -96,10 +96,12 @@ __global__ __launch_bounds__(64 * NW, 1) void gla_bwd_chunk_kernel(const GlaBwdA
   const T* dSst = static_cast<const T*>(a.dstates) + ((size_t)bh * N + ci) * a.dv * DK;
   const size_t gsk = (size_t)a.H * DK, gsv = (size_t)a.H * a.dv;
 
-  // ---- phase 1: decay prefix, rescaled Qt / Kt, intra block
+  // ---- phase 1: decay prefix, rescaled Qt / Kt, intra block (the chunk's
+  // rows loaded as row tiles: adjacent lanes along a row)
   {
-    ChunkTile<T, DK, NT> rq, rk;
-    ChunkTile<TG, DK, NT> rg;
+    typedef RowTile<T, DK, NT> TileQ;
+    TileQ rq, rk;
+    RowTile<TG, DK, NT> rg;
     rq.load(qc + tok_off(b, r0, h, a.T, a.H, DK), gsk, nrow);
     rk.load(k + tok_off(b, r0, h, a.T, a.H, DK), gsk, nrow);
     rg.load(gate + tok_off(b, r0, h, a.T, a.H, DK), gsk, nrow);
@@ -117,20 +119,20 @@ __global__ __launch_bounds__(64 * NW, 1) void gla_bwd_chunk_kernel(const GlaBwdA
       sBCm[tid] = __expf(x[C - 1] - x[C / 2 - 1]);
     }
     lds_barrier();
-    const int j = ChunkTile<T, DK, NT>::row();
 #pragma unroll
-    for (int u = 0; u < ChunkTile<T, DK, NT>::NV; ++u) {
-      const int c0 = ChunkTile<T, DK, NT>::col(u);
+    for (int u = 0; u < TileQ::NV; ++u) {
+      if (!TileQ::mine(u)) continue;
+      const int j = TileQ::row(u), c0 = TileQ::col(u);
       const auto xq = rq.get(u), xk = rk.get(u);
-      typename ChunkTile<T, DK, NT>::vec_t qo, ko;
+      typename TileQ::vec_t qo, ko;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float d = sG[j * LDG + c0 + e] - sG[(C / 2 - 1) * LDG + c0 + e];
         qo[e] = to<T>(f32(xq[e]) * __expf(d));
         ko[e] = to<T>(f32(xk[e]) * __expf(-d));
       }
-      *reinterpret_cast<typename ChunkTile<T, DK, NT>::vec_t*>(sQt + j * LDQ + c0) = qo;
-      *reinterpret_cast<typename ChunkTile<T, DK, NT>::vec_t*>(sKt + j * LDQ + c0) = ko;
+      *reinterpret_cast<typename TileQ::vec_t*>(sQt + j * LDQ + c0) = qo;
+      *reinterpret_cast<typename TileQ::vec_t*>(sKt + j * LDQ + c0) = ko;
     }
   }
   lds_barrier();
@@ -162,7 +164,7 @@ __global__ __launch_bounds__(64 * NW, 1) void gla_bwd_chunk_kernel(const GlaBwdA
   static_assert(NPS >= 1 && BV * DK / 8 % NT == 0, "piece split");
   struct Slice {
     v8 s[NPS], d[NPS];
-    ChunkTile<T, BV, NT> rv, rdo;
+    RowTile<T, BV, NT> rv, rdo;
   };
   auto load_slice = [&](Slice& sl, int vv0) {
 #pragma unroll

@@ -511,6 +511,16 @@ struct RowTile {
     for (int e = 0; e < VE; ++e) z[e] = static_cast<T>(0.f);
     return (full || ((ok >> u) & 1u)) ? v[u] : z;
   }
+  // fp32 copy, row-major (adjacent lanes write adjacent elements of a row)
+  __device__ __forceinline__ void store_f32(float* dst, int ld) const {
+#pragma unroll
+    for (int u = 0; u < NV; ++u)
+      if (mine(u)) {
+        const vec_t x = get(u);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) dst[row(u) * ld + col(u) + e] = static_cast<float>(x[e]);
+      }
+  }
   __device__ __forceinline__ void store(T* dst, int ld) const {
     if (full) {
 #pragma unroll
