@@ -24,6 +24,8 @@
 //   dlogalpha_s = sum_{i >= s} dgamma_i  (inside the chunk).
 // dQ is dL/dq_clean; the contraction's part of the gradients follows as for
 // GLA (ccq_bwd.hip).
+#include <type_traits>
+
 #include "ccq_device.h"
 #include "ccq_kernels.h"
 
@@ -148,12 +150,18 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_dstate_kernel(const GdnD
 #pragma unroll
   for (int tc = 0; tc < NCT; ++tc) D[tc] = zero4();
 
+  // q: with eight waves as a row tile (adjacent lanes along a row, coalesced;
+  // one decay per staged vector), else one row per lane (one decay per lane,
+  // fewer registers)
+  constexpr bool kRowQ = NT >= 512;
+  typedef typename std::conditional<kRowQ, RowTile<T, DK, NT>, ChunkTile<T, DK, NT>>::type QTile;
+  constexpr int NGQ = kRowQ ? RowTile<T, DK, NT>::NV : 1;
   struct Stage {
     RowTile<T, DK, NT> rk;
-    ChunkTile<T, DK, NT> rq;   // lane = token row, so one decay per lane
+    QTile rq;
     RowTile<T, C, NT> rp, rt;
     ChunkTile<T, BVS, NTO> rdo;
-    float gq;                  // gamma of this lane's token row
+    float gq[NGQ];             // gamma of the staged rows of q
     RowScalar cf[3];
   };
   Stage st;
@@ -172,7 +180,12 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_dstate_kernel(const GdnD
     st.rp.load(static_cast<const T*>(a.PT) + cidx * C * C, (size_t)C, C);
     st.rt.load(static_cast<const T*>(a.TmT) + cidx * C * C, (size_t)C, C);
     if (tid < NTO) st.rdo.load(dO + tok_off(b, r0, h, a.T, a.H, a.dv) + v0, (size_t)a.H * a.dv, nrow);
-    st.gq = a.gam[cidx * 5 * C + (tid & 63)];
+    if constexpr (kRowQ) {
+#pragma unroll
+      for (int u = 0; u < NGQ; ++u) st.gq[u] = a.gam[cidx * 5 * C + RowTile<T, DK, NT>::row(u)];
+    } else {
+      st.gq[0] = a.gam[cidx * 5 * C + (tid & 63)];
+    }
     if (tid < C) {
       st.cf[0].load(a.gam + (cidx * 5 + 3) * C, 1, tid, C);
       st.cf[1].load(a.gam + (cidx * 5 + 1) * C, 1, tid, C);
@@ -193,17 +206,25 @@ __global__ __launch_bounds__(64 * NPR * NH, 1) void gdn_dstate_kernel(const GdnD
     st.rp.store(sPT, LDP);
     st.rt.store(sTT, LDP);
     {
-      typedef typename ChunkTile<T, DK, NT>::vec_t vq;
-      const int row = ChunkTile<T, DK, NT>::row();
-      const float eg = __expf(st.gq);
+      typedef typename QTile::vec_t vq;
 #pragma unroll
-      for (int u = 0; u < ChunkTile<T, DK, NT>::NV; ++u) {
+      for (int u = 0; u < QTile::NV; ++u) {
+        int qrow;
+        float eg;
+        if constexpr (kRowQ) {
+          qrow = RowTile<T, DK, NT>::row(u);
+          eg = __expf(st.gq[u]);
+        } else {
+          qrow = ChunkTile<T, DK, NT>::row();
+          eg = __expf(st.gq[0]);
+        }
         const vq x = st.rq.get(u);
         vq y;
 #pragma unroll
         for (int e = 0; e < 8; ++e) y[e] = to<T>(eg * f32(x[e]));
-        *reinterpret_cast<vq*>(sQ + row * LDQ + ChunkTile<T, DK, NT>::col(u)) = y;
+        *reinterpret_cast<vq*>(sQ + qrow * LDQ + QTile::col(u)) = y;
       }
+      const int row = ChunkTile<T, BVS, NTO>::row();
       if (tid < NTO)
 #pragma unroll
         for (int u = 0; u < ChunkTile<T, BVS, NTO>::NV; ++u) {
