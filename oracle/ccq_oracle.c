@@ -20,8 +20,8 @@
  *
  * Three forward forms:
  *   form 0: token-by-token recurrence on the raw sums K_t = sum k k^T and
- *           m_t = sum k, divided by t at use (App. B: "normalization by 1/t is
- *           applied after the product");
+ *           m_t = sum k, divided by t at use (App. B divides by t only once
+ *           the product with the query is formed);
  *   form 1: Alg. 2 (recurrent inference), running-mean updates of Cbar, mu;
  *   chunk : Alg. 1 (chunkwise forward), with the backbone's chunk forms.
  * and two reverse passes (GLA + CCQ, Gated DeltaNet + CCQ), recomputing each
